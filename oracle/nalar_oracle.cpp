@@ -1,0 +1,224 @@
+// Reference ("oracle") implementation of Nalar's global policy pass.
+//
+// TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, obviously correct
+// CPU definition that the HIP implementation is checked against.  Only the test
+// suite, the package smoke check and the benchmark's CPU-baseline leg may load
+// it; the product path never calls it.  It shares no source, header, helper or
+// constant table with the GPU library.
+//
+// One single-threaded pass over a snapshot of the global view (the paper's
+// global controller runs one single-threaded policy loop, Section 4.2):
+//
+//   O1  validate the snapshot                                  -> -1 (EINVAL)
+//   O2  est'[v] = done[v] ? 0 : est[v]
+//   O3  successor lists = transpose of the dependency lists (Table 3:
+//       "dependencies" and "consumers")
+//   O4  reverse topological order by iterative depth-first post-order over
+//       successors; meeting a node still on the stack is a cycle  -> -2 (ECYCLE)
+//   O5  remaining critical path, visited in that post-order:
+//         rem[v] = est'[v] + max(0, max over successors s of rem[s])
+//       (the "least remaining work" of the SRTF policy, Section 6.3,
+//       generalised from a chain of stages to a DAG); rem > 2^62 -> -3 (ERANGE)
+//   O6  ready[v] = !done[v] and every dependency of v is done (push-based
+//       readiness, Section 4.3.1, property 3)
+//   O7  slack[v] = (deadline[wf[v]] - now) - rem[v]              (set_priority,
+//       Table 2)
+//   O8  route[v] = the instance i of type type[v] minimising
+//         cost = load[i] + est[v]*1000/speed[i]   (integer division)
+//              + (loc[v] >= 0 and loc[v] != i ? migration cost : 0)
+//       scanning i upward with a strict "<", so the lowest index wins ties;
+//       route = -1 and cost = INT64_MAX when no instance has the type
+//       (route / migrate, Table 2; state locality, Section 4.3.2)
+//   O9  order = the ready futures sorted by (slack, wf, v) ascending
+//   O10 write rem, order, slack, route, cost and the ready count.
+//
+// Precedence of errors: EINVAL, then ECYCLE, then ERANGE.
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <vector>
+
+namespace {
+
+constexpr int kOk = 0;
+constexpr int kEinval = -1;
+constexpr int kEcycle = -2;
+constexpr int kErange = -3;
+
+constexpr int64_t kMaxNodes = int64_t(1) << 30;
+constexpr int64_t kMaxEdges = (int64_t(1) << 31) - 1;
+constexpr int64_t kMaxWorkflows = int64_t(1) << 30;
+constexpr int64_t kMaxInstances = 1024;
+constexpr int64_t kEstMax = int64_t(1) << 40;
+constexpr int64_t kLoadMax = int64_t(1) << 60;
+constexpr int64_t kMigMax = int64_t(1) << 60;
+constexpr int64_t kHorizon = int64_t(1) << 61;   // |now| and |deadline - now|
+constexpr int64_t kRemMax = int64_t(1) << 62;
+
+// O1: every rule the snapshot must satisfy.  A self-dependency is left to the
+// cycle check (it is a cycle of length one).
+int validate(int64_t N, int64_t E, int64_t W, int64_t M, int64_t now, int64_t mig,
+             const int32_t* wf, const int32_t* type, const int64_t* est,
+             const uint8_t* done, const int32_t* loc, const int32_t* dep_off,
+             const int32_t* dep_idx, const int64_t* deadline, const int32_t* inst_type,
+             const int64_t* inst_load, const int32_t* inst_speed) {
+  if (N < 0 || N > kMaxNodes || E < 0 || E > kMaxEdges || W < 0 || W > kMaxWorkflows ||
+      M < 0 || M > kMaxInstances)
+    return kEinval;
+  if (now < -kHorizon || now > kHorizon || mig < 0 || mig > kMigMax) return kEinval;
+  if (N == 0 && E != 0) return kEinval;
+  if (N > 0 && (!wf || !type || !est || !done || !loc || !dep_off)) return kEinval;
+  if (E > 0 && !dep_idx) return kEinval;
+  if (W > 0 && !deadline) return kEinval;
+  if (M > 0 && (!inst_type || !inst_load || !inst_speed)) return kEinval;
+  for (int64_t w = 0; w < W; ++w)
+    if (deadline[w] < now - kHorizon || deadline[w] > now + kHorizon) return kEinval;
+  for (int64_t i = 0; i < M; ++i) {
+    if (inst_type[i] < 0) return kEinval;
+    if (inst_speed[i] < 1) return kEinval;
+    if (inst_load[i] < 0 || inst_load[i] > kLoadMax) return kEinval;
+  }
+  if (N == 0) return kOk;
+  if (dep_off[0] != 0 || dep_off[N] != E) return kEinval;
+  for (int64_t v = 0; v < N; ++v) {
+    if (dep_off[v] > dep_off[v + 1]) return kEinval;
+    if (wf[v] < 0 || wf[v] >= W) return kEinval;
+    if (type[v] < 0) return kEinval;
+    if (loc[v] < -1 || loc[v] >= M) return kEinval;
+    if (est[v] < 0 || est[v] > kEstMax) return kEinval;
+    if (done[v] > 1) return kEinval;
+  }
+  for (int64_t v = 0; v < N; ++v) {
+    for (int32_t e = dep_off[v]; e < dep_off[v + 1]; ++e) {
+      int32_t p = dep_idx[e];
+      if (p < 0 || p >= N) return kEinval;
+      if (wf[p] != wf[v]) return kEinval;
+    }
+  }
+  return kOk;
+}
+
+}  // namespace
+
+extern "C" {
+
+// The boundary of the oracle: host arrays in, host arrays out.  Output arrays
+// must hold n_nodes entries (rem) and n_nodes entries (order, slack, route,
+// cost); rem_out and cost_out may be NULL.  Returns 0 or a negative error code.
+int nalar_oracle_pass(int64_t N, int64_t E, int64_t W, int64_t M, int64_t now, int64_t mig,
+                      const int32_t* wf, const int32_t* type, const int64_t* est,
+                      const uint8_t* done, const int32_t* loc, const int32_t* dep_off,
+                      const int32_t* dep_idx, const int64_t* deadline,
+                      const int32_t* inst_type, const int64_t* inst_load,
+                      const int32_t* inst_speed, int64_t* rem_out, int32_t* order_out,
+                      int64_t* slack_out, int32_t* route_out, int64_t* cost_out,
+                      int64_t* n_ready_out) {
+  int rc = validate(N, E, W, M, now, mig, wf, type, est, done, loc, dep_off, dep_idx,
+                    deadline, inst_type, inst_load, inst_speed);
+  if (rc != kOk) return rc;
+  if (n_ready_out) *n_ready_out = 0;
+  if (N == 0) return kOk;
+  if (!order_out || !slack_out || !route_out) return kEinval;
+
+  // O2
+  std::vector<int64_t> est_eff(N);
+  for (int64_t v = 0; v < N; ++v) est_eff[v] = done[v] ? 0 : est[v];
+
+  // O3: successor CSR (counting sort of the edges by parent)
+  std::vector<int64_t> succ_off(N + 1, 0);
+  for (int64_t e = 0; e < E; ++e) succ_off[dep_idx[e] + 1]++;
+  for (int64_t v = 0; v < N; ++v) succ_off[v + 1] += succ_off[v];
+  std::vector<int32_t> succ(E);
+  {
+    std::vector<int64_t> fill(succ_off.begin(), succ_off.end() - 1);
+    for (int64_t v = 0; v < N; ++v)
+      for (int32_t e = dep_off[v]; e < dep_off[v + 1]; ++e) succ[fill[dep_idx[e]]++] = int32_t(v);
+  }
+
+  // O4 + O5: iterative DFS, post-order evaluation of rem.
+  enum : uint8_t { kWhite = 0, kGray = 1, kBlack = 2 };
+  std::vector<uint8_t> color(N, kWhite);
+  std::vector<int64_t> rem(N, 0);
+  bool overflow = false;
+  struct Frame { int64_t v; int64_t next; };
+  std::vector<Frame> stack;
+  for (int64_t root = 0; root < N; ++root) {
+    if (color[root] != kWhite) continue;
+    color[root] = kGray;
+    stack.push_back({root, succ_off[root]});
+    while (!stack.empty()) {
+      Frame& f = stack.back();
+      if (f.next < succ_off[f.v + 1]) {
+        int64_t s = succ[f.next++];
+        if (color[s] == kGray) return kEcycle;
+        if (color[s] == kWhite) {
+          color[s] = kGray;
+          stack.push_back({s, succ_off[s]});
+        }
+        continue;
+      }
+      // post-visit: every successor is finished
+      int64_t v = f.v;
+      int64_t best = 0;
+      for (int64_t k = succ_off[v]; k < succ_off[v + 1]; ++k) best = std::max(best, rem[succ[k]]);
+      int64_t r;
+      if (__builtin_add_overflow(est_eff[v], best, &r) || r > kRemMax) {
+        overflow = true;
+        r = kRemMax + 1;  // keep later sums finite; the pass fails anyway
+      }
+      rem[v] = r;
+      color[v] = kBlack;
+      stack.pop_back();
+    }
+  }
+  if (overflow) return kErange;
+
+  // O6 + O7 + O8
+  std::vector<int32_t> ready_ids;
+  for (int64_t v = 0; v < N; ++v) {
+    if (done[v]) continue;
+    bool all_done = true;
+    for (int32_t e = dep_off[v]; e < dep_off[v + 1]; ++e)
+      if (!done[dep_idx[e]]) { all_done = false; break; }
+    if (all_done) ready_ids.push_back(int32_t(v));
+  }
+  const int64_t R = int64_t(ready_ids.size());
+  std::vector<int64_t> slack(N, 0), cost(N, 0);
+  std::vector<int32_t> route(N, -1);
+  for (int64_t k = 0; k < R; ++k) {
+    int32_t v = ready_ids[k];
+    slack[v] = (deadline[wf[v]] - now) - rem[v];
+    int64_t best = INT64_MAX;
+    int32_t arg = -1;
+    for (int64_t i = 0; i < M; ++i) {
+      if (inst_type[i] != type[v]) continue;
+      int64_t c = inst_load[i] + (est[v] * 1000) / inst_speed[i];
+      if (loc[v] >= 0 && loc[v] != i) c += mig;
+      if (c < best) { best = c; arg = int32_t(i); }
+    }
+    route[v] = arg;
+    cost[v] = best;
+  }
+
+  // O9: the full key (slack, wf, v) is a total order, so the result is unique.
+  std::vector<int32_t> order(ready_ids);
+  std::sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+    if (slack[a] != slack[b]) return slack[a] < slack[b];
+    if (wf[a] != wf[b]) return wf[a] < wf[b];
+    return a < b;
+  });
+
+  // O10
+  if (rem_out) std::memcpy(rem_out, rem.data(), sizeof(int64_t) * N);
+  for (int64_t k = 0; k < R; ++k) {
+    int32_t v = order[k];
+    order_out[k] = v;
+    slack_out[k] = slack[v];
+    route_out[k] = route[v];
+    if (cost_out) cost_out[k] = cost[v];
+  }
+  if (n_ready_out) *n_ready_out = R;
+  return kOk;
+}
+
+}  // extern "C"

@@ -1,0 +1,419 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+The oracle is the reference every GPU result is compared with, so it is
+checked here against things other than itself:
+
+* hand-worked examples (tests/golden/, derivations written in each file);
+* exhaustive path enumeration on small random DAGs (remaining work is the
+  longest est'-weighted path, Section 6.3's "least remaining work");
+* a push-based replay of value deliveries for readiness (Section 4.3.1,
+  property 3), a different formulation from the oracle's pull check;
+* the optimality certificate of longest paths (edge inequality, equality on
+  some consumer, sinks equal their own service time) on the full configs;
+* closed forms (chains, unit service times, the map/reduce shape);
+* the routing special case with equal loads and speeds, and invariances;
+* uniqueness of a sorted permutation under a total order;
+* every validation and error rule of the boundary.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from golden_io import load as load_golden, names as golden_names
+from paper_2601_05109_amd import workloads as wl
+
+INT64_MAX = np.iinfo(np.int64).max
+
+
+# ---------------------------------------------------------------- helpers
+
+def consumers(p):
+    succ = [[] for _ in range(p.n_nodes)]
+    for v in range(p.n_nodes):
+        for e in range(p.dep_off[v], p.dep_off[v + 1]):
+            succ[int(p.dep_idx[e])].append(v)
+    return succ
+
+
+def brute_force_rem(p):
+    """Longest path by enumerating every directed path from each node."""
+    N = p.n_nodes
+    succ = consumers(p)
+    w = [0 if p.done[v] else int(p.est_us[v]) for v in range(N)]
+    out = []
+    for v in range(N):
+        best = 0
+        stack = [(v, w[v])]
+        while stack:
+            u, s = stack.pop()
+            best = max(best, s)
+            for c in succ[u]:
+                stack.append((c, s + w[c]))
+        out.append(best)
+    return np.array(out, np.int64)
+
+
+def push_replay_ready(p):
+    """Replay the pushes: each done future delivers its value once per
+    dependency edge to its consumers; a not-done future that has received every
+    delivery it waits for can run."""
+    N = p.n_nodes
+    need = np.diff(p.dep_off.astype(np.int64))
+    got = np.zeros(N, np.int64)
+    succ = consumers(p)
+    for u in range(N):
+        if p.done[u]:
+            for c in succ[u]:
+                got[c] += 1
+    return {v for v in range(N) if not p.done[v] and got[v] == need[v]}
+
+
+def assert_sorted_permutation(p, r):
+    """order is the ready set, strictly increasing in (slack, wf, v): a sorted
+    permutation under a total order is unique, so this pins the order."""
+    keys = [(int(s), int(p.wf[v]), int(v)) for v, s in zip(r.order, r.slack)]
+    assert all(a < b for a, b in zip(keys, keys[1:]))
+    assert len(set(r.order.tolist())) == len(r.order)
+
+
+def rem_certificate(p, rem):
+    """Longest-path certificate: for every edge u->c, rem[u] >= est'[u] + rem[c];
+    every node with consumers attains equality on one of them; a node without
+    consumers has rem = est'.  By induction over a reverse topological order,
+    these determine rem uniquely."""
+    N = p.n_nodes
+    e = np.where(p.done.astype(bool), 0, p.est_us).astype(np.int64)
+    child = np.repeat(np.arange(N), np.diff(p.dep_off.astype(np.int64)))
+    par = p.dep_idx.astype(np.int64)
+    lhs = rem[par]
+    rhs = e[par] + rem[child]
+    assert np.all(lhs >= rhs), "edge inequality violated"
+    best = np.full(N, -1, np.int64)
+    np.maximum.at(best, par, rem[child])
+    has = best >= 0
+    assert np.all(rem[has] == e[has] + best[has]), "no tight consumer"
+    assert np.all(rem[~has] == e[~has]), "sink base case"
+
+
+# ---------------------------------------------------------------- golden
+
+@pytest.mark.parametrize("name", golden_names())
+def test_golden_examples(name):
+    p, exp = load_golden(name)
+    r = oracle.run(p)
+    assert r.status == exp["status"][0]
+    assert r.rem.tolist() == exp["rem"]
+    assert r.order.tolist() == exp["order"]
+    assert r.slack.tolist() == exp["slack"]
+    assert r.route.tolist() == exp["route"]
+    assert r.cost.tolist() == exp["cost"]
+
+
+# ---------------------------------------------------------------- brute force
+
+@pytest.mark.parametrize("seed", range(120))
+def test_small_dags_against_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    p = wl.random_dag(seed, n_nodes=int(rng.integers(1, 11)), n_workflows=int(rng.integers(1, 4)),
+                      n_instances=int(rng.integers(0, 6)), n_types=int(rng.integers(1, 4)))
+    r = oracle.run(p)
+    assert r.status == oracle.OK
+    np.testing.assert_array_equal(r.rem, brute_force_rem(p))
+    assert set(r.order.tolist()) == push_replay_ready(p)
+    assert_sorted_permutation(p, r)
+    rem_certificate(p, r.rem)
+
+
+def test_brute_force_catches_planted_mistakes():
+    """The brute force and the certificate are sharp enough to reject a
+    perturbed rem (one wrong entry anywhere)."""
+    p = wl.random_dag(7, n_nodes=9, n_workflows=1, p_edge=0.5, zero_est=0.0, p_done=0.0)
+    r = oracle.run(p)
+    for v in range(p.n_nodes):
+        bad = r.rem.copy()
+        bad[v] += 1
+        assert not np.array_equal(bad, brute_force_rem(p))
+        with pytest.raises(AssertionError):
+            rem_certificate(p, bad)
+
+
+# ---------------------------------------------------------------- configs
+
+@pytest.fixture(scope="module", params=[0, 1, 2, 3])
+def config_run(request):
+    p = wl.CONFIGS[request.param]()
+    return request.param, p, oracle.run(p)
+
+
+def test_config_certificate(config_run):
+    _, p, r = config_run
+    assert r.status == oracle.OK
+    rem_certificate(p, r.rem)
+
+
+def test_config_order_and_ready(config_run):
+    c, p, r = config_run
+    assert_sorted_permutation(p, r)
+    ready = np.zeros(p.n_nodes, bool)
+    ready[r.order] = True
+    # readiness by definition, vectorised: not done and no not-done parent
+    child = np.repeat(np.arange(p.n_nodes), np.diff(p.dep_off.astype(np.int64)))
+    blocked = np.zeros(p.n_nodes, bool)
+    blocked[child[p.done[p.dep_idx] == 0]] = True
+    np.testing.assert_array_equal(ready, (p.done == 0) & ~blocked)
+    # stable-permutation property: the order equals a stable sort by
+    # (slack, wf) of the ready ids listed in ascending id order
+    ids = np.flatnonzero(ready)
+    slack_of = dict(zip(r.order.tolist(), r.slack.tolist()))
+    s = np.array([slack_of[v] for v in ids], np.int64)
+    st = ids[np.lexsort((p.wf[ids], s))]    # lexsort is stable
+    np.testing.assert_array_equal(st, r.order)
+
+
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_windowed_ready_locality(cfg):
+    """With the first 9 of 32 futures done and parents within the previous 8,
+    every ready future has local index 9..16, and local index 9 is always ready."""
+    p = wl.CONFIGS[cfg]()
+    r = oracle.run(p)
+    local = r.order % 32
+    assert local.min() >= 9 and local.max() <= 16
+    assert set(np.flatnonzero(p.wf >= 0)[9::32].tolist()) <= set(r.order.tolist())
+
+
+def test_mapreduce_closed_form():
+    """Root done -> tools -> reduce: rem[reduce] = est[reduce],
+    rem[tool] = est[tool] + est[reduce], rem[root] = max tool est + est[reduce];
+    the ready set is exactly the tools, with slack deadline - now - rem."""
+    p = wl.wide_mapreduce(W=8, fan=64)
+    r = oracle.run(p)
+    n = 66
+    est = p.est_us.reshape(8, n)
+    rem = r.rem.reshape(8, n)
+    np.testing.assert_array_equal(rem[:, -1], est[:, -1])
+    np.testing.assert_array_equal(rem[:, 1:-1], est[:, 1:-1] + est[:, -1:])
+    np.testing.assert_array_equal(rem[:, 0], est[:, 1:-1].max(axis=1) + est[:, -1])
+    tools = np.arange(8 * n).reshape(8, n)[:, 1:-1].reshape(-1)
+    assert sorted(r.order.tolist()) == tools.tolist()
+    w = p.wf[r.order]
+    np.testing.assert_array_equal(r.slack, p.deadline_us[w] - p.now_us - r.rem[r.order])
+
+
+def test_chain_suffix_sums():
+    N = 50
+    rng = np.random.default_rng(3)
+    est = rng.integers(0, 10**6, N).astype(np.int64)
+    done = (rng.random(N) < 0.3).astype(np.uint8)
+    p = wl.Problem("chain", 0, 0, np.zeros(N, np.int32), np.zeros(N, np.int32), est, done,
+                   -np.ones(N, np.int32), np.r_[0, 0, np.arange(1, N)].astype(np.int32),
+                   np.arange(N - 1).astype(np.int32), np.array([10**9], np.int64),
+                   np.zeros(0, np.int32), np.zeros(0, np.int64), np.zeros(0, np.int32), True)
+    r = oracle.run(p)
+    w = np.where(done == 1, 0, est)
+    np.testing.assert_array_equal(r.rem, np.cumsum(w[::-1])[::-1])
+
+
+def kahn_height(p):
+    """Longest path length in edges, by peeling sinks level by level."""
+    N = p.n_nodes
+    succ = consumers(p)
+    outdeg = np.array([len(s) for s in succ])
+    par = [[] for _ in range(N)]
+    for v in range(N):
+        par[v] = [int(u) for u in p.dep_idx[p.dep_off[v]:p.dep_off[v + 1]]]
+    h = np.zeros(N, np.int64)
+    frontier = [v for v in range(N) if outdeg[v] == 0]
+    level = 0
+    while frontier:
+        nxt = []
+        for v in frontier:
+            h[v] = level
+            for u in par[v]:
+                outdeg[u] -= 1
+                if outdeg[u] == 0:
+                    nxt.append(u)
+        frontier = nxt
+        level += 1
+    return h
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_unit_service_time_is_height(seed):
+    p = wl.deep_chains(seed=seed, W=4) if seed < 2 else wl.tiny(seed=seed)
+    q = p.copy(est_us=np.ones(p.n_nodes, np.int64), done=np.zeros(p.n_nodes, np.uint8))
+    r = oracle.run(q)
+    np.testing.assert_array_equal(r.rem, kahn_height(q) + 1)
+
+
+def test_relabelled_ids_give_relabelled_result():
+    """Renaming node ids renames rem and order (ties within a workflow follow
+    the new ids, so only the multiset of (slack, route, cost) per node is
+    compared)."""
+    p = wl.tiny()
+    perm = np.random.default_rng(1).permutation(p.n_nodes)
+    q = wl.relabel(p, perm)
+    a, b = oracle.run(p), oracle.run(q)
+    np.testing.assert_array_equal(b.rem[perm], a.rem)
+    da = {int(perm[v]): (s, rt, c) for v, s, rt, c in zip(a.order, a.slack, a.route, a.cost)}
+    db = {int(v): (s, rt, c) for v, s, rt, c in zip(b.order, b.slack, b.route, b.cost)}
+    assert da == db
+
+
+# ---------------------------------------------------------------- routing
+
+def test_route_equal_loads_closed_form():
+    """Equal loads and speed 1000 everywhere: the future goes where its state
+    is when that instance has its type, otherwise to the lowest-index instance
+    of its type, and to -1 when there is none."""
+    p = wl.tiny()
+    M = p.n_instances
+    q = p.copy(inst_load_us=np.full(M, 777, np.int64), inst_speed_permille=np.full(M, 1000, np.int32))
+    r = oracle.run(q)
+    for v, rt in zip(r.order.tolist(), r.route.tolist()):
+        t, l = int(q.type[v]), int(q.loc[v])
+        same = np.flatnonzero(q.inst_type == t)
+        if same.size == 0:
+            assert rt == -1
+        elif l >= 0 and q.inst_type[l] == t:
+            assert rt == l
+        else:
+            assert rt == same[0]
+
+
+def test_route_invariant_to_common_load_shift():
+    p = wl.tiny()
+    r0 = oracle.run(p)
+    r1 = oracle.run(p.copy(inst_load_us=p.inst_load_us + 123_456))
+    np.testing.assert_array_equal(r0.route, r1.route)
+    ok = r0.route >= 0
+    np.testing.assert_array_equal(r1.cost[ok], r0.cost[ok] + 123_456)
+
+
+def test_route_prohibitive_migration_keeps_state_local():
+    p = wl.tiny()
+    r = oracle.run(p.copy(migration_cost_us=1 << 60))
+    for v, rt in zip(r.order.tolist(), r.route.tolist()):
+        l = int(p.loc[v])
+        if l >= 0 and p.inst_type[l] == p.type[v]:
+            assert rt == l
+
+
+def test_route_no_instances():
+    p = wl.tiny()
+    q = p.copy(inst_type=np.zeros(0, np.int32), inst_load_us=np.zeros(0, np.int64),
+               inst_speed_permille=np.zeros(0, np.int32), loc=np.full(p.n_nodes, -1, np.int32))
+    r = oracle.run(q)
+    assert r.status == oracle.OK
+    assert np.all(r.route == -1) and np.all(r.cost == INT64_MAX)
+
+
+# ---------------------------------------------------------------- degenerate
+
+def _single(est=5, done=0):
+    return wl.Problem("one", 10, 7, np.zeros(1, np.int32), np.zeros(1, np.int32),
+                      np.array([est], np.int64), np.array([done], np.uint8), np.array([0], np.int32),
+                      np.array([0, 0], np.int32), np.zeros(0, np.int32), np.array([20], np.int64),
+                      np.array([0], np.int32), np.array([3], np.int64), np.array([1000], np.int32), True)
+
+
+def test_single_node():
+    r = oracle.run(_single())
+    assert r.status == 0 and r.order.tolist() == [0] and r.slack.tolist() == [5]
+    assert r.route.tolist() == [0] and r.cost.tolist() == [8] and r.rem.tolist() == [5]
+
+
+def test_empty_problem():
+    p = _single()
+    q = p.copy(wf=np.zeros(0, np.int32), type=np.zeros(0, np.int32), est_us=np.zeros(0, np.int64),
+               done=np.zeros(0, np.uint8), loc=np.zeros(0, np.int32), dep_off=np.array([0], np.int32))
+    r = oracle.run(q)
+    assert r.status == 0 and r.n_ready == 0
+
+
+def test_all_done():
+    p = wl.tiny()
+    r = oracle.run(p.copy(done=np.ones(p.n_nodes, np.uint8)))
+    assert r.status == 0 and r.n_ready == 0
+    assert np.all(r.rem == 0)
+
+
+def test_no_edges_everything_ready():
+    p = wl.tiny()
+    N = p.n_nodes
+    q = p.copy(dep_off=np.zeros(N + 1, np.int32), dep_idx=np.zeros(0, np.int32),
+               done=np.zeros(N, np.uint8))
+    r = oracle.run(q)
+    assert r.n_ready == N
+    np.testing.assert_array_equal(r.rem, q.est_us)
+
+
+# ---------------------------------------------------------------- errors
+
+def _bad(field, idx, value, base=None):
+    p = (base or wl.tiny()).copy()
+    getattr(p, field)[idx] = value
+    return p
+
+
+@pytest.mark.parametrize("case", [
+    ("wf", 5, -1), ("wf", 5, 64), ("type", 3, -1), ("loc", 7, -2), ("loc", 7, 16),
+    ("est_us", 9, -1), ("est_us", 9, (1 << 40) + 1), ("done", 4, 2),
+    ("dep_idx", 10, -1), ("dep_idx", 10, 2048), ("dep_idx", 10, 40),   # 40 lies in workflow 1
+    ("dep_off", 0, 1), ("dep_off", 2048, 1), ("inst_type", 0, -1),
+    ("inst_speed_permille", 2, 0), ("inst_load_us", 1, -1), ("inst_load_us", 1, (1 << 60) + 1),
+    ("deadline_us", 3, wl.NOW_US + (1 << 61) + 1),
+])
+def test_einval_rules(case):
+    assert oracle.run(_bad(*case)).status == oracle.EINVAL
+
+
+def test_einval_decreasing_offsets():
+    p = wl.tiny().copy()
+    p.dep_off[100], p.dep_off[101] = p.dep_off[101], p.dep_off[100]
+    if p.dep_off[100] == p.dep_off[101]:
+        pytest.skip("equal offsets")
+    assert oracle.run(p).status == oracle.EINVAL
+
+
+@pytest.mark.parametrize("ov", [dict(M=1025), dict(N=-1), dict(now=(1 << 61) + 1),
+                                dict(mig=-1), dict(mig=(1 << 60) + 1), dict(E=5),
+                                dict(wf=None), dict(dep_idx=None), dict(deadline_us=None),
+                                dict(inst_speed_permille=None)])
+def test_einval_scalars_and_nulls(ov):
+    assert oracle.run(wl.tiny(), override=ov).status == oracle.EINVAL
+
+
+def test_ecycle_self_loop_and_cycle():
+    p = wl.tiny().copy()
+    v = 12
+    p.dep_idx[p.dep_off[v]] = v          # self-dependency
+    assert oracle.run(p).status == oracle.ECYCLE
+    # 0 -> 1 -> 2 -> 0 (node 0 depends on 2, node 1 on 0, node 2 on 1)
+    N = 3
+    c = wl.Problem("cyc", 0, 0, np.zeros(N, np.int32), np.zeros(N, np.int32), np.ones(N, np.int64),
+                   np.zeros(N, np.uint8), -np.ones(N, np.int32), np.array([0, 1, 2, 3], np.int32),
+                   np.array([2, 0, 1], np.int32), np.array([100], np.int64), np.zeros(0, np.int32),
+                   np.zeros(0, np.int64), np.zeros(0, np.int32), True)
+    assert oracle.run(c).status == oracle.ECYCLE
+
+
+def test_erange_and_precedence():
+    N = 4100
+    # a chain of 4100 futures of 2^40 us each: rem reaches ~2^52, fine
+    chain = lambda est, n: wl.Problem(
+        "chain", 0, 0, np.zeros(n, np.int32), np.zeros(n, np.int32), np.full(n, est, np.int64),
+        np.zeros(n, np.uint8), -np.ones(n, np.int32), np.r_[0, 0, np.arange(1, n)].astype(np.int32),
+        np.arange(n - 1).astype(np.int32), np.array([0], np.int64), np.zeros(0, np.int32),
+        np.zeros(0, np.int64), np.zeros(0, np.int32), True)
+    assert oracle.run(chain(1 << 40, N)).status == oracle.OK
+    # 2^22 + 1 futures of 2^40 us exceed 2^62
+    big = chain(1 << 40, (1 << 22) + 1)
+    assert oracle.run(big).status == oracle.ERANGE
+    # a cycle takes precedence over an overflow
+    cyc = big.copy()
+    cyc.dep_idx[0] = 5       # node 1 depends on node 5, which descends from it
+    assert oracle.run(cyc).status == oracle.ECYCLE
+    # invalid input takes precedence over both
+    inv = cyc.copy()
+    inv.type[3] = -4
+    assert oracle.run(inv).status == oracle.EINVAL
