@@ -1,0 +1,186 @@
+#!/usr/bin/env python3
+"""Benchmark of the global policy pass on one MI355X.
+
+One step = one full pass (validation, remaining critical path, readiness,
+slack, routing, ordering) over the paper-scale snapshot: 4,096 workflows x 32
+futures = 131,072 in-flight futures (the largest point of the paper's
+scalability study, Section 6.4), inputs already resident in HBM.
+
+Prints one JSON line: futures/s per pass (whole job), ms per pass, the
+roofline of the dominant kernel (per-kernel HIP-event timing recorded by the
+library on its own stream during a second timed loop), and the CPU oracle timed
+on this host as a baseline.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload paper-scale]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+
+def alg_bytes(kernel: str, N: int, E: int, R: int, W: int, M: int, grouped: bool) -> float:
+    """Algorithmic bytes one launch of a kernel must move (each input read once,
+    each output written once; scratch traffic an implementation adds is not
+    counted)."""
+    if kernel == "sweep":
+        b = 21 * N + 4 * E + 32 * R + 12 * W + 32 * M
+        if grouped:
+            b += 4 * N + 4 * E
+        return float(b)
+    if kernel.startswith("sort_pass"):
+        return float(24 * R)
+    if kernel == "emit":
+        return float(48 * R)
+    if kernel == "nodes":
+        return float(4 * N + 4 * N + 8 * N + 1 * N + 4 * N + 4 * (N + 1) + 8 * W)
+    if kernel == "sort_hist":
+        return float(8 * R)
+    return 0.0
+
+
+def workload(name: str):
+    from paper_2601_05109_amd import workloads as wl
+    if name == "paper-scale":
+        return wl.paper_scale()
+    if name == "tiny":
+        return wl.tiny()
+    if name == "deep-chains":
+        return wl.deep_chains()
+    if name == "wide-mapreduce":
+        return wl.wide_mapreduce()
+    raise SystemExit(f"unknown workload {name}")
+
+
+def cpu_baseline(p, budget_s: float = 12.0) -> dict:
+    """The oracle as it stands, single-threaded on this host, repeated on the
+    same snapshot for about ``budget_s`` seconds."""
+    import oracle
+    oracle.build()
+    try:
+        os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
+    except (AttributeError, OSError):
+        pass
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        r = oracle.run(p)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    assert r.status == 0
+    return {"value": p.n_nodes * reps / el, "unit": "futures/s", "cores": 1, "kind": "oracle",
+            "sample": f"{reps} full passes of the oracle over the same {p.n_nodes}-future snapshot "
+                      f"({el:.1f} s, one thread pinned to one core)",
+            "ms_per_pass": 1e3 * el / reps}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="paper-scale")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the pass shards by "
+              "workflow across GPUs by design but that path is not built", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2601_05109_amd import nalar
+
+    p = workload(args.workload)
+    N, E, W, M = p.n_nodes, p.n_edges, p.n_workflows, p.n_instances
+    dev = torch.device("cuda", 0)
+    dp = nalar.DeviceProblem.from_host(p, dev)
+    out = nalar.DeviceResult.alloc(N, dev)
+    stream = torch.cuda.current_stream(dev)
+    pol = nalar.Policy(device=0, stream=stream, reserve_nodes=N, reserve_workflows=W)
+    cp = dp.c_struct()
+
+    def one_pass():
+        cr = out.c_struct()
+        rc = nalar.nalar_policy_pass(pol.handle, cp, cr)
+        if rc != nalar.NALAR_OK:
+            raise RuntimeError(f"pass failed {rc}: {pol.last_error()}")
+        return int(cr.n_ready)
+
+    for _ in range(args.warmup):
+        R = one_pass()
+    torch.cuda.synchronize()
+
+    # timed region 1: whole passes (the ABI call is synchronous)
+    lat = []
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        t = time.perf_counter()
+        one_pass()
+        lat.append(time.perf_counter() - t)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall0
+    gpu_ms = ev0.elapsed_time(ev1)
+    ms_per_step = 1e3 * wall / args.steps
+
+    # timed region 2: the same passes with per-kernel events on the library stream
+    pol.set_timing(True)
+    acc: dict[str, list[float]] = {}
+    for _ in range(args.steps):
+        one_pass()
+        for name, ms in pol.timing():
+            acc.setdefault(name, []).append(ms)
+    pol.set_timing(False)
+    kern = {k: statistics.mean(v) for k, v in acc.items()}
+    grouped = not p.wf_contiguous
+    dom = max((k for k in kern if alg_bytes(k, N, E, R, W, M, grouped) > 0), key=lambda k: kern[k])
+    b_dom = alg_bytes(dom, N, E, R, W, M, grouped)
+    achieved = b_dom / (kern[dom] * 1e-3) / 1e9
+
+    lat_us = sorted(1e6 * x for x in lat)
+    res = {
+        "metric": "futures/sec per global policy pass",
+        "value": N / (ms_per_step * 1e-3),
+        "unit": "futures/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic (seeded generator, paper-scale shape)",
+        "config": {"workload": f"{p.name}: {W} workflows x {N // max(W, 1)} futures = {N} futures, "
+                               f"{E} dependencies, {R} ready, K=8 types, {M} instances",
+                   "n_futures": N, "n_ready": R},
+        "latency_us": {"p50": lat_us[len(lat_us) // 2], "p99": lat_us[min(len(lat_us) - 1, int(0.99 * len(lat_us)))],
+                       "min": lat_us[0], "gpu_event_mean": 1e3 * gpu_ms / args.steps},
+        "kernels_us": {k: round(1e3 * v, 2) for k, v in kern.items()},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "alg_bytes_per_launch": b_dom},
+    }
+    pol.close()
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline(p, args.cpu_seconds)
+    print(json.dumps(res))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

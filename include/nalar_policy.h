@@ -1,0 +1,188 @@
+/*
+ * nalar_policy.h -- C ABI of the MI355X global policy pass.
+ *
+ * The global controller of Nalar's two-level control (Section 4.1) runs one
+ * periodic, single-threaded policy loop (Section 4.2).  One iteration of its
+ * policy computation over the dependency graph of every in-flight future is a
+ * "pass":
+ *
+ *   1. remaining critical path of every future: the longest service-time
+ *      path from the future through its consumers (the "least remaining work"
+ *      key of the SRTF policy, Section 6.3, taken over the whole DAG);
+ *   2. readiness: a future is runnable once it is not done and every future it
+ *      depends on is done (push-based readiness, Section 4.3.1, property 3);
+ *   3. priority: ready futures ranked by deadline slack, most urgent first
+ *      (set_priority, Table 2);
+ *   4. routing: each ready future sent to the instance of its component type
+ *      with the least load plus speed-scaled service time plus a migration
+ *      penalty when its managed state lives on another instance (route and
+ *      migrate, Table 2; state locality, Section 4.3.2).
+ *
+ * All times are int64 fixed-point microseconds and every result is an exact
+ * integer: the GPU output is bit-identical to the plain definition.
+ *
+ * Calls are synchronous: nalar_policy_pass returns after its GPU work on the
+ * handle's stream has finished.  A handle is not thread-safe; use one handle
+ * per host thread.  All integers are little-endian and naturally aligned.
+ */
+#ifndef NALAR_POLICY_H
+#define NALAR_POLICY_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes.  On any non-OK return the outputs are unspecified and the
+ * handle stays usable.  When several apply, the first in this order wins:
+ * EINVAL, ECYCLE, ERANGE.  ENOMEM and EDEVICE report the library's own
+ * failures (allocation, HIP runtime). */
+enum {
+  NALAR_OK = 0,
+  NALAR_EINVAL = -1,  /* a rule of nalar_problem or nalar_policy_config broken  */
+  NALAR_ECYCLE = -2,  /* the dependency graph has a cycle (a self-loop counts)  */
+  NALAR_ERANGE = -3,  /* a remaining critical path exceeds NALAR_REM_MAX        */
+  NALAR_ENOMEM = -4,  /* device or pinned host allocation failed                */
+  NALAR_EDEVICE = -5  /* a HIP runtime call failed; see nalar_policy_last_error */
+};
+
+/* Limits of the ABI (values outside them are NALAR_EINVAL). */
+#define NALAR_MAX_NODES      (INT64_C(1) << 30)
+#define NALAR_MAX_EDGES      (INT64_C(2147483647))
+#define NALAR_MAX_WORKFLOWS  (INT64_C(1) << 30)
+#define NALAR_MAX_INSTANCES  1024
+#define NALAR_EST_MAX        (INT64_C(1) << 40)  /* service time, us            */
+#define NALAR_LOAD_MAX       (INT64_C(1) << 60)  /* instance load, us            */
+#define NALAR_MIG_MAX        (INT64_C(1) << 60)  /* migration penalty, us        */
+#define NALAR_HORIZON_MAX    (INT64_C(1) << 61)  /* |now|, |deadline - now|      */
+#define NALAR_REM_MAX        (INT64_C(1) << 62)  /* remaining critical path, us  */
+
+/* nalar_problem.flags */
+#define NALAR_WF_CONTIGUOUS  1u  /* the nodes of workflow w are exactly the ids
+                                    [first_w, first_{w+1}) with first ascending in
+                                    w, i.e. wf[] is non-decreasing.  The caller
+                                    promises it; a violation is NALAR_EINVAL.
+                                    Without it the library groups nodes by
+                                    workflow itself (one extra sort).           */
+
+/* nalar_policy_config.flags (tuning and testing; 0 is the normal setting) */
+#define NALAR_FORCE_GLOBAL_SWEEP 1u  /* keep every workflow's sweep state in HBM
+                                        instead of LDS (exercises the path used
+                                        for workflows too large for LDS)         */
+
+typedef struct nalar_policy nalar_policy;   /* opaque handle */
+
+/* Creation-time settings.  Host memory, read during nalar_policy_create only. */
+typedef struct {
+  int32_t device;             /* HIP device ordinal                               */
+  uint32_t flags;             /* NALAR_FORCE_GLOBAL_SWEEP or 0                    */
+  void* stream;               /* hipStream_t the pass runs on; NULL = null stream */
+  int64_t reserve_nodes;      /* scratch pre-size hints (0 = size on first pass)  */
+  int64_t reserve_edges;
+  int64_t reserve_workflows;
+} nalar_policy_config;
+
+/* One snapshot of the global view (Table 3 future metadata, the managed
+ * state layer's location of each future's state, and the instance table).
+ * Struct in host memory; every array pointer is a DEVICE pointer, owned by the
+ * caller and only read during the call.  N = n_nodes, E = n_edges,
+ * W = n_workflows, M = n_instances. */
+typedef struct {
+  int64_t n_nodes;            /* [0, NALAR_MAX_NODES]                             */
+  int64_t n_edges;            /* [0, NALAR_MAX_EDGES]; 0 when N = 0              */
+  int64_t n_workflows;        /* [0, NALAR_MAX_WORKFLOWS]                         */
+  int64_t n_instances;        /* [0, NALAR_MAX_INSTANCES]                         */
+  int64_t now_us;             /* |now_us| <= NALAR_HORIZON_MAX                    */
+  int64_t migration_cost_us;  /* penalty for running a future away from the
+                                 instance holding its state, [0, NALAR_MIG_MAX]   */
+  uint32_t flags;             /* NALAR_WF_CONTIGUOUS or 0                         */
+  uint32_t reserved;          /* must be 0                                        */
+  const int32_t* wf;          /* [N] workflow (session) of each future, [0, W)    */
+  const int32_t* type;        /* [N] component type, >= 0                         */
+  const int64_t* est_us;      /* [N] estimated service time, [0, NALAR_EST_MAX]   */
+  const uint8_t* done;        /* [N] 1 = value materialised, 0 = not; else EINVAL */
+  const int32_t* loc;         /* [N] instance holding the future's managed state,
+                                 [0, M), or -1 for none                           */
+  const int32_t* dep_off;     /* [N+1] dependency CSR: dep_off[0] = 0,
+                                 non-decreasing, dep_off[N] = E                   */
+  const int32_t* dep_idx;     /* [E] futures each future depends on, in [0, N),
+                                 same workflow (else EINVAL), duplicates allowed;
+                                 a future listing itself is a cycle (ECYCLE)      */
+  const int64_t* deadline_us; /* [W] workflow deadline, |deadline - now| <=
+                                 NALAR_HORIZON_MAX                                */
+  const int32_t* inst_type;   /* [M] component type of each instance, >= 0       */
+  const int64_t* inst_load_us;/* [M] queued work, [0, NALAR_LOAD_MAX]            */
+  const int32_t* inst_speed_permille; /* [M] speed relative to nominal, >= 1      */
+} nalar_problem;
+
+/* Outputs.  Struct in host memory; array pointers are DEVICE pointers, owned by
+ * the caller, each with capacity >= n_nodes entries (the ready count R is not
+ * known before the call).  Entries past R are left untouched. */
+typedef struct {
+  int64_t* rem_us;      /* [N] remaining critical path of every future, or NULL */
+  int32_t* order;       /* [R] ready futures, ascending (slack, wf, id)          */
+  int64_t* slack_us;    /* [R] deadline[wf] - now - rem, aligned with order      */
+  int32_t* route;       /* [R] chosen instance, or -1 when no instance has the
+                           future's type; aligned with order                     */
+  int64_t* cost_us;     /* [R] cost of the chosen instance (INT64_MAX when route
+                           is -1), aligned with order; or NULL                   */
+  int64_t n_ready;      /* HOST field: R, written before a NALAR_OK return       */
+} nalar_result;
+
+/*
+ * Create a handle bound to cfg->device and cfg->stream.  *out receives the
+ * handle (NULL on failure).  Returns NALAR_OK, NALAR_EINVAL (NULL arguments,
+ * negative reserve hints, unknown flags), NALAR_ENOMEM or NALAR_EDEVICE.
+ * The library owns only its scratch memory (device and pinned host), which it
+ * allocates here (sized by the reserve hints) and grows, never shrinks, inside
+ * nalar_policy_pass.
+ */
+int nalar_policy_create(const nalar_policy_config* cfg, nalar_policy** out);
+
+/*
+ * Run one pass over the snapshot *p and write *r.  Definition of each output:
+ *   est'[v]  = done[v] ? 0 : est_us[v]
+ *   rem[v]   = est'[v] + max(0, max over futures s listing v in their
+ *              dependencies of rem[s])
+ *   ready[v] = !done[v] and done[u] for every u in v's dependencies
+ *   slack[v] = (deadline_us[wf[v]] - now_us) - rem[v]
+ *   cost(v,i)= inst_load_us[i] + floor(est_us[v]*1000 / inst_speed_permille[i])
+ *              + (loc[v] >= 0 && loc[v] != i ? migration_cost_us : 0)
+ *   route[v] = the instance i with inst_type[i] == type[v] minimising
+ *              (cost(v,i), i) lexicographically (the lowest index wins ties),
+ *              or -1 with cost INT64_MAX when there is none
+ *   order    = the ready futures sorted by (slack, wf, id) ascending
+ * Synchronous.  NULL p, r, or a required array (a node array when N > 0,
+ * dep_idx when E > 0, deadline_us when W > 0, an instance array when M > 0,
+ * order/slack_us/route when N > 0) is NALAR_EINVAL.  Error precedence and the
+ * state of the outputs after an error are as described at the return codes.
+ */
+int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r);
+
+/* Release the handle and its scratch.  NULL-safe.  Waits for the handle's
+ * stream first. */
+void nalar_policy_destroy(nalar_policy* h);
+
+/* Message describing the last non-OK return on this handle ("" if none).  The
+ * string is owned by the handle and valid until its next call.  h may be NULL
+ * (returns the message of the last failed nalar_policy_create on this thread). */
+const char* nalar_policy_last_error(const nalar_policy* h);
+
+/* Per-kernel timing of the following passes, measured with HIP events recorded
+ * on the handle's stream around each kernel (enable != 0 turns it on). */
+int nalar_policy_set_timing(nalar_policy* h, int enable);
+
+/* Kernel durations of the last timed pass, in milliseconds: names[i] (static
+ * strings owned by the library) and ms[i] for i < *count.  cap is the capacity
+ * of both arrays; *count receives the number of kernels the pass launched
+ * (entries past cap are dropped).  Returns NALAR_EINVAL if timing is off or no
+ * timed pass has run. */
+int nalar_policy_get_timing(const nalar_policy* h, const char** names, float* ms, int cap,
+                            int* count);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NALAR_POLICY_H */

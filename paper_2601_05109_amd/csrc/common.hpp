@@ -1,0 +1,228 @@
+// Device-side helpers shared by the policy-pass kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "nalar_policy.h"
+
+namespace nalar {
+
+// Status word bits (ORed by any kernel that finds a problem).
+constexpr uint32_t kStInval = 1u;
+constexpr uint32_t kStCycle = 2u;
+constexpr uint32_t kStRange = 4u;
+
+constexpr int kWave = 64;
+constexpr int kRadixBits = 8;
+constexpr int kRadixBuckets = 1 << kRadixBits;
+constexpr int kMaxSortPasses = 8;    // 64-bit keys
+constexpr int kMaxGroupPasses = 4;   // workflow ids < 2^30
+constexpr int kSortThreads = 256;
+constexpr int kSortItems = 16;
+constexpr int kSortTile = kSortThreads * kSortItems;
+
+// Decoupled look-back words: [63:40] epoch, [39:38] flag, [37:0] value.
+constexpr int kLbValueBits = 38;
+constexpr uint64_t kLbValueMask = (uint64_t(1) << kLbValueBits) - 1;
+constexpr uint64_t kLbAgg = uint64_t(1) << 38;    // aggregate of this tile only
+constexpr uint64_t kLbInc = uint64_t(2) << 38;    // inclusive prefix
+constexpr uint32_t kEpochMask = (1u << 24) - 1;
+
+__host__ __device__ inline uint64_t lb_pack(uint32_t epoch, uint64_t flag, uint64_t value) {
+  return (uint64_t(epoch & kEpochMask) << 40) | flag | (value & kLbValueMask);
+}
+
+// Per-pass control block in device memory.  Initialised by the setup kernel
+// at the start of every pass.
+struct Ctrl {
+  uint32_t status;
+  uint32_t sort_npass;           // digit passes the slack sort needs
+  int64_t n_ready;
+  int64_t slack_min;
+  int64_t slack_max;
+  uint32_t wf_ticket;            // next workflow for the sweep's blocks
+  uint32_t pad0;
+  uint32_t tile_ticket[16];      // per radix pass: [0,8) slack sort, [8,12) grouping
+};
+
+// Instance table sorted by (type, original index), plus the sorted position of
+// every original index (for the instance that holds a future's state).
+struct ITab {
+  int64_t* load;      // [M]
+  double* inv_speed;  // [M] 1.0 / speed
+  int32_t* type;      // [M]
+  int32_t* idx;       // [M] original index
+  int32_t* speed;     // [M]
+  int32_t* pos_of;    // [M] sorted position of original index i
+};
+
+// ----------------------------------------------------------------- wave ops
+
+__device__ inline int lane_id() { return __lane_id(); }
+
+__device__ inline uint64_t ballot(bool p) { return __ballot(p); }
+
+__device__ inline uint32_t lanes_below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi(uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
+}
+
+__device__ inline uint64_t lanemask_lt() {
+  const int l = lane_id();
+  return l == 0 ? 0ull : (~0ull >> (64 - l));
+}
+
+__device__ inline int readlane_i32(int x, int lane) { return __builtin_amdgcn_readlane(x, lane); }
+
+__device__ inline int64_t shfl_xor_i64(int64_t x, int m) {
+  int lo = int(uint32_t(uint64_t(x)));
+  int hi = int(uint32_t(uint64_t(x) >> 32));
+  lo = __shfl_xor(lo, m, kWave);
+  hi = __shfl_xor(hi, m, kWave);
+  return int64_t((uint64_t(uint32_t(hi)) << 32) | uint32_t(lo));
+}
+
+__device__ inline int64_t wave_max_i64(int64_t x) {
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) {
+    int64_t y = shfl_xor_i64(x, m);
+    x = y > x ? y : x;
+  }
+  return x;
+}
+
+__device__ inline int64_t wave_min_i64(int64_t x) {
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) {
+    int64_t y = shfl_xor_i64(x, m);
+    x = y < x ? y : x;
+  }
+  return x;
+}
+
+__device__ inline int64_t wave_sum_i64(int64_t x) {
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) x += shfl_xor_i64(x, m);
+  return x;
+}
+
+// Inclusive scan over the wave (all 64 lanes active).
+__device__ inline uint32_t wave_incl_scan_u32(uint32_t x) {
+  const int l = lane_id();
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    uint32_t y = __shfl_up(x, d, kWave);
+    if (l >= d) x += y;
+  }
+  return x;
+}
+
+// ----------------------------------------------------------------- atomics
+
+template <typename T>
+__device__ inline T ld_relaxed_agent(const T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ inline void st_relaxed_agent(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ inline T ld_wg(const T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+template <typename T>
+__device__ inline void st_wg(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+template <typename T>
+__device__ inline T add_wg(T* p, T v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+template <typename T>
+__device__ inline T max_wg(T* p, T v) {
+  return __hip_atomic_fetch_max(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+template <typename T>
+__device__ inline T add_agent(T* p, T v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ inline void flag_status(Ctrl* c, uint32_t bits) {
+  __hip_atomic_fetch_or(&c->status, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Exclusive prefix over earlier tiles/workflows by decoupled look-back.  The
+// caller has already published its own aggregate.  Every earlier slot was
+// claimed (by ticket) before the caller's, by a block that publishes its
+// aggregate without waiting on anything, so the spin always ends.
+__device__ inline uint64_t lookback_exclusive(const uint64_t* words, int64_t slot, int64_t stride,
+                                              uint32_t epoch) {
+  uint64_t excl = 0;
+  const uint64_t want = uint64_t(epoch & kEpochMask);
+  for (int64_t t = slot - 1; t >= 0; --t) {
+    uint64_t w;
+    do {
+      w = ld_relaxed_agent(words + t * stride);
+    } while ((w >> 40) != want || (w & (kLbAgg | kLbInc)) == 0);
+    excl += w & kLbValueMask;
+    if (w & kLbInc) break;
+  }
+  return excl;
+}
+
+// ----------------------------------------------------------------- routing
+
+// floor(A / d) for 0 <= A < 2^53, 1 <= d < 2^31, exact.  The double product
+// A * RN(1/d) is within 0.25 of A/d (relative error <= 2^-52, A < 2^50 here),
+// so its floor is off by at most one; the remainder, computed exactly by an
+// FMA (it is an integer below 2^33 in magnitude), corrects it.
+__host__ __device__ inline int64_t floordiv_exact(double a, int32_t d, double inv_d) {
+  double q = floor(a * inv_d);
+  double r = fma(-q, double(d), a);
+  q += (r < 0.0) ? -1.0 : ((r >= double(d)) ? 1.0 : 0.0);
+  return int64_t(q);
+}
+
+// Route one ready future against the sorted instance table (in LDS).
+// Candidates are the instances of type t, visited in ascending original index.
+// The migration penalty applies to every candidate except the one holding the
+// future's state, so the best candidate is either the unpenalised holder or the
+// best candidate overall plus the penalty (ties broken by index).
+__device__ inline void route_future(int32_t t, int64_t est, int32_t loc, int32_t M, int64_t mig,
+                                    const int32_t* s_type, const int32_t* s_idx,
+                                    const int64_t* s_load, const int32_t* s_speed,
+                                    const double* s_inv, const int32_t* s_pos, int32_t& route,
+                                    int64_t& cost) {
+  int lo = 0, hi = M;
+  while (lo < hi) {  // first position with type >= t
+    int mid = (lo + hi) >> 1;
+    if (s_type[mid] < t) lo = mid + 1; else hi = mid;
+  }
+  const double a = double(est * 1000);
+  int64_t best = INT64_MAX;
+  int bj = -1;
+  for (int j = lo; j < M && s_type[j] == t; ++j) {
+    int64_t c = s_load[j] + floordiv_exact(a, s_speed[j], s_inv[j]);
+    if (c < best) { best = c; bj = j; }
+  }
+  if (bj < 0) { route = -1; cost = INT64_MAX; return; }
+  const int32_t bidx = s_idx[bj];
+  if (loc >= 0) {
+    const int pl = s_pos[loc];
+    if (s_type[pl] == t) {
+      const int64_t cl = s_load[pl] + floordiv_exact(a, s_speed[pl], s_inv[pl]);
+      const int64_t cm = best + mig;
+      if (cl < cm || (cl == cm && loc < bidx)) { route = loc; cost = cl; }
+      else { route = bidx; cost = cm; }
+    } else {
+      route = bidx;
+      cost = best + mig;
+    }
+  } else {
+    route = bidx;
+    cost = best;
+  }
+}
+
+}  // namespace nalar

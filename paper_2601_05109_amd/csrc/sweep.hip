@@ -1,0 +1,795 @@
+// Per-workflow sweep: remaining critical path, readiness, slack, routing and
+// order-preserving compaction of the ready futures, in one kernel.
+//
+// Futures of different workflows never depend on each other (one global
+// controller per workflow, Section 4.1; cross-workflow dependencies are
+// rejected), so each workgroup takes whole workflows from a ticket counter and
+// runs the reverse level-synchronous max-plus sweep of each one with workgroup
+// barriers only:
+//
+//   cnt[u] = number of consumers of u (atomic out-degree counters)
+//   level 0 = futures with no consumer; a future joins a level when its last
+//   consumer is finalised; finalising u sets
+//       rem[u] = est'[u] + mx[u],   mx = running max of the consumers' rem
+//   and pushes rem[u] into mx[p] / decrements cnt[p] for each dependency p.
+//
+// Pushes (max, then decrement) and counter increments are order-free integer
+// atomics, so the result does not depend on scheduling.  When a whole wave
+// targets the same future (a fan-in such as a map/reduce root), the wave
+// reduces first and one lane issues a single atomic.
+//
+// Workflows up to `lds_cap` futures keep the counters in LDS and each thread
+// owns up to NPT futures, holding their service time and up to three
+// dependency indices in registers, so a level costs two workgroup barriers and
+// a few LDS operations.  Larger workflows keep the state in HBM (by position)
+// and process explicit frontier lists.  Futures with more dependencies than a
+// thread keeps are handled by the whole workgroup.
+//
+// Readiness is known before the sweep, so each workflow publishes its ready
+// count at once (decoupled look-back over workflow tickets) and later writes
+// its ready futures, routed and with their slack, at their final compacted
+// positions: workflows ascending, ids ascending inside a workflow.
+#include "internal.hpp"
+
+namespace nalar {
+
+namespace {
+
+constexpr int kPmax = 3;          // dependencies held in registers per future
+constexpr int kHeavyCap = 64;     // cooperative list capacity per phase
+constexpr int kHbmLight = 32;     // HBM path: more dependencies -> cooperative
+constexpr size_t kStaticLdsReserve = 4096;
+
+struct Layout {
+  const int32_t* node_of_pos;
+  const int32_t* pos_of_node;
+  int64_t N;
+};
+
+__device__ inline int32_t node_at(const Layout& L, int64_t q) {
+  return L.node_of_pos ? L.node_of_pos[q] : int32_t(q);
+}
+
+// Index of dependency p inside the workflow occupying positions [b, b+n), or
+// -1 if p lies outside it (out of range or another workflow).
+__device__ inline int32_t local_of(const Layout& L, int32_t p, int64_t b, int n) {
+  int64_t q;
+  if (L.pos_of_node) {
+    if (p < 0 || int64_t(p) >= L.N) return -1;
+    q = L.pos_of_node[p];
+  } else {
+    q = p;
+  }
+  const int64_t lp = q - b;
+  return (lp >= 0 && lp < n) ? int32_t(lp) : -1;
+}
+
+__device__ inline int32_t checked_dep(const Layout& L, int32_t p, int64_t b, int n, int k,
+                                      Ctrl* ctrl) {
+  const int32_t lp = local_of(L, p, b, n);
+  if (lp < 0) {
+    flag_status(ctrl, kStInval);
+    return -1;
+  }
+  if (lp == k) {
+    flag_status(ctrl, kStCycle);
+    return -1;
+  }
+  return lp;
+}
+
+// ---------------------------------------------------------------- LDS atomics
+
+__device__ inline void agg_count_lds(int32_t* cnt, int lp) {
+  const uint64_t act = ballot(lp >= 0);
+  if (act == 0) return;
+  const int lead = __builtin_ctzll(act);
+  const int first = readlane_i32(lp, lead);
+  if (ballot(lp >= 0 && lp != first) == 0) {
+    if (lane_id() == lead) atomicAdd(&cnt[first], int(__popcll(act)));
+  } else if (lp >= 0) {
+    atomicAdd(&cnt[lp], 1);
+  }
+}
+
+// Called with every lane of the wave active.
+__device__ inline void agg_push_lds(int64_t* mx, int32_t* cnt, int lp, int64_t r) {
+  const uint64_t act = ballot(lp >= 0);
+  if (act == 0) return;
+  const int lead = __builtin_ctzll(act);
+  const int first = readlane_i32(lp, lead);
+  if (ballot(lp >= 0 && lp != first) == 0) {
+    const int64_t m = wave_max_i64(lp >= 0 ? r : INT64_MIN);
+    if (lane_id() == lead) {
+      atomicMax(reinterpret_cast<long long*>(&mx[first]), (long long)m);
+      atomicSub(&cnt[first], int(__popcll(act)));
+    }
+  } else if (lp >= 0) {
+    atomicMax(reinterpret_cast<long long*>(&mx[lp]), (long long)r);
+    atomicSub(&cnt[lp], 1);
+  }
+}
+
+// ---------------------------------------------------------------- HBM atomics
+
+__device__ inline void agg_count_hbm(int32_t* cnt, int lp) {
+  const uint64_t act = ballot(lp >= 0);
+  if (act == 0) return;
+  const int lead = __builtin_ctzll(act);
+  const int first = readlane_i32(lp, lead);
+  if (ballot(lp >= 0 && lp != first) == 0) {
+    if (lane_id() == lead) add_wg(&cnt[first], int32_t(__popcll(act)));
+  } else if (lp >= 0) {
+    add_wg(&cnt[lp], int32_t(1));
+  }
+}
+
+__device__ inline void append_wave(bool in, int32_t val, int32_t* list, int* s_count) {
+  const uint64_t am = ballot(in);
+  if (am == 0) return;
+  const int lead = __builtin_ctzll(am);
+  int base = 0;
+  if (lane_id() == lead) base = atomicAdd(s_count, int(__popcll(am)));
+  base = readlane_i32(base, lead);
+  if (in) list[base + int(lanes_below(am))] = val;
+}
+
+// Called with every lane of the wave active.  A dependency whose counter
+// reaches zero is appended to the next frontier.
+__device__ inline void agg_push_hbm(int64_t* mx, int32_t* cnt, int lp, int64_t r, int32_t* nxt,
+                                    int* s_fnext) {
+  const uint64_t act = ballot(lp >= 0);
+  bool app = false;
+  int32_t app_lp = 0;
+  if (act != 0) {
+    const int lead = __builtin_ctzll(act);
+    const int first = readlane_i32(lp, lead);
+    if (ballot(lp >= 0 && lp != first) == 0) {
+      const int64_t m = wave_max_i64(lp >= 0 ? r : INT64_MIN);
+      if (lane_id() == lead) {
+        max_wg(&mx[first], m);
+        const int32_t c = int32_t(__popcll(act));
+        if (add_wg(&cnt[first], -c) == c) { app = true; app_lp = first; }
+      }
+    } else if (lp >= 0) {
+      max_wg(&mx[lp], r);
+      if (add_wg(&cnt[lp], int32_t(-1)) == 1) { app = true; app_lp = lp; }
+    }
+  }
+  append_wave(app, app_lp, nxt, s_fnext);
+}
+
+__device__ inline int64_t clamp_rem(int64_t r, bool& overflow) {
+  if (r > NALAR_REM_MAX) {
+    overflow = true;
+    return NALAR_REM_MAX + 1;
+  }
+  return r;
+}
+
+// Workgroup-shared bookkeeping of the sweep (one instance per workgroup).
+struct Shared {
+  int w;
+  int hcount;
+  int fcount;
+  int fnext;
+  int proc;
+  int32_t hk[kHeavyCap];
+  int32_t ho[kHeavyCap];
+  int32_t hd[kHeavyCap];
+  uint32_t wtot[128];      // [NPT][waves] (LDS path) or [waves] (HBM path)
+  int64_t base;
+  int64_t red[3][16];
+};
+
+struct ITabLds {
+  int64_t* load;
+  double* inv;
+  int32_t* type;
+  int32_t* idx;
+  int32_t* speed;
+  int32_t* pos;
+};
+
+struct Acc {
+  int64_t tmin = INT64_MAX;
+  int64_t tmax = INT64_MIN;
+  int64_t tready = 0;
+};
+
+__device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_t slot, int32_t v,
+                                   int64_t rem, int64_t est, int64_t dl, Acc& acc) {
+  const int64_t slack = dl - rem;
+  int32_t route;
+  int64_t cost;
+  route_future(a.p.type[v], est, a.p.loc[v], int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load,
+               it.speed, it.inv, it.pos, route, cost);
+  a.cmp_slack[slot] = slack;
+  a.cmp_v[slot] = v;
+  a.cmp_route[slot] = route;
+  a.cmp_cost[slot] = cost;
+  acc.tmin = slack < acc.tmin ? slack : acc.tmin;
+  acc.tmax = slack > acc.tmax ? slack : acc.tmax;
+}
+
+__device__ inline void publish_ready_count(const SweepArgs& a, int w, uint32_t count) {
+  st_relaxed_agent(&a.wf_lb[w], lb_pack(a.epoch, w == 0 ? kLbInc : kLbAgg, count));
+}
+
+// Exclusive ready prefix of workflow w (thread 0 only).
+__device__ inline int64_t ready_base(const SweepArgs& a, int w, uint32_t count) {
+  if (w == 0) return 0;
+  const uint64_t excl = lookback_exclusive(a.wf_lb, w, 1, a.epoch);
+  st_relaxed_agent(&a.wf_lb[w], lb_pack(a.epoch, kLbInc, excl + count));
+  return int64_t(excl);
+}
+
+// ------------------------------------------------------------ LDS workflow
+
+// Owned-future registers of the LDS path.  Local indices are below 2^16 there
+// (lds_cap < 65535), so the three dependency slots and the degree pack into two
+// words: p01 = d0 | d1 << 16, p2 = d2 | deg << 16 | heavy << 31 (0xFFFF = none).
+constexpr uint32_t kNoDep = 0xFFFFu;
+constexpr uint32_t kHeavyBit = 0x80000000u;
+
+__device__ inline int dep_at(uint32_t p01, uint32_t p2, int q) {
+  const uint32_t x = q == 0 ? (p01 & 0xFFFFu) : q == 1 ? (p01 >> 16) : (p2 & 0xFFFFu);
+  return x == kNoDep ? -1 : int(x);
+}
+
+template <int T, int NPT>
+__device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
+                          int64_t* mx, int32_t* cnt, uint8_t* dn, uint8_t* nr, int w, int64_t b,
+                          int n, int64_t dl, Acc& acc) {
+  constexpr int NW = T / kWave;
+  const int tid = threadIdx.x;
+  const int wv = tid / kWave;
+  Ctrl* ctrl = a.ctrl;
+
+  int32_t vv[NPT];
+  int64_t ee[NPT];
+  uint32_t p01[NPT], p2[NPT];
+  uint32_t fin = 0, ready = 0;
+
+  // A: load owned futures, reset their counters
+#pragma unroll
+  for (int j = 0; j < NPT; ++j) {
+    const int k = j * T + tid;
+    vv[j] = 0; ee[j] = 0; p01[j] = 0xFFFFFFFFu; p2[j] = kNoDep;
+    if (k < n) {
+      const int32_t v = node_at(L, b + k);
+      const uint8_t d = a.p.done[v];
+      vv[j] = v;
+      ee[j] = d ? 0 : a.p.est[v];
+      cnt[k] = 0;
+      mx[k] = 0;
+      dn[k] = d;
+      nr[k] = 0;
+    }
+  }
+  if (tid == 0) { S.hcount = 0; S.proc = 0; }
+  __syncthreads();
+
+  // B: out-degree counters and readiness (one pass over the dependencies)
+#pragma unroll
+  for (int j = 0; j < NPT; ++j) {
+    const int k = j * T + tid;
+    const bool own = k < n;
+    int32_t off = 0, deg = 0;
+    if (own) {
+      off = a.p.dep_off[vv[j]];
+      deg = a.p.dep_off[vv[j] + 1] - off;
+    }
+    const bool light = own && deg <= kPmax;
+    if (own && !light) {
+      p2[j] = kHeavyBit | kNoDep;
+      const int slot = atomicAdd(&S.hcount, 1);
+      if (slot < kHeavyCap) {
+        S.hk[slot] = k; S.ho[slot] = off; S.hd[slot] = deg;
+      } else {
+        bool blocked = false;
+        for (int e = 0; e < deg; ++e) {
+          const int32_t lp = checked_dep(L, a.p.dep_idx[off + e], b, n, k, ctrl);
+          if (lp >= 0) { atomicAdd(&cnt[lp], 1); blocked |= dn[lp] == 0; }
+        }
+        if (blocked) nr[k] = 1;
+      }
+    }
+    bool blocked = false;
+    uint32_t packed[kPmax];
+#pragma unroll
+    for (int q = 0; q < kPmax; ++q) {
+      int32_t lp = -1;
+      if (light && q < deg) lp = checked_dep(L, a.p.dep_idx[off + q], b, n, k, ctrl);
+      packed[q] = lp >= 0 ? uint32_t(lp) : kNoDep;
+      agg_count_lds(cnt, lp);
+      if (lp >= 0 && dn[lp] == 0) blocked = true;
+    }
+    if (light) {
+      p01[j] = packed[0] | (packed[1] << 16);
+      p2[j] = packed[2] | (uint32_t(deg) << 16);
+      if (blocked) nr[k] = 1;
+    }
+  }
+  __syncthreads();
+  {
+    const int hc = S.hcount < kHeavyCap ? S.hcount : kHeavyCap;
+    for (int h = 0; h < hc; ++h) {
+      const int k = S.hk[h], off = S.ho[h], deg = S.hd[h];
+      bool blocked = false;
+      for (int e0 = 0; e0 < deg; e0 += T) {
+        const int e = e0 + tid;
+        int32_t lp = -1;
+        if (e < deg) lp = checked_dep(L, a.p.dep_idx[off + e], b, n, k, ctrl);
+        agg_count_lds(cnt, lp);
+        if (lp >= 0 && dn[lp] == 0) blocked = true;
+      }
+      if (blocked) nr[k] = 1;
+    }
+  }
+  __syncthreads();
+
+  // ready flags, their compacted slots inside the workflow, the ready count
+  uint32_t slot[NPT];
+#pragma unroll
+  for (int j = 0; j < NPT; ++j) {
+    const int k = j * T + tid;
+    const bool rd = k < n && dn[k] == 0 && nr[k] == 0;
+    if (rd) ready |= 1u << j;
+    const uint64_t m = ballot(rd);
+    if (lane_id() == 0) S.wtot[j * NW + wv] = uint32_t(__popcll(m));
+    slot[j] = lanes_below(m);
+  }
+  __syncthreads();
+  uint32_t run = 0;
+#pragma unroll
+  for (int j = 0; j < NPT; ++j) {
+    uint32_t ctot = 0, before = 0;
+    for (int x = 0; x < NW; ++x) {
+      const uint32_t c = S.wtot[j * NW + x];
+      ctot += c;
+      before += x < wv ? c : 0u;
+    }
+    slot[j] += run + before;
+    run += ctot;
+  }
+  if (tid == 0) {
+    publish_ready_count(a, w, run);
+    acc.tready += run;
+    S.hcount = 0;
+  }
+
+  // C: levels
+  bool overflow = false;
+  for (;;) {
+    uint32_t cand = 0;
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+      const int k = j * T + tid;
+      if (k < n && !((fin >> j) & 1u) && cnt[k] == 0) cand |= 1u << j;
+    }
+    if (!__syncthreads_or(cand != 0)) break;
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+      const bool c = (cand >> j) & 1u;
+      const bool hv = (p2[j] & kHeavyBit) != 0;
+      const int k = j * T + tid;
+      int64_t r = 0;
+      if (c) {
+        r = clamp_rem(ee[j] + mx[k], overflow);
+        mx[k] = r;
+        if (a.rem_out) a.rem_out[vv[j]] = r;
+        fin |= 1u << j;
+        if (hv) {
+          const int32_t off = a.p.dep_off[vv[j]];
+          const int32_t deg = a.p.dep_off[vv[j] + 1] - off;
+          const int hs = atomicAdd(&S.hcount, 1);
+          if (hs < kHeavyCap) {
+            S.hk[hs] = k; S.ho[hs] = off; S.hd[hs] = deg;
+          } else {
+            for (int e = 0; e < deg; ++e) {
+              const int32_t lp = local_of(L, a.p.dep_idx[off + e], b, n);
+              if (lp >= 0 && lp != k) {
+                atomicMax(reinterpret_cast<long long*>(&mx[lp]), (long long)r);
+                atomicSub(&cnt[lp], 1);
+              }
+            }
+          }
+        }
+      }
+      const bool lightc = c && !hv;
+#pragma unroll
+      for (int q = 0; q < kPmax; ++q) agg_push_lds(mx, cnt, lightc ? dep_at(p01[j], p2[j], q) : -1, r);
+    }
+    __syncthreads();
+    const int hc = S.hcount < kHeavyCap ? S.hcount : kHeavyCap;
+    for (int h = 0; h < hc; ++h) {
+      const int k = S.hk[h], off = S.ho[h], deg = S.hd[h];
+      const int64_t r = mx[k];
+      for (int e0 = 0; e0 < deg; e0 += T) {
+        const int e = e0 + tid;
+        int32_t lp = -1;
+        if (e < deg) {
+          lp = local_of(L, a.p.dep_idx[off + e], b, n);
+          if (lp == k) lp = -1;
+        }
+        agg_push_lds(mx, cnt, lp, r);
+      }
+    }
+    __syncthreads();
+    if (tid == 0) S.hcount = 0;
+    __syncthreads();
+  }
+  if (overflow) flag_status(ctrl, kStRange);
+  if (fin) atomicAdd(&S.proc, __popc(fin));
+  __syncthreads();
+  if (tid == 0) {
+    if (S.proc != n) flag_status(ctrl, kStCycle);
+    S.base = ready_base(a, w, run);
+  }
+  __syncthreads();
+
+  // D: slack, route, write at the compacted slot
+  const int64_t base = S.base;
+#pragma unroll
+  for (int j = 0; j < NPT; ++j) {
+    if ((ready >> j) & 1u) {
+      const int k = j * T + tid;
+      write_ready(a, it, base + slot[j], vv[j], mx[k], ee[j], dl, acc);
+    }
+  }
+  __syncthreads();
+}
+
+// ------------------------------------------------------------ HBM workflow
+
+template <int T>
+__device__ void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
+                          int w, int64_t b, int n, int64_t dl, Acc& acc) {
+  constexpr int NW = T / kWave;
+  const int tid = threadIdx.x;
+  const int wv = tid / kWave;
+  Ctrl* ctrl = a.ctrl;
+  int32_t* cnt = a.g_cnt + b;
+  int64_t* mx = a.g_mx + b;
+  uint8_t* dn = a.g_dn + b;
+  uint8_t* nr = a.g_nr + b;
+
+  for (int k = tid; k < n; k += T) {
+    const int32_t v = node_at(L, b + k);
+    st_wg(&cnt[k], int32_t(0));
+    st_wg(&mx[k], int64_t(0));
+    dn[k] = a.p.done[v];
+    nr[k] = 0;
+  }
+  if (tid == 0) { S.hcount = 0; S.fcount = 0; }
+  __syncthreads();
+
+  // out-degree counters and readiness
+  for (int k0 = 0; k0 < n; k0 += T) {
+    const int k = k0 + tid;
+    const bool own = k < n;
+    int32_t v = 0, off = 0, deg = 0;
+    if (own) {
+      v = node_at(L, b + k);
+      off = a.p.dep_off[v];
+      deg = a.p.dep_off[v + 1] - off;
+    }
+    const bool light = own && deg <= kHbmLight;
+    if (own && !light) {
+      const int slot = atomicAdd(&S.hcount, 1);
+      if (slot < kHeavyCap) {
+        S.hk[slot] = k; S.ho[slot] = off; S.hd[slot] = deg;
+      } else {
+        bool blocked = false;
+        for (int e = 0; e < deg; ++e) {
+          const int32_t lp = checked_dep(L, a.p.dep_idx[off + e], b, n, k, ctrl);
+          if (lp >= 0) { add_wg(&cnt[lp], int32_t(1)); blocked |= dn[lp] == 0; }
+        }
+        if (blocked) nr[k] = 1;
+      }
+    }
+    bool blocked = false;
+    for (int q = 0;; ++q) {
+      const bool has = light && q < deg;
+      if (ballot(has) == 0) break;
+      int32_t lp = -1;
+      if (has) lp = checked_dep(L, a.p.dep_idx[off + q], b, n, k, ctrl);
+      agg_count_hbm(cnt, lp);
+      if (lp >= 0 && dn[lp] == 0) blocked = true;
+    }
+    if (light && blocked) nr[k] = 1;
+  }
+  __syncthreads();
+  {
+    const int hc = S.hcount < kHeavyCap ? S.hcount : kHeavyCap;
+    for (int h = 0; h < hc; ++h) {
+      const int k = S.hk[h], off = S.ho[h], deg = S.hd[h];
+      bool blocked = false;
+      for (int e0 = 0; e0 < deg; e0 += T) {
+        const int e = e0 + tid;
+        int32_t lp = -1;
+        if (e < deg) lp = checked_dep(L, a.p.dep_idx[off + e], b, n, k, ctrl);
+        agg_count_hbm(cnt, lp);
+        if (lp >= 0 && dn[lp] == 0) blocked = true;
+      }
+      if (blocked) nr[k] = 1;
+    }
+  }
+  __syncthreads();
+
+  // ready count
+  uint32_t mine = 0;
+  for (int k = tid; k < n; k += T) mine += (dn[k] == 0 && nr[k] == 0) ? 1u : 0u;
+  {
+    uint32_t s = mine;
+#pragma unroll
+    for (int m = 1; m < kWave; m <<= 1) s += __shfl_xor(s, m, kWave);
+    if (lane_id() == 0) S.wtot[wv] = s;
+  }
+  __syncthreads();
+  uint32_t total = 0;
+  for (int x = 0; x < NW; ++x) total += S.wtot[x];
+  if (tid == 0) {
+    publish_ready_count(a, w, total);
+    acc.tready += total;
+    S.hcount = 0;
+  }
+
+  // frontier 0: futures without consumers
+  int32_t* cur = a.g_front0 + b;
+  int32_t* nxt = a.g_front1 + b;
+  for (int k0 = 0; k0 < n; k0 += T) {
+    const int k = k0 + tid;
+    append_wave(k < n && ld_wg(&cnt[k]) == 0, k, cur, &S.fcount);
+  }
+  __syncthreads();
+  int fsize = S.fcount;
+  int64_t processed = 0;
+  bool overflow = false;
+  while (fsize > 0) {
+    processed += fsize;
+    if (tid == 0) { S.fnext = 0; S.hcount = 0; }
+    __syncthreads();
+    for (int i0 = 0; i0 < fsize; i0 += T) {
+      const int i = i0 + tid;
+      const bool act = i < fsize;
+      int32_t k = 0, off = 0, deg = 0;
+      int64_t r = 0;
+      if (act) {
+        k = cur[i];
+        const int32_t v = node_at(L, b + k);
+        r = clamp_rem((dn[k] ? 0 : a.p.est[v]) + ld_wg(&mx[k]), overflow);
+        st_wg(&mx[k], r);
+        if (a.rem_out) a.rem_out[v] = r;
+        off = a.p.dep_off[v];
+        deg = a.p.dep_off[v + 1] - off;
+        if (deg > kHbmLight) {
+          const int hs = atomicAdd(&S.hcount, 1);
+          if (hs < kHeavyCap) {
+            S.hk[hs] = k; S.ho[hs] = off; S.hd[hs] = deg;
+          } else {
+            for (int e = 0; e < deg; ++e) {
+              const int32_t lp = local_of(L, a.p.dep_idx[off + e], b, n);
+              if (lp >= 0 && lp != k) {
+                max_wg(&mx[lp], r);
+                if (add_wg(&cnt[lp], int32_t(-1)) == 1) {
+                  nxt[atomicAdd(&S.fnext, 1)] = lp;
+                }
+              }
+            }
+          }
+        }
+      }
+      const bool light = act && deg <= kHbmLight;
+      for (int q = 0;; ++q) {
+        const bool has = light && q < deg;
+        if (ballot(has) == 0) break;
+        int32_t lp = -1;
+        if (has) {
+          lp = local_of(L, a.p.dep_idx[off + q], b, n);
+          if (lp == k) lp = -1;
+        }
+        agg_push_hbm(mx, cnt, lp, r, nxt, &S.fnext);
+      }
+    }
+    __syncthreads();
+    const int hc = S.hcount < kHeavyCap ? S.hcount : kHeavyCap;
+    for (int h = 0; h < hc; ++h) {
+      const int k = S.hk[h], off = S.ho[h], deg = S.hd[h];
+      const int64_t r = ld_wg(&mx[k]);
+      for (int e0 = 0; e0 < deg; e0 += T) {
+        const int e = e0 + tid;
+        int32_t lp = -1;
+        if (e < deg) {
+          lp = local_of(L, a.p.dep_idx[off + e], b, n);
+          if (lp == k) lp = -1;
+        }
+        agg_push_hbm(mx, cnt, lp, r, nxt, &S.fnext);
+      }
+    }
+    __syncthreads();
+    fsize = S.fnext;
+    int32_t* t = cur; cur = nxt; nxt = t;
+    __syncthreads();
+  }
+  if (overflow) flag_status(ctrl, kStRange);
+  if (tid == 0) {
+    if (processed != n) flag_status(ctrl, kStCycle);
+    S.base = ready_base(a, w, total);
+  }
+  __syncthreads();
+
+  // slack, route, compacted write in position order
+  int64_t run = S.base;
+  for (int k0 = 0; k0 < n; k0 += T) {
+    const int k = k0 + tid;
+    const bool rd = k < n && dn[k] == 0 && nr[k] == 0;
+    const uint64_t m = ballot(rd);
+    __syncthreads();
+    if (lane_id() == 0) S.wtot[wv] = uint32_t(__popcll(m));
+    __syncthreads();
+    uint32_t before = 0, ctot = 0;
+    for (int x = 0; x < NW; ++x) {
+      const uint32_t c = S.wtot[x];
+      ctot += c;
+      before += x < wv ? c : 0u;
+    }
+    if (rd) {
+      const int32_t v = node_at(L, b + k);
+      write_ready(a, it, run + before + lanes_below(m), v, ld_wg(&mx[k]), a.p.est[v], dl, acc);
+    }
+    run += ctot;
+  }
+  __syncthreads();
+}
+
+// ------------------------------------------------------------ kernel
+
+template <int T, int NPT>
+__global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
+  constexpr int NW = T / kWave;
+  Ctrl* ctrl = a.ctrl;
+  if (ld_relaxed_agent(&ctrl->status) != 0) return;
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ Shared S;
+
+  const int M = int(a.p.M);
+  const int tid = threadIdx.x;
+  unsigned char* sp = smem;
+  ITabLds it;
+  it.load = reinterpret_cast<int64_t*>(sp); sp += 8 * size_t(M);
+  it.inv = reinterpret_cast<double*>(sp); sp += 8 * size_t(M);
+  int64_t* mx = reinterpret_cast<int64_t*>(sp); sp += 8 * size_t(lds_cap);
+  it.type = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  it.idx = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  it.speed = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  it.pos = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  int32_t* cnt = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(lds_cap);
+  uint8_t* dn = sp; sp += lds_cap;
+  uint8_t* nr = sp;
+
+  for (int i = tid; i < M; i += T) {
+    it.load[i] = a.itab.load[i];
+    it.inv[i] = a.itab.inv_speed[i];
+    it.type[i] = a.itab.type[i];
+    it.idx[i] = a.itab.idx[i];
+    it.speed[i] = a.itab.speed[i];
+    it.pos[i] = a.itab.pos_of[i];
+  }
+
+  const Layout L{a.node_of_pos, a.pos_of_node, a.p.N};
+  Acc acc;
+  for (;;) {
+    if (tid == 0) S.w = int(atomicAdd(&ctrl->wf_ticket, 1u));
+    __syncthreads();
+    const int w = S.w;
+    __syncthreads();
+    if (int64_t(w) >= a.p.W) break;
+    const int64_t b = a.wf_off[w];
+    const int n = a.wf_off[w + 1] - int32_t(b);
+    const int64_t dl = a.p.deadline[w] - a.p.now;
+    if (n <= 0) {
+      if (tid == 0) {
+        publish_ready_count(a, w, 0);
+        ready_base(a, w, 0);
+      }
+      continue;
+    }
+    if (!a.force_global && n <= lds_cap)
+      sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, w, b, n, dl, acc);
+    else
+      sweep_hbm<T>(a, L, it, S, w, b, n, dl, acc);
+  }
+
+  // fold the block's slack range and ready count into the control block
+  const int64_t mn = wave_min_i64(acc.tmin);
+  const int64_t mxv = wave_max_i64(acc.tmax);
+  const int64_t rd = wave_sum_i64(acc.tready);
+  const int wv = tid / kWave;
+  if (lane_id() == 0) { S.red[0][wv] = mn; S.red[1][wv] = mxv; S.red[2][wv] = rd; }
+  __syncthreads();
+  if (tid == 0) {
+    int64_t a0 = INT64_MAX, a1 = INT64_MIN, a2 = 0;
+    for (int x = 0; x < NW; ++x) {
+      a0 = S.red[0][x] < a0 ? S.red[0][x] : a0;
+      a1 = S.red[1][x] > a1 ? S.red[1][x] : a1;
+      a2 += S.red[2][x];
+    }
+    if (a2 > 0) {
+      __hip_atomic_fetch_min(&ctrl->slack_min, a0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_fetch_max(&ctrl->slack_max, a1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      add_agent(&ctrl->n_ready, a2);
+    }
+  }
+}
+
+struct Variant {
+  int threads, npt;
+  const void* fn;
+};
+
+const Variant kVariants[] = {
+    {64, 4, reinterpret_cast<const void*>(&k_sweep<64, 4>)},
+    {256, 4, reinterpret_cast<const void*>(&k_sweep<256, 4>)},
+    {512, 4, reinterpret_cast<const void*>(&k_sweep<512, 4>)},
+    {1024, 5, reinterpret_cast<const void*>(&k_sweep<1024, 5>)},
+};
+
+}  // namespace
+
+SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t lds_limit) {
+  const int64_t avg = W > 0 ? (N + W - 1) / W : 0;
+  int vi = 3;
+  if (avg <= 128) vi = 0;
+  else if (avg <= 512) vi = 1;
+  else if (avg <= 2048) vi = 2;
+  SweepShape s;
+  s.threads = kVariants[vi].threads;
+  s.npt = kVariants[vi].npt;
+  const size_t itab = 32 * size_t(M);
+  const size_t avail = lds_limit > kStaticLdsReserve + itab ? lds_limit - kStaticLdsReserve - itab : 0;
+  int64_t cap = int64_t(avail / 14);
+  if (cap > int64_t(s.threads) * s.npt) cap = int64_t(s.threads) * s.npt;
+  s.lds_cap = int(cap);
+  s.lds_bytes = itab + 14 * size_t(cap) + 16;
+  int64_t per_cu = 2048 / s.threads;
+  if (per_cu < 1) per_cu = 1;
+  int64_t blocks = int64_t(device_cus) * per_cu;
+  if (blocks > W) blocks = W;
+  if (blocks < 1) blocks = 1;
+  s.blocks = int(blocks);
+  return s;
+}
+
+hipError_t prepare_sweep_kernels(size_t lds_limit) {
+  const size_t dyn = lds_limit > kStaticLdsReserve ? lds_limit - kStaticLdsReserve : 0;
+  for (const Variant& v : kVariants) {
+    hipError_t e = hipFuncSetAttribute(v.fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(dyn));
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const SweepShape& sh) {
+  switch (sh.threads) {
+    case 64:
+      hipLaunchKernelGGL((k_sweep<64, 4>), dim3(sh.blocks), dim3(64), sh.lds_bytes, s, a, sh.lds_cap);
+      break;
+    case 256:
+      hipLaunchKernelGGL((k_sweep<256, 4>), dim3(sh.blocks), dim3(256), sh.lds_bytes, s, a,
+                         sh.lds_cap);
+      break;
+    case 512:
+      hipLaunchKernelGGL((k_sweep<512, 4>), dim3(sh.blocks), dim3(512), sh.lds_bytes, s, a,
+                         sh.lds_cap);
+      break;
+    default:
+      hipLaunchKernelGGL((k_sweep<1024, 5>), dim3(sh.blocks), dim3(1024), sh.lds_bytes, s, a,
+                         sh.lds_cap);
+      break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace nalar

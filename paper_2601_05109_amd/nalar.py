@@ -1,0 +1,261 @@
+"""ctypes binding of the C ABI in include/nalar_policy.h.
+
+Argument marshalling only: every step of the pass runs in the HIP library
+``libnalar_policy.so`` built from ``csrc/``.  Loading fails loudly when the
+library is missing; there is no other implementation behind these names.
+
+Functions with the C names (``nalar_policy_create``, ``nalar_policy_pass``,
+``nalar_policy_destroy``, ``nalar_policy_last_error``, ``nalar_policy_set_timing``,
+``nalar_policy_get_timing``) take and return the ctypes structures below.  The
+``Policy`` class and ``DeviceProblem`` are conveniences over them for torch
+device tensors.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libnalar_policy.so")
+
+NALAR_OK, NALAR_EINVAL, NALAR_ECYCLE, NALAR_ERANGE, NALAR_ENOMEM, NALAR_EDEVICE = 0, -1, -2, -3, -4, -5
+NALAR_WF_CONTIGUOUS = 1
+NALAR_FORCE_GLOBAL_SWEEP = 1
+NALAR_MAX_INSTANCES = 1024
+
+EXPORTED = ("nalar_policy_create", "nalar_policy_pass", "nalar_policy_destroy",
+            "nalar_policy_last_error", "nalar_policy_set_timing", "nalar_policy_get_timing")
+
+
+class NalarPolicyConfig(ctypes.Structure):
+    _fields_ = [("device", ctypes.c_int32), ("flags", ctypes.c_uint32),
+                ("stream", ctypes.c_void_p), ("reserve_nodes", ctypes.c_int64),
+                ("reserve_edges", ctypes.c_int64), ("reserve_workflows", ctypes.c_int64)]
+
+
+class NalarProblem(ctypes.Structure):
+    _fields_ = [("n_nodes", ctypes.c_int64), ("n_edges", ctypes.c_int64),
+                ("n_workflows", ctypes.c_int64), ("n_instances", ctypes.c_int64),
+                ("now_us", ctypes.c_int64), ("migration_cost_us", ctypes.c_int64),
+                ("flags", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("wf", ctypes.c_void_p), ("type", ctypes.c_void_p), ("est_us", ctypes.c_void_p),
+                ("done", ctypes.c_void_p), ("loc", ctypes.c_void_p), ("dep_off", ctypes.c_void_p),
+                ("dep_idx", ctypes.c_void_p), ("deadline_us", ctypes.c_void_p),
+                ("inst_type", ctypes.c_void_p), ("inst_load_us", ctypes.c_void_p),
+                ("inst_speed_permille", ctypes.c_void_p)]
+
+
+class NalarResult(ctypes.Structure):
+    _fields_ = [("rem_us", ctypes.c_void_p), ("order", ctypes.c_void_p),
+                ("slack_us", ctypes.c_void_p), ("route", ctypes.c_void_p),
+                ("cost_us", ctypes.c_void_p), ("n_ready", ctypes.c_int64)]
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with "
+                           "`python -m paper_2601_05109_amd.build` (hipcc, gfx950)")
+    lib = ctypes.CDLL(path)
+    H = ctypes.c_void_p
+    lib.nalar_policy_create.argtypes = [ctypes.POINTER(NalarPolicyConfig), ctypes.POINTER(H)]
+    lib.nalar_policy_create.restype = ctypes.c_int
+    lib.nalar_policy_pass.argtypes = [H, ctypes.POINTER(NalarProblem), ctypes.POINTER(NalarResult)]
+    lib.nalar_policy_pass.restype = ctypes.c_int
+    lib.nalar_policy_destroy.argtypes = [H]
+    lib.nalar_policy_destroy.restype = None
+    lib.nalar_policy_last_error.argtypes = [H]
+    lib.nalar_policy_last_error.restype = ctypes.c_char_p
+    lib.nalar_policy_set_timing.argtypes = [H, ctypes.c_int]
+    lib.nalar_policy_set_timing.restype = ctypes.c_int
+    lib.nalar_policy_get_timing.argtypes = [H, ctypes.POINTER(ctypes.c_char_p),
+                                            ctypes.POINTER(ctypes.c_float), ctypes.c_int,
+                                            ctypes.POINTER(ctypes.c_int)]
+    lib.nalar_policy_get_timing.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+# ---------------------------------------------------------------- C names
+
+def nalar_policy_create(cfg: NalarPolicyConfig) -> tuple[int, Optional[int]]:
+    h = ctypes.c_void_p()
+    rc = load_library().nalar_policy_create(ctypes.byref(cfg), ctypes.byref(h))
+    return rc, h.value
+
+
+def nalar_policy_pass(h: int, prob: NalarProblem, res: NalarResult) -> int:
+    return load_library().nalar_policy_pass(h, ctypes.byref(prob), ctypes.byref(res))
+
+
+def nalar_policy_destroy(h: Optional[int]) -> None:
+    load_library().nalar_policy_destroy(h)
+
+
+def nalar_policy_last_error(h: Optional[int]) -> str:
+    return (load_library().nalar_policy_last_error(h) or b"").decode()
+
+
+def nalar_policy_set_timing(h: int, enable: bool) -> int:
+    return load_library().nalar_policy_set_timing(h, 1 if enable else 0)
+
+
+def nalar_policy_get_timing(h: int, cap: int = 32) -> list[tuple[str, float]]:
+    names = (ctypes.c_char_p * cap)()
+    ms = (ctypes.c_float * cap)()
+    count = ctypes.c_int(0)
+    rc = load_library().nalar_policy_get_timing(h, names, ms, cap, ctypes.byref(count))
+    if rc != NALAR_OK:
+        raise RuntimeError("no timed pass available")
+    return [(names[i].decode(), float(ms[i])) for i in range(min(count.value, cap))]
+
+
+# ---------------------------------------------------------------- torch helpers
+
+class NalarError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"nalar_policy_pass returned {code}: {msg}")
+        self.code = code
+
+
+@dataclass
+class DeviceProblem:
+    """A snapshot held in device memory as torch tensors (plus the host scalars)."""
+    now_us: int
+    migration_cost_us: int
+    wf_contiguous: bool
+    tensors: dict
+
+    FIELDS = ("wf", "type", "est_us", "done", "loc", "dep_off", "dep_idx", "deadline_us",
+              "inst_type", "inst_load_us", "inst_speed_permille")
+
+    @classmethod
+    def from_host(cls, p, device="cuda") -> "DeviceProblem":
+        import torch
+        t = {}
+        for f in cls.FIELDS:
+            a = getattr(p, f)
+            t[f] = torch.from_numpy(a.copy() if not a.flags.c_contiguous else a).to(device)
+        return cls(int(p.now_us), int(p.migration_cost_us), bool(p.wf_contiguous), t)
+
+    @property
+    def n_nodes(self) -> int:
+        return int(self.tensors["wf"].shape[0])
+
+    def c_struct(self, flags: Optional[int] = None) -> NalarProblem:
+        t = self.tensors
+        ptr = lambda x: x.data_ptr() if x.numel() > 0 else None
+        return NalarProblem(
+            n_nodes=t["wf"].shape[0], n_edges=t["dep_idx"].shape[0],
+            n_workflows=t["deadline_us"].shape[0], n_instances=t["inst_type"].shape[0],
+            now_us=self.now_us, migration_cost_us=self.migration_cost_us,
+            flags=(NALAR_WF_CONTIGUOUS if self.wf_contiguous else 0) if flags is None else flags,
+            reserved=0, wf=ptr(t["wf"]), type=ptr(t["type"]), est_us=ptr(t["est_us"]),
+            done=ptr(t["done"]), loc=ptr(t["loc"]), dep_off=ptr(t["dep_off"]),
+            dep_idx=ptr(t["dep_idx"]), deadline_us=ptr(t["deadline_us"]),
+            inst_type=ptr(t["inst_type"]), inst_load_us=ptr(t["inst_load_us"]),
+            inst_speed_permille=ptr(t["inst_speed_permille"]))
+
+
+@dataclass
+class DeviceResult:
+    rem: object
+    order: object
+    slack: object
+    route: object
+    cost: object
+    n_ready: int = 0
+
+    @classmethod
+    def alloc(cls, n: int, device="cuda", rem: bool = True, cost: bool = True) -> "DeviceResult":
+        import torch
+        n1 = max(n, 1)
+        return cls(torch.empty(n1, dtype=torch.int64, device=device) if rem else None,
+                   torch.empty(n1, dtype=torch.int32, device=device),
+                   torch.empty(n1, dtype=torch.int64, device=device),
+                   torch.empty(n1, dtype=torch.int32, device=device),
+                   torch.empty(n1, dtype=torch.int64, device=device) if cost else None)
+
+    def c_struct(self) -> NalarResult:
+        p = lambda x: None if x is None else x.data_ptr()
+        return NalarResult(rem_us=p(self.rem), order=p(self.order), slack_us=p(self.slack),
+                           route=p(self.route), cost_us=p(self.cost), n_ready=0)
+
+
+class Policy:
+    """Owns one handle bound to a device and a stream."""
+
+    def __init__(self, device: int = 0, stream=None, flags: int = 0, reserve_nodes: int = 0,
+                 reserve_workflows: int = 0):
+        import torch
+        if stream is None:
+            stream = torch.cuda.current_stream(device)
+        self.stream = stream
+        cfg = NalarPolicyConfig(device=device, flags=flags, stream=stream.cuda_stream,
+                                reserve_nodes=reserve_nodes, reserve_edges=0,
+                                reserve_workflows=reserve_workflows)
+        rc, h = nalar_policy_create(cfg)
+        if rc != NALAR_OK:
+            raise NalarError(rc, nalar_policy_last_error(None))
+        self.handle = h
+
+    def close(self) -> None:
+        if self.handle:
+            nalar_policy_destroy(self.handle)
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def run_pass(self, prob: DeviceProblem, out: DeviceResult, flags: Optional[int] = None,
+                 raw: Optional[NalarProblem] = None) -> int:
+        """One synchronous pass; returns the C return code and fills out.n_ready."""
+        cp = raw if raw is not None else prob.c_struct(flags)
+        cr = out.c_struct()
+        rc = nalar_policy_pass(self.handle, cp, cr)
+        out.n_ready = int(cr.n_ready) if rc == NALAR_OK else 0
+        return rc
+
+    def last_error(self) -> str:
+        return nalar_policy_last_error(self.handle)
+
+    def set_timing(self, enable: bool) -> None:
+        nalar_policy_set_timing(self.handle, enable)
+
+    def timing(self) -> list[tuple[str, float]]:
+        return nalar_policy_get_timing(self.handle)
+
+
+def run(p, device: str = "cuda", policy: Optional[Policy] = None, flags: int = 0):
+    """Upload a host problem, run one pass, and return host numpy results:
+    (status, n_ready, rem, order, slack, route, cost)."""
+    dp = DeviceProblem.from_host(p, device)
+    out = DeviceResult.alloc(dp.n_nodes, device)
+    own = policy is None
+    pol = policy or Policy(flags=flags)
+    try:
+        rc = pol.run_pass(dp, out)
+    finally:
+        if own:
+            pol.close()
+    R = out.n_ready
+    N = dp.n_nodes
+    return (rc, R, out.rem[:N].cpu().numpy(), out.order[:R].cpu().numpy(),
+            out.slack[:R].cpu().numpy(), out.route[:R].cpu().numpy(), out.cost[:R].cpu().numpy())

@@ -1,0 +1,319 @@
+"""GPU parity: the HIP pass through the C ABI versus the CPU oracle.
+
+Every comparison is bit-exact (all arithmetic is integer): remaining critical
+path of every future, the ready order, slack, route and cost, and the return
+code.  Cases: hand-worked fixtures, small random DAGs (contiguous and shuffled
+ids, many instances/types, duplicate dependencies), the tiny / paper-scale /
+deep-chain / map-reduce workloads, relabelled ids (the library groups futures by
+workflow itself), the HBM sweep path forced on, every error rule, repeated
+passes, scratch reuse across sizes, and every step of the dynamic stream.
+"""
+import concurrent.futures as cf
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from golden_io import load as load_golden, names as golden_names
+from paper_2601_05109_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover - collected on CPU hosts too
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2601_05109_amd import nalar  # noqa: E402
+
+
+def say(msg):
+    sys.stdout.write(msg + "\n")
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def policy():
+    with nalar.Policy() as p:
+        yield p
+
+
+@pytest.fixture(scope="module")
+def policy_hbm():
+    with nalar.Policy(flags=nalar.NALAR_FORCE_GLOBAL_SWEEP) as p:
+        yield p
+
+
+def gpu_run(pol, p, flags=None):
+    dp = nalar.DeviceProblem.from_host(p)
+    out = nalar.DeviceResult.alloc(dp.n_nodes)
+    rc = pol.run_pass(dp, out, flags=flags)
+    torch.cuda.synchronize()
+    R = out.n_ready
+    N = dp.n_nodes
+    return dict(status=rc, n_ready=R, rem=out.rem[:N].cpu().numpy(),
+                order=out.order[:R].cpu().numpy(), slack=out.slack[:R].cpu().numpy(),
+                route=out.route[:R].cpu().numpy(), cost=out.cost[:R].cpu().numpy(),
+                err=pol.last_error())
+
+
+def assert_parity(g, o, label=""):
+    assert g["status"] == o.status, f"{label}: status gpu={g['status']} ({g['err']}) oracle={o.status}"
+    if o.status != oracle.OK:
+        return
+    assert g["n_ready"] == o.n_ready, f"{label}: n_ready {g['n_ready']} vs {o.n_ready}"
+    for f, ref in (("rem", o.rem), ("order", o.order), ("slack", o.slack), ("route", o.route),
+                   ("cost", o.cost)):
+        got = g[f]
+        if not np.array_equal(got, ref):
+            bad = np.flatnonzero(got != ref)
+            raise AssertionError(f"{label}: {f} differs at {bad.size} positions, first {bad[:5]}: "
+                                 f"gpu {got[bad[:5]]} oracle {ref[bad[:5]]}")
+
+
+def check(pol, p, label, flags=None):
+    say(f"[gpu] {label}: N={p.n_nodes} E={p.n_edges} W={p.n_workflows} M={p.n_instances}")
+    assert_parity(gpu_run(pol, p, flags), oracle.run(p), label)
+
+
+# ---------------------------------------------------------------- small cases
+
+@pytest.mark.parametrize("name", golden_names())
+def test_golden(policy, name):
+    p, exp = load_golden(name)
+    g = gpu_run(policy, p)
+    assert g["status"] == exp["status"][0]
+    assert g["rem"].tolist() == exp["rem"]
+    assert g["order"].tolist() == exp["order"]
+    assert g["slack"].tolist() == exp["slack"]
+    assert g["route"].tolist() == exp["route"]
+    assert g["cost"].tolist() == exp["cost"]
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_small_dags(policy, seed):
+    rng = np.random.default_rng(1000 + seed)
+    p = wl.random_dag(seed, n_nodes=int(rng.integers(1, 40)), n_workflows=int(rng.integers(1, 5)),
+                      n_instances=int(rng.integers(0, 9)), n_types=int(rng.integers(1, 5)),
+                      shuffle_ids=bool(seed % 2))
+    check(policy, p, f"random_dag seed={seed}")
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_medium_dags(policy, policy_hbm, seed):
+    """Several hundred futures per workflow, wide fan-in and fan-out (futures
+    with more dependencies than a thread keeps in registers), ids shuffled."""
+    p = wl.random_dag(500 + seed, n_nodes=600, n_workflows=3, n_instances=40, n_types=6,
+                      p_edge=0.02 + 0.01 * (seed % 4), est_max=10**9, load_max=10**12,
+                      speed_hi=1 << 30, shuffle_ids=seed % 3 != 0)
+    check(policy, p, f"medium seed={seed}")
+    check(policy_hbm, p, f"medium seed={seed} hbm")
+
+
+# ---------------------------------------------------------------- workloads
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
+def test_configs(policy, cfg):
+    check(policy, wl.CONFIGS[cfg](), f"config{cfg}")
+
+
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_configs_relabelled(policy, cfg):
+    p = wl.CONFIGS[cfg]()
+    q = wl.relabel(p, np.random.default_rng(cfg).permutation(p.n_nodes))
+    assert not q.wf_contiguous
+    check(policy, q, f"config{cfg} relabelled")
+
+
+def test_config_contiguous_flag_not_set(policy):
+    """The grouping path on ids that happen to be grouped already."""
+    check(policy, wl.paper_scale(), "config1 grouped by the library", flags=0)
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 3])
+def test_configs_hbm_sweep(policy_hbm, cfg):
+    check(policy_hbm, wl.CONFIGS[cfg](), f"config{cfg} hbm")
+
+
+def test_deep_chains_hbm_small(policy_hbm):
+    check(policy_hbm, wl.deep_chains(W=64), "deep chains W=64 hbm")
+
+
+def test_other_seeds(policy):
+    for s in (11, 12):
+        check(policy, wl.paper_scale(seed=s), f"paper-scale seed {s}")
+        check(policy, wl.wide_mapreduce(seed=s, W=32, fan=1000), f"mapreduce seed {s}")
+
+
+def test_repeat_is_deterministic(policy):
+    p = wl.wide_mapreduce(W=64)
+    a = gpu_run(policy, p)
+    for _ in range(3):
+        b = gpu_run(policy, p)
+        for f in ("rem", "order", "slack", "route", "cost"):
+            assert np.array_equal(a[f], b[f])
+
+
+def test_scratch_reuse_across_sizes(policy):
+    for p in (wl.tiny(), wl.wide_mapreduce(W=64), wl.tiny(seed=3), wl.paper_scale(),
+              wl.random_dag(5, n_nodes=30, n_workflows=2)):
+        check(policy, p, f"reuse {p.name}")
+
+
+def test_fresh_handle_each_call():
+    for _ in range(3):
+        with nalar.Policy() as pol:
+            check(pol, wl.tiny(), "fresh handle")
+
+
+# ---------------------------------------------------------------- degenerate
+
+def test_degenerate_cases(policy):
+    base = wl.tiny()
+    N = base.n_nodes
+    cases = {
+        "all done": base.copy(done=np.ones(N, np.uint8)),
+        "no edges": base.copy(dep_off=np.zeros(N + 1, np.int32), dep_idx=np.zeros(0, np.int32),
+                              done=np.zeros(N, np.uint8)),
+        "no instances": base.copy(inst_type=np.zeros(0, np.int32), inst_load_us=np.zeros(0, np.int64),
+                                  inst_speed_permille=np.zeros(0, np.int32),
+                                  loc=np.full(N, -1, np.int32)),
+        "one instance": base.copy(inst_type=np.zeros(1, np.int32), inst_load_us=np.zeros(1, np.int64),
+                                  inst_speed_permille=np.ones(1, np.int32),
+                                  loc=np.where(base.loc >= 0, 0, -1).astype(np.int32)),
+        "equal slack": base.copy(est_us=np.ones(N, np.int64), deadline_us=np.full(64, base.now_us + 10**6)),
+        "zero est": base.copy(est_us=np.zeros(N, np.int64)),
+        "negative slack": base.copy(deadline_us=base.deadline_us - 10**9),
+        "max est": base.copy(est_us=np.full(N, 1 << 40, np.int64)),
+        "max load": base.copy(inst_load_us=np.full(base.n_instances, 1 << 60, np.int64),
+                              migration_cost_us=1 << 60),
+        "single workflow": base.copy(wf=np.zeros(N, np.int32), deadline_us=base.deadline_us[:1].copy(),
+                                     dep_off=np.zeros(N + 1, np.int32), dep_idx=np.zeros(0, np.int32)),
+    }
+    for label, p in cases.items():
+        check(policy, p, label)
+
+
+def test_empty_and_single(policy):
+    one = wl.Problem("one", 10, 7, np.zeros(1, np.int32), np.zeros(1, np.int32),
+                     np.array([5], np.int64), np.zeros(1, np.uint8), np.array([0], np.int32),
+                     np.array([0, 0], np.int32), np.zeros(0, np.int32), np.array([20], np.int64),
+                     np.array([0], np.int32), np.array([3], np.int64), np.array([1000], np.int32), True)
+    check(policy, one, "single future")
+    empty = one.copy(wf=np.zeros(0, np.int32), type=np.zeros(0, np.int32), est_us=np.zeros(0, np.int64),
+                     done=np.zeros(0, np.uint8), loc=np.zeros(0, np.int32), dep_off=np.array([0], np.int32))
+    check(policy, empty, "no futures")
+    nowf = empty.copy(deadline_us=np.zeros(0, np.int64))
+    check(policy, nowf, "no futures, no workflows")
+
+
+# ---------------------------------------------------------------- errors
+
+ERROR_CASES = [
+    ("wf", 5, -1), ("wf", 5, 64), ("type", 3, -1), ("loc", 7, -2), ("loc", 7, 16),
+    ("est_us", 9, -1), ("est_us", 9, (1 << 40) + 1), ("done", 4, 2),
+    ("dep_idx", 10, -1), ("dep_idx", 10, 2048), ("dep_idx", 10, 40),
+    ("dep_off", 0, 1), ("dep_off", 2048, 1), ("inst_type", 0, -1),
+    ("inst_speed_permille", 2, 0), ("inst_load_us", 1, -1), ("inst_load_us", 1, (1 << 60) + 1),
+    ("deadline_us", 3, wl.NOW_US + (1 << 61) + 1),
+]
+
+
+@pytest.mark.parametrize("case", ERROR_CASES)
+def test_error_rules(policy, case):
+    field, idx, value = case
+    p = wl.tiny().copy()
+    getattr(p, field)[idx] = value
+    check(policy, p, f"error {case}")
+    q = wl.relabel(wl.tiny(), np.random.default_rng(9).permutation(2048)).copy()
+    if field in ("dep_off", "dep_idx"):
+        return
+    getattr(q, field)[idx] = value
+    check(policy, q, f"error {case} relabelled")
+
+
+def test_error_cycle_and_self_loop(policy, policy_hbm):
+    p = wl.tiny().copy()
+    p.dep_idx[p.dep_off[12]] = 12
+    check(policy, p, "self loop")
+    check(policy_hbm, p, "self loop hbm")
+    c = wl.Problem("cyc", 0, 0, np.zeros(3, np.int32), np.zeros(3, np.int32), np.ones(3, np.int64),
+                   np.zeros(3, np.uint8), -np.ones(3, np.int32), np.array([0, 1, 2, 3], np.int32),
+                   np.array([2, 0, 1], np.int32), np.array([100], np.int64), np.zeros(0, np.int32),
+                   np.zeros(0, np.int64), np.zeros(0, np.int32), True)
+    check(policy, c, "3-cycle")
+    check(policy_hbm, c, "3-cycle hbm")
+
+
+def test_error_contiguous_promise_broken(policy):
+    p = wl.relabel(wl.tiny(), np.random.default_rng(2).permutation(2048))
+    g = gpu_run(policy, p, flags=nalar.NALAR_WF_CONTIGUOUS)
+    assert g["status"] == nalar.NALAR_EINVAL
+
+
+def test_error_overflow_and_precedence(policy):
+    n = (1 << 22) + 1
+    chain = wl.Problem("chain", 0, 0, np.zeros(n, np.int32), np.zeros(n, np.int32),
+                       np.full(n, 1 << 40, np.int64), np.zeros(n, np.uint8), -np.ones(n, np.int32),
+                       np.r_[0, 0, np.arange(1, n)].astype(np.int32), np.arange(n - 1).astype(np.int32),
+                       np.array([0], np.int64), np.zeros(0, np.int32), np.zeros(0, np.int64),
+                       np.zeros(0, np.int32), True)
+    check(policy, chain, "overflowing chain")
+    cyc = chain.copy()
+    cyc.dep_idx[0] = 5
+    check(policy, cyc, "cycle beats overflow")
+
+
+def test_handle_usable_after_error(policy):
+    p = wl.tiny().copy()
+    p.type[0] = -1
+    assert gpu_run(policy, p)["status"] == nalar.NALAR_EINVAL
+    check(policy, wl.tiny(), "after error")
+
+
+def test_null_arguments(policy):
+    dp = nalar.DeviceProblem.from_host(wl.tiny())
+    out = nalar.DeviceResult.alloc(dp.n_nodes)
+    raw = dp.c_struct()
+    raw.dep_idx = None
+    assert policy.run_pass(dp, out, raw=raw) == nalar.NALAR_EINVAL
+    raw = dp.c_struct()
+    raw.reserved = 1
+    assert policy.run_pass(dp, out, raw=raw) == nalar.NALAR_EINVAL
+    cr = out.c_struct()
+    cr.order = None
+    assert nalar.nalar_policy_pass(policy.handle, dp.c_struct(), cr) == nalar.NALAR_EINVAL
+
+
+# ---------------------------------------------------------------- dynamic stream
+
+_stream_state = {}
+
+
+def _stream():
+    if "it" not in _stream_state:
+        _stream_state["it"] = wl.dynamic_stream(steps=100)
+        _stream_state["next"] = 0
+    return _stream_state
+
+
+@pytest.mark.parametrize("chunk", range(11))
+def test_dynamic_stream_every_step(policy, chunk):
+    """Steps 0..100 of the evolving map/reduce graph, bit-exact at every step."""
+    st = _stream()
+    lo, hi = chunk * 10, min(chunk * 10 + 9, 100) if chunk < 10 else 100
+    if chunk == 10:
+        lo = 100
+    assert st["next"] == lo, "dynamic stream chunks must run in order"
+    pool = cf.ThreadPoolExecutor(max_workers=8)
+    futs = []
+    for step in range(lo, hi + 1):
+        snap = next(st["it"]).copy()
+        st["next"] = step + 1
+        say(f"[gpu] dynamic step {step}: N={snap.n_nodes}")
+        g = gpu_run(policy, snap)
+        futs.append((step, g, pool.submit(oracle.run, snap)))
+    for step, g, f in futs:
+        assert_parity(g, f.result(), f"dynamic step {step}")
+    pool.shutdown()
