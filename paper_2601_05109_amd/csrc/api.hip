@@ -21,17 +21,15 @@ struct Arena {
   void* base = nullptr;
   size_t bytes = 0;
   size_t lookback_off = 0, lookback_bytes = 0;
-  size_t wflb_off = 0, wflb_bytes = 0;
   Ctrl* ctrl = nullptr;
   ITab itab{};
   uint32_t* ghist_slack = nullptr;
   uint32_t* ghist_group = nullptr;
   int32_t* wf_off = nullptr;
-  uint64_t* wf_lb = nullptr;
-  int64_t* cmp_slack = nullptr;
-  int32_t* cmp_v = nullptr;
-  int32_t* cmp_route = nullptr;
-  int64_t* cmp_cost = nullptr;
+  uint8_t* stg_ready = nullptr;
+  int64_t* stg_slack = nullptr;
+  int32_t* stg_route = nullptr;
+  int64_t* stg_cost = nullptr;
   uint64_t* skey[2] = {nullptr, nullptr};
   uint32_t* spay[2] = {nullptr, nullptr};
   uint64_t* slb = nullptr;
@@ -103,14 +101,10 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W) {
   a.ghist_slack = reinterpret_cast<uint32_t*>(take(4 * kMaxSortPasses * kRadixBuckets));
   a.ghist_group = reinterpret_cast<uint32_t*>(take(4 * kMaxGroupPasses * kRadixBuckets));
   a.wf_off = reinterpret_cast<int32_t*>(take(4 * size_t(w1 + 1)));
-  off = align_up(off, 256);
-  a.wflb_off = off;
-  a.wf_lb = reinterpret_cast<uint64_t*>(take(8 * size_t(w1)));
-  a.wflb_bytes = off - a.wflb_off;
-  a.cmp_slack = reinterpret_cast<int64_t*>(take(8 * size_t(n1)));
-  a.cmp_cost = reinterpret_cast<int64_t*>(take(8 * size_t(n1)));
-  a.cmp_v = reinterpret_cast<int32_t*>(take(4 * size_t(n1)));
-  a.cmp_route = reinterpret_cast<int32_t*>(take(4 * size_t(n1)));
+  a.stg_slack = reinterpret_cast<int64_t*>(take(8 * size_t(n1)));
+  a.stg_cost = reinterpret_cast<int64_t*>(take(8 * size_t(n1)));
+  a.stg_route = reinterpret_cast<int32_t*>(take(4 * size_t(n1)));
+  a.stg_ready = reinterpret_cast<uint8_t*>(take(size_t(n1)));
   for (int i = 0; i < 2; ++i) a.skey[i] = reinterpret_cast<uint64_t*>(take(8 * size_t(n1)));
   for (int i = 0; i < 2; ++i) a.spay[i] = reinterpret_cast<uint32_t*>(take(4 * size_t(n1)));
   for (int i = 0; i < 2; ++i) a.gkey[i] = reinterpret_cast<uint32_t*>(take(4 * size_t(n1)));
@@ -319,8 +313,6 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   h->epoch = (h->epoch + 1) & kEpochMask;
   if (h->epoch == 0) {  // tags wrapped: forget every old look-back word
     e = hipMemsetAsync(static_cast<char*>(A.base) + A.lookback_off, 0, A.lookback_bytes, s);
-    if (e == hipSuccess)
-      e = hipMemsetAsync(static_cast<char*>(A.base) + A.wflb_off, 0, A.wflb_bytes, s);
     if (e != hipSuccess) return hip_fail(h, e, "hipMemsetAsync(look-back)");
     h->epoch = 1;
   }
@@ -356,6 +348,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     g.pay_buf[1] = A.gpay[1];
     g.count_dev = nullptr;
     g.count_host = N;
+    g.first_span = N;
     g.lookback = A.glb;
     g.ghist = A.ghist_group;
     g.tiles_cap = tiles_of(A.capN);
@@ -381,11 +374,10 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     sa.node_of_pos = node_of_pos;
     sa.pos_of_node = pos_of_node;
     sa.rem_out = r->rem_us;
-    sa.cmp_slack = A.cmp_slack;
-    sa.cmp_v = A.cmp_v;
-    sa.cmp_route = A.cmp_route;
-    sa.cmp_cost = A.cmp_cost;
-    sa.wf_lb = A.wf_lb;
+    sa.stg_ready = A.stg_ready;
+    sa.stg_slack = A.stg_slack;
+    sa.stg_route = A.stg_route;
+    sa.stg_cost = A.stg_cost;
     sa.g_cnt = A.g_cnt;
     sa.g_mx = A.g_mx;
     sa.g_dn = A.g_dn;
@@ -393,35 +385,35 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     sa.g_front0 = A.g_front[0];
     sa.g_front1 = A.g_front[1];
     sa.ctrl = A.ctrl;
-    sa.epoch = epoch;
     sa.force_global = (h->flags & NALAR_FORCE_GLOBAL_SWEEP) ? 1 : 0;
     const SweepShape sh = plan_sweep(N, W, M, h->cus, h->lds_limit);
     NALAR_LAUNCH("sweep", launch_sweep(s, sa, sh));
 
     RadixDesc d{};
-    d.slack = A.cmp_slack;
+    d.stg_slack = A.stg_slack;
+    d.stg_ready = A.stg_ready;
     d.key_buf[0] = A.skey[0];
     d.key_buf[1] = A.skey[1];
     d.pay_buf[0] = A.spay[0];
     d.pay_buf[1] = A.spay[1];
     d.count_dev = &A.ctrl->n_ready;
     d.count_host = 0;
+    d.first_span = N;
     d.lookback = A.slb;
     d.ghist = A.ghist_slack;
     d.tiles_cap = tiles_of(A.capN);
     d.npass_host = -1;
     d.ticket_base = 0;
-    NALAR_LAUNCH("sort_hist", launch_radix_hist(s, d, A.ctrl, kSrcSlack, N, true));
+    NALAR_LAUNCH("sort_hist", launch_radix_hist(s, d, A.ctrl, kSrcStaged, N, true));
     for (int ps = 0; ps < kMaxSortPasses; ++ps)
       NALAR_LAUNCH(kSortPassNames[ps], launch_radix_pass(s, d, A.ctrl,
-                                                         ps == 0 ? kSrcSlack : kSrcBuffers, ps,
+                                                         ps == 0 ? kSrcStaged : kSrcBuffers, ps,
                                                          epoch, N, true));
     EmitArgs ea{};
     ea.ctrl = A.ctrl;
-    ea.cmp_slack = A.cmp_slack;
-    ea.cmp_v = A.cmp_v;
-    ea.cmp_route = A.cmp_route;
-    ea.cmp_cost = A.cmp_cost;
+    ea.node_of_pos = node_of_pos;
+    ea.stg_route = A.stg_route;
+    ea.stg_cost = A.stg_cost;
     ea.key_buf[0] = A.skey[0];
     ea.key_buf[1] = A.skey[1];
     ea.pay_buf[0] = A.spay[0];

@@ -34,16 +34,21 @@ __host__ __device__ inline uint64_t lb_pack(uint32_t epoch, uint64_t flag, uint6
 }
 
 // Per-pass control block in device memory.  Initialised by the setup kernel
-// at the start of every pass.
+// at the start of every pass.  The sweep folds each workgroup's slack range and
+// ready count into one of kParts slots (spreading the atomics over many
+// addresses); the histogram kernel reduces the slots.
+constexpr int kParts = 64;
+
 struct Ctrl {
   uint32_t status;
-  uint32_t sort_npass;           // digit passes the slack sort needs
+  uint32_t sort_npass;           // digit passes the slack sort runs
   int64_t n_ready;
   int64_t slack_min;
   int64_t slack_max;
-  uint32_t wf_ticket;            // next workflow for the sweep's blocks
-  uint32_t pad0;
   uint32_t tile_ticket[16];      // per radix pass: [0,8) slack sort, [8,12) grouping
+  int64_t part_min[kParts];
+  int64_t part_max[kParts];
+  int64_t part_cnt[kParts];
 };
 
 // Instance table sorted by (type, original index), plus the sorted position of

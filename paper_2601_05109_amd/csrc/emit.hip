@@ -13,24 +13,15 @@ __global__ __launch_bounds__(kEmitThreads) void k_emit(EmitArgs a) {
   const Ctrl* ctrl = a.ctrl;
   if (ctrl->status) return;
   const int64_t R = ctrl->n_ready;
-  const int npass = int(ctrl->sort_npass);
-  const int fin = (npass - 1) & 1;
+  const int fin = (int(ctrl->sort_npass) - 1) & 1;   // at least one pass ran when R > 0
   const int64_t smin = ctrl->slack_min;
   const int64_t stride = int64_t(gridDim.x) * kEmitThreads;
   for (int64_t i = int64_t(blockIdx.x) * kEmitThreads + threadIdx.x; i < R; i += stride) {
-    int64_t idx, slack;
-    if (npass == 0) {
-      // every ready future has the same slack: the compacted (wf, id) order is final
-      idx = i;
-      slack = a.cmp_slack[i];
-    } else {
-      idx = a.pay_buf[fin][i];
-      slack = int64_t(a.key_buf[fin][i] + uint64_t(smin));
-    }
-    a.order[i] = a.cmp_v[idx];
-    a.slack[i] = slack;
-    a.route[i] = a.cmp_route[idx];
-    if (a.cost) a.cost[i] = a.cmp_cost[idx];
+    const uint32_t pos = a.pay_buf[fin][i];
+    a.order[i] = a.node_of_pos ? a.node_of_pos[pos] : int32_t(pos);
+    a.slack[i] = int64_t(a.key_buf[fin][i] + uint64_t(smin));
+    a.route[i] = a.stg_route[pos];
+    if (a.cost) a.cost[i] = a.stg_cost[pos];
   }
 }
 

@@ -23,8 +23,12 @@ __global__ __launch_bounds__(kSetupThreads) void k_setup(ProblemDev p, Ctrl* ctr
     ctrl->n_ready = 0;
     ctrl->slack_min = INT64_MAX;
     ctrl->slack_max = INT64_MIN;
-    ctrl->wf_ticket = 0;
     for (int i = 0; i < 16; ++i) ctrl->tile_ticket[i] = 0;
+  }
+  for (int i = tid; i < kParts; i += kSetupThreads) {
+    ctrl->part_min[i] = INT64_MAX;
+    ctrl->part_max[i] = INT64_MIN;
+    ctrl->part_cnt[i] = 0;
   }
   for (int i = tid; i < kMaxSortPasses * kRadixBuckets; i += kSetupThreads) ghist_slack[i] = 0;
   for (int i = tid; i < kMaxGroupPasses * kRadixBuckets; i += kSetupThreads) ghist_group[i] = 0;

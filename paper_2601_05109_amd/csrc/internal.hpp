@@ -28,21 +28,25 @@ struct ProblemDev {
 // Radix-sort plumbing shared by the slack sort and the workflow grouping.
 enum RadixSource : int {
   kSrcBuffers = 0,  // keys/payloads from the ping-pong buffers (passes >= 1)
-  kSrcSlack = 1,    // key = slack - min slack, payload = index (slack sort, pass 0)
+  kSrcStaged = 1,   // ready futures staged by position: key = slack - min slack,
+                    // payload = position; non-ready positions are skipped, so the
+                    // first pass also compacts (slack sort, pass 0)
   kSrcWf = 2,       // key = workflow id, payload = node id (grouping, pass 0)
 };
 
 struct RadixDesc {
-  const int64_t* slack;     // kSrcSlack source
+  const int64_t* stg_slack; // kSrcStaged source
+  const uint8_t* stg_ready; // kSrcStaged validity
   const int32_t* wf;        // kSrcWf source
   void* key_buf[2];         // ping-pong keys (uint64 or uint32)
   uint32_t* pay_buf[2];     // ping-pong payloads
-  const int64_t* count_dev; // element count in device memory, or NULL
-  int64_t count_host;       // element count when count_dev is NULL
+  const int64_t* count_dev; // dense element count in device memory, or NULL
+  int64_t count_host;       // dense element count when count_dev is NULL
+  int64_t first_span;       // positions scanned by the histogram and pass 0
   uint64_t* lookback;       // [passes][tiles_cap][256]
   uint32_t* ghist;          // [passes][256]
   int64_t tiles_cap;
-  int npass_host;           // -1: read Ctrl::sort_npass
+  int npass_host;           // -1: the histogram kernel decides (slack sort)
   int ticket_base;          // first Ctrl::tile_ticket slot of this sort
 };
 
@@ -53,11 +57,10 @@ struct SweepArgs {
   const int32_t* node_of_pos;   // NULL: position == node id
   const int32_t* pos_of_node;   // NULL: position == node id
   int64_t* rem_out;             // [N] or NULL
-  int64_t* cmp_slack;           // [R] compacted in (wf, id) order
-  int32_t* cmp_v;
-  int32_t* cmp_route;
-  int64_t* cmp_cost;
-  uint64_t* wf_lb;              // [W] look-back words of the ready counts
+  uint8_t* stg_ready;           // [N] by position: 1 = ready
+  int64_t* stg_slack;           // [N] by position, written for ready futures
+  int32_t* stg_route;
+  int64_t* stg_cost;
   int32_t* g_cnt;               // HBM sweep state, by position
   int64_t* g_mx;
   uint8_t* g_dn;
@@ -65,16 +68,14 @@ struct SweepArgs {
   int32_t* g_front0;
   int32_t* g_front1;
   Ctrl* ctrl;
-  uint32_t epoch;
   int force_global;
 };
 
 struct EmitArgs {
   Ctrl* ctrl;
-  const int64_t* cmp_slack;
-  const int32_t* cmp_v;
-  const int32_t* cmp_route;
-  const int64_t* cmp_cost;
+  const int32_t* node_of_pos;   // NULL: position == node id
+  const int32_t* stg_route;
+  const int64_t* stg_cost;
   const uint64_t* key_buf[2];
   const uint32_t* pay_buf[2];
   int32_t* order;

@@ -5,8 +5,10 @@
 //
 // Used twice per pass:
 //  * the slack sort: key = slack - min slack (range-reduced, so only the digits
-//    the key range needs are sorted), payload = position in the compacted ready
-//    list, whose (wf, id) order stability carries into the final order;
+//    the key range needs are sorted), payload = position of the ready future;
+//    its first pass reads the futures staged by position and skips the
+//    positions that are not ready, so it also compacts them, and the stable
+//    passes keep (wf, id) order among equal slacks;
 //  * grouping futures by workflow when the caller's ids are not grouped:
 //    key = wf, payload = id.
 //
@@ -22,31 +24,55 @@ namespace {
 constexpr int kWavesPerTile = kSortThreads / kWave;
 
 template <typename K>
-__device__ inline K load_key(const RadixDesc& d, int src, int64_t i, const Ctrl* ctrl,
-                             int64_t slack_min) {
-  if (src == kSrcSlack) return K(uint64_t(d.slack[i] - slack_min));
-  if (src == kSrcWf) return K(uint32_t(d.wf[i]));
-  return static_cast<const K*>(d.key_buf[0])[i];
+__device__ inline K first_key(const RadixDesc& d, int src, int64_t i, int64_t slack_min) {
+  if (src == kSrcStaged) return K(uint64_t(d.stg_slack[i] - slack_min));
+  return K(uint32_t(d.wf[i]));
 }
 
-__device__ inline int64_t radix_count(const RadixDesc& d) {
-  return d.count_dev ? *d.count_dev : d.count_host;
+__device__ inline bool first_valid(const RadixDesc& d, int src, int64_t i) {
+  return i < d.first_span && (src != kSrcStaged || d.stg_ready[i] != 0);
 }
 
-// Digit histograms of all passes the key range needs.
+// Slack range and ready count of the staged futures, from the sweep's slots.
+struct StagedRange {
+  int64_t smin, smax, count;
+};
+
+__device__ inline StagedRange reduce_parts(const Ctrl* ctrl) {
+  StagedRange r{INT64_MAX, INT64_MIN, 0};
+  for (int i = 0; i < kParts; ++i) {
+    const int64_t a = ctrl->part_min[i], b = ctrl->part_max[i];
+    r.smin = a < r.smin ? a : r.smin;
+    r.smax = b > r.smax ? b : r.smax;
+    r.count += ctrl->part_cnt[i];
+  }
+  return r;
+}
+
+// Digit histograms of all passes the key range needs.  For the slack sort this
+// kernel also settles the ready count, the slack range and the pass count
+// (at least one pass when anything is ready: the first pass compacts).
 template <typename K>
 __global__ __launch_bounds__(kSortThreads) void k_radix_hist(RadixDesc d, Ctrl* ctrl, int src) {
   if (ctrl->status) return;
-  const int64_t R = radix_count(d);
-  if (R <= 0) return;
   int npass;
   int64_t smin = 0;
   if (d.npass_host < 0) {
-    smin = ctrl->slack_min;
-    const uint64_t range = uint64_t(ctrl->slack_max - smin);
-    const int nbits = range ? 64 - __builtin_clzll(range) : 0;
-    npass = (nbits + kRadixBits - 1) / kRadixBits;
-    if (blockIdx.x == 0 && threadIdx.x == 0) ctrl->sort_npass = uint32_t(npass);
+    const StagedRange r = reduce_parts(ctrl);
+    smin = r.smin;
+    int nbits = 0;
+    if (r.count > 0) {
+      const uint64_t range = uint64_t(r.smax - r.smin);
+      nbits = range ? 64 - __builtin_clzll(range) : 0;
+    }
+    npass = r.count > 0 ? (nbits + kRadixBits - 1) / kRadixBits : 0;
+    if (r.count > 0 && npass == 0) npass = 1;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      ctrl->slack_min = r.smin;
+      ctrl->slack_max = r.smax;
+      ctrl->n_ready = r.count;
+      ctrl->sort_npass = uint32_t(npass);
+    }
   } else {
     npass = d.npass_host;
   }
@@ -55,11 +81,12 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_hist(RadixDesc d, Ctrl* 
   for (int i = threadIdx.x; i < kMaxSortPasses * kRadixBuckets; i += kSortThreads)
     (&h[0][0])[i] = 0;
   __syncthreads();
+  const int64_t span = d.first_span;
   const int64_t stride = int64_t(gridDim.x) * kSortThreads;
-  for (int64_t base = int64_t(blockIdx.x) * kSortThreads; base < R; base += stride) {
+  for (int64_t base = int64_t(blockIdx.x) * kSortThreads; base < span; base += stride) {
     const int64_t i = base + threadIdx.x;
-    const bool valid = i < R;
-    K key = valid ? load_key<K>(d, src, i, ctrl, smin) : K(0);
+    const bool valid = first_valid(d, src, i);
+    const K key = valid ? first_key<K>(d, src, i, smin) : K(0);
     for (int ps = 0; ps < npass; ++ps) {
       const uint32_t dg = uint32_t(key >> (ps * kRadixBits)) & (kRadixBuckets - 1);
       // most high digits are shared by the whole wave: one add instead of 64
@@ -97,14 +124,17 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixDesc d, Ctrl* 
   if (ctrl->status) return;
   const int npass = d.npass_host >= 0 ? d.npass_host : int(ctrl->sort_npass);
   if (pass >= npass) return;
-  const int64_t R = radix_count(d);
-  const int64_t ntiles = (R + kSortTile - 1) / kSortTile;
+  const bool first = pass == 0 && src != kSrcBuffers;
+  const int64_t R = d.count_dev ? *d.count_dev : d.count_host;   // dense count
+  const int64_t span = first ? d.first_span : R;                  // items scanned
+  const int64_t ntiles = (span + kSortTile - 1) / kSortTile;
 
   __shared__ uint32_t s_tile;
   __shared__ uint32_t s_whist[kWavesPerTile][kRadixBuckets];
   __shared__ uint32_t s_tprefix[kRadixBuckets];
   __shared__ uint64_t s_gstart[kRadixBuckets];
   __shared__ uint32_t s_tmp[kWavesPerTile];
+  __shared__ uint32_t s_intile;
   __shared__ K s_key[kSortTile];
   __shared__ uint32_t s_pay[kSortTile];
 
@@ -119,7 +149,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixDesc d, Ctrl* 
   const int ln = lane_id();
   const int shift = pass * kRadixBits;
   const int64_t seg = tile * kSortTile + int64_t(wv) * (kWave * kSortItems);
-  const int64_t smin = (src == kSrcSlack) ? ctrl->slack_min : 0;
+  const int64_t smin = (src == kSrcStaged) ? ctrl->slack_min : 0;
   const K* kin = static_cast<const K*>(d.key_buf[(pass + 1) & 1]);
   const uint32_t* pin = d.pay_buf[(pass + 1) & 1];
   K* kout = static_cast<K*>(d.key_buf[pass & 1]);
@@ -128,20 +158,22 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixDesc d, Ctrl* 
   K key[kSortItems];
   uint32_t pay[kSortItems];
   uint32_t rank[kSortItems];
+  uint32_t validm = 0;
 #pragma unroll
   for (int j = 0; j < kSortItems; ++j) {
     const int64_t i = seg + j * kWave + ln;
-    if (i < R) {
-      if (pass == 0 && src != kSrcBuffers) {
-        key[j] = load_key<K>(d, src, i, ctrl, smin);
+    key[j] = K(0);
+    pay[j] = 0;
+    if (first) {
+      if (first_valid(d, src, i)) {
+        key[j] = first_key<K>(d, src, i, smin);
         pay[j] = uint32_t(i);
-      } else {
-        key[j] = kin[i];
-        pay[j] = pin[i];
+        validm |= 1u << j;
       }
-    } else {
-      key[j] = K(0);
-      pay[j] = 0;
+    } else if (i < span) {
+      key[j] = kin[i];
+      pay[j] = pin[i];
+      validm |= 1u << j;
     }
   }
 
@@ -150,7 +182,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixDesc d, Ctrl* 
   uint32_t* wh = s_whist[wv];
 #pragma unroll
   for (int j = 0; j < kSortItems; ++j) {
-    const bool valid = seg + j * kWave + ln < R;
+    const bool valid = (validm >> j) & 1u;
     const uint32_t dg = uint32_t(key[j] >> shift) & (kRadixBuckets - 1);
     uint64_t peers = ballot(valid);
 #pragma unroll
@@ -188,13 +220,14 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixDesc d, Ctrl* 
   }
   s_tprefix[dg] = texcl;
   s_gstart[dg] = uint64_t(gexcl) + excl;
+  if (dg == kRadixBuckets - 1) s_intile = texcl + tot;
   __syncthreads();
 
   // Stage the tile in digit order in LDS, then write runs of equal digits to
   // consecutive global addresses.
 #pragma unroll
   for (int j = 0; j < kSortItems; ++j) {
-    if (seg + j * kWave + ln < R) {
+    if ((validm >> j) & 1u) {
       const uint32_t dgt = uint32_t(key[j] >> shift) & (kRadixBuckets - 1);
       const uint32_t pos = s_tprefix[dgt] + s_whist[wv][dgt] + rank[j];
       s_key[pos] = key[j];
@@ -202,7 +235,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixDesc d, Ctrl* 
     }
   }
   __syncthreads();
-  const int64_t in_tile = (R - tile * kSortTile) < kSortTile ? (R - tile * kSortTile) : kSortTile;
+  const int in_tile = int(s_intile);
   for (int i = tid; i < in_tile; i += kSortThreads) {
     const K k = s_key[i];
     const uint32_t dgt = uint32_t(k >> shift) & (kRadixBuckets - 1);

@@ -3,8 +3,7 @@
 //
 // Futures of different workflows never depend on each other (one global
 // controller per workflow, Section 4.1; cross-workflow dependencies are
-// rejected), so each workgroup takes whole workflows from a ticket counter and
-// runs the reverse level-synchronous max-plus sweep of each one with workgroup
+// rejected), so each workgroup takes whole workflows and runs the reverse level-synchronous max-plus sweep of each one with workgroup
 // barriers only:
 //
 //   cnt[u] = number of consumers of u (atomic out-degree counters)
@@ -25,10 +24,11 @@
 // and process explicit frontier lists.  Futures with more dependencies than a
 // thread keeps are handled by the whole workgroup.
 //
-// Readiness is known before the sweep, so each workflow publishes its ready
-// count at once (decoupled look-back over workflow tickets) and later writes
-// its ready futures, routed and with their slack, at their final compacted
-// positions: workflows ascending, ids ascending inside a workflow.
+// Workgroups take workflows round-robin and never wait on each other.  Each
+// ready future is routed and written, with its slack, at its own position
+// (workflows ascending, ids ascending inside a workflow); the first digit pass
+// of the slack sort skips the other positions, which compacts the list without
+// disturbing that order.
 #include "internal.hpp"
 
 namespace nalar {
@@ -169,7 +169,6 @@ __device__ inline int64_t clamp_rem(int64_t r, bool& overflow) {
 
 // Workgroup-shared bookkeeping of the sweep (one instance per workgroup).
 struct Shared {
-  int w;
   int hcount;
   int fcount;
   int fnext;
@@ -177,8 +176,6 @@ struct Shared {
   int32_t hk[kHeavyCap];
   int32_t ho[kHeavyCap];
   int32_t hd[kHeavyCap];
-  uint32_t wtot[128];      // [NPT][waves] (LDS path) or [waves] (HBM path)
-  int64_t base;
   int64_t red[3][16];
 };
 
@@ -197,31 +194,19 @@ struct Acc {
   int64_t tready = 0;
 };
 
-__device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_t slot, int32_t v,
+__device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_t pos, int32_t v,
                                    int64_t rem, int64_t est, int64_t dl, Acc& acc) {
   const int64_t slack = dl - rem;
   int32_t route;
   int64_t cost;
   route_future(a.p.type[v], est, a.p.loc[v], int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load,
                it.speed, it.inv, it.pos, route, cost);
-  a.cmp_slack[slot] = slack;
-  a.cmp_v[slot] = v;
-  a.cmp_route[slot] = route;
-  a.cmp_cost[slot] = cost;
+  a.stg_slack[pos] = slack;
+  a.stg_route[pos] = route;
+  a.stg_cost[pos] = cost;
   acc.tmin = slack < acc.tmin ? slack : acc.tmin;
   acc.tmax = slack > acc.tmax ? slack : acc.tmax;
-}
-
-__device__ inline void publish_ready_count(const SweepArgs& a, int w, uint32_t count) {
-  st_relaxed_agent(&a.wf_lb[w], lb_pack(a.epoch, w == 0 ? kLbInc : kLbAgg, count));
-}
-
-// Exclusive ready prefix of workflow w (thread 0 only).
-__device__ inline int64_t ready_base(const SweepArgs& a, int w, uint32_t count) {
-  if (w == 0) return 0;
-  const uint64_t excl = lookback_exclusive(a.wf_lb, w, 1, a.epoch);
-  st_relaxed_agent(&a.wf_lb[w], lb_pack(a.epoch, kLbInc, excl + count));
-  return int64_t(excl);
+  acc.tready += 1;
 }
 
 // ------------------------------------------------------------ LDS workflow
@@ -241,9 +226,7 @@ template <int T, int NPT>
 __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
                           int64_t* mx, int32_t* cnt, uint8_t* dn, uint8_t* nr, int w, int64_t b,
                           int n, int64_t dl, Acc& acc) {
-  constexpr int NW = T / kWave;
   const int tid = threadIdx.x;
-  const int wv = tid / kWave;
   Ctrl* ctrl = a.ctrl;
 
   int32_t vv[NPT];
@@ -329,35 +312,17 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
   }
   __syncthreads();
 
-  // ready flags, their compacted slots inside the workflow, the ready count
-  uint32_t slot[NPT];
+  // ready flags (staged by position for the sort's first pass)
 #pragma unroll
   for (int j = 0; j < NPT; ++j) {
     const int k = j * T + tid;
-    const bool rd = k < n && dn[k] == 0 && nr[k] == 0;
-    if (rd) ready |= 1u << j;
-    const uint64_t m = ballot(rd);
-    if (lane_id() == 0) S.wtot[j * NW + wv] = uint32_t(__popcll(m));
-    slot[j] = lanes_below(m);
-  }
-  __syncthreads();
-  uint32_t run = 0;
-#pragma unroll
-  for (int j = 0; j < NPT; ++j) {
-    uint32_t ctot = 0, before = 0;
-    for (int x = 0; x < NW; ++x) {
-      const uint32_t c = S.wtot[j * NW + x];
-      ctot += c;
-      before += x < wv ? c : 0u;
+    if (k < n) {
+      const bool rd = dn[k] == 0 && nr[k] == 0;
+      if (rd) ready |= 1u << j;
+      a.stg_ready[b + k] = rd ? 1 : 0;
     }
-    slot[j] += run + before;
-    run += ctot;
   }
-  if (tid == 0) {
-    publish_ready_count(a, w, run);
-    acc.tready += run;
-    S.hcount = 0;
-  }
+  if (tid == 0) S.hcount = 0;
 
   // C: levels
   bool overflow = false;
@@ -423,19 +388,14 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
   if (overflow) flag_status(ctrl, kStRange);
   if (fin) atomicAdd(&S.proc, __popc(fin));
   __syncthreads();
-  if (tid == 0) {
-    if (S.proc != n) flag_status(ctrl, kStCycle);
-    S.base = ready_base(a, w, run);
-  }
-  __syncthreads();
+  if (tid == 0 && S.proc != n) flag_status(ctrl, kStCycle);
 
-  // D: slack, route, write at the compacted slot
-  const int64_t base = S.base;
+  // D: slack, route, staged at the future's position
 #pragma unroll
   for (int j = 0; j < NPT; ++j) {
     if ((ready >> j) & 1u) {
       const int k = j * T + tid;
-      write_ready(a, it, base + slot[j], vv[j], mx[k], ee[j], dl, acc);
+      write_ready(a, it, b + k, vv[j], mx[k], ee[j], dl, acc);
     }
   }
   __syncthreads();
@@ -446,9 +406,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
 template <int T>
 __device__ void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
                           int w, int64_t b, int n, int64_t dl, Acc& acc) {
-  constexpr int NW = T / kWave;
   const int tid = threadIdx.x;
-  const int wv = tid / kWave;
   Ctrl* ctrl = a.ctrl;
   int32_t* cnt = a.g_cnt + b;
   int64_t* mx = a.g_mx + b;
@@ -518,23 +476,8 @@ __device__ void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it
   }
   __syncthreads();
 
-  // ready count
-  uint32_t mine = 0;
-  for (int k = tid; k < n; k += T) mine += (dn[k] == 0 && nr[k] == 0) ? 1u : 0u;
-  {
-    uint32_t s = mine;
-#pragma unroll
-    for (int m = 1; m < kWave; m <<= 1) s += __shfl_xor(s, m, kWave);
-    if (lane_id() == 0) S.wtot[wv] = s;
-  }
-  __syncthreads();
-  uint32_t total = 0;
-  for (int x = 0; x < NW; ++x) total += S.wtot[x];
-  if (tid == 0) {
-    publish_ready_count(a, w, total);
-    acc.tready += total;
-    S.hcount = 0;
-  }
+  for (int k = tid; k < n; k += T) a.stg_ready[b + k] = (dn[k] == 0 && nr[k] == 0) ? 1 : 0;
+  if (tid == 0) S.hcount = 0;
 
   // frontier 0: futures without consumers
   int32_t* cur = a.g_front0 + b;
@@ -614,32 +557,14 @@ __device__ void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it
     __syncthreads();
   }
   if (overflow) flag_status(ctrl, kStRange);
-  if (tid == 0) {
-    if (processed != n) flag_status(ctrl, kStCycle);
-    S.base = ready_base(a, w, total);
-  }
-  __syncthreads();
+  if (tid == 0 && processed != n) flag_status(ctrl, kStCycle);
 
-  // slack, route, compacted write in position order
-  int64_t run = S.base;
-  for (int k0 = 0; k0 < n; k0 += T) {
-    const int k = k0 + tid;
-    const bool rd = k < n && dn[k] == 0 && nr[k] == 0;
-    const uint64_t m = ballot(rd);
-    __syncthreads();
-    if (lane_id() == 0) S.wtot[wv] = uint32_t(__popcll(m));
-    __syncthreads();
-    uint32_t before = 0, ctot = 0;
-    for (int x = 0; x < NW; ++x) {
-      const uint32_t c = S.wtot[x];
-      ctot += c;
-      before += x < wv ? c : 0u;
-    }
-    if (rd) {
+  // slack, route, staged at the future's position
+  for (int k = tid; k < n; k += T) {
+    if (dn[k] == 0 && nr[k] == 0) {
       const int32_t v = node_at(L, b + k);
-      write_ready(a, it, run + before + lanes_below(m), v, ld_wg(&mx[k]), a.p.est[v], dl, acc);
+      write_ready(a, it, b + k, v, ld_wg(&mx[k]), a.p.est[v], dl, acc);
     }
-    run += ctot;
   }
   __syncthreads();
 }
@@ -680,26 +605,15 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
 
   const Layout L{a.node_of_pos, a.pos_of_node, a.p.N};
   Acc acc;
-  for (;;) {
-    if (tid == 0) S.w = int(atomicAdd(&ctrl->wf_ticket, 1u));
-    __syncthreads();
-    const int w = S.w;
-    __syncthreads();
-    if (int64_t(w) >= a.p.W) break;
+  for (int64_t w = blockIdx.x; w < a.p.W; w += gridDim.x) {
     const int64_t b = a.wf_off[w];
     const int n = a.wf_off[w + 1] - int32_t(b);
+    if (n <= 0) continue;
     const int64_t dl = a.p.deadline[w] - a.p.now;
-    if (n <= 0) {
-      if (tid == 0) {
-        publish_ready_count(a, w, 0);
-        ready_base(a, w, 0);
-      }
-      continue;
-    }
     if (!a.force_global && n <= lds_cap)
-      sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, w, b, n, dl, acc);
+      sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, int(w), b, n, dl, acc);
     else
-      sweep_hbm<T>(a, L, it, S, w, b, n, dl, acc);
+      sweep_hbm<T>(a, L, it, S, int(w), b, n, dl, acc);
   }
 
   // fold the block's slack range and ready count into the control block
@@ -717,9 +631,10 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
       a2 += S.red[2][x];
     }
     if (a2 > 0) {
-      __hip_atomic_fetch_min(&ctrl->slack_min, a0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_fetch_max(&ctrl->slack_max, a1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      add_agent(&ctrl->n_ready, a2);
+      const int slot = blockIdx.x & (kParts - 1);
+      __hip_atomic_fetch_min(&ctrl->part_min[slot], a0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_fetch_max(&ctrl->part_max[slot], a1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      add_agent(&ctrl->part_cnt[slot], a2);
     }
   }
 }
