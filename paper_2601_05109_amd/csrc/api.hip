@@ -1,8 +1,20 @@
 // C ABI of the policy pass: handle, scratch arena, launch sequence, status.
+//
+// A pass is a fixed sequence of launches on the handle's stream:
+//   nodes  -> validate the snapshot, sort the instance table, workflow offsets
+//   group  -> (only when the caller's ids are not grouped by workflow) stable
+//             radix sort of the ids by workflow
+//   sweep  -> remaining critical path, readiness, slack and routing
+//   sort   -> slack histogram and range, then four digit passes (those the
+//             range does not need return at once); the last needed pass
+//             gathers into the caller's arrays and writes the status into
+//             pinned host memory
+// followed by one stream synchronisation.  A slack range wider than 32 bits
+// reports "continue" and the remaining passes follow after a second
+// synchronisation.  The node kernel resets the next pass's control block.
 #include <cstdio>
 #include <cstring>
 #include <string>
-#include <vector>
 
 #include "internal.hpp"
 
@@ -10,7 +22,7 @@ using namespace nalar;
 
 namespace {
 
-constexpr int kMaxTimed = 32;
+constexpr int kMaxTimed = 24;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -21,10 +33,8 @@ struct Arena {
   void* base = nullptr;
   size_t bytes = 0;
   size_t lookback_off = 0, lookback_bytes = 0;
-  Ctrl* ctrl = nullptr;
+  Ctrl* ctrl[2] = {nullptr, nullptr};
   ITab itab{};
-  uint32_t* ghist_slack = nullptr;
-  uint32_t* ghist_group = nullptr;
   int32_t* wf_off = nullptr;
   uint8_t* stg_ready = nullptr;
   int64_t* stg_slack = nullptr;
@@ -54,9 +64,11 @@ struct nalar_policy {
   int cus = 0;
   size_t lds_limit = 0;
   uint32_t epoch = 0;
+  uint64_t passes = 0;           // selects the control block of the next pass
+  bool ctrl_dirty[2] = {true, true};
   std::string err;
   Arena ar;
-  Ctrl* host_ctrl = nullptr;  // pinned readback
+  HostStatus* host = nullptr;    // pinned, written by the sort kernel
   bool timing = false;
   int n_timed = 0;
   bool timed_valid = false;
@@ -91,15 +103,14 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W) {
   const int64_t n1 = N > 0 ? N : 1;
   const int64_t w1 = W > 0 ? W : 1;
   const int64_t tiles = tiles_of(n1);
-  a.ctrl = reinterpret_cast<Ctrl*>(take(sizeof(Ctrl)));
+  a.ctrl[0] = reinterpret_cast<Ctrl*>(take(sizeof(Ctrl)));
+  a.ctrl[1] = reinterpret_cast<Ctrl*>(take(sizeof(Ctrl)));
   a.itab.load = reinterpret_cast<int64_t*>(take(8 * NALAR_MAX_INSTANCES));
   a.itab.inv_speed = reinterpret_cast<double*>(take(8 * NALAR_MAX_INSTANCES));
   a.itab.type = reinterpret_cast<int32_t*>(take(4 * NALAR_MAX_INSTANCES));
   a.itab.idx = reinterpret_cast<int32_t*>(take(4 * NALAR_MAX_INSTANCES));
   a.itab.speed = reinterpret_cast<int32_t*>(take(4 * NALAR_MAX_INSTANCES));
   a.itab.pos_of = reinterpret_cast<int32_t*>(take(4 * NALAR_MAX_INSTANCES));
-  a.ghist_slack = reinterpret_cast<uint32_t*>(take(4 * kMaxSortPasses * kRadixBuckets));
-  a.ghist_group = reinterpret_cast<uint32_t*>(take(4 * kMaxGroupPasses * kRadixBuckets));
   a.wf_off = reinterpret_cast<int32_t*>(take(4 * size_t(w1 + 1)));
   a.stg_slack = reinterpret_cast<int64_t*>(take(8 * size_t(n1)));
   a.stg_cost = reinterpret_cast<int64_t*>(take(8 * size_t(n1)));
@@ -156,6 +167,7 @@ int ensure_capacity(nalar_policy* h, int64_t N, int64_t W) {
   fresh.capW = newW;
   h->ar = fresh;
   h->epoch = 0;
+  h->ctrl_dirty[0] = h->ctrl_dirty[1] = true;
   return NALAR_OK;
 }
 
@@ -195,18 +207,12 @@ struct Timer {
     h->names[n] = name;
     ++n;
   }
+  static void cb(void* self, const char* name) { static_cast<Timer*>(self)->mark(name); }
   void end() {
     if (!h->timing) return;
-    const int k = n < kMaxTimed ? n : kMaxTimed;
-    (void)hipEventRecord(h->ev[k], h->stream);
+    (void)hipEventRecord(h->ev[n < kMaxTimed ? n : kMaxTimed], h->stream);
   }
 };
-
-const char* kSortPassNames[kMaxSortPasses] = {"sort_pass0", "sort_pass1", "sort_pass2",
-                                              "sort_pass3", "sort_pass4", "sort_pass5",
-                                              "sort_pass6", "sort_pass7"};
-const char* kGroupPassNames[kMaxGroupPasses] = {"group_pass0", "group_pass1", "group_pass2",
-                                                "group_pass3"};
 
 }  // namespace
 
@@ -247,7 +253,7 @@ int nalar_policy_create(const nalar_policy_config* cfg, nalar_policy** out) {
   h->lds_limit = prop.sharedMemPerBlock;
   e = prepare_sweep_kernels(h->lds_limit);
   if (e != hipSuccess) return bail(e, "hipFuncSetAttribute");
-  e = hipHostMalloc(reinterpret_cast<void**>(&h->host_ctrl), sizeof(Ctrl), hipHostMallocDefault);
+  e = hipHostMalloc(reinterpret_cast<void**>(&h->host), sizeof(HostStatus), hipHostMallocCoherent);
   if (e != hipSuccess) return bail(e, "hipHostMalloc");
   for (int i = 0; i <= kMaxTimed; ++i) {
     e = hipEventCreate(&h->ev[i]);
@@ -268,7 +274,7 @@ void nalar_policy_destroy(nalar_policy* h) {
   (void)hipSetDevice(h->device);
   (void)hipStreamSynchronize(h->stream);
   if (h->ar.base) (void)hipFree(h->ar.base);
-  if (h->host_ctrl) (void)hipHostFree(h->host_ctrl);
+  if (h->host) (void)hipHostFree(h->host);
   for (int i = 0; i <= kMaxTimed; ++i)
     if (h->ev[i]) (void)hipEventDestroy(h->ev[i]);
   delete h;
@@ -309,6 +315,9 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   if (rc != NALAR_OK) return rc;
   Arena& A = h->ar;
   hipStream_t s = h->stream;
+  const int cur = int(h->passes & 1);
+  const int nxt = cur ^ 1;
+  Ctrl* ctrl = A.ctrl[cur];
 
   h->epoch = (h->epoch + 1) & kEpochMask;
   if (h->epoch == 0) {  // tags wrapped: forget every old look-back word
@@ -317,6 +326,11 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     h->epoch = 1;
   }
   const uint32_t epoch = h->epoch;
+  // This pass uses block `cur` (reset first if an earlier pass left it stale)
+  // and its sort kernel resets block `nxt`; until that has run, both are stale.
+  const bool need_reset = h->ctrl_dirty[cur];
+  h->ctrl_dirty[cur] = true;
+  h->ctrl_dirty[nxt] = true;
 
   ProblemDev pd{N, p->n_edges, W, M, p->now_us, p->migration_cost_us,
                 p->wf, p->type, p->est_us, p->done, p->loc, p->dep_off, p->dep_idx,
@@ -324,122 +338,113 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   const bool contiguous = (p->flags & NALAR_WF_CONTIGUOUS) != 0 || W <= 1;
 
   Timer tm{h};
-#define NALAR_LAUNCH(name, call)                  \
-  do {                                            \
-    tm.mark(name);                                \
-    hipError_t le_ = (call);                      \
-    if (le_ != hipSuccess) return hip_fail(h, le_, name); \
+#define NALAR_LAUNCH(name, call)                            \
+  do {                                                      \
+    tm.mark(name);                                          \
+    hipError_t le_ = (call);                                \
+    if (le_ != hipSuccess) return hip_fail(h, le_, name);   \
   } while (0)
 
-  NALAR_LAUNCH("setup", launch_setup(s, pd, A.ctrl, A.itab, A.ghist_slack, A.ghist_group));
-  NALAR_LAUNCH("nodes", launch_nodes(s, pd, A.ctrl, A.wf_off, contiguous ? 1 : 0));
+  if (need_reset) NALAR_LAUNCH("reset", launch_reset(s, ctrl));
+  NALAR_LAUNCH("nodes", launch_nodes(s, pd, ctrl, A.ctrl[nxt], A.itab, A.wf_off, contiguous ? 1 : 0));
 
   const int32_t* node_of_pos = nullptr;
   const int32_t* pos_of_node = nullptr;
   if (N > 0 && !contiguous) {
     int bits = 0;
     while ((int64_t(1) << bits) < W) ++bits;
-    const int gpass = (bits + kRadixBits - 1) / kRadixBits;
-    RadixDesc g{};
-    g.wf = p->wf;
-    g.key_buf[0] = A.gkey[0];
-    g.key_buf[1] = A.gkey[1];
-    g.pay_buf[0] = A.gpay[0];
-    g.pay_buf[1] = A.gpay[1];
-    g.count_dev = nullptr;
-    g.count_host = N;
-    g.first_span = N;
+    GroupArgs g{};
+    g.p = pd;
+    g.ctrl = ctrl;
+    g.npass = (bits + kRadixBits - 1) / kRadixBits;
+    for (int i = 0; i < 2; ++i) {
+      g.key[i] = A.gkey[i];
+      g.pay[i] = A.gpay[i];
+    }
     g.lookback = A.glb;
-    g.ghist = A.ghist_group;
     g.tiles_cap = tiles_of(A.capN);
-    g.npass_host = gpass;
-    g.ticket_base = 8;
-    NALAR_LAUNCH("group_hist", launch_radix_hist(s, g, A.ctrl, kSrcWf, N, false));
-    for (int ps = 0; ps < gpass; ++ps)
-      NALAR_LAUNCH(kGroupPassNames[ps],
-                   launch_radix_pass(s, g, A.ctrl, ps == 0 ? kSrcWf : kSrcBuffers, ps, epoch, N,
-                                     false));
-    const int fin = (gpass - 1) & 1;
-    NALAR_LAUNCH("group_finish", launch_group_finish(s, pd, A.ctrl, A.gkey[fin], A.gpay[fin],
-                                                     A.pos_of_node, A.wf_off));
-    node_of_pos = reinterpret_cast<const int32_t*>(A.gpay[fin]);
+    g.epoch = epoch;
+    g.pos_of_node = A.pos_of_node;
+    g.wf_off = A.wf_off;
+    e = launch_group(s, g, Timer::cb, &tm);
+    if (e != hipSuccess) return hip_fail(h, e, "group");
+    node_of_pos = reinterpret_cast<const int32_t*>(A.gpay[(g.npass - 1) & 1]);
     pos_of_node = A.pos_of_node;
   }
 
   if (N > 0) {
-    SweepArgs sa{};
-    sa.p = pd;
-    sa.itab = A.itab;
-    sa.wf_off = A.wf_off;
-    sa.node_of_pos = node_of_pos;
-    sa.pos_of_node = pos_of_node;
-    sa.rem_out = r->rem_us;
-    sa.stg_ready = A.stg_ready;
-    sa.stg_slack = A.stg_slack;
-    sa.stg_route = A.stg_route;
-    sa.stg_cost = A.stg_cost;
-    sa.g_cnt = A.g_cnt;
-    sa.g_mx = A.g_mx;
-    sa.g_dn = A.g_dn;
-    sa.g_nr = A.g_nr;
-    sa.g_front0 = A.g_front[0];
-    sa.g_front1 = A.g_front[1];
-    sa.ctrl = A.ctrl;
-    sa.force_global = (h->flags & NALAR_FORCE_GLOBAL_SWEEP) ? 1 : 0;
+    SweepArgs sw{};
+    sw.p = pd;
+    sw.itab = A.itab;
+    sw.wf_off = A.wf_off;
+    sw.node_of_pos = node_of_pos;
+    sw.pos_of_node = pos_of_node;
+    sw.rem_out = r->rem_us;
+    sw.stg_ready = A.stg_ready;
+    sw.stg_slack = A.stg_slack;
+    sw.stg_route = A.stg_route;
+    sw.stg_cost = A.stg_cost;
+    sw.g_cnt = A.g_cnt;
+    sw.g_mx = A.g_mx;
+    sw.g_dn = A.g_dn;
+    sw.g_nr = A.g_nr;
+    sw.g_front0 = A.g_front[0];
+    sw.g_front1 = A.g_front[1];
+    sw.ctrl = ctrl;
+    sw.force_global = (h->flags & NALAR_FORCE_GLOBAL_SWEEP) ? 1 : 0;
     const SweepShape sh = plan_sweep(N, W, M, h->cus, h->lds_limit);
-    NALAR_LAUNCH("sweep", launch_sweep(s, sa, sh));
-
-    RadixDesc d{};
-    d.stg_slack = A.stg_slack;
-    d.stg_ready = A.stg_ready;
-    d.key_buf[0] = A.skey[0];
-    d.key_buf[1] = A.skey[1];
-    d.pay_buf[0] = A.spay[0];
-    d.pay_buf[1] = A.spay[1];
-    d.count_dev = &A.ctrl->n_ready;
-    d.count_host = 0;
-    d.first_span = N;
-    d.lookback = A.slb;
-    d.ghist = A.ghist_slack;
-    d.tiles_cap = tiles_of(A.capN);
-    d.npass_host = -1;
-    d.ticket_base = 0;
-    NALAR_LAUNCH("sort_hist", launch_radix_hist(s, d, A.ctrl, kSrcStaged, N, true));
-    for (int ps = 0; ps < kMaxSortPasses; ++ps)
-      NALAR_LAUNCH(kSortPassNames[ps], launch_radix_pass(s, d, A.ctrl,
-                                                         ps == 0 ? kSrcStaged : kSrcBuffers, ps,
-                                                         epoch, N, true));
-    EmitArgs ea{};
-    ea.ctrl = A.ctrl;
-    ea.node_of_pos = node_of_pos;
-    ea.stg_route = A.stg_route;
-    ea.stg_cost = A.stg_cost;
-    ea.key_buf[0] = A.skey[0];
-    ea.key_buf[1] = A.skey[1];
-    ea.pay_buf[0] = A.spay[0];
-    ea.pay_buf[1] = A.spay[1];
-    ea.order = r->order;
-    ea.slack = r->slack_us;
-    ea.route = r->route;
-    ea.cost = r->cost_us;
-    NALAR_LAUNCH("emit", launch_emit(s, ea, N));
+    NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
   }
-#undef NALAR_LAUNCH
+
+  SortArgs sa{};
+  sa.ctrl = ctrl;
+  sa.next_ctrl = A.ctrl[nxt];
+  sa.host = h->host;
+  sa.stg_slack = A.stg_slack;
+  sa.stg_ready = A.stg_ready;
+  sa.stg_route = A.stg_route;
+  sa.stg_cost = A.stg_cost;
+  sa.node_of_pos = node_of_pos;
+  sa.span = N;
+  for (int i = 0; i < 2; ++i) {
+    sa.key[i] = A.skey[i];
+    sa.pay[i] = A.spay[i];
+  }
+  sa.lookback = A.slb;
+  sa.tiles_cap = tiles_of(A.capN);
+  sa.epoch = epoch;
+  sa.order = r->order;
+  sa.slack = r->slack_us;
+  sa.route = r->route;
+  sa.cost = r->cost_us;
+  __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);  // the kernels overwrite it
+  e = launch_slack_sort(s, sa, 0, kSortLaunched - 1, Timer::cb, &tm);
+  if (e != hipSuccess) return hip_fail(h, e, "sort");
   tm.end();
-  e = hipMemcpyAsync(h->host_ctrl, A.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, s);
-  if (e != hipSuccess) return hip_fail(h, e, "hipMemcpyAsync(status)");
   e = hipStreamSynchronize(s);
   if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
+  if (__atomic_load_n(&h->host->status, __ATOMIC_ACQUIRE) == kStatusContinue) {
+    __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);
+    e = launch_slack_sort(s, sa, kSortLaunched, kMaxSortPasses - 1, Timer::cb, &tm);
+    if (e != hipSuccess) return hip_fail(h, e, "sort");
+    tm.end();
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
+  }
+#undef NALAR_LAUNCH
+  h->passes += 1;
+  h->ctrl_dirty[nxt] = false;
   if (h->timing) {
     h->n_timed = tm.n;
     for (int i = 0; i < tm.n; ++i) (void)hipEventElapsedTime(&h->ms[i], h->ev[i], h->ev[i + 1]);
     h->timed_valid = true;
   }
-  const uint32_t st = h->host_ctrl->status;
+  const uint32_t st = __atomic_load_n(&h->host->status, __ATOMIC_ACQUIRE);
+  if (st == 0xFFFFFFFFu) return fail(h, NALAR_EDEVICE, "status was not written");
   if (st & kStInval) return fail(h, NALAR_EINVAL, "invalid problem data");
   if (st & kStCycle) return fail(h, NALAR_ECYCLE, "dependency cycle");
   if (st & kStRange) return fail(h, NALAR_ERANGE, "remaining critical path exceeds 2^62 us");
-  r->n_ready = N > 0 ? h->host_ctrl->n_ready : 0;
+  r->n_ready = __atomic_load_n(&h->host->n_ready, __ATOMIC_ACQUIRE);
   return NALAR_OK;
 }
 

@@ -33,10 +33,11 @@ __host__ __device__ inline uint64_t lb_pack(uint32_t epoch, uint64_t flag, uint6
   return (uint64_t(epoch & kEpochMask) << 40) | flag | (value & kLbValueMask);
 }
 
-// Per-pass control block in device memory.  Initialised by the setup kernel
-// at the start of every pass.  The sweep folds each workgroup's slack range and
-// ready count into one of kParts slots (spreading the atomics over many
-// addresses); the histogram kernel reduces the slots.
+// Per-pass control block in device memory.  Two of them alternate between
+// passes: the last kernel of a pass resets the block the next pass will use.
+// The sweep folds each workgroup's slack range and ready count into one of
+// kParts slots (spreading the atomics over many addresses); the sort reduces
+// the slots with one wave.
 constexpr int kParts = 64;
 
 struct Ctrl {
@@ -49,7 +50,41 @@ struct Ctrl {
   int64_t part_min[kParts];
   int64_t part_max[kParts];
   int64_t part_cnt[kParts];
+  uint32_t ghist_slack[kMaxSortPasses * kRadixBuckets];
+  uint32_t ghist_group[kMaxGroupPasses * kRadixBuckets];
 };
+
+// Slack-sort digit passes launched before the host looks at the status; a
+// wider slack range reports kStatusContinue and the host launches the rest.
+constexpr int kSortLaunched = 4;
+constexpr uint32_t kStatusContinue = 0x40000000u;
+
+// Written by the last kernel of a pass into pinned host memory.
+struct HostStatus {
+  uint32_t status;
+  uint32_t pad;
+  int64_t n_ready;
+};
+
+// Resets a control block for a later pass (run by one workgroup).
+__device__ inline void reset_ctrl(Ctrl* c) {
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    c->status = 0;
+    c->sort_npass = 0;
+    c->n_ready = 0;
+    c->slack_min = INT64_MAX;
+    c->slack_max = INT64_MIN;
+  }
+  for (int i = tid; i < 16; i += blockDim.x) c->tile_ticket[i] = 0;
+  for (int i = tid; i < kParts; i += blockDim.x) {
+    c->part_min[i] = INT64_MAX;
+    c->part_max[i] = INT64_MIN;
+    c->part_cnt[i] = 0;
+  }
+  for (int i = tid; i < kMaxSortPasses * kRadixBuckets; i += blockDim.x) c->ghist_slack[i] = 0;
+  for (int i = tid; i < kMaxGroupPasses * kRadixBuckets; i += blockDim.x) c->ghist_group[i] = 0;
+}
 
 // Instance table sorted by (type, original index), plus the sorted position of
 // every original index (for the instance that holds a future's state).
@@ -157,21 +192,34 @@ __device__ inline void flag_status(Ctrl* c, uint32_t bits) {
   __hip_atomic_fetch_or(&c->status, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Exclusive prefix over earlier tiles/workflows by decoupled look-back.  The
-// caller has already published its own aggregate.  Every earlier slot was
-// claimed (by ticket) before the caller's, by a block that publishes its
-// aggregate without waiting on anything, so the spin always ends.
+// Exclusive prefix over earlier tiles by decoupled look-back.  The caller has
+// already published its own aggregate.  Every earlier tile was claimed (by
+// ticket) before the caller's, by a workgroup that publishes its aggregate
+// without waiting on anything, so every spin ends.  The predecessors are read a
+// window of kLbWindow at a time (independent loads), so walking back over t
+// tiles costs about t / kLbWindow load round trips instead of t.
+constexpr int kLbWindow = 16;
+
 __device__ inline uint64_t lookback_exclusive(const uint64_t* words, int64_t slot, int64_t stride,
                                               uint32_t epoch) {
   uint64_t excl = 0;
   const uint64_t want = uint64_t(epoch & kEpochMask);
-  for (int64_t t = slot - 1; t >= 0; --t) {
-    uint64_t w;
-    do {
-      w = ld_relaxed_agent(words + t * stride);
-    } while ((w >> 40) != want || (w & (kLbAgg | kLbInc)) == 0);
-    excl += w & kLbValueMask;
-    if (w & kLbInc) break;
+  int64_t t = slot - 1;
+  while (t >= 0) {
+    uint64_t w[kLbWindow];
+#pragma unroll
+    for (int i = 0; i < kLbWindow; ++i) w[i] = (t - i >= 0) ? ld_relaxed_agent(words + (t - i) * stride) : 0;
+    bool found = false;
+#pragma unroll
+    for (int i = 0; i < kLbWindow; ++i) {
+      if (found || t - i < 0) continue;
+      while ((w[i] >> 40) != want || (w[i] & (kLbAgg | kLbInc)) == 0)
+        w[i] = ld_relaxed_agent(words + (t - i) * stride);
+      excl += w[i] & kLbValueMask;
+      found = (w[i] & kLbInc) != 0;
+    }
+    if (found) break;
+    t -= kLbWindow;
   }
   return excl;
 }

@@ -25,29 +25,43 @@ struct ProblemDev {
   const int32_t* inst_speed;
 };
 
-// Radix-sort plumbing shared by the slack sort and the workflow grouping.
 enum RadixSource : int {
-  kSrcBuffers = 0,  // keys/payloads from the ping-pong buffers (passes >= 1)
-  kSrcStaged = 1,   // ready futures staged by position: key = slack - min slack,
-                    // payload = position; non-ready positions are skipped, so the
-                    // first pass also compacts (slack sort, pass 0)
-  kSrcWf = 2,       // key = workflow id, payload = node id (grouping, pass 0)
+  kSrcStaged = 1,   // ready futures staged by position (slack sort)
+  kSrcWf = 2,       // workflow ids (grouping)
 };
 
-struct RadixDesc {
-  const int64_t* stg_slack; // kSrcStaged source
-  const uint8_t* stg_ready; // kSrcStaged validity
-  const int32_t* wf;        // kSrcWf source
-  void* key_buf[2];         // ping-pong keys (uint64 or uint32)
-  uint32_t* pay_buf[2];     // ping-pong payloads
-  const int64_t* count_dev; // dense element count in device memory, or NULL
-  int64_t count_host;       // dense element count when count_dev is NULL
-  int64_t first_span;       // positions scanned by the histogram and pass 0
-  uint64_t* lookback;       // [passes][tiles_cap][256]
-  uint32_t* ghist;          // [passes][256]
+struct SortArgs {
+  Ctrl* ctrl;
+  Ctrl* next_ctrl;              // reset here for the following pass
+  HostStatus* host;             // pinned: status and ready count for the host
+  const int64_t* stg_slack;     // [N] by position
+  const uint8_t* stg_ready;
+  const int32_t* stg_route;
+  const int64_t* stg_cost;
+  const int32_t* node_of_pos;   // NULL: position == node id
+  int64_t span;                 // N
+  uint64_t* key[2];             // ping-pong buffers
+  uint32_t* pay[2];
+  uint64_t* lookback;           // [passes][tiles_cap][256]
   int64_t tiles_cap;
-  int npass_host;           // -1: the histogram kernel decides (slack sort)
-  int ticket_base;          // first Ctrl::tile_ticket slot of this sort
+  uint32_t epoch;
+  int32_t* order;
+  int64_t* slack;
+  int32_t* route;
+  int64_t* cost;
+};
+
+struct GroupArgs {
+  ProblemDev p;
+  Ctrl* ctrl;
+  int npass;                    // digit passes over the workflow ids
+  uint32_t* key[2];
+  uint32_t* pay[2];
+  uint64_t* lookback;
+  int64_t tiles_cap;
+  uint32_t epoch;
+  int32_t* pos_of_node;
+  int32_t* wf_off;
 };
 
 struct SweepArgs {
@@ -71,33 +85,16 @@ struct SweepArgs {
   int force_global;
 };
 
-struct EmitArgs {
-  Ctrl* ctrl;
-  const int32_t* node_of_pos;   // NULL: position == node id
-  const int32_t* stg_route;
-  const int64_t* stg_cost;
-  const uint64_t* key_buf[2];
-  const uint32_t* pay_buf[2];
-  int32_t* order;
-  int64_t* slack;
-  int32_t* route;
-  int64_t* cost;
-};
-
 // ingest.hip
-hipError_t launch_setup(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, ITab itab,
-                        uint32_t* ghist_slack, uint32_t* ghist_group);
-hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, int32_t* wf_off,
-                        int contiguous);
-hipError_t launch_group_finish(hipStream_t s, const ProblemDev& p, Ctrl* ctrl,
-                               const uint32_t* sorted_wf, const uint32_t* sorted_ids,
-                               int32_t* pos_of_node, int32_t* wf_off);
+hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
+                        int32_t* wf_off, int contiguous);
 
-// sort.hip
-hipError_t launch_radix_hist(hipStream_t s, const RadixDesc& d, Ctrl* ctrl, int src,
-                             int64_t max_count, bool key64);
-hipError_t launch_radix_pass(hipStream_t s, const RadixDesc& d, Ctrl* ctrl, int src, int pass,
-                             uint32_t epoch, int64_t max_count, bool key64);
+// sort.hip (mark(ctx, name) is called before each launch, for timing)
+hipError_t launch_reset(hipStream_t s, Ctrl* c);
+hipError_t launch_slack_sort(hipStream_t s, const SortArgs& a, int first_pass, int last_pass,
+                             void (*mark)(void*, const char*), void* ctx);
+hipError_t launch_group(hipStream_t s, const GroupArgs& a, void (*mark)(void*, const char*),
+                        void* ctx);
 
 // sweep.hip
 struct SweepShape {
@@ -110,8 +107,5 @@ struct SweepShape {
 SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t lds_limit);
 hipError_t prepare_sweep_kernels(size_t lds_limit);
 hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const SweepShape& shape);
-
-// emit.hip
-hipError_t launch_emit(hipStream_t s, const EmitArgs& a, int64_t max_count);
 
 }  // namespace nalar

@@ -1,16 +1,21 @@
-// Stable LSD radix sort of (key, payload) pairs with one launch per 8-bit
-// digit ("onesweep": a single upfront histogram of every digit, then each digit
-// pass ranks its tile in LDS and finds its global offsets by decoupled
-// look-back over earlier tiles, so no separate scan kernel is needed).
+// Stable LSD radix sort of (key, payload) pairs.  Each 8-bit digit pass is one
+// launch that ranks tiles of 4096 items in LDS and finds their global offsets
+// by decoupled look-back over earlier tiles ("onesweep": one upfront histogram
+// of every digit instead of a scan per pass).  Passes beyond what the key
+// range needs return at once; for the slack sort only kSortLaunched passes
+// (32-bit key ranges, the usual case) are launched up front.
 //
-// Used twice per pass:
-//  * the slack sort: key = slack - min slack (range-reduced, so only the digits
-//    the key range needs are sorted), payload = position of the ready future;
-//    its first pass reads the futures staged by position and skips the
-//    positions that are not ready, so it also compacts them, and the stable
-//    passes keep (wf, id) order among equal slacks;
+// Two sorts use it:
+//  * the slack sort (set_priority, Table 2): key = slack - min slack, payload =
+//    position of the ready future.  Its first pass reads the futures staged by
+//    position and skips positions that are not ready, so it also compacts them;
+//    the passes are stable, so equal slacks keep (wf, id) order, which makes the
+//    order exactly ascending (slack, wf, id).  Its last pass gathers each
+//    ready future's id, slack, route and cost straight into the caller's
+//    arrays;
 //  * grouping futures by workflow when the caller's ids are not grouped:
-//    key = wf, payload = id.
+//    key = wf, payload = id; it ends by recording each node's position and
+//    each workflow's first position.
 //
 // Tile layout: 256 threads (4 waves), 16 items per thread, wave w owning a
 // contiguous run of 1024 items with item j of lane l at offset j*64 + l, so
@@ -24,86 +29,35 @@ namespace {
 constexpr int kWavesPerTile = kSortThreads / kWave;
 
 template <typename K>
-__device__ inline K first_key(const RadixDesc& d, int src, int64_t i, int64_t slack_min) {
-  if (src == kSrcStaged) return K(uint64_t(d.stg_slack[i] - slack_min));
-  return K(uint32_t(d.wf[i]));
-}
-
-__device__ inline bool first_valid(const RadixDesc& d, int src, int64_t i) {
-  return i < d.first_span && (src != kSrcStaged || d.stg_ready[i] != 0);
-}
-
-// Slack range and ready count of the staged futures, from the sweep's slots.
-struct StagedRange {
-  int64_t smin, smax, count;
+struct TileSmem {
+  uint32_t whist[kWavesPerTile][kRadixBuckets];
+  uint32_t tprefix[kRadixBuckets];
+  uint64_t gstart[kRadixBuckets];
+  uint32_t tmp[kWavesPerTile];
+  uint32_t intile;
+  uint32_t tile;
+  K key[kSortTile];
+  uint32_t pay[kSortTile];
 };
 
-__device__ inline StagedRange reduce_parts(const Ctrl* ctrl) {
-  StagedRange r{INT64_MAX, INT64_MIN, 0};
-  for (int i = 0; i < kParts; ++i) {
-    const int64_t a = ctrl->part_min[i], b = ctrl->part_max[i];
-    r.smin = a < r.smin ? a : r.smin;
-    r.smax = b > r.smax ? b : r.smax;
-    r.count += ctrl->part_cnt[i];
-  }
-  return r;
+// Where the first pass reads its items.
+struct FirstSource {
+  int mode;                 // kSrcStaged or kSrcWf
+  const int64_t* stg_slack;
+  const uint8_t* stg_ready;
+  const int32_t* wf;
+  int64_t span;             // positions scanned
+  int64_t smin;             // staged: key = slack - smin
+};
+
+__device__ inline bool first_valid(const FirstSource& f, int64_t i) {
+  return i < f.span && (f.mode != kSrcStaged || f.stg_ready[i] != 0);
 }
 
-// Digit histograms of all passes the key range needs.  For the slack sort this
-// kernel also settles the ready count, the slack range and the pass count
-// (at least one pass when anything is ready: the first pass compacts).
 template <typename K>
-__global__ __launch_bounds__(kSortThreads) void k_radix_hist(RadixDesc d, Ctrl* ctrl, int src) {
-  if (ctrl->status) return;
-  int npass;
-  int64_t smin = 0;
-  if (d.npass_host < 0) {
-    const StagedRange r = reduce_parts(ctrl);
-    smin = r.smin;
-    int nbits = 0;
-    if (r.count > 0) {
-      const uint64_t range = uint64_t(r.smax - r.smin);
-      nbits = range ? 64 - __builtin_clzll(range) : 0;
-    }
-    npass = r.count > 0 ? (nbits + kRadixBits - 1) / kRadixBits : 0;
-    if (r.count > 0 && npass == 0) npass = 1;
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-      ctrl->slack_min = r.smin;
-      ctrl->slack_max = r.smax;
-      ctrl->n_ready = r.count;
-      ctrl->sort_npass = uint32_t(npass);
-    }
-  } else {
-    npass = d.npass_host;
-  }
-  if (npass == 0) return;
-  __shared__ uint32_t h[kMaxSortPasses][kRadixBuckets];
-  for (int i = threadIdx.x; i < kMaxSortPasses * kRadixBuckets; i += kSortThreads)
-    (&h[0][0])[i] = 0;
-  __syncthreads();
-  const int64_t span = d.first_span;
-  const int64_t stride = int64_t(gridDim.x) * kSortThreads;
-  for (int64_t base = int64_t(blockIdx.x) * kSortThreads; base < span; base += stride) {
-    const int64_t i = base + threadIdx.x;
-    const bool valid = first_valid(d, src, i);
-    const K key = valid ? first_key<K>(d, src, i, smin) : K(0);
-    for (int ps = 0; ps < npass; ++ps) {
-      const uint32_t dg = uint32_t(key >> (ps * kRadixBits)) & (kRadixBuckets - 1);
-      // most high digits are shared by the whole wave: one add instead of 64
-      const uint64_t act = ballot(valid);
-      const int first = readlane_i32(int(dg), act ? __builtin_ctzll(act) : 0);
-      const uint64_t same = ballot(valid && int(dg) == first);
-      if (same == act) {
-        if (act && lane_id() == __builtin_ctzll(act)) atomicAdd(&h[ps][dg], uint32_t(__popcll(act)));
-      } else if (valid) {
-        atomicAdd(&h[ps][dg], 1u);
-      }
-    }
-  }
-  __syncthreads();
-  for (int ps = 0; ps < npass; ++ps)
-    for (int b = threadIdx.x; b < kRadixBuckets; b += kSortThreads)
-      if (h[ps][b]) atomicAdd(&d.ghist[ps * kRadixBuckets + b], h[ps][b]);
+__device__ inline K first_key(const FirstSource& f, int64_t i) {
+  if (f.mode == kSrcStaged) return K(uint64_t(f.stg_slack[i] - f.smin));
+  return K(uint32_t(f.wf[i]));
 }
 
 // Exclusive scan of one value per thread over the 256-thread block.
@@ -118,42 +72,63 @@ __device__ inline uint32_t block_excl_scan(uint32_t x, uint32_t* s_tmp) {
   return off + inc - x;
 }
 
+// Digit histograms (all npass digits) of the first pass's items, added into
+// ghist.  H is a workgroup-private [kMaxSortPasses][256] array.
 template <typename K>
-__global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixDesc d, Ctrl* ctrl, int src,
-                                                             int pass, uint32_t epoch) {
-  if (ctrl->status) return;
-  const int npass = d.npass_host >= 0 ? d.npass_host : int(ctrl->sort_npass);
-  if (pass >= npass) return;
-  const bool first = pass == 0 && src != kSrcBuffers;
-  const int64_t R = d.count_dev ? *d.count_dev : d.count_host;   // dense count
-  const int64_t span = first ? d.first_span : R;                  // items scanned
-  const int64_t ntiles = (span + kSortTile - 1) / kSortTile;
-
-  __shared__ uint32_t s_tile;
-  __shared__ uint32_t s_whist[kWavesPerTile][kRadixBuckets];
-  __shared__ uint32_t s_tprefix[kRadixBuckets];
-  __shared__ uint64_t s_gstart[kRadixBuckets];
-  __shared__ uint32_t s_tmp[kWavesPerTile];
-  __shared__ uint32_t s_intile;
-  __shared__ K s_key[kSortTile];
-  __shared__ uint32_t s_pay[kSortTile];
-
-  const int tid = threadIdx.x;
-  if (tid == 0) s_tile = atomicAdd(&ctrl->tile_ticket[d.ticket_base + pass], 1u);
-  for (int i = tid; i < kWavesPerTile * kRadixBuckets; i += kSortThreads) (&s_whist[0][0])[i] = 0;
+__device__ void histogram(const FirstSource& f, int npass, uint32_t (*H)[kRadixBuckets],
+                          uint32_t* ghist) {
+  for (int i = threadIdx.x; i < kMaxSortPasses * kRadixBuckets; i += kSortThreads) (&H[0][0])[i] = 0;
   __syncthreads();
-  const int64_t tile = s_tile;
-  if (tile >= ntiles) return;
+  const int64_t stride = int64_t(gridDim.x) * kSortThreads;
+  for (int64_t base = int64_t(blockIdx.x) * kSortThreads; base < f.span; base += stride) {
+    const int64_t i = base + threadIdx.x;
+    const bool valid = first_valid(f, i);
+    const K key = valid ? first_key<K>(f, i) : K(0);
+    for (int ps = 0; ps < npass; ++ps) {
+      const uint32_t dg = uint32_t(key >> (ps * kRadixBits)) & (kRadixBuckets - 1);
+      // most high digits are shared by the whole wave: one add instead of 64
+      const uint64_t act = ballot(valid);
+      const int first = readlane_i32(int(dg), act ? __builtin_ctzll(act) : 0);
+      const uint64_t same = ballot(valid && int(dg) == first);
+      if (same == act) {
+        if (act && lane_id() == __builtin_ctzll(act)) atomicAdd(&H[ps][dg], uint32_t(__popcll(act)));
+      } else if (valid) {
+        atomicAdd(&H[ps][dg], 1u);
+      }
+    }
+  }
+  __syncthreads();
+  for (int ps = 0; ps < npass; ++ps)
+    for (int b = threadIdx.x; b < kRadixBuckets; b += kSortThreads)
+      if (H[ps][b]) atomicAdd(&ghist[ps * kRadixBuckets + b], H[ps][b]);
+}
 
+// One tile of one digit pass.  Every thread of the workgroup calls it.
+// Where the last pass of the slack sort writes: the caller's arrays.
+struct FinalOut {
+  bool on;
+  const int32_t* node_of_pos;   // NULL: position == node id
+  const int32_t* stg_route;
+  const int64_t* stg_cost;
+  int64_t smin;
+  int32_t* order;
+  int64_t* slack;
+  int32_t* route;
+  int64_t* cost;
+};
+
+template <typename K>
+__device__ void radix_tile(TileSmem<K>& S, const FirstSource& f, bool first, int pass, int64_t tile,
+                           int64_t span, int64_t R, const K* kin, const uint32_t* pin, K* kout,
+                           uint32_t* pout, const uint32_t* ghist_row, uint64_t* lb_pass,
+                           uint32_t epoch, const FinalOut& fo) {
+  const int tid = threadIdx.x;
   const int wv = tid / kWave;
   const int ln = lane_id();
   const int shift = pass * kRadixBits;
+  for (int i = tid; i < kWavesPerTile * kRadixBuckets; i += kSortThreads) (&S.whist[0][0])[i] = 0;
+  __syncthreads();
   const int64_t seg = tile * kSortTile + int64_t(wv) * (kWave * kSortItems);
-  const int64_t smin = (src == kSrcStaged) ? ctrl->slack_min : 0;
-  const K* kin = static_cast<const K*>(d.key_buf[(pass + 1) & 1]);
-  const uint32_t* pin = d.pay_buf[(pass + 1) & 1];
-  K* kout = static_cast<K*>(d.key_buf[pass & 1]);
-  uint32_t* pout = d.pay_buf[pass & 1];
 
   K key[kSortItems];
   uint32_t pay[kSortItems];
@@ -165,8 +140,8 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixDesc d, Ctrl* 
     key[j] = K(0);
     pay[j] = 0;
     if (first) {
-      if (first_valid(d, src, i)) {
-        key[j] = first_key<K>(d, src, i, smin);
+      if (first_valid(f, i)) {
+        key[j] = first_key<K>(f, i);
         pay[j] = uint32_t(i);
         validm |= 1u << j;
       }
@@ -179,7 +154,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixDesc d, Ctrl* 
 
   // In-wave stable ranking: lanes with equal digits found by 8 ballots; the
   // per-wave running count of each digit lives in LDS.
-  uint32_t* wh = s_whist[wv];
+  uint32_t* wh = S.whist[wv];
 #pragma unroll
   for (int j = 0; j < kSortItems; ++j) {
     const bool valid = (validm >> j) & 1u;
@@ -204,23 +179,22 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixDesc d, Ctrl* 
   uint32_t tot = 0;
 #pragma unroll
   for (int w = 0; w < kWavesPerTile; ++w) {
-    const uint32_t c = s_whist[w][dg];
-    s_whist[w][dg] = tot;
+    const uint32_t c = S.whist[w][dg];
+    S.whist[w][dg] = tot;
     tot += c;
   }
-  uint64_t* lb = d.lookback + (int64_t(pass) * d.tiles_cap) * kRadixBuckets + dg;
+  uint64_t* lb = lb_pass + dg;
   st_relaxed_agent(lb + tile * kRadixBuckets, lb_pack(epoch, tile == 0 ? kLbInc : kLbAgg, tot));
-  const uint32_t gh = d.ghist[pass * kRadixBuckets + dg];
-  const uint32_t gexcl = block_excl_scan(gh, s_tmp);
-  const uint32_t texcl = block_excl_scan(tot, s_tmp);
+  const uint32_t gexcl = block_excl_scan(ghist_row[dg], S.tmp);
+  const uint32_t texcl = block_excl_scan(tot, S.tmp);
   uint64_t excl = 0;
   if (tile > 0) {
     excl = lookback_exclusive(lb, tile, kRadixBuckets, epoch);
     st_relaxed_agent(lb + tile * kRadixBuckets, lb_pack(epoch, kLbInc, excl + tot));
   }
-  s_tprefix[dg] = texcl;
-  s_gstart[dg] = uint64_t(gexcl) + excl;
-  if (dg == kRadixBuckets - 1) s_intile = texcl + tot;
+  S.tprefix[dg] = texcl;
+  S.gstart[dg] = uint64_t(gexcl) + excl;
+  if (dg == kRadixBuckets - 1) S.intile = texcl + tot;
   __syncthreads();
 
   // Stage the tile in digit order in LDS, then write runs of equal digits to
@@ -229,54 +203,215 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixDesc d, Ctrl* 
   for (int j = 0; j < kSortItems; ++j) {
     if ((validm >> j) & 1u) {
       const uint32_t dgt = uint32_t(key[j] >> shift) & (kRadixBuckets - 1);
-      const uint32_t pos = s_tprefix[dgt] + s_whist[wv][dgt] + rank[j];
-      s_key[pos] = key[j];
-      s_pay[pos] = pay[j];
+      const uint32_t pos = S.tprefix[dgt] + S.whist[wv][dgt] + rank[j];
+      S.key[pos] = key[j];
+      S.pay[pos] = pay[j];
     }
   }
   __syncthreads();
-  const int in_tile = int(s_intile);
+  const int in_tile = int(S.intile);
   for (int i = tid; i < in_tile; i += kSortThreads) {
-    const K k = s_key[i];
+    const K k = S.key[i];
     const uint32_t dgt = uint32_t(k >> shift) & (kRadixBuckets - 1);
-    const uint64_t g = s_gstart[dgt] + uint64_t(i - int(s_tprefix[dgt]));
-    if (g < uint64_t(R)) {
+    const uint64_t g = S.gstart[dgt] + uint64_t(i - int(S.tprefix[dgt]));
+    if (g >= uint64_t(R)) continue;
+    if (fo.on) {  // last pass: gather the ready future's decision into place
+      const uint32_t pos = S.pay[i];
+      fo.order[g] = fo.node_of_pos ? fo.node_of_pos[pos] : int32_t(pos);
+      fo.slack[g] = int64_t(uint64_t(k) + uint64_t(fo.smin));
+      fo.route[g] = fo.stg_route[pos];
+      if (fo.cost) fo.cost[g] = fo.stg_cost[pos];
+    } else {
       kout[g] = k;
-      pout[g] = s_pay[i];
+      pout[g] = S.pay[i];
     }
   }
 }
 
-int hist_grid(int64_t n) {
-  int64_t b = (n + kSortTile - 1) / kSortTile;
+__global__ __launch_bounds__(kSortThreads) void k_reset(Ctrl* c) { reset_ctrl(c); }
+
+// Slack range, ready count and pass count from the sweep's slots (one wave).
+__device__ void settle_range(Ctrl* ctrl, int64_t* s_range, bool write) {
+  if (threadIdx.x < kWave) {
+    const int64_t mn = wave_min_i64(ctrl->part_min[threadIdx.x]);
+    const int64_t mx = wave_max_i64(ctrl->part_max[threadIdx.x]);
+    const int64_t ct = wave_sum_i64(ctrl->part_cnt[threadIdx.x]);
+    if (threadIdx.x == 0) {
+      int npass = 0;
+      if (ct > 0) {
+        const uint64_t range = uint64_t(mx - mn);
+        const int nbits = range ? 64 - __builtin_clzll(range) : 0;
+        npass = (nbits + kRadixBits - 1) / kRadixBits;
+        if (npass == 0) npass = 1;  // the first pass also compacts
+      }
+      s_range[0] = mn;
+      s_range[1] = ct;
+      s_range[2] = npass;
+      if (write) {
+        ctrl->n_ready = ct;
+        ctrl->slack_min = mn;
+        ctrl->slack_max = mx;
+        ctrl->sort_npass = uint32_t(npass);
+      }
+    }
+  }
+  __syncthreads();
+}
+
+__device__ inline void publish_status(HostStatus* host, uint32_t status, int64_t n_ready) {
+  __hip_atomic_store(&host->n_ready, n_ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&host->status, status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+__global__ __launch_bounds__(kSortThreads) void k_slack_hist(SortArgs a) {
+  __shared__ uint32_t H[kMaxSortPasses][kRadixBuckets];
+  __shared__ int64_t s_range[3];
+  Ctrl* ctrl = a.ctrl;
+  const uint32_t status = ctrl->status;
+  if (status) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) publish_status(a.host, status, 0);
+    return;
+  }
+  settle_range(ctrl, s_range, blockIdx.x == 0);
+  const int npass = int(s_range[2]);
+  if (npass == 0) {  // nothing ready: no pass runs, so report here
+    if (blockIdx.x == 0 && threadIdx.x == 0) publish_status(a.host, 0, 0);
+    return;
+  }
+  const FirstSource f{kSrcStaged, a.stg_slack, a.stg_ready, nullptr, a.span, s_range[0]};
+  histogram<uint64_t>(f, npass, H, ctrl->ghist_slack);
+}
+
+// One digit pass of the slack sort.  The last pass the key range needs writes
+// the caller's arrays and the host status; pass kSortLaunched-1 of a wider range
+// asks the host for the remaining passes instead.
+__global__ __launch_bounds__(kSortThreads) void k_slack_pass(SortArgs a, int pass) {
+  __shared__ TileSmem<uint64_t> S;
+  Ctrl* ctrl = a.ctrl;
+  if (ctrl->status) return;
+  const int npass = int(ctrl->sort_npass);
+  if (pass >= npass) return;
+  const int64_t R = ctrl->n_ready;
+  const bool first = pass == 0;
+  const bool last = pass == npass - 1;
+  const int64_t span = first ? a.span : R;
+  const int64_t ntiles = (span + kSortTile - 1) / kSortTile;
+  if (threadIdx.x == 0) S.tile = atomicAdd(&ctrl->tile_ticket[pass], 1u);
+  __syncthreads();
+  const int64_t tile = S.tile;
+  if (tile >= ntiles) return;
+  const int64_t smin = ctrl->slack_min;
+  const FirstSource f{kSrcStaged, a.stg_slack, a.stg_ready, nullptr, a.span, smin};
+  const FinalOut fo{last, a.node_of_pos, a.stg_route, a.stg_cost, smin,
+                    a.order, a.slack, a.route, a.cost};
+  radix_tile<uint64_t>(S, f, first, pass, tile, span, R, a.key[(pass + 1) & 1],
+                       a.pay[(pass + 1) & 1], a.key[pass & 1], a.pay[pass & 1],
+                       ctrl->ghist_slack + pass * kRadixBuckets,
+                       a.lookback + int64_t(pass) * a.tiles_cap * kRadixBuckets, a.epoch, fo);
+  if (tile == 0 && threadIdx.x == 0) {
+    if (last) publish_status(a.host, 0, R);
+    else if (pass == kSortLaunched - 1) publish_status(a.host, kStatusContinue, R);
+  }
+}
+
+__global__ __launch_bounds__(kSortThreads) void k_group_hist(GroupArgs a) {
+  __shared__ uint32_t H[kMaxSortPasses][kRadixBuckets];
+  if (a.ctrl->status) return;
+  const FirstSource f{kSrcWf, nullptr, nullptr, a.p.wf, a.p.N, 0};
+  histogram<uint32_t>(f, a.npass, H, a.ctrl->ghist_group);
+}
+
+__global__ __launch_bounds__(kSortThreads) void k_group_pass(GroupArgs a, int pass) {
+  __shared__ TileSmem<uint32_t> S;
+  Ctrl* ctrl = a.ctrl;
+  if (ctrl->status) return;
+  const int64_t N = a.p.N;
+  const int64_t ntiles = (N + kSortTile - 1) / kSortTile;
+  if (threadIdx.x == 0) S.tile = atomicAdd(&ctrl->tile_ticket[8 + pass], 1u);
+  __syncthreads();
+  const int64_t tile = S.tile;
+  if (tile >= ntiles) return;
+  const FirstSource f{kSrcWf, nullptr, nullptr, a.p.wf, N, 0};
+  radix_tile<uint32_t>(S, f, pass == 0, pass, tile, N, N, a.key[(pass + 1) & 1],
+                       a.pay[(pass + 1) & 1], a.key[pass & 1], a.pay[pass & 1],
+                       ctrl->ghist_group + pass * kRadixBuckets,
+                       a.lookback + int64_t(pass) * a.tiles_cap * kRadixBuckets, a.epoch,
+                       FinalOut{false, nullptr, nullptr, nullptr, 0, nullptr, nullptr, nullptr, nullptr});
+}
+
+// Position of every node and first position of every workflow.
+__global__ __launch_bounds__(kSortThreads) void k_group_finish(GroupArgs a) {
+  if (a.ctrl->status) return;
+  const int64_t N = a.p.N, W = a.p.W;
+  const int fin = (a.npass - 1) & 1;
+  const uint32_t* sorted_wf = a.key[fin];
+  const uint32_t* sorted_id = a.pay[fin];
+  const int64_t stride = int64_t(gridDim.x) * kSortThreads;
+  const int64_t g0 = int64_t(blockIdx.x) * kSortThreads + threadIdx.x;
+  for (int64_t q = g0; q < N; q += stride) a.pos_of_node[sorted_id[q]] = int32_t(q);
+  for (int64_t w = g0; w <= W; w += stride) {
+    int64_t lo = 0, hi = N;
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) >> 1;
+      if (int64_t(sorted_wf[mid]) < w) lo = mid + 1; else hi = mid;
+    }
+    a.wf_off[w] = int32_t(lo);
+  }
+}
+
+unsigned grid_of(int64_t n, int64_t per, int64_t cap) {
+  int64_t b = (n + per - 1) / per;
   if (b < 1) b = 1;
-  if (b > 2048) b = 2048;
-  return int(b);
+  if (b > cap) b = cap;
+  return unsigned(b);
 }
 
 }  // namespace
 
-hipError_t launch_radix_hist(hipStream_t s, const RadixDesc& d, Ctrl* ctrl, int src,
-                             int64_t max_count, bool key64) {
-  if (key64)
-    hipLaunchKernelGGL(k_radix_hist<uint64_t>, dim3(hist_grid(max_count)), dim3(kSortThreads), 0,
-                       s, d, ctrl, src);
-  else
-    hipLaunchKernelGGL(k_radix_hist<uint32_t>, dim3(hist_grid(max_count)), dim3(kSortThreads), 0,
-                       s, d, ctrl, src);
+hipError_t launch_reset(hipStream_t s, Ctrl* c) {
+  hipLaunchKernelGGL(k_reset, dim3(1), dim3(kSortThreads), 0, s, c);
   return hipGetLastError();
 }
 
-hipError_t launch_radix_pass(hipStream_t s, const RadixDesc& d, Ctrl* ctrl, int src, int pass,
-                             uint32_t epoch, int64_t max_count, bool key64) {
-  int64_t tiles = (max_count + kSortTile - 1) / kSortTile;
-  if (tiles < 1) tiles = 1;
-  if (key64)
-    hipLaunchKernelGGL(k_radix_pass<uint64_t>, dim3(unsigned(tiles)), dim3(kSortThreads), 0, s, d,
-                       ctrl, src, pass, epoch);
-  else
-    hipLaunchKernelGGL(k_radix_pass<uint32_t>, dim3(unsigned(tiles)), dim3(kSortThreads), 0, s, d,
-                       ctrl, src, pass, epoch);
+hipError_t launch_slack_sort(hipStream_t s, const SortArgs& a, int first_pass, int last_pass,
+                             void (*mark)(void*, const char*), void* ctx) {
+  hipError_t e;
+  if (first_pass == 0) {
+    mark(ctx, "sort_hist");
+    hipLaunchKernelGGL(k_slack_hist, dim3(grid_of(a.span, 4 * kSortThreads, 2048)),
+                       dim3(kSortThreads), 0, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  static const char* names[kMaxSortPasses] = {"sort_pass0", "sort_pass1", "sort_pass2", "sort_pass3",
+                                              "sort_pass4", "sort_pass5", "sort_pass6", "sort_pass7"};
+  for (int ps = first_pass; ps <= last_pass; ++ps) {
+    mark(ctx, names[ps]);
+    hipLaunchKernelGGL(k_slack_pass, dim3(grid_of(a.span, kSortTile, INT32_MAX)), dim3(kSortThreads),
+                       0, s, a, ps);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_group(hipStream_t s, const GroupArgs& a, void (*mark)(void*, const char*),
+                        void* ctx) {
+  mark(ctx, "group_hist");
+  hipLaunchKernelGGL(k_group_hist, dim3(grid_of(a.p.N, 4 * kSortThreads, 2048)), dim3(kSortThreads), 0, s,
+                     a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  for (int ps = 0; ps < a.npass; ++ps) {
+    mark(ctx, "group_pass");
+    hipLaunchKernelGGL(k_group_pass, dim3(grid_of(a.p.N, kSortTile, INT32_MAX)), dim3(kSortThreads),
+                       0, s, a, ps);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  mark(ctx, "group_finish");
+  hipLaunchKernelGGL(k_group_finish, dim3(grid_of(a.p.N + a.p.W + 1, kSortThreads, 4096)),
+                     dim3(kSortThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -83,28 +83,34 @@ __device__ inline int32_t checked_dep(const Layout& L, int32_t p, int64_t b, int
 __device__ inline void agg_count_lds(int32_t* cnt, int lp) {
   const uint64_t act = ballot(lp >= 0);
   if (act == 0) return;
-  const int lead = __builtin_ctzll(act);
-  const int first = readlane_i32(lp, lead);
-  if (ballot(lp >= 0 && lp != first) == 0) {
-    if (lane_id() == lead) atomicAdd(&cnt[first], int(__popcll(act)));
-  } else if (lp >= 0) {
-    atomicAdd(&cnt[lp], 1);
+  if ((act & (act - 1)) != 0) {
+    const int lead = __builtin_ctzll(act);
+    const int first = readlane_i32(lp, lead);
+    if (ballot(lp >= 0 && lp != first) == 0) {  // the whole wave feeds one future
+      if (lane_id() == lead) atomicAdd(&cnt[first], int(__popcll(act)));
+      return;
+    }
   }
+  if (lp >= 0) atomicAdd(&cnt[lp], 1);
 }
 
 // Called with every lane of the wave active.
 __device__ inline void agg_push_lds(int64_t* mx, int32_t* cnt, int lp, int64_t r) {
   const uint64_t act = ballot(lp >= 0);
   if (act == 0) return;
-  const int lead = __builtin_ctzll(act);
-  const int first = readlane_i32(lp, lead);
-  if (ballot(lp >= 0 && lp != first) == 0) {
-    const int64_t m = wave_max_i64(lp >= 0 ? r : INT64_MIN);
-    if (lane_id() == lead) {
-      atomicMax(reinterpret_cast<long long*>(&mx[first]), (long long)m);
-      atomicSub(&cnt[first], int(__popcll(act)));
+  if ((act & (act - 1)) != 0) {
+    const int lead = __builtin_ctzll(act);
+    const int first = readlane_i32(lp, lead);
+    if (ballot(lp >= 0 && lp != first) == 0) {  // fan-in: reduce, then one atomic
+      const int64_t m = wave_max_i64(lp >= 0 ? r : INT64_MIN);
+      if (lane_id() == lead) {
+        atomicMax(reinterpret_cast<long long*>(&mx[first]), (long long)m);
+        atomicSub(&cnt[first], int(__popcll(act)));
+      }
+      return;
     }
-  } else if (lp >= 0) {
+  }
+  if (lp >= 0) {
     atomicMax(reinterpret_cast<long long*>(&mx[lp]), (long long)r);
     atomicSub(&cnt[lp], 1);
   }
@@ -115,13 +121,15 @@ __device__ inline void agg_push_lds(int64_t* mx, int32_t* cnt, int lp, int64_t r
 __device__ inline void agg_count_hbm(int32_t* cnt, int lp) {
   const uint64_t act = ballot(lp >= 0);
   if (act == 0) return;
-  const int lead = __builtin_ctzll(act);
-  const int first = readlane_i32(lp, lead);
-  if (ballot(lp >= 0 && lp != first) == 0) {
-    if (lane_id() == lead) add_wg(&cnt[first], int32_t(__popcll(act)));
-  } else if (lp >= 0) {
-    add_wg(&cnt[lp], int32_t(1));
+  if ((act & (act - 1)) != 0) {
+    const int lead = __builtin_ctzll(act);
+    const int first = readlane_i32(lp, lead);
+    if (ballot(lp >= 0 && lp != first) == 0) {
+      if (lane_id() == lead) add_wg(&cnt[first], int32_t(__popcll(act)));
+      return;
+    }
   }
+  if (lp >= 0) add_wg(&cnt[lp], int32_t(1));
 }
 
 __device__ inline void append_wave(bool in, int32_t val, int32_t* list, int* s_count) {
@@ -144,7 +152,7 @@ __device__ inline void agg_push_hbm(int64_t* mx, int32_t* cnt, int lp, int64_t r
   if (act != 0) {
     const int lead = __builtin_ctzll(act);
     const int first = readlane_i32(lp, lead);
-    if (ballot(lp >= 0 && lp != first) == 0) {
+    if ((act & (act - 1)) != 0 && ballot(lp >= 0 && lp != first) == 0) {
       const int64_t m = wave_max_i64(lp >= 0 ? r : INT64_MIN);
       if (lane_id() == lead) {
         max_wg(&mx[first], m);
@@ -194,13 +202,13 @@ struct Acc {
   int64_t tready = 0;
 };
 
-__device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_t pos, int32_t v,
-                                   int64_t rem, int64_t est, int64_t dl, Acc& acc) {
+__device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_t pos, int32_t type,
+                                   int32_t loc, int64_t rem, int64_t est, int64_t dl, Acc& acc) {
   const int64_t slack = dl - rem;
   int32_t route;
   int64_t cost;
-  route_future(a.p.type[v], est, a.p.loc[v], int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load,
-               it.speed, it.inv, it.pos, route, cost);
+  route_future(type, est, loc, int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load, it.speed,
+               it.inv, it.pos, route, cost);
   a.stg_slack[pos] = slack;
   a.stg_route[pos] = route;
   a.stg_cost[pos] = cost;
@@ -224,26 +232,34 @@ __device__ inline int dep_at(uint32_t p01, uint32_t p2, int q) {
 
 template <int T, int NPT>
 __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
-                          int64_t* mx, int32_t* cnt, uint8_t* dn, uint8_t* nr, int w, int64_t b,
+                          int64_t* mx, int32_t* cnt, uint8_t* dn, uint8_t* nr, int lds_cap, int64_t b,
                           int n, int64_t dl, Acc& acc) {
   const int tid = threadIdx.x;
   Ctrl* ctrl = a.ctrl;
 
   int32_t vv[NPT];
   int64_t ee[NPT];
+  int32_t off[NPT], deg[NPT], ty[NPT], lc[NPT];
   uint32_t p01[NPT], p2[NPT];
-  uint32_t fin = 0, ready = 0;
+  uint32_t own = 0, fin = 0, ready = 0;
 
-  // A: load owned futures, reset their counters
+  // A: everything the workflow needs from HBM about its own futures, in one
+  // round trip; reset their counters
 #pragma unroll
   for (int j = 0; j < NPT; ++j) {
     const int k = j * T + tid;
-    vv[j] = 0; ee[j] = 0; p01[j] = 0xFFFFFFFFu; p2[j] = kNoDep;
+    vv[j] = 0; ee[j] = 0; off[j] = 0; deg[j] = 0; ty[j] = 0; lc[j] = -1;
+    p01[j] = 0xFFFFFFFFu; p2[j] = kNoDep;
     if (k < n) {
+      own |= 1u << j;
       const int32_t v = node_at(L, b + k);
       const uint8_t d = a.p.done[v];
       vv[j] = v;
       ee[j] = d ? 0 : a.p.est[v];
+      off[j] = a.p.dep_off[v];
+      deg[j] = a.p.dep_off[v + 1] - off[j];
+      ty[j] = a.p.type[v];
+      lc[j] = a.p.loc[v];
       cnt[k] = 0;
       mx[k] = 0;
       dn[k] = d;
@@ -256,23 +272,19 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
   // B: out-degree counters and readiness (one pass over the dependencies)
 #pragma unroll
   for (int j = 0; j < NPT; ++j) {
+    if (ballot((own >> j) & 1u) == 0) continue;   // wave-uniform: no future in this slot
     const int k = j * T + tid;
-    const bool own = k < n;
-    int32_t off = 0, deg = 0;
-    if (own) {
-      off = a.p.dep_off[vv[j]];
-      deg = a.p.dep_off[vv[j] + 1] - off;
-    }
-    const bool light = own && deg <= kPmax;
-    if (own && !light) {
+    const bool mine = (own >> j) & 1u;
+    const bool light = mine && deg[j] <= kPmax;
+    if (mine && !light) {
       p2[j] = kHeavyBit | kNoDep;
       const int slot = atomicAdd(&S.hcount, 1);
       if (slot < kHeavyCap) {
-        S.hk[slot] = k; S.ho[slot] = off; S.hd[slot] = deg;
+        S.hk[slot] = k; S.ho[slot] = off[j]; S.hd[slot] = deg[j];
       } else {
         bool blocked = false;
-        for (int e = 0; e < deg; ++e) {
-          const int32_t lp = checked_dep(L, a.p.dep_idx[off + e], b, n, k, ctrl);
+        for (int e = 0; e < deg[j]; ++e) {
+          const int32_t lp = checked_dep(L, a.p.dep_idx[off[j] + e], b, n, k, ctrl);
           if (lp >= 0) { atomicAdd(&cnt[lp], 1); blocked |= dn[lp] == 0; }
         }
         if (blocked) nr[k] = 1;
@@ -283,27 +295,29 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
 #pragma unroll
     for (int q = 0; q < kPmax; ++q) {
       int32_t lp = -1;
-      if (light && q < deg) lp = checked_dep(L, a.p.dep_idx[off + q], b, n, k, ctrl);
+      if (light && q < deg[j]) lp = checked_dep(L, a.p.dep_idx[off[j] + q], b, n, k, ctrl);
       packed[q] = lp >= 0 ? uint32_t(lp) : kNoDep;
       agg_count_lds(cnt, lp);
       if (lp >= 0 && dn[lp] == 0) blocked = true;
     }
     if (light) {
       p01[j] = packed[0] | (packed[1] << 16);
-      p2[j] = packed[2] | (uint32_t(deg) << 16);
+      p2[j] = packed[2] | (uint32_t(deg[j]) << 16);
       if (blocked) nr[k] = 1;
     }
   }
   __syncthreads();
+  const int hc0 = S.hcount;          // futures with many dependencies, if any
+  const bool any_heavy = hc0 > 0;
   {
-    const int hc = S.hcount < kHeavyCap ? S.hcount : kHeavyCap;
+    const int hc = hc0 < kHeavyCap ? hc0 : kHeavyCap;
     for (int h = 0; h < hc; ++h) {
-      const int k = S.hk[h], off = S.ho[h], deg = S.hd[h];
+      const int k = S.hk[h], o = S.ho[h], dg = S.hd[h];
       bool blocked = false;
-      for (int e0 = 0; e0 < deg; e0 += T) {
+      for (int e0 = 0; e0 < dg; e0 += T) {
         const int e = e0 + tid;
         int32_t lp = -1;
-        if (e < deg) lp = checked_dep(L, a.p.dep_idx[off + e], b, n, k, ctrl);
+        if (e < dg) lp = checked_dep(L, a.p.dep_idx[o + e], b, n, k, ctrl);
         agg_count_lds(cnt, lp);
         if (lp >= 0 && dn[lp] == 0) blocked = true;
       }
@@ -315,8 +329,8 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
   // ready flags (staged by position for the sort's first pass)
 #pragma unroll
   for (int j = 0; j < NPT; ++j) {
-    const int k = j * T + tid;
-    if (k < n) {
+    if ((own >> j) & 1u) {
+      const int k = j * T + tid;
       const bool rd = dn[k] == 0 && nr[k] == 0;
       if (rd) ready |= 1u << j;
       a.stg_ready[b + k] = rd ? 1 : 0;
@@ -324,36 +338,36 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
   }
   if (tid == 0) S.hcount = 0;
 
-  // C: levels
+  // C: levels.  A future whose consumers are all finalised (cnt == 0) is
+  // finalised and pushes its rem to its dependencies.
   bool overflow = false;
   for (;;) {
+    int32_t cv[NPT];
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) cv[j] = (j * T + tid < lds_cap) ? cnt[j * T + tid] : 1;
     uint32_t cand = 0;
 #pragma unroll
-    for (int j = 0; j < NPT; ++j) {
-      const int k = j * T + tid;
-      if (k < n && !((fin >> j) & 1u) && cnt[k] == 0) cand |= 1u << j;
-    }
+    for (int j = 0; j < NPT; ++j)
+      if ((((own & ~fin) >> j) & 1u) && cv[j] == 0) cand |= 1u << j;
     if (!__syncthreads_or(cand != 0)) break;
 #pragma unroll
     for (int j = 0; j < NPT; ++j) {
       const bool c = (cand >> j) & 1u;
+      if (ballot(c) == 0) continue;               // wave-uniform
       const bool hv = (p2[j] & kHeavyBit) != 0;
       const int k = j * T + tid;
       int64_t r = 0;
       if (c) {
         r = clamp_rem(ee[j] + mx[k], overflow);
         mx[k] = r;
-        if (a.rem_out) a.rem_out[vv[j]] = r;
         fin |= 1u << j;
         if (hv) {
-          const int32_t off = a.p.dep_off[vv[j]];
-          const int32_t deg = a.p.dep_off[vv[j] + 1] - off;
           const int hs = atomicAdd(&S.hcount, 1);
           if (hs < kHeavyCap) {
-            S.hk[hs] = k; S.ho[hs] = off; S.hd[hs] = deg;
+            S.hk[hs] = k; S.ho[hs] = off[j]; S.hd[hs] = deg[j];
           } else {
-            for (int e = 0; e < deg; ++e) {
-              const int32_t lp = local_of(L, a.p.dep_idx[off + e], b, n);
+            for (int e = 0; e < deg[j]; ++e) {
+              const int32_t lp = local_of(L, a.p.dep_idx[off[j] + e], b, n);
               if (lp >= 0 && lp != k) {
                 atomicMax(reinterpret_cast<long long*>(&mx[lp]), (long long)r);
                 atomicSub(&cnt[lp], 1);
@@ -366,27 +380,34 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
 #pragma unroll
       for (int q = 0; q < kPmax; ++q) agg_push_lds(mx, cnt, lightc ? dep_at(p01[j], p2[j], q) : -1, r);
     }
-    __syncthreads();
-    const int hc = S.hcount < kHeavyCap ? S.hcount : kHeavyCap;
-    for (int h = 0; h < hc; ++h) {
-      const int k = S.hk[h], off = S.ho[h], deg = S.hd[h];
-      const int64_t r = mx[k];
-      for (int e0 = 0; e0 < deg; e0 += T) {
-        const int e = e0 + tid;
-        int32_t lp = -1;
-        if (e < deg) {
-          lp = local_of(L, a.p.dep_idx[off + e], b, n);
-          if (lp == k) lp = -1;
+    if (any_heavy) {
+      __syncthreads();
+      const int hc = S.hcount < kHeavyCap ? S.hcount : kHeavyCap;
+      for (int h = 0; h < hc; ++h) {
+        const int k = S.hk[h], o = S.ho[h], dg = S.hd[h];
+        const int64_t r = mx[k];
+        for (int e0 = 0; e0 < dg; e0 += T) {
+          const int e = e0 + tid;
+          int32_t lp = -1;
+          if (e < dg) {
+            lp = local_of(L, a.p.dep_idx[o + e], b, n);
+            if (lp == k) lp = -1;
+          }
+          agg_push_lds(mx, cnt, lp, r);
         }
-        agg_push_lds(mx, cnt, lp, r);
       }
+      __syncthreads();
+      if (tid == 0) S.hcount = 0;
     }
-    __syncthreads();
-    if (tid == 0) S.hcount = 0;
     __syncthreads();
   }
   if (overflow) flag_status(ctrl, kStRange);
   if (fin) atomicAdd(&S.proc, __popc(fin));
+  if (a.rem_out) {  // rem stayed in LDS during the levels; store it once
+#pragma unroll
+    for (int j = 0; j < NPT; ++j)
+      if ((fin >> j) & 1u) a.rem_out[vv[j]] = mx[j * T + tid];
+  }
   __syncthreads();
   if (tid == 0 && S.proc != n) flag_status(ctrl, kStCycle);
 
@@ -395,7 +416,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
   for (int j = 0; j < NPT; ++j) {
     if ((ready >> j) & 1u) {
       const int k = j * T + tid;
-      write_ready(a, it, b + k, vv[j], mx[k], ee[j], dl, acc);
+      write_ready(a, it, b + k, ty[j], lc[j], mx[k], ee[j], dl, acc);
     }
   }
   __syncthreads();
@@ -563,10 +584,242 @@ __device__ void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it
   for (int k = tid; k < n; k += T) {
     if (dn[k] == 0 && nr[k] == 0) {
       const int32_t v = node_at(L, b + k);
-      write_ready(a, it, b + k, v, ld_wg(&mx[k]), a.p.est[v], dl, acc);
+      write_ready(a, it, b + k, a.p.type[v], a.p.loc[v], ld_wg(&mx[k]), a.p.est[v], dl, acc);
     }
   }
   __syncthreads();
+}
+
+// ------------------------------------------------------------ wave workflow
+
+// One wave sweeps a workflow of at most 64 * NPTW futures on its own LDS slice.
+// The LDS operations of one wave complete in program order, so no barrier is
+// needed: each read observes every earlier write and atomic of the same wave.
+// wave_order() only keeps the compiler from moving LDS accesses across a phase
+// boundary; it emits no wait, so outstanding HBM stores never stall the wave.
+__device__ inline void wave_order() { __asm__ __volatile__("" ::: "memory"); }
+
+// LDS slice of one wave (cap futures).
+struct WaveSlice {
+  int64_t* mx;      // running max of the consumers' rem, then rem
+  int64_t* ee;      // est' (0 when done)
+  int32_t* cnt;     // consumers not yet finalised
+  uint32_t* pa;     // dependencies 0 and 1 (local, 16 bits each)
+  uint32_t* pb;     // dependency 2 | degree << 16 | heavy bit
+  uint8_t* dn;      // done
+  uint8_t* nr;      // some dependency not done
+  uint16_t* queue;  // futures whose consumers are all finalised, not yet taken
+};
+
+// Sweep of one workflow by one wave.  Instead of scanning for a level at a
+// time, the lane whose decrement brings a dependency's counter to zero goes on
+// with that dependency at once (further ones join a wave-shared queue), so a
+// chain of levels costs two LDS round trips per level.  Futures with many
+// dependencies are pushed by the whole wave.
+template <int NPTW>
+__device__ void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& it,
+                           const WaveSlice& W, int64_t b, int n, int64_t dl, Acc& acc) {
+  const int ln = lane_id();
+  Ctrl* ctrl = a.ctrl;
+  int32_t vv[NPTW], ty[NPTW], lc[NPTW];
+  uint32_t own = 0, ready = 0;
+
+  // A: attributes in one round trip; reset the state
+  int32_t off[NPTW], deg[NPTW];
+#pragma unroll
+  for (int j = 0; j < NPTW; ++j) {
+    const int k = j * kWave + ln;
+    vv[j] = 0; ty[j] = 0; lc[j] = -1; off[j] = 0; deg[j] = 0;
+    if (k < n) {
+      own |= 1u << j;
+      const int32_t v = node_at(L, b + k);
+      const uint8_t d = a.p.done[v];
+      vv[j] = v;
+      off[j] = a.p.dep_off[v];
+      deg[j] = a.p.dep_off[v + 1] - off[j];
+      ty[j] = a.p.type[v];
+      lc[j] = a.p.loc[v];
+      W.ee[k] = d ? 0 : a.p.est[v];
+      W.cnt[k] = 0;
+      W.mx[k] = 0;
+      W.dn[k] = d;
+      W.nr[k] = 0;
+    }
+  }
+  wave_order();
+
+  // B: out-degree counters, readiness, dependency lists into LDS
+#pragma unroll
+  for (int j = 0; j < NPTW; ++j) {
+    if (ballot((own >> j) & 1u) == 0) continue;
+    const int k = j * kWave + ln;
+    const bool mine = (own >> j) & 1u;
+    const bool light = mine && deg[j] <= kPmax;
+    bool blocked = false;
+    uint32_t packed[kPmax];
+#pragma unroll
+    for (int q = 0; q < kPmax; ++q) {
+      int32_t lp = -1;
+      if (light && q < deg[j]) lp = checked_dep(L, a.p.dep_idx[off[j] + q], b, n, k, ctrl);
+      packed[q] = lp >= 0 ? uint32_t(lp) : kNoDep;
+      if (lp >= 0) {
+        atomicAdd(&W.cnt[lp], 1);
+        blocked |= W.dn[lp] == 0;
+      }
+    }
+    if (mine) {
+      W.pa[k] = light ? (packed[0] | (packed[1] << 16)) : 0xFFFFFFFFu;
+      W.pb[k] = light ? (packed[2] | (uint32_t(deg[j]) << 16)) : (kHeavyBit | kNoDep);
+      if (light && blocked) W.nr[k] = 1;
+    }
+    for (uint64_t hm = ballot(mine && !light); hm; hm &= hm - 1) {
+      const int src = __builtin_ctzll(hm);
+      const int kh = j * kWave + src;
+      const int o = readlane_i32(off[j], src);
+      const int d = readlane_i32(deg[j], src);
+      bool blk = false;
+      for (int e0 = 0; e0 < d; e0 += kWave) {
+        const int e = e0 + ln;
+        if (e < d) {
+          const int32_t lp = checked_dep(L, a.p.dep_idx[o + e], b, n, kh, ctrl);
+          if (lp >= 0) {
+            atomicAdd(&W.cnt[lp], 1);
+            blk |= W.dn[lp] == 0;
+          }
+        }
+      }
+      if (ballot(blk) != 0 && ln == 0) W.nr[kh] = 1;
+    }
+  }
+  wave_order();
+
+  // ready flags (staged by position for the sort's first pass); sinks queued
+  int tail = 0;
+#pragma unroll
+  for (int j = 0; j < NPTW; ++j) {
+    const int k = j * kWave + ln;
+    const bool mine = (own >> j) & 1u;
+    if (mine) {
+      const bool rd = W.dn[k] == 0 && W.nr[k] == 0;
+      if (rd) ready |= 1u << j;
+      a.stg_ready[b + k] = rd ? 1 : 0;
+    }
+    const bool sink = mine && W.cnt[k] == 0;
+    const uint64_t m = ballot(sink);
+    if (sink) W.queue[tail + int(lanes_below(m))] = uint16_t(k);
+    tail += int(__popcll(m));
+  }
+  wave_order();
+
+  // C: walk up the DAG
+  bool overflow = false;
+  int head = 0;
+  int cur = -1;
+  int processed = 0;
+  for (;;) {
+    // idle lanes take queued futures
+    const uint64_t idle = ballot(cur < 0);
+    const int avail = tail - head;
+    if (avail > 0 && idle != 0) {
+      const int rank = int(lanes_below(idle));
+      if (cur < 0 && rank < avail) cur = W.queue[head + rank];
+      const int took = int(__popcll(idle)) < avail ? int(__popcll(idle)) : avail;
+      head += took;
+    }
+    if (ballot(cur >= 0) == 0) break;
+    // the future's dependency slots, est' and running max in one LDS round trip
+    const int cs = cur >= 0 ? cur : 0;
+    const uint32_t pa0 = W.pa[cs];
+    const uint32_t pb0 = W.pb[cs];
+    const int64_t ec = W.ee[cs];
+    const int64_t mc = W.mx[cs];
+    const uint32_t pa = cur >= 0 ? pa0 : 0xFFFFFFFFu;
+    const uint32_t pb = cur >= 0 ? pb0 : kNoDep;
+    const bool hv = cur >= 0 && (pb & kHeavyBit) != 0;
+    int next = -1, extra0 = -1, extra1 = -1;
+    if (cur >= 0 && !hv) {
+      const int64_t r = clamp_rem(ec + mc, overflow);
+      W.mx[cur] = r;
+      ++processed;
+      // all pushes first, then look at the returned counts (one round trip)
+      int lp[kPmax], old[kPmax];
+#pragma unroll
+      for (int q = 0; q < kPmax; ++q) {
+        lp[q] = dep_at(pa, pb, q);
+        old[q] = 0;
+        if (lp[q] >= 0) {
+          atomicMax(reinterpret_cast<long long*>(&W.mx[lp[q]]), (long long)r);
+          old[q] = atomicSub(&W.cnt[lp[q]], 1);
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < kPmax; ++q) {
+        if (lp[q] >= 0 && old[q] == 1) {
+          if (next < 0) next = lp[q];
+          else if (extra0 < 0) extra0 = lp[q];
+          else extra1 = lp[q];
+        }
+      }
+    }
+    // whole-wave push of futures with many dependencies
+    for (uint64_t hm = ballot(hv); hm; hm &= hm - 1) {
+      const int src = __builtin_ctzll(hm);
+      const int kh = readlane_i32(cur, src);
+      const int64_t r = clamp_rem(W.ee[kh] + W.mx[kh], overflow);
+      const int32_t v = node_at(L, b + kh);
+      const int o = a.p.dep_off[v];
+      const int d = a.p.dep_off[v + 1] - o;
+      if (ln == 0) {
+        W.mx[kh] = r;
+        ++processed;
+      }
+      for (int e0 = 0; e0 < d; e0 += kWave) {
+        const int e = e0 + ln;
+        bool app = false;
+        int32_t lp = -1;
+        if (e < d) {
+          lp = local_of(L, a.p.dep_idx[o + e], b, n);
+          if (lp >= 0 && lp != kh) {
+            atomicMax(reinterpret_cast<long long*>(&W.mx[lp]), (long long)r);
+            app = atomicSub(&W.cnt[lp], 1) == 1;
+          }
+        }
+        const uint64_t m = ballot(app);
+        if (app) W.queue[tail + int(lanes_below(m))] = uint16_t(lp);
+        tail += int(__popcll(m));
+      }
+    }
+    if (hv) cur = -1;
+    // futures beyond the first one a lane released join the queue
+    {
+      const uint64_t m0 = ballot(extra0 >= 0);
+      if (extra0 >= 0) W.queue[tail + int(lanes_below(m0))] = uint16_t(extra0);
+      tail += int(__popcll(m0));
+      const uint64_t m1 = ballot(extra1 >= 0);
+      if (extra1 >= 0) W.queue[tail + int(lanes_below(m1))] = uint16_t(extra1);
+      tail += int(__popcll(m1));
+    }
+    if (!hv) cur = next;
+    wave_order();
+  }
+  if (overflow) flag_status(ctrl, kStRange);
+  if (a.rem_out) {  // rem stayed in LDS during the walk; store it once
+#pragma unroll
+    for (int j = 0; j < NPTW; ++j)
+      if ((own >> j) & 1u) a.rem_out[vv[j]] = W.mx[j * kWave + ln];
+  }
+  const int64_t done_cnt = wave_sum_i64(processed);
+  if (ln == 0 && done_cnt != n) flag_status(ctrl, kStCycle);
+
+  // D: slack, route, staged at the future's position
+#pragma unroll
+  for (int j = 0; j < NPTW; ++j) {
+    if ((ready >> j) & 1u) {
+      const int k = j * kWave + ln;
+      write_ready(a, it, b + k, ty[j], lc[j], W.mx[k], W.ee[k], dl, acc);
+    }
+  }
+  wave_order();
 }
 
 // ------------------------------------------------------------ kernel
@@ -611,7 +864,7 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
     if (n <= 0) continue;
     const int64_t dl = a.p.deadline[w] - a.p.now;
     if (!a.force_global && n <= lds_cap)
-      sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, int(w), b, n, dl, acc);
+      sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, lds_cap, b, n, dl, acc);
     else
       sweep_hbm<T>(a, L, it, S, int(w), b, n, dl, acc);
   }
@@ -639,71 +892,143 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
   }
 }
 
-struct Variant {
-  int threads, npt;
-  const void* fn;
-};
+constexpr int kWaveNpt = 8;                  // futures per lane in the wave path
+constexpr int kWaveCap = kWave * kWaveNpt;     // at most 512 futures per wave
+constexpr int kWaveBlock = 256;                // four independent waves per workgroup
+constexpr int kWavesPerBlock = kWaveBlock / kWave;
+constexpr size_t kWaveSliceBytesPerFuture = 8 + 8 + 4 + 4 + 4 + 1 + 1 + 2;
 
-const Variant kVariants[] = {
-    {64, 4, reinterpret_cast<const void*>(&k_sweep<64, 4>)},
-    {256, 4, reinterpret_cast<const void*>(&k_sweep<256, 4>)},
-    {512, 4, reinterpret_cast<const void*>(&k_sweep<512, 4>)},
-    {1024, 5, reinterpret_cast<const void*>(&k_sweep<1024, 5>)},
-};
+// Small workflows: one wave each, no workgroup barriers.  Workflows larger than
+// a wave's slice (wcap futures) are swept afterwards by whole workgroups with
+// HBM state.
+__global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap) {
+  Ctrl* ctrl = a.ctrl;
+  if (ld_relaxed_agent(&ctrl->status) != 0) return;
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ Shared S;
+  const int M = int(a.p.M);
+  const int tid = threadIdx.x;
+  const int wv = tid / kWave;
+  const size_t nw = size_t(kWavesPerBlock) * size_t(wcap);
+  unsigned char* sp = smem;
+  ITabLds it;
+  WaveSlice Wv;
+  it.load = reinterpret_cast<int64_t*>(sp); sp += 8 * size_t(M);
+  it.inv = reinterpret_cast<double*>(sp); sp += 8 * size_t(M);
+  Wv.mx = reinterpret_cast<int64_t*>(sp) + size_t(wv) * wcap; sp += 8 * nw;
+  Wv.ee = reinterpret_cast<int64_t*>(sp) + size_t(wv) * wcap; sp += 8 * nw;
+  it.type = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  it.idx = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  it.speed = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  it.pos = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  Wv.cnt = reinterpret_cast<int32_t*>(sp) + size_t(wv) * wcap; sp += 4 * nw;
+  Wv.pa = reinterpret_cast<uint32_t*>(sp) + size_t(wv) * wcap; sp += 4 * nw;
+  Wv.pb = reinterpret_cast<uint32_t*>(sp) + size_t(wv) * wcap; sp += 4 * nw;
+  Wv.queue = reinterpret_cast<uint16_t*>(sp) + size_t(wv) * wcap; sp += 2 * nw;
+  Wv.dn = sp + size_t(wv) * wcap; sp += nw;
+  Wv.nr = sp + size_t(wv) * wcap;
+  for (int i = tid; i < M; i += kWaveBlock) {
+    it.load[i] = a.itab.load[i];
+    it.inv[i] = a.itab.inv_speed[i];
+    it.type[i] = a.itab.type[i];
+    it.idx[i] = a.itab.idx[i];
+    it.speed[i] = a.itab.speed[i];
+    it.pos[i] = a.itab.pos_of[i];
+  }
+  __syncthreads();
+
+  const Layout L{a.node_of_pos, a.pos_of_node, a.p.N};
+  Acc acc;
+  const int64_t gw = int64_t(blockIdx.x) * kWavesPerBlock + wv;
+  const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
+  if (!a.force_global) {
+    for (int64_t w = gw; w < a.p.W; w += nwaves) {
+      const int64_t b = a.wf_off[w];
+      const int n = a.wf_off[w + 1] - int32_t(b);
+      if (n <= 0 || n > wcap) continue;
+      sweep_wave<kWaveNpt>(a, L, it, Wv, b, n, a.p.deadline[w] - a.p.now, acc);
+    }
+  }
+  __syncthreads();
+  for (int64_t w = blockIdx.x; w < a.p.W; w += gridDim.x) {
+    const int64_t b = a.wf_off[w];
+    const int n = a.wf_off[w + 1] - int32_t(b);
+    if (n <= 0 || (n <= wcap && !a.force_global)) continue;
+    sweep_hbm<kWaveBlock>(a, L, it, S, int(w), b, n, a.p.deadline[w] - a.p.now, acc);
+  }
+
+  const int64_t mn = wave_min_i64(acc.tmin);
+  const int64_t mxv = wave_max_i64(acc.tmax);
+  const int64_t rd = wave_sum_i64(acc.tready);
+  if (lane_id() == 0) { S.red[0][wv] = mn; S.red[1][wv] = mxv; S.red[2][wv] = rd; }
+  __syncthreads();
+  if (tid == 0) {
+    int64_t a0 = INT64_MAX, a1 = INT64_MIN, a2 = 0;
+    for (int x = 0; x < kWavesPerBlock; ++x) {
+      a0 = S.red[0][x] < a0 ? S.red[0][x] : a0;
+      a1 = S.red[1][x] > a1 ? S.red[1][x] : a1;
+      a2 += S.red[2][x];
+    }
+    if (a2 > 0) {
+      const int slot = blockIdx.x & (kParts - 1);
+      __hip_atomic_fetch_min(&ctrl->part_min[slot], a0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_fetch_max(&ctrl->part_max[slot], a1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      add_agent(&ctrl->part_cnt[slot], a2);
+    }
+  }
+}
+
+constexpr int kBlockT = 1024;
+constexpr int kBlockNpt = 5;
 
 }  // namespace
 
 SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t lds_limit) {
   const int64_t avg = W > 0 ? (N + W - 1) / W : 0;
-  int vi = 3;
-  if (avg <= 128) vi = 0;
-  else if (avg <= 512) vi = 1;
-  else if (avg <= 2048) vi = 2;
-  SweepShape s;
-  s.threads = kVariants[vi].threads;
-  s.npt = kVariants[vi].npt;
   const size_t itab = 32 * size_t(M);
+  SweepShape s;
+  if (avg <= kWaveCap) {  // one wave per workflow
+    int64_t wcap = 64;       // room for workflows up to twice the average size
+    while (wcap < 2 * avg && wcap < kWaveCap) wcap *= 2;
+    s.threads = kWaveBlock;
+    s.npt = kWaveNpt;
+    s.lds_cap = int(wcap);
+    s.lds_bytes = itab + kWaveSliceBytesPerFuture * size_t(kWavesPerBlock) * size_t(wcap) + 16;
+    int64_t blocks = (W + kWavesPerBlock - 1) / kWavesPerBlock;
+    const int64_t most = int64_t(device_cus) * 8;
+    if (blocks > most) blocks = most;
+    s.blocks = int(blocks < 1 ? 1 : blocks);
+    return s;
+  }
+  s.threads = kBlockT;
+  s.npt = kBlockNpt;
   const size_t avail = lds_limit > kStaticLdsReserve + itab ? lds_limit - kStaticLdsReserve - itab : 0;
   int64_t cap = int64_t(avail / 14);
-  if (cap > int64_t(s.threads) * s.npt) cap = int64_t(s.threads) * s.npt;
+  if (cap > int64_t(kBlockT) * kBlockNpt) cap = int64_t(kBlockT) * kBlockNpt;
   s.lds_cap = int(cap);
   s.lds_bytes = itab + 14 * size_t(cap) + 16;
-  int64_t per_cu = 2048 / s.threads;
-  if (per_cu < 1) per_cu = 1;
-  int64_t blocks = int64_t(device_cus) * per_cu;
+  int64_t blocks = int64_t(device_cus) * 2;
   if (blocks > W) blocks = W;
-  if (blocks < 1) blocks = 1;
-  s.blocks = int(blocks);
+  s.blocks = int(blocks < 1 ? 1 : blocks);
   return s;
 }
 
 hipError_t prepare_sweep_kernels(size_t lds_limit) {
   const size_t dyn = lds_limit > kStaticLdsReserve ? lds_limit - kStaticLdsReserve : 0;
-  for (const Variant& v : kVariants) {
-    hipError_t e = hipFuncSetAttribute(v.fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(dyn));
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sweep<kBlockT, kBlockNpt>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(dyn));
+  if (e != hipSuccess) return e;
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sweep_wave),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, int(dyn));
 }
 
 hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const SweepShape& sh) {
-  switch (sh.threads) {
-    case 64:
-      hipLaunchKernelGGL((k_sweep<64, 4>), dim3(sh.blocks), dim3(64), sh.lds_bytes, s, a, sh.lds_cap);
-      break;
-    case 256:
-      hipLaunchKernelGGL((k_sweep<256, 4>), dim3(sh.blocks), dim3(256), sh.lds_bytes, s, a,
-                         sh.lds_cap);
-      break;
-    case 512:
-      hipLaunchKernelGGL((k_sweep<512, 4>), dim3(sh.blocks), dim3(512), sh.lds_bytes, s, a,
-                         sh.lds_cap);
-      break;
-    default:
-      hipLaunchKernelGGL((k_sweep<1024, 5>), dim3(sh.blocks), dim3(1024), sh.lds_bytes, s, a,
-                         sh.lds_cap);
-      break;
-  }
+  if (sh.threads == kWaveBlock)
+    hipLaunchKernelGGL(k_sweep_wave, dim3(sh.blocks), dim3(kWaveBlock), sh.lds_bytes, s, a,
+                       sh.lds_cap);
+  else
+    hipLaunchKernelGGL((k_sweep<kBlockT, kBlockNpt>), dim3(sh.blocks), dim3(kBlockT), sh.lds_bytes, s,
+                       a, sh.lds_cap);
   return hipGetLastError();
 }
 
