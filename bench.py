@@ -4,7 +4,7 @@
 One step = one full pass (validation, remaining critical path, readiness,
 slack, routing, ordering) over the paper-scale snapshot: 4,096 workflows x 32
 futures = 131,072 in-flight futures (the largest point of the paper's
-scalability study, Section 6.4), inputs already resident in HBM.
+scalability study, Section 6.3), inputs already resident in HBM.
 
 Prints one JSON line: futures/s per pass (whole job), ms per pass, the
 roofline of the dominant kernel (per-kernel HIP-event timing recorded by the
@@ -72,7 +72,7 @@ def pass_alg_bytes(N: int, E: int, R: int, W: int, M: int) -> float:
 # copy of known size (`python3 bench.py --copy-calibration`).  Valid only for
 # the kernel sources it was taken on: a different source digest reports null.
 TRAFFIC = {
-    ("paper-scale", "sweep"): {"src_sha256": "cb6c946ad151e049eef7b9b357de28a9963c76abd163c1e50189b7cd9263658f",
+    ("paper-scale", "sweep"): {"src_sha256": "4f65702664701add8a9e8100c456bd6db5e6203327d3056ebfabd1e2c17d052b",
                                "bytes_per_launch": 6412921},
 }
 
@@ -80,7 +80,7 @@ TRAFFIC = {
 def source_digest() -> str:
     import hashlib
     h = hashlib.sha256()
-    for sub in ("paper_2601_05109_amd/csrc", "include"):
+    for sub in ("paper_2601_05109_amd/csrc",):
         d = os.path.join(ROOT, sub)
         for f in sorted(os.listdir(d)):
             if f.endswith((".hip", ".hpp", ".h")):

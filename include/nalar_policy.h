@@ -7,8 +7,8 @@
  * "pass":
  *
  *   1. remaining critical path of every future: the longest service-time
- *      path from the future through its consumers (the "least remaining work"
- *      key of the SRTF policy, Section 6.3, taken over the whole DAG);
+ *      path from the future through its consumers (the remaining-work key
+ *      of the SRTF policy, Section 6.2, taken over the whole DAG);
  *   2. readiness: a future is runnable once it is not done and every future it
  *      depends on is done (push-based readiness, Section 4.3.1, property 3);
  *   3. priority: ready futures ranked by deadline slack, most urgent first

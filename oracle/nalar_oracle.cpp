@@ -17,7 +17,7 @@
 //       successors; meeting a node still on the stack is a cycle  -> -2 (ECYCLE)
 //   O5  remaining critical path, visited in that post-order:
 //         rem[v] = est'[v] + max(0, max over successors s of rem[s])
-//       (the "least remaining work" of the SRTF policy, Section 6.3,
+//       (the remaining work by which the SRTF policy ranks jobs, Section 6.2,
 //       generalised from a chain of stages to a DAG); rem > 2^62 -> -3 (ERANGE)
 //   O6  ready[v] = !done[v] and every dependency of v is done (push-based
 //       readiness, Section 4.3.1, property 3)

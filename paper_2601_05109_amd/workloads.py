@@ -7,7 +7,7 @@ routing computation), so that the CPU oracle and the HIP path can both consume
 its arrays without sharing any code of the method.
 
 The shapes and value distributions stand in for the paper's emulated
-scalability workload (Section 6.4: 1,024 to 131K futures, profiled LLM call
+scalability workload (Section 6.3: 1,024 to 131K futures, profiled LLM call
 latencies replacing inference, 64/128 agents).  Every array is int64 for time
 values (fixed-point microseconds), int32 for ids and offsets, uint8 for flags.
 

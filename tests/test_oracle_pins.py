@@ -5,7 +5,7 @@ checked here against things other than itself:
 
 * hand-worked examples (tests/golden/, derivations written in each file);
 * exhaustive path enumeration on small random DAGs (remaining work is the
-  longest est'-weighted path, Section 6.3's "least remaining work");
+  longest est'-weighted path, the remaining work ranked by SRTF, Section 6.2);
 * a push-based replay of value deliveries for readiness (Section 4.3.1,
   property 3), a different formulation from the oracle's pull check;
 * the optimality certificate of longest paths (edge inequality, equality on
