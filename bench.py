@@ -42,6 +42,8 @@ def alg_bytes(kernel: str, N: int, E: int, R: int, W: int, M: int, grouped: bool
     sort_pass  per ready future 24 (key 8 + payload 4, read and written)
     last pass  per ready future 48 (key, payload, staged route and cost read;
                order, slack, route, cost written)
+    sort_bucket per ready future 48 (bucketed slack, position, route, cost
+               read; order, slack, route, cost written)
     """
     if kernel == "sweep":
         b = 21 * N + 4 * E + 28 * R + 8 * W + 16 * M
@@ -50,6 +52,8 @@ def alg_bytes(kernel: str, N: int, E: int, R: int, W: int, M: int, grouped: bool
         return float(b)
     if kernel == "nodes":
         return float(25 * N + 8 * W + 16 * M)
+    if kernel == "sort_bucket":
+        return float(48 * R)
     if kernel == "sort_hist":
         return float(8 * R)
     if kernel == "sort_pass3":

@@ -70,13 +70,18 @@ enum {
 #define NALAR_FORCE_GLOBAL_SWEEP 1u  /* keep every workflow's sweep state in HBM
                                         instead of LDS (exercises the path used
                                         for workflows too large for LDS)         */
+#define NALAR_FORCE_TILED_SORT   2u  /* always order the ready futures with the
+                                        tiled radix sort (the path otherwise used
+                                        on a handle's first pass, above 131072
+                                        ready futures and when a bucket of the
+                                        bucketed sort overflows)                 */
 
 typedef struct nalar_policy nalar_policy;   /* opaque handle */
 
 /* Creation-time settings.  Host memory, read during nalar_policy_create only. */
 typedef struct {
   int32_t device;             /* HIP device ordinal                               */
-  uint32_t flags;             /* NALAR_FORCE_GLOBAL_SWEEP or 0                    */
+  uint32_t flags;             /* NALAR_FORCE_* bits or 0                          */
   void* stream;               /* hipStream_t the pass runs on; NULL = null stream */
   int64_t reserve_nodes;      /* scratch pre-size hints (0 = size on first pass)  */
   int64_t reserve_edges;

@@ -5,13 +5,21 @@
 //   group  -> (only when the caller's ids are not grouped by workflow) stable
 //             radix sort of the ids by workflow
 //   sweep  -> remaining critical path, readiness, slack and routing
-//   sort   -> slack histogram and range, then four digit passes (those the
-//             range does not need return at once); the last needed pass
-//             gathers into the caller's arrays and writes the status into
-//             pinned host memory
-// followed by one stream synchronisation.  A slack range wider than 32 bits
-// reports "continue" and the remaining passes follow after a second
-// synchronisation.  The node kernel resets the next pass's control block.
+//   sort   -> bucketed: the sweep has dropped every ready future into a
+//             bucket of a slack range guessed from the previous pass, and one
+//             kernel orders each bucket and writes it at its offset; or tiled:
+//             slack histogram and range, then four digit passes (those the
+//             range does not need return at once).  The last kernel gathers
+//             into the caller's arrays and writes the status into pinned host
+//             memory
+// followed by one stream synchronisation.  The bucketed sort is used once a
+// previous pass has given a slack range and at most kBucketMaxReady futures
+// were ready; if a bucket overflows, the kernel reports "tiled" and the tiled
+// sort follows after the synchronisation (then the bucketed sort is skipped for
+// a few passes).  A slack range wider than 32 bits reports "continue" from the
+// tiled sort and its remaining passes follow after another synchronisation.
+// The node kernel resets the next pass's control block and clears the bucket
+// counters.
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -52,7 +60,10 @@ struct Arena {
   uint8_t* g_dn = nullptr;
   uint8_t* g_nr = nullptr;
   int32_t* g_front[2] = {nullptr, nullptr};
-  int64_t capN = -1, capW = -1;
+  uint32_t* bcnt = nullptr;
+  uint32_t* bgroup = nullptr;
+  BucketSlot* bslot = nullptr;
+  int64_t capN = -1, capW = -1, capB = -1;
 };
 
 }  // namespace
@@ -66,6 +77,11 @@ struct nalar_policy {
   uint32_t epoch = 0;
   uint64_t passes = 0;           // selects the control block of the next pass
   bool ctrl_dirty[2] = {true, true};
+  // slack range and ready count of the last successful pass (bucket hint)
+  bool hint_valid = false;
+  int64_t hint_ready = 0, hint_min = 0, hint_max = 0;
+  int bucket_skip = 0;           // passes left before the bucketed sort is tried again
+  int bucket_backoff = 1;
   std::string err;
   Arena ar;
   HostStatus* host = nullptr;    // pinned, written by the sort kernel
@@ -92,7 +108,7 @@ int hip_fail(nalar_policy* h, hipError_t e, const char* what) {
 }
 
 // Lay out (or measure, when base is null) the arena for the given capacities.
-size_t carve(Arena& a, char* base, int64_t N, int64_t W) {
+size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B) {
   size_t off = 0;
   auto take = [&](size_t bytes) {
     off = align_up(off, 256);
@@ -126,6 +142,10 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W) {
   for (int i = 0; i < 2; ++i) a.g_front[i] = reinterpret_cast<int32_t*>(take(4 * size_t(n1)));
   a.g_dn = reinterpret_cast<uint8_t*>(take(size_t(n1)));
   a.g_nr = reinterpret_cast<uint8_t*>(take(size_t(n1)));
+  const int64_t b1 = B > 0 ? B : 0;
+  a.bcnt = reinterpret_cast<uint32_t*>(take(4 * size_t(b1 + 1)));
+  a.bgroup = reinterpret_cast<uint32_t*>(take(4 * size_t(b1 / kBucketGroup + 1)));
+  a.bslot = reinterpret_cast<BucketSlot*>(take(sizeof(BucketSlot) * size_t(b1) * kBucketCap));
   off = align_up(off, 256);
   a.lookback_off = off;
   a.slb = reinterpret_cast<uint64_t*>(take(8 * size_t(kMaxSortPasses) * tiles * kRadixBuckets));
@@ -134,11 +154,12 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W) {
   return align_up(off, 256);
 }
 
-int ensure_capacity(nalar_policy* h, int64_t N, int64_t W) {
+int ensure_capacity(nalar_policy* h, int64_t N, int64_t W, int64_t B) {
   Arena& a = h->ar;
-  if (a.base && N <= a.capN && W <= a.capW) return NALAR_OK;
+  if (a.base && N <= a.capN && W <= a.capW && B <= a.capB) return NALAR_OK;
   int64_t newN = a.capN > N ? a.capN : N;
   int64_t newW = a.capW > W ? a.capW : W;
+  int64_t newB = a.capB > B ? a.capB : B;
   if (a.base) {  // grow geometrically so a slowly growing graph reallocates rarely
     if (N > a.capN) newN = N + N / 4;
     if (W > a.capW) newW = W + W / 4;
@@ -148,11 +169,11 @@ int ensure_capacity(nalar_policy* h, int64_t N, int64_t W) {
     a.base = nullptr;
   }
   Arena fresh;
-  const size_t bytes = carve(fresh, nullptr, newN, newW);
+  const size_t bytes = carve(fresh, nullptr, newN, newW, newB);
   void* p = nullptr;
   hipError_t e = hipMalloc(&p, bytes);
   if (e != hipSuccess) {
-    a.capN = a.capW = -1;
+    a.capN = a.capW = a.capB = -1;
     return hip_fail(h, e, "hipMalloc(scratch)");
   }
   e = hipMemset(p, 0, bytes);  // look-back words must start untagged
@@ -160,15 +181,35 @@ int ensure_capacity(nalar_policy* h, int64_t N, int64_t W) {
     (void)hipFree(p);
     return hip_fail(h, e, "hipMemset(scratch)");
   }
-  carve(fresh, static_cast<char*>(p), newN, newW);
+  carve(fresh, static_cast<char*>(p), newN, newW, newB);
   fresh.base = p;
   fresh.bytes = bytes;
   fresh.capN = newN;
   fresh.capW = newW;
+  fresh.capB = newB;
   h->ar = fresh;
   h->epoch = 0;
   h->ctrl_dirty[0] = h->ctrl_dirty[1] = true;
   return NALAR_OK;
+}
+
+// Buckets for this pass from the previous pass's ready count and slack range
+// (nb == 0: use the tiled sort).
+BucketArgs plan_buckets(const nalar_policy* h, int64_t N) {
+  BucketArgs bk{};
+  if ((h->flags & NALAR_FORCE_TILED_SORT) || !h->hint_valid || h->bucket_skip > 0 || N == 0 ||
+      h->hint_ready > kBucketMaxReady)
+    return bk;
+  int64_t nb = kBucketMin;
+  while (nb < kBucketMax && nb * 2 <= h->hint_ready) nb *= 2;
+  int lognb = 0;
+  while ((int64_t(1) << lognb) < nb) ++lognb;
+  const uint64_t range = uint64_t(h->hint_max) - uint64_t(h->hint_min);
+  const int bits = range ? 64 - __builtin_clzll(range) : 0;
+  bk.lo = h->hint_min;
+  bk.shift = bits > lognb ? bits - lognb : 0;
+  bk.nb = int32_t(nb);
+  return bk;
 }
 
 bool in_range(int64_t v, int64_t lo, int64_t hi) { return v >= lo && v <= hi; }
@@ -225,7 +266,7 @@ int nalar_policy_create(const nalar_policy_config* cfg, nalar_policy** out) {
     g_create_error = "NULL config or output";
     return NALAR_EINVAL;
   }
-  if ((cfg->flags & ~NALAR_FORCE_GLOBAL_SWEEP) != 0 || cfg->reserve_nodes < 0 ||
+  if ((cfg->flags & ~(NALAR_FORCE_GLOBAL_SWEEP | NALAR_FORCE_TILED_SORT)) != 0 || cfg->reserve_nodes < 0 ||
       cfg->reserve_edges < 0 || cfg->reserve_workflows < 0 ||
       cfg->reserve_nodes > NALAR_MAX_NODES || cfg->reserve_workflows > NALAR_MAX_WORKFLOWS) {
     g_create_error = "invalid config";
@@ -259,7 +300,7 @@ int nalar_policy_create(const nalar_policy_config* cfg, nalar_policy** out) {
     e = hipEventCreate(&h->ev[i]);
     if (e != hipSuccess) return bail(e, "hipEventCreate");
   }
-  int rc = ensure_capacity(h, cfg->reserve_nodes, cfg->reserve_workflows);
+  int rc = ensure_capacity(h, cfg->reserve_nodes, cfg->reserve_workflows, 0);
   if (rc != NALAR_OK) {
     g_create_error = h->err;
     nalar_policy_destroy(h);
@@ -311,9 +352,14 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   hipError_t e = hipSetDevice(h->device);
   if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
   const int64_t N = p->n_nodes, W = p->n_workflows, M = p->n_instances;
-  rc = ensure_capacity(h, N, W);
+  BucketArgs bk = plan_buckets(h, N);
+  if (h->bucket_skip > 0) --h->bucket_skip;
+  rc = ensure_capacity(h, N, W, bk.nb);
   if (rc != NALAR_OK) return rc;
   Arena& A = h->ar;
+  bk.cnt = A.bcnt;
+  bk.group_cnt = A.bgroup;
+  bk.slot = A.bslot;
   hipStream_t s = h->stream;
   const int cur = int(h->passes & 1);
   const int nxt = cur ^ 1;
@@ -346,7 +392,8 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   } while (0)
 
   if (need_reset) NALAR_LAUNCH("reset", launch_reset(s, ctrl));
-  NALAR_LAUNCH("nodes", launch_nodes(s, pd, ctrl, A.ctrl[nxt], A.itab, A.wf_off, contiguous ? 1 : 0));
+  NALAR_LAUNCH("nodes",
+               launch_nodes(s, pd, ctrl, A.ctrl[nxt], A.itab, A.wf_off, contiguous ? 1 : 0, bk));
 
   const int32_t* node_of_pos = nullptr;
   const int32_t* pos_of_node = nullptr;
@@ -391,6 +438,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     sw.g_front0 = A.g_front[0];
     sw.g_front1 = A.g_front[1];
     sw.ctrl = ctrl;
+    sw.bk = bk;
     sw.force_global = (h->flags & NALAR_FORCE_GLOBAL_SWEEP) ? 1 : 0;
     const SweepShape sh = plan_sweep(N, W, M, h->cus, h->lds_limit);
     NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
@@ -418,18 +466,35 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   sa.route = r->route;
   sa.cost = r->cost_us;
   __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);  // the kernels overwrite it
-  e = launch_slack_sort(s, sa, 0, kSortLaunched - 1, Timer::cb, &tm);
-  if (e != hipSuccess) return hip_fail(h, e, "sort");
-  tm.end();
-  e = hipStreamSynchronize(s);
-  if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
-  if (__atomic_load_n(&h->host->status, __ATOMIC_ACQUIRE) == kStatusContinue) {
-    __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);
-    e = launch_slack_sort(s, sa, kSortLaunched, kMaxSortPasses - 1, Timer::cb, &tm);
+  bool tiled = bk.nb == 0;
+  if (!tiled) {
+    NALAR_LAUNCH("sort_bucket", launch_bucket_sort(s, sa, bk));
+    tm.end();
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
+    if (__atomic_load_n(&h->host->status, __ATOMIC_ACQUIRE) == kStatusTiled) {
+      __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);
+      tiled = true;
+      h->bucket_skip = h->bucket_backoff;
+      h->bucket_backoff = h->bucket_backoff < 64 ? 2 * h->bucket_backoff : 64;
+    } else {
+      h->bucket_backoff = 1;
+    }
+  }
+  if (tiled) {
+    e = launch_slack_sort(s, sa, 0, kSortLaunched - 1, Timer::cb, &tm);
     if (e != hipSuccess) return hip_fail(h, e, "sort");
     tm.end();
     e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
+    if (__atomic_load_n(&h->host->status, __ATOMIC_ACQUIRE) == kStatusContinue) {
+      __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);
+      e = launch_slack_sort(s, sa, kSortLaunched, kMaxSortPasses - 1, Timer::cb, &tm);
+      if (e != hipSuccess) return hip_fail(h, e, "sort");
+      tm.end();
+      e = hipStreamSynchronize(s);
+      if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
+    }
   }
 #undef NALAR_LAUNCH
   h->passes += 1;
@@ -445,6 +510,10 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   if (st & kStCycle) return fail(h, NALAR_ECYCLE, "dependency cycle");
   if (st & kStRange) return fail(h, NALAR_ERANGE, "remaining critical path exceeds 2^62 us");
   r->n_ready = __atomic_load_n(&h->host->n_ready, __ATOMIC_ACQUIRE);
+  h->hint_valid = true;
+  h->hint_ready = r->n_ready;
+  h->hint_min = r->n_ready ? __atomic_load_n(&h->host->slack_min, __ATOMIC_ACQUIRE) : 0;
+  h->hint_max = r->n_ready ? __atomic_load_n(&h->host->slack_max, __ATOMIC_ACQUIRE) : 0;
   return NALAR_OK;
 }
 

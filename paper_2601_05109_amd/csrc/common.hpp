@@ -43,6 +43,8 @@ constexpr int kParts = 64;
 struct Ctrl {
   uint32_t status;
   uint32_t sort_npass;           // digit passes the slack sort runs
+  uint32_t bucket_overflow;      // a bucket of the bucketed sort overflowed
+  uint32_t pad;
   int64_t n_ready;
   int64_t slack_min;
   int64_t slack_max;
@@ -59,11 +61,32 @@ struct Ctrl {
 constexpr int kSortLaunched = 4;
 constexpr uint32_t kStatusContinue = 0x40000000u;
 
+// Bucketed slack sort.  With the slack range of the previous pass as a hint,
+// the sweep drops each ready future into one of nb buckets of increasing slack
+// (kBucketCap slots each, unordered inside a bucket); one kernel then orders
+// every bucket and writes it at its offset.  A bucket that overflows reports
+// kStatusTiled and the host runs the tiled radix sort instead.
+constexpr int kBucketCap = 64;            // slots per bucket
+constexpr int kBucketGroup = 16;          // buckets per workgroup of the bucket kernel
+constexpr int kBucketMin = 64;            // bucket counts are powers of two in
+constexpr int kBucketMax = 65536;         //   [kBucketMin, kBucketMax]
+constexpr int64_t kBucketMaxReady = 131072;  // larger ready sets use the tiled sort
+constexpr uint32_t kStatusTiled = 0x20000000u;
+
+struct BucketSlot {
+  int64_t slack;
+  int64_t cost;
+  int32_t pos;
+  int32_t route;
+};
+
 // Written by the last kernel of a pass into pinned host memory.
 struct HostStatus {
   uint32_t status;
-  uint32_t pad;
+  uint32_t key_bits;   // significant bits of the slack range
   int64_t n_ready;
+  int64_t slack_min;   // range of this pass (the next pass's bucket hint)
+  int64_t slack_max;
 };
 
 // Resets a control block for a later pass (run by one workgroup).
@@ -72,6 +95,7 @@ __device__ inline void reset_ctrl(Ctrl* c) {
   if (tid == 0) {
     c->status = 0;
     c->sort_npass = 0;
+    c->bucket_overflow = 0;
     c->n_ready = 0;
     c->slack_min = INT64_MAX;
     c->slack_max = INT64_MIN;

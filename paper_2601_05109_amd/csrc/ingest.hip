@@ -45,9 +45,11 @@ __device__ inline int64_t lower_bound_from(const int32_t* a, int64_t n, int64_t 
 
 // Grid-stride over nodes, workflows and instances.  Workgroup 0 also sorts the
 // instance table by (type, index) so each future's candidates form one
-// contiguous run, and resets the control block of the next pass.
+// contiguous run, and resets the control block of the next pass.  The bucket
+// counters of this pass's bucketed sort are cleared here, before the sweep.
 __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl, Ctrl* next_ctrl,
-                                                       ITab it, int32_t* wf_off, int contiguous) {
+                                                       ITab it, int32_t* wf_off, int contiguous,
+                                                       BucketArgs bk) {
   const int64_t N = p.N, W = p.W, M = p.M;
   const int64_t stride = int64_t(gridDim.x) * kNodeThreads;
   const int64_t g0 = int64_t(blockIdx.x) * kNodeThreads + threadIdx.x;
@@ -81,6 +83,10 @@ __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl
       const int64_t guess = W > 0 ? (w * N) / W : 0;
       wf_off[w] = int32_t(lower_bound_from(p.wf, N, w, guess));
     }
+  }
+  for (int64_t i = g0; i < bk.nb; i += stride) {  // empty buckets for the sweep
+    bk.cnt[i] = 0;
+    if (i < bk.nb / kBucketGroup) bk.group_cnt[i] = 0;
   }
   if (__ballot(bad) != 0 && lane_id() == 0) flag_status(ctrl, kStInval);
 
@@ -117,10 +123,11 @@ int grid_for(int64_t n, int threads, int cap) {
 }  // namespace
 
 hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
-                        int32_t* wf_off, int contiguous) {
+                        int32_t* wf_off, int contiguous, const BucketArgs& bk) {
   int64_t n = p.N > p.W + 1 ? p.N : p.W + 1;
+  if (n < bk.nb) n = bk.nb;
   hipLaunchKernelGGL(k_nodes, dim3(grid_for(n, kNodeThreads, 4096)), dim3(kNodeThreads), 0, s, p,
-                     ctrl, next_ctrl, itab, wf_off, contiguous);
+                     ctrl, next_ctrl, itab, wf_off, contiguous, bk);
   return hipGetLastError();
 }
 

@@ -64,6 +64,17 @@ struct GroupArgs {
   int32_t* wf_off;
 };
 
+// Buckets of the bucketed slack sort (nb == 0: not used this pass).  Bucket of
+// a slack s: min((s - lo) >> shift, nb - 1), 0 below lo.
+struct BucketArgs {
+  int64_t lo;
+  int32_t shift;
+  int32_t nb;
+  uint32_t* cnt;                // [nb] futures dropped into each bucket
+  uint32_t* group_cnt;          // [nb / kBucketGroup] the same per group of buckets
+  BucketSlot* slot;             // [nb * kBucketCap]
+};
+
 struct SweepArgs {
   ProblemDev p;
   ITab itab;
@@ -82,15 +93,17 @@ struct SweepArgs {
   int32_t* g_front0;
   int32_t* g_front1;
   Ctrl* ctrl;
+  BucketArgs bk;
   int force_global;
 };
 
 // ingest.hip
 hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
-                        int32_t* wf_off, int contiguous);
+                        int32_t* wf_off, int contiguous, const BucketArgs& bk);
 
 // sort.hip (mark(ctx, name) is called before each launch, for timing)
 hipError_t launch_reset(hipStream_t s, Ctrl* c);
+hipError_t launch_bucket_sort(hipStream_t s, const SortArgs& a, const BucketArgs& bk);
 hipError_t launch_slack_sort(hipStream_t s, const SortArgs& a, int first_pass, int last_pass,
                              void (*mark)(void*, const char*), void* ctx);
 hipError_t launch_group(hipStream_t s, const GroupArgs& a, void (*mark)(void*, const char*),

@@ -231,22 +231,26 @@ __device__ void radix_tile(TileSmem<K>& S, const FirstSource& f, bool first, int
 __global__ __launch_bounds__(kSortThreads) void k_reset(Ctrl* c) { reset_ctrl(c); }
 
 // Slack range, ready count and pass count from the sweep's slots (one wave).
+// s_range = {min slack, ready count, digit passes, significant key bits,
+// max slack}.
 __device__ void settle_range(Ctrl* ctrl, int64_t* s_range, bool write) {
   if (threadIdx.x < kWave) {
     const int64_t mn = wave_min_i64(ctrl->part_min[threadIdx.x]);
     const int64_t mx = wave_max_i64(ctrl->part_max[threadIdx.x]);
     const int64_t ct = wave_sum_i64(ctrl->part_cnt[threadIdx.x]);
     if (threadIdx.x == 0) {
-      int npass = 0;
+      int npass = 0, nbits = 0;
       if (ct > 0) {
         const uint64_t range = uint64_t(mx - mn);
-        const int nbits = range ? 64 - __builtin_clzll(range) : 0;
+        nbits = range ? 64 - __builtin_clzll(range) : 0;
         npass = (nbits + kRadixBits - 1) / kRadixBits;
         if (npass == 0) npass = 1;  // the first pass also compacts
       }
       s_range[0] = mn;
       s_range[1] = ct;
       s_range[2] = npass;
+      s_range[3] = nbits;
+      s_range[4] = mx;
       if (write) {
         ctrl->n_ready = ct;
         ctrl->slack_min = mn;
@@ -258,24 +262,115 @@ __device__ void settle_range(Ctrl* ctrl, int64_t* s_range, bool write) {
   __syncthreads();
 }
 
-__device__ inline void publish_status(HostStatus* host, uint32_t status, int64_t n_ready) {
+// Status, ready count and slack range for the host (one thread).
+__device__ inline void publish_status(HostStatus* host, uint32_t status, int64_t n_ready,
+                                      int key_bits, int64_t smin, int64_t smax) {
   __hip_atomic_store(&host->n_ready, n_ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&host->key_bits, uint32_t(key_bits), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&host->slack_min, smin, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&host->slack_max, smax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __hip_atomic_store(&host->status, status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// ------------------------------------------------------------ bucketed sort
+
+constexpr int kBucketThreads = 256;
+constexpr int kGroupSlots = kBucketGroup * kBucketCap;
+
+// One workgroup per group of kBucketGroup buckets.  Buckets ascend in slack, so
+// a future's place in the order is: futures in earlier groups (a sum of group
+// counts), plus futures in earlier buckets of its group, plus its rank among
+// its bucket-mates by (slack, position).  Positions ascend in (workflow, id),
+// so that is the rank by (slack, workflow, id).
+__global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, BucketArgs bk) {
+  __shared__ int64_t s_range[5];
+  __shared__ uint32_t s_off[kBucketGroup + 1];
+  __shared__ uint32_t s_red[kBucketThreads / kWave];
+  __shared__ int64_t s_slack[kGroupSlots];
+  __shared__ int64_t s_cost[kGroupSlots];
+  __shared__ int32_t s_pos[kGroupSlots];
+  __shared__ int32_t s_route[kGroupSlots];
+  __shared__ uint8_t s_bkt[kGroupSlots];
+  const int tid = threadIdx.x;
+  const int g = blockIdx.x;
+  Ctrl* ctrl = a.ctrl;
+  const uint32_t status = ctrl->status;
+  if (status) {
+    if (g == 0 && tid == 0) publish_status(a.host, status, 0, 0, 0, 0);
+    return;
+  }
+  settle_range(ctrl, s_range, g == 0);
+  const int64_t R = s_range[1];
+  if (ld_relaxed_agent(&ctrl->bucket_overflow) != 0) {
+    if (g == 0 && tid == 0)
+      publish_status(a.host, kStatusTiled, R, int(s_range[3]), s_range[0], s_range[4]);
+    return;
+  }
+  if (g == 0 && tid == 0) publish_status(a.host, 0, R, int(s_range[3]), s_range[0], s_range[4]);
+
+  // futures in earlier groups
+  uint32_t part = 0;
+  for (int i = tid; i < g; i += kBucketThreads) part += bk.group_cnt[i];
+  part = uint32_t(wave_sum_i64(int64_t(part)));
+  if (lane_id() == 0) s_red[tid / kWave] = part;
+  if (tid < kWave) {  // bucket offsets inside the group (wave 0)
+    uint32_t c = tid < kBucketGroup ? bk.cnt[g * kBucketGroup + tid] : 0u;
+    c = c < uint32_t(kBucketCap) ? c : uint32_t(kBucketCap);  // overflow was handled above
+    const uint32_t inc = wave_incl_scan_u32(c);
+    if (tid < kBucketGroup) s_off[tid + 1] = inc;
+    if (tid == 0) s_off[0] = 0;
+  }
+  __syncthreads();
+  int64_t base = 0;
+#pragma unroll
+  for (int w = 0; w < kBucketThreads / kWave; ++w) base += s_red[w];
+  const int T = int(s_off[kBucketGroup]);
+  if (T == 0) return;
+
+  // this group's futures into LDS, bucket by bucket
+  for (int i = tid; i < T; i += kBucketThreads) {
+    int b = 0;
+#pragma unroll
+    for (int k = 1; k < kBucketGroup; ++k) b += int(s_off[k]) <= i;
+    const BucketSlot* sl = bk.slot + (int64_t(g) * kBucketGroup + b) * kBucketCap + (i - int(s_off[b]));
+    s_slack[i] = sl->slack;
+    s_cost[i] = sl->cost;
+    s_pos[i] = sl->pos;
+    s_route[i] = sl->route;
+    s_bkt[i] = uint8_t(b);
+  }
+  __syncthreads();
+  for (int i = tid; i < T; i += kBucketThreads) {
+    const int b = s_bkt[i];
+    const int lo = int(s_off[b]), hi = int(s_off[b + 1]);
+    const int64_t sk = s_slack[i];
+    const int32_t ps = s_pos[i];
+    int rank = 0;
+    for (int j = lo; j < hi; ++j) {
+      const int64_t o = s_slack[j];
+      rank += (o < sk) | ((o == sk) & (s_pos[j] < ps));
+    }
+    const int64_t out = base + lo + rank;
+    a.order[out] = a.node_of_pos ? a.node_of_pos[ps] : ps;
+    a.slack[out] = sk;
+    a.route[out] = s_route[i];
+    if (a.cost) a.cost[out] = s_cost[i];
+  }
 }
 
 __global__ __launch_bounds__(kSortThreads) void k_slack_hist(SortArgs a) {
   __shared__ uint32_t H[kMaxSortPasses][kRadixBuckets];
-  __shared__ int64_t s_range[3];
+  __shared__ int64_t s_range[5];
   Ctrl* ctrl = a.ctrl;
   const uint32_t status = ctrl->status;
   if (status) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) publish_status(a.host, status, 0);
+    if (blockIdx.x == 0 && threadIdx.x == 0) publish_status(a.host, status, 0, 0, 0, 0);
     return;
   }
   settle_range(ctrl, s_range, blockIdx.x == 0);
   const int npass = int(s_range[2]);
   if (npass == 0) {  // nothing ready: no pass runs, so report here
-    if (blockIdx.x == 0 && threadIdx.x == 0) publish_status(a.host, 0, 0);
+    if (blockIdx.x == 0 && threadIdx.x == 0) publish_status(a.host, 0, 0, 0, 0, 0);
     return;
   }
   const FirstSource f{kSrcStaged, a.stg_slack, a.stg_ready, nullptr, a.span, s_range[0]};
@@ -309,8 +404,10 @@ __global__ __launch_bounds__(kSortThreads) void k_slack_pass(SortArgs a, int pas
                        ctrl->ghist_slack + pass * kRadixBuckets,
                        a.lookback + int64_t(pass) * a.tiles_cap * kRadixBuckets, a.epoch, fo);
   if (tile == 0 && threadIdx.x == 0) {
-    if (last) publish_status(a.host, 0, R);
-    else if (pass == kSortLaunched - 1) publish_status(a.host, kStatusContinue, R);
+    const int64_t smax = ctrl->slack_max;
+    const int nbits = 64 - __builtin_clzll(uint64_t(smax - smin) | 1);
+    if (last) publish_status(a.host, 0, R, nbits, smin, smax);
+    else if (pass == kSortLaunched - 1) publish_status(a.host, kStatusContinue, R, nbits, smin, smax);
   }
 }
 
@@ -370,6 +467,11 @@ unsigned grid_of(int64_t n, int64_t per, int64_t cap) {
 
 hipError_t launch_reset(hipStream_t s, Ctrl* c) {
   hipLaunchKernelGGL(k_reset, dim3(1), dim3(kSortThreads), 0, s, c);
+  return hipGetLastError();
+}
+
+hipError_t launch_bucket_sort(hipStream_t s, const SortArgs& a, const BucketArgs& bk) {
+  hipLaunchKernelGGL(k_bucket_sort, dim3(bk.nb / kBucketGroup), dim3(kBucketThreads), 0, s, a, bk);
   return hipGetLastError();
 }
 

@@ -212,6 +212,23 @@ __device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_
   a.stg_slack[pos] = slack;
   a.stg_route[pos] = route;
   a.stg_cost[pos] = cost;
+  if (a.bk.nb > 0) {  // drop into its bucket for the bucketed sort
+    const BucketArgs& bk = a.bk;
+    const uint64_t d = slack > bk.lo ? uint64_t(slack) - uint64_t(bk.lo) : 0;
+    const uint64_t q = d >> bk.shift;
+    const uint32_t bkt = q < uint64_t(bk.nb) ? uint32_t(q) : uint32_t(bk.nb - 1);
+    const uint32_t s = add_agent(bk.cnt + bkt, 1u);
+    add_agent(bk.group_cnt + bkt / kBucketGroup, 1u);
+    if (s < uint32_t(kBucketCap)) {
+      BucketSlot* sl = bk.slot + int64_t(bkt) * kBucketCap + s;
+      sl->slack = slack;
+      sl->cost = cost;
+      sl->pos = int32_t(pos);
+      sl->route = route;
+    } else {
+      st_relaxed_agent(&a.ctrl->bucket_overflow, 1u);
+    }
+  }
   acc.tmin = slack < acc.tmin ? slack : acc.tmin;
   acc.tmax = slack > acc.tmax ? slack : acc.tmax;
   acc.tready += 1;

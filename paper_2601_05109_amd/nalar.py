@@ -23,6 +23,7 @@ LIB_PATH = os.path.join(HERE, "libnalar_policy.so")
 NALAR_OK, NALAR_EINVAL, NALAR_ECYCLE, NALAR_ERANGE, NALAR_ENOMEM, NALAR_EDEVICE = 0, -1, -2, -3, -4, -5
 NALAR_WF_CONTIGUOUS = 1
 NALAR_FORCE_GLOBAL_SWEEP = 1
+NALAR_FORCE_TILED_SORT = 2
 NALAR_MAX_INSTANCES = 1024
 
 EXPORTED = ("nalar_policy_create", "nalar_policy_pass", "nalar_policy_destroy",

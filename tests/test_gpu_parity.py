@@ -45,6 +45,12 @@ def policy_hbm():
         yield p
 
 
+@pytest.fixture(scope="module")
+def policy_tiled():
+    with nalar.Policy(flags=nalar.NALAR_FORCE_TILED_SORT) as p:
+        yield p
+
+
 def gpu_run(pol, p, flags=None):
     dp = nalar.DeviceProblem.from_host(p)
     out = nalar.DeviceResult.alloc(dp.n_nodes)
@@ -138,6 +144,65 @@ def test_configs_hbm_sweep(policy_hbm, cfg):
 
 def test_deep_chains_hbm_small(policy_hbm):
     check(policy_hbm, wl.deep_chains(W=64), "deep chains W=64 hbm")
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2])
+def test_configs_tiled_sort(policy_tiled, cfg):
+    check(policy_tiled, wl.CONFIGS[cfg](), f"config{cfg} tiled sort")
+
+
+def test_configs_relabelled_tiled_sort(policy_tiled):
+    p = wl.tiny()
+    check(policy_tiled, wl.relabel(p, np.random.default_rng(7).permutation(p.n_nodes)),
+          "config0 relabelled tiled sort")
+
+
+def _flat(deadline_offsets, per_wf=3):
+    """Workflows of independent futures, none done, zero estimates: every
+    future is ready and its slack is its workflow's deadline offset."""
+    W = len(deadline_offsets)
+    N = W * per_wf
+    now = 1_000_000
+    return wl.Problem("flat", now, 7, np.repeat(np.arange(W), per_wf).astype(np.int32),
+                      np.zeros(N, np.int32), np.zeros(N, np.int64), np.zeros(N, np.uint8),
+                      np.full(N, -1, np.int32), np.zeros(N + 1, np.int32), np.zeros(0, np.int32),
+                      (now + np.asarray(deadline_offsets, np.int64)).astype(np.int64),
+                      np.zeros(2, np.int32), np.array([5, 3], np.int64), np.array([1000, 7], np.int32),
+                      wf_contiguous=True)
+
+
+def test_sort_path_switching():
+    """One handle through changing snapshots, so the host's choice between the
+    bucketed sort (slack range guessed from the previous pass) and the tiled
+    sort moves back and forth: first pass, overflowing buckets, a slack range
+    far from the guess, more than 131072 ready futures, none ready."""
+    p1 = wl.paper_scale()
+    shifted = p1.copy(deadline_us=p1.deadline_us + 3_600_000_000)
+    cases = [
+        ("tiny first pass", wl.tiny()),
+        ("tiny again", wl.tiny()),
+        ("tiny other seed", wl.tiny(seed=3)),
+        ("paper-scale after tiny", p1),
+        ("paper-scale again", p1),
+        ("paper-scale third", p1),
+        ("all equal slack", _flat([3] * 200)),
+        ("paper-scale", p1),
+        ("deadlines shifted by an hour", shifted),
+        ("shifted again", shifted),
+        ("R=131072", wl.wide_mapreduce(W=32, fan=4096)),
+        ("R=131072 again", wl.wide_mapreduce(W=32, fan=4096, seed=4)),
+        ("R=262144", wl.wide_mapreduce(W=64, fan=4096)),
+        ("paper-scale after R=262144", p1),
+        ("none ready", p1.copy(done=np.ones(p1.n_nodes, np.uint8))),
+        ("after none ready", p1),
+        ("relabelled tiny", wl.relabel(wl.tiny(), np.random.default_rng(3).permutation(2048))),
+        ("relabelled tiny again", wl.relabel(wl.tiny(), np.random.default_rng(4).permutation(2048))),
+        ("range 2^40", _flat([-(1 << 39), 1 << 39, 0])),
+        ("range 2^40 again", _flat([-(1 << 39), 1 << 39, 0])),
+    ]
+    with nalar.Policy() as pol:
+        for label, p in cases:
+            check(pol, p, label)
 
 
 def test_other_seeds(policy):
