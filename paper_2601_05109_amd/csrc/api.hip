@@ -127,6 +127,7 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B) {
   a.itab.idx = reinterpret_cast<int32_t*>(take(4 * NALAR_MAX_INSTANCES));
   a.itab.speed = reinterpret_cast<int32_t*>(take(4 * NALAR_MAX_INSTANCES));
   a.itab.pos_of = reinterpret_cast<int32_t*>(take(4 * NALAR_MAX_INSTANCES));
+  a.itab.run = reinterpret_cast<uint32_t*>(take(4 * kTypeDirect));
   a.wf_off = reinterpret_cast<int32_t*>(take(4 * size_t(w1 + 1)));
   a.stg_slack = reinterpret_cast<int64_t*>(take(8 * size_t(n1)));
   a.stg_cost = reinterpret_cast<int64_t*>(take(8 * size_t(n1)));
@@ -392,8 +393,9 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   } while (0)
 
   if (need_reset) NALAR_LAUNCH("reset", launch_reset(s, ctrl));
-  NALAR_LAUNCH("nodes",
-               launch_nodes(s, pd, ctrl, A.ctrl[nxt], A.itab, A.wf_off, contiguous ? 1 : 0, bk));
+  const SweepShape sh = plan_sweep(N, W, M, h->cus, h->lds_limit);
+  NALAR_LAUNCH("nodes", launch_nodes(s, pd, ctrl, A.ctrl[nxt], A.itab, A.wf_off, contiguous ? 1 : 0,
+                                     bk, sh.large_cap));
 
   const int32_t* node_of_pos = nullptr;
   const int32_t* pos_of_node = nullptr;
@@ -413,6 +415,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     g.epoch = epoch;
     g.pos_of_node = A.pos_of_node;
     g.wf_off = A.wf_off;
+    g.large_cap = sh.large_cap;
     e = launch_group(s, g, Timer::cb, &tm);
     if (e != hipSuccess) return hip_fail(h, e, "group");
     node_of_pos = reinterpret_cast<const int32_t*>(A.gpay[(g.npass - 1) & 1]);
@@ -440,7 +443,6 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     sw.ctrl = ctrl;
     sw.bk = bk;
     sw.force_global = (h->flags & NALAR_FORCE_GLOBAL_SWEEP) ? 1 : 0;
-    const SweepShape sh = plan_sweep(N, W, M, h->cus, h->lds_limit);
     NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
   }
 

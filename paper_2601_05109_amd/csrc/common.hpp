@@ -41,9 +41,11 @@ __host__ __device__ inline uint64_t lb_pack(uint32_t epoch, uint64_t flag, uint6
 constexpr int kParts = 64;
 
 struct Ctrl {
-  uint32_t status;
+  uint32_t status;               // problems found before the sweep (validation)
+  uint32_t status_sweep;         // problems found by the sweep (cycles, ranges)
   uint32_t sort_npass;           // digit passes the slack sort runs
   uint32_t bucket_overflow;      // a bucket of the bucketed sort overflowed
+  uint32_t n_large;              // workflows too large for one wave's slice
   uint32_t pad;
   int64_t n_ready;
   int64_t slack_min;
@@ -94,8 +96,10 @@ __device__ inline void reset_ctrl(Ctrl* c) {
   const int tid = threadIdx.x;
   if (tid == 0) {
     c->status = 0;
+    c->status_sweep = 0;
     c->sort_npass = 0;
     c->bucket_overflow = 0;
+    c->n_large = 0;
     c->n_ready = 0;
     c->slack_min = INT64_MAX;
     c->slack_max = INT64_MIN;
@@ -111,7 +115,10 @@ __device__ inline void reset_ctrl(Ctrl* c) {
 }
 
 // Instance table sorted by (type, original index), plus the sorted position of
-// every original index (for the instance that holds a future's state).
+// every original index (for the instance that holds a future's state) and,
+// for types below kTypeDirect, the run of sorted positions holding that type.
+constexpr int kTypeDirect = 64;
+
 struct ITab {
   int64_t* load;      // [M]
   double* inv_speed;  // [M] 1.0 / speed
@@ -119,6 +126,7 @@ struct ITab {
   int32_t* idx;       // [M] original index
   int32_t* speed;     // [M]
   int32_t* pos_of;    // [M] sorted position of original index i
+  uint32_t* run;      // [kTypeDirect] first | end << 16 (0: no instance)
 };
 
 // ----------------------------------------------------------------- wave ops
@@ -216,6 +224,12 @@ __device__ inline void flag_status(Ctrl* c, uint32_t bits) {
   __hip_atomic_fetch_or(&c->status, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// The sweep reports into a word of its own, so that the status it reads at its
+// start (validation) cannot change while it runs.
+__device__ inline void flag_sweep(Ctrl* c, uint32_t bits) {
+  __hip_atomic_fetch_or(&c->status_sweep, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Exclusive prefix over earlier tiles by decoupled look-back.  The caller has
 // already published its own aggregate.  Every earlier tile was claimed (by
 // ticket) before the caller's, by a workgroup that publishes its aggregate
@@ -269,19 +283,37 @@ __host__ __device__ inline int64_t floordiv_exact(double a, int32_t d, double in
 __device__ inline void route_future(int32_t t, int64_t est, int32_t loc, int32_t M, int64_t mig,
                                     const int32_t* s_type, const int32_t* s_idx,
                                     const int64_t* s_load, const int32_t* s_speed,
-                                    const double* s_inv, const int32_t* s_pos, int32_t& route,
-                                    int64_t& cost) {
-  int lo = 0, hi = M;
-  while (lo < hi) {  // first position with type >= t
-    int mid = (lo + hi) >> 1;
-    if (s_type[mid] < t) lo = mid + 1; else hi = mid;
+                                    const double* s_inv, const int32_t* s_pos,
+                                    const uint32_t* s_run, int32_t& route, int64_t& cost) {
+  int lo, hi;
+  if (uint32_t(t) < uint32_t(kTypeDirect)) {
+    const uint32_t rn = s_run[t];
+    lo = int(rn & 0xFFFFu);
+    hi = int(rn >> 16);
+  } else {
+    lo = 0;
+    hi = M;
+    while (lo < hi) {  // first position with type >= t
+      int mid = (lo + hi) >> 1;
+      if (s_type[mid] < t) lo = mid + 1; else hi = mid;
+    }
+    hi = lo;
+    while (hi < M && s_type[hi] == t) ++hi;
   }
   const double a = double(est * 1000);
   int64_t best = INT64_MAX;
   int bj = -1;
-  for (int j = lo; j < M && s_type[j] == t; ++j) {
-    int64_t c = s_load[j] + floordiv_exact(a, s_speed[j], s_inv[j]);
-    if (c < best) { best = c; bj = j; }
+  // candidates four at a time (independent LDS reads), compared in index order
+  for (int j0 = lo; j0 < hi; j0 += 4) {
+    int64_t c[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int j = j0 + u < hi ? j0 + u : j0;
+      c[u] = s_load[j] + floordiv_exact(a, s_speed[j], s_inv[j]);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (j0 + u < hi && c[u] < best) { best = c[u]; bj = j0 + u; }
   }
   if (bj < 0) { route = -1; cost = INT64_MAX; return; }
   const int32_t bidx = s_idx[bj];

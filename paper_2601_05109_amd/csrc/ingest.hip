@@ -11,12 +11,18 @@ namespace {
 constexpr int kNodeThreads = 256;
 
 // First index i in [0, n] with a[i] >= key for non-decreasing a, found by
-// galloping from `guess` (exact in two loads when workflows have equal size).
-__device__ inline int64_t lower_bound_from(const int32_t* a, int64_t n, int64_t key,
-                                           int64_t guess) {
+// galloping from `guess`.  a[guess - 1] and a[guess] are read together, so an
+// exact guess (equal-sized workflows) costs one round trip.
+__device__ inline int64_t lower_bound_from(const int32_t* a, int64_t n, int64_t key, int64_t guess) {
+  guess = guess < 0 ? 0 : (guess > n ? n : guess);
+  const int32_t before = guess >= 1 && guess - 1 < n ? a[guess - 1] : INT32_MIN;
+  const int32_t at = guess < n ? a[guess] : INT32_MAX;
+  const bool ok_before = guess == 0 || int64_t(before) < key;
+  const bool ok_at = guess >= n || int64_t(at) >= key;
+  if (ok_before && ok_at) return guess;
   int64_t lo, hi;
-  if (guess >= n || int64_t(a[guess]) >= key) {
-    hi = guess < n ? guess : n;
+  if (!ok_before) {  // answer below guess
+    hi = guess - 1;
     int64_t step = 1;
     lo = hi - 1;
     while (lo >= 0 && int64_t(a[lo]) >= key) {
@@ -25,7 +31,7 @@ __device__ inline int64_t lower_bound_from(const int32_t* a, int64_t n, int64_t 
       step <<= 1;
     }
     lo = lo < 0 ? 0 : lo + 1;
-  } else {
+  } else {           // answer above guess
     lo = guess + 1;
     hi = lo;
     int64_t step = 1;
@@ -43,15 +49,59 @@ __device__ inline int64_t lower_bound_from(const int32_t* a, int64_t n, int64_t 
   return lo;
 }
 
-// Grid-stride over nodes, workflows and instances.  Workgroup 0 also sorts the
-// instance table by (type, index) so each future's candidates form one
-// contiguous run, and resets the control block of the next pass.  The bucket
-// counters of this pass's bucketed sort are cleared here, before the sweep.
+// Instance table sorted by (type, original index) and the run of each small
+// type; resets the next pass's control block (one workgroup).
+__device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl) {
+  const int64_t M = p.M;
+  reset_ctrl(next_ctrl);  // unused by this pass; ready for the next one
+  __shared__ int32_t s_type[NALAR_MAX_INSTANCES];
+  __shared__ int32_t s_sorted[NALAR_MAX_INSTANCES];
+  for (int i = threadIdx.x; i < M; i += kNodeThreads) s_type[i] = p.inst_type[i];
+  for (int t = threadIdx.x; t < kTypeDirect; t += kNodeThreads) it.run[t] = 0;
+  __syncthreads();
+  for (int i = threadIdx.x; i < M; i += kNodeThreads) {
+    const int32_t t = s_type[i];
+    int rank = 0;
+    for (int j = 0; j < M; ++j) {
+      const int32_t u = s_type[j];
+      rank += (u < t) | ((u == t) & (j < i));
+    }
+    const int32_t sp = p.inst_speed[i];
+    it.type[rank] = t;
+    it.idx[rank] = i;
+    it.load[rank] = p.inst_load[i];
+    it.speed[rank] = sp;
+    it.inv_speed[rank] = sp >= 1 ? 1.0 / double(sp) : 0.0;
+    it.pos_of[i] = rank;
+    s_sorted[rank] = t;
+  }
+  __syncthreads();
+  // run of sorted positions per small type: from where the type starts to
+  // where the next one does (or M)
+  for (int r = threadIdx.x; r < M; r += kNodeThreads) {
+    const int32_t t = s_sorted[r];
+    if (t >= 0 && t < kTypeDirect && (r == 0 || s_sorted[r - 1] != t)) {
+      int e = r + 1;
+      while (e < M && s_sorted[e] == t) ++e;
+      it.run[t] = uint32_t(r) | (uint32_t(e) << 16);
+    }
+  }
+}
+
+// Grid-stride over nodes, workflows and instances.  The last workgroup only
+// sorts the instance table by (type, index), so each future's candidates form
+// one contiguous run, and resets the control block of the next pass.  The
+// bucket counters of this pass's bucketed sort are cleared here, before the
+// sweep.
 __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl, Ctrl* next_ctrl,
                                                        ITab it, int32_t* wf_off, int contiguous,
-                                                       BucketArgs bk) {
+                                                       BucketArgs bk, int64_t large_cap) {
   const int64_t N = p.N, W = p.W, M = p.M;
-  const int64_t stride = int64_t(gridDim.x) * kNodeThreads;
+  if (blockIdx.x == gridDim.x - 1) {
+    instance_table(p, it, next_ctrl);
+    return;
+  }
+  const int64_t stride = int64_t(gridDim.x - 1) * kNodeThreads;
   const int64_t g0 = int64_t(blockIdx.x) * kNodeThreads + threadIdx.x;
   bool bad = false;
   for (int64_t v = g0; v < N; v += stride) {
@@ -81,7 +131,12 @@ __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl
     // if it is not, the pass fails with EINVAL and the offsets are never used)
     for (int64_t w = g0; w <= W; w += stride) {
       const int64_t guess = W > 0 ? (w * N) / W : 0;
-      wf_off[w] = int32_t(lower_bound_from(p.wf, N, w, guess));
+      const int64_t lo = lower_bound_from(p.wf, N, w, guess);
+      wf_off[w] = int32_t(lo);
+      if (w < W) {  // size of workflow w, for the sweep's choice of path
+        const int64_t hi = lower_bound_from(p.wf, N, w + 1, ((w + 1) * N) / W);
+        if (hi - lo > large_cap) add_agent(&ctrl->n_large, 1u);
+      }
     }
   }
   for (int64_t i = g0; i < bk.nb; i += stride) {  // empty buckets for the sweep
@@ -90,27 +145,6 @@ __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl
   }
   if (__ballot(bad) != 0 && lane_id() == 0) flag_status(ctrl, kStInval);
 
-  if (blockIdx.x == 0) {
-    reset_ctrl(next_ctrl);  // unused by this pass; ready for the next one
-    __shared__ int32_t s_type[NALAR_MAX_INSTANCES];
-    for (int i = threadIdx.x; i < M; i += kNodeThreads) s_type[i] = p.inst_type[i];
-    __syncthreads();
-    for (int i = threadIdx.x; i < M; i += kNodeThreads) {
-      const int32_t t = s_type[i];
-      int rank = 0;
-      for (int j = 0; j < M; ++j) {
-        const int32_t u = s_type[j];
-        rank += (u < t) | ((u == t) & (j < i));
-      }
-      const int32_t sp = p.inst_speed[i];
-      it.type[rank] = t;
-      it.idx[rank] = i;
-      it.load[rank] = p.inst_load[i];
-      it.speed[rank] = sp;
-      it.inv_speed[rank] = sp >= 1 ? 1.0 / double(sp) : 0.0;
-      it.pos_of[i] = rank;
-    }
-  }
 }
 
 int grid_for(int64_t n, int threads, int cap) {
@@ -123,11 +157,11 @@ int grid_for(int64_t n, int threads, int cap) {
 }  // namespace
 
 hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
-                        int32_t* wf_off, int contiguous, const BucketArgs& bk) {
+                        int32_t* wf_off, int contiguous, const BucketArgs& bk, int64_t large_cap) {
   int64_t n = p.N > p.W + 1 ? p.N : p.W + 1;
   if (n < bk.nb) n = bk.nb;
-  hipLaunchKernelGGL(k_nodes, dim3(grid_for(n, kNodeThreads, 4096)), dim3(kNodeThreads), 0, s, p,
-                     ctrl, next_ctrl, itab, wf_off, contiguous, bk);
+  hipLaunchKernelGGL(k_nodes, dim3(grid_for(n, kNodeThreads, 4096) + 1), dim3(kNodeThreads), 0, s, p,
+                     ctrl, next_ctrl, itab, wf_off, contiguous, bk, large_cap);
   return hipGetLastError();
 }
 

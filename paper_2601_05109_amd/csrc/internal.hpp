@@ -62,6 +62,7 @@ struct GroupArgs {
   uint32_t epoch;
   int32_t* pos_of_node;
   int32_t* wf_off;
+  int64_t large_cap;            // workflows above this size are counted in n_large
 };
 
 // Buckets of the bucketed slack sort (nb == 0: not used this pass).  Bucket of
@@ -99,7 +100,7 @@ struct SweepArgs {
 
 // ingest.hip
 hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
-                        int32_t* wf_off, int contiguous, const BucketArgs& bk);
+                        int32_t* wf_off, int contiguous, const BucketArgs& bk, int64_t large_cap);
 
 // sort.hip (mark(ctx, name) is called before each launch, for timing)
 hipError_t launch_reset(hipStream_t s, Ctrl* c);
@@ -116,6 +117,7 @@ struct SweepShape {
   int lds_cap;    // largest workflow handled in LDS
   size_t lds_bytes;
   int blocks;
+  int64_t large_cap;  // wave path: larger workflows need the workgroup pass
 };
 SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t lds_limit);
 hipError_t prepare_sweep_kernels(size_t lds_limit);

@@ -294,7 +294,7 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, Buck
   const int tid = threadIdx.x;
   const int g = blockIdx.x;
   Ctrl* ctrl = a.ctrl;
-  const uint32_t status = ctrl->status;
+  const uint32_t status = ctrl->status | ctrl->status_sweep;
   if (status) {
     if (g == 0 && tid == 0) publish_status(a.host, status, 0, 0, 0, 0);
     return;
@@ -362,7 +362,7 @@ __global__ __launch_bounds__(kSortThreads) void k_slack_hist(SortArgs a) {
   __shared__ uint32_t H[kMaxSortPasses][kRadixBuckets];
   __shared__ int64_t s_range[5];
   Ctrl* ctrl = a.ctrl;
-  const uint32_t status = ctrl->status;
+  const uint32_t status = ctrl->status | ctrl->status_sweep;
   if (status) {
     if (blockIdx.x == 0 && threadIdx.x == 0) publish_status(a.host, status, 0, 0, 0, 0);
     return;
@@ -383,7 +383,7 @@ __global__ __launch_bounds__(kSortThreads) void k_slack_hist(SortArgs a) {
 __global__ __launch_bounds__(kSortThreads) void k_slack_pass(SortArgs a, int pass) {
   __shared__ TileSmem<uint64_t> S;
   Ctrl* ctrl = a.ctrl;
-  if (ctrl->status) return;
+  if (ctrl->status | ctrl->status_sweep) return;
   const int npass = int(ctrl->sort_npass);
   if (pass >= npass) return;
   const int64_t R = ctrl->n_ready;
@@ -453,6 +453,14 @@ __global__ __launch_bounds__(kSortThreads) void k_group_finish(GroupArgs a) {
       if (int64_t(sorted_wf[mid]) < w) lo = mid + 1; else hi = mid;
     }
     a.wf_off[w] = int32_t(lo);
+    if (w < W) {  // size of workflow w, for the sweep's choice of path
+      int64_t e = lo, f = N;
+      while (e < f) {
+        const int64_t mid = (e + f) >> 1;
+        if (int64_t(sorted_wf[mid]) < w + 1) e = mid + 1; else f = mid;
+      }
+      if (e - lo > a.large_cap) add_agent(&a.ctrl->n_large, 1u);
+    }
   }
 }
 

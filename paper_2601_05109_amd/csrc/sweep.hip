@@ -68,11 +68,11 @@ __device__ inline int32_t checked_dep(const Layout& L, int32_t p, int64_t b, int
                                       Ctrl* ctrl) {
   const int32_t lp = local_of(L, p, b, n);
   if (lp < 0) {
-    flag_status(ctrl, kStInval);
+    flag_sweep(ctrl, kStInval);
     return -1;
   }
   if (lp == k) {
-    flag_status(ctrl, kStCycle);
+    flag_sweep(ctrl, kStCycle);
     return -1;
   }
   return lp;
@@ -194,6 +194,7 @@ struct ITabLds {
   int32_t* idx;
   int32_t* speed;
   int32_t* pos;
+  uint32_t* run;    // [kTypeDirect]
 };
 
 struct Acc {
@@ -205,22 +206,26 @@ struct Acc {
 __device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_t pos, int32_t type,
                                    int32_t loc, int64_t rem, int64_t est, int64_t dl, Acc& acc) {
   const int64_t slack = dl - rem;
+  // bucket slot first: the atomic's round trip overlaps the routing below
+  const BucketArgs& bk = a.bk;
+  uint32_t bkt = 0, slot = 0;
+  if (bk.nb > 0) {
+    const uint64_t d = slack > bk.lo ? uint64_t(slack) - uint64_t(bk.lo) : 0;
+    const uint64_t q = d >> bk.shift;
+    bkt = q < uint64_t(bk.nb) ? uint32_t(q) : uint32_t(bk.nb - 1);
+    slot = add_agent(bk.cnt + bkt, 1u);
+    add_agent(bk.group_cnt + bkt / kBucketGroup, 1u);
+  }
   int32_t route;
   int64_t cost;
   route_future(type, est, loc, int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load, it.speed,
-               it.inv, it.pos, route, cost);
+               it.inv, it.pos, it.run, route, cost);
   a.stg_slack[pos] = slack;
   a.stg_route[pos] = route;
   a.stg_cost[pos] = cost;
-  if (a.bk.nb > 0) {  // drop into its bucket for the bucketed sort
-    const BucketArgs& bk = a.bk;
-    const uint64_t d = slack > bk.lo ? uint64_t(slack) - uint64_t(bk.lo) : 0;
-    const uint64_t q = d >> bk.shift;
-    const uint32_t bkt = q < uint64_t(bk.nb) ? uint32_t(q) : uint32_t(bk.nb - 1);
-    const uint32_t s = add_agent(bk.cnt + bkt, 1u);
-    add_agent(bk.group_cnt + bkt / kBucketGroup, 1u);
-    if (s < uint32_t(kBucketCap)) {
-      BucketSlot* sl = bk.slot + int64_t(bkt) * kBucketCap + s;
+  if (bk.nb > 0) {  // the future in its bucket, for the bucketed sort
+    if (slot < uint32_t(kBucketCap)) {
+      BucketSlot* sl = bk.slot + int64_t(bkt) * kBucketCap + slot;
       sl->slack = slack;
       sl->cost = cost;
       sl->pos = int32_t(pos);
@@ -418,7 +423,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
     }
     __syncthreads();
   }
-  if (overflow) flag_status(ctrl, kStRange);
+  if (overflow) flag_sweep(ctrl, kStRange);
   if (fin) atomicAdd(&S.proc, __popc(fin));
   if (a.rem_out) {  // rem stayed in LDS during the levels; store it once
 #pragma unroll
@@ -426,7 +431,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
       if ((fin >> j) & 1u) a.rem_out[vv[j]] = mx[j * T + tid];
   }
   __syncthreads();
-  if (tid == 0 && S.proc != n) flag_status(ctrl, kStCycle);
+  if (tid == 0 && S.proc != n) flag_sweep(ctrl, kStCycle);
 
   // D: slack, route, staged at the future's position
 #pragma unroll
@@ -594,8 +599,8 @@ __device__ void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it
     int32_t* t = cur; cur = nxt; nxt = t;
     __syncthreads();
   }
-  if (overflow) flag_status(ctrl, kStRange);
-  if (tid == 0 && processed != n) flag_status(ctrl, kStCycle);
+  if (overflow) flag_sweep(ctrl, kStRange);
+  if (tid == 0 && processed != n) flag_sweep(ctrl, kStCycle);
 
   // slack, route, staged at the future's position
   for (int k = tid; k < n; k += T) {
@@ -609,6 +614,55 @@ __device__ void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it
 
 // ------------------------------------------------------------ wave workflow
 
+// Instance tables of at most kWaveItabMax entries get one LDS copy per wave:
+// the wave loads its entries into registers at kernel start and writes them
+// to its copy just before it first routes, so the load's latency hides behind
+// the sweep and no workgroup barrier is needed.
+constexpr int kWaveItabMax = 2 * kWave;
+
+struct ItabStage {
+  int64_t load[2];
+  double inv[2];
+  int32_t type[2], idx[2], speed[2], pos[2];
+  uint32_t run;
+  bool pending;
+};
+
+__device__ inline void itab_stage_load(ItabStage& st, const ITab& g, int M, int ln) {
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int i = ln + u * kWave;
+    if (i < M) {
+      st.load[u] = g.load[i];
+      st.inv[u] = g.inv_speed[i];
+      st.type[u] = g.type[i];
+      st.idx[u] = g.idx[i];
+      st.speed[u] = g.speed[i];
+      st.pos[u] = g.pos_of[i];
+    }
+  }
+  st.run = g.run[ln];  // kTypeDirect == kWave entries
+  st.pending = true;
+}
+
+__device__ inline void itab_stage_store(ItabStage& st, const ITabLds& it, int M, int ln) {
+  if (!st.pending) return;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int i = ln + u * kWave;
+    if (i < M) {
+      it.load[i] = st.load[u];
+      it.inv[i] = st.inv[u];
+      it.type[i] = st.type[u];
+      it.idx[i] = st.idx[u];
+      it.speed[i] = st.speed[u];
+      it.pos[i] = st.pos[u];
+    }
+  }
+  it.run[ln] = st.run;
+  st.pending = false;
+}
+
 // One wave sweeps a workflow of at most 64 * NPTW futures on its own LDS slice.
 // The LDS operations of one wave complete in program order, so no barrier is
 // needed: each read observes every earlier write and atomic of the same wave.
@@ -619,34 +673,36 @@ __device__ inline void wave_order() { __asm__ __volatile__("" ::: "memory"); }
 // LDS slice of one wave (cap futures).
 struct WaveSlice {
   int64_t* mx;      // running max of the consumers' rem, then rem
-  int64_t* ee;      // est' (0 when done)
   int32_t* cnt;     // consumers not yet finalised
-  uint32_t* pa;     // dependencies 0 and 1 (local, 16 bits each)
-  uint32_t* pb;     // dependency 2 | degree << 16 | heavy bit
   uint8_t* dn;      // done
   uint8_t* nr;      // some dependency not done
-  uint16_t* queue;  // futures whose consumers are all finalised, not yet taken
 };
 
-// Sweep of one workflow by one wave.  Instead of scanning for a level at a
-// time, the lane whose decrement brings a dependency's counter to zero goes on
-// with that dependency at once (further ones join a wave-shared queue), so a
-// chain of levels costs two LDS round trips per level.  Futures with many
-// dependencies are pushed by the whole wave.
+// Sweep of one workflow by one wave.  Lane l owns futures l, l+64, ... of the
+// workflow and keeps their estimate and (up to three) dependencies in
+// registers.  Each round, every owned future whose consumers are all finalised
+// (counter zero) is finalised: rem = est' + running max, pushed into its
+// dependencies' running max, whose counters drop by one.  Pushes return
+// nothing, so a round costs one LDS round trip (the counter and running-max
+// reads) however many futures it finalises.  Futures with more dependencies
+// are pushed by the whole wave from the dependency list.
 template <int NPTW>
 __device__ void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& it,
-                           const WaveSlice& W, int64_t b, int n, int64_t dl, Acc& acc) {
+                           const WaveSlice& W, int64_t b, int n, int64_t dl, Acc& acc,
+                           ItabStage& st) {
   const int ln = lane_id();
   Ctrl* ctrl = a.ctrl;
-  int32_t vv[NPTW], ty[NPTW], lc[NPTW];
-  uint32_t own = 0, ready = 0;
+  int32_t vv[NPTW], ty[NPTW], lc[NPTW], off[NPTW], deg[NPTW];
+  int64_t ee[NPTW];
+  uint32_t p01[NPTW], p2[NPTW];
+  uint32_t own = 0, ready = 0, heavy = 0;
 
   // A: attributes in one round trip; reset the state
-  int32_t off[NPTW], deg[NPTW];
 #pragma unroll
   for (int j = 0; j < NPTW; ++j) {
     const int k = j * kWave + ln;
-    vv[j] = 0; ty[j] = 0; lc[j] = -1; off[j] = 0; deg[j] = 0;
+    vv[j] = 0; ty[j] = 0; lc[j] = -1; off[j] = 0; deg[j] = 0; ee[j] = 0;
+    p01[j] = 0xFFFFFFFFu; p2[j] = kNoDep;
     if (k < n) {
       own |= 1u << j;
       const int32_t v = node_at(L, b + k);
@@ -656,7 +712,7 @@ __device__ void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& i
       deg[j] = a.p.dep_off[v + 1] - off[j];
       ty[j] = a.p.type[v];
       lc[j] = a.p.loc[v];
-      W.ee[k] = d ? 0 : a.p.est[v];
+      ee[j] = d ? 0 : a.p.est[v];
       W.cnt[k] = 0;
       W.mx[k] = 0;
       W.dn[k] = d;
@@ -665,7 +721,7 @@ __device__ void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& i
   }
   wave_order();
 
-  // B: out-degree counters, readiness, dependency lists into LDS
+  // B: out-degree counters, readiness, dependency lists into registers
 #pragma unroll
   for (int j = 0; j < NPTW; ++j) {
     if (ballot((own >> j) & 1u) == 0) continue;
@@ -684,11 +740,12 @@ __device__ void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& i
         blocked |= W.dn[lp] == 0;
       }
     }
-    if (mine) {
-      W.pa[k] = light ? (packed[0] | (packed[1] << 16)) : 0xFFFFFFFFu;
-      W.pb[k] = light ? (packed[2] | (uint32_t(deg[j]) << 16)) : (kHeavyBit | kNoDep);
-      if (light && blocked) W.nr[k] = 1;
+    if (light) {
+      p01[j] = packed[0] | (packed[1] << 16);
+      p2[j] = packed[2];
+      if (blocked) W.nr[k] = 1;
     }
+    if (mine && !light) heavy |= 1u << j;
     for (uint64_t hm = ballot(mine && !light); hm; hm &= hm - 1) {
       const int src = __builtin_ctzll(hm);
       const int kh = j * kWave + src;
@@ -710,130 +767,105 @@ __device__ void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& i
   }
   wave_order();
 
-  // ready flags (staged by position for the sort's first pass); sinks queued
-  int tail = 0;
+  // ready flags (staged by position for the tiled sort's first pass)
 #pragma unroll
   for (int j = 0; j < NPTW; ++j) {
-    const int k = j * kWave + ln;
-    const bool mine = (own >> j) & 1u;
-    if (mine) {
+    if ((own >> j) & 1u) {
+      const int k = j * kWave + ln;
       const bool rd = W.dn[k] == 0 && W.nr[k] == 0;
       if (rd) ready |= 1u << j;
       a.stg_ready[b + k] = rd ? 1 : 0;
     }
-    const bool sink = mine && W.cnt[k] == 0;
-    const uint64_t m = ballot(sink);
-    if (sink) W.queue[tail + int(lanes_below(m))] = uint16_t(k);
-    tail += int(__popcll(m));
   }
   wave_order();
 
-  // C: walk up the DAG
+  // C: rounds of finalisation
   bool overflow = false;
-  int head = 0;
-  int cur = -1;
   int processed = 0;
+  uint32_t fin = 0;
+  int64_t rr[NPTW];
+#pragma unroll
+  for (int j = 0; j < NPTW; ++j) rr[j] = 0;
   for (;;) {
-    // idle lanes take queued futures
-    const uint64_t idle = ballot(cur < 0);
-    const int avail = tail - head;
-    if (avail > 0 && idle != 0) {
-      const int rank = int(lanes_below(idle));
-      if (cur < 0 && rank < avail) cur = W.queue[head + rank];
-      const int took = int(__popcll(idle)) < avail ? int(__popcll(idle)) : avail;
-      head += took;
-    }
-    if (ballot(cur >= 0) == 0) break;
-    // the future's dependency slots, est' and running max in one LDS round trip
-    const int cs = cur >= 0 ? cur : 0;
-    const uint32_t pa0 = W.pa[cs];
-    const uint32_t pb0 = W.pb[cs];
-    const int64_t ec = W.ee[cs];
-    const int64_t mc = W.mx[cs];
-    const uint32_t pa = cur >= 0 ? pa0 : 0xFFFFFFFFu;
-    const uint32_t pb = cur >= 0 ? pb0 : kNoDep;
-    const bool hv = cur >= 0 && (pb & kHeavyBit) != 0;
-    int next = -1, extra0 = -1, extra1 = -1;
-    if (cur >= 0 && !hv) {
-      const int64_t r = clamp_rem(ec + mc, overflow);
-      W.mx[cur] = r;
-      ++processed;
-      // all pushes first, then look at the returned counts (one round trip)
-      int lp[kPmax], old[kPmax];
+    uint32_t act = 0;
+    int64_t mv[NPTW];
 #pragma unroll
-      for (int q = 0; q < kPmax; ++q) {
-        lp[q] = dep_at(pa, pb, q);
-        old[q] = 0;
-        if (lp[q] >= 0) {
-          atomicMax(reinterpret_cast<long long*>(&W.mx[lp[q]]), (long long)r);
-          old[q] = atomicSub(&W.cnt[lp[q]], 1);
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < kPmax; ++q) {
-        if (lp[q] >= 0 && old[q] == 1) {
-          if (next < 0) next = lp[q];
-          else if (extra0 < 0) extra0 = lp[q];
-          else extra1 = lp[q];
+    for (int j = 0; j < NPTW; ++j) {
+      mv[j] = 0;
+      if (((own & ~fin) >> j) & 1u) {
+        const int k = j * kWave + ln;
+        const int32_t c = W.cnt[k];
+        const int64_t m = W.mx[k];
+        if (c == 0) {
+          act |= 1u << j;
+          mv[j] = m;
         }
       }
     }
-    // whole-wave push of futures with many dependencies
-    for (uint64_t hm = ballot(hv); hm; hm &= hm - 1) {
-      const int src = __builtin_ctzll(hm);
-      const int kh = readlane_i32(cur, src);
-      const int64_t r = clamp_rem(W.ee[kh] + W.mx[kh], overflow);
-      const int32_t v = node_at(L, b + kh);
-      const int o = a.p.dep_off[v];
-      const int d = a.p.dep_off[v + 1] - o;
-      if (ln == 0) {
-        W.mx[kh] = r;
+    if (ballot(act != 0) == 0) break;
+#pragma unroll
+    for (int j = 0; j < NPTW; ++j) {
+      if ((act >> j) & 1u) {
+        const int k = j * kWave + ln;
+        const int64_t r = clamp_rem(ee[j] + mv[j], overflow);
+        rr[j] = r;
         ++processed;
-      }
-      for (int e0 = 0; e0 < d; e0 += kWave) {
-        const int e = e0 + ln;
-        bool app = false;
-        int32_t lp = -1;
-        if (e < d) {
-          lp = local_of(L, a.p.dep_idx[o + e], b, n);
-          if (lp >= 0 && lp != kh) {
-            atomicMax(reinterpret_cast<long long*>(&W.mx[lp]), (long long)r);
-            app = atomicSub(&W.cnt[lp], 1) == 1;
+        if ((heavy >> j) & 1u) {
+          W.mx[k] = r;  // read by the whole wave below
+        } else {
+#pragma unroll
+          for (int q = 0; q < kPmax; ++q) {
+            const int lp = dep_at(p01[j], p2[j], q);
+            if (lp >= 0) {
+              atomicMax(reinterpret_cast<long long*>(&W.mx[lp]), (long long)r);
+              atomicSub(&W.cnt[lp], 1);
+            }
           }
         }
-        const uint64_t m = ballot(app);
-        if (app) W.queue[tail + int(lanes_below(m))] = uint16_t(lp);
-        tail += int(__popcll(m));
       }
     }
-    if (hv) cur = -1;
-    // futures beyond the first one a lane released join the queue
-    {
-      const uint64_t m0 = ballot(extra0 >= 0);
-      if (extra0 >= 0) W.queue[tail + int(lanes_below(m0))] = uint16_t(extra0);
-      tail += int(__popcll(m0));
-      const uint64_t m1 = ballot(extra1 >= 0);
-      if (extra1 >= 0) W.queue[tail + int(lanes_below(m1))] = uint16_t(extra1);
-      tail += int(__popcll(m1));
+    fin |= act;
+    // futures with many dependencies: the whole wave pushes each one
+    const uint32_t hact = act & heavy;
+    for (uint64_t hs = ballot(hact != 0); hs; hs &= hs - 1) {
+      const int src = __builtin_ctzll(hs);
+      for (uint32_t hj = uint32_t(readlane_i32(int(hact), src)); hj; hj &= hj - 1) {
+        const int kh = __builtin_ctz(hj) * kWave + src;
+        const int64_t r = W.mx[kh];
+        const int32_t vh = node_at(L, b + kh);
+        const int o = a.p.dep_off[vh];
+        const int d = a.p.dep_off[vh + 1] - o;
+        for (int e0 = 0; e0 < d; e0 += kWave) {
+          const int e = e0 + ln;
+          if (e < d) {
+            const int32_t lp = local_of(L, a.p.dep_idx[o + e], b, n);
+            if (lp >= 0 && lp != kh) {
+              atomicMax(reinterpret_cast<long long*>(&W.mx[lp]), (long long)r);
+              atomicSub(&W.cnt[lp], 1);
+            }
+          }
+        }
+      }
     }
-    if (!hv) cur = next;
     wave_order();
   }
-  if (overflow) flag_status(ctrl, kStRange);
-  if (a.rem_out) {  // rem stayed in LDS during the walk; store it once
+  if (overflow) flag_sweep(ctrl, kStRange);
+  if (a.rem_out) {
 #pragma unroll
     for (int j = 0; j < NPTW; ++j)
-      if ((own >> j) & 1u) a.rem_out[vv[j]] = W.mx[j * kWave + ln];
+      if ((own >> j) & 1u) a.rem_out[vv[j]] = rr[j];
   }
   const int64_t done_cnt = wave_sum_i64(processed);
-  if (ln == 0 && done_cnt != n) flag_status(ctrl, kStCycle);
+  if (ln == 0 && done_cnt != n) flag_sweep(ctrl, kStCycle);
 
   // D: slack, route, staged at the future's position
+  itab_stage_store(st, it, int(a.p.M), ln);
+  wave_order();
 #pragma unroll
   for (int j = 0; j < NPTW; ++j) {
     if ((ready >> j) & 1u) {
       const int k = j * kWave + ln;
-      write_ready(a, it, b + k, ty[j], lc[j], W.mx[k], W.ee[k], dl, acc);
+      write_ready(a, it, b + k, ty[j], lc[j], rr[j], ee[j], dl, acc);
     }
   }
   wave_order();
@@ -860,6 +892,7 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
   it.idx = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
   it.speed = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
   it.pos = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  it.run = reinterpret_cast<uint32_t*>(sp); sp += 4 * size_t(kTypeDirect);
   int32_t* cnt = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(lds_cap);
   uint8_t* dn = sp; sp += lds_cap;
   uint8_t* nr = sp;
@@ -872,6 +905,7 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
     it.speed[i] = a.itab.speed[i];
     it.pos[i] = a.itab.pos_of[i];
   }
+  for (int t = tid; t < kTypeDirect; t += blockDim.x) it.run[t] = a.itab.run[t];
 
   const Layout L{a.node_of_pos, a.pos_of_node, a.p.N};
   Acc acc;
@@ -913,85 +947,115 @@ constexpr int kWaveNpt = 8;                  // futures per lane in the wave pat
 constexpr int kWaveCap = kWave * kWaveNpt;     // at most 512 futures per wave
 constexpr int kWaveBlock = 256;                // four independent waves per workgroup
 constexpr int kWavesPerBlock = kWaveBlock / kWave;
-constexpr size_t kWaveSliceBytesPerFuture = 8 + 8 + 4 + 4 + 4 + 1 + 1 + 2;
+constexpr size_t kWaveSliceBytesPerFuture = 8 + 4 + 1 + 1;
 
-// Small workflows: one wave each, no workgroup barriers.  Workflows larger than
-// a wave's slice (wcap futures) are swept afterwards by whole workgroups with
-// HBM state.
-__global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap) {
-  Ctrl* ctrl = a.ctrl;
-  if (ld_relaxed_agent(&ctrl->status) != 0) return;
-  extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ Shared S;
-  const int M = int(a.p.M);
-  const int tid = threadIdx.x;
-  const int wv = tid / kWave;
-  const size_t nw = size_t(kWavesPerBlock) * size_t(wcap);
-  unsigned char* sp = smem;
+// LDS of the instance tables of one wave workgroup.
+__host__ __device__ inline size_t itab_lds_wave(int64_t M) {
+  const size_t one = 32 * size_t(M) + 4 * kTypeDirect;
+  return M <= kWaveItabMax ? one * kWavesPerBlock : one;
+}
+
+__device__ inline ITabLds carve_itab(unsigned char* sp, int M) {
   ITabLds it;
-  WaveSlice Wv;
   it.load = reinterpret_cast<int64_t*>(sp); sp += 8 * size_t(M);
   it.inv = reinterpret_cast<double*>(sp); sp += 8 * size_t(M);
-  Wv.mx = reinterpret_cast<int64_t*>(sp) + size_t(wv) * wcap; sp += 8 * nw;
-  Wv.ee = reinterpret_cast<int64_t*>(sp) + size_t(wv) * wcap; sp += 8 * nw;
   it.type = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
   it.idx = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
   it.speed = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
   it.pos = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  it.run = reinterpret_cast<uint32_t*>(sp);
+  return it;
+}
+
+// Small workflows: one wave each, no workgroup barrier on the way.  Each wave
+// fetches its first workflow's bounds and deadline together with the status
+// word, so the sweep starts after one round trip.  Workflows larger than a
+// wave's slice (wcap futures; k_nodes counts them) are swept afterwards by
+// whole workgroups with HBM state.  Each wave folds its slack range and ready
+// count into one of the control block's partial slots.
+template <int NPTW>
+__global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ Shared S;
+  Ctrl* ctrl = a.ctrl;
+  const int M = int(a.p.M);
+  const int tid = threadIdx.x;
+  const int wv = tid / kWave;
+  const int ln = lane_id();
+  const bool per_wave = M <= kWaveItabMax;
+  const int64_t gw = int64_t(blockIdx.x) * kWavesPerBlock + wv;
+  const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
+
+  // one round trip: validation status, large-workflow count, first workflow,
+  // this wave's instance table entries
+  const uint32_t status = ld_relaxed_agent(&ctrl->status);
+  const uint32_t n_large = ld_relaxed_agent(&ctrl->n_large);
+  int64_t b0 = 0, dl0 = 0;
+  int n0 = 0;
+  if (gw < a.p.W) {
+    b0 = a.wf_off[gw];
+    n0 = a.wf_off[gw + 1] - int32_t(b0);
+    dl0 = a.p.deadline[gw] - a.p.now;
+  }
+  ItabStage st;
+  st.pending = false;
+  if (per_wave) itab_stage_load(st, a.itab, M, ln);
+
+  const size_t nw = size_t(kWavesPerBlock) * size_t(wcap);
+  const size_t itab_one = 32 * size_t(M) + 4 * kTypeDirect;
+  unsigned char* sp = smem;
+  const ITabLds it = carve_itab(sp + (per_wave ? size_t(wv) * itab_one : 0), M);
+  sp += itab_lds_wave(M);
+  WaveSlice Wv;
+  Wv.mx = reinterpret_cast<int64_t*>(sp) + size_t(wv) * wcap; sp += 8 * nw;
   Wv.cnt = reinterpret_cast<int32_t*>(sp) + size_t(wv) * wcap; sp += 4 * nw;
-  Wv.pa = reinterpret_cast<uint32_t*>(sp) + size_t(wv) * wcap; sp += 4 * nw;
-  Wv.pb = reinterpret_cast<uint32_t*>(sp) + size_t(wv) * wcap; sp += 4 * nw;
-  Wv.queue = reinterpret_cast<uint16_t*>(sp) + size_t(wv) * wcap; sp += 2 * nw;
   Wv.dn = sp + size_t(wv) * wcap; sp += nw;
   Wv.nr = sp + size_t(wv) * wcap;
-  for (int i = tid; i < M; i += kWaveBlock) {
-    it.load[i] = a.itab.load[i];
-    it.inv[i] = a.itab.inv_speed[i];
-    it.type[i] = a.itab.type[i];
-    it.idx[i] = a.itab.idx[i];
-    it.speed[i] = a.itab.speed[i];
-    it.pos[i] = a.itab.pos_of[i];
+  if (!per_wave) {  // one shared copy (every thread reaches this barrier)
+    for (int i = tid; i < M; i += kWaveBlock) {
+      it.load[i] = a.itab.load[i];
+      it.inv[i] = a.itab.inv_speed[i];
+      it.type[i] = a.itab.type[i];
+      it.idx[i] = a.itab.idx[i];
+      it.speed[i] = a.itab.speed[i];
+      it.pos[i] = a.itab.pos_of[i];
+    }
+    for (int t = tid; t < kTypeDirect; t += kWaveBlock) it.run[t] = a.itab.run[t];
+    __syncthreads();
   }
-  __syncthreads();
+  // the validation status cannot change during this kernel (the sweep reports
+  // into its own word), so every wave of every workgroup leaves together
+  if (status != 0) return;
 
   const Layout L{a.node_of_pos, a.pos_of_node, a.p.N};
   Acc acc;
-  const int64_t gw = int64_t(blockIdx.x) * kWavesPerBlock + wv;
-  const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
   if (!a.force_global) {
     for (int64_t w = gw; w < a.p.W; w += nwaves) {
-      const int64_t b = a.wf_off[w];
-      const int n = a.wf_off[w + 1] - int32_t(b);
+      const int64_t b = w == gw ? b0 : a.wf_off[w];
+      const int n = w == gw ? n0 : a.wf_off[w + 1] - int32_t(b);
       if (n <= 0 || n > wcap) continue;
-      sweep_wave<kWaveNpt>(a, L, it, Wv, b, n, a.p.deadline[w] - a.p.now, acc);
+      sweep_wave<NPTW>(a, L, it, Wv, b, n, w == gw ? dl0 : a.p.deadline[w] - a.p.now, acc, st);
     }
   }
-  __syncthreads();
-  for (int64_t w = blockIdx.x; w < a.p.W; w += gridDim.x) {
-    const int64_t b = a.wf_off[w];
-    const int n = a.wf_off[w + 1] - int32_t(b);
-    if (n <= 0 || (n <= wcap && !a.force_global)) continue;
-    sweep_hbm<kWaveBlock>(a, L, it, S, int(w), b, n, a.p.deadline[w] - a.p.now, acc);
+  if (n_large > 0 || a.force_global) {  // the same for the whole workgroup
+    itab_stage_store(st, it, M, ln);
+    __syncthreads();
+    for (int64_t w = blockIdx.x; w < a.p.W; w += gridDim.x) {
+      const int64_t b = a.wf_off[w];
+      const int n = a.wf_off[w + 1] - int32_t(b);
+      if (n <= 0 || (n <= wcap && !a.force_global)) continue;
+      sweep_hbm<kWaveBlock>(a, L, it, S, int(w), b, n, a.p.deadline[w] - a.p.now, acc);
+    }
   }
 
   const int64_t mn = wave_min_i64(acc.tmin);
   const int64_t mxv = wave_max_i64(acc.tmax);
   const int64_t rd = wave_sum_i64(acc.tready);
-  if (lane_id() == 0) { S.red[0][wv] = mn; S.red[1][wv] = mxv; S.red[2][wv] = rd; }
-  __syncthreads();
-  if (tid == 0) {
-    int64_t a0 = INT64_MAX, a1 = INT64_MIN, a2 = 0;
-    for (int x = 0; x < kWavesPerBlock; ++x) {
-      a0 = S.red[0][x] < a0 ? S.red[0][x] : a0;
-      a1 = S.red[1][x] > a1 ? S.red[1][x] : a1;
-      a2 += S.red[2][x];
-    }
-    if (a2 > 0) {
-      const int slot = blockIdx.x & (kParts - 1);
-      __hip_atomic_fetch_min(&ctrl->part_min[slot], a0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_fetch_max(&ctrl->part_max[slot], a1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      add_agent(&ctrl->part_cnt[slot], a2);
-    }
+  if (ln == 0 && rd > 0) {
+    const int slot = int(gw & (kParts - 1));
+    __hip_atomic_fetch_min(&ctrl->part_min[slot], mn, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_fetch_max(&ctrl->part_max[slot], mxv, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    add_agent(&ctrl->part_cnt[slot], rd);
   }
 }
 
@@ -1002,15 +1066,16 @@ constexpr int kBlockNpt = 5;
 
 SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t lds_limit) {
   const int64_t avg = W > 0 ? (N + W - 1) / W : 0;
-  const size_t itab = 32 * size_t(M);
+  const size_t itab = 32 * size_t(M) + 4 * kTypeDirect;
   SweepShape s;
   if (avg <= kWaveCap) {  // one wave per workflow
     int64_t wcap = 64;       // room for workflows up to twice the average size
     while (wcap < 2 * avg && wcap < kWaveCap) wcap *= 2;
     s.threads = kWaveBlock;
-    s.npt = kWaveNpt;
+    s.npt = int(wcap / kWave);
     s.lds_cap = int(wcap);
-    s.lds_bytes = itab + kWaveSliceBytesPerFuture * size_t(kWavesPerBlock) * size_t(wcap) + 16;
+    s.lds_bytes = itab_lds_wave(M) + kWaveSliceBytesPerFuture * size_t(kWavesPerBlock) * size_t(wcap) + 16;
+    s.large_cap = wcap;
     int64_t blocks = (W + kWavesPerBlock - 1) / kWavesPerBlock;
     const int64_t most = int64_t(device_cus) * 8;
     if (blocks > most) blocks = most;
@@ -1024,6 +1089,7 @@ SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t ld
   if (cap > int64_t(kBlockT) * kBlockNpt) cap = int64_t(kBlockT) * kBlockNpt;
   s.lds_cap = int(cap);
   s.lds_bytes = itab + 14 * size_t(cap) + 16;
+  s.large_cap = INT64_MAX;
   int64_t blocks = int64_t(device_cus) * 2;
   if (blocks > W) blocks = W;
   s.blocks = int(blocks < 1 ? 1 : blocks);
@@ -1035,15 +1101,35 @@ hipError_t prepare_sweep_kernels(size_t lds_limit) {
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sweep<kBlockT, kBlockNpt>),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(dyn));
   if (e != hipSuccess) return e;
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sweep_wave),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, int(dyn));
+  for (const void* k : {reinterpret_cast<const void*>(&k_sweep_wave<1>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<2>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<4>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<8>)}) {
+    e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, int(dyn));
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const SweepShape& sh) {
-  if (sh.threads == kWaveBlock)
-    hipLaunchKernelGGL(k_sweep_wave, dim3(sh.blocks), dim3(kWaveBlock), sh.lds_bytes, s, a,
-                       sh.lds_cap);
-  else
+  if (sh.threads == kWaveBlock) {
+    // futures per lane = slice capacity / 64 (a power of two up to kWaveNpt)
+    switch (sh.npt) {
+      case 1:
+        hipLaunchKernelGGL(k_sweep_wave<1>, dim3(sh.blocks), dim3(kWaveBlock), sh.lds_bytes, s, a, sh.lds_cap);
+        break;
+      case 2:
+        hipLaunchKernelGGL(k_sweep_wave<2>, dim3(sh.blocks), dim3(kWaveBlock), sh.lds_bytes, s, a, sh.lds_cap);
+        break;
+      case 4:
+        hipLaunchKernelGGL(k_sweep_wave<4>, dim3(sh.blocks), dim3(kWaveBlock), sh.lds_bytes, s, a, sh.lds_cap);
+        break;
+      default:
+        hipLaunchKernelGGL(k_sweep_wave<kWaveNpt>, dim3(sh.blocks), dim3(kWaveBlock), sh.lds_bytes, s, a,
+                           sh.lds_cap);
+        break;
+    }
+  } else
     hipLaunchKernelGGL((k_sweep<kBlockT, kBlockNpt>), dim3(sh.blocks), dim3(kBlockT), sh.lds_bytes, s,
                        a, sh.lds_cap);
   return hipGetLastError();
