@@ -61,7 +61,6 @@ struct Arena {
   uint8_t* g_nr = nullptr;
   int32_t* g_front[2] = {nullptr, nullptr};
   uint32_t* bcnt = nullptr;
-  uint32_t* bgroup = nullptr;
   BucketSlot* bslot = nullptr;
   int64_t capN = -1, capW = -1, capB = -1;
 };
@@ -145,7 +144,6 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B) {
   a.g_nr = reinterpret_cast<uint8_t*>(take(size_t(n1)));
   const int64_t b1 = B > 0 ? B : 0;
   a.bcnt = reinterpret_cast<uint32_t*>(take(4 * size_t(b1 + 1)));
-  a.bgroup = reinterpret_cast<uint32_t*>(take(4 * size_t(b1 / kBucketGroup + 1)));
   a.bslot = reinterpret_cast<BucketSlot*>(take(sizeof(BucketSlot) * size_t(b1) * kBucketCap));
   off = align_up(off, 256);
   a.lookback_off = off;
@@ -359,7 +357,6 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   if (rc != NALAR_OK) return rc;
   Arena& A = h->ar;
   bk.cnt = A.bcnt;
-  bk.group_cnt = A.bgroup;
   bk.slot = A.bslot;
   hipStream_t s = h->stream;
   const int cur = int(h->passes & 1);

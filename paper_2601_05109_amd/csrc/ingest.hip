@@ -139,10 +139,7 @@ __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl
       }
     }
   }
-  for (int64_t i = g0; i < bk.nb; i += stride) {  // empty buckets for the sweep
-    bk.cnt[i] = 0;
-    if (i < bk.nb / kBucketGroup) bk.group_cnt[i] = 0;
-  }
+  for (int64_t i = g0; i < bk.nb; i += stride) bk.cnt[i] = 0;  // empty buckets for the sweep
   if (__ballot(bad) != 0 && lane_id() == 0) flag_status(ctrl, kStInval);
 
 }

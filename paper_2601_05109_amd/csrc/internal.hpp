@@ -71,8 +71,7 @@ struct BucketArgs {
   int64_t lo;
   int32_t shift;
   int32_t nb;
-  uint32_t* cnt;                // [nb] futures dropped into each bucket
-  uint32_t* group_cnt;          // [nb / kBucketGroup] the same per group of buckets
+  uint32_t* cnt;                // [nb] futures dropped into each bucket (16-byte aligned)
   BucketSlot* slot;             // [nb * kBucketCap]
 };
 

@@ -308,9 +308,13 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, Buck
   }
   if (g == 0 && tid == 0) publish_status(a.host, 0, R, int(s_range[3]), s_range[0], s_range[4]);
 
-  // futures in earlier groups
+  // futures in earlier groups: the counts of buckets [0, 16 g), four at a time
   uint32_t part = 0;
-  for (int i = tid; i < g; i += kBucketThreads) part += bk.group_cnt[i];
+  const uint4* cnt4 = reinterpret_cast<const uint4*>(bk.cnt);
+  for (int i = tid; i < g * (kBucketGroup / 4); i += kBucketThreads) {
+    const uint4 c = cnt4[i];
+    part += c.x + c.y + c.z + c.w;
+  }
   part = uint32_t(wave_sum_i64(int64_t(part)));
   if (lane_id() == 0) s_red[tid / kWave] = part;
   if (tid < kWave) {  // bucket offsets inside the group (wave 0)

@@ -203,18 +203,35 @@ struct Acc {
   int64_t tready = 0;
 };
 
+// Bucket of a slack under this pass's bucket boundaries, and a slot in it
+// (one returning atomic; claim early so that its latency overlaps other work).
+__device__ inline uint32_t bucket_of(const BucketArgs& bk, int64_t slack) {
+  const uint64_t d = slack > bk.lo ? uint64_t(slack) - uint64_t(bk.lo) : 0;
+  const uint64_t q = d >> bk.shift;
+  return q < uint64_t(bk.nb) ? uint32_t(q) : uint32_t(bk.nb - 1);
+}
+
+__device__ inline void bucket_put(const SweepArgs& a, uint32_t bkt, uint32_t slot, int64_t slack,
+                                  int64_t pos, int32_t route, int64_t cost) {
+  if (slot < uint32_t(kBucketCap)) {
+    BucketSlot* sl = a.bk.slot + int64_t(bkt) * kBucketCap + slot;
+    sl->slack = slack;
+    sl->cost = cost;
+    sl->pos = int32_t(pos);
+    sl->route = route;
+  } else {
+    st_relaxed_agent(&a.ctrl->bucket_overflow, 1u);
+  }
+}
+
 __device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_t pos, int32_t type,
                                    int32_t loc, int64_t rem, int64_t est, int64_t dl, Acc& acc) {
   const int64_t slack = dl - rem;
-  // bucket slot first: the atomic's round trip overlaps the routing below
   const BucketArgs& bk = a.bk;
   uint32_t bkt = 0, slot = 0;
   if (bk.nb > 0) {
-    const uint64_t d = slack > bk.lo ? uint64_t(slack) - uint64_t(bk.lo) : 0;
-    const uint64_t q = d >> bk.shift;
-    bkt = q < uint64_t(bk.nb) ? uint32_t(q) : uint32_t(bk.nb - 1);
+    bkt = bucket_of(bk, slack);
     slot = add_agent(bk.cnt + bkt, 1u);
-    add_agent(bk.group_cnt + bkt / kBucketGroup, 1u);
   }
   int32_t route;
   int64_t cost;
@@ -223,17 +240,7 @@ __device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_
   a.stg_slack[pos] = slack;
   a.stg_route[pos] = route;
   a.stg_cost[pos] = cost;
-  if (bk.nb > 0) {  // the future in its bucket, for the bucketed sort
-    if (slot < uint32_t(kBucketCap)) {
-      BucketSlot* sl = bk.slot + int64_t(bkt) * kBucketCap + slot;
-      sl->slack = slack;
-      sl->cost = cost;
-      sl->pos = int32_t(pos);
-      sl->route = route;
-    } else {
-      st_relaxed_agent(&a.ctrl->bucket_overflow, 1u);
-    }
-  }
+  if (bk.nb > 0) bucket_put(a, bkt, slot, slack, pos, route, cost);
   acc.tmin = slack < acc.tmin ? slack : acc.tmin;
   acc.tmax = slack > acc.tmax ? slack : acc.tmax;
   acc.tready += 1;
@@ -678,6 +685,84 @@ struct WaveSlice {
   uint8_t* nr;      // some dependency not done
 };
 
+// Rounds of the wave sweep: every owned future whose consumers are all
+// finalised (counter zero) is finalised, rem = est' + running max, and pushed
+// into its dependencies.  kHeavy adds whole-wave pushes for futures with more
+// than kPmax dependencies, read from the dependency list in global memory.
+template <int NPTW, bool kHeavy>
+__device__ __attribute__((always_inline)) inline void rounds(
+    const SweepArgs& a, const Layout& L, const WaveSlice& W, int64_t b, int n, uint32_t own,
+    uint32_t heavy, const int64_t* ee, const uint32_t* p01, const uint32_t* p2, int64_t* rr,
+    int& processed, bool& overflow) {
+  const int ln = lane_id();
+  uint32_t fin = 0;
+#pragma unroll
+  for (int j = 0; j < NPTW; ++j) rr[j] = 0;
+  for (;;) {
+    uint32_t act = 0;
+    int64_t mv[NPTW];
+#pragma unroll
+    for (int j = 0; j < NPTW; ++j) {
+      mv[j] = 0;
+      if (((own & ~fin) >> j) & 1u) {  // counter and running max in one round trip
+        const int k = j * kWave + ln;
+        const int32_t c = W.cnt[k];
+        const int64_t m = W.mx[k];
+        act |= uint32_t(c == 0) << j;
+        mv[j] = m;
+      }
+    }
+    if (ballot(act != 0) == 0) break;
+#pragma unroll
+    for (int j = 0; j < NPTW; ++j) {
+      if ((act >> j) & 1u) {
+        const int k = j * kWave + ln;
+        const int64_t r = clamp_rem(ee[j] + mv[j], overflow);
+        rr[j] = r;
+        ++processed;
+        if ((heavy >> j) & 1u) {
+          W.mx[k] = r;  // read by the whole wave below
+        } else {
+#pragma unroll
+          for (int q = 0; q < kPmax; ++q) {
+            const int lp = dep_at(p01[j], p2[j], q);
+            if (lp >= 0) {
+              atomicMax(reinterpret_cast<long long*>(&W.mx[lp]), (long long)r);
+              atomicSub(&W.cnt[lp], 1);
+            }
+          }
+        }
+      }
+    }
+    fin |= act;
+    // futures with many dependencies: the whole wave pushes each one
+    if (kHeavy) {
+      const uint32_t hact = act & heavy;
+      for (uint64_t hs = ballot(hact != 0); hs; hs &= hs - 1) {
+        const int src = __builtin_ctzll(hs);
+        for (uint32_t hj = uint32_t(readlane_i32(int(hact), src)); hj; hj &= hj - 1) {
+          const int kh = __builtin_ctz(hj) * kWave + src;
+          const int64_t r = W.mx[kh];
+          const int32_t vh = node_at(L, b + kh);
+          const int o = a.p.dep_off[vh];
+          const int d = a.p.dep_off[vh + 1] - o;
+          for (int e0 = 0; e0 < d; e0 += kWave) {
+            const int e = e0 + ln;
+            if (e < d) {
+              const int32_t lp = local_of(L, a.p.dep_idx[o + e], b, n);
+              if (lp >= 0 && lp != kh) {
+                atomicMax(reinterpret_cast<long long*>(&W.mx[lp]), (long long)r);
+                atomicSub(&W.cnt[lp], 1);
+              }
+            }
+          }
+        }
+      }
+    }
+    wave_order();
+  }
+}
+
 // Sweep of one workflow by one wave.  Lane l owns futures l, l+64, ... of the
 // workflow and keeps their estimate and (up to three) dependencies in
 // registers.  Each round, every owned future whose consumers are all finalised
@@ -767,105 +852,76 @@ __device__ void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& i
   }
   wave_order();
 
-  // ready flags (staged by position for the tiled sort's first pass)
+  // the instance table's LDS copy, now that its loads have long returned and
+  // no store is in flight (a wait here costs nothing)
+  itab_stage_store(st, it, int(a.p.M), ln);
+
+  // readiness (stored after the rounds: no store may be in flight during
+  // them, or every round would wait for it)
 #pragma unroll
   for (int j = 0; j < NPTW; ++j) {
     if ((own >> j) & 1u) {
       const int k = j * kWave + ln;
-      const bool rd = W.dn[k] == 0 && W.nr[k] == 0;
-      if (rd) ready |= 1u << j;
-      a.stg_ready[b + k] = rd ? 1 : 0;
+      if (W.dn[k] == 0 && W.nr[k] == 0) ready |= 1u << j;
     }
   }
   wave_order();
 
-  // C: rounds of finalisation
+  // C: rounds of finalisation (the variant without futures of many
+  // dependencies touches no global memory inside its loop, so nothing there
+  // waits on outstanding loads or stores)
   bool overflow = false;
   int processed = 0;
-  uint32_t fin = 0;
   int64_t rr[NPTW];
-#pragma unroll
-  for (int j = 0; j < NPTW; ++j) rr[j] = 0;
-  for (;;) {
-    uint32_t act = 0;
-    int64_t mv[NPTW];
-#pragma unroll
-    for (int j = 0; j < NPTW; ++j) {
-      mv[j] = 0;
-      if (((own & ~fin) >> j) & 1u) {
-        const int k = j * kWave + ln;
-        const int32_t c = W.cnt[k];
-        const int64_t m = W.mx[k];
-        if (c == 0) {
-          act |= 1u << j;
-          mv[j] = m;
-        }
-      }
-    }
-    if (ballot(act != 0) == 0) break;
-#pragma unroll
-    for (int j = 0; j < NPTW; ++j) {
-      if ((act >> j) & 1u) {
-        const int k = j * kWave + ln;
-        const int64_t r = clamp_rem(ee[j] + mv[j], overflow);
-        rr[j] = r;
-        ++processed;
-        if ((heavy >> j) & 1u) {
-          W.mx[k] = r;  // read by the whole wave below
-        } else {
-#pragma unroll
-          for (int q = 0; q < kPmax; ++q) {
-            const int lp = dep_at(p01[j], p2[j], q);
-            if (lp >= 0) {
-              atomicMax(reinterpret_cast<long long*>(&W.mx[lp]), (long long)r);
-              atomicSub(&W.cnt[lp], 1);
-            }
-          }
-        }
-      }
-    }
-    fin |= act;
-    // futures with many dependencies: the whole wave pushes each one
-    const uint32_t hact = act & heavy;
-    for (uint64_t hs = ballot(hact != 0); hs; hs &= hs - 1) {
-      const int src = __builtin_ctzll(hs);
-      for (uint32_t hj = uint32_t(readlane_i32(int(hact), src)); hj; hj &= hj - 1) {
-        const int kh = __builtin_ctz(hj) * kWave + src;
-        const int64_t r = W.mx[kh];
-        const int32_t vh = node_at(L, b + kh);
-        const int o = a.p.dep_off[vh];
-        const int d = a.p.dep_off[vh + 1] - o;
-        for (int e0 = 0; e0 < d; e0 += kWave) {
-          const int e = e0 + ln;
-          if (e < d) {
-            const int32_t lp = local_of(L, a.p.dep_idx[o + e], b, n);
-            if (lp >= 0 && lp != kh) {
-              atomicMax(reinterpret_cast<long long*>(&W.mx[lp]), (long long)r);
-              atomicSub(&W.cnt[lp], 1);
-            }
-          }
-        }
-      }
-    }
-    wave_order();
-  }
+  if (NPTW > 2 || ballot(heavy != 0) != 0)  // larger slices: one variant (registers)
+    rounds<NPTW, true>(a, L, W, b, n, own, heavy, ee, p01, p2, rr, processed, overflow);
+  else
+    rounds<NPTW, false>(a, L, W, b, n, own, heavy, ee, p01, p2, rr, processed, overflow);
   if (overflow) flag_sweep(ctrl, kStRange);
-  if (a.rem_out) {
-#pragma unroll
-    for (int j = 0; j < NPTW; ++j)
-      if ((own >> j) & 1u) a.rem_out[vv[j]] = rr[j];
-  }
   const int64_t done_cnt = wave_sum_i64(processed);
   if (ln == 0 && done_cnt != n) flag_sweep(ctrl, kStCycle);
 
-  // D: slack, route, staged at the future's position
-  itab_stage_store(st, it, int(a.p.M), ln);
-  wave_order();
+  // D: bucket slots first, then the routing (LDS only) while the slot
+  // atomics are in flight, then every store.  No store is issued between the
+  // atomics and the routing, so nothing makes the routing wait for them.
+  const BucketArgs& bk = a.bk;
+  uint32_t bkt[NPTW], slot[NPTW];
 #pragma unroll
   for (int j = 0; j < NPTW; ++j) {
+    bkt[j] = 0;
+    slot[j] = 0;
+    if (bk.nb > 0 && ((ready >> j) & 1u)) {
+      bkt[j] = bucket_of(bk, dl - rr[j]);
+      slot[j] = add_agent(bk.cnt + bkt[j], 1u);
+    }
+  }
+  int32_t route[NPTW];
+  int64_t cost[NPTW];
+#pragma unroll
+  for (int j = 0; j < NPTW; ++j) {
+    route[j] = -1;
+    cost[j] = 0;
+    if ((ready >> j) & 1u)
+      route_future(ty[j], ee[j], lc[j], int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load,
+                   it.speed, it.inv, it.pos, it.run, route[j], cost[j]);
+  }
+#pragma unroll
+  for (int j = 0; j < NPTW; ++j) __asm__ __volatile__("" : "+v"(slot[j]) :: "memory");
+#pragma unroll
+  for (int j = 0; j < NPTW; ++j) {
+    if (!((own >> j) & 1u)) continue;
+    const int64_t pos = b + j * kWave + ln;
+    a.stg_ready[pos] = uint8_t((ready >> j) & 1u);
+    if (a.rem_out) a.rem_out[vv[j]] = rr[j];
     if ((ready >> j) & 1u) {
-      const int k = j * kWave + ln;
-      write_ready(a, it, b + k, ty[j], lc[j], rr[j], ee[j], dl, acc);
+      const int64_t slack = dl - rr[j];
+      a.stg_slack[pos] = slack;
+      a.stg_route[pos] = route[j];
+      a.stg_cost[pos] = cost[j];
+      if (bk.nb > 0) bucket_put(a, bkt[j], slot[j], slack, pos, route[j], cost[j]);
+      acc.tmin = slack < acc.tmin ? slack : acc.tmin;
+      acc.tmax = slack > acc.tmax ? slack : acc.tmax;
+      acc.tready += 1;
     }
   }
   wave_order();
