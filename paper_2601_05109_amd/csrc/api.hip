@@ -60,7 +60,7 @@ struct Arena {
   uint8_t* g_dn = nullptr;
   uint8_t* g_nr = nullptr;
   int32_t* g_front[2] = {nullptr, nullptr};
-  uint32_t* bcnt = nullptr;
+  uint32_t* bcnt[2] = {nullptr, nullptr};  // bucket counters, by pass parity
   BucketSlot* bslot = nullptr;
   int64_t capN = -1, capW = -1, capB = -1;
 };
@@ -76,6 +76,7 @@ struct nalar_policy {
   uint32_t epoch = 0;
   uint64_t passes = 0;           // selects the control block of the next pass
   bool ctrl_dirty[2] = {true, true};
+  bool bcnt_clean[2] = {true, true};  // bucket counters known to be zero
   // slack range and ready count of the last successful pass (bucket hint)
   bool hint_valid = false;
   int64_t hint_ready = 0, hint_min = 0, hint_max = 0;
@@ -143,7 +144,7 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B) {
   a.g_dn = reinterpret_cast<uint8_t*>(take(size_t(n1)));
   a.g_nr = reinterpret_cast<uint8_t*>(take(size_t(n1)));
   const int64_t b1 = B > 0 ? B : 0;
-  a.bcnt = reinterpret_cast<uint32_t*>(take(4 * size_t(b1 + 1)));
+  for (int i = 0; i < 2; ++i) a.bcnt[i] = reinterpret_cast<uint32_t*>(take(4 * size_t(b1 + 1)));
   a.bslot = reinterpret_cast<BucketSlot*>(take(sizeof(BucketSlot) * size_t(b1) * kBucketCap));
   off = align_up(off, 256);
   a.lookback_off = off;
@@ -189,6 +190,7 @@ int ensure_capacity(nalar_policy* h, int64_t N, int64_t W, int64_t B) {
   h->ar = fresh;
   h->epoch = 0;
   h->ctrl_dirty[0] = h->ctrl_dirty[1] = true;
+  h->bcnt_clean[0] = h->bcnt_clean[1] = true;
   return NALAR_OK;
 }
 
@@ -356,11 +358,11 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   rc = ensure_capacity(h, N, W, bk.nb);
   if (rc != NALAR_OK) return rc;
   Arena& A = h->ar;
-  bk.cnt = A.bcnt;
-  bk.slot = A.bslot;
   hipStream_t s = h->stream;
   const int cur = int(h->passes & 1);
   const int nxt = cur ^ 1;
+  bk.cnt = A.bcnt[cur];
+  bk.slot = A.bslot;
   Ctrl* ctrl = A.ctrl[cur];
 
   h->epoch = (h->epoch + 1) & kEpochMask;
@@ -389,10 +391,15 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     if (le_ != hipSuccess) return hip_fail(h, le_, name);   \
   } while (0)
 
-  if (need_reset) NALAR_LAUNCH("reset", launch_reset(s, ctrl));
+  // bucket counters of this pass: zeroed by the previous pass's sweep, else here
+  const bool need_clear = bk.nb > 0 && !h->bcnt_clean[cur];
+  if (need_reset || need_clear)
+    NALAR_LAUNCH("reset", launch_reset(s, need_reset ? ctrl : nullptr, bk.cnt, need_clear ? bk.nb : 0));
+  if (bk.nb > 0) h->bcnt_clean[cur] = false;
   const SweepShape sh = plan_sweep(N, W, M, h->cus, h->lds_limit);
-  NALAR_LAUNCH("nodes", launch_nodes(s, pd, ctrl, A.ctrl[nxt], A.itab, A.wf_off, contiguous ? 1 : 0,
-                                     bk, sh.large_cap));
+  const bool fused = N > 0 && sweep_can_fuse(sh, M, contiguous);
+  if (!fused)
+    NALAR_LAUNCH("nodes", launch_nodes(s, pd, ctrl, A.ctrl[nxt], A.itab, A.wf_off, contiguous ? 1 : 0));
 
   const int32_t* node_of_pos = nullptr;
   const int32_t* pos_of_node = nullptr;
@@ -412,7 +419,6 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     g.epoch = epoch;
     g.pos_of_node = A.pos_of_node;
     g.wf_off = A.wf_off;
-    g.large_cap = sh.large_cap;
     e = launch_group(s, g, Timer::cb, &tm);
     if (e != hipSuccess) return hip_fail(h, e, "group");
     node_of_pos = reinterpret_cast<const int32_t*>(A.gpay[(g.npass - 1) & 1]);
@@ -439,8 +445,13 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     sw.g_front1 = A.g_front[1];
     sw.ctrl = ctrl;
     sw.bk = bk;
+    sw.fused = fused ? 1 : 0;
+    sw.next_ctrl = A.ctrl[nxt];
+    sw.bk_clear = A.bcnt[nxt];
+    sw.bk_clear_n = A.capB > 0 ? A.capB : 0;
     sw.force_global = (h->flags & NALAR_FORCE_GLOBAL_SWEEP) ? 1 : 0;
     NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
+    h->bcnt_clean[nxt] = true;  // the sweep cleared them for the next pass
   }
 
   SortArgs sa{};

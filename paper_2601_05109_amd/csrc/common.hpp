@@ -45,8 +45,7 @@ struct Ctrl {
   uint32_t status_sweep;         // problems found by the sweep (cycles, ranges)
   uint32_t sort_npass;           // digit passes the slack sort runs
   uint32_t bucket_overflow;      // a bucket of the bucketed sort overflowed
-  uint32_t n_large;              // workflows too large for one wave's slice
-  uint32_t pad;
+  uint32_t pad[2];
   int64_t n_ready;
   int64_t slack_min;
   int64_t slack_max;
@@ -99,7 +98,6 @@ __device__ inline void reset_ctrl(Ctrl* c) {
     c->status_sweep = 0;
     c->sort_npass = 0;
     c->bucket_overflow = 0;
-    c->n_large = 0;
     c->n_ready = 0;
     c->slack_min = INT64_MAX;
     c->slack_max = INT64_MIN;
@@ -146,36 +144,48 @@ __device__ inline uint64_t lanemask_lt() {
 
 __device__ inline int readlane_i32(int x, int lane) { return __builtin_amdgcn_readlane(x, lane); }
 
-__device__ inline int64_t shfl_xor_i64(int64_t x, int m) {
-  int lo = int(uint32_t(uint64_t(x)));
-  int hi = int(uint32_t(uint64_t(x) >> 32));
-  lo = __shfl_xor(lo, m, kWave);
-  hi = __shfl_xor(hi, m, kWave);
+// Whole-wave reductions (all 64 lanes active): a butterfly inside each row of
+// 16 lanes by DPP (quad swaps, then row rotations by 4 and 8), then the four
+// row results through scalar registers.  No LDS traffic.
+template <int kCtrl>
+__device__ inline int64_t dpp_i64(int64_t x) {
+  const int lo = __builtin_amdgcn_update_dpp(0, int(uint32_t(uint64_t(x))), kCtrl, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, int(uint32_t(uint64_t(x) >> 32)), kCtrl, 0xF, 0xF, false);
   return int64_t((uint64_t(uint32_t(hi)) << 32) | uint32_t(lo));
 }
 
+__device__ inline int64_t readlane_i64(int64_t x, int lane) {
+  const int lo = __builtin_amdgcn_readlane(int(uint32_t(uint64_t(x))), lane);
+  const int hi = __builtin_amdgcn_readlane(int(uint32_t(uint64_t(x) >> 32)), lane);
+  return int64_t((uint64_t(uint32_t(hi)) << 32) | uint32_t(lo));
+}
+
+constexpr int kDppXor1 = 0xB1;   // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;   // quad_perm [2,3,0,1]
+constexpr int kDppRor4 = 0x124;  // row_ror:4
+constexpr int kDppRor8 = 0x128;  // row_ror:8
+
+template <typename Op>
+__device__ inline int64_t wave_reduce_i64(int64_t x, Op op) {
+  x = op(x, dpp_i64<kDppXor1>(x));
+  x = op(x, dpp_i64<kDppXor2>(x));
+  x = op(x, dpp_i64<kDppRor4>(x));
+  x = op(x, dpp_i64<kDppRor8>(x));
+  const int64_t r01 = op(readlane_i64(x, 0), readlane_i64(x, 16));
+  const int64_t r23 = op(readlane_i64(x, 32), readlane_i64(x, 48));
+  return op(r01, r23);
+}
+
 __device__ inline int64_t wave_max_i64(int64_t x) {
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) {
-    int64_t y = shfl_xor_i64(x, m);
-    x = y > x ? y : x;
-  }
-  return x;
+  return wave_reduce_i64(x, [](int64_t u, int64_t v) { return u > v ? u : v; });
 }
 
 __device__ inline int64_t wave_min_i64(int64_t x) {
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) {
-    int64_t y = shfl_xor_i64(x, m);
-    x = y < x ? y : x;
-  }
-  return x;
+  return wave_reduce_i64(x, [](int64_t u, int64_t v) { return u < v ? u : v; });
 }
 
 __device__ inline int64_t wave_sum_i64(int64_t x) {
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) x += shfl_xor_i64(x, m);
-  return x;
+  return wave_reduce_i64(x, [](int64_t u, int64_t v) { return u + v; });
 }
 
 // Inclusive scan over the wave (all 64 lanes active).
@@ -260,6 +270,45 @@ __device__ inline uint64_t lookback_exclusive(const uint64_t* words, int64_t slo
     t -= kLbWindow;
   }
   return excl;
+}
+
+// First index i in [0, n] with a[i] >= key for non-decreasing a, found by
+// galloping from `guess`.  a[guess - 1] and a[guess] are read together, so an
+// exact guess (equal-sized workflows) costs one round trip.
+__device__ inline int64_t lower_bound_from(const int32_t* a, int64_t n, int64_t key, int64_t guess) {
+  guess = guess < 0 ? 0 : (guess > n ? n : guess);
+  const int32_t before = guess >= 1 && guess - 1 < n ? a[guess - 1] : INT32_MIN;
+  const int32_t at = guess < n ? a[guess] : INT32_MAX;
+  const bool ok_before = guess == 0 || int64_t(before) < key;
+  const bool ok_at = guess >= n || int64_t(at) >= key;
+  if (ok_before && ok_at) return guess;
+  int64_t lo, hi;
+  if (!ok_before) {  // answer below guess
+    hi = guess - 1;
+    int64_t step = 1;
+    lo = hi - 1;
+    while (lo >= 0 && int64_t(a[lo]) >= key) {
+      hi = lo;
+      lo = hi - step;
+      step <<= 1;
+    }
+    lo = lo < 0 ? 0 : lo + 1;
+  } else {           // answer above guess
+    lo = guess + 1;
+    hi = lo;
+    int64_t step = 1;
+    while (hi < n && int64_t(a[hi]) < key) {
+      lo = hi + 1;
+      hi = lo + step;
+      if (hi > n) hi = n;
+      step <<= 1;
+    }
+  }
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (int64_t(a[mid]) < key) lo = mid + 1; else hi = mid;
+  }
+  return lo;
 }
 
 // ----------------------------------------------------------------- routing

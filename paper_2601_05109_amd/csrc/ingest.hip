@@ -10,45 +10,6 @@ namespace {
 
 constexpr int kNodeThreads = 256;
 
-// First index i in [0, n] with a[i] >= key for non-decreasing a, found by
-// galloping from `guess`.  a[guess - 1] and a[guess] are read together, so an
-// exact guess (equal-sized workflows) costs one round trip.
-__device__ inline int64_t lower_bound_from(const int32_t* a, int64_t n, int64_t key, int64_t guess) {
-  guess = guess < 0 ? 0 : (guess > n ? n : guess);
-  const int32_t before = guess >= 1 && guess - 1 < n ? a[guess - 1] : INT32_MIN;
-  const int32_t at = guess < n ? a[guess] : INT32_MAX;
-  const bool ok_before = guess == 0 || int64_t(before) < key;
-  const bool ok_at = guess >= n || int64_t(at) >= key;
-  if (ok_before && ok_at) return guess;
-  int64_t lo, hi;
-  if (!ok_before) {  // answer below guess
-    hi = guess - 1;
-    int64_t step = 1;
-    lo = hi - 1;
-    while (lo >= 0 && int64_t(a[lo]) >= key) {
-      hi = lo;
-      lo = hi - step;
-      step <<= 1;
-    }
-    lo = lo < 0 ? 0 : lo + 1;
-  } else {           // answer above guess
-    lo = guess + 1;
-    hi = lo;
-    int64_t step = 1;
-    while (hi < n && int64_t(a[hi]) < key) {
-      lo = hi + 1;
-      hi = lo + step;
-      if (hi > n) hi = n;
-      step <<= 1;
-    }
-  }
-  while (lo < hi) {
-    const int64_t mid = (lo + hi) >> 1;
-    if (int64_t(a[mid]) < key) lo = mid + 1; else hi = mid;
-  }
-  return lo;
-}
-
 // Instance table sorted by (type, original index) and the run of each small
 // type; resets the next pass's control block (one workgroup).
 __device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl) {
@@ -90,12 +51,9 @@ __device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl) {
 
 // Grid-stride over nodes, workflows and instances.  The last workgroup only
 // sorts the instance table by (type, index), so each future's candidates form
-// one contiguous run, and resets the control block of the next pass.  The
-// bucket counters of this pass's bucketed sort are cleared here, before the
-// sweep.
+// one contiguous run, and resets the control block of the next pass.
 __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl, Ctrl* next_ctrl,
-                                                       ITab it, int32_t* wf_off, int contiguous,
-                                                       BucketArgs bk, int64_t large_cap) {
+                                                       ITab it, int32_t* wf_off, int contiguous) {
   const int64_t N = p.N, W = p.W, M = p.M;
   if (blockIdx.x == gridDim.x - 1) {
     instance_table(p, it, next_ctrl);
@@ -131,15 +89,9 @@ __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl
     // if it is not, the pass fails with EINVAL and the offsets are never used)
     for (int64_t w = g0; w <= W; w += stride) {
       const int64_t guess = W > 0 ? (w * N) / W : 0;
-      const int64_t lo = lower_bound_from(p.wf, N, w, guess);
-      wf_off[w] = int32_t(lo);
-      if (w < W) {  // size of workflow w, for the sweep's choice of path
-        const int64_t hi = lower_bound_from(p.wf, N, w + 1, ((w + 1) * N) / W);
-        if (hi - lo > large_cap) add_agent(&ctrl->n_large, 1u);
-      }
+      wf_off[w] = int32_t(lower_bound_from(p.wf, N, w, guess));
     }
   }
-  for (int64_t i = g0; i < bk.nb; i += stride) bk.cnt[i] = 0;  // empty buckets for the sweep
   if (__ballot(bad) != 0 && lane_id() == 0) flag_status(ctrl, kStInval);
 
 }
@@ -154,11 +106,10 @@ int grid_for(int64_t n, int threads, int cap) {
 }  // namespace
 
 hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
-                        int32_t* wf_off, int contiguous, const BucketArgs& bk, int64_t large_cap) {
+                        int32_t* wf_off, int contiguous) {
   int64_t n = p.N > p.W + 1 ? p.N : p.W + 1;
-  if (n < bk.nb) n = bk.nb;
   hipLaunchKernelGGL(k_nodes, dim3(grid_for(n, kNodeThreads, 4096) + 1), dim3(kNodeThreads), 0, s, p,
-                     ctrl, next_ctrl, itab, wf_off, contiguous, bk, large_cap);
+                     ctrl, next_ctrl, itab, wf_off, contiguous);
   return hipGetLastError();
 }
 

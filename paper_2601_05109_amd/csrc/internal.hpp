@@ -62,7 +62,6 @@ struct GroupArgs {
   uint32_t epoch;
   int32_t* pos_of_node;
   int32_t* wf_off;
-  int64_t large_cap;            // workflows above this size are counted in n_large
 };
 
 // Buckets of the bucketed slack sort (nb == 0: not used this pass).  Bucket of
@@ -95,14 +94,21 @@ struct SweepArgs {
   Ctrl* ctrl;
   BucketArgs bk;
   int force_global;
+  // fused mode (workflow-contiguous ids, wave path): the sweep itself
+  // validates the snapshot, finds each workflow's bounds, builds the
+  // instance table and resets the next pass's control block
+  int fused;
+  Ctrl* next_ctrl;
+  uint32_t* bk_clear;           // bucket counters of the next pass, zeroed here
+  int64_t bk_clear_n;
 };
 
 // ingest.hip
 hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
-                        int32_t* wf_off, int contiguous, const BucketArgs& bk, int64_t large_cap);
+                        int32_t* wf_off, int contiguous);
 
 // sort.hip (mark(ctx, name) is called before each launch, for timing)
-hipError_t launch_reset(hipStream_t s, Ctrl* c);
+hipError_t launch_reset(hipStream_t s, Ctrl* c, uint32_t* clear, int64_t n_clear);
 hipError_t launch_bucket_sort(hipStream_t s, const SortArgs& a, const BucketArgs& bk);
 hipError_t launch_slack_sort(hipStream_t s, const SortArgs& a, int first_pass, int last_pass,
                              void (*mark)(void*, const char*), void* ctx);
@@ -116,10 +122,13 @@ struct SweepShape {
   int lds_cap;    // largest workflow handled in LDS
   size_t lds_bytes;
   int blocks;
-  int64_t large_cap;  // wave path: larger workflows need the workgroup pass
+  int wave_path;      // one wave per workflow (k_sweep_wave)
 };
 SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t lds_limit);
 hipError_t prepare_sweep_kernels(size_t lds_limit);
 hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const SweepShape& shape);
+// Whether the sweep can do validation, workflow bounds and the instance table
+// itself (no node kernel): ids grouped by workflow, wave path, small table.
+bool sweep_can_fuse(const SweepShape& shape, int64_t M, bool contiguous);
 
 }  // namespace nalar

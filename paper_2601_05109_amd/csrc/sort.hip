@@ -228,7 +228,13 @@ __device__ void radix_tile(TileSmem<K>& S, const FirstSource& f, bool first, int
   }
 }
 
-__global__ __launch_bounds__(kSortThreads) void k_reset(Ctrl* c) { reset_ctrl(c); }
+// Resets a control block (workgroup 0, if given) and clears n counters.
+__global__ __launch_bounds__(kSortThreads) void k_reset(Ctrl* c, uint32_t* clear, int64_t n) {
+  if (c && blockIdx.x == 0) reset_ctrl(c);
+  for (int64_t i = int64_t(blockIdx.x) * kSortThreads + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * kSortThreads)
+    clear[i] = 0;
+}
 
 // Slack range, ready count and pass count from the sweep's slots (one wave).
 // s_range = {min slack, ready count, digit passes, significant key bits,
@@ -457,14 +463,6 @@ __global__ __launch_bounds__(kSortThreads) void k_group_finish(GroupArgs a) {
       if (int64_t(sorted_wf[mid]) < w) lo = mid + 1; else hi = mid;
     }
     a.wf_off[w] = int32_t(lo);
-    if (w < W) {  // size of workflow w, for the sweep's choice of path
-      int64_t e = lo, f = N;
-      while (e < f) {
-        const int64_t mid = (e + f) >> 1;
-        if (int64_t(sorted_wf[mid]) < w + 1) e = mid + 1; else f = mid;
-      }
-      if (e - lo > a.large_cap) add_agent(&a.ctrl->n_large, 1u);
-    }
   }
 }
 
@@ -477,8 +475,9 @@ unsigned grid_of(int64_t n, int64_t per, int64_t cap) {
 
 }  // namespace
 
-hipError_t launch_reset(hipStream_t s, Ctrl* c) {
-  hipLaunchKernelGGL(k_reset, dim3(1), dim3(kSortThreads), 0, s, c);
+hipError_t launch_reset(hipStream_t s, Ctrl* c, uint32_t* clear, int64_t n_clear) {
+  hipLaunchKernelGGL(k_reset, dim3(grid_of(n_clear, kSortThreads, 256)), dim3(kSortThreads), 0, s, c,
+                     clear, n_clear);
   return hipGetLastError();
 }
 

@@ -177,6 +177,7 @@ __device__ inline int64_t clamp_rem(int64_t r, bool& overflow) {
 
 // Workgroup-shared bookkeeping of the sweep (one instance per workgroup).
 struct Shared {
+  int bad;
   int hcount;
   int fcount;
   int fnext;
@@ -453,8 +454,8 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
 
 // ------------------------------------------------------------ HBM workflow
 
-template <int T>
-__device__ void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
+template <int T, bool kFused>
+__device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
                           int w, int64_t b, int n, int64_t dl, Acc& acc) {
   const int tid = threadIdx.x;
   Ctrl* ctrl = a.ctrl;
@@ -470,8 +471,25 @@ __device__ void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it
     dn[k] = a.p.done[v];
     nr[k] = 0;
   }
-  if (tid == 0) { S.hcount = 0; S.fcount = 0; }
+  if (tid == 0) { S.hcount = 0; S.fcount = 0; S.bad = 0; }
   __syncthreads();
+  if (kFused) {  // the rules of nalar_problem for this workflow's futures
+    for (int k = tid; k < n; k += T) {
+      const int32_t v = node_at(L, b + k);
+      const int32_t o0 = a.p.dep_off[v], o1 = a.p.dep_off[v + 1];
+      const int32_t t = a.p.type[v], l = a.p.loc[v];
+      const int64_t e = a.p.est[v];
+      if ((a.p.wf[v] != w) | (t < 0) | (l < -1) | (int64_t(l) >= a.p.M) | (e < 0) |
+          (e > NALAR_EST_MAX) | (dn[k] > 1) | (o0 < 0) | (o1 < o0) | (int64_t(o1) > a.p.E))
+        S.bad = 1;
+    }
+    __syncthreads();
+    if (S.bad) {  // reported; the workflow is left alone (the pass fails)
+      __syncthreads();  // everyone has read the flag before it is reused
+      if (tid == 0) flag_sweep(ctrl, kStInval);
+      return;
+    }
+  }
 
   // out-degree counters and readiness
   for (int k0 = 0; k0 < n; k0 += T) {
@@ -693,9 +711,9 @@ template <int NPTW, bool kHeavy>
 __device__ __attribute__((always_inline)) inline void rounds(
     const SweepArgs& a, const Layout& L, const WaveSlice& W, int64_t b, int n, uint32_t own,
     uint32_t heavy, const int64_t* ee, const uint32_t* p01, const uint32_t* p2, int64_t* rr,
-    int& processed, bool& overflow) {
+    uint32_t& fin, bool& overflow) {
   const int ln = lane_id();
-  uint32_t fin = 0;
+  fin = 0;
 #pragma unroll
   for (int j = 0; j < NPTW; ++j) rr[j] = 0;
   for (;;) {
@@ -719,7 +737,6 @@ __device__ __attribute__((always_inline)) inline void rounds(
         const int k = j * kWave + ln;
         const int64_t r = clamp_rem(ee[j] + mv[j], overflow);
         rr[j] = r;
-        ++processed;
         if ((heavy >> j) & 1u) {
           W.mx[k] = r;  // read by the whole wave below
         } else {
@@ -771,9 +788,9 @@ __device__ __attribute__((always_inline)) inline void rounds(
 // nothing, so a round costs one LDS round trip (the counter and running-max
 // reads) however many futures it finalises.  Futures with more dependencies
 // are pushed by the whole wave from the dependency list.
-template <int NPTW>
-__device__ void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& it,
-                           const WaveSlice& W, int64_t b, int n, int64_t dl, Acc& acc,
+template <int NPTW, bool kFused>
+__device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& it,
+                           const WaveSlice& W, int64_t w, int64_t b, int n, int64_t dl, Acc& acc,
                            ItabStage& st) {
   const int ln = lane_id();
   Ctrl* ctrl = a.ctrl;
@@ -791,13 +808,28 @@ __device__ void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& i
     if (k < n) {
       own |= 1u << j;
       const int32_t v = node_at(L, b + k);
-      const uint8_t d = a.p.done[v];
+      uint8_t d = a.p.done[v];
+      int32_t o0 = a.p.dep_off[v];
+      int32_t o1 = a.p.dep_off[v + 1];
+      int32_t t = a.p.type[v];
+      int32_t l = a.p.loc[v];
+      int64_t e = a.p.est[v];
+      if (kFused) {  // the rules of nalar_problem for this future
+        const bool bad = (a.p.wf[v] != w) | (t < 0) | (l < -1) | (int64_t(l) >= a.p.M) | (e < 0) |
+                         (e > NALAR_EST_MAX) | (d > 1) | (o0 < 0) | (o1 < o0) | (int64_t(o1) > a.p.E);
+        if (bad) {  // reported; neutralised so that no access leaves its array
+          flag_sweep(ctrl, kStInval);
+          o0 = o1 = 0;
+          l = -1;
+          d = 1;
+        }
+      }
       vv[j] = v;
-      off[j] = a.p.dep_off[v];
-      deg[j] = a.p.dep_off[v + 1] - off[j];
-      ty[j] = a.p.type[v];
-      lc[j] = a.p.loc[v];
-      ee[j] = d ? 0 : a.p.est[v];
+      off[j] = o0;
+      deg[j] = o1 - o0;
+      ty[j] = t;
+      lc[j] = l;
+      ee[j] = d ? 0 : e;
       W.cnt[k] = 0;
       W.mx[k] = 0;
       W.dn[k] = d;
@@ -854,7 +886,7 @@ __device__ void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& i
 
   // the instance table's LDS copy, now that its loads have long returned and
   // no store is in flight (a wait here costs nothing)
-  itab_stage_store(st, it, int(a.p.M), ln);
+  if (!kFused) itab_stage_store(st, it, int(a.p.M), ln);
 
   // readiness (stored after the rounds: no store may be in flight during
   // them, or every round would wait for it)
@@ -871,15 +903,15 @@ __device__ void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& i
   // dependencies touches no global memory inside its loop, so nothing there
   // waits on outstanding loads or stores)
   bool overflow = false;
-  int processed = 0;
+  uint32_t fin = 0;
   int64_t rr[NPTW];
   if (NPTW > 2 || ballot(heavy != 0) != 0)  // larger slices: one variant (registers)
-    rounds<NPTW, true>(a, L, W, b, n, own, heavy, ee, p01, p2, rr, processed, overflow);
+    rounds<NPTW, true>(a, L, W, b, n, own, heavy, ee, p01, p2, rr, fin, overflow);
   else
-    rounds<NPTW, false>(a, L, W, b, n, own, heavy, ee, p01, p2, rr, processed, overflow);
+    rounds<NPTW, false>(a, L, W, b, n, own, heavy, ee, p01, p2, rr, fin, overflow);
   if (overflow) flag_sweep(ctrl, kStRange);
-  const int64_t done_cnt = wave_sum_i64(processed);
-  if (ln == 0 && done_cnt != n) flag_sweep(ctrl, kStCycle);
+  // a future never finalised lies on a cycle (or depends on one)
+  if (ballot((own & ~fin) != 0) != 0 && ln == 0) flag_sweep(ctrl, kStCycle);
 
   // D: bucket slots first, then the routing (LDS only) while the slot
   // atomics are in flight, then every store.  No store is issued between the
@@ -933,6 +965,8 @@ template <int T, int NPT>
 __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
   constexpr int NW = T / kWave;
   Ctrl* ctrl = a.ctrl;
+  for (int64_t i = int64_t(blockIdx.x) * T + threadIdx.x; i < a.bk_clear_n; i += int64_t(gridDim.x) * T)
+    a.bk_clear[i] = 0;  // the next pass's bucket counters
   if (ld_relaxed_agent(&ctrl->status) != 0) return;
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ Shared S;
@@ -973,7 +1007,7 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
     if (!a.force_global && n <= lds_cap)
       sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, lds_cap, b, n, dl, acc);
     else
-      sweep_hbm<T>(a, L, it, S, int(w), b, n, dl, acc);
+      sweep_hbm<T, false>(a, L, it, S, int(w), b, n, dl, acc);
   }
 
   // fold the block's slack range and ready count into the control block
@@ -1003,7 +1037,81 @@ constexpr int kWaveNpt = 8;                  // futures per lane in the wave pat
 constexpr int kWaveCap = kWave * kWaveNpt;     // at most 512 futures per wave
 constexpr int kWaveBlock = 256;                // four independent waves per workgroup
 constexpr int kWavesPerBlock = kWaveBlock / kWave;
+static_assert(kWavesPerBlock == 4, "the wave kernel's flags assume four waves");
 constexpr size_t kWaveSliceBytesPerFuture = 8 + 4 + 1 + 1;
+
+// Instance table of the fused mode, built by the whole workgroup into its LDS
+// (M <= kWaveItabMax): validation of every instance, rank by (type, index),
+// then the run of each small type.  Every thread of the workgroup calls it.
+__device__ __attribute__((always_inline)) void build_itab_block(const ProblemDev& p, const ITabLds& it, Ctrl* ctrl,
+                                 int32_t* s_type) {
+  const int M = int(p.M);
+  const int tid = threadIdx.x;
+  int32_t t[2], sp[2];
+  int64_t ld[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int i = tid + u * kWaveBlock;
+    t[u] = 0; sp[u] = 1; ld[u] = 0;
+    if (i < M) {
+      t[u] = p.inst_type[i];
+      sp[u] = p.inst_speed[i];
+      ld[u] = p.inst_load[i];
+      if ((t[u] < 0) | (sp[u] < 1) | (ld[u] < 0) | (ld[u] > NALAR_LOAD_MAX)) flag_sweep(ctrl, kStInval);
+      s_type[i] = t[u];
+    }
+  }
+  if (tid < kTypeDirect) it.run[tid] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int i = tid + u * kWaveBlock;
+    if (i < M) {
+      int rank = 0;
+      for (int j = 0; j < M; ++j) {
+        const int32_t o = s_type[j];
+        rank += (o < t[u]) | ((o == t[u]) & (j < i));
+      }
+      it.type[rank] = t[u];
+      it.idx[rank] = i;
+      it.load[rank] = ld[u];
+      it.speed[rank] = sp[u];
+      it.inv[rank] = sp[u] >= 1 ? 1.0 / double(sp[u]) : 0.0;
+      it.pos[i] = rank;
+    }
+  }
+  __syncthreads();
+  for (int r = tid; r < M; r += kWaveBlock) {
+    const int32_t ty = it.type[r];
+    if (ty >= 0 && ty < kTypeDirect && (r == 0 || it.type[r - 1] != ty)) {
+      int e = r + 1;
+      while (e < M && it.type[e] == ty) ++e;
+      it.run[ty] = uint32_t(r) | (uint32_t(e) << 16);
+    }
+  }
+  __syncthreads();
+}
+
+// Bounds of workflow w: from the offsets computed before the sweep, or (fused
+// mode, ids grouped by workflow) as lower bounds of w and w + 1 in wf, found
+// by lanes 0 and 1 of the wave (wave-uniform call).
+__device__ inline void wf_bounds(const SweepArgs& a, int64_t w, int64_t& b, int& n) {
+  if (!a.fused) {
+    b = a.wf_off[w];
+    n = a.wf_off[w + 1] - int32_t(b);
+    return;
+  }
+  const int64_t N = a.p.N, Wn = a.p.W;
+  const int ln = lane_id();
+  int32_t lb = 0;
+  if (ln < 2) lb = int32_t(lower_bound_from(a.p.wf, N, w + ln, ((w + ln) * N) / Wn));
+  const int32_t lo = readlane_i32(lb, 0), hi = readlane_i32(lb, 1);
+  b = lo;
+  n = hi - lo;
+  // the ranges must tile [0, N): none negative, the first at 0, the last at N
+  if (ln == 0 && ((n < 0) | ((w == 0) & (lo != 0)) | ((w == Wn - 1) & (int64_t(hi) != N))))
+    flag_sweep(a.ctrl, kStInval);
+}
 
 // LDS of the instance tables of one wave workgroup.
 __host__ __device__ inline size_t itab_lds_wave(int64_t M) {
@@ -1023,39 +1131,39 @@ __device__ inline ITabLds carve_itab(unsigned char* sp, int M) {
   return it;
 }
 
-// Small workflows: one wave each, no workgroup barrier on the way.  Each wave
-// fetches its first workflow's bounds and deadline together with the status
-// word, so the sweep starts after one round trip.  Workflows larger than a
-// wave's slice (wcap futures; k_nodes counts them) are swept afterwards by
-// whole workgroups with HBM state.  Each wave folds its slack range and ready
-// count into one of the control block's partial slots.
-template <int NPTW>
+// Small workflows: one wave each, no workgroup barrier on the way (fused mode:
+// after the instance table is built).  Workflows larger than a wave's slice
+// (wcap futures) are swept at the end by whole workgroups with HBM state.
+// Each wave folds its slack range and ready count into one of the control
+// block's partial slots.
+template <int NPTW, bool kFused>
 __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ Shared S;
+  __shared__ int32_t s_itype[kWaveItabMax];
+  __shared__ int s_big[kWavesPerBlock];
   Ctrl* ctrl = a.ctrl;
   const int M = int(a.p.M);
   const int tid = threadIdx.x;
   const int wv = tid / kWave;
   const int ln = lane_id();
-  const bool per_wave = M <= kWaveItabMax;
+  const bool per_wave = !kFused && M <= kWaveItabMax;
   const int64_t gw = int64_t(blockIdx.x) * kWavesPerBlock + wv;
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
 
-  // one round trip: validation status, large-workflow count, first workflow,
-  // this wave's instance table entries
+  // one round trip: validation status, this wave's first workflow, the
+  // instance table
   const uint32_t status = ld_relaxed_agent(&ctrl->status);
-  const uint32_t n_large = ld_relaxed_agent(&ctrl->n_large);
-  int64_t b0 = 0, dl0 = 0;
+  int64_t b0 = 0, dl0 = 0, raw0 = 0;
   int n0 = 0;
   if (gw < a.p.W) {
-    b0 = a.wf_off[gw];
-    n0 = a.wf_off[gw + 1] - int32_t(b0);
-    dl0 = a.p.deadline[gw] - a.p.now;
+    wf_bounds(a, gw, b0, n0);
+    raw0 = a.p.deadline[gw];
+    dl0 = raw0 - a.p.now;
   }
   ItabStage st;
   st.pending = false;
-  if (per_wave) itab_stage_load(st, a.itab, M, ln);
+  if (!kFused && per_wave) itab_stage_load(st, a.itab, M, ln);
 
   const size_t nw = size_t(kWavesPerBlock) * size_t(wcap);
   const size_t itab_one = 32 * size_t(M) + 4 * kTypeDirect;
@@ -1067,40 +1175,76 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap
   Wv.cnt = reinterpret_cast<int32_t*>(sp) + size_t(wv) * wcap; sp += 4 * nw;
   Wv.dn = sp + size_t(wv) * wcap; sp += nw;
   Wv.nr = sp + size_t(wv) * wcap;
-  if (!per_wave) {  // one shared copy (every thread reaches this barrier)
-    for (int i = tid; i < M; i += kWaveBlock) {
-      it.load[i] = a.itab.load[i];
-      it.inv[i] = a.itab.inv_speed[i];
-      it.type[i] = a.itab.type[i];
-      it.idx[i] = a.itab.idx[i];
-      it.speed[i] = a.itab.speed[i];
-      it.pos[i] = a.itab.pos_of[i];
+  if (kFused) {
+    if (blockIdx.x == 0) reset_ctrl(a.next_ctrl);  // unused by this pass; ready for the next
+    for (int64_t i = int64_t(blockIdx.x) * kWaveBlock + tid; i < a.bk_clear_n;
+         i += int64_t(gridDim.x) * kWaveBlock)
+      a.bk_clear[i] = 0;
+    if (gw == 0 && ln == 0 && (a.p.dep_off[0] != 0 || int64_t(a.p.dep_off[a.p.N]) != a.p.E))
+      flag_sweep(ctrl, kStInval);
+    if (gw < a.p.W && ln == 0 &&
+        ((raw0 < a.p.now - NALAR_HORIZON_MAX) | (raw0 > a.p.now + NALAR_HORIZON_MAX)))
+      flag_sweep(ctrl, kStInval);
+    build_itab_block(a.p, it, ctrl, s_itype);
+  } else {
+    for (int64_t i = int64_t(blockIdx.x) * kWaveBlock + tid; i < a.bk_clear_n;
+         i += int64_t(gridDim.x) * kWaveBlock)
+      a.bk_clear[i] = 0;
+    if (!per_wave) {  // one shared copy (every thread reaches this barrier)
+      for (int i = tid; i < M; i += kWaveBlock) {
+        it.load[i] = a.itab.load[i];
+        it.inv[i] = a.itab.inv_speed[i];
+        it.type[i] = a.itab.type[i];
+        it.idx[i] = a.itab.idx[i];
+        it.speed[i] = a.itab.speed[i];
+        it.pos[i] = a.itab.pos_of[i];
+      }
+      for (int t = tid; t < kTypeDirect; t += kWaveBlock) it.run[t] = a.itab.run[t];
+      __syncthreads();
     }
-    for (int t = tid; t < kTypeDirect; t += kWaveBlock) it.run[t] = a.itab.run[t];
-    __syncthreads();
   }
-  // the validation status cannot change during this kernel (the sweep reports
-  // into its own word), so every wave of every workgroup leaves together
+  // the validation status read above cannot change during this kernel (the
+  // sweep reports into its own word), so every wave of every workgroup
+  // leaves together
   if (status != 0) return;
 
   const Layout L{a.node_of_pos, a.pos_of_node, a.p.N};
   Acc acc;
-  if (!a.force_global) {
-    for (int64_t w = gw; w < a.p.W; w += nwaves) {
-      const int64_t b = w == gw ? b0 : a.wf_off[w];
-      const int n = w == gw ? n0 : a.wf_off[w + 1] - int32_t(b);
-      if (n <= 0 || n > wcap) continue;
-      sweep_wave<NPTW>(a, L, it, Wv, b, n, w == gw ? dl0 : a.p.deadline[w] - a.p.now, acc, st);
+  bool big = false;
+  for (int64_t w = gw; w < a.p.W; w += nwaves) {
+    int64_t b = b0;
+    int n = n0;
+    int64_t dl = dl0;
+    if (w != gw) {
+      wf_bounds(a, w, b, n);
+      const int64_t raw = a.p.deadline[w];
+      dl = raw - a.p.now;
+      if (kFused && ln == 0 &&
+          ((raw < a.p.now - NALAR_HORIZON_MAX) | (raw > a.p.now + NALAR_HORIZON_MAX)))
+        flag_sweep(ctrl, kStInval);
     }
+    if (n <= 0) continue;
+    if (n > wcap || a.force_global) {
+      big = true;
+      continue;
+    }
+    sweep_wave<NPTW, kFused>(a, L, it, Wv, w, b, n, dl, acc, st);
   }
-  if (n_large > 0 || a.force_global) {  // the same for the whole workgroup
+  if (ln == 0) s_big[wv] = big ? 1 : 0;
+  __syncthreads();
+  if (s_big[0] | s_big[1] | s_big[2] | s_big[3]) {  // the workgroup's large workflows (HBM state)
     itab_stage_store(st, it, M, ln);
     __syncthreads();
-    for (int64_t w = blockIdx.x; w < a.p.W; w += gridDim.x) {
-      const int64_t b = a.wf_off[w];
-      const int n = a.wf_off[w + 1] - int32_t(b);
-      if (n <= 0 || (n <= wcap && !a.force_global)) continue;
-      sweep_hbm<kWaveBlock>(a, L, it, S, int(w), b, n, a.p.deadline[w] - a.p.now, acc);
+    for (int64_t base = int64_t(blockIdx.x) * kWavesPerBlock; base < a.p.W; base += nwaves) {
+      for (int i = 0; i < kWavesPerBlock; ++i) {
+        const int64_t w = base + i;
+        if (w >= a.p.W) break;
+        int64_t b;
+        int n;
+        wf_bounds(a, w, b, n);
+        if (n <= 0 || (n <= wcap && !a.force_global)) continue;
+        sweep_hbm<kWaveBlock, kFused>(a, L, it, S, int(w), b, n, a.p.deadline[w] - a.p.now, acc);
+      }
     }
   }
 
@@ -1131,7 +1275,7 @@ SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t ld
     s.npt = int(wcap / kWave);
     s.lds_cap = int(wcap);
     s.lds_bytes = itab_lds_wave(M) + kWaveSliceBytesPerFuture * size_t(kWavesPerBlock) * size_t(wcap) + 16;
-    s.large_cap = wcap;
+    s.wave_path = 1;
     int64_t blocks = (W + kWavesPerBlock - 1) / kWavesPerBlock;
     const int64_t most = int64_t(device_cus) * 8;
     if (blocks > most) blocks = most;
@@ -1145,11 +1289,15 @@ SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t ld
   if (cap > int64_t(kBlockT) * kBlockNpt) cap = int64_t(kBlockT) * kBlockNpt;
   s.lds_cap = int(cap);
   s.lds_bytes = itab + 14 * size_t(cap) + 16;
-  s.large_cap = INT64_MAX;
+  s.wave_path = 0;
   int64_t blocks = int64_t(device_cus) * 2;
   if (blocks > W) blocks = W;
   s.blocks = int(blocks < 1 ? 1 : blocks);
   return s;
+}
+
+bool sweep_can_fuse(const SweepShape& shape, int64_t M, bool contiguous) {
+  return contiguous && shape.wave_path && M <= kWaveItabMax;
 }
 
 hipError_t prepare_sweep_kernels(size_t lds_limit) {
@@ -1157,10 +1305,14 @@ hipError_t prepare_sweep_kernels(size_t lds_limit) {
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sweep<kBlockT, kBlockNpt>),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(dyn));
   if (e != hipSuccess) return e;
-  for (const void* k : {reinterpret_cast<const void*>(&k_sweep_wave<1>),
-                        reinterpret_cast<const void*>(&k_sweep_wave<2>),
-                        reinterpret_cast<const void*>(&k_sweep_wave<4>),
-                        reinterpret_cast<const void*>(&k_sweep_wave<8>)}) {
+  for (const void* k : {reinterpret_cast<const void*>(&k_sweep_wave<1, false>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<2, false>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<4, false>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<8, false>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<1, true>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<2, true>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<4, true>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<8, true>)}) {
     e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, int(dyn));
     if (e != hipSuccess) return e;
   }
@@ -1170,20 +1322,23 @@ hipError_t prepare_sweep_kernels(size_t lds_limit) {
 hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const SweepShape& sh) {
   if (sh.threads == kWaveBlock) {
     // futures per lane = slice capacity / 64 (a power of two up to kWaveNpt)
-    switch (sh.npt) {
-      case 1:
-        hipLaunchKernelGGL(k_sweep_wave<1>, dim3(sh.blocks), dim3(kWaveBlock), sh.lds_bytes, s, a, sh.lds_cap);
-        break;
-      case 2:
-        hipLaunchKernelGGL(k_sweep_wave<2>, dim3(sh.blocks), dim3(kWaveBlock), sh.lds_bytes, s, a, sh.lds_cap);
-        break;
-      case 4:
-        hipLaunchKernelGGL(k_sweep_wave<4>, dim3(sh.blocks), dim3(kWaveBlock), sh.lds_bytes, s, a, sh.lds_cap);
-        break;
-      default:
-        hipLaunchKernelGGL(k_sweep_wave<kWaveNpt>, dim3(sh.blocks), dim3(kWaveBlock), sh.lds_bytes, s, a,
-                           sh.lds_cap);
-        break;
+    const dim3 g(sh.blocks), t(kWaveBlock);
+    const size_t lds = sh.lds_bytes;
+    const int cap = sh.lds_cap;
+    if (a.fused) {
+      switch (sh.npt) {
+        case 1: hipLaunchKernelGGL((k_sweep_wave<1, true>), g, t, lds, s, a, cap); break;
+        case 2: hipLaunchKernelGGL((k_sweep_wave<2, true>), g, t, lds, s, a, cap); break;
+        case 4: hipLaunchKernelGGL((k_sweep_wave<4, true>), g, t, lds, s, a, cap); break;
+        default: hipLaunchKernelGGL((k_sweep_wave<kWaveNpt, true>), g, t, lds, s, a, cap); break;
+      }
+    } else {
+      switch (sh.npt) {
+        case 1: hipLaunchKernelGGL((k_sweep_wave<1, false>), g, t, lds, s, a, cap); break;
+        case 2: hipLaunchKernelGGL((k_sweep_wave<2, false>), g, t, lds, s, a, cap); break;
+        case 4: hipLaunchKernelGGL((k_sweep_wave<4, false>), g, t, lds, s, a, cap); break;
+        default: hipLaunchKernelGGL((k_sweep_wave<kWaveNpt, false>), g, t, lds, s, a, cap); break;
+      }
     }
   } else
     hipLaunchKernelGGL((k_sweep<kBlockT, kBlockNpt>), dim3(sh.blocks), dim3(kBlockT), sh.lds_bytes, s,

@@ -298,6 +298,57 @@ def test_error_rules(policy, case):
     check(policy, q, f"error {case} relabelled")
 
 
+@pytest.mark.parametrize("case", ERROR_CASES)
+def test_error_rules_hbm_sweep(policy_hbm, case):
+    """The same rules when every workflow takes the workgroup (HBM) path."""
+    field, idx, value = case
+    p = wl.tiny().copy()
+    getattr(p, field)[idx] = value
+    check(policy_hbm, p, f"error {case} hbm")
+
+
+def _mixed_sizes(sizes, seed, n_instances=24, n_types=5):
+    """Workflows of the given sizes, ids grouped by workflow; future i of a
+    workflow depends on up to three of the four futures before it."""
+    rng = np.random.default_rng(seed)
+    W = len(sizes)
+    N = int(sum(sizes))
+    wf = np.repeat(np.arange(W), sizes).astype(np.int32)
+    starts = np.r_[0, np.cumsum(sizes)[:-1]]
+    deps, off = [], [0]
+    for w, n in enumerate(sizes):
+        for i in range(n):
+            k = int(rng.integers(0, min(i, 3) + 1))
+            par = rng.choice(np.arange(max(0, i - 4), i), size=k, replace=False) if k else []
+            deps.extend(int(starts[w] + q) for q in sorted(par))
+            off.append(len(deps))
+    types = rng.integers(0, n_types, N).astype(np.int32)
+    est = rng.integers(1, 10**6, N).astype(np.int64)
+    done = (rng.random(N) < 0.2).astype(np.uint8)
+    loc = np.where(rng.random(N) < 0.5, rng.integers(0, n_instances, N), -1).astype(np.int32)
+    now = 10**12
+    return wl.Problem("mixed", now, 5000, wf, types, est, done, loc, np.array(off, np.int32),
+                      np.array(deps, np.int32), now + rng.integers(10**6, 10**8, W).astype(np.int64),
+                      rng.integers(0, n_types, n_instances).astype(np.int32),
+                      rng.integers(0, 10**6, n_instances).astype(np.int64),
+                      rng.integers(1, 3000, n_instances).astype(np.int32), wf_contiguous=True)
+
+
+def test_mixed_workflow_sizes(policy):
+    """Small workflows with a few far larger than a wave's slice: the large
+    ones are swept by whole workgroups in the same launch."""
+    sizes = [8] * 300 + [2000] + [8] * 100 + [700, 3] + [1] * 50
+    p = _mixed_sizes(sizes, 1)
+    check(policy, p, "mixed sizes")
+    for field, idx, value in (("type", 300 * 8 + 1500, -1), ("loc", 300 * 8 + 10, 24),
+                              ("est_us", 300 * 8 + 2000 + 8 * 100 + 650, -5),
+                              ("done", 5, 3), ("wf", 300 * 8 + 1999, 302),
+                              ("deadline_us", 300, 1 << 62)):
+        q = p.copy()
+        getattr(q, field)[idx] = value
+        check(policy, q, f"mixed sizes, {field}[{idx}] = {value}")
+
+
 def test_error_cycle_and_self_loop(policy, policy_hbm):
     p = wl.tiny().copy()
     p.dep_idx[p.dep_off[12]] = 12
