@@ -112,6 +112,28 @@ __device__ inline void reset_ctrl(Ctrl* c) {
   for (int i = tid; i < kMaxGroupPasses * kRadixBuckets; i += blockDim.x) c->ghist_group[i] = 0;
 }
 
+// The same reset spread over a grid: thread gi of gstride writes every
+// gstride-th word (gi = blockIdx.x * blockDim.x + threadIdx.x).
+__device__ inline void reset_ctrl_spread(Ctrl* c, int64_t gi, int64_t gstride) {
+  if (gi == 0) {
+    c->status = 0;
+    c->status_sweep = 0;
+    c->sort_npass = 0;
+    c->bucket_overflow = 0;
+    c->n_ready = 0;
+    c->slack_min = INT64_MAX;
+    c->slack_max = INT64_MIN;
+  }
+  for (int64_t i = gi; i < 16; i += gstride) c->tile_ticket[i] = 0;
+  for (int64_t i = gi; i < kParts; i += gstride) {
+    c->part_min[i] = INT64_MAX;
+    c->part_max[i] = INT64_MIN;
+    c->part_cnt[i] = 0;
+  }
+  for (int64_t i = gi; i < kMaxSortPasses * kRadixBuckets; i += gstride) c->ghist_slack[i] = 0;
+  for (int64_t i = gi; i < kMaxGroupPasses * kRadixBuckets; i += gstride) c->ghist_group[i] = 0;
+}
+
 // Instance table sorted by (type, original index), plus the sorted position of
 // every original index (for the instance that holds a future's state) and,
 // for types below kTypeDirect, the run of sorted positions holding that type.

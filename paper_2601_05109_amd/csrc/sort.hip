@@ -307,7 +307,7 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, Buck
   }
   settle_range(ctrl, s_range, g == 0);
   const int64_t R = s_range[1];
-  if (ld_relaxed_agent(&ctrl->bucket_overflow) != 0) {
+  if (ctrl->bucket_overflow != 0) {  // written by the sweep, an earlier kernel
     if (g == 0 && tid == 0)
       publish_status(a.host, kStatusTiled, R, int(s_range[3]), s_range[0], s_range[4]);
     return;

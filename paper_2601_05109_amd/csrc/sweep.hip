@@ -639,6 +639,13 @@ __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, con
 
 // ------------------------------------------------------------ wave workflow
 
+// The LDS operations of one wave complete in program order, so a wave working
+// on LDS of its own needs no barrier: each read observes every earlier write
+// and atomic of the same wave.  wave_order() only keeps the compiler from
+// moving LDS accesses across a phase boundary; it emits no wait, so
+// outstanding HBM stores never stall the wave.
+__device__ inline void wave_order() { __asm__ __volatile__("" ::: "memory"); }
+
 // Instance tables of at most kWaveItabMax entries get one LDS copy per wave:
 // the wave loads its entries into registers at kernel start and writes them
 // to its copy just before it first routes, so the load's latency hides behind
@@ -651,6 +658,7 @@ struct ItabStage {
   int32_t type[2], idx[2], speed[2], pos[2];
   uint32_t run;
   bool pending;
+  bool build;   // entry `lane` of the caller's table is in type/speed/load[0]: sort it here
 };
 
 __device__ inline void itab_stage_load(ItabStage& st, const ITab& g, int M, int ln) {
@@ -670,8 +678,67 @@ __device__ inline void itab_stage_load(ItabStage& st, const ITab& g, int M, int 
   st.pending = true;
 }
 
+// Sorts an instance table of at most 64 entries (entry l held by lane l) into
+// the wave's LDS copy, with no workgroup barrier.  Types in [0, 64) (the usual
+// case) are ranked with ballots: lanes of equal type from six bit ballots, the
+// count of each type through LDS and one wave scan.  Other types fall back to a
+// comparison against every entry.
+__device__ inline void itab_wave_build(const ItabStage& st, const ITabLds& it, int M, int ln) {
+  const bool valid = ln < M;
+  const int32_t t = valid ? st.type[0] : 0;
+  int less = 0, eq = 0, eq_below = 0;
+  if (ballot(valid && uint32_t(t) >= uint32_t(kTypeDirect)) == 0) {
+    uint64_t peers = ballot(valid);
+#pragma unroll
+    for (int bit = 0; bit < 6; ++bit) {
+      const bool on = (t >> bit) & 1;
+      const uint64_t m = ballot(valid && on);
+      peers &= on ? m : ~m;
+    }
+    eq = valid ? int(__popcll(peers)) : 0;
+    eq_below = valid ? int(__popcll(peers & lanemask_lt())) : 0;
+    it.run[ln] = 0;                       // count of each type, then its run
+    wave_order();
+    if (valid && eq_below == 0) it.run[t] = uint32_t(eq);
+    wave_order();
+    const uint32_t c = it.run[ln];
+    const uint32_t base = wave_incl_scan_u32(c) - c;
+    wave_order();
+    it.run[ln] = base | ((base + c) << 16);
+    wave_order();
+    less = valid ? int(it.run[t] & 0xFFFFu) : 0;
+  } else {
+    for (int j = 0; j < M; ++j) {
+      const int32_t o = readlane_i32(t, j);
+      less += o < t;
+      eq += o == t;
+      eq_below += (o == t) & (j < ln);
+    }
+    it.run[ln] = 0;
+    wave_order();
+    if (valid && t >= 0 && t < kTypeDirect && eq_below == 0)
+      it.run[t] = uint32_t(less) | (uint32_t(less + eq) << 16);
+  }
+  if (valid) {
+    const int rank = less + eq_below;
+    const int32_t sp = st.speed[0];
+    it.type[rank] = t;
+    it.idx[rank] = ln;
+    it.load[rank] = st.load[0];
+    it.speed[rank] = sp;
+    it.inv[rank] = sp >= 1 ? 1.0 / double(sp) : 0.0;
+    it.pos[ln] = rank;
+  }
+  wave_order();
+}
+
 __device__ inline void itab_stage_store(ItabStage& st, const ITabLds& it, int M, int ln) {
   if (!st.pending) return;
+  if (st.build) {
+    itab_wave_build(st, it, M, ln);
+    st.pending = false;
+    return;
+  }
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int i = ln + u * kWave;
@@ -689,11 +756,6 @@ __device__ inline void itab_stage_store(ItabStage& st, const ITabLds& it, int M,
 }
 
 // One wave sweeps a workflow of at most 64 * NPTW futures on its own LDS slice.
-// The LDS operations of one wave complete in program order, so no barrier is
-// needed: each read observes every earlier write and atomic of the same wave.
-// wave_order() only keeps the compiler from moving LDS accesses across a phase
-// boundary; it emits no wait, so outstanding HBM stores never stall the wave.
-__device__ inline void wave_order() { __asm__ __volatile__("" ::: "memory"); }
 
 // LDS slice of one wave (cap futures).
 struct WaveSlice {
@@ -886,7 +948,7 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
 
   // the instance table's LDS copy, now that its loads have long returned and
   // no store is in flight (a wait here costs nothing)
-  if (!kFused) itab_stage_store(st, it, int(a.p.M), ln);
+  itab_stage_store(st, it, int(a.p.M), ln);
 
   // readiness (stored after the rounds: no store may be in flight during
   // them, or every round would wait for it)
@@ -967,7 +1029,7 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
   Ctrl* ctrl = a.ctrl;
   for (int64_t i = int64_t(blockIdx.x) * T + threadIdx.x; i < a.bk_clear_n; i += int64_t(gridDim.x) * T)
     a.bk_clear[i] = 0;  // the next pass's bucket counters
-  if (ld_relaxed_agent(&ctrl->status) != 0) return;
+  if (ctrl->status != 0) return;  // written by earlier kernels only
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ Shared S;
 
@@ -1041,53 +1103,49 @@ static_assert(kWavesPerBlock == 4, "the wave kernel's flags assume four waves");
 constexpr size_t kWaveSliceBytesPerFuture = 8 + 4 + 1 + 1;
 
 // Instance table of the fused mode, built by the whole workgroup into its LDS
-// (M <= kWaveItabMax): validation of every instance, rank by (type, index),
-// then the run of each small type.  Every thread of the workgroup calls it.
-__device__ __attribute__((always_inline)) void build_itab_block(const ProblemDev& p, const ITabLds& it, Ctrl* ctrl,
-                                 int32_t* s_type) {
-  const int M = int(p.M);
-  const int tid = threadIdx.x;
-  int32_t t[2], sp[2];
-  int64_t ld[2];
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int i = tid + u * kWaveBlock;
-    t[u] = 0; sp[u] = 1; ld[u] = 0;
-    if (i < M) {
-      t[u] = p.inst_type[i];
-      sp[u] = p.inst_speed[i];
-      ld[u] = p.inst_load[i];
-      if ((t[u] < 0) | (sp[u] < 1) | (ld[u] < 0) | (ld[u] > NALAR_LOAD_MAX)) flag_sweep(ctrl, kStInval);
-      s_type[i] = t[u];
-    }
-  }
-  if (tid < kTypeDirect) it.run[tid] = 0;
+// (M <= kWaveItabMax, entry i held by thread i, loaded by the caller): rank by
+// (type, index), and the run of each small type from the counts of smaller
+// and equal types.  Every thread of the workgroup calls it; two barriers.
+__device__ __attribute__((always_inline)) void build_itab_block(const ITabLds& it, int M, int32_t t,
+                                                                int32_t sp, int64_t ld,
+                                                                int32_t* s_type) {
+  const int i = threadIdx.x;
+  if (i < M) s_type[i] = t;
+  if (i < kTypeDirect) it.run[i] = 0;
   __syncthreads();
+  if (i < M) {
+    // four types per LDS read; the bound lives in a vector register (as a
+    // scalar it would be reloaded from the arguments, waiting on every LDS
+    // read in flight).  Each comparison feeds one add right away, so no
+    // comparison mask stays live (those live in scalar registers).
+    int mv;
+    __asm__ __volatile__("v_mov_b32 %0, %1" : "=v"(mv) : "s"(M));
+    int less = 0, eq_below = 0, eq = 0;
+    const int4* s4 = reinterpret_cast<const int4*>(s_type);
+#pragma unroll 1
+    for (int j0 = 0; j0 < mv; j0 += 4) {
+      const int4 v = s4[j0 >> 2];
+      const int32_t o[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int i = tid + u * kWaveBlock;
-    if (i < M) {
-      int rank = 0;
-      for (int j = 0; j < M; ++j) {
-        const int32_t o = s_type[j];
-        rank += (o < t[u]) | ((o == t[u]) & (j < i));
+      for (int q = 0; q < 4; ++q) {
+        const int j = j0 + q;
+        const int in = j < mv ? 1 : 0;
+        const int lt = o[q] < t ? in : 0;
+        const int e = o[q] == t ? in : 0;
+        less += lt;
+        eq += e;
+        eq_below += j < i ? e : 0;
       }
-      it.type[rank] = t[u];
-      it.idx[rank] = i;
-      it.load[rank] = ld[u];
-      it.speed[rank] = sp[u];
-      it.inv[rank] = sp[u] >= 1 ? 1.0 / double(sp[u]) : 0.0;
-      it.pos[i] = rank;
     }
-  }
-  __syncthreads();
-  for (int r = tid; r < M; r += kWaveBlock) {
-    const int32_t ty = it.type[r];
-    if (ty >= 0 && ty < kTypeDirect && (r == 0 || it.type[r - 1] != ty)) {
-      int e = r + 1;
-      while (e < M && it.type[e] == ty) ++e;
-      it.run[ty] = uint32_t(r) | (uint32_t(e) << 16);
-    }
+    const int rank = less + eq_below;
+    it.type[rank] = t;
+    it.idx[rank] = i;
+    it.load[rank] = ld;
+    it.speed[rank] = sp;
+    it.inv[rank] = sp >= 1 ? 1.0 / double(sp) : 0.0;
+    it.pos[i] = rank;
+    if (t >= 0 && t < kTypeDirect && eq_below == 0)
+      it.run[t] = uint32_t(less) | (uint32_t(less + eq) << 16);
   }
   __syncthreads();
 }
@@ -1131,6 +1189,39 @@ __device__ inline ITabLds carve_itab(unsigned char* sp, int M) {
   return it;
 }
 
+// Brings the six 64-byte lines of the sweep's kernel arguments into the
+// scalar cache with loads that are all in flight at once.  The argument block
+// is large and the compiler reloads its fields on demand, one wait each; cold
+// lines would otherwise cost a round trip apiece.
+static_assert(sizeof(SweepArgs) > 5 * 64 && sizeof(SweepArgs) <= 6 * 64,
+              "warm_kernargs covers exactly the argument block's lines");
+__device__ inline void warm_kernargs() {
+  const auto kp = __builtin_amdgcn_kernarg_segment_ptr();
+  uint32_t v0, v1, v2, v3, v4, v5;
+  __asm__ __volatile__(
+      "s_load_dword %0, %6, 0\n"
+      "s_load_dword %1, %6, 64\n"
+      "s_load_dword %2, %6, 128\n"
+      "s_load_dword %3, %6, 192\n"
+      "s_load_dword %4, %6, 256\n"
+      "s_load_dword %5, %6, 320\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&s"(v0), "=&s"(v1), "=&s"(v2), "=&s"(v3), "=&s"(v4), "=&s"(v5)
+      : "s"(kp));
+  (void)v0; (void)v1; (void)v2; (void)v3; (void)v4; (void)v5;
+}
+
+// The next pass's bucket counters and, in fused mode, its control block.
+// Done last: a store in flight would make every later wait for a load wait
+// for it too (one counter covers both).
+template <bool kFused>
+__device__ inline void clear_for_next_pass(const SweepArgs& a) {
+  const int64_t gi = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t gstride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t i = gi; i < a.bk_clear_n; i += gstride) a.bk_clear[i] = 0;
+  if (kFused) reset_ctrl_spread(a.next_ctrl, gi, gstride);
+}
+
 // Small workflows: one wave each, no workgroup barrier on the way (fused mode:
 // after the instance table is built).  Workflows larger than a wave's slice
 // (wcap futures) are swept at the end by whole workgroups with HBM state.
@@ -1138,31 +1229,59 @@ __device__ inline ITabLds carve_itab(unsigned char* sp, int M) {
 // block's partial slots.
 template <int NPTW, bool kFused>
 __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap) {
+  warm_kernargs();
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ Shared S;
-  __shared__ int32_t s_itype[kWaveItabMax];
+  __shared__ __align__(16) int32_t s_itype[kWaveItabMax];
   __shared__ int s_big[kWavesPerBlock];
   Ctrl* ctrl = a.ctrl;
   const int M = int(a.p.M);
   const int tid = threadIdx.x;
   const int wv = tid / kWave;
   const int ln = lane_id();
-  const bool per_wave = !kFused && M <= kWaveItabMax;
+  const bool wave_itab = kFused && M <= kWave;  // sorted by each wave itself, no barrier
+  const bool per_wave = (!kFused && M <= kWaveItabMax) || wave_itab;
   const int64_t gw = int64_t(blockIdx.x) * kWavesPerBlock + wv;
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
 
   // one round trip: validation status, this wave's first workflow, the
-  // instance table
-  const uint32_t status = ld_relaxed_agent(&ctrl->status);
+  // instance table (every load is issued before any is used)
+  // (fused: nothing ran before this kernel in the pass; otherwise written by
+  // earlier kernels only, so a plain load sees it; an uncached load of one
+  // word by every wave would queue at the memory controller)
+  const uint32_t status = kFused ? 0u : ctrl->status;
   int64_t b0 = 0, dl0 = 0, raw0 = 0;
   int n0 = 0;
-  if (gw < a.p.W) {
+  int32_t it_t = 0, it_sp = 1, spec_before = INT32_MIN, spec_at = INT32_MAX;
+  int64_t it_ld = 0, spec_g = 0;
+  int32_t off_first = 0, off_last = 0;
+  if (kFused) {
+    const int ie = wave_itab ? ln : tid;  // the instance this thread loads
+    if (ie < M) {
+      it_t = a.p.inst_type[ie];
+      it_sp = a.p.inst_speed[ie];
+      it_ld = a.p.inst_load[ie];
+    }
+    if (gw < a.p.W) {
+      raw0 = a.p.deadline[gw];
+      if (ln < 2) {  // speculative lower bounds of gw and gw + 1 (lanes 0 and 1)
+        spec_g = ((gw + ln) * a.p.N) / a.p.W;
+        if (spec_g >= 1) spec_before = a.p.wf[spec_g - 1];
+        if (spec_g < a.p.N) spec_at = a.p.wf[spec_g];
+      }
+    }
+    if (gw == 0 && ln == 0) {
+      off_first = a.p.dep_off[0];
+      off_last = a.p.dep_off[a.p.N];
+    }
+  } else if (gw < a.p.W) {
     wf_bounds(a, gw, b0, n0);
     raw0 = a.p.deadline[gw];
-    dl0 = raw0 - a.p.now;
   }
+  dl0 = raw0 - a.p.now;
   ItabStage st;
   st.pending = false;
+  st.build = false;
   if (!kFused && per_wave) itab_stage_load(st, a.itab, M, ln);
 
   const size_t nw = size_t(kWavesPerBlock) * size_t(wcap);
@@ -1176,20 +1295,36 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap
   Wv.dn = sp + size_t(wv) * wcap; sp += nw;
   Wv.nr = sp + size_t(wv) * wcap;
   if (kFused) {
-    if (blockIdx.x == 0) reset_ctrl(a.next_ctrl);  // unused by this pass; ready for the next
-    for (int64_t i = int64_t(blockIdx.x) * kWaveBlock + tid; i < a.bk_clear_n;
-         i += int64_t(gridDim.x) * kWaveBlock)
-      a.bk_clear[i] = 0;
-    if (gw == 0 && ln == 0 && (a.p.dep_off[0] != 0 || int64_t(a.p.dep_off[a.p.N]) != a.p.E))
+    if ((wave_itab ? ln : tid) < M && ((it_t < 0) | (it_sp < 1) | (it_ld < 0) | (it_ld > NALAR_LOAD_MAX)))
       flag_sweep(ctrl, kStInval);
-    if (gw < a.p.W && ln == 0 &&
-        ((raw0 < a.p.now - NALAR_HORIZON_MAX) | (raw0 > a.p.now + NALAR_HORIZON_MAX)))
+    if (gw == 0 && ln == 0 && (off_first != 0 || int64_t(off_last) != a.p.E))
       flag_sweep(ctrl, kStInval);
-    build_itab_block(a.p, it, ctrl, s_itype);
+    if (gw < a.p.W) {
+      // workflow bounds: the speculative guess, else a search (lanes 0 and 1)
+      int32_t lb = 0;
+      if (ln < 2) {
+        const int64_t key = gw + ln;
+        const bool ok = (spec_g == 0 || int64_t(spec_before) < key) &&
+                        (spec_g >= a.p.N || int64_t(spec_at) >= key);
+        lb = ok ? int32_t(spec_g) : int32_t(lower_bound_from(a.p.wf, a.p.N, key, spec_g));
+      }
+      const int32_t lo = readlane_i32(lb, 0), hi = readlane_i32(lb, 1);
+      b0 = lo;
+      n0 = hi - lo;
+      if (ln == 0 && ((n0 < 0) | ((gw == 0) & (lo != 0)) | ((gw == a.p.W - 1) & (int64_t(hi) != a.p.N)) |
+                      (raw0 < a.p.now - NALAR_HORIZON_MAX) | (raw0 > a.p.now + NALAR_HORIZON_MAX)))
+        flag_sweep(ctrl, kStInval);
+    }
+    if (wave_itab) {
+      st.type[0] = it_t;
+      st.speed[0] = it_sp;
+      st.load[0] = it_ld;
+      st.pending = true;
+      st.build = true;
+    } else {
+      build_itab_block(it, M, it_t, it_sp, it_ld, s_itype);
+    }
   } else {
-    for (int64_t i = int64_t(blockIdx.x) * kWaveBlock + tid; i < a.bk_clear_n;
-         i += int64_t(gridDim.x) * kWaveBlock)
-      a.bk_clear[i] = 0;
     if (!per_wave) {  // one shared copy (every thread reaches this barrier)
       for (int i = tid; i < M; i += kWaveBlock) {
         it.load[i] = a.itab.load[i];
@@ -1206,7 +1341,10 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap
   // the validation status read above cannot change during this kernel (the
   // sweep reports into its own word), so every wave of every workgroup
   // leaves together
-  if (status != 0) return;
+  if (status != 0) {
+    clear_for_next_pass<kFused>(a);
+    return;
+  }
 
   const Layout L{a.node_of_pos, a.pos_of_node, a.p.N};
   Acc acc;
@@ -1257,6 +1395,7 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap
     __hip_atomic_fetch_max(&ctrl->part_max[slot], mxv, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     add_agent(&ctrl->part_cnt[slot], rd);
   }
+  clear_for_next_pass<kFused>(a);
 }
 
 constexpr int kBlockT = 1024;
