@@ -76,8 +76,8 @@ def pass_alg_bytes(N: int, E: int, R: int, W: int, M: int) -> float:
 # copy of known size (`python3 bench.py --copy-calibration`).  Valid only for
 # the kernel sources it was taken on: a different source digest reports null.
 TRAFFIC = {
-    ("paper-scale", "sweep"): {"src_sha256": "4f65702664701add8a9e8100c456bd6db5e6203327d3056ebfabd1e2c17d052b",
-                               "bytes_per_launch": 6412921},
+    ("paper-scale", "sweep"): {"src_sha256": "512931106841e2bfdde6beda4afdffaab6b6cada4d822cf52860c3f67b27dca9",
+                               "bytes_per_launch": 8414523},
 }
 
 
