@@ -54,6 +54,7 @@ struct Arena {
   uint32_t* gkey[2] = {nullptr, nullptr};
   uint32_t* gpay[2] = {nullptr, nullptr};
   uint64_t* glb = nullptr;
+  uint64_t* bagg = nullptr;  // bucket-group totals of the look-back bucket kernel
   int32_t* pos_of_node = nullptr;
   int32_t* g_cnt = nullptr;
   int64_t* g_mx = nullptr;
@@ -150,6 +151,7 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B) {
   a.lookback_off = off;
   a.slb = reinterpret_cast<uint64_t*>(take(8 * size_t(kMaxSortPasses) * tiles * kRadixBuckets));
   a.glb = reinterpret_cast<uint64_t*>(take(8 * size_t(kMaxGroupPasses) * tiles * kRadixBuckets));
+  a.bagg = reinterpret_cast<uint64_t*>(take(8 * size_t(kBucketLbGroups)));
   a.lookback_bytes = off - a.lookback_off;
   return align_up(off, 256);
 }
@@ -201,8 +203,11 @@ BucketArgs plan_buckets(const nalar_policy* h, int64_t N) {
   if ((h->flags & NALAR_FORCE_TILED_SORT) || !h->hint_valid || h->bucket_skip > 0 || N == 0 ||
       h->hint_ready > kBucketMaxReady)
     return bk;
+  // about two futures per bucket, four for large ready sets (fewer buckets to
+  // scan and clear; the 64 slots of a bucket still leave ample headroom)
+  const int64_t per = h->hint_ready <= kBucketDense ? 2 : 4;
   int64_t nb = kBucketMin;
-  while (nb < kBucketMax && nb * 2 <= h->hint_ready) nb *= 2;
+  while (nb < kBucketMax && nb * per <= h->hint_ready) nb *= 2;
   int lognb = 0;
   while ((int64_t(1) << lognb) < nb) ++lognb;
   const uint64_t range = uint64_t(h->hint_max) - uint64_t(h->hint_min);
@@ -425,8 +430,8 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     pos_of_node = A.pos_of_node;
   }
 
+  SweepArgs sw{};
   if (N > 0) {
-    SweepArgs sw{};
     sw.p = pd;
     sw.itab = A.itab;
     sw.wf_off = A.wf_off;
@@ -470,6 +475,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   }
   sa.lookback = A.slb;
   sa.tiles_cap = tiles_of(A.capN);
+  sa.bagg = A.bagg;
   sa.epoch = epoch;
   sa.order = r->order;
   sa.slack = r->slack_us;
@@ -483,10 +489,17 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
     if (__atomic_load_n(&h->host->status, __ATOMIC_ACQUIRE) == kStatusTiled) {
+      // A bucket overflowed.  With buckets planned the sweep staged nothing
+      // for the tiled sort, so sweep again without buckets (same results,
+      // staged by position) after resetting the control block it accumulates
+      // into; the next pass's control block and counters are reset again too.
       __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);
       tiled = true;
       h->bucket_skip = h->bucket_backoff;
       h->bucket_backoff = h->bucket_backoff < 64 ? 2 * h->bucket_backoff : 64;
+      NALAR_LAUNCH("reset", launch_reset(s, ctrl, nullptr, 0));
+      sw.bk = BucketArgs{};
+      NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
     } else {
       h->bucket_backoff = 1;
     }

@@ -68,10 +68,19 @@ constexpr uint32_t kStatusContinue = 0x40000000u;
 // every bucket and writes it at its offset.  A bucket that overflows reports
 // kStatusTiled and the host runs the tiled radix sort instead.
 constexpr int kBucketCap = 64;            // slots per bucket
-constexpr int kBucketGroup = 16;          // buckets per workgroup of the bucket kernel
+constexpr int kBucketGroup = 16;          // buckets per workgroup of the small bucket kernel
 constexpr int kBucketMin = 64;            // bucket counts are powers of two in
-constexpr int kBucketMax = 65536;         //   [kBucketMin, kBucketMax]
-constexpr int64_t kBucketMaxReady = 131072;  // larger ready sets use the tiled sort
+constexpr int kBucketMax = 1 << 19;       //   [kBucketMin, kBucketMax]
+constexpr int64_t kBucketMaxReady = int64_t(1) << 22;  // larger ready sets use the tiled sort
+constexpr int64_t kBucketDense = 131072;  // up to here about 2 futures per bucket, then 4
+// From kBucketLbMin buckets on, a first kernel totals each group of
+// kBucketLbGroup buckets and the sort kernel (one workgroup per group) adds up
+// the totals of earlier groups instead of every earlier bucket counter.
+constexpr int kBucketLbMin = 16384;
+constexpr int kBucketLbGroup = 256;
+constexpr int kBucketLbGroups = kBucketMax / kBucketLbGroup;
+static_assert(kBucketLbGroup == 4 * kWave, "one uint4 of counters per lane and group");
+static_assert(kBucketLbMin % kBucketLbGroup == 0, "whole groups");
 constexpr uint32_t kStatusTiled = 0x20000000u;
 
 struct BucketSlot {
@@ -351,7 +360,7 @@ __host__ __device__ inline int64_t floordiv_exact(double a, int32_t d, double in
 // The migration penalty applies to every candidate except the one holding the
 // future's state, so the best candidate is either the unpenalised holder or the
 // best candidate overall plus the penalty (ties broken by index).
-__device__ inline void route_future(int32_t t, int64_t est, int32_t loc, int32_t M, int64_t mig,
+__host__ __device__ inline void route_future(int32_t t, int64_t est, int32_t loc, int32_t M, int64_t mig,
                                     const int32_t* s_type, const int32_t* s_idx,
                                     const int64_t* s_load, const int32_t* s_speed,
                                     const double* s_inv, const int32_t* s_pos,

@@ -44,6 +44,7 @@ struct SortArgs {
   uint32_t* pay[2];
   uint64_t* lookback;           // [passes][tiles_cap][256]
   int64_t tiles_cap;
+  uint64_t* bagg;               // [kBucketLbGroups] futures per group of buckets
   uint32_t epoch;
   int32_t* order;
   int64_t* slack;

@@ -368,6 +368,143 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, Buck
   }
 }
 
+// Large bucket counts.  k_bucket_totals writes the number of futures in each
+// group of kBucketLbGroup buckets; k_bucket_sort_lb then runs one workgroup per
+// group (one bucket per thread), whose base is the sum of the totals of all
+// earlier groups (plain loads: the totals come from the previous kernel, so
+// they are cached like any input).  A future's rank inside its bucket is
+// counted against its bucket-mates' slots directly (a few on average).
+__global__ __launch_bounds__(kBucketLbGroup) void k_bucket_totals(SortArgs a, BucketArgs bk) {
+  constexpr int kPerBlock = kBucketLbGroup / kWave;  // groups per workgroup, one per wave
+  Ctrl* ctrl = a.ctrl;
+  if ((ctrl->status | ctrl->status_sweep) != 0 || ctrl->bucket_overflow != 0) return;
+  const int wv = threadIdx.x / kWave;
+  const int64_t grp = int64_t(blockIdx.x) * kPerBlock + wv;
+  if (grp * kBucketLbGroup >= bk.nb) return;
+  const uint4 c = reinterpret_cast<const uint4*>(bk.cnt + grp * kBucketLbGroup)[lane_id()];
+  const uint32_t cap = uint32_t(kBucketCap);
+  const int64_t t = int64_t((c.x < cap ? c.x : cap) + (c.y < cap ? c.y : cap) +
+                            (c.z < cap ? c.z : cap) + (c.w < cap ? c.w : cap));
+  const int64_t sum = wave_sum_i64(t);
+  if (lane_id() == 0) a.bagg[grp] = uint64_t(sum);
+}
+
+constexpr int kLbStage = 2048;  // futures of a bucket group staged in LDS at once
+static_assert(kLbStage % kBucketLbGroup == 0, "whole rows of the workgroup");
+
+__global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, BucketArgs bk) {
+  __shared__ int64_t s_range[5];
+  __shared__ uint32_t s_off[kBucketLbGroup + 1];
+  __shared__ uint32_t s_red[kBucketLbGroup / kWave];
+  __shared__ int64_t s_base[kBucketLbGroup / kWave];
+  __shared__ int64_t s_slack[kLbStage];
+  __shared__ int32_t s_pos[kLbStage];
+  __shared__ uint8_t s_b[kLbStage];
+  const int tid = threadIdx.x;
+  const int wv = tid / kWave;
+  const int g = blockIdx.x;
+  Ctrl* ctrl = a.ctrl;
+  const uint32_t status = ctrl->status | ctrl->status_sweep;
+  if (status) {
+    if (g == 0 && tid == 0) publish_status(a.host, status, 0, 0, 0, 0);
+    return;
+  }
+  settle_range(ctrl, s_range, g == 0);
+  const int64_t R = s_range[1];
+  if (ctrl->bucket_overflow != 0) {  // written by the sweep, an earlier kernel
+    if (g == 0 && tid == 0)
+      publish_status(a.host, kStatusTiled, R, int(s_range[3]), s_range[0], s_range[4]);
+    return;
+  }
+  if (g == 0 && tid == 0) publish_status(a.host, 0, R, int(s_range[3]), s_range[0], s_range[4]);
+
+  // futures in earlier groups
+  int64_t part = 0;
+  for (int j = tid; j < g; j += kBucketLbGroup) part += int64_t(a.bagg[j]);
+  part = wave_sum_i64(part);
+  // bucket offsets inside the group
+  const int64_t b0 = int64_t(g) * kBucketLbGroup;
+  uint32_t c = bk.cnt[b0 + tid];
+  c = c < uint32_t(kBucketCap) ? c : uint32_t(kBucketCap);  // overflow was handled above
+  const uint32_t inc = wave_incl_scan_u32(c);
+  if (lane_id() == kWave - 1) s_red[wv] = inc;
+  if (lane_id() == 0) s_base[wv] = part;
+  __syncthreads();
+  uint32_t before = 0;
+  int64_t base = 0;
+#pragma unroll
+  for (int w = 0; w < kBucketLbGroup / kWave; ++w) {
+    before += w < wv ? s_red[w] : 0u;
+    base += s_base[w];
+  }
+  s_off[tid + 1] = before + inc;
+  if (tid == 0) s_off[0] = 0;
+  __syncthreads();
+
+  // The group's futures go through LDS in chunks of kLbStage: bucket ids first
+  // (each thread writes its own bucket's), then every slot of the chunk with
+  // independent loads, then each future is ranked among its bucket-mates.  A
+  // bucket cut by a chunk boundary is ranked from its slots in global memory.
+  const int T = int(s_off[kBucketLbGroup]);
+  const int my0 = int(before + inc - c), my1 = int(before + inc);
+  for (int cs = 0; cs < T; cs += kLbStage) {
+    const int ce = T < cs + kLbStage ? T : cs + kLbStage;
+    for (int i = my0 > cs ? my0 : cs; i < (my1 < ce ? my1 : ce); ++i) s_b[i - cs] = uint8_t(tid);
+    __syncthreads();
+    // Addresses first, then every load with no branch between them (a branch
+    // makes the compiler wait for the previous load before the next address).
+    // Past the chunk's end a lane loads slot 0, which always exists, and drops it.
+    int64_t at[kLbStage / kBucketLbGroup];
+#pragma unroll
+    for (int u = 0; u < kLbStage / kBucketLbGroup; ++u) {
+      const int i = cs + u * kBucketLbGroup + tid;
+      const bool ok = i < ce;
+      const int lb = s_b[ok ? i - cs : 0];
+      const int64_t q = (b0 + lb) * kBucketCap + (i - int(s_off[lb]));
+      at[u] = ok ? q : 0;
+    }
+    BucketSlot v[kLbStage / kBucketLbGroup];
+#pragma unroll
+    for (int u = 0; u < kLbStage / kBucketLbGroup; ++u) v[u] = bk.slot[at[u]];
+#pragma unroll
+    for (int u = 0; u < kLbStage / kBucketLbGroup; ++u) {
+      const int i = cs + u * kBucketLbGroup + tid;
+      if (i < ce) {
+        s_slack[i - cs] = v[u].slack;
+        s_pos[i - cs] = v[u].pos;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kLbStage / kBucketLbGroup; ++u) {
+      const int i = cs + u * kBucketLbGroup + tid;
+      if (i >= ce) continue;
+      const int lb = s_b[i - cs];
+      const int k0 = int(s_off[lb]);
+      const int k1 = int(s_off[lb + 1]);
+      int rank = 0;
+      if (k0 >= cs && k1 <= ce) {
+        for (int j = k0 - cs; j < k1 - cs; ++j) {
+          const int64_t o = s_slack[j];
+          rank += (o < v[u].slack) | ((o == v[u].slack) & (s_pos[j] < v[u].pos));
+        }
+      } else {
+        const BucketSlot* sl = bk.slot + (b0 + lb) * kBucketCap;
+        for (int j = 0; j < k1 - k0; ++j) {
+          const int64_t o = sl[j].slack;
+          rank += (o < v[u].slack) | ((o == v[u].slack) & (sl[j].pos < v[u].pos));
+        }
+      }
+      const int64_t out = base + k0 + rank;
+      a.order[out] = a.node_of_pos ? a.node_of_pos[v[u].pos] : v[u].pos;
+      a.slack[out] = v[u].slack;
+      a.route[out] = v[u].route;
+      if (a.cost) a.cost[out] = v[u].cost;
+    }
+    __syncthreads();
+  }
+}
+
 __global__ __launch_bounds__(kSortThreads) void k_slack_hist(SortArgs a) {
   __shared__ uint32_t H[kMaxSortPasses][kRadixBuckets];
   __shared__ int64_t s_range[5];
@@ -482,7 +619,16 @@ hipError_t launch_reset(hipStream_t s, Ctrl* c, uint32_t* clear, int64_t n_clear
 }
 
 hipError_t launch_bucket_sort(hipStream_t s, const SortArgs& a, const BucketArgs& bk) {
-  hipLaunchKernelGGL(k_bucket_sort, dim3(bk.nb / kBucketGroup), dim3(kBucketThreads), 0, s, a, bk);
+  if (bk.nb >= kBucketLbMin) {
+    const int groups = bk.nb / kBucketLbGroup;
+    const int per_block = kBucketLbGroup / kWave;
+    hipLaunchKernelGGL(k_bucket_totals, dim3((groups + per_block - 1) / per_block), dim3(kBucketLbGroup),
+                       0, s, a, bk);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_bucket_sort_lb, dim3(groups), dim3(kBucketLbGroup), 0, s, a, bk);
+  } else
+    hipLaunchKernelGGL(k_bucket_sort, dim3(bk.nb / kBucketGroup), dim3(kBucketThreads), 0, s, a, bk);
   return hipGetLastError();
 }
 

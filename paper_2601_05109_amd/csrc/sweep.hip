@@ -238,10 +238,13 @@ __device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_
   int64_t cost;
   route_future(type, est, loc, int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load, it.speed,
                it.inv, it.pos, it.run, route, cost);
-  a.stg_slack[pos] = slack;
-  a.stg_route[pos] = route;
-  a.stg_cost[pos] = cost;
-  if (bk.nb > 0) bucket_put(a, bkt, slot, slack, pos, route, cost);
+  if (bk.nb > 0) {
+    bucket_put(a, bkt, slot, slack, pos, route, cost);
+  } else {  // staged by position for the tiled sort
+    a.stg_slack[pos] = slack;
+    a.stg_route[pos] = route;
+    a.stg_cost[pos] = cost;
+  }
   acc.tmin = slack < acc.tmin ? slack : acc.tmin;
   acc.tmax = slack > acc.tmax ? slack : acc.tmax;
   acc.tready += 1;
@@ -363,7 +366,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
       const int k = j * T + tid;
       const bool rd = dn[k] == 0 && nr[k] == 0;
       if (rd) ready |= 1u << j;
-      a.stg_ready[b + k] = rd ? 1 : 0;
+      if (a.bk.nb == 0) a.stg_ready[b + k] = rd ? 1 : 0;
     }
   }
   if (tid == 0) S.hcount = 0;
@@ -433,23 +436,58 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
   }
   if (overflow) flag_sweep(ctrl, kStRange);
   if (fin) atomicAdd(&S.proc, __popc(fin));
+  __syncthreads();  // nothing is in flight here, so this barrier waits for no store
+  if (tid == 0 && S.proc != n) flag_sweep(ctrl, kStCycle);
+
+  // D: every bucket-slot atomic first, then the rem stores, then the routing
+  // (LDS and arithmetic only) while the atomics are in flight, then the
+  // stores of the ready futures.  No barrier follows: the next workflow of
+  // this workgroup touches only its own threads' LDS entries before its
+  // first barrier.
+  const BucketArgs& bk = a.bk;
+  uint32_t bkt[NPT], slot[NPT];
+#pragma unroll
+  for (int j = 0; j < NPT; ++j) {
+    bkt[j] = 0;
+    slot[j] = 0;
+    if (bk.nb > 0 && ((ready >> j) & 1u)) {
+      bkt[j] = bucket_of(bk, dl - mx[j * T + tid]);
+      slot[j] = add_agent(bk.cnt + bkt[j], 1u);
+    }
+  }
   if (a.rem_out) {  // rem stayed in LDS during the levels; store it once
 #pragma unroll
     for (int j = 0; j < NPT; ++j)
       if ((fin >> j) & 1u) a.rem_out[vv[j]] = mx[j * T + tid];
   }
-  __syncthreads();
-  if (tid == 0 && S.proc != n) flag_sweep(ctrl, kStCycle);
-
-  // D: slack, route, staged at the future's position
+  int32_t route[NPT];
+  int64_t cost[NPT];
 #pragma unroll
   for (int j = 0; j < NPT; ++j) {
-    if ((ready >> j) & 1u) {
-      const int k = j * T + tid;
-      write_ready(a, it, b + k, ty[j], lc[j], mx[k], ee[j], dl, acc);
-    }
+    route[j] = -1;
+    cost[j] = 0;
+    if ((ready >> j) & 1u)
+      route_future(ty[j], ee[j], lc[j], int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load, it.speed,
+                   it.inv, it.pos, it.run, route[j], cost[j]);
   }
-  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < NPT; ++j) __asm__ __volatile__("" : "+v"(slot[j]) :: "memory");
+#pragma unroll
+  for (int j = 0; j < NPT; ++j) {
+    if (!((ready >> j) & 1u)) continue;
+    const int k = j * T + tid;
+    const int64_t slack = dl - mx[k];
+    if (bk.nb > 0) {
+      bucket_put(a, bkt[j], slot[j], slack, b + k, route[j], cost[j]);
+    } else {
+      a.stg_slack[b + k] = slack;
+      a.stg_route[b + k] = route[j];
+      a.stg_cost[b + k] = cost[j];
+    }
+    acc.tmin = slack < acc.tmin ? slack : acc.tmin;
+    acc.tmax = slack > acc.tmax ? slack : acc.tmax;
+    acc.tready += 1;
+  }
 }
 
 // ------------------------------------------------------------ HBM workflow
@@ -544,7 +582,8 @@ __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, con
   }
   __syncthreads();
 
-  for (int k = tid; k < n; k += T) a.stg_ready[b + k] = (dn[k] == 0 && nr[k] == 0) ? 1 : 0;
+  if (a.bk.nb == 0)
+    for (int k = tid; k < n; k += T) a.stg_ready[b + k] = (dn[k] == 0 && nr[k] == 0) ? 1 : 0;
   if (tid == 0) S.hcount = 0;
 
   // frontier 0: futures without consumers
@@ -1005,14 +1044,17 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
   for (int j = 0; j < NPTW; ++j) {
     if (!((own >> j) & 1u)) continue;
     const int64_t pos = b + j * kWave + ln;
-    a.stg_ready[pos] = uint8_t((ready >> j) & 1u);
+    if (bk.nb == 0) a.stg_ready[pos] = uint8_t((ready >> j) & 1u);
     if (a.rem_out) a.rem_out[vv[j]] = rr[j];
     if ((ready >> j) & 1u) {
       const int64_t slack = dl - rr[j];
-      a.stg_slack[pos] = slack;
-      a.stg_route[pos] = route[j];
-      a.stg_cost[pos] = cost[j];
-      if (bk.nb > 0) bucket_put(a, bkt[j], slot[j], slack, pos, route[j], cost[j]);
+      if (bk.nb > 0) {
+        bucket_put(a, bkt[j], slot[j], slack, pos, route[j], cost[j]);
+      } else {  // staged by position for the tiled sort
+        a.stg_slack[pos] = slack;
+        a.stg_route[pos] = route[j];
+        a.stg_cost[pos] = cost[j];
+      }
       acc.tmin = slack < acc.tmin ? slack : acc.tmin;
       acc.tmax = slack > acc.tmax ? slack : acc.tmax;
       acc.tready += 1;

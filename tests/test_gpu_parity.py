@@ -205,6 +205,23 @@ def test_sort_path_switching():
             check(pol, p, label)
 
 
+def test_large_ready_set_bucketed():
+    """About a million ready futures on one handle: the first pass uses the
+    tiled sort, later passes the bucketed sort whose workgroups find their base
+    from the published totals of earlier workgroups; every pass matches."""
+    p = wl.wide_mapreduce()
+    o = oracle.run(p)
+    with nalar.Policy() as pol:
+        pol.set_timing(True)
+        for i in range(3):
+            g = gpu_run(pol, p)
+            assert_parity(g, o, f"wide map/reduce pass {i}")
+            names = [n for n, _ in pol.timing()]
+            say(f"[gpu] pass {i}: {names}")
+            if i > 0:
+                assert "sort_bucket" in names
+
+
 def test_other_seeds(policy):
     for s in (11, 12):
         check(policy, wl.paper_scale(seed=s), f"paper-scale seed {s}")

@@ -98,3 +98,18 @@ def test_exact_division_helper(tmp_path):
     r = subprocess.run([str(exe)], capture_output=True, text=True)
     assert r.returncode == 0, r.stdout
     assert "mismatches 0" in r.stdout
+
+
+def test_routing_scorer(tmp_path):
+    """The routing scorer against a plain integer argmin on random, tied and
+    near-tied instance tables, loads near 2^60, speeds near 2^31 and
+    estimates near 2^40."""
+    exe = tmp_path / "routing_check"
+    hipcc = "/opt/rocm/bin/hipcc"
+    subprocess.run([hipcc, "-O2", "-std=c++17", "-I", os.path.join(ROOT, "include"),
+                    "-I", os.path.join(ROOT, "paper_2601_05109_amd", "csrc"),
+                    os.path.join(ROOT, "tests", "routing_check.cpp"), "-o", str(exe)],
+                   check=True, capture_output=True)
+    r = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stdout
+    assert "mismatches 0" in r.stdout
