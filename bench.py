@@ -12,6 +12,9 @@ library on its own stream during a second timed loop), and the CPU oracle timed
 on this host as a baseline.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload paper-scale]
+
+Other workloads: tiny, deep-chains, wide-mapreduce, and dynamic (the evolving
+map/reduce graph: per-step pass latency over 100 steps, p50/p99).
 """
 from __future__ import annotations
 
@@ -155,6 +158,91 @@ def cpu_baseline(p, budget_s: float = 12.0) -> dict:
             "ms_per_pass": 1e3 * el / reps}
 
 
+def dynamic(args) -> int:
+    """The evolving map/reduce graph (1% of running futures complete and 1% of
+    nodes gain 1-4 children per step): every snapshot is uploaded (timed
+    apart, not part of the pass), passed once untimed (scratch growth), then
+    ``--dyn-reps`` times with HIP events on the library stream; a step's
+    latency is the median of its reps."""
+    import torch
+    from paper_2601_05109_amd import nalar, workloads as wl
+
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream(dev)
+    pol = nalar.Policy(device=0, stream=stream)
+    out = None
+    rows = []
+    t_all = time.perf_counter()
+    for step, p in enumerate(wl.dynamic_stream(steps=args.dyn_steps)):
+        t = time.perf_counter()
+        dp = nalar.DeviceProblem.from_host(p, dev)
+        torch.cuda.synchronize()
+        up_ms = 1e3 * (time.perf_counter() - t)
+        N = p.n_nodes
+        if out is None or out.order.shape[0] < N:
+            out = nalar.DeviceResult.alloc(int(N * 1.3), dev)
+        cp = dp.c_struct()
+
+        def one_pass():
+            cr = out.c_struct()
+            rc = nalar.nalar_policy_pass(pol.handle, cp, cr)
+            if rc != nalar.NALAR_OK:
+                raise RuntimeError(f"step {step}: pass failed {rc}: {pol.last_error()}")
+            return int(cr.n_ready)
+
+        R = one_pass()
+        times = []
+        for _ in range(args.dyn_reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            one_pass()
+            e1.record(stream)
+            e1.synchronize()
+            times.append(1e3 * e0.elapsed_time(e1))
+        row = {"step": step, "n": N, "e": p.n_edges, "ready": R, "us": statistics.median(times),
+               "upload_ms": up_ms}
+        if step % 25 == 0:  # per-kernel events on the library stream
+            pol.set_timing(True)
+            one_pass()
+            row["kernels_us"] = {}
+            for name, ms in pol.timing():
+                row["kernels_us"][name] = round(row["kernels_us"].get(name, 0.0) + 1e3 * ms, 2)
+            pol.set_timing(False)
+        rows.append(row)
+        if step % 10 == 0:
+            print(f"step {step}: N={N} R={R} pass {rows[-1]['us']:.1f} us (upload {up_ms:.1f} ms)",
+                  file=sys.stderr, flush=True)
+    pol.close()
+    lat = sorted(r["us"] for r in rows[1:]) or [rows[0]["us"]]
+    q = lambda f: lat[min(len(lat) - 1, int(f * len(lat)))]
+    rates = sorted(r["n"] / (r["us"] * 1e-6) for r in rows[1:]) or [rows[0]["n"] / (rows[0]["us"] * 1e-6)]
+    first, last = rows[0], rows[-1]
+    res = {
+        "metric": "futures/sec per global policy pass",
+        "value": rates[len(rates) // 2],
+        "unit": "futures/s",
+        "n_gpus": 1,
+        "steps": len(rows),
+        "warmup": 1,
+        "ms_per_step": q(0.5) * 1e-3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic (seeded generator, evolving map/reduce graph)",
+        "config": {"workload": f"dynamic-stream: {first['n']} -> {last['n']} futures over "
+                               f"{len(rows) - 1} steps, ids not workflow-contiguous after step 0",
+                   "n_futures_first": first["n"], "n_futures_last": last["n"]},
+        "latency_us": {"p50": q(0.5), "p99": q(0.99), "step0": first["us"], "last_step": last["us"]},
+        "per_step": [{k: (round(v, 2) if isinstance(v, float) else v) for k, v in r.items()}
+                     for r in rows],
+        "wall_s": time.perf_counter() - t_all,
+    }
+    print(json.dumps(res))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -163,6 +251,8 @@ def main() -> int:
     ap.add_argument("--workload", default="paper-scale")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--dyn-steps", type=int, default=100, help="dynamic workload: steps after step 0")
+    ap.add_argument("--dyn-reps", type=int, default=5, help="dynamic workload: timed passes per step")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only plain copies of known size (for scaling HBM byte counters)")
     args = ap.parse_args()
@@ -172,6 +262,8 @@ def main() -> int:
         return 2
     if args.copy_calibration:
         return copy_calibration()
+    if args.workload == "dynamic":
+        return dynamic(args)
 
     import torch
     from paper_2601_05109_amd import nalar
