@@ -249,6 +249,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="paper-scale")
+    ap.add_argument("--policy", default="srtf", choices=["srtf", "lpt", "stateful", "lpt+stateful"],
+                    help="policy variant: order by slack (srtf) or by remaining work (lpt); "
+                         "stateful pins futures to the instance holding their state")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--dyn-steps", type=int, default=100, help="dynamic workload: steps after step 0")
@@ -275,7 +278,9 @@ def main() -> int:
     out = nalar.DeviceResult.alloc(N, dev)
     stream = torch.cuda.current_stream(dev)
     pol = nalar.Policy(device=0, stream=stream, reserve_nodes=N, reserve_workflows=W)
-    cp = dp.c_struct()
+    bits = {"srtf": 0, "lpt": nalar.NALAR_ORDER_LPT, "stateful": nalar.NALAR_ROUTE_STATEFUL,
+            "lpt+stateful": nalar.NALAR_ORDER_LPT | nalar.NALAR_ROUTE_STATEFUL}[args.policy]
+    cp = dp.c_struct(policy=bits)
 
     def one_pass():
         cr = out.c_struct()
@@ -338,7 +343,7 @@ def main() -> int:
         "data": "synthetic (seeded generator, paper-scale shape)",
         "config": {"workload": f"{p.name}: {W} workflows x {N // max(W, 1)} futures = {N} futures, "
                                f"{E} dependencies, {R} ready, K=8 types, {M} instances",
-                   "n_futures": N, "n_ready": R},
+                   "n_futures": N, "n_ready": R, "policy": args.policy},
         "latency_us": {"p50": lat_us[len(lat_us) // 2], "p99": lat_us[min(len(lat_us) - 1, int(0.99 * len(lat_us)))],
                        "min": lat_us[0], "gpu_event_mean": 1e3 * gpu_ms / args.steps},
         "kernels_us": {k: round(1e3 * v, 2) for k, v in kern.items()},

@@ -65,6 +65,19 @@ enum {
                                     promises it; a violation is NALAR_EINVAL.
                                     Without it the library groups nodes by
                                     workflow itself (one extra sort).           */
+/* Policy variants of the same pass (nalar_problem.flags; 0 = the default
+ * SRTF-by-slack order and load-and-locality routing): */
+#define NALAR_ORDER_LPT      2u  /* order = ready futures by (-rem, wf, id)
+                                    ascending: longest remaining processing
+                                    first (the LPT policy, Section 6.2); the
+                                    slack output is unchanged                   */
+#define NALAR_ROUTE_STATEFUL 4u  /* a ready future whose state lives on an
+                                    instance of its own type (loc[v] >= 0 and
+                                    inst_type[loc[v]] == type[v]) is routed there
+                                    with no other candidate and no migration
+                                    penalty (the stateful directive, Table 1;
+                                    managed-state routing, Section 4.3.2); every
+                                    other future is routed by the default rule */
 
 /* nalar_policy_config.flags (tuning and testing; 0 is the normal setting) */
 #define NALAR_FORCE_GLOBAL_SWEEP 1u  /* keep every workflow's sweep state in HBM
@@ -101,7 +114,8 @@ typedef struct {
   int64_t now_us;             /* |now_us| <= NALAR_HORIZON_MAX                    */
   int64_t migration_cost_us;  /* penalty for running a future away from the
                                  instance holding its state, [0, NALAR_MIG_MAX]   */
-  uint32_t flags;             /* NALAR_WF_CONTIGUOUS or 0                         */
+  uint32_t flags;             /* NALAR_WF_CONTIGUOUS, NALAR_ORDER_LPT,
+                                 NALAR_ROUTE_STATEFUL bits, or 0                  */
   uint32_t reserved;          /* must be 0                                        */
   const int32_t* wf;          /* [N] workflow (session) of each future, [0, W)    */
   const int32_t* type;        /* [N] component type, >= 0                         */
@@ -158,6 +172,8 @@ int nalar_policy_create(const nalar_policy_config* cfg, nalar_policy** out);
  *              (cost(v,i), i) lexicographically (the lowest index wins ties),
  *              or -1 with cost INT64_MAX when there is none
  *   order    = the ready futures sorted by (slack, wf, id) ascending
+ * (the NALAR_ORDER_LPT and NALAR_ROUTE_STATEFUL bits change order and route as
+ * described at their definitions).
  * Synchronous.  NULL p, r, or a required array (a node array when N > 0,
  * dep_idx when E > 0, deadline_us when W > 0, an instance array when M > 0,
  * order/slack_us/route when N > 0) is NALAR_EINVAL.  Error precedence and the

@@ -24,6 +24,10 @@ CXXFLAGS = ["-O2", "-std=c++17", "-shared", "-fPIC", "-Wall", "-Wextra"]
 
 OK, EINVAL, ECYCLE, ERANGE = 0, -1, -2, -3
 
+# policy variants (the same bits as the library's problem flags)
+POLICY_LPT = 2        # order by remaining critical path, longest first
+POLICY_STATEFUL = 4   # a future whose state lives on an instance of its type runs there
+
 _lock = threading.Lock()
 _lib: Optional[ctypes.CDLL] = None
 
@@ -48,6 +52,8 @@ def _load() -> ctypes.CDLL:
         I64 = ctypes.c_int64
         lib.nalar_oracle_pass.restype = ctypes.c_int
         lib.nalar_oracle_pass.argtypes = [I64] * 6 + [P] * 17
+        lib.nalar_oracle_pass_policy.restype = ctypes.c_int
+        lib.nalar_oracle_pass_policy.argtypes = [I64] * 6 + [ctypes.c_uint32] + [P] * 17
         _lib = lib
     return _lib
 
@@ -67,10 +73,11 @@ def _ptr(a: Optional[np.ndarray]):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
 
-def run(p, *, want_rem: bool = True, override: Optional[dict] = None) -> OracleResult:
+def run(p, *, want_rem: bool = True, override: Optional[dict] = None,
+        policy: int = 0) -> OracleResult:
     """Run the oracle on a problem (any object with the workloads.Problem
     fields).  ``override`` may replace scalar sizes or set arrays to None, to
-    exercise validation."""
+    exercise validation; ``policy`` selects the variants (POLICY_* bits)."""
     lib = _load()
     o = dict(N=p.n_nodes, E=p.n_edges, W=p.n_workflows, M=p.n_instances,
              now=p.now_us, mig=p.migration_cost_us)
@@ -90,8 +97,8 @@ def run(p, *, want_rem: bool = True, override: Optional[dict] = None) -> OracleR
     route = np.zeros(n_out, np.int32)
     cost = np.zeros(n_out, np.int64)
     n_ready = ctypes.c_int64(0)
-    rc = lib.nalar_oracle_pass(
-        o["N"], o["E"], o["W"], o["M"], o["now"], o["mig"],
+    rc = lib.nalar_oracle_pass_policy(
+        o["N"], o["E"], o["W"], o["M"], o["now"], o["mig"], policy,
         *[_ptr(arrays[f]) for f in ("wf", "type", "est_us", "done", "loc", "dep_off",
                                     "dep_idx", "deadline_us", "inst_type", "inst_load_us",
                                     "inst_speed_permille")],

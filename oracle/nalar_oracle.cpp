@@ -32,6 +32,16 @@
 //   O9  order = the ready futures sorted by (slack, wf, v) ascending
 //   O10 write rem, order, slack, route, cost and the ready count.
 //
+// Policy variants (the policy word of nalar_oracle_pass_policy):
+//   kLpt       O9 sorts by (-rem, wf, v) instead: the future with the longest
+//              remaining processing first (the LPT policy, Section 6.2); slack
+//              is still reported as in O7
+//   kStateful  O8 for a future whose state lives on an instance of its own
+//              type: route = that instance, cost without migration penalty,
+//              no other candidate (the stateful directive, Table 1, and the
+//              managed-state routing guarantee, Section 4.3.2); other futures
+//              are routed as in O8
+//
 // Precedence of errors: EINVAL, then ECYCLE, then ERANGE.
 #include <algorithm>
 #include <cstdint>
@@ -44,6 +54,9 @@ constexpr int kOk = 0;
 constexpr int kEinval = -1;
 constexpr int kEcycle = -2;
 constexpr int kErange = -3;
+
+constexpr uint32_t kLpt = 2u;
+constexpr uint32_t kStateful = 4u;
 
 constexpr int64_t kMaxNodes = int64_t(1) << 30;
 constexpr int64_t kMaxEdges = (int64_t(1) << 31) - 1;
@@ -105,14 +118,15 @@ extern "C" {
 // The boundary of the oracle: host arrays in, host arrays out.  Output arrays
 // must hold n_nodes entries (rem) and n_nodes entries (order, slack, route,
 // cost); rem_out and cost_out may be NULL.  Returns 0 or a negative error code.
-int nalar_oracle_pass(int64_t N, int64_t E, int64_t W, int64_t M, int64_t now, int64_t mig,
-                      const int32_t* wf, const int32_t* type, const int64_t* est,
-                      const uint8_t* done, const int32_t* loc, const int32_t* dep_off,
-                      const int32_t* dep_idx, const int64_t* deadline,
-                      const int32_t* inst_type, const int64_t* inst_load,
-                      const int32_t* inst_speed, int64_t* rem_out, int32_t* order_out,
-                      int64_t* slack_out, int32_t* route_out, int64_t* cost_out,
-                      int64_t* n_ready_out) {
+int nalar_oracle_pass_policy(int64_t N, int64_t E, int64_t W, int64_t M, int64_t now, int64_t mig,
+                             uint32_t policy, const int32_t* wf, const int32_t* type,
+                             const int64_t* est, const uint8_t* done, const int32_t* loc,
+                             const int32_t* dep_off, const int32_t* dep_idx,
+                             const int64_t* deadline, const int32_t* inst_type,
+                             const int64_t* inst_load, const int32_t* inst_speed, int64_t* rem_out,
+                             int32_t* order_out, int64_t* slack_out, int32_t* route_out,
+                             int64_t* cost_out, int64_t* n_ready_out) {
+  if ((policy & ~(kLpt | kStateful)) != 0) return kEinval;
   int rc = validate(N, E, W, M, now, mig, wf, type, est, done, loc, dep_off, dep_idx,
                     deadline, inst_type, inst_load, inst_speed);
   if (rc != kOk) return rc;
@@ -188,6 +202,12 @@ int nalar_oracle_pass(int64_t N, int64_t E, int64_t W, int64_t M, int64_t now, i
   for (int64_t k = 0; k < R; ++k) {
     int32_t v = ready_ids[k];
     slack[v] = (deadline[wf[v]] - now) - rem[v];
+    if ((policy & kStateful) && loc[v] >= 0 && inst_type[loc[v]] == type[v]) {
+      const int32_t i = loc[v];
+      route[v] = i;
+      cost[v] = inst_load[i] + (est[v] * 1000) / inst_speed[i];
+      continue;
+    }
     int64_t best = INT64_MAX;
     int32_t arg = -1;
     for (int64_t i = 0; i < M; ++i) {
@@ -200,10 +220,14 @@ int nalar_oracle_pass(int64_t N, int64_t E, int64_t W, int64_t M, int64_t now, i
     cost[v] = best;
   }
 
-  // O9: the full key (slack, wf, v) is a total order, so the result is unique.
+  // O9: the full key (slack, wf, v), or (-rem, wf, v) under kLpt, is a total
+  // order, so the result is unique.
+  const bool lpt = (policy & kLpt) != 0;
   std::vector<int32_t> order(ready_ids);
   std::sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
-    if (slack[a] != slack[b]) return slack[a] < slack[b];
+    const int64_t ka = lpt ? -rem[a] : slack[a];
+    const int64_t kb = lpt ? -rem[b] : slack[b];
+    if (ka != kb) return ka < kb;
     if (wf[a] != wf[b]) return wf[a] < wf[b];
     return a < b;
   });
@@ -219,6 +243,20 @@ int nalar_oracle_pass(int64_t N, int64_t E, int64_t W, int64_t M, int64_t now, i
   }
   if (n_ready_out) *n_ready_out = R;
   return kOk;
+}
+
+// The default policy (SRTF order by slack, load-and-locality routing).
+int nalar_oracle_pass(int64_t N, int64_t E, int64_t W, int64_t M, int64_t now, int64_t mig,
+                      const int32_t* wf, const int32_t* type, const int64_t* est,
+                      const uint8_t* done, const int32_t* loc, const int32_t* dep_off,
+                      const int32_t* dep_idx, const int64_t* deadline,
+                      const int32_t* inst_type, const int64_t* inst_load,
+                      const int32_t* inst_speed, int64_t* rem_out, int32_t* order_out,
+                      int64_t* slack_out, int32_t* route_out, int64_t* cost_out,
+                      int64_t* n_ready_out) {
+  return nalar_oracle_pass_policy(N, E, W, M, now, mig, 0u, wf, type, est, done, loc, dep_off,
+                                  dep_idx, deadline, inst_type, inst_load, inst_speed, rem_out,
+                                  order_out, slack_out, route_out, cost_out, n_ready_out);
 }
 
 }  // extern "C"

@@ -48,6 +48,7 @@ struct Arena {
   int64_t* stg_slack = nullptr;
   int32_t* stg_route = nullptr;
   int64_t* stg_cost = nullptr;
+  int64_t* stg_oslack = nullptr;  // slack by position when the order key is not the slack
   uint64_t* skey[2] = {nullptr, nullptr};
   uint32_t* spay[2] = {nullptr, nullptr};
   uint64_t* slb = nullptr;
@@ -134,6 +135,7 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B) {
   a.stg_cost = reinterpret_cast<int64_t*>(take(8 * size_t(n1)));
   a.stg_route = reinterpret_cast<int32_t*>(take(4 * size_t(n1)));
   a.stg_ready = reinterpret_cast<uint8_t*>(take(size_t(n1)));
+  a.stg_oslack = reinterpret_cast<int64_t*>(take(8 * size_t(n1)));
   for (int i = 0; i < 2; ++i) a.skey[i] = reinterpret_cast<uint64_t*>(take(8 * size_t(n1)));
   for (int i = 0; i < 2; ++i) a.spay[i] = reinterpret_cast<uint32_t*>(take(4 * size_t(n1)));
   for (int i = 0; i < 2; ++i) a.gkey[i] = reinterpret_cast<uint32_t*>(take(4 * size_t(n1)));
@@ -231,7 +233,8 @@ int check_problem(nalar_policy* h, const nalar_problem* p, const nalar_result* r
     return fail(h, NALAR_EINVAL, "now_us out of range");
   if (!in_range(p->migration_cost_us, 0, NALAR_MIG_MAX))
     return fail(h, NALAR_EINVAL, "migration_cost_us out of range");
-  if ((p->flags & ~NALAR_WF_CONTIGUOUS) != 0 || p->reserved != 0)
+  if ((p->flags & ~(NALAR_WF_CONTIGUOUS | NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL)) != 0 ||
+      p->reserved != 0)
     return fail(h, NALAR_EINVAL, "unknown problem flags");
   if (N == 0 && E != 0) return fail(h, NALAR_EINVAL, "edges without nodes");
   if (N > 0 && (!p->wf || !p->type || !p->est_us || !p->done || !p->loc || !p->dep_off))
@@ -383,7 +386,8 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   h->ctrl_dirty[cur] = true;
   h->ctrl_dirty[nxt] = true;
 
-  ProblemDev pd{N, p->n_edges, W, M, p->now_us, p->migration_cost_us,
+  const uint32_t policy = p->flags & (NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL);
+  ProblemDev pd{N, p->n_edges, W, M, p->now_us, p->migration_cost_us, policy, 0u,
                 p->wf, p->type, p->est_us, p->done, p->loc, p->dep_off, p->dep_idx,
                 p->deadline_us, p->inst_type, p->inst_load_us, p->inst_speed_permille};
   const bool contiguous = (p->flags & NALAR_WF_CONTIGUOUS) != 0 || W <= 1;
@@ -442,6 +446,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     sw.stg_slack = A.stg_slack;
     sw.stg_route = A.stg_route;
     sw.stg_cost = A.stg_cost;
+    sw.stg_oslack = A.stg_oslack;
     sw.g_cnt = A.g_cnt;
     sw.g_mx = A.g_mx;
     sw.g_dn = A.g_dn;
@@ -468,6 +473,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   sa.stg_route = A.stg_route;
   sa.stg_cost = A.stg_cost;
   sa.node_of_pos = node_of_pos;
+  sa.out_slack = (policy & NALAR_ORDER_LPT) ? A.stg_oslack : nullptr;
   sa.span = N;
   for (int i = 0; i < 2; ++i) {
     sa.key[i] = A.skey[i];

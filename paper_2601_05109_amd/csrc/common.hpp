@@ -84,7 +84,7 @@ static_assert(kBucketLbMin % kBucketLbGroup == 0, "whole groups");
 constexpr uint32_t kStatusTiled = 0x20000000u;
 
 struct BucketSlot {
-  int64_t slack;
+  int64_t key;      // the order key: the slack, or -rem under NALAR_ORDER_LPT
   int64_t cost;
   int32_t pos;
   int32_t route;
@@ -359,12 +359,23 @@ __host__ __device__ inline int64_t floordiv_exact(double a, int32_t d, double in
 // Candidates are the instances of type t, visited in ascending original index.
 // The migration penalty applies to every candidate except the one holding the
 // future's state, so the best candidate is either the unpenalised holder or the
-// best candidate overall plus the penalty (ties broken by index).
+// best candidate overall plus the penalty (ties broken by index).  With
+// `stateful`, a future whose state lives on an instance of its own type runs
+// there, at that instance's cost and with no other candidate.
 __host__ __device__ inline void route_future(int32_t t, int64_t est, int32_t loc, int32_t M, int64_t mig,
                                     const int32_t* s_type, const int32_t* s_idx,
                                     const int64_t* s_load, const int32_t* s_speed,
                                     const double* s_inv, const int32_t* s_pos,
-                                    const uint32_t* s_run, int32_t& route, int64_t& cost) {
+                                    const uint32_t* s_run, bool stateful, int32_t& route,
+                                    int64_t& cost) {
+  if (stateful && loc >= 0) {
+    const int pl = s_pos[loc];
+    if (s_type[pl] == t) {
+      route = loc;
+      cost = s_load[pl] + floordiv_exact(double(est * 1000), s_speed[pl], s_inv[pl]);
+      return;
+    }
+  }
   int lo, hi;
   if (uint32_t(t) < uint32_t(kTypeDirect)) {
     const uint32_t rn = s_run[t];

@@ -12,6 +12,8 @@ namespace nalar {
 struct ProblemDev {
   int64_t N, E, W, M;
   int64_t now, mig;
+  uint32_t policy;              // NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL bits
+  uint32_t pad_;
   const int32_t* wf;
   const int32_t* type;
   const int64_t* est;
@@ -39,6 +41,7 @@ struct SortArgs {
   const int32_t* stg_route;
   const int64_t* stg_cost;
   const int32_t* node_of_pos;   // NULL: position == node id
+  const int64_t* out_slack;     // [N] by position, or NULL: the slack is the key
   int64_t span;                 // N
   uint64_t* key[2];             // ping-pong buffers
   uint32_t* pay[2];
@@ -83,6 +86,8 @@ struct SweepArgs {
   const int32_t* pos_of_node;   // NULL: position == node id
   int64_t* rem_out;             // [N] or NULL
   uint8_t* stg_ready;           // [N] by position: 1 = ready
+  int64_t* stg_oslack;          // [N] by position: slack of ready futures when the
+                                //   sort key is not the slack (NALAR_ORDER_LPT)
   int64_t* stg_slack;           // [N] by position, written for ready futures
   int32_t* stg_route;
   int64_t* stg_cost;

@@ -108,6 +108,7 @@ __device__ void histogram(const FirstSource& f, int npass, uint32_t (*H)[kRadixB
 struct FinalOut {
   bool on;
   const int32_t* node_of_pos;   // NULL: position == node id
+  const int64_t* out_slack;     // by position, or NULL: the slack is the key
   const int32_t* stg_route;
   const int64_t* stg_cost;
   int64_t smin;
@@ -218,7 +219,7 @@ __device__ void radix_tile(TileSmem<K>& S, const FirstSource& f, bool first, int
     if (fo.on) {  // last pass: gather the ready future's decision into place
       const uint32_t pos = S.pay[i];
       fo.order[g] = fo.node_of_pos ? fo.node_of_pos[pos] : int32_t(pos);
-      fo.slack[g] = int64_t(uint64_t(k) + uint64_t(fo.smin));
+      fo.slack[g] = fo.out_slack ? fo.out_slack[pos] : int64_t(uint64_t(k) + uint64_t(fo.smin));
       fo.route[g] = fo.stg_route[pos];
       if (fo.cost) fo.cost[g] = fo.stg_cost[pos];
     } else {
@@ -343,7 +344,7 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, Buck
 #pragma unroll
     for (int k = 1; k < kBucketGroup; ++k) b += int(s_off[k]) <= i;
     const BucketSlot* sl = bk.slot + (int64_t(g) * kBucketGroup + b) * kBucketCap + (i - int(s_off[b]));
-    s_slack[i] = sl->slack;
+    s_slack[i] = sl->key;
     s_cost[i] = sl->cost;
     s_pos[i] = sl->pos;
     s_route[i] = sl->route;
@@ -362,7 +363,7 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, Buck
     }
     const int64_t out = base + lo + rank;
     a.order[out] = a.node_of_pos ? a.node_of_pos[ps] : ps;
-    a.slack[out] = sk;
+    a.slack[out] = a.out_slack ? a.out_slack[ps] : sk;
     a.route[out] = s_route[i];
     if (a.cost) a.cost[out] = s_cost[i];
   }
@@ -470,7 +471,7 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
     for (int u = 0; u < kLbStage / kBucketLbGroup; ++u) {
       const int i = cs + u * kBucketLbGroup + tid;
       if (i < ce) {
-        s_slack[i - cs] = v[u].slack;
+        s_slack[i - cs] = v[u].key;
         s_pos[i - cs] = v[u].pos;
       }
     }
@@ -486,18 +487,18 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
       if (k0 >= cs && k1 <= ce) {
         for (int j = k0 - cs; j < k1 - cs; ++j) {
           const int64_t o = s_slack[j];
-          rank += (o < v[u].slack) | ((o == v[u].slack) & (s_pos[j] < v[u].pos));
+          rank += (o < v[u].key) | ((o == v[u].key) & (s_pos[j] < v[u].pos));
         }
       } else {
         const BucketSlot* sl = bk.slot + (b0 + lb) * kBucketCap;
         for (int j = 0; j < k1 - k0; ++j) {
-          const int64_t o = sl[j].slack;
-          rank += (o < v[u].slack) | ((o == v[u].slack) & (sl[j].pos < v[u].pos));
+          const int64_t o = sl[j].key;
+          rank += (o < v[u].key) | ((o == v[u].key) & (sl[j].pos < v[u].pos));
         }
       }
       const int64_t out = base + k0 + rank;
       a.order[out] = a.node_of_pos ? a.node_of_pos[v[u].pos] : v[u].pos;
-      a.slack[out] = v[u].slack;
+      a.slack[out] = a.out_slack ? a.out_slack[v[u].pos] : v[u].key;
       a.route[out] = v[u].route;
       if (a.cost) a.cost[out] = v[u].cost;
     }
@@ -544,7 +545,7 @@ __global__ __launch_bounds__(kSortThreads) void k_slack_pass(SortArgs a, int pas
   if (tile >= ntiles) return;
   const int64_t smin = ctrl->slack_min;
   const FirstSource f{kSrcStaged, a.stg_slack, a.stg_ready, nullptr, a.span, smin};
-  const FinalOut fo{last, a.node_of_pos, a.stg_route, a.stg_cost, smin,
+  const FinalOut fo{last, a.node_of_pos, a.out_slack, a.stg_route, a.stg_cost, smin,
                     a.order, a.slack, a.route, a.cost};
   radix_tile<uint64_t>(S, f, first, pass, tile, span, R, a.key[(pass + 1) & 1],
                        a.pay[(pass + 1) & 1], a.key[pass & 1], a.pay[pass & 1],
@@ -580,7 +581,7 @@ __global__ __launch_bounds__(kSortThreads) void k_group_pass(GroupArgs a, int pa
                        a.pay[(pass + 1) & 1], a.key[pass & 1], a.pay[pass & 1],
                        ctrl->ghist_group + pass * kRadixBuckets,
                        a.lookback + int64_t(pass) * a.tiles_cap * kRadixBuckets, a.epoch,
-                       FinalOut{false, nullptr, nullptr, nullptr, 0, nullptr, nullptr, nullptr, nullptr});
+                       FinalOut{false, nullptr, nullptr, nullptr, nullptr, 0, nullptr, nullptr, nullptr, nullptr});
 }
 
 // Position of every node and first position of every workflow.

@@ -212,11 +212,11 @@ __device__ inline uint32_t bucket_of(const BucketArgs& bk, int64_t slack) {
   return q < uint64_t(bk.nb) ? uint32_t(q) : uint32_t(bk.nb - 1);
 }
 
-__device__ inline void bucket_put(const SweepArgs& a, uint32_t bkt, uint32_t slot, int64_t slack,
+__device__ inline void bucket_put(const SweepArgs& a, uint32_t bkt, uint32_t slot, int64_t key,
                                   int64_t pos, int32_t route, int64_t cost) {
   if (slot < uint32_t(kBucketCap)) {
     BucketSlot* sl = a.bk.slot + int64_t(bkt) * kBucketCap + slot;
-    sl->slack = slack;
+    sl->key = key;
     sl->cost = cost;
     sl->pos = int32_t(pos);
     sl->route = route;
@@ -225,29 +225,44 @@ __device__ inline void bucket_put(const SweepArgs& a, uint32_t bkt, uint32_t slo
   }
 }
 
+// The key the ready futures are ordered by: the slack, or under
+// NALAR_ORDER_LPT the negated remaining critical path (longest first).
+__device__ inline int64_t order_key(const SweepArgs& a, int64_t rem, int64_t dl) {
+  return (a.p.policy & NALAR_ORDER_LPT) ? -rem : dl - rem;
+}
+
+// Stores of one ready future: its bucket slot (bucketed sort) or its staged
+// values by position (tiled sort), and its slack by position when the key is
+// not the slack.
+__device__ inline void store_ready(const SweepArgs& a, uint32_t bkt, uint32_t slot, int64_t key,
+                                   int64_t slack, int64_t pos, int32_t route, int64_t cost, Acc& acc) {
+  if (a.bk.nb > 0) {
+    bucket_put(a, bkt, slot, key, pos, route, cost);
+  } else {
+    a.stg_slack[pos] = key;
+    a.stg_route[pos] = route;
+    a.stg_cost[pos] = cost;
+  }
+  if (a.p.policy & NALAR_ORDER_LPT) a.stg_oslack[pos] = slack;
+  acc.tmin = key < acc.tmin ? key : acc.tmin;
+  acc.tmax = key > acc.tmax ? key : acc.tmax;
+  acc.tready += 1;
+}
+
 __device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_t pos, int32_t type,
                                    int32_t loc, int64_t rem, int64_t est, int64_t dl, Acc& acc) {
-  const int64_t slack = dl - rem;
+  const int64_t key = order_key(a, rem, dl);
   const BucketArgs& bk = a.bk;
   uint32_t bkt = 0, slot = 0;
   if (bk.nb > 0) {
-    bkt = bucket_of(bk, slack);
+    bkt = bucket_of(bk, key);
     slot = add_agent(bk.cnt + bkt, 1u);
   }
   int32_t route;
   int64_t cost;
   route_future(type, est, loc, int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load, it.speed,
-               it.inv, it.pos, it.run, route, cost);
-  if (bk.nb > 0) {
-    bucket_put(a, bkt, slot, slack, pos, route, cost);
-  } else {  // staged by position for the tiled sort
-    a.stg_slack[pos] = slack;
-    a.stg_route[pos] = route;
-    a.stg_cost[pos] = cost;
-  }
-  acc.tmin = slack < acc.tmin ? slack : acc.tmin;
-  acc.tmax = slack > acc.tmax ? slack : acc.tmax;
-  acc.tready += 1;
+               it.inv, it.pos, it.run, (a.p.policy & NALAR_ROUTE_STATEFUL) != 0, route, cost);
+  store_ready(a, bkt, slot, key, dl - rem, pos, route, cost, acc);
 }
 
 // ------------------------------------------------------------ LDS workflow
@@ -451,7 +466,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
     bkt[j] = 0;
     slot[j] = 0;
     if (bk.nb > 0 && ((ready >> j) & 1u)) {
-      bkt[j] = bucket_of(bk, dl - mx[j * T + tid]);
+      bkt[j] = bucket_of(bk, order_key(a, mx[j * T + tid], dl));
       slot[j] = add_agent(bk.cnt + bkt[j], 1u);
     }
   }
@@ -468,7 +483,8 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
     cost[j] = 0;
     if ((ready >> j) & 1u)
       route_future(ty[j], ee[j], lc[j], int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load, it.speed,
-                   it.inv, it.pos, it.run, route[j], cost[j]);
+                   it.inv, it.pos, it.run, (a.p.policy & NALAR_ROUTE_STATEFUL) != 0, route[j],
+                   cost[j]);
   }
 #pragma unroll
   for (int j = 0; j < NPT; ++j) __asm__ __volatile__("" : "+v"(slot[j]) :: "memory");
@@ -476,17 +492,8 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
   for (int j = 0; j < NPT; ++j) {
     if (!((ready >> j) & 1u)) continue;
     const int k = j * T + tid;
-    const int64_t slack = dl - mx[k];
-    if (bk.nb > 0) {
-      bucket_put(a, bkt[j], slot[j], slack, b + k, route[j], cost[j]);
-    } else {
-      a.stg_slack[b + k] = slack;
-      a.stg_route[b + k] = route[j];
-      a.stg_cost[b + k] = cost[j];
-    }
-    acc.tmin = slack < acc.tmin ? slack : acc.tmin;
-    acc.tmax = slack > acc.tmax ? slack : acc.tmax;
-    acc.tready += 1;
+    store_ready(a, bkt[j], slot[j], order_key(a, mx[k], dl), dl - mx[k], b + k, route[j], cost[j],
+                acc);
   }
 }
 
@@ -1024,7 +1031,7 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
     bkt[j] = 0;
     slot[j] = 0;
     if (bk.nb > 0 && ((ready >> j) & 1u)) {
-      bkt[j] = bucket_of(bk, dl - rr[j]);
+      bkt[j] = bucket_of(bk, order_key(a, rr[j], dl));
       slot[j] = add_agent(bk.cnt + bkt[j], 1u);
     }
   }
@@ -1036,7 +1043,8 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
     cost[j] = 0;
     if ((ready >> j) & 1u)
       route_future(ty[j], ee[j], lc[j], int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load,
-                   it.speed, it.inv, it.pos, it.run, route[j], cost[j]);
+                   it.speed, it.inv, it.pos, it.run, (a.p.policy & NALAR_ROUTE_STATEFUL) != 0,
+                   route[j], cost[j]);
   }
 #pragma unroll
   for (int j = 0; j < NPTW; ++j) __asm__ __volatile__("" : "+v"(slot[j]) :: "memory");
@@ -1046,19 +1054,9 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
     const int64_t pos = b + j * kWave + ln;
     if (bk.nb == 0) a.stg_ready[pos] = uint8_t((ready >> j) & 1u);
     if (a.rem_out) a.rem_out[vv[j]] = rr[j];
-    if ((ready >> j) & 1u) {
-      const int64_t slack = dl - rr[j];
-      if (bk.nb > 0) {
-        bucket_put(a, bkt[j], slot[j], slack, pos, route[j], cost[j]);
-      } else {  // staged by position for the tiled sort
-        a.stg_slack[pos] = slack;
-        a.stg_route[pos] = route[j];
-        a.stg_cost[pos] = cost[j];
-      }
-      acc.tmin = slack < acc.tmin ? slack : acc.tmin;
-      acc.tmax = slack > acc.tmax ? slack : acc.tmax;
-      acc.tready += 1;
-    }
+    if ((ready >> j) & 1u)
+      store_ready(a, bkt[j], slot[j], order_key(a, rr[j], dl), dl - rr[j], pos, route[j], cost[j],
+                  acc);
   }
   wave_order();
 }
@@ -1231,26 +1229,27 @@ __device__ inline ITabLds carve_itab(unsigned char* sp, int M) {
   return it;
 }
 
-// Brings the six 64-byte lines of the sweep's kernel arguments into the
+// Brings the seven 64-byte lines of the sweep's kernel arguments into the
 // scalar cache with loads that are all in flight at once.  The argument block
 // is large and the compiler reloads its fields on demand, one wait each; cold
 // lines would otherwise cost a round trip apiece.
-static_assert(sizeof(SweepArgs) > 5 * 64 && sizeof(SweepArgs) <= 6 * 64,
+static_assert(sizeof(SweepArgs) + sizeof(int) > 6 * 64 && sizeof(SweepArgs) + sizeof(int) <= 7 * 64,
               "warm_kernargs covers exactly the argument block's lines");
 __device__ inline void warm_kernargs() {
   const auto kp = __builtin_amdgcn_kernarg_segment_ptr();
-  uint32_t v0, v1, v2, v3, v4, v5;
+  uint32_t v0, v1, v2, v3, v4, v5, v6;
   __asm__ __volatile__(
-      "s_load_dword %0, %6, 0\n"
-      "s_load_dword %1, %6, 64\n"
-      "s_load_dword %2, %6, 128\n"
-      "s_load_dword %3, %6, 192\n"
-      "s_load_dword %4, %6, 256\n"
-      "s_load_dword %5, %6, 320\n"
+      "s_load_dword %0, %7, 0\n"
+      "s_load_dword %1, %7, 64\n"
+      "s_load_dword %2, %7, 128\n"
+      "s_load_dword %3, %7, 192\n"
+      "s_load_dword %4, %7, 256\n"
+      "s_load_dword %5, %7, 320\n"
+      "s_load_dword %6, %7, 384\n"
       "s_waitcnt lgkmcnt(0)"
-      : "=&s"(v0), "=&s"(v1), "=&s"(v2), "=&s"(v3), "=&s"(v4), "=&s"(v5)
+      : "=&s"(v0), "=&s"(v1), "=&s"(v2), "=&s"(v3), "=&s"(v4), "=&s"(v5), "=&s"(v6)
       : "s"(kp));
-  (void)v0; (void)v1; (void)v2; (void)v3; (void)v4; (void)v5;
+  (void)v0; (void)v1; (void)v2; (void)v3; (void)v4; (void)v5; (void)v6;
 }
 
 // The next pass's bucket counters and, in fused mode, its control block.

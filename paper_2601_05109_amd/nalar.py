@@ -22,6 +22,8 @@ LIB_PATH = os.path.join(HERE, "libnalar_policy.so")
 
 NALAR_OK, NALAR_EINVAL, NALAR_ECYCLE, NALAR_ERANGE, NALAR_ENOMEM, NALAR_EDEVICE = 0, -1, -2, -3, -4, -5
 NALAR_WF_CONTIGUOUS = 1
+NALAR_ORDER_LPT = 2          # problem flag: order by remaining critical path, longest first
+NALAR_ROUTE_STATEFUL = 4     # problem flag: route a future to the instance of its type holding its state
 NALAR_FORCE_GLOBAL_SWEEP = 1
 NALAR_FORCE_TILED_SORT = 2
 NALAR_MAX_INSTANCES = 1024
@@ -151,14 +153,17 @@ class DeviceProblem:
     def n_nodes(self) -> int:
         return int(self.tensors["wf"].shape[0])
 
-    def c_struct(self, flags: Optional[int] = None) -> NalarProblem:
+    def c_struct(self, flags: Optional[int] = None, policy: int = 0) -> NalarProblem:
+        """The C struct of this problem.  ``flags`` replaces the default
+        problem flags (the contiguity bit when the ids are workflow-contiguous);
+        ``policy`` (NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL bits) is ORed in."""
         t = self.tensors
         ptr = lambda x: x.data_ptr() if x.numel() > 0 else None
         return NalarProblem(
             n_nodes=t["wf"].shape[0], n_edges=t["dep_idx"].shape[0],
             n_workflows=t["deadline_us"].shape[0], n_instances=t["inst_type"].shape[0],
             now_us=self.now_us, migration_cost_us=self.migration_cost_us,
-            flags=(NALAR_WF_CONTIGUOUS if self.wf_contiguous else 0) if flags is None else flags,
+            flags=((NALAR_WF_CONTIGUOUS if self.wf_contiguous else 0) if flags is None else flags) | policy,
             reserved=0, wf=ptr(t["wf"]), type=ptr(t["type"]), est_us=ptr(t["est_us"]),
             done=ptr(t["done"]), loc=ptr(t["loc"]), dep_off=ptr(t["dep_off"]),
             dep_idx=ptr(t["dep_idx"]), deadline_us=ptr(t["deadline_us"]),
@@ -226,9 +231,9 @@ class Policy:
             pass
 
     def run_pass(self, prob: DeviceProblem, out: DeviceResult, flags: Optional[int] = None,
-                 raw: Optional[NalarProblem] = None) -> int:
+                 raw: Optional[NalarProblem] = None, policy: int = 0) -> int:
         """One synchronous pass; returns the C return code and fills out.n_ready."""
-        cp = raw if raw is not None else prob.c_struct(flags)
+        cp = raw if raw is not None else prob.c_struct(flags, policy)
         cr = out.c_struct()
         rc = nalar_policy_pass(self.handle, cp, cr)
         out.n_ready = int(cr.n_ready) if rc == NALAR_OK else 0

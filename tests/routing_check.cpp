@@ -1,5 +1,7 @@
 // Host-side check of the routing scorer (per-type argmin over the sorted
-// instance table with the exact fp64 floor division and the migration rule).
+// instance table with the exact fp64 floor division and the migration rule,
+// and the stateful variant that pins a future to the same-type instance
+// holding its state).
 // Random instance tables are laid out as the kernels lay them out (sorted by
 // type, then index, with the run of each type), and route_future is compared
 // with a plain integer argmin over every instance.  Cases cover random values, exact and near ties (equal loads,
@@ -26,7 +28,12 @@ static int64_t uni(int64_t lo, int64_t hi) {  // inclusive
 struct Inst { int32_t type; int64_t load; int32_t speed; };
 
 static void brute(const std::vector<Inst>& in, int32_t t, int64_t est, int32_t loc, int64_t mig,
-                  int32_t& route, int64_t& cost) {
+                  bool stateful, int32_t& route, int64_t& cost) {
+  if (stateful && loc >= 0 && in[loc].type == t) {
+    route = loc;
+    cost = in[loc].load + est * 1000 / in[loc].speed;
+    return;
+  }
   route = -1;
   cost = INT64_MAX;
   for (int i = 0; i < int(in.size()); ++i) {
@@ -67,9 +74,10 @@ static void run_case(const std::vector<Inst>& in, int n_types, int futures, int6
     const int32_t loc = (next_rand() & 1) ? int32_t(uni(0, M > 0 ? M - 1 : 0)) : -1;
     int32_t r0, r1;
     int64_t c0, c1;
-    brute(in, t, est, M > 0 ? loc : -1, mig, r0, c0);
+    const bool stateful = (f % 3) == 1;
+    brute(in, t, est, M > 0 ? loc : -1, mig, stateful, r0, c0);
     nalar::route_future(t, est, M > 0 ? loc : -1, M, mig, type.data(), idx.data(), load.data(),
-                        speed.data(), inv.data(), pos.data(), run.data(), r1, c1);
+                        speed.data(), inv.data(), pos.data(), run.data(), stateful, r1, c1);
     ++checked;
     if (r0 != r1 || c0 != c1) {
       if (bad < 10)

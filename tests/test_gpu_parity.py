@@ -51,10 +51,10 @@ def policy_tiled():
         yield p
 
 
-def gpu_run(pol, p, flags=None):
+def gpu_run(pol, p, flags=None, policy=0):
     dp = nalar.DeviceProblem.from_host(p)
     out = nalar.DeviceResult.alloc(dp.n_nodes)
-    rc = pol.run_pass(dp, out, flags=flags)
+    rc = pol.run_pass(dp, out, flags=flags, policy=policy)
     torch.cuda.synchronize()
     R = out.n_ready
     N = dp.n_nodes
@@ -78,9 +78,9 @@ def assert_parity(g, o, label=""):
                                  f"gpu {got[bad[:5]]} oracle {ref[bad[:5]]}")
 
 
-def check(pol, p, label, flags=None):
-    say(f"[gpu] {label}: N={p.n_nodes} E={p.n_edges} W={p.n_workflows} M={p.n_instances}")
-    assert_parity(gpu_run(pol, p, flags), oracle.run(p), label)
+def check(pol, p, label, flags=None, policy=0):
+    say(f"[gpu] {label}: N={p.n_nodes} E={p.n_edges} W={p.n_workflows} M={p.n_instances} policy={policy}")
+    assert_parity(gpu_run(pol, p, flags, policy), oracle.run(p, policy=policy), label)
 
 
 # ---------------------------------------------------------------- small cases
@@ -220,6 +220,51 @@ def test_large_ready_set_bucketed():
             say(f"[gpu] pass {i}: {names}")
             if i > 0:
                 assert "sort_bucket" in names
+
+
+# ---------------------------------------------------------------- policy variants
+
+VARIANTS = [nalar.NALAR_ORDER_LPT, nalar.NALAR_ROUTE_STATEFUL,
+            nalar.NALAR_ORDER_LPT | nalar.NALAR_ROUTE_STATEFUL]
+
+
+@pytest.mark.parametrize("bits", VARIANTS)
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
+def test_policy_variants_configs(policy, cfg, bits):
+    p = wl.CONFIGS[cfg]()
+    check(policy, p, f"config{cfg} policy {bits}", policy=bits)
+    check(policy, p, f"config{cfg} policy {bits} again", policy=bits)
+
+
+@pytest.mark.parametrize("bits", VARIANTS)
+def test_policy_variants_other_paths(policy_tiled, policy_hbm, bits):
+    """Relabelled ids (grouping), the tiled sort, the HBM sweep and small
+    random DAGs under each variant."""
+    p = wl.tiny()
+    q = wl.relabel(p, np.random.default_rng(9).permutation(p.n_nodes))
+    check(policy_tiled, q, f"relabelled tiny tiled policy {bits}", policy=bits)
+    check(policy_hbm, p, f"tiny hbm policy {bits}", policy=bits)
+    for seed in range(8):
+        d = wl.random_dag(700 + seed, n_nodes=120, n_workflows=3, n_instances=10, n_types=3,
+                          shuffle_ids=bool(seed % 2))
+        check(policy_tiled, d, f"random {seed} tiled policy {bits}", policy=bits)
+        check(policy_hbm, d, f"random {seed} hbm policy {bits}", policy=bits)
+
+
+def test_policy_switch_on_one_handle():
+    """Changing the order key between passes on one handle: the bucket range
+    planned from the previous pass's keys no longer fits, which the fallback
+    must absorb."""
+    p = wl.paper_scale()
+    with nalar.Policy() as pol:
+        for bits in (0, 0, nalar.NALAR_ORDER_LPT, nalar.NALAR_ORDER_LPT, 0, nalar.NALAR_ROUTE_STATEFUL):
+            check(pol, p, f"switch policy {bits}", policy=bits)
+
+
+def test_policy_unknown_bits_rejected(policy):
+    dp = nalar.DeviceProblem.from_host(wl.tiny())
+    out = nalar.DeviceResult.alloc(dp.n_nodes)
+    assert policy.run_pass(dp, out, policy=8) == nalar.NALAR_EINVAL
 
 
 def test_other_seeds(policy):

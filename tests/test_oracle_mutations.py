@@ -16,7 +16,9 @@ import pytest
 import oracle
 from golden_io import load as load_golden, names as golden_names
 from paper_2601_05109_amd import workloads as wl
-from test_oracle_pins import brute_force_rem, push_replay_ready, rem_certificate
+from test_oracle_pins import (brute_force_rem, push_replay_ready, rem_certificate,
+                              test_lpt_equals_srtf_when_deadlines_are_equal,
+                              test_lpt_independent_futures_closed_form, test_stateful_routing_pins)
 
 MUTATIONS = {
     "drop_est_term": ("if (__builtin_add_overflow(est_eff[v], best, &r)",
@@ -29,14 +31,20 @@ MUTATIONS = {
     "penalty_inverted": ("if (loc[v] >= 0 && loc[v] != i) c += mig;",
                          "if (loc[v] >= 0 && loc[v] == i) c += mig;"),
     "penalty_dropped": ("if (loc[v] >= 0 && loc[v] != i) c += mig;", ""),
-    "division_transposed": ("(est[v] * 1000) / inst_speed[i]", "(inst_speed[i] * 1000) / (est[v] + 1)"),
+    "division_transposed": ("int64_t c = inst_load[i] + (est[v] * 1000) / inst_speed[i];",
+                            "int64_t c = inst_load[i] + (inst_speed[i] * 1000) / (est[v] + 1);"),
     "tie_to_highest": ("if (c < best) { best = c;", "if (c <= best) { best = c;"),
     "ready_any_parent": ("if (!done[dep_idx[e]]) { all_done = false; break; }",
                          "if (done[dep_idx[e]]) { all_done = true; break; } else all_done = false;"),
     "order_wf_desc": ("if (wf[a] != wf[b]) return wf[a] < wf[b];",
                       "if (wf[a] != wf[b]) return wf[a] > wf[b];"),
-    "order_slack_desc": ("if (slack[a] != slack[b]) return slack[a] < slack[b];",
-                         "if (slack[a] != slack[b]) return slack[a] > slack[b];"),
+    "order_slack_desc": ("if (ka != kb) return ka < kb;", "if (ka != kb) return ka > kb;"),
+    "lpt_shortest_first": ("const int64_t ka = lpt ? -rem[a] : slack[a];",
+                           "const int64_t ka = lpt ? rem[a] : slack[a];"),
+    "stateful_pays_penalty": ("cost[v] = inst_load[i] + (est[v] * 1000) / inst_speed[i];",
+                              "cost[v] = inst_load[i] + (est[v] * 1000) / inst_speed[i] + mig;"),
+    "stateful_any_type": ("if ((policy & kStateful) && loc[v] >= 0 && inst_type[loc[v]] == type[v]) {",
+                          "if ((policy & kStateful) && loc[v] >= 0) {"),
     "max_with_first_successor_only": (
         "for (int64_t k = succ_off[v]; k < succ_off[v + 1]; ++k) best = std::max(best, rem[succ[k]]);",
         "if (succ_off[v] < succ_off[v + 1]) best = rem[succ[succ_off[v]]];"),
@@ -61,6 +69,8 @@ def _pins_pass(lib_path):
     lib = ctypes.CDLL(lib_path)
     lib.nalar_oracle_pass.restype = ctypes.c_int
     lib.nalar_oracle_pass.argtypes = [ctypes.c_int64] * 6 + [ctypes.c_void_p] * 17
+    lib.nalar_oracle_pass_policy.restype = ctypes.c_int
+    lib.nalar_oracle_pass_policy.argtypes = [ctypes.c_int64] * 6 + [ctypes.c_uint32] + [ctypes.c_void_p] * 17
     oracle._lib = lib
     try:
         for g in golden_names():
@@ -82,6 +92,12 @@ def _pins_pass(lib_path):
                 return False
             try:
                 rem_certificate(p, r.rem)
+            except AssertionError:
+                return False
+        for pin in (test_lpt_equals_srtf_when_deadlines_are_equal,
+                    test_lpt_independent_futures_closed_form, test_stateful_routing_pins):
+            try:
+                pin()
             except AssertionError:
                 return False
         return True

@@ -13,7 +13,10 @@ checked here against things other than itself:
 * closed forms (chains, unit service times, the map/reduce shape);
 * the routing special case with equal loads and speeds, and invariances;
 * uniqueness of a sorted permutation under a total order;
-* every validation and error rule of the boundary.
+* every validation and error rule of the boundary;
+* the policy variants: LPT equals the slack order when deadlines are equal,
+  its order certificate and a closed form; stateful routing against Python
+  integer costs and against the default rule under prohibitive migration.
 """
 import numpy as np
 import pytest
@@ -305,6 +308,89 @@ def test_route_no_instances():
     r = oracle.run(q)
     assert r.status == oracle.OK
     assert np.all(r.route == -1) and np.all(r.cost == INT64_MAX)
+
+
+# ---------------------------------------------------------------- policy variants
+
+LPT, STATEFUL = oracle.POLICY_LPT, oracle.POLICY_STATEFUL
+
+
+def test_lpt_equals_srtf_when_deadlines_are_equal():
+    """With one deadline for every workflow, slack = D - now - rem, so the
+    slack order (pinned above) and the longest-remaining-work order (the LPT
+    policy, Section 6.2) coincide, tie-breaks included."""
+    for p in (wl.tiny(), wl.paper_scale(), wl.random_dag(7, n_nodes=300, n_workflows=5)):
+        q = p.copy(deadline_us=np.full(p.n_workflows, p.now_us + 5_000_000, np.int64))
+        a, b = oracle.run(q), oracle.run(q, policy=LPT)
+        for f in ("order", "slack", "route", "cost", "rem"):
+            np.testing.assert_array_equal(getattr(a, f), getattr(b, f))
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 3])
+def test_lpt_order_certificate(cfg):
+    """The LPT order is a permutation of the ready set (the same set as the
+    default pass) strictly increasing in (-rem, wf, v): unique under a total
+    order; slack, route and cost are those of the default pass, permuted."""
+    p = wl.CONFIGS[cfg]()
+    a, b = oracle.run(p), oracle.run(p, policy=LPT)
+    assert b.n_ready == a.n_ready
+    assert sorted(b.order.tolist()) == sorted(a.order.tolist())
+    keys = [(-int(b.rem[v]), int(p.wf[v]), int(v)) for v in b.order.tolist()]
+    assert all(x < y for x, y in zip(keys, keys[1:]))
+    by_v = {int(v): i for i, v in enumerate(a.order.tolist())}
+    idx = np.array([by_v[int(v)] for v in b.order.tolist()], np.int64)
+    for f in ("slack", "route", "cost"):
+        np.testing.assert_array_equal(getattr(b, f), getattr(a, f)[idx])
+
+
+def test_lpt_independent_futures_closed_form():
+    """Independent futures (no dependencies, none done): rem = est, so LPT lists
+    them by est descending, ties by workflow then id."""
+    N, W = 40, 3
+    rng = np.random.default_rng(5)
+    p = wl.random_dag(3, n_nodes=N, n_workflows=W, p_edge=0.0)
+    p = p.copy(done=np.zeros(N, np.uint8), est_us=rng.integers(0, 6, N).astype(np.int64))
+    r = oracle.run(p, policy=LPT)
+    want = sorted(range(N), key=lambda v: (-int(p.est_us[v]), int(p.wf[v]), v))
+    assert r.order.tolist() == want
+
+
+def test_stateful_routing_pins():
+    """Futures whose state lives on an instance of their own type run there at
+    that instance's cost (load + floor(est*1000/speed), computed here with
+    Python integers); every other future is routed as by the default rule.
+    Equivalently, the stateful choice is what the default rule picks when
+    migration is prohibitively expensive."""
+    p = wl.paper_scale()
+    a = oracle.run(p)
+    s = oracle.run(p, policy=STATEFUL)
+    h = oracle.run(p.copy(migration_cost_us=1 << 60))
+    assert s.order.tolist() == a.order.tolist()
+    pinned = 0
+    for k, v in enumerate(s.order.tolist()):
+        l, t = int(p.loc[v]), int(p.type[v])
+        if l >= 0 and int(p.inst_type[l]) == t:
+            pinned += 1
+            assert s.route[k] == l == h.route[k]
+            assert s.cost[k] == int(p.inst_load_us[l]) + int(p.est_us[v]) * 1000 // int(p.inst_speed_permille[l])
+            assert s.cost[k] == h.cost[k]
+        else:
+            assert s.route[k] == a.route[k] and s.cost[k] == a.cost[k]
+    assert pinned > 500
+
+
+def test_stateful_without_state_is_default():
+    p = wl.tiny()
+    q = p.copy(loc=np.full(p.n_nodes, -1, np.int32))
+    a, s = oracle.run(q), oracle.run(q, policy=STATEFUL | LPT)
+    b = oracle.run(q, policy=LPT)
+    for f in ("order", "slack", "route", "cost"):
+        np.testing.assert_array_equal(getattr(s, f), getattr(b, f))
+    np.testing.assert_array_equal(np.sort(a.route), np.sort(s.route))
+
+
+def test_unknown_policy_bits_rejected():
+    assert oracle.run(wl.tiny(), policy=8).status == oracle.EINVAL
 
 
 # ---------------------------------------------------------------- degenerate
