@@ -13,8 +13,9 @@ on this host as a baseline.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload paper-scale]
 
-Other workloads: tiny, deep-chains, wide-mapreduce, and dynamic (the evolving
-map/reduce graph: per-step pass latency over 100 steps, p50/p99).
+Other workloads: tiny, deep-chains, wide-mapreduce, dynamic (the evolving
+map/reduce graph: per-step pass latency over 100 steps, p50/p99), and levels
+(one-level versus two-level control over 1K-131K futures).
 """
 from __future__ import annotations
 
@@ -243,6 +244,63 @@ def dynamic(args) -> int:
     return 0
 
 
+def levels(args) -> int:
+    """One-level versus two-level control (the comparison of the paper's
+    Table 4, Section 6.3) on this engine, over 1,024 ... 131,072 futures of the
+    paper-scale generator.  Two-level: one batched pass installs every ready
+    future's priority and route at once.  One-level: the central controller
+    takes every future event itself, each a decision over the global view (a
+    pass over the snapshot); a burst of N events queues N of them, so the
+    k-th event waits k decisions.  Every number comes from timed synchronous
+    passes; the burst figures are those times multiplied out."""
+    import torch
+    from paper_2601_05109_amd import nalar, workloads as wl
+
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream(dev)
+    pol = nalar.Policy(device=0, stream=stream)
+    rows = []
+    W = 32
+    while W * 32 <= 131072:
+        p = wl.windowed(W)
+        dp = nalar.DeviceProblem.from_host(p, dev)
+        out = nalar.DeviceResult.alloc(p.n_nodes, dev)
+        cp = dp.c_struct()
+
+        def one_pass():
+            cr = out.c_struct()
+            rc = nalar.nalar_policy_pass(pol.handle, cp, cr)
+            if rc != nalar.NALAR_OK:
+                raise RuntimeError(f"pass failed {rc}: {pol.last_error()}")
+            return int(cr.n_ready)
+
+        for _ in range(10):
+            R = one_pass()
+        ts = []
+        for _ in range(100):
+            t = time.perf_counter()
+            one_pass()
+            ts.append(time.perf_counter() - t)
+        ts.sort()
+        t_us = 1e6 * ts[len(ts) // 2]
+        N = p.n_nodes
+        rows.append({"futures": N, "ready": R,
+                     "two_level_pass_us": round(t_us, 2),
+                     "two_level_per_future_ns": round(1e3 * t_us / N, 3),
+                     "one_level_per_event_us": round(t_us, 2),
+                     "one_level_burst_ms": round(N * t_us / 1e3, 1),
+                     "one_level_mean_wait_ms": round((N + 1) / 2 * t_us / 1e3, 1)})
+        print(f"N={N}: pass {t_us:.1f} us", file=sys.stderr, flush=True)
+        W *= 2
+    pol.close()
+    res = {"metric": "schedule time, one-level vs two-level control", "unit": "us",
+           "n_gpus": 1, "higher_is_better": False, "dtype": "int64",
+           "data": "synthetic (seeded generator, paper-scale shape, 32 futures per workflow)",
+           "config": {"workload": "futures sweep 1,024 ... 131,072"}, "rows": rows}
+    print(json.dumps(res))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -267,6 +325,8 @@ def main() -> int:
         return copy_calibration()
     if args.workload == "dynamic":
         return dynamic(args)
+    if args.workload == "levels":
+        return levels(args)
 
     import torch
     from paper_2601_05109_amd import nalar

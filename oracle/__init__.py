@@ -27,6 +27,7 @@ OK, EINVAL, ECYCLE, ERANGE = 0, -1, -2, -3
 # policy variants (the same bits as the library's problem flags)
 POLICY_LPT = 2        # order by remaining critical path, longest first
 POLICY_STATEFUL = 4   # a future whose state lives on an instance of its type runs there
+POLICY_GREEDY = 8     # route in output order, each future adding its service time to its instance
 
 _lock = threading.Lock()
 _lib: Optional[ctypes.CDLL] = None

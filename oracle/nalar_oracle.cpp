@@ -41,6 +41,12 @@
 //              no other candidate (the stateful directive, Table 1, and the
 //              managed-state routing guarantee, Section 4.3.2); other futures
 //              are routed as in O8
+//   kGreedy    routing is redone after O9, one future at a time in the output
+//              order: each takes the cheapest candidate (the O8 rule, or its
+//              pin under kStateful) under the loads left by the futures before
+//              it, then adds its service time on that instance,
+//              est*1000/speed, to that instance's load (routing that balances
+//              load across instances, Section 6.1); a load above 2^62 -> -3
 //
 // Precedence of errors: EINVAL, then ECYCLE, then ERANGE.
 #include <algorithm>
@@ -57,6 +63,7 @@ constexpr int kErange = -3;
 
 constexpr uint32_t kLpt = 2u;
 constexpr uint32_t kStateful = 4u;
+constexpr uint32_t kGreedy = 8u;
 
 constexpr int64_t kMaxNodes = int64_t(1) << 30;
 constexpr int64_t kMaxEdges = (int64_t(1) << 31) - 1;
@@ -126,7 +133,7 @@ int nalar_oracle_pass_policy(int64_t N, int64_t E, int64_t W, int64_t M, int64_t
                              const int64_t* inst_load, const int32_t* inst_speed, int64_t* rem_out,
                              int32_t* order_out, int64_t* slack_out, int32_t* route_out,
                              int64_t* cost_out, int64_t* n_ready_out) {
-  if ((policy & ~(kLpt | kStateful)) != 0) return kEinval;
+  if ((policy & ~(kLpt | kStateful | kGreedy)) != 0) return kEinval;
   int rc = validate(N, E, W, M, now, mig, wf, type, est, done, loc, dep_off, dep_idx,
                     deadline, inst_type, inst_load, inst_speed);
   if (rc != kOk) return rc;
@@ -231,6 +238,32 @@ int nalar_oracle_pass_policy(int64_t N, int64_t E, int64_t W, int64_t M, int64_t
     if (wf[a] != wf[b]) return wf[a] < wf[b];
     return a < b;
   });
+
+  // O9b (kGreedy): route again in the output order with running loads.
+  if (policy & kGreedy) {
+    std::vector<int64_t> load(inst_load, inst_load + M);
+    for (int32_t v : order) {
+      int32_t arg = -1;
+      int64_t best = INT64_MAX;
+      if ((policy & kStateful) && loc[v] >= 0 && inst_type[loc[v]] == type[v]) {
+        arg = loc[v];
+        best = load[arg] + (est[v] * 1000) / inst_speed[arg];
+      } else {
+        for (int64_t i = 0; i < M; ++i) {
+          if (inst_type[i] != type[v]) continue;
+          int64_t c = load[i] + (est[v] * 1000) / inst_speed[i];
+          if (loc[v] >= 0 && loc[v] != i) c += mig;
+          if (c < best) { best = c; arg = int32_t(i); }
+        }
+      }
+      route[v] = arg;
+      cost[v] = best;
+      if (arg >= 0) {
+        load[arg] += (est[v] * 1000) / inst_speed[arg];
+        if (load[arg] > kRemMax) return kErange;
+      }
+    }
+  }
 
   // O10
   if (rem_out) std::memcpy(rem_out, rem.data(), sizeof(int64_t) * N);

@@ -205,6 +205,12 @@ def paper_scale(seed: Optional[int] = None) -> Problem:
                      4096, 32, 8, 64)
 
 
+def windowed(W: int, seed: Optional[int] = None) -> Problem:
+    """W workflows x 32 futures from the paper-scale generator (K=8, 64
+    instances): the futures-count sweep of the scalability study."""
+    return _windowed(f"windowed-{W}x32", SEED_BASE + 1 if seed is None else seed, W, 32, 8, 64)
+
+
 def deep_chains(seed: Optional[int] = None, W: int = 1024) -> Problem:
     """1,024 workflows x 512 futures: 128 layers of width 4, each node with 1-3
     distinct parents in the previous layer; K=8, 128 instances."""

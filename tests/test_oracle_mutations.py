@@ -18,7 +18,9 @@ from golden_io import load as load_golden, names as golden_names
 from paper_2601_05109_amd import workloads as wl
 from test_oracle_pins import (brute_force_rem, push_replay_ready, rem_certificate,
                               test_lpt_equals_srtf_when_deadlines_are_equal,
-                              test_lpt_independent_futures_closed_form, test_stateful_routing_pins)
+                              test_lpt_independent_futures_closed_form, test_stateful_routing_pins,
+                              test_greedy_single_instance_prefix_sums,
+                              test_greedy_identical_instances_round_robin)
 
 MUTATIONS = {
     "drop_est_term": ("if (__builtin_add_overflow(est_eff[v], best, &r)",
@@ -28,12 +30,13 @@ MUTATIONS = {
                    "slack[v] = (deadline[wf[v]] - now) + rem[v];"),
     "slack_wrong_index": ("slack[v] = (deadline[wf[v]] - now) - rem[v];",
                           "slack[v] = (deadline[type[v] % (W ? W : 1)] - now) - rem[v];"),
-    "penalty_inverted": ("if (loc[v] >= 0 && loc[v] != i) c += mig;",
-                         "if (loc[v] >= 0 && loc[v] == i) c += mig;"),
-    "penalty_dropped": ("if (loc[v] >= 0 && loc[v] != i) c += mig;", ""),
+    "penalty_inverted": ("inst_speed[i];\n      if (loc[v] >= 0 && loc[v] != i) c += mig;",
+                         "inst_speed[i];\n      if (loc[v] >= 0 && loc[v] == i) c += mig;"),
+    "penalty_dropped": ("inst_speed[i];\n      if (loc[v] >= 0 && loc[v] != i) c += mig;", "inst_speed[i];"),
     "division_transposed": ("int64_t c = inst_load[i] + (est[v] * 1000) / inst_speed[i];",
                             "int64_t c = inst_load[i] + (inst_speed[i] * 1000) / (est[v] + 1);"),
-    "tie_to_highest": ("if (c < best) { best = c;", "if (c <= best) { best = c;"),
+    "tie_to_highest": ("      if (c < best) { best = c; arg = int32_t(i); }\n    }\n    route[v] = arg;\n    cost[v] = best;\n  }",
+                       "      if (c <= best) { best = c; arg = int32_t(i); }\n    }\n    route[v] = arg;\n    cost[v] = best;\n  }"),
     "ready_any_parent": ("if (!done[dep_idx[e]]) { all_done = false; break; }",
                          "if (done[dep_idx[e]]) { all_done = true; break; } else all_done = false;"),
     "order_wf_desc": ("if (wf[a] != wf[b]) return wf[a] < wf[b];",
@@ -43,8 +46,10 @@ MUTATIONS = {
                            "const int64_t ka = lpt ? rem[a] : slack[a];"),
     "stateful_pays_penalty": ("cost[v] = inst_load[i] + (est[v] * 1000) / inst_speed[i];",
                               "cost[v] = inst_load[i] + (est[v] * 1000) / inst_speed[i] + mig;"),
-    "stateful_any_type": ("if ((policy & kStateful) && loc[v] >= 0 && inst_type[loc[v]] == type[v]) {",
-                          "if ((policy & kStateful) && loc[v] >= 0) {"),
+    "greedy_no_load_update": ("        load[arg] += (est[v] * 1000) / inst_speed[arg];\n", ""),
+    "greedy_adds_cost": ("load[arg] += (est[v] * 1000) / inst_speed[arg];", "load[arg] += best;"),
+    "stateful_any_type": ("if ((policy & kStateful) && loc[v] >= 0 && inst_type[loc[v]] == type[v]) {\n      const int32_t i",
+                          "if ((policy & kStateful) && loc[v] >= 0) {\n      const int32_t i"),
     "max_with_first_successor_only": (
         "for (int64_t k = succ_off[v]; k < succ_off[v + 1]; ++k) best = std::max(best, rem[succ[k]]);",
         "if (succ_off[v] < succ_off[v + 1]) best = rem[succ[succ_off[v]]];"),
@@ -95,7 +100,9 @@ def _pins_pass(lib_path):
             except AssertionError:
                 return False
         for pin in (test_lpt_equals_srtf_when_deadlines_are_equal,
-                    test_lpt_independent_futures_closed_form, test_stateful_routing_pins):
+                    test_lpt_independent_futures_closed_form, test_stateful_routing_pins,
+                    test_greedy_single_instance_prefix_sums,
+                    test_greedy_identical_instances_round_robin):
             try:
                 pin()
             except AssertionError:

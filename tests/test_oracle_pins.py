@@ -16,7 +16,9 @@ checked here against things other than itself:
 * every validation and error rule of the boundary;
 * the policy variants: LPT equals the slack order when deadlines are equal,
   its order certificate and a closed form; stateful routing against Python
-  integer costs and against the default rule under prohibitive migration.
+  integer costs and against the default rule under prohibitive migration;
+  greedy load-aware routing against prefix sums, round-robin and list
+  scheduling closed forms, and monotonicity against the snapshot loads.
 """
 import numpy as np
 import pytest
@@ -390,7 +392,88 @@ def test_stateful_without_state_is_default():
 
 
 def test_unknown_policy_bits_rejected():
-    assert oracle.run(wl.tiny(), policy=8).status == oracle.EINVAL
+    assert oracle.run(wl.tiny(), policy=16).status == oracle.EINVAL
+
+
+GREEDY = oracle.POLICY_GREEDY
+
+
+def _one_type_problem(n_inst, loads, speeds, est, loc=None, mig=200_000, deadline_spread=True):
+    """Independent futures (no dependencies, none done) of one type in one
+    workflow each, against n_inst instances of that type."""
+    N = len(est)
+    rng = np.random.default_rng(N)
+    dl = 1_000_000 + (rng.permutation(N) * 1000 if deadline_spread else np.zeros(N, np.int64))
+    now = 1_000
+    return wl.Problem("one-type", now, mig, np.arange(N, dtype=np.int32), np.zeros(N, np.int32),
+                      np.asarray(est, np.int64), np.zeros(N, np.uint8),
+                      np.full(N, -1, np.int32) if loc is None else np.asarray(loc, np.int32),
+                      np.zeros(N + 1, np.int32), np.zeros(0, np.int32),
+                      (now + dl).astype(np.int64), np.zeros(n_inst, np.int32),
+                      np.asarray(loads, np.int64), np.asarray(speeds, np.int32), wf_contiguous=True)
+
+
+def test_greedy_single_instance_prefix_sums():
+    """One instance: every future goes there and waits for all before it in the
+    output order, so its cost is the initial load plus the prefix sum of
+    service times (est * 1000 // speed) up to and including itself."""
+    rng = np.random.default_rng(1)
+    est = rng.integers(0, 10**6, 50)
+    p = _one_type_problem(1, [12345], [750], est)
+    r = oracle.run(p, policy=GREEDY)
+    svc = np.array([int(est[v]) * 1000 // 750 for v in r.order.tolist()], np.int64)
+    assert np.all(r.route == 0)
+    np.testing.assert_array_equal(r.cost, 12345 + np.cumsum(svc))
+
+
+def test_greedy_identical_instances_round_robin():
+    """Identical instances and identical futures: list scheduling deals them
+    out in index order (ties go to the lowest index): route k mod m, and the
+    k-th future waits k // m service times before its own."""
+    m, n = 3, 20
+    p = _one_type_problem(m, [500] * m, [1000] * m, [40] * n)
+    r = oracle.run(p, policy=GREEDY)
+    k = np.arange(n)
+    np.testing.assert_array_equal(r.route, k % m)
+    np.testing.assert_array_equal(r.cost, 500 + (k // m + 1) * 40)
+
+
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_greedy_invariants(cfg):
+    """Loads only grow, so no future costs less than under the snapshot loads;
+    the first future of each type in the order is routed exactly as by the
+    default rule; order and slack are untouched."""
+    p = wl.CONFIGS[cfg]()
+    a, g = oracle.run(p), oracle.run(p, policy=GREEDY)
+    for f in ("order", "slack", "rem"):
+        np.testing.assert_array_equal(getattr(a, f), getattr(g, f))
+    ok = a.route >= 0
+    assert np.all((g.route >= 0) == ok)
+    assert np.all(g.cost[ok] >= a.cost[ok])
+    seen = set()
+    for k, v in enumerate(a.order.tolist()):
+        t = int(p.type[v])
+        if t not in seen:
+            seen.add(t)
+            assert g.route[k] == a.route[k] and g.cost[k] == a.cost[k]
+
+
+def test_greedy_balances_identical_instances():
+    """List scheduling of equal jobs on identical machines: the final loads
+    differ by at most one service time."""
+    m, n = 4, 37
+    p = _one_type_problem(m, [0] * m, [1000] * m, [25] * n)
+    r = oracle.run(p, policy=GREEDY)
+    counts = np.bincount(r.route, minlength=m)
+    assert counts.max() - counts.min() <= 1
+
+
+def test_greedy_load_overflow_is_erange():
+    # each future adds 2^40 * 1000 (about 2^50) to the one instance's load,
+    # which starts at 2^60: the 3072nd addition or so passes 2^62
+    p = _one_type_problem(1, [1 << 60], [1], [1 << 40] * 3200)
+    assert oracle.run(p).status == oracle.OK
+    assert oracle.run(p, policy=GREEDY).status == oracle.ERANGE
 
 
 # ---------------------------------------------------------------- degenerate
