@@ -307,9 +307,11 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="paper-scale")
-    ap.add_argument("--policy", default="srtf", choices=["srtf", "lpt", "stateful", "lpt+stateful"],
+    ap.add_argument("--policy", default="srtf",
+                    choices=["srtf", "lpt", "stateful", "lpt+stateful", "greedy", "greedy+stateful"],
                     help="policy variant: order by slack (srtf) or by remaining work (lpt); "
-                         "stateful pins futures to the instance holding their state")
+                         "stateful pins futures to the instance holding their state; greedy "
+                         "routes in output order with running instance loads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--dyn-steps", type=int, default=100, help="dynamic workload: steps after step 0")
@@ -339,7 +341,9 @@ def main() -> int:
     stream = torch.cuda.current_stream(dev)
     pol = nalar.Policy(device=0, stream=stream, reserve_nodes=N, reserve_workflows=W)
     bits = {"srtf": 0, "lpt": nalar.NALAR_ORDER_LPT, "stateful": nalar.NALAR_ROUTE_STATEFUL,
-            "lpt+stateful": nalar.NALAR_ORDER_LPT | nalar.NALAR_ROUTE_STATEFUL}[args.policy]
+            "lpt+stateful": nalar.NALAR_ORDER_LPT | nalar.NALAR_ROUTE_STATEFUL,
+            "greedy": nalar.NALAR_ROUTE_GREEDY,
+            "greedy+stateful": nalar.NALAR_ROUTE_GREEDY | nalar.NALAR_ROUTE_STATEFUL}[args.policy]
     cp = dp.c_struct(policy=bits)
 
     def one_pass():

@@ -78,6 +78,18 @@ enum {
                                     penalty (the stateful directive, Table 1;
                                     managed-state routing, Section 4.3.2); every
                                     other future is routed by the default rule */
+#define NALAR_ROUTE_GREEDY   8u  /* load-aware routing: after ordering, the
+                                    ready futures are routed one at a time in
+                                    output order; each takes the (route rule)
+                                    cheapest candidate under the loads left by
+                                    the futures before it, then adds its service
+                                    time floor(est*1000/speed) on the chosen
+                                    instance to that instance's load (routing
+                                    that balances load, Section 6.1).  A load
+                                    past NALAR_REM_MAX is NALAR_ERANGE.  Futures
+                                    of different types are independent
+                                    sequences, so this runs one wavefront per
+                                    component type                              */
 
 /* nalar_policy_config.flags (tuning and testing; 0 is the normal setting) */
 #define NALAR_FORCE_GLOBAL_SWEEP 1u  /* keep every workflow's sweep state in HBM
@@ -115,7 +127,8 @@ typedef struct {
   int64_t migration_cost_us;  /* penalty for running a future away from the
                                  instance holding its state, [0, NALAR_MIG_MAX]   */
   uint32_t flags;             /* NALAR_WF_CONTIGUOUS, NALAR_ORDER_LPT,
-                                 NALAR_ROUTE_STATEFUL bits, or 0                  */
+                                 NALAR_ROUTE_STATEFUL, NALAR_ROUTE_GREEDY bits,
+                                 or 0                                             */
   uint32_t reserved;          /* must be 0                                        */
   const int32_t* wf;          /* [N] workflow (session) of each future, [0, W)    */
   const int32_t* type;        /* [N] component type, >= 0                         */
@@ -172,8 +185,8 @@ int nalar_policy_create(const nalar_policy_config* cfg, nalar_policy** out);
  *              (cost(v,i), i) lexicographically (the lowest index wins ties),
  *              or -1 with cost INT64_MAX when there is none
  *   order    = the ready futures sorted by (slack, wf, id) ascending
- * (the NALAR_ORDER_LPT and NALAR_ROUTE_STATEFUL bits change order and route as
- * described at their definitions).
+ * (the NALAR_ORDER_LPT, NALAR_ROUTE_STATEFUL and NALAR_ROUTE_GREEDY bits change
+ * order and route as described at their definitions).
  * Synchronous.  NULL p, r, or a required array (a node array when N > 0,
  * dep_idx when E > 0, deadline_us when W > 0, an instance array when M > 0,
  * order/slack_us/route when N > 0) is NALAR_EINVAL.  Error precedence and the

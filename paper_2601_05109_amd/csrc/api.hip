@@ -233,7 +233,8 @@ int check_problem(nalar_policy* h, const nalar_problem* p, const nalar_result* r
     return fail(h, NALAR_EINVAL, "now_us out of range");
   if (!in_range(p->migration_cost_us, 0, NALAR_MIG_MAX))
     return fail(h, NALAR_EINVAL, "migration_cost_us out of range");
-  if ((p->flags & ~(NALAR_WF_CONTIGUOUS | NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL)) != 0 ||
+  if ((p->flags & ~(NALAR_WF_CONTIGUOUS | NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL |
+                    NALAR_ROUTE_GREEDY)) != 0 ||
       p->reserved != 0)
     return fail(h, NALAR_EINVAL, "unknown problem flags");
   if (N == 0 && E != 0) return fail(h, NALAR_EINVAL, "edges without nodes");
@@ -386,7 +387,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   h->ctrl_dirty[cur] = true;
   h->ctrl_dirty[nxt] = true;
 
-  const uint32_t policy = p->flags & (NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL);
+  const uint32_t policy = p->flags & (NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL | NALAR_ROUTE_GREEDY);
   ProblemDev pd{N, p->n_edges, W, M, p->now_us, p->migration_cost_us, policy, 0u,
                 p->wf, p->type, p->est_us, p->done, p->loc, p->dep_off, p->dep_idx,
                 p->deadline_us, p->inst_type, p->inst_load_us, p->inst_speed_permille};
@@ -525,20 +526,33 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
       if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
     }
   }
-#undef NALAR_LAUNCH
   h->passes += 1;
   h->ctrl_dirty[nxt] = false;
-  if (h->timing) {
-    h->n_timed = tm.n;
-    for (int i = 0; i < tm.n; ++i) (void)hipEventElapsedTime(&h->ms[i], h->ev[i], h->ev[i + 1]);
-    h->timed_valid = true;
-  }
   const uint32_t st = __atomic_load_n(&h->host->status, __ATOMIC_ACQUIRE);
   if (st == 0xFFFFFFFFu) return fail(h, NALAR_EDEVICE, "status was not written");
   if (st & kStInval) return fail(h, NALAR_EINVAL, "invalid problem data");
   if (st & kStCycle) return fail(h, NALAR_ECYCLE, "dependency cycle");
   if (st & kStRange) return fail(h, NALAR_ERANGE, "remaining critical path exceeds 2^62 us");
   r->n_ready = __atomic_load_n(&h->host->n_ready, __ATOMIC_ACQUIRE);
+  if ((policy & NALAR_ROUTE_GREEDY) && r->n_ready > 0 && M > 0) {
+    // route again in output order with running loads (one wavefront per type)
+    __atomic_store_n(&h->host->aux_status, 0u, __ATOMIC_RELEASE);
+    GreedyArgs g{r->order, r->n_ready, p->type, p->est_us, p->loc, p->inst_type, p->inst_load_us,
+                 p->inst_speed_permille, int32_t(M), (policy & NALAR_ROUTE_STATEFUL) ? 1 : 0,
+                 p->migration_cost_us, r->route, r->cost_us, h->host};
+    NALAR_LAUNCH("route_greedy", launch_route_greedy(s, g));
+    tm.end();
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
+    if (__atomic_load_n(&h->host->aux_status, __ATOMIC_ACQUIRE) & kStRange)
+      return fail(h, NALAR_ERANGE, "an instance load exceeds 2^62 us under load-aware routing");
+  }
+#undef NALAR_LAUNCH
+  if (h->timing) {
+    h->n_timed = tm.n;
+    for (int i = 0; i < tm.n; ++i) (void)hipEventElapsedTime(&h->ms[i], h->ev[i], h->ev[i + 1]);
+    h->timed_valid = true;
+  }
   h->hint_valid = true;
   h->hint_ready = r->n_ready;
   h->hint_min = r->n_ready ? __atomic_load_n(&h->host->slack_min, __ATOMIC_ACQUIRE) : 0;

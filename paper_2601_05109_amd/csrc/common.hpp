@@ -97,6 +97,8 @@ struct HostStatus {
   int64_t n_ready;
   int64_t slack_min;   // range of this pass (the next pass's bucket hint)
   int64_t slack_max;
+  uint32_t aux_status; // status bits of the load-aware routing kernel
+  uint32_t pad_;
 };
 
 // Resets a control block for a later pass (run by one workgroup).

@@ -109,6 +109,25 @@ struct SweepArgs {
   int64_t bk_clear_n;
 };
 
+// Load-aware routing over the ordered ready futures (greedy.hip).
+struct GreedyArgs {
+  const int32_t* order;         // [R] the pass's output order
+  int64_t R;
+  const int32_t* type;
+  const int64_t* est;
+  const int32_t* loc;
+  const int32_t* inst_type;
+  const int64_t* inst_load;
+  const int32_t* inst_speed;
+  int32_t M;
+  int32_t stateful;             // NALAR_ROUTE_STATEFUL pins apply
+  int64_t mig;
+  int32_t* route;               // [R] overwritten, aligned with order
+  int64_t* cost;                // [R] or NULL
+  HostStatus* host;             // aux_status receives kStRange on a load overflow
+};
+hipError_t launch_route_greedy(hipStream_t s, const GreedyArgs& g);
+
 // ingest.hip
 hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
                         int32_t* wf_off, int contiguous);

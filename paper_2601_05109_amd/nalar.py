@@ -24,6 +24,7 @@ NALAR_OK, NALAR_EINVAL, NALAR_ECYCLE, NALAR_ERANGE, NALAR_ENOMEM, NALAR_EDEVICE 
 NALAR_WF_CONTIGUOUS = 1
 NALAR_ORDER_LPT = 2          # problem flag: order by remaining critical path, longest first
 NALAR_ROUTE_STATEFUL = 4     # problem flag: route a future to the instance of its type holding its state
+NALAR_ROUTE_GREEDY = 8       # problem flag: route in output order with running instance loads
 NALAR_FORCE_GLOBAL_SWEEP = 1
 NALAR_FORCE_TILED_SORT = 2
 NALAR_MAX_INSTANCES = 1024

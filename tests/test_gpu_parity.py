@@ -225,7 +225,9 @@ def test_large_ready_set_bucketed():
 # ---------------------------------------------------------------- policy variants
 
 VARIANTS = [nalar.NALAR_ORDER_LPT, nalar.NALAR_ROUTE_STATEFUL,
-            nalar.NALAR_ORDER_LPT | nalar.NALAR_ROUTE_STATEFUL]
+            nalar.NALAR_ORDER_LPT | nalar.NALAR_ROUTE_STATEFUL, nalar.NALAR_ROUTE_GREEDY,
+            nalar.NALAR_ROUTE_GREEDY | nalar.NALAR_ROUTE_STATEFUL,
+            nalar.NALAR_ROUTE_GREEDY | nalar.NALAR_ORDER_LPT]
 
 
 @pytest.mark.parametrize("bits", VARIANTS)
@@ -264,7 +266,35 @@ def test_policy_switch_on_one_handle():
 def test_policy_unknown_bits_rejected(policy):
     dp = nalar.DeviceProblem.from_host(wl.tiny())
     out = nalar.DeviceResult.alloc(dp.n_nodes)
-    assert policy.run_pass(dp, out, policy=8) == nalar.NALAR_EINVAL
+    assert policy.run_pass(dp, out, policy=16) == nalar.NALAR_EINVAL
+
+
+def _one_type(n_inst, loads, speeds, est, loc=None, mig=200_000):
+    N = len(est)
+    now = 1_000
+    dl = 1_000_000 + np.random.default_rng(N).permutation(N).astype(np.int64) * 1000
+    return wl.Problem("one-type", now, mig, np.arange(N, dtype=np.int32), np.zeros(N, np.int32),
+                      np.asarray(est, np.int64), np.zeros(N, np.uint8),
+                      np.full(N, -1, np.int32) if loc is None else np.asarray(loc, np.int32),
+                      np.zeros(N + 1, np.int32), np.zeros(0, np.int32), (now + dl).astype(np.int64),
+                      np.zeros(n_inst, np.int32), np.asarray(loads, np.int64),
+                      np.asarray(speeds, np.int32), wf_contiguous=True)
+
+
+def test_greedy_many_candidates_and_overflow(policy):
+    """More candidates of one type than lanes in a wave (the candidate loop),
+    identical instances (every decision a tie), and a load overflow (ERANGE)."""
+    rng = np.random.default_rng(4)
+    G = nalar.NALAR_ROUTE_GREEDY
+    p = _one_type(300, rng.integers(0, 10**6, 300), rng.integers(500, 2000, 300),
+                  rng.integers(0, 10**6, 2000), loc=np.where(rng.random(2000) < 0.5, rng.integers(0, 300, 2000), -1))
+    check(policy, p, "greedy 300 candidates", policy=G)
+    check(policy, p, "greedy 300 candidates stateful", policy=G | nalar.NALAR_ROUTE_STATEFUL)
+    q = _one_type(5, [700] * 5, [1000] * 5, [33] * 500)
+    check(policy, q, "greedy identical instances", policy=G)
+    o = _one_type(1, [1 << 60], [1], [1 << 40] * 3200)
+    check(policy, o, "greedy load overflow", policy=G)
+    check(policy, wl.tiny(), "after greedy overflow")
 
 
 def test_other_seeds(policy):
