@@ -165,28 +165,48 @@ def dynamic(args) -> int:
     apart, not part of the pass), passed once untimed (scratch growth), then
     ``--dyn-reps`` times with HIP events on the library stream; a step's
     latency is the median of its reps."""
+    import numpy as np
     import torch
     from paper_2601_05109_amd import nalar, workloads as wl
 
     dev = torch.device("cuda", 0)
     stream = torch.cuda.current_stream(dev)
     pol = nalar.Policy(device=0, stream=stream)
+    store = nalar.Store(pol) if args.store else None
+    prev_n, prev_done = 0, None
     out = None
     rows = []
     t_all = time.perf_counter()
     for step, p in enumerate(wl.dynamic_stream(steps=args.dyn_steps)):
+        N = p.n_nodes
         t = time.perf_counter()
-        dp = nalar.DeviceProblem.from_host(p, dev)
+        if store is None:  # upload the whole snapshot
+            dp = nalar.DeviceProblem.from_host(p, dev)
+            cp = dp.c_struct()
+        else:  # upload the delta since the previous step into the store
+            if prev_n == 0:
+                store.set_workflows(p.deadline_us)
+                store.set_instances(p.inst_type, p.inst_load_us, p.inst_speed_permille)
+            else:
+                store.complete(np.flatnonzero((p.done[:prev_n] == 1) & (prev_done == 0)).astype(np.int32))
+            e0, e1 = int(p.dep_off[prev_n]), int(p.dep_off[N])
+            rc = store.append(p.wf[prev_n:N], p.type[prev_n:N], p.est_us[prev_n:N], p.done[prev_n:N],
+                              p.loc[prev_n:N], p.dep_off[prev_n:N + 1] - e0, p.dep_idx[e0:e1],
+                              contiguous=bool(p.wf_contiguous))
+            if rc != nalar.NALAR_OK:
+                raise RuntimeError(f"step {step}: append failed {rc}: {pol.last_error()}")
+            prev_n, prev_done = N, p.done[:N].copy()
         torch.cuda.synchronize()
         up_ms = 1e3 * (time.perf_counter() - t)
-        N = p.n_nodes
         if out is None or out.order.shape[0] < N:
             out = nalar.DeviceResult.alloc(int(N * 1.3), dev)
-        cp = dp.c_struct()
 
         def one_pass():
             cr = out.c_struct()
-            rc = nalar.nalar_policy_pass(pol.handle, cp, cr)
+            if store is None:
+                rc = nalar.nalar_policy_pass(pol.handle, cp, cr)
+            else:
+                rc = nalar.nalar_store_pass(store.handle, p.now_us, p.migration_cost_us, 0, cr)
             if rc != nalar.NALAR_OK:
                 raise RuntimeError(f"step {step}: pass failed {rc}: {pol.last_error()}")
             return int(cr.n_ready)
@@ -214,6 +234,8 @@ def dynamic(args) -> int:
         if step % 10 == 0:
             print(f"step {step}: N={N} R={R} pass {rows[-1]['us']:.1f} us (upload {up_ms:.1f} ms)",
                   file=sys.stderr, flush=True)
+    if store is not None:
+        store.close()
     pol.close()
     lat = sorted(r["us"] for r in rows[1:]) or [rows[0]["us"]]
     q = lambda f: lat[min(len(lat) - 1, int(f * len(lat)))]
@@ -234,6 +256,8 @@ def dynamic(args) -> int:
         "data": "synthetic (seeded generator, evolving map/reduce graph)",
         "config": {"workload": f"dynamic-stream: {first['n']} -> {last['n']} futures over "
                                f"{len(rows) - 1} steps, ids not workflow-contiguous after step 0",
+                   "input": "device-resident graph store fed by deltas" if args.store
+                            else "whole snapshot uploaded every step",
                    "n_futures_first": first["n"], "n_futures_last": last["n"]},
         "latency_us": {"p50": q(0.5), "p99": q(0.99), "step0": first["us"], "last_step": last["us"]},
         "per_step": [{k: (round(v, 2) if isinstance(v, float) else v) for k, v in r.items()}
@@ -316,6 +340,8 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--dyn-steps", type=int, default=100, help="dynamic workload: steps after step 0")
     ap.add_argument("--dyn-reps", type=int, default=5, help="dynamic workload: timed passes per step")
+    ap.add_argument("--store", action="store_true",
+                    help="dynamic workload: feed the device-resident graph store by deltas")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only plain copies of known size (for scaling HBM byte counters)")
     args = ap.parse_args()

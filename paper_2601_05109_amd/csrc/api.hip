@@ -267,6 +267,10 @@ struct Timer {
 
 }  // namespace
 
+hipStream_t nalar::policy_stream(const nalar_policy* h) { return h->stream; }
+int nalar::policy_device(const nalar_policy* h) { return h->device; }
+int nalar::policy_fail(nalar_policy* h, int code, const char* msg) { return fail(h, code, msg); }
+
 extern "C" {
 
 int nalar_policy_create(const nalar_policy_config* cfg, nalar_policy** out) {

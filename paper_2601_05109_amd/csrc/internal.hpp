@@ -128,6 +128,11 @@ struct GreedyArgs {
 };
 hipError_t launch_route_greedy(hipStream_t s, const GreedyArgs& g);
 
+// Handle accessors for the graph store (store.hip), defined in api.hip.
+hipStream_t policy_stream(const nalar_policy* h);
+int policy_device(const nalar_policy* h);
+int policy_fail(nalar_policy* h, int code, const char* msg);
+
 // ingest.hip
 hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
                         int32_t* wf_off, int contiguous);

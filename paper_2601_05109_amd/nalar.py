@@ -30,7 +30,10 @@ NALAR_FORCE_TILED_SORT = 2
 NALAR_MAX_INSTANCES = 1024
 
 EXPORTED = ("nalar_policy_create", "nalar_policy_pass", "nalar_policy_destroy",
-            "nalar_policy_last_error", "nalar_policy_set_timing", "nalar_policy_get_timing")
+            "nalar_policy_last_error", "nalar_policy_set_timing", "nalar_policy_get_timing",
+            "nalar_store_create", "nalar_store_destroy", "nalar_store_append", "nalar_store_complete",
+            "nalar_store_set_workflows", "nalar_store_set_instances", "nalar_store_n_nodes",
+            "nalar_store_pass")
 
 
 class NalarPolicyConfig(ctypes.Structure):
@@ -84,6 +87,23 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                             ctypes.POINTER(ctypes.c_float), ctypes.c_int,
                                             ctypes.POINTER(ctypes.c_int)]
     lib.nalar_policy_get_timing.restype = ctypes.c_int
+    P, I64, U32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32
+    lib.nalar_store_create.argtypes = [H, ctypes.POINTER(H)]
+    lib.nalar_store_create.restype = ctypes.c_int
+    lib.nalar_store_destroy.argtypes = [H]
+    lib.nalar_store_destroy.restype = None
+    lib.nalar_store_append.argtypes = [H, I64, I64, P, P, P, P, P, P, P, U32]
+    lib.nalar_store_append.restype = ctypes.c_int
+    lib.nalar_store_complete.argtypes = [H, I64, P]
+    lib.nalar_store_complete.restype = ctypes.c_int
+    lib.nalar_store_set_workflows.argtypes = [H, I64, P]
+    lib.nalar_store_set_workflows.restype = ctypes.c_int
+    lib.nalar_store_set_instances.argtypes = [H, I64, P, P, P]
+    lib.nalar_store_set_instances.restype = ctypes.c_int
+    lib.nalar_store_n_nodes.argtypes = [H]
+    lib.nalar_store_n_nodes.restype = I64
+    lib.nalar_store_pass.argtypes = [H, I64, I64, U32, ctypes.POINTER(NalarResult)]
+    lib.nalar_store_pass.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -120,6 +140,44 @@ def nalar_policy_get_timing(h: int, cap: int = 32) -> list[tuple[str, float]]:
     if rc != NALAR_OK:
         raise RuntimeError("no timed pass available")
     return [(names[i].decode(), float(ms[i])) for i in range(min(count.value, cap))]
+
+
+def nalar_store_create(h: int) -> tuple[int, Optional[int]]:
+    s = ctypes.c_void_p()
+    rc = load_library().nalar_store_create(h, ctypes.byref(s))
+    return rc, s.value
+
+
+def nalar_store_destroy(s: Optional[int]) -> None:
+    load_library().nalar_store_destroy(s)
+
+
+def nalar_store_append(s: int, n_new: int, n_new_edges: int, wf, type, est_us, done, loc, dep_off,
+                       dep_idx, flags: int = 0) -> int:
+    return load_library().nalar_store_append(s, n_new, n_new_edges, wf, type, est_us, done, loc,
+                                             dep_off, dep_idx, flags)
+
+
+def nalar_store_complete(s: int, n: int, ids) -> int:
+    return load_library().nalar_store_complete(s, n, ids)
+
+
+def nalar_store_set_workflows(s: int, n_workflows: int, deadline_us) -> int:
+    return load_library().nalar_store_set_workflows(s, n_workflows, deadline_us)
+
+
+def nalar_store_set_instances(s: int, n_instances: int, inst_type, inst_load_us,
+                              inst_speed_permille) -> int:
+    return load_library().nalar_store_set_instances(s, n_instances, inst_type, inst_load_us,
+                                                    inst_speed_permille)
+
+
+def nalar_store_n_nodes(s: Optional[int]) -> int:
+    return int(load_library().nalar_store_n_nodes(s))
+
+
+def nalar_store_pass(s: int, now_us: int, migration_cost_us: int, policy: int, res: NalarResult) -> int:
+    return load_library().nalar_store_pass(s, now_us, migration_cost_us, policy, ctypes.byref(res))
 
 
 # ---------------------------------------------------------------- torch helpers
@@ -248,6 +306,79 @@ class Policy:
 
     def timing(self) -> list[tuple[str, float]]:
         return nalar_policy_get_timing(self.handle)
+
+
+class Store:
+    """A device-resident graph store bound to a Policy: the snapshot is kept in
+    HBM across passes and updated by deltas (arrays are torch device tensors
+    or numpy arrays, uploaded first).  Copies are enqueued on the policy's
+    stream, which is the stream torch allocated the tensors on, so a tensor may
+    be dropped right after the call."""
+
+    def __init__(self, policy: "Policy"):
+        rc, h = nalar_store_create(policy.handle)
+        if rc != NALAR_OK:
+            raise NalarError(rc, policy.last_error())
+        self.policy = policy
+        self.handle = h
+
+    @staticmethod
+    def _dev(a, dtype, device="cuda"):
+        import numpy as np
+        import torch
+        if isinstance(a, np.ndarray):
+            a = torch.from_numpy(np.ascontiguousarray(a.astype(dtype, copy=False))).to(device)
+        return a
+
+    @staticmethod
+    def _ptr(t):
+        return t.data_ptr() if t is not None and t.numel() > 0 else None
+
+    def append(self, wf, type, est_us, done, loc, dep_off, dep_idx, contiguous: bool = False) -> int:
+        import numpy as np
+        t = [self._dev(a, d) for a, d in ((wf, np.int32), (type, np.int32), (est_us, np.int64),
+                                          (done, np.uint8), (loc, np.int32), (dep_off, np.int32),
+                                          (dep_idx, np.int32))]
+        n, e = int(t[0].shape[0]), int(t[6].shape[0])
+        return nalar_store_append(self.handle, n, e, *[self._ptr(x) for x in t],
+                                  NALAR_WF_CONTIGUOUS if contiguous else 0)
+
+    def complete(self, ids) -> int:
+        import numpy as np
+        t = self._dev(ids, np.int32)
+        return nalar_store_complete(self.handle, int(t.shape[0]), self._ptr(t))
+
+    def set_workflows(self, deadline_us) -> int:
+        import numpy as np
+        t = self._dev(deadline_us, np.int64)
+        return nalar_store_set_workflows(self.handle, int(t.shape[0]), self._ptr(t))
+
+    def set_instances(self, inst_type, inst_load_us, inst_speed_permille) -> int:
+        import numpy as np
+        t = [self._dev(inst_type, np.int32), self._dev(inst_load_us, np.int64),
+             self._dev(inst_speed_permille, np.int32)]
+        return nalar_store_set_instances(self.handle, int(t[0].shape[0]), *[self._ptr(x) for x in t])
+
+    @property
+    def n_nodes(self) -> int:
+        return nalar_store_n_nodes(self.handle)
+
+    def run_pass(self, out: "DeviceResult", now_us: int, migration_cost_us: int, policy: int = 0) -> int:
+        cr = out.c_struct()
+        rc = nalar_store_pass(self.handle, now_us, migration_cost_us, policy, cr)
+        out.n_ready = int(cr.n_ready) if rc == NALAR_OK else 0
+        return rc
+
+    def close(self) -> None:
+        if self.handle:
+            nalar_store_destroy(self.handle)
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
 
 
 def run(p, device: str = "cuda", policy: Optional[Policy] = None, flags: int = 0):

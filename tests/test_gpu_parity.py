@@ -525,3 +525,95 @@ def test_dynamic_stream_every_step(policy, chunk):
     for step, g, f in futs:
         assert_parity(g, f.result(), f"dynamic step {step}")
     pool.shutdown()
+
+
+# ---------------------------------------------------------------- graph store
+
+def _store_step(st, p, prev_n, prev_done):
+    """Feed snapshot p to the store as the delta from the previous one."""
+    N = p.n_nodes
+    if prev_n == 0:
+        assert st.set_workflows(p.deadline_us) == nalar.NALAR_OK
+        assert st.set_instances(p.inst_type, p.inst_load_us, p.inst_speed_permille) == nalar.NALAR_OK
+    else:
+        newly = np.flatnonzero((p.done[:prev_n] == 1) & (prev_done == 0)).astype(np.int32)
+        assert st.complete(newly) == nalar.NALAR_OK
+    e0, e1 = int(p.dep_off[prev_n]), int(p.dep_off[N])
+    rc = st.append(p.wf[prev_n:N], p.type[prev_n:N], p.est_us[prev_n:N], p.done[prev_n:N],
+                   p.loc[prev_n:N], p.dep_off[prev_n:N + 1] - e0, p.dep_idx[e0:e1],
+                   contiguous=bool(p.wf_contiguous))
+    assert rc == nalar.NALAR_OK
+    return N, p.done[:N].copy()
+
+
+def test_store_follows_dynamic_stream():
+    """The evolving map/reduce graph fed to the device-resident store as
+    deltas (completions, appended futures): every pass over the store equals
+    the oracle on the full snapshot."""
+    with nalar.Policy() as pol:
+        st = nalar.Store(pol)
+        try:
+            prev_n, prev_done = 0, None
+            for step, p in enumerate(wl.dynamic_stream(steps=30)):
+                prev_n, prev_done = _store_step(st, p, prev_n, prev_done)
+                assert st.n_nodes == p.n_nodes
+                if step % 3 == 0 or step == 30:
+                    out = nalar.DeviceResult.alloc(p.n_nodes)
+                    rc = st.run_pass(out, p.now_us, p.migration_cost_us)
+                    torch.cuda.synchronize()
+                    R = out.n_ready
+                    g = dict(status=rc, n_ready=R, rem=out.rem[:p.n_nodes].cpu().numpy(),
+                             order=out.order[:R].cpu().numpy(), slack=out.slack[:R].cpu().numpy(),
+                             route=out.route[:R].cpu().numpy(), cost=out.cost[:R].cpu().numpy(),
+                             err=pol.last_error())
+                    say(f"[gpu] store step {step}: N={p.n_nodes}")
+                    assert_parity(g, oracle.run(p), f"store step {step}")
+        finally:
+            st.close()
+
+
+def test_store_small_graphs_and_errors():
+    """Random DAGs built up in several appends (ids contiguous or not, policy
+    variants), an out-of-range completion reported by the next pass only, and
+    argument errors."""
+    with nalar.Policy() as pol:
+        for seed in range(6):
+            p = wl.random_dag(900 + seed, n_nodes=200, n_workflows=4, n_instances=12, n_types=3,
+                              shuffle_ids=bool(seed % 2))
+            st = nalar.Store(pol)
+            try:
+                assert st.set_workflows(p.deadline_us) == 0
+                assert st.set_instances(p.inst_type, p.inst_load_us, p.inst_speed_permille) == 0
+                cuts = [0, 37, 120, 120, 200]
+                for a, b in zip(cuts, cuts[1:]):
+                    e0, e1 = int(p.dep_off[a]), int(p.dep_off[b])
+                    assert st.append(p.wf[a:b], p.type[a:b], p.est_us[a:b], p.done[a:b], p.loc[a:b],
+                                     p.dep_off[a:b + 1] - e0, p.dep_idx[e0:e1],
+                                     contiguous=bool(p.wf_contiguous)) == 0
+                for bits in (0, nalar.NALAR_ORDER_LPT | nalar.NALAR_ROUTE_GREEDY):
+                    out = nalar.DeviceResult.alloc(p.n_nodes)
+                    rc = st.run_pass(out, p.now_us, p.migration_cost_us, policy=bits)
+                    torch.cuda.synchronize()
+                    R = out.n_ready
+                    g = dict(status=rc, n_ready=R, rem=out.rem[:p.n_nodes].cpu().numpy(),
+                             order=out.order[:R].cpu().numpy(), slack=out.slack[:R].cpu().numpy(),
+                             route=out.route[:R].cpu().numpy(), cost=out.cost[:R].cpu().numpy(),
+                             err=pol.last_error())
+                    assert_parity(g, oracle.run(p, policy=bits), f"store seed {seed} policy {bits}")
+                # an id out of range: the next pass fails, the one after is fine
+                assert st.complete(np.array([p.n_nodes + 5], np.int32)) == 0
+                out = nalar.DeviceResult.alloc(p.n_nodes)
+                assert st.run_pass(out, p.now_us, p.migration_cost_us) == nalar.NALAR_EINVAL
+                rc = st.run_pass(out, p.now_us, p.migration_cost_us)
+                assert rc == nalar.NALAR_OK, pol.last_error()
+                # argument errors
+                z = np.zeros(0, np.int32)
+                assert nalar.nalar_store_append(st.handle, -1, 0, None, None, None, None, None, None,
+                                                None, 0) == nalar.NALAR_EINVAL
+                assert nalar.nalar_store_append(st.handle, 1, 0, None, None, None, None, None, None,
+                                                None, 0) == nalar.NALAR_EINVAL
+                assert nalar.nalar_store_complete(st.handle, -1, None) == nalar.NALAR_EINVAL
+                assert nalar.nalar_store_pass(st.handle, 0, 0, 16, out.c_struct()) == nalar.NALAR_EINVAL
+                del z
+            finally:
+                st.close()

@@ -11,13 +11,17 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "nalar_policy.h")
+HEADERS = [os.path.join(ROOT, "include", f) for f in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if f.endswith(".h")]
 LIB = os.path.join(ROOT, "paper_2601_05109_amd", "libnalar_policy.so")
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(nalar_policy_\w+)\s*\(", text)))
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(nalar_(?:policy|store)_\w+)\s*\(", text))
+    return sorted(names)
 
 
 @pytest.fixture(scope="module")
@@ -31,7 +35,8 @@ def lib():
 def test_header_declares_the_abi():
     names = declared_functions()
     for required in ("nalar_policy_create", "nalar_policy_pass", "nalar_policy_destroy",
-                     "nalar_policy_last_error"):
+                     "nalar_policy_last_error", "nalar_store_create", "nalar_store_append",
+                     "nalar_store_complete", "nalar_store_pass"):
         assert required in names
 
 
