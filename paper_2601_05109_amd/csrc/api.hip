@@ -1,25 +1,31 @@
 // C ABI of the policy pass: handle, scratch arena, launch sequence, status.
 //
-// A pass is a fixed sequence of launches on the handle's stream:
-//   nodes  -> validate the snapshot, sort the instance table, workflow offsets
-//   group  -> (only when the caller's ids are not grouped by workflow) stable
-//             radix sort of the ids by workflow
-//   sweep  -> remaining critical path, readiness, slack and routing
-//   sort   -> bucketed: the sweep has dropped every ready future into a
-//             bucket of a slack range guessed from the previous pass, and one
-//             kernel orders each bucket and writes it at its offset; or tiled:
-//             slack histogram and range, then four digit passes (those the
-//             range does not need return at once).  The last kernel gathers
-//             into the caller's arrays and writes the status into pinned host
-//             memory
-// followed by one stream synchronisation.  The bucketed sort is used once a
-// previous pass has given a slack range and at most kBucketMaxReady futures
-// were ready; if a bucket overflows, the kernel reports "tiled" and the tiled
-// sort follows after the synchronisation (then the bucketed sort is skipped for
-// a few passes).  A slack range wider than 32 bits reports "continue" from the
-// tiled sort and its remaining passes follow after another synchronisation.
-// The node kernel resets the next pass's control block and clears the bucket
-// counters.
+// A pass is a short sequence of launches on the handle's stream:
+//   [reset]  -> only when a control block or bucket counters are stale
+//   [nodes]  -> unless the sweep is fused: validate the snapshot, sort the
+//               instance table, workflow offsets
+//   [group]  -> only when the caller's ids are not grouped by workflow: stable
+//               radix sort of the ids by workflow
+//   sweep    -> remaining critical path, readiness, order key and routing;
+//               in fused mode (contiguous ids, workflows of at most 512
+//               futures, at most 128 instances) also validation, workflow
+//               bounds, the instance table and the reset of the next pass's
+//               control block and bucket counters
+//   sort     -> bucketed: the sweep has dropped every ready future into a
+//               bucket of a key range planned from the previous pass, and one
+//               kernel (two for many buckets) orders each bucket and writes it
+//               at its offset; or tiled: key histogram and range, then up to
+//               four digit passes.  The last kernel writes the caller's arrays
+//               and the status into pinned host memory
+//   [greedy] -> NALAR_ROUTE_GREEDY only: routing again in output order
+// with one stream synchronisation after the sort (and one after greedy
+// routing).  The bucketed sort is used once a previous pass has given a key
+// range and at most kBucketMaxReady futures were ready; if a bucket
+// overflows, the kernel reports "tiled", and after the synchronisation the
+// host resets the control block, sweeps again without buckets and runs the
+// tiled sort (then skips the bucketed sort for a few passes).  A key range
+// wider than 32 bits reports "continue" from the tiled sort and its remaining
+// passes follow after another synchronisation.
 #include <cstdio>
 #include <cstring>
 #include <string>

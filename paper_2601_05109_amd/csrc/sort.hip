@@ -1,4 +1,13 @@
-// Stable LSD radix sort of (key, payload) pairs.  Each 8-bit digit pass is one
+// The order of the ready futures, and the grouping of ids by workflow.
+//
+// Bucketed sort (the usual pass): the sweep has dropped every ready future
+// into one of nb buckets of its order key, planned from the previous pass's
+// range; k_bucket_sort (or k_bucket_totals + k_bucket_sort_lb for many
+// buckets) finds each bucket's offset, ranks the futures inside a bucket by
+// (key, position) and writes order, slack, route and cost in place.
+//
+// Tiled sort (first pass, bucket overflow, very large ready sets):
+// stable LSD radix sort of (key, payload) pairs.  Each 8-bit digit pass is one
 // launch that ranks tiles of 4096 items in LDS and finds their global offsets
 // by decoupled look-back over earlier tiles ("onesweep": one upfront histogram
 // of every digit instead of a scan per pass).  Passes beyond what the key

@@ -1,10 +1,10 @@
-// Per-workflow sweep: remaining critical path, readiness, slack, routing and
-// order-preserving compaction of the ready futures, in one kernel.
+// Per-workflow sweep: remaining critical path, readiness, order key and
+// routing of every future, in one kernel.
 //
 // Futures of different workflows never depend on each other (one global
 // controller per workflow, Section 4.1; cross-workflow dependencies are
-// rejected), so each workgroup takes whole workflows and runs the reverse level-synchronous max-plus sweep of each one with workgroup
-// barriers only:
+// rejected), so workflows are swept independently, each by the reverse
+// level-synchronous max-plus sweep:
 //
 //   cnt[u] = number of consumers of u (atomic out-degree counters)
 //   level 0 = futures with no consumer; a future joins a level when its last
@@ -17,18 +17,21 @@
 // targets the same future (a fan-in such as a map/reduce root), the wave
 // reduces first and one lane issues a single atomic.
 //
-// Workflows up to `lds_cap` futures keep the counters in LDS and each thread
-// owns up to NPT futures, holding their service time and up to three
-// dependency indices in registers, so a level costs two workgroup barriers and
-// a few LDS operations.  Larger workflows keep the state in HBM (by position)
-// and process explicit frontier lists.  Futures with more dependencies than a
-// thread keeps are handled by the whole workgroup.
+// Three shapes:
+//  * k_sweep_wave: one wavefront per workflow of at most 512 futures (four
+//    independent waves per workgroup, no workgroup barrier in the sweep), the
+//    workflow's state in a 14-byte-per-future LDS slice, each lane owning up
+//    to eight futures with their dependencies in registers; the levels are
+//    rounds of LDS atomics.  In fused mode it also validates the snapshot,
+//    finds each workflow's bounds and builds the routing table itself.
+//  * k_sweep: one workgroup per workflow of up to 5,120 futures (LDS state).
+//  * workflows larger than that (or all, under NALAR_FORCE_GLOBAL_SWEEP) keep
+//    their state in HBM by position and process explicit frontier lists,
+//    swept by the workgroup that met them.
 //
-// Workgroups take workflows round-robin and never wait on each other.  Each
-// ready future is routed and written, with its slack, at its own position
-// (workflows ascending, ids ascending inside a workflow); the first digit pass
-// of the slack sort skips the other positions, which compacts the list without
-// disturbing that order.
+// Every ready future is routed against the pass-start instance table and then
+// either dropped into its order-key bucket (one returning atomic for a slot)
+// or, when the tiled sort is planned, staged by position.
 #include "internal.hpp"
 
 namespace nalar {
