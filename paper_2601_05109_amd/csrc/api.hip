@@ -90,6 +90,8 @@ struct nalar_policy {
   int64_t hint_ready = 0, hint_min = 0, hint_max = 0;
   int bucket_skip = 0;           // passes left before the bucketed sort is tried again
   int bucket_backoff = 1;
+  int bucket_dense = 0;          // buckets doubled this many times after overflows
+  int bucket_calm = 0;           // bucketed passes without overflow since the last change
   std::string err;
   Arena ar;
   HostStatus* host = nullptr;    // pinned, written by the sort kernel
@@ -213,9 +215,12 @@ BucketArgs plan_buckets(const nalar_policy* h, int64_t N) {
     return bk;
   // about two futures per bucket, four for large ready sets (fewer buckets to
   // scan and clear; the 64 slots of a bucket still leave ample headroom)
+  // after an overflow (keys crowded into a few buckets, e.g. a long-tailed
+  // key), later passes try twice, four or eight times as many buckets
   const int64_t per = h->hint_ready <= kBucketDense ? 2 : 4;
   int64_t nb = kBucketMin;
   while (nb < kBucketMax && nb * per <= h->hint_ready) nb *= 2;
+  for (int i = 0; i < h->bucket_dense && nb < kBucketMax; ++i) nb *= 2;
   int lognb = 0;
   while ((int64_t(1) << lognb) < nb) ++lognb;
   const uint64_t range = uint64_t(h->hint_max) - uint64_t(h->hint_min);
@@ -512,13 +517,22 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
       // into; the next pass's control block and counters are reset again too.
       __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);
       tiled = true;
-      h->bucket_skip = h->bucket_backoff;
-      h->bucket_backoff = h->bucket_backoff < 64 ? 2 * h->bucket_backoff : 64;
+      h->bucket_calm = 0;
+      if (h->bucket_dense < 3) {  // retry at once with more buckets
+        ++h->bucket_dense;
+      } else {                    // then back off
+        h->bucket_skip = h->bucket_backoff;
+        h->bucket_backoff = h->bucket_backoff < 64 ? 2 * h->bucket_backoff : 64;
+      }
       NALAR_LAUNCH("reset", launch_reset(s, ctrl, nullptr, 0));
       sw.bk = BucketArgs{};
       NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
     } else {
       h->bucket_backoff = 1;
+      if (h->bucket_dense > 0 && ++h->bucket_calm >= 64) {  // try fewer buckets again
+        --h->bucket_dense;
+        h->bucket_calm = 0;
+      }
     }
   }
   if (tiled) {
