@@ -54,7 +54,7 @@ def _load() -> ctypes.CDLL:
         lib.nalar_oracle_pass.restype = ctypes.c_int
         lib.nalar_oracle_pass.argtypes = [I64] * 6 + [P] * 17
         lib.nalar_oracle_pass_policy.restype = ctypes.c_int
-        lib.nalar_oracle_pass_policy.argtypes = [I64] * 6 + [ctypes.c_uint32] + [P] * 17
+        lib.nalar_oracle_pass_policy.argtypes = [I64] * 6 + [ctypes.c_uint32] + [P] * 18
         _lib = lib
     return _lib
 
@@ -75,10 +75,11 @@ def _ptr(a: Optional[np.ndarray]):
 
 
 def run(p, *, want_rem: bool = True, override: Optional[dict] = None,
-        policy: int = 0) -> OracleResult:
+        policy: int = 0, priority: Optional[np.ndarray] = None) -> OracleResult:
     """Run the oracle on a problem (any object with the workloads.Problem
     fields).  ``override`` may replace scalar sizes or set arrays to None, to
-    exercise validation; ``policy`` selects the variants (POLICY_* bits)."""
+    exercise validation; ``policy`` selects the variants (POLICY_* bits) and
+    ``priority`` (uint8 per workflow, or None) the priority levels."""
     lib = _load()
     o = dict(N=p.n_nodes, E=p.n_edges, W=p.n_workflows, M=p.n_instances,
              now=p.now_us, mig=p.migration_cost_us)
@@ -98,8 +99,9 @@ def run(p, *, want_rem: bool = True, override: Optional[dict] = None,
     route = np.zeros(n_out, np.int32)
     cost = np.zeros(n_out, np.int64)
     n_ready = ctypes.c_int64(0)
+    prio = None if priority is None else np.ascontiguousarray(priority, dtype=np.uint8)
     rc = lib.nalar_oracle_pass_policy(
-        o["N"], o["E"], o["W"], o["M"], o["now"], o["mig"], policy,
+        o["N"], o["E"], o["W"], o["M"], o["now"], o["mig"], policy, _ptr(prio),
         *[_ptr(arrays[f]) for f in ("wf", "type", "est_us", "done", "loc", "dep_off",
                                     "dep_idx", "deadline_us", "inst_type", "inst_load_us",
                                     "inst_speed_permille")],

@@ -47,6 +47,10 @@
 //              it, then adds its service time on that instance,
 //              est*1000/speed, to that instance's load (routing that balances
 //              load across instances, Section 6.1); a load above 2^62 -> -3
+//   priorities (a per-workflow level 0..15, set_priority of Table 2): O9
+//              sorts by (-priority[wf], key, wf, v), the higher level first;
+//              a level above 15 -> -1, and a ready future whose key (slack,
+//              or -rem under kLpt) lies outside (-2^58, 2^58) -> -3
 //
 // Precedence of errors: EINVAL, then ECYCLE, then ERANGE.
 #include <algorithm>
@@ -64,6 +68,8 @@ constexpr int kErange = -3;
 constexpr uint32_t kLpt = 2u;
 constexpr uint32_t kStateful = 4u;
 constexpr uint32_t kGreedy = 8u;
+constexpr int kMaxPriority = 15;
+constexpr int64_t kPrioKeyBound = int64_t(1) << 58;
 
 constexpr int64_t kMaxNodes = int64_t(1) << 30;
 constexpr int64_t kMaxEdges = (int64_t(1) << 31) - 1;
@@ -126,7 +132,8 @@ extern "C" {
 // must hold n_nodes entries (rem) and n_nodes entries (order, slack, route,
 // cost); rem_out and cost_out may be NULL.  Returns 0 or a negative error code.
 int nalar_oracle_pass_policy(int64_t N, int64_t E, int64_t W, int64_t M, int64_t now, int64_t mig,
-                             uint32_t policy, const int32_t* wf, const int32_t* type,
+                             uint32_t policy, const uint8_t* priority, const int32_t* wf,
+                             const int32_t* type,
                              const int64_t* est, const uint8_t* done, const int32_t* loc,
                              const int32_t* dep_off, const int32_t* dep_idx,
                              const int64_t* deadline, const int32_t* inst_type,
@@ -134,6 +141,9 @@ int nalar_oracle_pass_policy(int64_t N, int64_t E, int64_t W, int64_t M, int64_t
                              int32_t* order_out, int64_t* slack_out, int32_t* route_out,
                              int64_t* cost_out, int64_t* n_ready_out) {
   if ((policy & ~(kLpt | kStateful | kGreedy)) != 0) return kEinval;
+  if (priority)
+    for (int64_t w = 0; w < W; ++w)
+      if (priority[w] > kMaxPriority) return kEinval;
   int rc = validate(N, E, W, M, now, mig, wf, type, est, done, loc, dep_off, dep_idx,
                     deadline, inst_type, inst_load, inst_speed);
   if (rc != kOk) return rc;
@@ -227,11 +237,18 @@ int nalar_oracle_pass_policy(int64_t N, int64_t E, int64_t W, int64_t M, int64_t
     cost[v] = best;
   }
 
-  // O9: the full key (slack, wf, v), or (-rem, wf, v) under kLpt, is a total
-  // order, so the result is unique.
+  // O9: the full key (slack, wf, v), or (-rem, wf, v) under kLpt, behind the
+  // workflow's priority level when given, is a total order, so the result is
+  // unique.
   const bool lpt = (policy & kLpt) != 0;
+  if (priority)
+    for (int32_t v : ready_ids) {
+      const int64_t k = lpt ? -rem[v] : slack[v];
+      if (k <= -kPrioKeyBound || k >= kPrioKeyBound) return kErange;
+    }
   std::vector<int32_t> order(ready_ids);
   std::sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+    if (priority && priority[wf[a]] != priority[wf[b]]) return priority[wf[a]] > priority[wf[b]];
     const int64_t ka = lpt ? -rem[a] : slack[a];
     const int64_t kb = lpt ? -rem[b] : slack[b];
     if (ka != kb) return ka < kb;
@@ -287,7 +304,7 @@ int nalar_oracle_pass(int64_t N, int64_t E, int64_t W, int64_t M, int64_t now, i
                       const int32_t* inst_speed, int64_t* rem_out, int32_t* order_out,
                       int64_t* slack_out, int32_t* route_out, int64_t* cost_out,
                       int64_t* n_ready_out) {
-  return nalar_oracle_pass_policy(N, E, W, M, now, mig, 0u, wf, type, est, done, loc, dep_off,
+  return nalar_oracle_pass_policy(N, E, W, M, now, mig, 0u, nullptr, wf, type, est, done, loc, dep_off,
                                   dep_idx, deadline, inst_type, inst_load, inst_speed, rem_out,
                                   order_out, slack_out, route_out, cost_out, n_ready_out);
 }

@@ -20,7 +20,8 @@ from test_oracle_pins import (brute_force_rem, push_replay_ready, rem_certificat
                               test_lpt_equals_srtf_when_deadlines_are_equal,
                               test_lpt_independent_futures_closed_form, test_stateful_routing_pins,
                               test_greedy_single_instance_prefix_sums,
-                              test_greedy_identical_instances_round_robin)
+                              test_greedy_identical_instances_round_robin,
+                              test_priority_levels_partition_the_order)
 
 MUTATIONS = {
     "drop_est_term": ("if (__builtin_add_overflow(est_eff[v], best, &r)",
@@ -48,6 +49,8 @@ MUTATIONS = {
                               "cost[v] = inst_load[i] + (est[v] * 1000) / inst_speed[i] + mig;"),
     "greedy_no_load_update": ("        load[arg] += (est[v] * 1000) / inst_speed[arg];\n", ""),
     "greedy_adds_cost": ("load[arg] += (est[v] * 1000) / inst_speed[arg];", "load[arg] += best;"),
+    "priority_low_first": ("return priority[wf[a]] > priority[wf[b]];",
+                           "return priority[wf[a]] < priority[wf[b]];"),
     "stateful_any_type": ("if ((policy & kStateful) && loc[v] >= 0 && inst_type[loc[v]] == type[v]) {\n      const int32_t i",
                           "if ((policy & kStateful) && loc[v] >= 0) {\n      const int32_t i"),
     "max_with_first_successor_only": (
@@ -75,7 +78,7 @@ def _pins_pass(lib_path):
     lib.nalar_oracle_pass.restype = ctypes.c_int
     lib.nalar_oracle_pass.argtypes = [ctypes.c_int64] * 6 + [ctypes.c_void_p] * 17
     lib.nalar_oracle_pass_policy.restype = ctypes.c_int
-    lib.nalar_oracle_pass_policy.argtypes = [ctypes.c_int64] * 6 + [ctypes.c_uint32] + [ctypes.c_void_p] * 17
+    lib.nalar_oracle_pass_policy.argtypes = [ctypes.c_int64] * 6 + [ctypes.c_uint32] + [ctypes.c_void_p] * 18
     oracle._lib = lib
     try:
         for g in golden_names():
@@ -105,6 +108,11 @@ def _pins_pass(lib_path):
                     test_greedy_identical_instances_round_robin):
             try:
                 pin()
+            except AssertionError:
+                return False
+        for pin in (test_priority_levels_partition_the_order,):
+            try:
+                pin(0)
             except AssertionError:
                 return False
         return True

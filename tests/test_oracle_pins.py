@@ -476,6 +476,40 @@ def test_greedy_load_overflow_is_erange():
     assert oracle.run(p, policy=GREEDY).status == oracle.ERANGE
 
 
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_priority_levels_partition_the_order(cfg):
+    """set_priority levels per workflow: the order is the default order split
+    stably by level, highest level first; slack, route and cost travel with
+    their futures; equal levels change nothing."""
+    p = wl.CONFIGS[cfg]()
+    rng = np.random.default_rng(cfg)
+    base = oracle.run(p)
+    flat = oracle.run(p, priority=np.full(p.n_workflows, 7, np.uint8))
+    for f in ("order", "slack", "route", "cost", "rem"):
+        np.testing.assert_array_equal(getattr(base, f), getattr(flat, f))
+    for bits in (0, LPT):
+        pr = rng.integers(0, 16, p.n_workflows).astype(np.uint8)
+        a, b = oracle.run(p, policy=bits), oracle.run(p, policy=bits, priority=pr)
+        lv = pr[p.wf[a.order]]
+        want = np.concatenate([a.order[lv == x] for x in range(15, -1, -1)])
+        np.testing.assert_array_equal(b.order, want)
+        pos = {int(v): i for i, v in enumerate(a.order.tolist())}
+        idx = np.array([pos[int(v)] for v in b.order.tolist()], np.int64)
+        for f in ("slack", "route", "cost"):
+            np.testing.assert_array_equal(getattr(b, f), getattr(a, f)[idx])
+
+
+def test_priority_level_and_key_rules():
+    p = wl.tiny()
+    pr = np.zeros(p.n_workflows, np.uint8)
+    pr[3] = 16
+    assert oracle.run(p, priority=pr).status == oracle.EINVAL
+    far = p.copy(deadline_us=p.deadline_us.copy())
+    far.deadline_us[0] = p.now_us + (1 << 60)   # slack beyond 2^58
+    assert oracle.run(far).status == oracle.OK
+    assert oracle.run(far, priority=np.zeros(p.n_workflows, np.uint8)).status == oracle.ERANGE
+
+
 # ---------------------------------------------------------------- degenerate
 
 def _single(est=5, done=0):
