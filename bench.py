@@ -338,6 +338,8 @@ def main() -> int:
                          "routes in output order with running instance loads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--priority-levels", type=int, default=0,
+                    help="give every workflow a seeded priority level in [0, L) (set_priority); 0 = none")
     ap.add_argument("--dyn-steps", type=int, default=100, help="dynamic workload: steps after step 0")
     ap.add_argument("--dyn-reps", type=int, default=5, help="dynamic workload: timed passes per step")
     ap.add_argument("--store", action="store_true",
@@ -370,7 +372,12 @@ def main() -> int:
             "lpt+stateful": nalar.NALAR_ORDER_LPT | nalar.NALAR_ROUTE_STATEFUL,
             "greedy": nalar.NALAR_ROUTE_GREEDY,
             "greedy+stateful": nalar.NALAR_ROUTE_GREEDY | nalar.NALAR_ROUTE_STATEFUL}[args.policy]
-    cp = dp.c_struct(policy=bits)
+    prio = None
+    if args.priority_levels > 0:
+        import numpy as np
+        lv = np.random.default_rng(7).integers(0, args.priority_levels, W).astype(np.uint8)
+        prio = torch.from_numpy(lv).to(dev)
+    cp = dp.c_struct(policy=bits, priority=prio)
 
     def one_pass():
         cr = out.c_struct()
@@ -433,7 +440,8 @@ def main() -> int:
         "data": "synthetic (seeded generator, paper-scale shape)",
         "config": {"workload": f"{p.name}: {W} workflows x {N // max(W, 1)} futures = {N} futures, "
                                f"{E} dependencies, {R} ready, K=8 types, {M} instances",
-                   "n_futures": N, "n_ready": R, "policy": args.policy},
+                   "n_futures": N, "n_ready": R, "policy": args.policy,
+                   "priority_levels": args.priority_levels},
         "latency_us": {"p50": lat_us[len(lat_us) // 2], "p99": lat_us[min(len(lat_us) - 1, int(0.99 * len(lat_us)))],
                        "min": lat_us[0], "gpu_event_mean": 1e3 * gpu_ms / args.steps},
         "kernels_us": {k: round(1e3 * v, 2) for k, v in kern.items()},

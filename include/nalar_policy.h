@@ -57,6 +57,8 @@ enum {
 #define NALAR_MIG_MAX        (INT64_C(1) << 60)  /* migration penalty, us        */
 #define NALAR_HORIZON_MAX    (INT64_C(1) << 61)  /* |now|, |deadline - now|      */
 #define NALAR_REM_MAX        (INT64_C(1) << 62)  /* remaining critical path, us  */
+#define NALAR_PRIORITY_MAX   15                  /* highest priority level       */
+#define NALAR_PRIORITY_KEY   (INT64_C(1) << 58)  /* |order key| bound with levels */
 
 /* nalar_problem.flags */
 #define NALAR_WF_CONTIGUOUS  1u  /* the nodes of workflow w are exactly the ids
@@ -146,6 +148,14 @@ typedef struct {
   const int32_t* inst_type;   /* [M] component type of each instance, >= 0       */
   const int64_t* inst_load_us;/* [M] queued work, [0, NALAR_LOAD_MAX]            */
   const int32_t* inst_speed_permille; /* [M] speed relative to nominal, >= 1      */
+  const uint8_t* wf_priority; /* [W] priority level of each workflow (session),
+                                 0..NALAR_PRIORITY_MAX, or NULL for none: the
+                                 ready futures of a higher level come first in
+                                 the order, whatever their key (set_priority,
+                                 Table 2).  With levels, every ready future's
+                                 order key (the slack, or -rem under
+                                 NALAR_ORDER_LPT) must lie strictly inside
+                                 +-NALAR_PRIORITY_KEY, else NALAR_ERANGE         */
 } nalar_problem;
 
 /* Outputs.  Struct in host memory; array pointers are DEVICE pointers, owned by
@@ -184,7 +194,9 @@ int nalar_policy_create(const nalar_policy_config* cfg, nalar_policy** out);
  *   route[v] = the instance i with inst_type[i] == type[v] minimising
  *              (cost(v,i), i) lexicographically (the lowest index wins ties),
  *              or -1 with cost INT64_MAX when there is none
- *   order    = the ready futures sorted by (slack, wf, id) ascending
+ *   order    = the ready futures sorted by (slack, wf, id) ascending (behind
+ *              the priority level of their workflow, highest first, when
+ *              wf_priority is given)
  * (the NALAR_ORDER_LPT, NALAR_ROUTE_STATEFUL and NALAR_ROUTE_GREEDY bits change
  * order and route as described at their definitions).
  * Synchronous.  NULL p, r, or a required array (a node array when N > 0,

@@ -208,9 +208,11 @@ int ensure_capacity(nalar_policy* h, int64_t N, int64_t W, int64_t B) {
 
 // Buckets for this pass from the previous pass's ready count and slack range
 // (nb == 0: use the tiled sort).
-BucketArgs plan_buckets(const nalar_policy* h, int64_t N) {
+BucketArgs plan_buckets(const nalar_policy* h, int64_t N, bool levels) {
   BucketArgs bk{};
-  if ((h->flags & NALAR_FORCE_TILED_SORT) || !h->hint_valid || h->bucket_skip > 0 || N == 0 ||
+  // priority levels put keys 2^59 apart: buckets over that range would put a
+  // whole level in one bucket, so those passes take the tiled sort
+  if (levels || (h->flags & NALAR_FORCE_TILED_SORT) || !h->hint_valid || h->bucket_skip > 0 || N == 0 ||
       h->hint_ready > kBucketMaxReady)
     return bk;
   // about two futures per bucket, four for large ready sets (fewer buckets to
@@ -253,6 +255,7 @@ int check_problem(nalar_policy* h, const nalar_problem* p, const nalar_result* r
     return fail(h, NALAR_EINVAL, "NULL node array");
   if (E > 0 && !p->dep_idx) return fail(h, NALAR_EINVAL, "NULL dep_idx");
   if (W > 0 && !p->deadline_us) return fail(h, NALAR_EINVAL, "NULL deadline_us");
+  if (W == 0 && p->wf_priority) return fail(h, NALAR_EINVAL, "wf_priority without workflows");
   if (M > 0 && (!p->inst_type || !p->inst_load_us || !p->inst_speed_permille))
     return fail(h, NALAR_EINVAL, "NULL instance array");
   if (N > 0 && (!r->order || !r->slack_us || !r->route))
@@ -377,7 +380,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   hipError_t e = hipSetDevice(h->device);
   if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
   const int64_t N = p->n_nodes, W = p->n_workflows, M = p->n_instances;
-  BucketArgs bk = plan_buckets(h, N);
+  BucketArgs bk = plan_buckets(h, N, p->wf_priority != nullptr);
   if (h->bucket_skip > 0) --h->bucket_skip;
   rc = ensure_capacity(h, N, W, bk.nb);
   if (rc != NALAR_OK) return rc;
@@ -405,7 +408,8 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   const uint32_t policy = p->flags & (NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL | NALAR_ROUTE_GREEDY);
   ProblemDev pd{N, p->n_edges, W, M, p->now_us, p->migration_cost_us, policy, 0u,
                 p->wf, p->type, p->est_us, p->done, p->loc, p->dep_off, p->dep_idx,
-                p->deadline_us, p->inst_type, p->inst_load_us, p->inst_speed_permille};
+                p->deadline_us, p->inst_type, p->inst_load_us, p->inst_speed_permille,
+                p->wf_priority};
   const bool contiguous = (p->flags & NALAR_WF_CONTIGUOUS) != 0 || W <= 1;
 
   Timer tm{h};
@@ -489,7 +493,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   sa.stg_route = A.stg_route;
   sa.stg_cost = A.stg_cost;
   sa.node_of_pos = node_of_pos;
-  sa.out_slack = (policy & NALAR_ORDER_LPT) ? A.stg_oslack : nullptr;
+  sa.out_slack = ((policy & NALAR_ORDER_LPT) || p->wf_priority) ? A.stg_oslack : nullptr;
   sa.span = N;
   for (int i = 0; i < 2; ++i) {
     sa.key[i] = A.skey[i];

@@ -9,6 +9,11 @@
 namespace nalar {
 
 // Status word bits (ORed by any kernel that finds a problem).
+// Priority levels shift the order key by level * 2^kPrioShift; keys must stay
+// inside (-kPrioKeyBound, kPrioKeyBound) so that levels never interleave.
+constexpr int kPrioShift = 59;
+constexpr int64_t kPrioKeyBound = int64_t(1) << 58;
+
 constexpr uint32_t kStInval = 1u;
 constexpr uint32_t kStCycle = 2u;
 constexpr uint32_t kStRange = 4u;

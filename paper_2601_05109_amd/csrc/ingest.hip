@@ -78,7 +78,8 @@ __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl
   }
   for (int64_t w = g0; w < W; w += stride) {
     const int64_t dl = p.deadline[w];
-    bad |= (dl < p.now - NALAR_HORIZON_MAX) | (dl > p.now + NALAR_HORIZON_MAX);
+    bad |= (dl < p.now - NALAR_HORIZON_MAX) | (dl > p.now + NALAR_HORIZON_MAX) |
+           (p.prio != nullptr && p.prio[w] > NALAR_PRIORITY_MAX);
   }
   for (int64_t i = g0; i < M; i += stride) {
     const int64_t ld = p.inst_load[i];

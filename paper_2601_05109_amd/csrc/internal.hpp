@@ -25,6 +25,7 @@ struct ProblemDev {
   const int32_t* inst_type;
   const int64_t* inst_load;
   const int32_t* inst_speed;
+  const uint8_t* prio;          // [W] priority level per workflow, or NULL
 };
 
 enum RadixSource : int {

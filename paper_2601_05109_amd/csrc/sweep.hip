@@ -229,16 +229,28 @@ __device__ inline void bucket_put(const SweepArgs& a, uint32_t bkt, uint32_t slo
 }
 
 // The key the ready futures are ordered by: the slack, or under
-// NALAR_ORDER_LPT the negated remaining critical path (longest first).
-__device__ inline int64_t order_key(const SweepArgs& a, int64_t rem, int64_t dl) {
-  return (a.p.policy & NALAR_ORDER_LPT) ? -rem : dl - rem;
+// NALAR_ORDER_LPT the negated remaining critical path (longest first); with
+// priority levels, minus level * 2^59 (kofs), so that a higher level comes
+// first while keys stay inside (-2^58, 2^58) (checked in store_ready).
+__device__ inline int64_t order_key(const SweepArgs& a, int64_t rem, int64_t dl, int64_t kofs) {
+  return ((a.p.policy & NALAR_ORDER_LPT) ? -rem : dl - rem) + kofs;
+}
+
+// The key offset of workflow w's priority level (0 without levels).
+__device__ inline int64_t prio_offset(const SweepArgs& a, int64_t w) {
+  return a.p.prio ? -(int64_t(a.p.prio[w]) << kPrioShift) : 0;
 }
 
 // Stores of one ready future: its bucket slot (bucketed sort) or its staged
 // values by position (tiled sort), and its slack by position when the key is
 // not the slack.
 __device__ inline void store_ready(const SweepArgs& a, uint32_t bkt, uint32_t slot, int64_t key,
-                                   int64_t slack, int64_t pos, int32_t route, int64_t cost, Acc& acc) {
+                                   int64_t kofs, int64_t slack, int64_t pos, int32_t route, int64_t cost,
+                                   Acc& acc) {
+  if (a.p.prio) {
+    const int64_t k0 = key - kofs;
+    if (k0 <= -kPrioKeyBound || k0 >= kPrioKeyBound) flag_sweep(a.ctrl, kStRange);
+  }
   if (a.bk.nb > 0) {
     bucket_put(a, bkt, slot, key, pos, route, cost);
   } else {
@@ -246,15 +258,16 @@ __device__ inline void store_ready(const SweepArgs& a, uint32_t bkt, uint32_t sl
     a.stg_route[pos] = route;
     a.stg_cost[pos] = cost;
   }
-  if (a.p.policy & NALAR_ORDER_LPT) a.stg_oslack[pos] = slack;
+  if ((a.p.policy & NALAR_ORDER_LPT) || a.p.prio) a.stg_oslack[pos] = slack;
   acc.tmin = key < acc.tmin ? key : acc.tmin;
   acc.tmax = key > acc.tmax ? key : acc.tmax;
   acc.tready += 1;
 }
 
 __device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_t pos, int32_t type,
-                                   int32_t loc, int64_t rem, int64_t est, int64_t dl, Acc& acc) {
-  const int64_t key = order_key(a, rem, dl);
+                                   int32_t loc, int64_t rem, int64_t est, int64_t dl, int64_t kofs,
+                                   Acc& acc) {
+  const int64_t key = order_key(a, rem, dl, kofs);
   const BucketArgs& bk = a.bk;
   uint32_t bkt = 0, slot = 0;
   if (bk.nb > 0) {
@@ -265,7 +278,7 @@ __device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_
   int64_t cost;
   route_future(type, est, loc, int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load, it.speed,
                it.inv, it.pos, it.run, (a.p.policy & NALAR_ROUTE_STATEFUL) != 0, route, cost);
-  store_ready(a, bkt, slot, key, dl - rem, pos, route, cost, acc);
+  store_ready(a, bkt, slot, key, kofs, dl - rem, pos, route, cost, acc);
 }
 
 // ------------------------------------------------------------ LDS workflow
@@ -284,7 +297,7 @@ __device__ inline int dep_at(uint32_t p01, uint32_t p2, int q) {
 template <int T, int NPT>
 __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
                           int64_t* mx, int32_t* cnt, uint8_t* dn, uint8_t* nr, int lds_cap, int64_t b,
-                          int n, int64_t dl, Acc& acc) {
+                          int n, int64_t dl, int64_t kofs, Acc& acc) {
   const int tid = threadIdx.x;
   Ctrl* ctrl = a.ctrl;
 
@@ -469,7 +482,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
     bkt[j] = 0;
     slot[j] = 0;
     if (bk.nb > 0 && ((ready >> j) & 1u)) {
-      bkt[j] = bucket_of(bk, order_key(a, mx[j * T + tid], dl));
+      bkt[j] = bucket_of(bk, order_key(a, mx[j * T + tid], dl, kofs));
       slot[j] = add_agent(bk.cnt + bkt[j], 1u);
     }
   }
@@ -495,8 +508,8 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
   for (int j = 0; j < NPT; ++j) {
     if (!((ready >> j) & 1u)) continue;
     const int k = j * T + tid;
-    store_ready(a, bkt[j], slot[j], order_key(a, mx[k], dl), dl - mx[k], b + k, route[j], cost[j],
-                acc);
+    store_ready(a, bkt[j], slot[j], order_key(a, mx[k], dl, kofs), kofs, dl - mx[k], b + k, route[j],
+                cost[j], acc);
   }
 }
 
@@ -504,7 +517,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
 
 template <int T, bool kFused>
 __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
-                          int w, int64_t b, int n, int64_t dl, Acc& acc) {
+                          int w, int64_t b, int n, int64_t dl, int64_t kofs, Acc& acc) {
   const int tid = threadIdx.x;
   Ctrl* ctrl = a.ctrl;
   int32_t* cnt = a.g_cnt + b;
@@ -680,7 +693,7 @@ __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, con
   for (int k = tid; k < n; k += T) {
     if (dn[k] == 0 && nr[k] == 0) {
       const int32_t v = node_at(L, b + k);
-      write_ready(a, it, b + k, a.p.type[v], a.p.loc[v], ld_wg(&mx[k]), a.p.est[v], dl, acc);
+      write_ready(a, it, b + k, a.p.type[v], a.p.loc[v], ld_wg(&mx[k]), a.p.est[v], dl, kofs, acc);
     }
   }
   __syncthreads();
@@ -901,7 +914,8 @@ __device__ __attribute__((always_inline)) inline void rounds(
 // are pushed by the whole wave from the dependency list.
 template <int NPTW, bool kFused>
 __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& it,
-                           const WaveSlice& W, int64_t w, int64_t b, int n, int64_t dl, Acc& acc,
+                           const WaveSlice& W, int64_t w, int64_t b, int n, int64_t dl, int64_t kofs,
+                           Acc& acc,
                            ItabStage& st) {
   const int ln = lane_id();
   Ctrl* ctrl = a.ctrl;
@@ -1034,7 +1048,7 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
     bkt[j] = 0;
     slot[j] = 0;
     if (bk.nb > 0 && ((ready >> j) & 1u)) {
-      bkt[j] = bucket_of(bk, order_key(a, rr[j], dl));
+      bkt[j] = bucket_of(bk, order_key(a, rr[j], dl, kofs));
       slot[j] = add_agent(bk.cnt + bkt[j], 1u);
     }
   }
@@ -1058,8 +1072,8 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
     if (bk.nb == 0) a.stg_ready[pos] = uint8_t((ready >> j) & 1u);
     if (a.rem_out) a.rem_out[vv[j]] = rr[j];
     if ((ready >> j) & 1u)
-      store_ready(a, bkt[j], slot[j], order_key(a, rr[j], dl), dl - rr[j], pos, route[j], cost[j],
-                  acc);
+      store_ready(a, bkt[j], slot[j], order_key(a, rr[j], dl, kofs), kofs, dl - rr[j], pos, route[j],
+                  cost[j], acc);
   }
   wave_order();
 }
@@ -1110,9 +1124,9 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
     if (n <= 0) continue;
     const int64_t dl = a.p.deadline[w] - a.p.now;
     if (!a.force_global && n <= lds_cap)
-      sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, lds_cap, b, n, dl, acc);
+      sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, lds_cap, b, n, dl, prio_offset(a, w), acc);
     else
-      sweep_hbm<T, false>(a, L, it, S, int(w), b, n, dl, acc);
+      sweep_hbm<T, false>(a, L, it, S, int(w), b, n, dl, prio_offset(a, w), acc);
   }
 
   // fold the block's slack range and ready count into the control block
@@ -1356,7 +1370,8 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap
       b0 = lo;
       n0 = hi - lo;
       if (ln == 0 && ((n0 < 0) | ((gw == 0) & (lo != 0)) | ((gw == a.p.W - 1) & (int64_t(hi) != a.p.N)) |
-                      (raw0 < a.p.now - NALAR_HORIZON_MAX) | (raw0 > a.p.now + NALAR_HORIZON_MAX)))
+                      (raw0 < a.p.now - NALAR_HORIZON_MAX) | (raw0 > a.p.now + NALAR_HORIZON_MAX) |
+                      (a.p.prio != nullptr && a.p.prio[gw] > NALAR_PRIORITY_MAX)))
         flag_sweep(ctrl, kStInval);
     }
     if (wave_itab) {
@@ -1402,7 +1417,8 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap
       const int64_t raw = a.p.deadline[w];
       dl = raw - a.p.now;
       if (kFused && ln == 0 &&
-          ((raw < a.p.now - NALAR_HORIZON_MAX) | (raw > a.p.now + NALAR_HORIZON_MAX)))
+          ((raw < a.p.now - NALAR_HORIZON_MAX) | (raw > a.p.now + NALAR_HORIZON_MAX) |
+           (a.p.prio != nullptr && a.p.prio[w] > NALAR_PRIORITY_MAX)))
         flag_sweep(ctrl, kStInval);
     }
     if (n <= 0) continue;
@@ -1410,7 +1426,7 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap
       big = true;
       continue;
     }
-    sweep_wave<NPTW, kFused>(a, L, it, Wv, w, b, n, dl, acc, st);
+    sweep_wave<NPTW, kFused>(a, L, it, Wv, w, b, n, dl, prio_offset(a, w), acc, st);
   }
   if (ln == 0) s_big[wv] = big ? 1 : 0;
   __syncthreads();
@@ -1425,7 +1441,8 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap
         int n;
         wf_bounds(a, w, b, n);
         if (n <= 0 || (n <= wcap && !a.force_global)) continue;
-        sweep_hbm<kWaveBlock, kFused>(a, L, it, S, int(w), b, n, a.p.deadline[w] - a.p.now, acc);
+        sweep_hbm<kWaveBlock, kFused>(a, L, it, S, int(w), b, n, a.p.deadline[w] - a.p.now,
+                                      prio_offset(a, w), acc);
       }
     }
   }

@@ -51,7 +51,7 @@ class NalarProblem(ctypes.Structure):
                 ("done", ctypes.c_void_p), ("loc", ctypes.c_void_p), ("dep_off", ctypes.c_void_p),
                 ("dep_idx", ctypes.c_void_p), ("deadline_us", ctypes.c_void_p),
                 ("inst_type", ctypes.c_void_p), ("inst_load_us", ctypes.c_void_p),
-                ("inst_speed_permille", ctypes.c_void_p)]
+                ("inst_speed_permille", ctypes.c_void_p), ("wf_priority", ctypes.c_void_p)]
 
 
 class NalarResult(ctypes.Structure):
@@ -212,10 +212,12 @@ class DeviceProblem:
     def n_nodes(self) -> int:
         return int(self.tensors["wf"].shape[0])
 
-    def c_struct(self, flags: Optional[int] = None, policy: int = 0) -> NalarProblem:
+    def c_struct(self, flags: Optional[int] = None, policy: int = 0, priority=None) -> NalarProblem:
         """The C struct of this problem.  ``flags`` replaces the default
         problem flags (the contiguity bit when the ids are workflow-contiguous);
-        ``policy`` (NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL bits) is ORed in."""
+        ``policy`` (NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL | NALAR_ROUTE_GREEDY
+        bits) is ORed in; ``priority`` is a uint8 device tensor of one level per
+        workflow, or None."""
         t = self.tensors
         ptr = lambda x: x.data_ptr() if x.numel() > 0 else None
         return NalarProblem(
@@ -227,7 +229,8 @@ class DeviceProblem:
             done=ptr(t["done"]), loc=ptr(t["loc"]), dep_off=ptr(t["dep_off"]),
             dep_idx=ptr(t["dep_idx"]), deadline_us=ptr(t["deadline_us"]),
             inst_type=ptr(t["inst_type"]), inst_load_us=ptr(t["inst_load_us"]),
-            inst_speed_permille=ptr(t["inst_speed_permille"]))
+            inst_speed_permille=ptr(t["inst_speed_permille"]),
+            wf_priority=None if priority is None else priority.data_ptr())
 
 
 @dataclass
@@ -290,9 +293,9 @@ class Policy:
             pass
 
     def run_pass(self, prob: DeviceProblem, out: DeviceResult, flags: Optional[int] = None,
-                 raw: Optional[NalarProblem] = None, policy: int = 0) -> int:
+                 raw: Optional[NalarProblem] = None, policy: int = 0, priority=None) -> int:
         """One synchronous pass; returns the C return code and fills out.n_ready."""
-        cp = raw if raw is not None else prob.c_struct(flags, policy)
+        cp = raw if raw is not None else prob.c_struct(flags, policy, priority)
         cr = out.c_struct()
         rc = nalar_policy_pass(self.handle, cp, cr)
         out.n_ready = int(cr.n_ready) if rc == NALAR_OK else 0

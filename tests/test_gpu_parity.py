@@ -51,10 +51,11 @@ def policy_tiled():
         yield p
 
 
-def gpu_run(pol, p, flags=None, policy=0):
+def gpu_run(pol, p, flags=None, policy=0, priority=None):
     dp = nalar.DeviceProblem.from_host(p)
     out = nalar.DeviceResult.alloc(dp.n_nodes)
-    rc = pol.run_pass(dp, out, flags=flags, policy=policy)
+    pr = None if priority is None else torch.from_numpy(np.ascontiguousarray(priority, np.uint8)).cuda()
+    rc = pol.run_pass(dp, out, flags=flags, policy=policy, priority=pr)
     torch.cuda.synchronize()
     R = out.n_ready
     N = dp.n_nodes
@@ -78,9 +79,10 @@ def assert_parity(g, o, label=""):
                                  f"gpu {got[bad[:5]]} oracle {ref[bad[:5]]}")
 
 
-def check(pol, p, label, flags=None, policy=0):
+def check(pol, p, label, flags=None, policy=0, priority=None):
     say(f"[gpu] {label}: N={p.n_nodes} E={p.n_edges} W={p.n_workflows} M={p.n_instances} policy={policy}")
-    assert_parity(gpu_run(pol, p, flags, policy), oracle.run(p, policy=policy), label)
+    assert_parity(gpu_run(pol, p, flags, policy, priority), oracle.run(p, policy=policy, priority=priority),
+                  label)
 
 
 # ---------------------------------------------------------------- small cases
@@ -261,6 +263,31 @@ def test_policy_switch_on_one_handle():
     with nalar.Policy() as pol:
         for bits in (0, 0, nalar.NALAR_ORDER_LPT, nalar.NALAR_ORDER_LPT, 0, nalar.NALAR_ROUTE_STATEFUL):
             check(pol, p, f"switch policy {bits}", policy=bits)
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 3])
+def test_priority_levels(policy, policy_tiled, policy_hbm, cfg):
+    """Per-workflow priority levels (set_priority) with and without LPT, on
+    every sort and sweep path, plus the level and key-range rules."""
+    p = wl.CONFIGS[cfg]()
+    rng = np.random.default_rng(20 + cfg)
+    for levels in (rng.integers(0, 16, p.n_workflows), rng.integers(0, 2, p.n_workflows),
+                   np.full(p.n_workflows, 15)):
+        pr = levels.astype(np.uint8)
+        check(policy, p, f"config{cfg} levels", priority=pr)
+        check(policy, p, f"config{cfg} levels lpt", policy=nalar.NALAR_ORDER_LPT, priority=pr)
+    if cfg == 0:
+        pr = rng.integers(0, 16, p.n_workflows).astype(np.uint8)
+        q = wl.relabel(p, np.random.default_rng(5).permutation(p.n_nodes))
+        check(policy_tiled, q, "relabelled levels", priority=pr)
+        check(policy_hbm, p, "hbm levels", priority=pr)
+        bad = pr.copy()
+        bad[7] = 16
+        check(policy, p, "level 16", priority=bad)
+        far = p.copy(deadline_us=p.deadline_us.copy())
+        far.deadline_us[0] = p.now_us + (1 << 60)
+        check(policy, far, "key beyond 2^58 with levels", priority=pr)
+        check(policy, far, "same without levels")
 
 
 def test_policy_unknown_bits_rejected(policy):

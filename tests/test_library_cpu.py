@@ -62,8 +62,9 @@ def test_struct_layouts_match_header():
 #include "nalar_policy.h"
 int main(void) {
   printf("%zu %zu %zu\n", sizeof(nalar_policy_config), sizeof(nalar_problem), sizeof(nalar_result));
-  printf("%zu %zu %zu %zu\n", offsetof(nalar_problem, flags), offsetof(nalar_problem, wf),
-         offsetof(nalar_problem, inst_speed_permille), offsetof(nalar_result, n_ready));
+  printf("%zu %zu %zu %zu %zu\n", offsetof(nalar_problem, flags), offsetof(nalar_problem, wf),
+         offsetof(nalar_problem, inst_speed_permille), offsetof(nalar_problem, wf_priority),
+         offsetof(nalar_result, n_ready));
   printf("%zu\n", offsetof(nalar_policy_config, reserve_workflows));
   return 0;
 }
@@ -78,7 +79,7 @@ int main(void) {
     got = list(map(int, out))
     P, C, R = nalar.NalarProblem, nalar.NalarPolicyConfig, nalar.NalarResult
     assert got == [ctypes.sizeof(C), ctypes.sizeof(P), ctypes.sizeof(R), P.flags.offset,
-                   P.wf.offset, P.inst_speed_permille.offset, R.n_ready.offset,
+                   P.wf.offset, P.inst_speed_permille.offset, P.wf_priority.offset, R.n_ready.offset,
                    C.reserve_workflows.offset]
 
 
