@@ -1030,7 +1030,7 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
   bool overflow = false;
   uint32_t fin = 0;
   int64_t rr[NPTW];
-  if (NPTW > 2 || ballot(heavy != 0) != 0)  // larger slices: one variant (registers)
+  if (ballot(heavy != 0) != 0)  // a future with many dependencies: the variant that pushes it
     rounds<NPTW, true>(a, L, W, b, n, own, heavy, ee, p01, p2, rr, fin, overflow);
   else
     rounds<NPTW, false>(a, L, W, b, n, own, heavy, ee, p01, p2, rr, fin, overflow);
