@@ -80,8 +80,8 @@ def pass_alg_bytes(N: int, E: int, R: int, W: int, M: int) -> float:
 # copy of known size (`python3 bench.py --copy-calibration`).  Valid only for
 # the kernel sources it was taken on: a different source digest reports null.
 TRAFFIC = {
-    ("paper-scale", "sweep"): {"src_sha256": "512931106841e2bfdde6beda4afdffaab6b6cada4d822cf52860c3f67b27dca9",
-                               "bytes_per_launch": 8414523},
+    ("paper-scale", "sweep"): {"src_sha256": "ddfcfb54dead285ac3357c427b48d938ae89fa39da8f1ca3c15ce284efcc1894",
+                               "bytes_per_launch": 7727960},
 }
 
 
