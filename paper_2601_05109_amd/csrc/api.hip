@@ -88,6 +88,7 @@ struct nalar_policy {
   // slack range and ready count of the last successful pass (bucket hint)
   bool hint_valid = false;
   int64_t hint_ready = 0, hint_min = 0, hint_max = 0;
+  uint32_t hint_levels = 0;      // priority levels of the previous pass (bit l: level l)
   int bucket_skip = 0;           // passes left before the bucketed sort is tried again
   int bucket_backoff = 1;
   int bucket_dense = 0;          // buckets doubled this many times after overflows
@@ -206,15 +207,23 @@ int ensure_capacity(nalar_policy* h, int64_t N, int64_t W, int64_t B) {
   return NALAR_OK;
 }
 
-// Buckets for this pass from the previous pass's ready count and slack range
-// (nb == 0: use the tiled sort).
-BucketArgs plan_buckets(const nalar_policy* h, int64_t N, bool levels) {
+// Buckets for this pass from the previous pass's ready count and key range
+// (nb == 0: use the tiled sort).  With priority levels the buckets form one
+// group per level between the lowest and the highest level seen, each spread
+// over the range of the key within its level; only the one-wave-per-workflow
+// sweep maps keys to level groups, so with the block sweep levels take the
+// tiled sort.
+BucketArgs plan_buckets(const nalar_policy* h, int64_t N, bool levels, bool wave_sweep) {
   BucketArgs bk{};
-  // priority levels put keys 2^59 apart: buckets over that range would put a
-  // whole level in one bucket, so those passes take the tiled sort
-  if (levels || (h->flags & NALAR_FORCE_TILED_SORT) || !h->hint_valid || h->bucket_skip > 0 || N == 0 ||
-      h->hint_ready > kBucketMaxReady)
+  if ((h->flags & NALAR_FORCE_TILED_SORT) || !h->hint_valid || h->bucket_skip > 0 || N == 0 ||
+      h->hint_ready > kBucketMaxReady || (levels && (h->hint_levels == 0 || !wave_sweep)))
     return bk;
+  int groups = 1, lvl_hi = 0;
+  if (levels) {
+    const int l0 = __builtin_ctz(h->hint_levels);
+    lvl_hi = 31 - __builtin_clz(h->hint_levels);
+    groups = lvl_hi - l0 + 1;
+  }
   // about two futures per bucket, four for large ready sets (fewer buckets to
   // scan and clear; the 64 slots of a bucket still leave ample headroom)
   // after an overflow (keys crowded into a few buckets, e.g. a long-tailed
@@ -223,13 +232,22 @@ BucketArgs plan_buckets(const nalar_policy* h, int64_t N, bool levels) {
   int64_t nb = kBucketMin;
   while (nb < kBucketMax && nb * per <= h->hint_ready) nb *= 2;
   for (int i = 0; i < h->bucket_dense && nb < kBucketMax; ++i) nb *= 2;
+  // per level group: a power of two, at least one small-kernel group of
+  // buckets, all groups together within kBucketMax
+  int64_t nbl = kBucketGroup;
+  while (nbl * groups < nb && nbl * 2 * groups <= kBucketMax) nbl *= 2;
   int lognb = 0;
-  while ((int64_t(1) << lognb) < nb) ++lognb;
+  while ((int64_t(1) << lognb) < nbl) ++lognb;
   const uint64_t range = uint64_t(h->hint_max) - uint64_t(h->hint_min);
   const int bits = range ? 64 - __builtin_clzll(range) : 0;
   bk.lo = h->hint_min;
   bk.shift = bits > lognb ? bits - lognb : 0;
-  bk.nb = int32_t(nb);
+  bk.nb = int32_t(nbl * groups);
+  if (levels) {
+    bk.lvl_hi = lvl_hi;
+    bk.ngroups = int16_t(groups);
+    bk.lshift = int16_t(lognb);
+  }
   return bk;
 }
 
@@ -380,7 +398,8 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   hipError_t e = hipSetDevice(h->device);
   if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
   const int64_t N = p->n_nodes, W = p->n_workflows, M = p->n_instances;
-  BucketArgs bk = plan_buckets(h, N, p->wf_priority != nullptr);
+  const SweepShape sh = plan_sweep(N, W, M, h->cus, h->lds_limit);
+  BucketArgs bk = plan_buckets(h, N, p->wf_priority != nullptr, sh.wave_path != 0);
   if (h->bucket_skip > 0) --h->bucket_skip;
   rc = ensure_capacity(h, N, W, bk.nb);
   if (rc != NALAR_OK) return rc;
@@ -425,7 +444,6 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   if (need_reset || need_clear)
     NALAR_LAUNCH("reset", launch_reset(s, need_reset ? ctrl : nullptr, bk.cnt, need_clear ? bk.nb : 0));
   if (bk.nb > 0) h->bcnt_clean[cur] = false;
-  const SweepShape sh = plan_sweep(N, W, M, h->cus, h->lds_limit);
   const bool fused = N > 0 && sweep_can_fuse(sh, M, contiguous);
   if (!fused)
     NALAR_LAUNCH("nodes", launch_nodes(s, pd, ctrl, A.ctrl[nxt], A.itab, A.wf_off, contiguous ? 1 : 0));
@@ -503,6 +521,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   sa.tiles_cap = tiles_of(A.capN);
   sa.bagg = A.bagg;
   sa.epoch = epoch;
+  sa.levels = p->wf_priority ? 1u : 0u;
   sa.order = r->order;
   sa.slack = r->slack_us;
   sa.route = r->route;
@@ -585,6 +604,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   h->hint_ready = r->n_ready;
   h->hint_min = r->n_ready ? __atomic_load_n(&h->host->slack_min, __ATOMIC_ACQUIRE) : 0;
   h->hint_max = r->n_ready ? __atomic_load_n(&h->host->slack_max, __ATOMIC_ACQUIRE) : 0;
+  h->hint_levels = r->n_ready && p->wf_priority ? __atomic_load_n(&h->host->level_mask, __ATOMIC_ACQUIRE) : 0u;
   return NALAR_OK;
 }
 

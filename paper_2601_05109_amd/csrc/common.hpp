@@ -42,7 +42,8 @@ __host__ __device__ inline uint64_t lb_pack(uint32_t epoch, uint64_t flag, uint6
 // passes: the last kernel of a pass resets the block the next pass will use.
 // The sweep folds each workgroup's slack range and ready count into one of
 // kParts slots (spreading the atomics over many addresses); the sort reduces
-// the slots with one wave.
+// the slots with one wave.  With priority levels the slots hold the range of
+// the key within its level (key + level * 2^59) and a mask of the levels seen.
 constexpr int kParts = 64;
 
 struct Ctrl {
@@ -50,14 +51,18 @@ struct Ctrl {
   uint32_t status_sweep;         // problems found by the sweep (cycles, ranges)
   uint32_t sort_npass;           // digit passes the slack sort runs
   uint32_t bucket_overflow;      // a bucket of the bucketed sort overflowed
-  uint32_t pad[2];
+  uint32_t level_mask;           // priority levels seen (the next pass's bucket hint)
+  uint32_t pad;
   int64_t n_ready;
-  int64_t slack_min;
+  int64_t slack_min;             // key range of the ready futures (all keys lie inside)
   int64_t slack_max;
+  int64_t hint_min;              // the range the host plans the next buckets from:
+  int64_t hint_max;              //   the key range, or with levels the in-level range
   uint32_t tile_ticket[16];      // per radix pass: [0,8) slack sort, [8,12) grouping
   int64_t part_min[kParts];
   int64_t part_max[kParts];
   int64_t part_cnt[kParts];
+  uint32_t part_lvl[kParts];
   uint32_t ghist_slack[kMaxSortPasses * kRadixBuckets];
   uint32_t ghist_group[kMaxGroupPasses * kRadixBuckets];
 };
@@ -100,10 +105,10 @@ struct HostStatus {
   uint32_t status;
   uint32_t key_bits;   // significant bits of the slack range
   int64_t n_ready;
-  int64_t slack_min;   // range of this pass (the next pass's bucket hint)
-  int64_t slack_max;
+  int64_t slack_min;   // range of this pass (the next pass's bucket hint; with
+  int64_t slack_max;   //   priority levels the range of the key within its level)
   uint32_t aux_status; // status bits of the load-aware routing kernel
-  uint32_t pad_;
+  uint32_t level_mask; // priority levels of this pass (bit l: level l; with levels only)
 };
 
 // Resets a control block for a later pass (run by one workgroup).
@@ -123,6 +128,7 @@ __device__ inline void reset_ctrl(Ctrl* c) {
     c->part_min[i] = INT64_MAX;
     c->part_max[i] = INT64_MIN;
     c->part_cnt[i] = 0;
+    c->part_lvl[i] = 0;
   }
   for (int i = tid; i < kMaxSortPasses * kRadixBuckets; i += blockDim.x) c->ghist_slack[i] = 0;
   for (int i = tid; i < kMaxGroupPasses * kRadixBuckets; i += blockDim.x) c->ghist_group[i] = 0;
@@ -145,6 +151,7 @@ __device__ inline void reset_ctrl_spread(Ctrl* c, int64_t gi, int64_t gstride) {
     c->part_min[i] = INT64_MAX;
     c->part_max[i] = INT64_MIN;
     c->part_cnt[i] = 0;
+    c->part_lvl[i] = 0;
   }
   for (int64_t i = gi; i < kMaxSortPasses * kRadixBuckets; i += gstride) c->ghist_slack[i] = 0;
   for (int64_t i = gi; i < kMaxGroupPasses * kRadixBuckets; i += gstride) c->ghist_group[i] = 0;
@@ -224,6 +231,10 @@ __device__ inline int64_t wave_min_i64(int64_t x) {
 
 __device__ inline int64_t wave_sum_i64(int64_t x) {
   return wave_reduce_i64(x, [](int64_t u, int64_t v) { return u + v; });
+}
+
+__device__ inline uint32_t wave_or_u32(uint32_t x) {
+  return uint32_t(wave_reduce_i64(int64_t(x), [](int64_t u, int64_t v) { return u | v; }));
 }
 
 // Inclusive scan over the wave (all 64 lanes active).

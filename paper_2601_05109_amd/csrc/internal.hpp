@@ -50,6 +50,7 @@ struct SortArgs {
   int64_t tiles_cap;
   uint64_t* bagg;               // [kBucketLbGroups] futures per group of buckets
   uint32_t epoch;
+  uint32_t levels;              // nonzero: the keys carry priority levels
   int32_t* order;
   int64_t* slack;
   int32_t* route;
@@ -70,13 +71,21 @@ struct GroupArgs {
 };
 
 // Buckets of the bucketed slack sort (nb == 0: not used this pass).  Bucket of
-// a slack s: min((s - lo) >> shift, nb - 1), 0 below lo.
+// a key k: min((k - lo) >> shift, nb - 1), 0 below lo.  With priority levels
+// (ngroups > 0) the buckets form ngroups groups of 2^lshift, one per level from
+// lvl_hi down; a key of level l falls into group lvl_hi - l by its in-level
+// value k + l * 2^59 (same mapping, 2^lshift buckets); a level above lvl_hi
+// takes bucket 0 and one below the last group bucket nb - 1, so buckets still
+// ascend with the key.
 struct BucketArgs {
   int64_t lo;
   int32_t shift;
   int32_t nb;
   uint32_t* cnt;                // [nb] futures dropped into each bucket (16-byte aligned)
   BucketSlot* slot;             // [nb * kBucketCap]
+  int32_t lvl_hi;
+  int16_t ngroups;
+  int16_t lshift;
 };
 
 struct SweepArgs {

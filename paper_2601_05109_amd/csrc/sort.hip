@@ -247,14 +247,24 @@ __global__ __launch_bounds__(kSortThreads) void k_reset(Ctrl* c, uint32_t* clear
 }
 
 // Slack range, ready count and pass count from the sweep's slots (one wave).
-// s_range = {min slack, ready count, digit passes, significant key bits,
-// max slack}.
-__device__ void settle_range(Ctrl* ctrl, int64_t* s_range, bool write) {
+// s_range = {min key, ready count, digit passes, significant key bits, max
+// key, hint min, hint max, level mask}.  Without levels the hint is the key
+// range.  With levels the slots hold the in-level range [lo, hi] and the
+// levels seen [l0, l1]: every key lies in [lo - l1 * 2^59, hi - l0 * 2^59],
+// the range the radix passes cover, and the hint is [lo, hi] with the mask.
+__device__ void settle_range(Ctrl* ctrl, int64_t* s_range, bool write, bool levels) {
   if (threadIdx.x < kWave) {
-    const int64_t mn = wave_min_i64(ctrl->part_min[threadIdx.x]);
-    const int64_t mx = wave_max_i64(ctrl->part_max[threadIdx.x]);
+    int64_t mn = wave_min_i64(ctrl->part_min[threadIdx.x]);
+    int64_t mx = wave_max_i64(ctrl->part_max[threadIdx.x]);
     const int64_t ct = wave_sum_i64(ctrl->part_cnt[threadIdx.x]);
+    const uint32_t lm = levels ? wave_or_u32(ctrl->part_lvl[threadIdx.x]) : 0u;
     if (threadIdx.x == 0) {
+      const int64_t hmin = mn, hmax = mx;
+      if (levels && ct > 0 && lm != 0) {
+        const int l0 = __builtin_ctz(lm), l1 = 31 - __builtin_clz(lm);
+        mn -= int64_t(l1) << kPrioShift;
+        mx -= int64_t(l0) << kPrioShift;
+      }
       int npass = 0, nbits = 0;
       if (ct > 0) {
         const uint64_t range = uint64_t(mx - mn);
@@ -267,10 +277,16 @@ __device__ void settle_range(Ctrl* ctrl, int64_t* s_range, bool write) {
       s_range[2] = npass;
       s_range[3] = nbits;
       s_range[4] = mx;
+      s_range[5] = hmin;
+      s_range[6] = hmax;
+      s_range[7] = int64_t(lm);
       if (write) {
         ctrl->n_ready = ct;
         ctrl->slack_min = mn;
         ctrl->slack_max = mx;
+        ctrl->hint_min = hmin;
+        ctrl->hint_max = hmax;
+        ctrl->level_mask = lm;
         ctrl->sort_npass = uint32_t(npass);
       }
     }
@@ -278,14 +294,21 @@ __device__ void settle_range(Ctrl* ctrl, int64_t* s_range, bool write) {
   __syncthreads();
 }
 
-// Status, ready count and slack range for the host (one thread).
+// Status, ready count, the next pass's bucket hint (key range, levels) and the
+// significant key bits for the host (one thread).
 __device__ inline void publish_status(HostStatus* host, uint32_t status, int64_t n_ready,
-                                      int key_bits, int64_t smin, int64_t smax) {
+                                      int key_bits, int64_t hmin, int64_t hmax, uint32_t lmask) {
   __hip_atomic_store(&host->n_ready, n_ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __hip_atomic_store(&host->key_bits, uint32_t(key_bits), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-  __hip_atomic_store(&host->slack_min, smin, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-  __hip_atomic_store(&host->slack_max, smax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&host->slack_min, hmin, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&host->slack_max, hmax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&host->level_mask, lmask, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __hip_atomic_store(&host->status, status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+__device__ inline void publish_range(HostStatus* host, uint32_t status, const int64_t* s_range) {
+  publish_status(host, status, s_range[1], int(s_range[3]), s_range[5], s_range[6],
+                 uint32_t(s_range[7]));
 }
 
 // ------------------------------------------------------------ bucketed sort
@@ -299,7 +322,7 @@ constexpr int kGroupSlots = kBucketGroup * kBucketCap;
 // its bucket-mates by (slack, position).  Positions ascend in (workflow, id),
 // so that is the rank by (slack, workflow, id).
 __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, BucketArgs bk) {
-  __shared__ int64_t s_range[5];
+  __shared__ int64_t s_range[8];
   __shared__ uint32_t s_off[kBucketGroup + 1];
   __shared__ uint32_t s_red[kBucketThreads / kWave];
   __shared__ int64_t s_slack[kGroupSlots];
@@ -312,17 +335,15 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, Buck
   Ctrl* ctrl = a.ctrl;
   const uint32_t status = ctrl->status | ctrl->status_sweep;
   if (status) {
-    if (g == 0 && tid == 0) publish_status(a.host, status, 0, 0, 0, 0);
+    if (g == 0 && tid == 0) publish_status(a.host, status, 0, 0, 0, 0, 0u);
     return;
   }
-  settle_range(ctrl, s_range, g == 0);
-  const int64_t R = s_range[1];
+  settle_range(ctrl, s_range, g == 0, a.levels != 0);
   if (ctrl->bucket_overflow != 0) {  // written by the sweep, an earlier kernel
-    if (g == 0 && tid == 0)
-      publish_status(a.host, kStatusTiled, R, int(s_range[3]), s_range[0], s_range[4]);
+    if (g == 0 && tid == 0) publish_range(a.host, kStatusTiled, s_range);
     return;
   }
-  if (g == 0 && tid == 0) publish_status(a.host, 0, R, int(s_range[3]), s_range[0], s_range[4]);
+  if (g == 0 && tid == 0) publish_range(a.host, 0, s_range);
 
   // futures in earlier groups: the counts of buckets [0, 16 g), four at a time
   uint32_t part = 0;
@@ -403,7 +424,7 @@ constexpr int kLbStage = 2048;  // futures of a bucket group staged in LDS at on
 static_assert(kLbStage % kBucketLbGroup == 0, "whole rows of the workgroup");
 
 __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, BucketArgs bk) {
-  __shared__ int64_t s_range[5];
+  __shared__ int64_t s_range[8];
   __shared__ uint32_t s_off[kBucketLbGroup + 1];
   __shared__ uint32_t s_red[kBucketLbGroup / kWave];
   __shared__ int64_t s_base[kBucketLbGroup / kWave];
@@ -416,17 +437,15 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
   Ctrl* ctrl = a.ctrl;
   const uint32_t status = ctrl->status | ctrl->status_sweep;
   if (status) {
-    if (g == 0 && tid == 0) publish_status(a.host, status, 0, 0, 0, 0);
+    if (g == 0 && tid == 0) publish_status(a.host, status, 0, 0, 0, 0, 0u);
     return;
   }
-  settle_range(ctrl, s_range, g == 0);
-  const int64_t R = s_range[1];
+  settle_range(ctrl, s_range, g == 0, a.levels != 0);
   if (ctrl->bucket_overflow != 0) {  // written by the sweep, an earlier kernel
-    if (g == 0 && tid == 0)
-      publish_status(a.host, kStatusTiled, R, int(s_range[3]), s_range[0], s_range[4]);
+    if (g == 0 && tid == 0) publish_range(a.host, kStatusTiled, s_range);
     return;
   }
-  if (g == 0 && tid == 0) publish_status(a.host, 0, R, int(s_range[3]), s_range[0], s_range[4]);
+  if (g == 0 && tid == 0) publish_range(a.host, 0, s_range);
 
   // futures in earlier groups
   int64_t part = 0;
@@ -517,17 +536,17 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
 
 __global__ __launch_bounds__(kSortThreads) void k_slack_hist(SortArgs a) {
   __shared__ uint32_t H[kMaxSortPasses][kRadixBuckets];
-  __shared__ int64_t s_range[5];
+  __shared__ int64_t s_range[8];
   Ctrl* ctrl = a.ctrl;
   const uint32_t status = ctrl->status | ctrl->status_sweep;
   if (status) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) publish_status(a.host, status, 0, 0, 0, 0);
+    if (blockIdx.x == 0 && threadIdx.x == 0) publish_status(a.host, status, 0, 0, 0, 0, 0u);
     return;
   }
-  settle_range(ctrl, s_range, blockIdx.x == 0);
+  settle_range(ctrl, s_range, blockIdx.x == 0, a.levels != 0);
   const int npass = int(s_range[2]);
   if (npass == 0) {  // nothing ready: no pass runs, so report here
-    if (blockIdx.x == 0 && threadIdx.x == 0) publish_status(a.host, 0, 0, 0, 0, 0);
+    if (blockIdx.x == 0 && threadIdx.x == 0) publish_status(a.host, 0, 0, 0, 0, 0, 0u);
     return;
   }
   const FirstSource f{kSrcStaged, a.stg_slack, a.stg_ready, nullptr, a.span, s_range[0]};
@@ -563,8 +582,9 @@ __global__ __launch_bounds__(kSortThreads) void k_slack_pass(SortArgs a, int pas
   if (tile == 0 && threadIdx.x == 0) {
     const int64_t smax = ctrl->slack_max;
     const int nbits = 64 - __builtin_clzll(uint64_t(smax - smin) | 1);
-    if (last) publish_status(a.host, 0, R, nbits, smin, smax);
-    else if (pass == kSortLaunched - 1) publish_status(a.host, kStatusContinue, R, nbits, smin, smax);
+    const uint32_t st = last ? 0u : kStatusContinue;
+    if (last || pass == kSortLaunched - 1)
+      publish_status(a.host, st, R, nbits, ctrl->hint_min, ctrl->hint_max, ctrl->level_mask);
   }
 }
 

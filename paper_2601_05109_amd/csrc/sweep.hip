@@ -207,12 +207,27 @@ struct Acc {
   int64_t tready = 0;
 };
 
-// Bucket of a slack under this pass's bucket boundaries, and a slot in it
-// (one returning atomic; claim early so that its latency overlaps other work).
-__device__ inline uint32_t bucket_of(const BucketArgs& bk, int64_t slack) {
-  const uint64_t d = slack > bk.lo ? uint64_t(slack) - uint64_t(bk.lo) : 0;
+// Bucket of a key under this pass's bucket boundaries (kofs: the key offset of
+// its priority level), and a slot in it (one returning atomic; claim early so
+// that its latency overlaps other work).  Every result lies in [0, nb).
+// kLevels: the mapping may have level groups (the block kernel takes none,
+// which keeps it within its registers; the host then plans no buckets).
+template <bool kLevels>
+__device__ inline uint32_t bucket_of(const BucketArgs& bk, int64_t key, int64_t kofs) {
+  // the workflow's part (the same on every lane): its level's group of
+  // buckets [base, base + last] and the lower bound shifted by the key offset
+  int64_t lo = bk.lo;
+  uint32_t base = 0, last = uint32_t(bk.nb - 1);
+  if (kLevels && bk.ngroups > 0) {
+    const int32_t g = bk.lvl_hi - int32_t(uint32_t(uint64_t(-kofs) >> kPrioShift) & 31u);
+    const bool in = g >= 0 && g < bk.ngroups;
+    base = g < 0 ? 0u : (in ? uint32_t(g) << bk.lshift : last);
+    last = in ? (1u << bk.lshift) - 1u : 0u;
+    lo = int64_t(uint64_t(lo) + uint64_t(kofs));
+  }
+  const uint64_t d = key > lo ? uint64_t(key) - uint64_t(lo) : 0;
   const uint64_t q = d >> bk.shift;
-  return q < uint64_t(bk.nb) ? uint32_t(q) : uint32_t(bk.nb - 1);
+  return base + (q < uint64_t(last) ? uint32_t(q) : last);
 }
 
 __device__ inline void bucket_put(const SweepArgs& a, uint32_t bkt, uint32_t slot, int64_t key,
@@ -236,9 +251,15 @@ __device__ inline int64_t order_key(const SweepArgs& a, int64_t rem, int64_t dl,
   return ((a.p.policy & NALAR_ORDER_LPT) ? -rem : dl - rem) + kofs;
 }
 
-// The key offset of workflow w's priority level (0 without levels).
+// The key offset of workflow w's priority level (0 without levels); w is the
+// same on every lane, so the level goes to a scalar register.
 __device__ inline int64_t prio_offset(const SweepArgs& a, int64_t w) {
-  return a.p.prio ? -(int64_t(a.p.prio[w]) << kPrioShift) : 0;
+  return a.p.prio ? -(int64_t(__builtin_amdgcn_readfirstlane(int(a.p.prio[w]))) << kPrioShift) : 0;
+}
+
+// The mask bit of the level a key offset stands for.
+__device__ inline uint32_t level_bit(int64_t kofs) {
+  return 1u << (uint32_t(uint64_t(-kofs) >> kPrioShift) & 31u);
 }
 
 // Stores of one ready future: its bucket slot (bucketed sort) or its staged
@@ -247,10 +268,8 @@ __device__ inline int64_t prio_offset(const SweepArgs& a, int64_t w) {
 __device__ inline void store_ready(const SweepArgs& a, uint32_t bkt, uint32_t slot, int64_t key,
                                    int64_t kofs, int64_t slack, int64_t pos, int32_t route, int64_t cost,
                                    Acc& acc) {
-  if (a.p.prio) {
-    const int64_t k0 = key - kofs;
-    if (k0 <= -kPrioKeyBound || k0 >= kPrioKeyBound) flag_sweep(a.ctrl, kStRange);
-  }
+  const int64_t kr = a.p.prio ? key - kofs : key;  // the key within its level
+  if (a.p.prio && (kr <= -kPrioKeyBound || kr >= kPrioKeyBound)) flag_sweep(a.ctrl, kStRange);
   if (a.bk.nb > 0) {
     bucket_put(a, bkt, slot, key, pos, route, cost);
   } else {
@@ -259,11 +278,12 @@ __device__ inline void store_ready(const SweepArgs& a, uint32_t bkt, uint32_t sl
     a.stg_cost[pos] = cost;
   }
   if ((a.p.policy & NALAR_ORDER_LPT) || a.p.prio) a.stg_oslack[pos] = slack;
-  acc.tmin = key < acc.tmin ? key : acc.tmin;
-  acc.tmax = key > acc.tmax ? key : acc.tmax;
+  acc.tmin = kr < acc.tmin ? kr : acc.tmin;
+  acc.tmax = kr > acc.tmax ? kr : acc.tmax;
   acc.tready += 1;
 }
 
+template <bool kLevels>
 __device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_t pos, int32_t type,
                                    int32_t loc, int64_t rem, int64_t est, int64_t dl, int64_t kofs,
                                    Acc& acc) {
@@ -271,7 +291,7 @@ __device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_
   const BucketArgs& bk = a.bk;
   uint32_t bkt = 0, slot = 0;
   if (bk.nb > 0) {
-    bkt = bucket_of(bk, key);
+    bkt = bucket_of<kLevels>(bk, key, kofs);
     slot = add_agent(bk.cnt + bkt, 1u);
   }
   int32_t route;
@@ -482,7 +502,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
     bkt[j] = 0;
     slot[j] = 0;
     if (bk.nb > 0 && ((ready >> j) & 1u)) {
-      bkt[j] = bucket_of(bk, order_key(a, mx[j * T + tid], dl, kofs));
+      bkt[j] = bucket_of<false>(bk, order_key(a, mx[j * T + tid], dl, kofs), kofs);
       slot[j] = add_agent(bk.cnt + bkt[j], 1u);
     }
   }
@@ -515,7 +535,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
 
 // ------------------------------------------------------------ HBM workflow
 
-template <int T, bool kFused>
+template <int T, bool kFused, bool kLevels>
 __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
                           int w, int64_t b, int n, int64_t dl, int64_t kofs, Acc& acc) {
   const int tid = threadIdx.x;
@@ -693,7 +713,7 @@ __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, con
   for (int k = tid; k < n; k += T) {
     if (dn[k] == 0 && nr[k] == 0) {
       const int32_t v = node_at(L, b + k);
-      write_ready(a, it, b + k, a.p.type[v], a.p.loc[v], ld_wg(&mx[k]), a.p.est[v], dl, kofs, acc);
+      write_ready<kLevels>(a, it, b + k, a.p.type[v], a.p.loc[v], ld_wg(&mx[k]), a.p.est[v], dl, kofs, acc);
     }
   }
   __syncthreads();
@@ -1048,7 +1068,7 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
     bkt[j] = 0;
     slot[j] = 0;
     if (bk.nb > 0 && ((ready >> j) & 1u)) {
-      bkt[j] = bucket_of(bk, order_key(a, rr[j], dl, kofs));
+      bkt[j] = bucket_of<true>(bk, order_key(a, rr[j], dl, kofs), kofs);
       slot[j] = add_agent(bk.cnt + bkt[j], 1u);
     }
   }
@@ -1118,15 +1138,18 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
 
   const Layout L{a.node_of_pos, a.pos_of_node, a.p.N};
   Acc acc;
+  uint32_t lmask = 0;  // priority levels of the block's workflows
   for (int64_t w = blockIdx.x; w < a.p.W; w += gridDim.x) {
     const int64_t b = a.wf_off[w];
     const int n = a.wf_off[w + 1] - int32_t(b);
     if (n <= 0) continue;
     const int64_t dl = a.p.deadline[w] - a.p.now;
+    const int64_t kofs = prio_offset(a, w);
+    lmask |= level_bit(kofs);
     if (!a.force_global && n <= lds_cap)
-      sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, lds_cap, b, n, dl, prio_offset(a, w), acc);
+      sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, lds_cap, b, n, dl, kofs, acc);
     else
-      sweep_hbm<T, false>(a, L, it, S, int(w), b, n, dl, prio_offset(a, w), acc);
+      sweep_hbm<T, false, false>(a, L, it, S, int(w), b, n, dl, kofs, acc);
   }
 
   // fold the block's slack range and ready count into the control block
@@ -1148,6 +1171,8 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
       __hip_atomic_fetch_min(&ctrl->part_min[slot], a0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_fetch_max(&ctrl->part_max[slot], a1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       add_agent(&ctrl->part_cnt[slot], a2);
+      if (a.p.prio)
+        __hip_atomic_fetch_or(&ctrl->part_lvl[slot], lmask, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -1295,7 +1320,7 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap
   Ctrl* ctrl = a.ctrl;
   const int M = int(a.p.M);
   const int tid = threadIdx.x;
-  const int wv = tid / kWave;
+  const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);  // wave-uniform: scalar registers
   const int ln = lane_id();
   const bool wave_itab = kFused && M <= kWave;  // sorted by each wave itself, no barrier
   const bool per_wave = (!kFused && M <= kWaveItabMax) || wave_itab;
@@ -1408,6 +1433,7 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap
   const Layout L{a.node_of_pos, a.pos_of_node, a.p.N};
   Acc acc;
   bool big = false;
+  uint32_t lmask = 0;  // priority levels of the wave's workflows
   for (int64_t w = gw; w < a.p.W; w += nwaves) {
     int64_t b = b0;
     int n = n0;
@@ -1422,11 +1448,13 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap
         flag_sweep(ctrl, kStInval);
     }
     if (n <= 0) continue;
+    const int64_t kofs = prio_offset(a, w);
+    lmask |= level_bit(kofs);
     if (n > wcap || a.force_global) {
       big = true;
       continue;
     }
-    sweep_wave<NPTW, kFused>(a, L, it, Wv, w, b, n, dl, prio_offset(a, w), acc, st);
+    sweep_wave<NPTW, kFused>(a, L, it, Wv, w, b, n, dl, kofs, acc, st);
   }
   if (ln == 0) s_big[wv] = big ? 1 : 0;
   __syncthreads();
@@ -1441,8 +1469,9 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap
         int n;
         wf_bounds(a, w, b, n);
         if (n <= 0 || (n <= wcap && !a.force_global)) continue;
-        sweep_hbm<kWaveBlock, kFused>(a, L, it, S, int(w), b, n, a.p.deadline[w] - a.p.now,
-                                      prio_offset(a, w), acc);
+        const int64_t kofs = prio_offset(a, w);
+        lmask |= level_bit(kofs);
+        sweep_hbm<kWaveBlock, kFused, true>(a, L, it, S, int(w), b, n, a.p.deadline[w] - a.p.now, kofs, acc);
       }
     }
   }
@@ -1455,6 +1484,8 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap
     __hip_atomic_fetch_min(&ctrl->part_min[slot], mn, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_fetch_max(&ctrl->part_max[slot], mxv, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     add_agent(&ctrl->part_cnt[slot], rd);
+    if (a.p.prio)
+      __hip_atomic_fetch_or(&ctrl->part_lvl[slot], lmask, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   clear_for_next_pass<kFused>(a);
 }

@@ -290,6 +290,32 @@ def test_priority_levels(policy, policy_tiled, policy_hbm, cfg):
         check(policy, far, "same without levels")
 
 
+def test_priority_levels_bucketed():
+    """Repeated passes with priority levels on one handle: after the first pass
+    the bucketed sort maps each level to its own group of buckets.  Level sets
+    then move above and below the planned groups (keys clamped to the end
+    buckets, a few of them or whole levels that overflow and fall back), with
+    and without LPT; every pass must match the oracle."""
+    p = wl.paper_scale()
+    rng = np.random.default_rng(77)
+    base = rng.integers(2, 6, p.n_workflows).astype(np.uint8)
+    mixed = base.copy()
+    mixed[[3, 500, 2000]] = 0
+    mixed[[7, 1000]] = 1
+    mixed[[11, 3000, 4095]] = 12
+    seq = [(base, 0), (base, 0), (base, 0), (mixed, 0), (base + 6, 0), (base, 0),
+           (base, nalar.NALAR_ORDER_LPT), (base, nalar.NALAR_ORDER_LPT), (mixed, nalar.NALAR_ORDER_LPT)]
+    with nalar.Policy() as pol:
+        pol.set_timing(True)
+        bucketed = 0
+        for i, (pr, bits) in enumerate(seq):
+            check(pol, p, f"levels pass {i} policy {bits}", policy=bits, priority=pr)
+            names = [n for n, _ in pol.timing()]
+            if "sort_bucket" in names and "sort_pass0" not in names:
+                bucketed += 1
+        assert bucketed >= 3, f"only {bucketed} level passes took the bucketed sort"
+
+
 def test_policy_unknown_bits_rejected(policy):
     dp = nalar.DeviceProblem.from_host(wl.tiny())
     out = nalar.DeviceResult.alloc(dp.n_nodes)
