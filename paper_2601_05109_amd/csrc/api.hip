@@ -93,6 +93,8 @@ struct nalar_policy {
   int bucket_backoff = 1;
   int bucket_dense = 0;          // buckets doubled this many times after overflows
   int bucket_calm = 0;           // bucketed passes without overflow since the last change
+  int bucket_relax = 64;         // calm passes before fewer buckets are tried again
+  bool bucket_relaxed = false;   // the last pass tried fewer buckets
   std::string err;
   Arena ar;
   HostStatus* host = nullptr;    // pinned, written by the sort kernel
@@ -541,6 +543,9 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
       __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);
       tiled = true;
       h->bucket_calm = 0;
+      // fewer buckets overflowed at once: wait twice as long before trying again
+      if (h->bucket_relaxed && h->bucket_relax < 4096) h->bucket_relax *= 2;
+      h->bucket_relaxed = false;
       if (h->bucket_dense < 3) {  // retry at once with more buckets
         ++h->bucket_dense;
       } else {                    // then back off
@@ -552,9 +557,11 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
       NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
     } else {
       h->bucket_backoff = 1;
-      if (h->bucket_dense > 0 && ++h->bucket_calm >= 64) {  // try fewer buckets again
+      h->bucket_relaxed = false;
+      if (h->bucket_dense > 0 && ++h->bucket_calm >= h->bucket_relax) {  // try fewer buckets again
         --h->bucket_dense;
         h->bucket_calm = 0;
+        h->bucket_relaxed = true;
       }
     }
   }

@@ -246,18 +246,38 @@ __global__ __launch_bounds__(kSortThreads) void k_reset(Ctrl* c, uint32_t* clear
     clear[i] = 0;
 }
 
-// Slack range, ready count and pass count from the sweep's slots (one wave).
-// s_range = {min key, ready count, digit passes, significant key bits, max
-// key, hint min, hint max, level mask}.  Without levels the hint is the key
-// range.  With levels the slots hold the in-level range [lo, hi] and the
-// levels seen [l0, l1]: every key lies in [lo - l1 * 2^59, hi - l0 * 2^59],
-// the range the radix passes cover, and the hint is [lo, hi] with the mask.
-__device__ void settle_range(Ctrl* ctrl, int64_t* s_range, bool write, bool levels) {
+// The sweep's per-slot range, count and level words as one wave holds them
+// (lane l: slot l; other threads hold the identities), loaded ahead of use.
+struct RangeLanes {
+  int64_t mn = INT64_MAX, mx = INT64_MIN, ct = 0;
+  uint32_t lm = 0;
+};
+
+__device__ inline RangeLanes load_range_lanes(const Ctrl* ctrl, bool levels) {
+  RangeLanes r;
   if (threadIdx.x < kWave) {
-    int64_t mn = wave_min_i64(ctrl->part_min[threadIdx.x]);
-    int64_t mx = wave_max_i64(ctrl->part_max[threadIdx.x]);
-    const int64_t ct = wave_sum_i64(ctrl->part_cnt[threadIdx.x]);
-    const uint32_t lm = levels ? wave_or_u32(ctrl->part_lvl[threadIdx.x]) : 0u;
+    r.mn = ctrl->part_min[threadIdx.x];
+    r.mx = ctrl->part_max[threadIdx.x];
+    r.ct = ctrl->part_cnt[threadIdx.x];
+    if (levels) r.lm = ctrl->part_lvl[threadIdx.x];
+  }
+  return r;
+}
+
+// Slack range, ready count and pass count from the sweep's slots (one wave;
+// every thread of the workgroup calls it).  s_range = {min key, ready count,
+// digit passes, significant key bits, max key, hint min, hint max, level
+// mask}.  Without levels the hint is the key range.  With levels the slots
+// hold the in-level range [lo, hi] and the levels seen [l0, l1]: every key
+// lies in [lo - l1 * 2^59, hi - l0 * 2^59], the range the radix passes cover,
+// and the hint is [lo, hi] with the mask.
+__device__ void settle_range(const RangeLanes& rl, Ctrl* ctrl, int64_t* s_range, bool write,
+                             bool levels) {
+  if (threadIdx.x < kWave) {
+    int64_t mn = wave_min_i64(rl.mn);
+    int64_t mx = wave_max_i64(rl.mx);
+    const int64_t ct = wave_sum_i64(rl.ct);
+    const uint32_t lm = levels ? wave_or_u32(rl.lm) : 0u;
     if (threadIdx.x == 0) {
       const int64_t hmin = mn, hmax = mx;
       if (levels && ct > 0 && lm != 0) {
@@ -292,6 +312,10 @@ __device__ void settle_range(Ctrl* ctrl, int64_t* s_range, bool write, bool leve
     }
   }
   __syncthreads();
+}
+
+__device__ void settle_range(Ctrl* ctrl, int64_t* s_range, bool write, bool levels) {
+  settle_range(load_range_lanes(ctrl, levels), ctrl, s_range, write, levels);
 }
 
 // Status, ready count, the next pass's bucket hint (key range, levels) and the
@@ -333,29 +357,37 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, Buck
   const int tid = threadIdx.x;
   const int g = blockIdx.x;
   Ctrl* ctrl = a.ctrl;
+  // Every load of the prologue is issued before any of them decides anything
+  // (they all read memory that exists whatever the status says): the status
+  // words, the sweep's range slots (workgroup 0, which reports to the host),
+  // the counts of buckets [0, 16 g) four at a time, and this group's counts.
   const uint32_t status = ctrl->status | ctrl->status_sweep;
-  if (status) {
-    if (g == 0 && tid == 0) publish_status(a.host, status, 0, 0, 0, 0, 0u);
-    return;
-  }
-  settle_range(ctrl, s_range, g == 0, a.levels != 0);
-  if (ctrl->bucket_overflow != 0) {  // written by the sweep, an earlier kernel
-    if (g == 0 && tid == 0) publish_range(a.host, kStatusTiled, s_range);
-    return;
-  }
-  if (g == 0 && tid == 0) publish_range(a.host, 0, s_range);
-
-  // futures in earlier groups: the counts of buckets [0, 16 g), four at a time
+  const uint32_t overflow = ctrl->bucket_overflow;  // written by the sweep, an earlier kernel
+  RangeLanes rl;
+  if (g == 0) rl = load_range_lanes(ctrl, a.levels != 0);
   uint32_t part = 0;
   const uint4* cnt4 = reinterpret_cast<const uint4*>(bk.cnt);
+#pragma unroll 4
   for (int i = tid; i < g * (kBucketGroup / 4); i += kBucketThreads) {
     const uint4 c = cnt4[i];
     part += c.x + c.y + c.z + c.w;
   }
+  uint32_t cg = tid < kBucketGroup ? bk.cnt[g * kBucketGroup + tid] : 0u;
+  if (status) {
+    if (g == 0 && tid == 0) publish_status(a.host, status, 0, 0, 0, 0, 0u);
+    return;
+  }
+  if (g == 0) {
+    settle_range(rl, ctrl, s_range, true, a.levels != 0);
+    if (tid == 0) publish_range(a.host, overflow ? kStatusTiled : 0u, s_range);
+  }
+  if (overflow) return;
+
+  // futures in earlier groups
   part = uint32_t(wave_sum_i64(int64_t(part)));
   if (lane_id() == 0) s_red[tid / kWave] = part;
   if (tid < kWave) {  // bucket offsets inside the group (wave 0)
-    uint32_t c = tid < kBucketGroup ? bk.cnt[g * kBucketGroup + tid] : 0u;
+    uint32_t c = cg;
     c = c < uint32_t(kBucketCap) ? c : uint32_t(kBucketCap);  // overflow was handled above
     const uint32_t inc = wave_incl_scan_u32(c);
     if (tid < kBucketGroup) s_off[tid + 1] = inc;
@@ -387,7 +419,8 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, Buck
     const int64_t sk = s_slack[i];
     const int32_t ps = s_pos[i];
     int rank = 0;
-    for (int j = lo; j < hi; ++j) {
+#pragma unroll 8
+    for (int j = lo; j < hi; ++j) {  // independent LDS loads: unrolled, they overlap
       const int64_t o = s_slack[j];
       rank += (o < sk) | ((o == sk) & (s_pos[j] < ps));
     }
@@ -408,11 +441,12 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, Buck
 __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_totals(SortArgs a, BucketArgs bk) {
   constexpr int kPerBlock = kBucketLbGroup / kWave;  // groups per workgroup, one per wave
   Ctrl* ctrl = a.ctrl;
-  if ((ctrl->status | ctrl->status_sweep) != 0 || ctrl->bucket_overflow != 0) return;
   const int wv = threadIdx.x / kWave;
   const int64_t grp = int64_t(blockIdx.x) * kPerBlock + wv;
   if (grp * kBucketLbGroup >= bk.nb) return;
+  const uint32_t bad = ctrl->status | ctrl->status_sweep | ctrl->bucket_overflow;
   const uint4 c = reinterpret_cast<const uint4*>(bk.cnt + grp * kBucketLbGroup)[lane_id()];
+  if (bad != 0) return;
   const uint32_t cap = uint32_t(kBucketCap);
   const int64_t t = int64_t((c.x < cap ? c.x : cap) + (c.y < cap ? c.y : cap) +
                             (c.z < cap ? c.z : cap) + (c.w < cap ? c.w : cap));
@@ -435,25 +469,30 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
   const int wv = tid / kWave;
   const int g = blockIdx.x;
   Ctrl* ctrl = a.ctrl;
+  // every load of the prologue first (as in k_bucket_sort): status words,
+  // range slots (workgroup 0), the totals of earlier groups, this bucket's count
   const uint32_t status = ctrl->status | ctrl->status_sweep;
+  const uint32_t overflow = ctrl->bucket_overflow;  // written by the sweep, an earlier kernel
+  RangeLanes rl;
+  if (g == 0) rl = load_range_lanes(ctrl, a.levels != 0);
+  int64_t part = 0;
+#pragma unroll 4
+  for (int j = tid; j < g; j += kBucketLbGroup) part += int64_t(a.bagg[j]);
+  const int64_t b0 = int64_t(g) * kBucketLbGroup;
+  uint32_t c = bk.cnt[b0 + tid];
   if (status) {
     if (g == 0 && tid == 0) publish_status(a.host, status, 0, 0, 0, 0, 0u);
     return;
   }
-  settle_range(ctrl, s_range, g == 0, a.levels != 0);
-  if (ctrl->bucket_overflow != 0) {  // written by the sweep, an earlier kernel
-    if (g == 0 && tid == 0) publish_range(a.host, kStatusTiled, s_range);
-    return;
+  if (g == 0) {
+    settle_range(rl, ctrl, s_range, true, a.levels != 0);
+    if (tid == 0) publish_range(a.host, overflow ? kStatusTiled : 0u, s_range);
   }
-  if (g == 0 && tid == 0) publish_range(a.host, 0, s_range);
+  if (overflow) return;
 
   // futures in earlier groups
-  int64_t part = 0;
-  for (int j = tid; j < g; j += kBucketLbGroup) part += int64_t(a.bagg[j]);
   part = wave_sum_i64(part);
   // bucket offsets inside the group
-  const int64_t b0 = int64_t(g) * kBucketLbGroup;
-  uint32_t c = bk.cnt[b0 + tid];
   c = c < uint32_t(kBucketCap) ? c : uint32_t(kBucketCap);  // overflow was handled above
   const uint32_t inc = wave_incl_scan_u32(c);
   if (lane_id() == kWave - 1) s_red[wv] = inc;
@@ -470,19 +509,32 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
   if (tid == 0) s_off[0] = 0;
   __syncthreads();
 
-  // The group's futures go through LDS in chunks of kLbStage: bucket ids first
-  // (each thread writes its own bucket's), then every slot of the chunk with
-  // independent loads, then each future is ranked among its bucket-mates.  A
-  // bucket cut by a chunk boundary is ranked from its slots in global memory.
+  // The group's futures go through LDS in chunks of at most kLbStage that end
+  // at a bucket boundary (a bucket holds at most kBucketCap < kLbStage, so
+  // every chunk holds at least one whole bucket): bucket ids first (each
+  // thread writes its own bucket's), then every slot of the chunk with
+  // independent loads, then each future is ranked among its bucket-mates.
   const int T = int(s_off[kBucketLbGroup]);
   const int my0 = int(before + inc - c), my1 = int(before + inc);
-  for (int cs = 0; cs < T; cs += kLbStage) {
-    const int ce = T < cs + kLbStage ? T : cs + kLbStage;
+  for (int cs = 0, ce = 0; cs < T; cs = ce) {
+    ce = T;
+    if (T - cs > kLbStage) {  // the last boundary within kLbStage of cs
+      int lo = 0, hi = kBucketLbGroup;  // s_off[lo] <= cs + kLbStage < s_off[hi]
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (int(s_off[mid]) <= cs + kLbStage) lo = mid; else hi = mid;
+      }
+      ce = int(s_off[lo]);
+    }
     for (int i = my0 > cs ? my0 : cs; i < (my1 < ce ? my1 : ce); ++i) s_b[i - cs] = uint8_t(tid);
     __syncthreads();
-    // Addresses first, then every load with no branch between them (a branch
-    // makes the compiler wait for the previous load before the next address).
-    // Past the chunk's end a lane loads slot 0, which always exists, and drops it.
+    // Addresses first, then every load with no per-lane branch between them
+    // (such a branch makes the compiler wait for the previous load before the
+    // next address).  Only the rows the chunk fills are loaded (a bound the
+    // same on every lane); a lane past the chunk's end loads the group's first
+    // slot, which always exists, and drops it (one line per group, not one
+    // address that every group queues on).
+    const int rows = (ce - cs + kBucketLbGroup - 1) / kBucketLbGroup;
     int64_t at[kLbStage / kBucketLbGroup];
 #pragma unroll
     for (int u = 0; u < kLbStage / kBucketLbGroup; ++u) {
@@ -490,11 +542,24 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
       const bool ok = i < ce;
       const int lb = s_b[ok ? i - cs : 0];
       const int64_t q = (b0 + lb) * kBucketCap + (i - int(s_off[lb]));
-      at[u] = ok ? q : 0;
+      at[u] = ok ? q : b0 * kBucketCap;
     }
     BucketSlot v[kLbStage / kBucketLbGroup];
 #pragma unroll
-    for (int u = 0; u < kLbStage / kBucketLbGroup; ++u) v[u] = bk.slot[at[u]];
+    for (int u = 0; u < kLbStage / kBucketLbGroup; ++u)
+      if (u < rows) v[u] = bk.slot[at[u]];
+    // the gathers by position (output slack, node id) are issued here, so
+    // that their latency overlaps the staging and the ranking
+    int64_t os[kLbStage / kBucketLbGroup];
+    int32_t on[kLbStage / kBucketLbGroup];
+#pragma unroll
+    for (int u = 0; u < kLbStage / kBucketLbGroup; ++u) {
+      if (u >= rows) continue;
+      const bool ok = cs + u * kBucketLbGroup + tid < ce;
+      const int32_t ps = ok ? v[u].pos : 0;  // a dropped lane's slot may be stale
+      os[u] = a.out_slack ? a.out_slack[ps] : v[u].key;
+      on[u] = a.node_of_pos ? a.node_of_pos[ps] : ps;
+    }
 #pragma unroll
     for (int u = 0; u < kLbStage / kBucketLbGroup; ++u) {
       const int i = cs + u * kBucketLbGroup + tid;
@@ -510,23 +575,16 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
       if (i >= ce) continue;
       const int lb = s_b[i - cs];
       const int k0 = int(s_off[lb]);
-      const int k1 = int(s_off[lb + 1]);
+      const int k1 = int(s_off[lb + 1]);  // inside [cs, ce]: chunks end at bucket boundaries
       int rank = 0;
-      if (k0 >= cs && k1 <= ce) {
-        for (int j = k0 - cs; j < k1 - cs; ++j) {
-          const int64_t o = s_slack[j];
-          rank += (o < v[u].key) | ((o == v[u].key) & (s_pos[j] < v[u].pos));
-        }
-      } else {
-        const BucketSlot* sl = bk.slot + (b0 + lb) * kBucketCap;
-        for (int j = 0; j < k1 - k0; ++j) {
-          const int64_t o = sl[j].key;
-          rank += (o < v[u].key) | ((o == v[u].key) & (sl[j].pos < v[u].pos));
-        }
+#pragma unroll 8
+      for (int j = k0 - cs; j < k1 - cs; ++j) {  // independent LDS loads: unrolled, they overlap
+        const int64_t o = s_slack[j];
+        rank += (o < v[u].key) | ((o == v[u].key) & (s_pos[j] < v[u].pos));
       }
       const int64_t out = base + k0 + rank;
-      a.order[out] = a.node_of_pos ? a.node_of_pos[v[u].pos] : v[u].pos;
-      a.slack[out] = a.out_slack ? a.out_slack[v[u].pos] : v[u].key;
+      a.order[out] = on[u];
+      a.slack[out] = os[u];
       a.route[out] = v[u].route;
       if (a.cost) a.cost[out] = v[u].cost;
     }

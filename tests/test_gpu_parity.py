@@ -316,6 +316,23 @@ def test_priority_levels_bucketed():
         assert bucketed >= 3, f"only {bucketed} level passes took the bucketed sort"
 
 
+def test_lpt_repeated_bucketed():
+    """LPT's long-tailed key at paper scale on one handle: the first passes
+    overflow the base plan and settle on denser buckets (the large-bucket
+    kernels, whose busiest group holds more futures than one LDS chunk);
+    every pass must match the oracle and most must take the bucketed sort."""
+    p = wl.paper_scale()
+    with nalar.Policy() as pol:
+        pol.set_timing(True)
+        bucketed = 0
+        for i in range(8):
+            check(pol, p, f"lpt pass {i}", policy=nalar.NALAR_ORDER_LPT)
+            names = [n for n, _ in pol.timing()]
+            if "sort_bucket" in names and "sort_pass0" not in names:
+                bucketed += 1
+        assert bucketed >= 5, f"only {bucketed} LPT passes took the bucketed sort"
+
+
 def test_policy_unknown_bits_rejected(policy):
     dp = nalar.DeviceProblem.from_host(wl.tiny())
     out = nalar.DeviceResult.alloc(dp.n_nodes)
