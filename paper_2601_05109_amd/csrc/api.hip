@@ -528,6 +528,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   sa.slack = r->slack_us;
   sa.route = r->route;
   sa.cost = r->cost_us;
+  __atomic_store_n(&h->host->max_bucket, 0u, __ATOMIC_RELAXED);       // written by the large-bucket sort
   __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);  // the kernels overwrite it
   bool tiled = bk.nb == 0;
   if (!tiled) {
@@ -557,8 +558,17 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
       NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
     } else {
       h->bucket_backoff = 1;
+      const bool crowded = __atomic_load_n(&h->host->max_bucket, __ATOMIC_ACQUIRE) > kBucketCrowded;
+      const bool was_relaxed = h->bucket_relaxed;
       h->bucket_relaxed = false;
-      if (h->bucket_dense > 0 && ++h->bucket_calm >= h->bucket_relax) {  // try fewer buckets again
+      if (crowded && h->bucket_dense < 3 && bk.nb < kBucketMax) {
+        // sorted, but a bucket is crowded (its futures rank one another one by
+        // one, and its group of buckets outweighs the rest): add buckets, and
+        // if fewer buckets were just tried, wait longer before trying again
+        ++h->bucket_dense;
+        h->bucket_calm = 0;
+        if (was_relaxed && h->bucket_relax < 4096) h->bucket_relax *= 2;
+      } else if (h->bucket_dense > 0 && ++h->bucket_calm >= h->bucket_relax) {  // try fewer buckets again
         --h->bucket_dense;
         h->bucket_calm = 0;
         h->bucket_relaxed = true;

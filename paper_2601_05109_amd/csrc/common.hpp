@@ -63,6 +63,7 @@ struct Ctrl {
   int64_t part_max[kParts];
   int64_t part_cnt[kParts];
   uint32_t part_lvl[kParts];
+  uint32_t part_crowd[kParts];   // fullest bucket seen by the large-bucket totals kernel
   uint32_t ghist_slack[kMaxSortPasses * kRadixBuckets];
   uint32_t ghist_group[kMaxGroupPasses * kRadixBuckets];
 };
@@ -90,6 +91,9 @@ constexpr int kBucketLbMin = 16384;
 constexpr int kBucketLbGroup = 256;
 constexpr int kBucketLbGroups = kBucketMax / kBucketLbGroup;
 static_assert(kBucketLbGroup == 4 * kWave, "one uint4 of counters per lane and group");
+// A bucket with more futures than this after a large-bucket sort asks for a
+// denser plan next time (the sort still succeeded).
+constexpr uint32_t kBucketCrowded = 16;
 static_assert(kBucketLbMin % kBucketLbGroup == 0, "whole groups");
 constexpr uint32_t kStatusTiled = 0x20000000u;
 
@@ -109,6 +113,8 @@ struct HostStatus {
   int64_t slack_max;   //   priority levels the range of the key within its level)
   uint32_t aux_status; // status bits of the load-aware routing kernel
   uint32_t level_mask; // priority levels of this pass (bit l: level l; with levels only)
+  uint32_t max_bucket; // futures in the fullest bucket (large-bucket sort only, else 0)
+  uint32_t pad_;
 };
 
 // Resets a control block for a later pass (run by one workgroup).
@@ -129,6 +135,7 @@ __device__ inline void reset_ctrl(Ctrl* c) {
     c->part_max[i] = INT64_MIN;
     c->part_cnt[i] = 0;
     c->part_lvl[i] = 0;
+    c->part_crowd[i] = 0;
   }
   for (int i = tid; i < kMaxSortPasses * kRadixBuckets; i += blockDim.x) c->ghist_slack[i] = 0;
   for (int i = tid; i < kMaxGroupPasses * kRadixBuckets; i += blockDim.x) c->ghist_group[i] = 0;
@@ -152,6 +159,7 @@ __device__ inline void reset_ctrl_spread(Ctrl* c, int64_t gi, int64_t gstride) {
     c->part_max[i] = INT64_MIN;
     c->part_cnt[i] = 0;
     c->part_lvl[i] = 0;
+    c->part_crowd[i] = 0;
   }
   for (int64_t i = gi; i < kMaxSortPasses * kRadixBuckets; i += gstride) c->ghist_slack[i] = 0;
   for (int64_t i = gi; i < kMaxGroupPasses * kRadixBuckets; i += gstride) c->ghist_group[i] = 0;

@@ -451,7 +451,15 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_totals(SortArgs a, Bu
   const int64_t t = int64_t((c.x < cap ? c.x : cap) + (c.y < cap ? c.y : cap) +
                             (c.z < cap ? c.z : cap) + (c.w < cap ? c.w : cap));
   const int64_t sum = wave_sum_i64(t);
-  if (lane_id() == 0) a.bagg[grp] = uint64_t(sum);
+  // the fullest bucket (how crowded the plan is: the host adds buckets when
+  // it is), folded into one of kParts slots
+  const uint32_t m01 = c.x > c.y ? c.x : c.y, m23 = c.z > c.w ? c.z : c.w;
+  const int64_t mx = wave_max_i64(int64_t(m01 > m23 ? m01 : m23));
+  if (lane_id() == 0) {
+    a.bagg[grp] = uint64_t(sum);
+    __hip_atomic_fetch_max(&ctrl->part_crowd[grp & (kParts - 1)], uint32_t(mx), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
 constexpr int kLbStage = 2048;  // futures of a bucket group staged in LDS at once
@@ -474,7 +482,11 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
   const uint32_t status = ctrl->status | ctrl->status_sweep;
   const uint32_t overflow = ctrl->bucket_overflow;  // written by the sweep, an earlier kernel
   RangeLanes rl;
-  if (g == 0) rl = load_range_lanes(ctrl, a.levels != 0);
+  uint32_t crowd = 0;
+  if (g == 0) {
+    rl = load_range_lanes(ctrl, a.levels != 0);
+    if (tid < kWave) crowd = ctrl->part_crowd[tid];
+  }
   int64_t part = 0;
 #pragma unroll 4
   for (int j = tid; j < g; j += kBucketLbGroup) part += int64_t(a.bagg[j]);
@@ -485,6 +497,8 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
     return;
   }
   if (g == 0) {
+    crowd = uint32_t(wave_max_i64(int64_t(crowd)));  // wave 0 holds the slots
+    if (tid == 0) __hip_atomic_store(&a.host->max_bucket, crowd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     settle_range(rl, ctrl, s_range, true, a.levels != 0);
     if (tid == 0) publish_range(a.host, overflow ? kStatusTiled : 0u, s_range);
   }
