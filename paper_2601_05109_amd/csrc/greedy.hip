@@ -5,18 +5,242 @@
 // load across instances, Section 6.1).
 //
 // Futures of different types never share a candidate, so each type is an
-// independent sequence: one wavefront per type walks the output order, picks
-// its own futures with a ballot, and routes them in turn.  The candidates of
-// the type and their running loads stay in the wave's LDS; a future's costs are
-// evaluated lane-parallel over the candidates and the lexicographic minimum of
-// (cost, candidate index) is found with a wave reduction and a ballot.
+// independent sequence: one wavefront per type walks the output order and
+// picks its own futures with a ballot.  With at most 64 candidates, lane q
+// holds candidate q and its running load; the type's futures are queued in LDS
+// and routed in batches of 64:
+//   1. lane j takes future j of the batch and computes its service time on
+//      every candidate (independent work, all lanes busy) into an LDS table;
+//   2. the futures are then routed in order: lane q adds its running load to
+//      the table entry of (future, q), the lexicographic minimum of (cost,
+//      candidate) comes from a reduction over as few lanes as there are
+//      candidates and a ballot, and the winner updates its load.
+// Only step 2 is sequential, and its chain per future is an add, the
+// reduction and a compare.  More than 64 candidates stay in LDS and each
+// future scans them lane-parallel.
 #include "internal.hpp"
 
 namespace nalar {
 
 namespace {
 
-constexpr int kGreedyThreads = kWave;  // one wavefront per workgroup
+constexpr int kGreedyThreads = kWave;       // one wavefront per workgroup
+constexpr int kWalk = 16;                   // chunks of the output order loaded at once
+constexpr int kGreedyRing = 2048;           // queued futures of the type: under 64 + one walk block
+constexpr int kSvStride = kWave + 1;        // padded row: lanes writing one column spread over banks
+static_assert(kGreedyRing >= kWave - 1 + kWalk * kWave, "the queue holds a batch's remainder and a block");
+
+// DPP controls that stay inside a row of 16 lanes.
+constexpr int kDppHalfMirror = 0x141;       // lane i <- lane 7 - i within each 8 lanes
+constexpr int kDppMirror = 0x140;           // lane i <- lane 15 - i within each 16 lanes
+
+// A DPP move whose pattern reads a lane of the same row for every lane (the
+// quad permutations and mirrors), so no lane keeps its old value.
+template <int kCtrl>
+__device__ inline int64_t row_dpp_i64(int64_t x) {
+  const int lo = __builtin_amdgcn_mov_dpp(int(uint32_t(uint64_t(x))), kCtrl, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_mov_dpp(int(uint32_t(uint64_t(x) >> 32)), kCtrl, 0xF, 0xF, false);
+  return int64_t((uint64_t(uint32_t(hi)) << 32) | uint32_t(lo));
+}
+
+// Minimum of lanes [0, W) (lanes past the candidates hold INT64_MAX), read
+// from lane 0.
+template <int W>
+__device__ inline int64_t lanes_min_i64(int64_t x) {
+  auto mn = [](int64_t u, int64_t v) { return u < v ? u : v; };
+  if constexpr (W > 16) {
+    return wave_min_i64(x);
+  } else {
+    x = mn(x, row_dpp_i64<kDppXor1>(x));
+    x = mn(x, row_dpp_i64<kDppXor2>(x));
+    x = mn(x, row_dpp_i64<kDppHalfMirror>(x));
+    if constexpr (W > 8) x = mn(x, row_dpp_i64<kDppMirror>(x));
+    return readlane_i64(x, 0);
+  }
+}
+
+struct Cand {  // the type's candidates in LDS (candidate q = the q-th instance of the type)
+  int64_t* load;
+  double* inv;
+  int32_t* speed;
+  int32_t* idx;
+  int32_t* q_of;   // candidate of an instance of the type
+  int32_t* itype;  // type of every instance
+};
+
+// Routes the queued futures [head, head + B) of type t (B <= 64): lane q < nc
+// holds candidate q's index and running load.
+template <int W>
+__device__ inline void route_batch(const GreedyArgs& g, const Cand& cd, int32_t t, int nc, int head, int B,
+                                   const int32_t* r_out, const int64_t* r_est, const int32_t* r_loc,
+                                   int64_t* sv, int64_t& my_load, int32_t my_idx, bool& bad) {
+  const int ln = lane_id();
+  const int slot = (head + ln) & (kGreedyRing - 1);
+  const bool act = ln < B;
+  const int32_t out_j = act ? r_out[slot] : 0;
+  const int64_t e_j = act ? r_est[slot] : 0;
+  const int32_t l_j = act ? r_loc[slot] : -1;
+  // a future whose state lives on an instance of its own type runs there
+  const int32_t pin_j = (g.stateful && l_j >= 0 && cd.itype[l_j] == t) ? cd.q_of[l_j] : -1;
+  // 1. service times of future j (lane j) on every candidate
+  const double a = double(e_j * 1000);
+  for (int q = 0; q < nc; ++q) sv[ln * kSvStride + q] = floordiv_exact(a, cd.speed[q], cd.inv[q]);
+  // One wavefront: its LDS accesses complete in program order; only the
+  // compiler must not move the reads below above these writes.
+  __asm__ __volatile__("" ::: "memory");
+  // 2. in order.  Only the running loads carry from one future to the next;
+  // the winner and cost of future j go to lane j and the batch's outputs are
+  // stored together at the end.
+  const bool cand = ln < nc;
+  int32_t qv = 0;
+  int64_t cv = 0;
+  int64_t svc_next = sv[ln];  // the next future's entry is read one step ahead
+  for (int j = 0; j < B; ++j) {
+    const int64_t svc = svc_next;  // a lane past the candidates reads a spare entry
+    if (j + 1 < B) svc_next = sv[(j + 1) * kSvStride + ln];
+    const int32_t l = readlane_i32(l_j, j);
+    const int32_t pq = readlane_i32(pin_j, j);
+    const int64_t mt = (pq < 0 && l >= 0 && l != my_idx) ? g.mig : 0;
+    const int64_t c = cand ? my_load + svc + mt : INT64_MAX;
+    int qb;
+    int64_t cb;
+    if (pq >= 0) {
+      qb = pq;
+      cb = readlane_i64(c, qb);
+    } else {
+      cb = lanes_min_i64<W>(c);
+      qb = __builtin_ctzll(ballot(c == cb));  // lanes ascend with the index: lowest wins
+    }
+    my_load += ln == qb ? svc : 0;
+    qv = ln == j ? qb : qv;
+    cv = ln == j ? cb : cv;
+  }
+  if (act) {
+    g.route[out_j] = cd.idx[qv];
+    if (g.cost) g.cost[out_j] = cv;
+  }
+  // loads only grow, and a batch adds at most 64 service times (each below
+  // 2^50), so one check per batch sees every load that passes the limit
+  bad |= cand && my_load > NALAR_REM_MAX;
+  __asm__ __volatile__("" ::: "memory");  // the next batch overwrites the table
+}
+
+struct Queue {  // LDS: the queued futures and the batch's service-time table
+  int32_t out[kGreedyRing];
+  int64_t est[kGreedyRing];
+  int32_t loc[kGreedyRing];
+  int64_t sv[kWave * kSvStride];
+};
+
+// The type's futures in output order, queued through LDS and routed in
+// batches of 64 (candidates in registers, nc <= W <= 64).
+template <int W>
+__device__ void route_type_regs(const GreedyArgs& g, const Cand& cd, int32_t t, int nc, Queue& Q, bool& bad) {
+  int32_t* r_out = Q.out;
+  int64_t* r_est = Q.est;
+  int32_t* r_loc = Q.loc;
+  int64_t* sv = Q.sv;
+  const int ln = lane_id();
+  int64_t my_load = 0;
+  int32_t my_idx = -1;
+  if (ln < nc) {
+    my_load = cd.load[ln];
+    my_idx = cd.idx[ln];
+  }
+  // The output order is walked kWalk chunks of 64 at a time: every attribute
+  // load of a block is issued before any is used, and the next block's ids are
+  // loaded while this block is routed, so a block costs one memory latency.
+  const int64_t R = g.R;
+  constexpr int64_t kBlock = int64_t(kWalk) * kWave;
+  int32_t vn[kWalk];
+#pragma unroll
+  for (int u = 0; u < kWalk; ++u) vn[u] = u * kWave + ln < R ? g.order[u * kWave + ln] : 0;
+  int head = 0, tail = 0;  // queue positions (the same on every lane)
+  for (int64_t k0 = 0; k0 < R; k0 += kBlock) {
+    int32_t tt[kWalk], ll[kWalk];
+    int64_t ee[kWalk];
+#pragma unroll
+    for (int u = 0; u < kWalk; ++u) {
+      const bool in = k0 + u * kWave + ln < R;
+      tt[u] = in ? g.type[vn[u]] : -1;
+      ee[u] = in ? g.est[vn[u]] : 0;
+      ll[u] = in ? g.loc[vn[u]] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < kWalk; ++u) {
+      const int64_t k = k0 + kBlock + u * kWave + ln;
+      vn[u] = k < R ? g.order[k] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kWalk; ++u) {
+      const uint64_t mk = ballot(tt[u] == t);
+      if (tt[u] == t) {
+        const int s = (tail + int(lanes_below(mk))) & (kGreedyRing - 1);
+        r_out[s] = int32_t(k0 + u * kWave + ln);
+        r_est[s] = ee[u];
+        r_loc[s] = ll[u];
+      }
+      tail += int(__popcll(mk));
+    }
+    __asm__ __volatile__("" ::: "memory");
+    for (; tail - head >= kWave; head += kWave)
+      route_batch<W>(g, cd, t, nc, head, kWave, r_out, r_est, r_loc, sv, my_load, my_idx, bad);
+  }
+  if (tail > head) route_batch<W>(g, cd, t, nc, head, tail - head, r_out, r_est, r_loc, sv, my_load, my_idx, bad);
+}
+
+// More than 64 candidates: every future scans them lane-parallel in LDS.
+__device__ void route_type_lds(const GreedyArgs& g, const Cand& cd, int32_t t, int nc, bool& bad) {
+  const int ln = lane_id();
+  const int64_t R = g.R;
+  for (int64_t k0 = 0; k0 < R; k0 += kWave) {
+    const int64_t k = k0 + ln;
+    int32_t tk = -1, lk = -1;
+    int64_t ek = 0;
+    if (k < R) {
+      const int32_t v = g.order[k];
+      tk = g.type[v];
+      ek = g.est[v];
+      lk = g.loc[v];
+    }
+    uint64_t mk = ballot(tk == t);
+    while (mk != 0) {  // this chunk's futures of type t, in order
+      const int src = __builtin_ctzll(mk);
+      mk &= mk - 1;
+      const int64_t e = readlane_i64(ek, src);
+      const int32_t l = readlane_i32(lk, src);
+      const double a = double(e * 1000);
+      const bool pinned = g.stateful && l >= 0 && cd.itype[l] == t;
+      int qb;
+      int64_t cb;
+      if (pinned) {
+        qb = cd.q_of[l];
+        cb = cd.load[qb] + floordiv_exact(a, cd.speed[qb], cd.inv[qb]);
+      } else {
+        int64_t bc = INT64_MAX;
+        int bq = INT32_MAX;
+        for (int q = ln; q < nc; q += kWave) {  // ascending q per lane: strict < keeps the lowest
+          int64_t c = cd.load[q] + floordiv_exact(a, cd.speed[q], cd.inv[q]);
+          if (l >= 0 && l != cd.idx[q]) c += g.mig;
+          if (c < bc) { bc = c; bq = q; }
+        }
+        cb = wave_min_i64(bc);
+        qb = int(wave_min_i64(bc == cb ? int64_t(bq) : int64_t(INT32_MAX)));
+      }
+      if (ln == 0) {
+        g.route[k0 + src] = cd.idx[qb];
+        if (g.cost) g.cost[k0 + src] = cb;
+        const int64_t nl = cd.load[qb] + floordiv_exact(a, cd.speed[qb], cd.inv[qb]);
+        cd.load[qb] = nl;
+        bad |= nl > NALAR_REM_MAX;
+      }
+      // One wavefront: its LDS accesses complete in program order, so the
+      // next future's reads see this update; only the compiler must not
+      // move them (a barrier would also wait for the stores above).
+      __asm__ __volatile__("" ::: "memory");
+    }
+  }
+}
 
 __global__ __launch_bounds__(kGreedyThreads) void k_route_greedy(GreedyArgs g) {
   __shared__ int64_t s_load[NALAR_MAX_INSTANCES];   // running load of candidate q
@@ -25,6 +249,7 @@ __global__ __launch_bounds__(kGreedyThreads) void k_route_greedy(GreedyArgs g) {
   __shared__ int32_t s_idx[NALAR_MAX_INSTANCES];    // instance id of candidate q
   __shared__ int32_t s_q[NALAR_MAX_INSTANCES];      // candidate of instance i (type t only)
   __shared__ int32_t s_itype[NALAR_MAX_INSTANCES];  // type of every instance
+  __shared__ Queue Q;
   const int w = blockIdx.x;
   const int ln = lane_id();
   const int M = g.M;
@@ -54,99 +279,16 @@ __global__ __launch_bounds__(kGreedyThreads) void k_route_greedy(GreedyArgs g) {
   }
   __syncthreads();
 
-  // Up to 64 candidates live in registers (lane q holds candidate q and its
-  // running load); more stay in LDS.
-  const bool in_regs = nc <= kWave;
-  int64_t my_load = 0;
-  int32_t my_speed = 1, my_idx = -1;
-  double my_inv = 0.0;
-  if (in_regs && ln < nc) {
-    my_load = s_load[ln];
-    my_speed = s_speed[ln];
-    my_inv = s_inv[ln];
-    my_idx = s_idx[ln];
-  }
-
-  // The output order is read a chunk of 64 ahead (ids two chunks ahead, their
-  // attributes one chunk ahead), so its latency overlaps the routing.
+  const Cand cd{s_load, s_inv, s_speed, s_idx, s_q, s_itype};
   bool bad = false;
-  const int64_t R = g.R;
-  int32_t v_next = ln < R ? g.order[ln] : 0;
-  int32_t v_after = kWave + ln < R ? g.order[kWave + ln] : 0;
-  int32_t t_cur = ln < R ? g.type[v_next] : -1;
-  int64_t e_cur = ln < R ? g.est[v_next] : 0;
-  int32_t l_cur = ln < R ? g.loc[v_next] : -1;
-  for (int64_t k0 = 0; k0 < R; k0 += kWave) {
-    const int32_t t_this = t_cur;
-    const int64_t e_this = e_cur;
-    const int32_t l_this = l_cur;
-    {  // prefetch
-      const int64_t k1 = k0 + kWave + ln, k2 = k0 + 2 * kWave + ln;
-      const int32_t v1 = v_after;
-      t_cur = k1 < R ? g.type[v1] : -1;
-      e_cur = k1 < R ? g.est[v1] : 0;
-      l_cur = k1 < R ? g.loc[v1] : -1;
-      v_after = k2 < R ? g.order[k2] : 0;
-    }
-    uint64_t mk = ballot(t_this == t);
-    while (mk != 0) {  // this chunk's futures of type t, in order
-      const int src = __builtin_ctzll(mk);
-      mk &= mk - 1;
-      const int64_t e = readlane_i64(e_this, src);
-      const int32_t l = readlane_i32(l_this, src);
-      const double a = double(e * 1000);
-      const bool pinned = g.stateful && l >= 0 && s_itype[l] == t;
-      if (in_regs) {
-        const int64_t svc = ln < nc ? floordiv_exact(a, my_speed, my_inv) : 0;
-        int64_t c = INT64_MAX;
-        if (ln < nc) c = my_load + svc + ((!pinned && l >= 0 && l != my_idx) ? g.mig : 0);
-        int qb;
-        int64_t cb;
-        if (pinned) {
-          qb = s_q[l];
-          cb = readlane_i64(c, qb);
-        } else {
-          cb = wave_min_i64(c);
-          qb = __builtin_ctzll(ballot(c == cb));  // lanes ascend with the index: lowest wins
-        }
-        if (ln == qb) {
-          g.route[k0 + src] = my_idx;
-          if (g.cost) g.cost[k0 + src] = cb;
-          my_load += svc;
-          bad |= my_load > NALAR_REM_MAX;
-        }
-      } else {
-        int qb;
-        int64_t cb;
-        if (pinned) {
-          qb = s_q[l];
-          cb = s_load[qb] + floordiv_exact(a, s_speed[qb], s_inv[qb]);
-        } else {
-          int64_t bc = INT64_MAX;
-          int bq = INT32_MAX;
-          for (int q = ln; q < nc; q += kWave) {  // ascending q per lane: strict < keeps the lowest
-            int64_t c = s_load[q] + floordiv_exact(a, s_speed[q], s_inv[q]);
-            if (l >= 0 && l != s_idx[q]) c += g.mig;
-            if (c < bc) { bc = c; bq = q; }
-          }
-          cb = wave_min_i64(bc);
-          qb = int(wave_min_i64(bc == cb ? int64_t(bq) : int64_t(INT32_MAX)));
-        }
-        if (ln == 0) {
-          g.route[k0 + src] = s_idx[qb];
-          if (g.cost) g.cost[k0 + src] = cb;
-          const int64_t nl = s_load[qb] + floordiv_exact(a, s_speed[qb], s_inv[qb]);
-          s_load[qb] = nl;
-          bad |= nl > NALAR_REM_MAX;
-        }
-        // One wavefront: its LDS accesses complete in program order, so the
-        // next future's reads see this update; only the compiler must not
-        // move them (a barrier would also wait for the stores above).
-        __asm__ __volatile__("" ::: "memory");
-      }
-    }
-    (void)v_next;
-  }
+  if (nc <= 8)
+    route_type_regs<8>(g, cd, t, nc, Q, bad);
+  else if (nc <= 16)
+    route_type_regs<16>(g, cd, t, nc, Q, bad);
+  else if (nc <= kWave)
+    route_type_regs<kWave>(g, cd, t, nc, Q, bad);
+  else
+    route_type_lds(g, cd, t, nc, bad);
   bad = ballot(bad) != 0;
   if (ln == 0 && bad)
     __hip_atomic_fetch_or(&g.host->aux_status, kStRange, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);

@@ -367,6 +367,24 @@ def test_greedy_many_candidates_and_overflow(policy):
     check(policy, wl.tiny(), "after greedy overflow")
 
 
+@pytest.mark.parametrize("n_inst", [1, 7, 8, 9, 16, 17, 63, 64, 65])
+def test_greedy_candidate_counts(policy, n_inst):
+    """Load-aware routing around every width the kernel distinguishes (up to
+    8, 16 and 64 candidates in registers, more in LDS), with enough futures of
+    the type to wrap its queue and leave a partial last batch; plain, pinned
+    (stateful) and with heavy ties (equal speeds and loads)."""
+    rng = np.random.default_rng(40 + n_inst)
+    G = nalar.NALAR_ROUTE_GREEDY
+    n = 777
+    loc = np.where(rng.random(n) < 0.4, rng.integers(0, n_inst, n), -1)
+    p = _one_type(n_inst, rng.integers(0, 10**6, n_inst), rng.integers(300, 3000, n_inst),
+                  rng.integers(0, 10**5, n), loc=loc)
+    check(policy, p, f"greedy {n_inst} candidates", policy=G)
+    check(policy, p, f"greedy {n_inst} candidates stateful", policy=G | nalar.NALAR_ROUTE_STATEFUL)
+    q = _one_type(n_inst, [500] * n_inst, [1000] * n_inst, rng.integers(1, 4, n) * 10, loc=loc)
+    check(policy, q, f"greedy {n_inst} tied candidates", policy=G)
+
+
 def test_other_seeds(policy):
     for s in (11, 12):
         check(policy, wl.paper_scale(seed=s), f"paper-scale seed {s}")
