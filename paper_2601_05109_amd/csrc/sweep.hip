@@ -1271,14 +1271,23 @@ __device__ inline ITabLds carve_itab(unsigned char* sp, int M) {
   return it;
 }
 
-// Brings the seven 64-byte lines of the sweep's kernel arguments into the
-// scalar cache with loads that are all in flight at once.  The argument block
-// is large and the compiler reloads its fields on demand, one wait each; cold
-// lines would otherwise cost a round trip apiece.
-static_assert(sizeof(SweepArgs) + sizeof(int) > 6 * 64 && sizeof(SweepArgs) + sizeof(int) <= 7 * 64,
+// The wave kernel's arguments as they lie in the kernel-argument segment
+// (explicit arguments in order at their natural alignment, from offset 0).
+struct WaveKernArgs {
+  SweepArgs a;
+  int wcap;
+};
+
+// Brings the seven 64-byte lines of the wave kernel's arguments into the
+// scalar cache with loads that are all in flight at once, and returns the
+// argument block through a pointer the compiler cannot read ahead of them:
+// the block is large and its fields are reloaded on demand, so every field
+// read is then a scalar-cache hit instead of a round trip per cold line.
+static_assert(sizeof(WaveKernArgs) > 6 * 64 && sizeof(WaveKernArgs) <= 7 * 64,
               "warm_kernargs covers exactly the argument block's lines");
-__device__ inline void warm_kernargs() {
-  const auto kp = __builtin_amdgcn_kernarg_segment_ptr();
+typedef __attribute__((address_space(4))) const WaveKernArgs* WaveKernArgsPtr;
+__device__ inline const WaveKernArgs* warm_kernargs() {
+  WaveKernArgsPtr kp = (WaveKernArgsPtr)__builtin_amdgcn_kernarg_segment_ptr();
   uint32_t v0, v1, v2, v3, v4, v5, v6;
   __asm__ __volatile__(
       "s_load_dword %0, %7, 0\n"
@@ -1289,9 +1298,9 @@ __device__ inline void warm_kernargs() {
       "s_load_dword %5, %7, 320\n"
       "s_load_dword %6, %7, 384\n"
       "s_waitcnt lgkmcnt(0)"
-      : "=&s"(v0), "=&s"(v1), "=&s"(v2), "=&s"(v3), "=&s"(v4), "=&s"(v5), "=&s"(v6)
-      : "s"(kp));
+      : "=&s"(v0), "=&s"(v1), "=&s"(v2), "=&s"(v3), "=&s"(v4), "=&s"(v5), "=&s"(v6), "+s"(kp));
   (void)v0; (void)v1; (void)v2; (void)v3; (void)v4; (void)v5; (void)v6;
+  return (const WaveKernArgs*)kp;
 }
 
 // The next pass's bucket counters and, in fused mode, its control block.
@@ -1311,8 +1320,12 @@ __device__ inline void clear_for_next_pass(const SweepArgs& a) {
 // Each wave folds its slack range and ready count into one of the control
 // block's partial slots.
 template <int NPTW, bool kFused>
-__global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a, int wcap) {
-  warm_kernargs();
+__global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a_arg, int wcap_arg) {
+  (void)a_arg;
+  (void)wcap_arg;
+  const WaveKernArgs* kargs = warm_kernargs();  // the same two arguments, read after the warm-up
+  const SweepArgs& a = kargs->a;
+  const int wcap = kargs->wcap;
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ Shared S;
   __shared__ __align__(16) int32_t s_itype[kWaveItabMax];
