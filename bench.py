@@ -80,8 +80,8 @@ def pass_alg_bytes(N: int, E: int, R: int, W: int, M: int) -> float:
 # copy of known size (`python3 bench.py --copy-calibration`).  Valid only for
 # the kernel sources it was taken on: a different source digest reports null.
 TRAFFIC = {
-    ("paper-scale", "sweep"): {"src_sha256": "ddfcfb54dead285ac3357c427b48d938ae89fa39da8f1ca3c15ce284efcc1894",
-                               "bytes_per_launch": 7727960},
+    ("paper-scale", "sweep"): {"src_sha256": "fccd7efccde326fab98f0aa28c054569cbbf11d3f8bfd8f7d8ef932a0b3b4d00",
+                               "bytes_per_launch": 7657115},
 }
 
 
