@@ -17,6 +17,8 @@ HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 ARCH = "gfx950"
 FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         # leading scalar kernel arguments arrive preloaded in scalar registers
+         "-mllvm", "-amdgpu-kernarg-preload-count=16",
          f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}", "-Wall", "-Wextra",
          "-Wno-unused-parameter"]
 

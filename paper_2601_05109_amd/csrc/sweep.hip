@@ -1271,36 +1271,69 @@ __device__ inline ITabLds carve_itab(unsigned char* sp, int M) {
   return it;
 }
 
+// The first things a wave reads: the pointers and sizes its opening loads
+// need, passed as the wave kernel's leading scalar arguments so that they
+// arrive preloaded in scalar registers (the library is built with
+// kernel-argument preloading; fourteen dwords fit beside the segment
+// pointer) and the opening loads start at once.
+struct WaveHead {
+  const int32_t* inst_type;
+  const int32_t* inst_speed;
+  const int64_t* inst_load;
+  const int64_t* deadline;
+  const int32_t* wf;
+  int64_t N;
+  int32_t W;
+  int32_t M;
+};
+static_assert(sizeof(WaveHead) == 14 * 4, "the preloaded arguments fill fourteen dwords");
+
 // The wave kernel's arguments as they lie in the kernel-argument segment
 // (explicit arguments in order at their natural alignment, from offset 0).
 struct WaveKernArgs {
+  WaveHead head;
   SweepArgs a;
   int wcap;
 };
+constexpr int kKernArgLines = int((sizeof(WaveKernArgs) + 63) / 64);
+static_assert(kKernArgLines == 8, "warm_kernargs loads eight lines");
 
-// Brings the seven 64-byte lines of the wave kernel's arguments into the
-// scalar cache with loads that are all in flight at once, and returns the
-// argument block through a pointer the compiler cannot read ahead of them:
-// the block is large and its fields are reloaded on demand, so every field
-// read is then a scalar-cache hit instead of a round trip per cold line.
-static_assert(sizeof(WaveKernArgs) > 6 * 64 && sizeof(WaveKernArgs) <= 7 * 64,
-              "warm_kernargs covers exactly the argument block's lines");
+// The eight 64-byte lines of the wave kernel's arguments are brought into the
+// scalar cache with loads that are all in flight at once (issued before the
+// opening loads, waited for after them), and the argument block is then read
+// through a pointer the compiler cannot read ahead of the wait: the block is
+// large and its fields are reloaded on demand, so every field read is a
+// scalar-cache hit instead of a round trip per cold line.
 typedef __attribute__((address_space(4))) const WaveKernArgs* WaveKernArgsPtr;
-__device__ inline const WaveKernArgs* warm_kernargs() {
-  WaveKernArgsPtr kp = (WaveKernArgsPtr)__builtin_amdgcn_kernarg_segment_ptr();
-  uint32_t v0, v1, v2, v3, v4, v5, v6;
+struct KernArgWarm {
+  uint32_t v[kKernArgLines];
+  WaveKernArgsPtr kp;
+};
+
+__device__ inline void warm_kernargs_issue(KernArgWarm& w) {
+  w.kp = (WaveKernArgsPtr)__builtin_amdgcn_kernarg_segment_ptr();
   __asm__ __volatile__(
-      "s_load_dword %0, %7, 0\n"
-      "s_load_dword %1, %7, 64\n"
-      "s_load_dword %2, %7, 128\n"
-      "s_load_dword %3, %7, 192\n"
-      "s_load_dword %4, %7, 256\n"
-      "s_load_dword %5, %7, 320\n"
-      "s_load_dword %6, %7, 384\n"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&s"(v0), "=&s"(v1), "=&s"(v2), "=&s"(v3), "=&s"(v4), "=&s"(v5), "=&s"(v6), "+s"(kp));
-  (void)v0; (void)v1; (void)v2; (void)v3; (void)v4; (void)v5; (void)v6;
-  return (const WaveKernArgs*)kp;
+      "s_load_dword %0, %8, 0\n"
+      "s_load_dword %1, %8, 64\n"
+      "s_load_dword %2, %8, 128\n"
+      "s_load_dword %3, %8, 192\n"
+      "s_load_dword %4, %8, 256\n"
+      "s_load_dword %5, %8, 320\n"
+      "s_load_dword %6, %8, 384\n"
+      "s_load_dword %7, %8, 448"
+      : "=&s"(w.v[0]), "=&s"(w.v[1]), "=&s"(w.v[2]), "=&s"(w.v[3]), "=&s"(w.v[4]), "=&s"(w.v[5]),
+        "=&s"(w.v[6]), "=&s"(w.v[7])
+      : "s"(w.kp));
+}
+
+// The destinations of the loads above stay reserved until this wait (they are
+// its inputs), so nothing else lands in a register a load is still writing.
+__device__ inline const WaveKernArgs* warm_kernargs_wait(KernArgWarm& w) {
+  __asm__ __volatile__("s_waitcnt lgkmcnt(0)"
+                       : "+s"(w.kp)
+                       : "s"(w.v[0]), "s"(w.v[1]), "s"(w.v[2]), "s"(w.v[3]), "s"(w.v[4]), "s"(w.v[5]),
+                         "s"(w.v[6]), "s"(w.v[7]));
+  return (const WaveKernArgs*)w.kp;
 }
 
 // The next pass's bucket counters and, in fused mode, its control block.
@@ -1320,18 +1353,20 @@ __device__ inline void clear_for_next_pass(const SweepArgs& a) {
 // Each wave folds its slack range and ready count into one of the control
 // block's partial slots.
 template <int NPTW, bool kFused>
-__global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a_arg, int wcap_arg) {
+__global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
+    const int32_t* inst_type, const int32_t* inst_speed, const int64_t* inst_load, const int64_t* deadline,
+    const int32_t* wf, int64_t N, int32_t W, int32_t M_, SweepArgs a_arg, int wcap_arg) {
   (void)a_arg;
   (void)wcap_arg;
-  const WaveKernArgs* kargs = warm_kernargs();  // the same two arguments, read after the warm-up
-  const SweepArgs& a = kargs->a;
-  const int wcap = kargs->wcap;
+  // scalar arguments (an aggregate is not preloaded); the same fields as WaveHead
+  const WaveHead h{inst_type, inst_speed, inst_load, deadline, wf, N, W, M_};
+  KernArgWarm warm;
+  warm_kernargs_issue(warm);
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ Shared S;
   __shared__ __align__(16) int32_t s_itype[kWaveItabMax];
   __shared__ int s_big[kWavesPerBlock];
-  Ctrl* ctrl = a.ctrl;
-  const int M = int(a.p.M);
+  const int M = h.M;
   const int tid = threadIdx.x;
   const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);  // wave-uniform: scalar registers
   const int ln = lane_id();
@@ -1340,12 +1375,8 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a_arg, int 
   const int64_t gw = int64_t(blockIdx.x) * kWavesPerBlock + wv;
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
 
-  // one round trip: validation status, this wave's first workflow, the
-  // instance table (every load is issued before any is used)
-  // (fused: nothing ran before this kernel in the pass; otherwise written by
-  // earlier kernels only, so a plain load sees it; an uncached load of one
-  // word by every wave would queue at the memory controller)
-  const uint32_t status = kFused ? 0u : ctrl->status;
+  // one round trip, from the preloaded arguments: this wave's first workflow
+  // (fused) and the instance table; every load is issued before any is used
   int64_t b0 = 0, dl0 = 0, raw0 = 0;
   int n0 = 0;
   int32_t it_t = 0, it_sp = 1, spec_before = INT32_MIN, spec_at = INT32_MAX;
@@ -1354,23 +1385,34 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a_arg, int 
   if (kFused) {
     const int ie = wave_itab ? ln : tid;  // the instance this thread loads
     if (ie < M) {
-      it_t = a.p.inst_type[ie];
-      it_sp = a.p.inst_speed[ie];
-      it_ld = a.p.inst_load[ie];
+      it_t = h.inst_type[ie];
+      it_sp = h.inst_speed[ie];
+      it_ld = h.inst_load[ie];
     }
-    if (gw < a.p.W) {
-      raw0 = a.p.deadline[gw];
+    if (gw < h.W) {
+      raw0 = h.deadline[gw];
       if (ln < 2) {  // speculative lower bounds of gw and gw + 1 (lanes 0 and 1)
-        spec_g = ((gw + ln) * a.p.N) / a.p.W;
-        if (spec_g >= 1) spec_before = a.p.wf[spec_g - 1];
-        if (spec_g < a.p.N) spec_at = a.p.wf[spec_g];
+        spec_g = ((gw + ln) * h.N) / h.W;
+        if (spec_g >= 1) spec_before = h.wf[spec_g - 1];
+        if (spec_g < h.N) spec_at = h.wf[spec_g];
       }
     }
-    if (gw == 0 && ln == 0) {
-      off_first = a.p.dep_off[0];
-      off_last = a.p.dep_off[a.p.N];
-    }
-  } else if (gw < a.p.W) {
+  }
+  const WaveKernArgs* kargs = warm_kernargs_wait(warm);  // the rest, read after the warm-up
+  const SweepArgs& a = kargs->a;
+  const int wcap = kargs->wcap;
+  // the offsets' first and last entries (checked at the end: every future's
+  // own offsets are checked where they are used, so nothing waits for these)
+  if (kFused && gw == 0 && ln == 0) {
+    off_first = a.p.dep_off[0];
+    off_last = a.p.dep_off[a.p.N];
+  }
+  Ctrl* ctrl = a.ctrl;
+  // (fused: nothing ran before this kernel in the pass; otherwise written by
+  // earlier kernels only, so a plain load sees it; an uncached load of one
+  // word by every wave would queue at the memory controller)
+  const uint32_t status = kFused ? 0u : ctrl->status;
+  if (!kFused && gw < a.p.W) {
     wf_bounds(a, gw, b0, n0);
     raw0 = a.p.deadline[gw];
   }
@@ -1392,8 +1434,6 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a_arg, int 
   Wv.nr = sp + size_t(wv) * wcap;
   if (kFused) {
     if ((wave_itab ? ln : tid) < M && ((it_t < 0) | (it_sp < 1) | (it_ld < 0) | (it_ld > NALAR_LOAD_MAX)))
-      flag_sweep(ctrl, kStInval);
-    if (gw == 0 && ln == 0 && (off_first != 0 || int64_t(off_last) != a.p.E))
       flag_sweep(ctrl, kStInval);
     if (gw < a.p.W) {
       // workflow bounds: the speculative guess, else a search (lanes 0 and 1)
@@ -1489,6 +1529,8 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(SweepArgs a_arg, int 
     }
   }
 
+  if (kFused && gw == 0 && ln == 0 && (off_first != 0 || int64_t(off_last) != a.p.E))
+    flag_sweep(ctrl, kStInval);
   const int64_t mn = wave_min_i64(acc.tmin);
   const int64_t mxv = wave_max_i64(acc.tmax);
   const int64_t rd = wave_sum_i64(acc.tready);
@@ -1563,6 +1605,13 @@ hipError_t prepare_sweep_kernels(size_t lds_limit) {
   return hipSuccess;
 }
 
+// The wave kernel with its preloaded leading arguments taken from a.
+template <int NPTW, bool kFused>
+void launch_wave(hipStream_t s, dim3 g, dim3 t, size_t lds, const SweepArgs& a, int cap) {
+  hipLaunchKernelGGL((k_sweep_wave<NPTW, kFused>), g, t, lds, s, a.p.inst_type, a.p.inst_speed,
+                     a.p.inst_load, a.p.deadline, a.p.wf, a.p.N, int32_t(a.p.W), int32_t(a.p.M), a, cap);
+}
+
 hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const SweepShape& sh) {
   if (sh.threads == kWaveBlock) {
     // futures per lane = slice capacity / 64 (a power of two up to kWaveNpt)
@@ -1571,17 +1620,17 @@ hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const SweepShape& sh)
     const int cap = sh.lds_cap;
     if (a.fused) {
       switch (sh.npt) {
-        case 1: hipLaunchKernelGGL((k_sweep_wave<1, true>), g, t, lds, s, a, cap); break;
-        case 2: hipLaunchKernelGGL((k_sweep_wave<2, true>), g, t, lds, s, a, cap); break;
-        case 4: hipLaunchKernelGGL((k_sweep_wave<4, true>), g, t, lds, s, a, cap); break;
-        default: hipLaunchKernelGGL((k_sweep_wave<kWaveNpt, true>), g, t, lds, s, a, cap); break;
+        case 1: launch_wave<1, true>(s, g, t, lds, a, cap); break;
+        case 2: launch_wave<2, true>(s, g, t, lds, a, cap); break;
+        case 4: launch_wave<4, true>(s, g, t, lds, a, cap); break;
+        default: launch_wave<kWaveNpt, true>(s, g, t, lds, a, cap); break;
       }
     } else {
       switch (sh.npt) {
-        case 1: hipLaunchKernelGGL((k_sweep_wave<1, false>), g, t, lds, s, a, cap); break;
-        case 2: hipLaunchKernelGGL((k_sweep_wave<2, false>), g, t, lds, s, a, cap); break;
-        case 4: hipLaunchKernelGGL((k_sweep_wave<4, false>), g, t, lds, s, a, cap); break;
-        default: hipLaunchKernelGGL((k_sweep_wave<kWaveNpt, false>), g, t, lds, s, a, cap); break;
+        case 1: launch_wave<1, false>(s, g, t, lds, a, cap); break;
+        case 2: launch_wave<2, false>(s, g, t, lds, a, cap); break;
+        case 4: launch_wave<4, false>(s, g, t, lds, a, cap); break;
+        default: launch_wave<kWaveNpt, false>(s, g, t, lds, a, cap); break;
       }
     }
   } else
