@@ -924,6 +924,15 @@ __device__ __attribute__((always_inline)) inline void rounds(
   }
 }
 
+// Attributes of future spec + lane loaded before the workflow's bounds are
+// known, spec being the bound that equal workflow sizes would give (the
+// fused one-future-per-lane wave sweep; valid when the bound turns out so).
+struct PreAttr {
+  int64_t e = 0;
+  int32_t o0 = 0, o1 = 0, t = 0, l = -1, wfv = -1;
+  uint8_t d = 1;
+};
+
 // Sweep of one workflow by one wave.  Lane l owns futures l, l+64, ... of the
 // workflow and keeps their estimate and (up to three) dependencies in
 // registers.  Each round, every owned future whose consumers are all finalised
@@ -935,8 +944,7 @@ __device__ __attribute__((always_inline)) inline void rounds(
 template <int NPTW, bool kFused>
 __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& it,
                            const WaveSlice& W, int64_t w, int64_t b, int n, int64_t dl, int64_t kofs,
-                           Acc& acc,
-                           ItabStage& st) {
+                           Acc& acc, ItabStage& st, const PreAttr& pre, bool use_pre) {
   const int ln = lane_id();
   Ctrl* ctrl = a.ctrl;
   int32_t vv[NPTW], ty[NPTW], lc[NPTW], off[NPTW], deg[NPTW];
@@ -953,14 +961,28 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
     if (k < n) {
       own |= 1u << j;
       const int32_t v = node_at(L, b + k);
-      uint8_t d = a.p.done[v];
-      int32_t o0 = a.p.dep_off[v];
-      int32_t o1 = a.p.dep_off[v + 1];
-      int32_t t = a.p.type[v];
-      int32_t l = a.p.loc[v];
-      int64_t e = a.p.est[v];
+      uint8_t d;
+      int32_t o0, o1, t, l, wfv = 0;
+      int64_t e;
+      if (NPTW == 1 && kFused && use_pre) {  // loaded ahead (the same future: b is the guess)
+        d = pre.d;
+        o0 = pre.o0;
+        o1 = pre.o1;
+        t = pre.t;
+        l = pre.l;
+        e = pre.e;
+        wfv = pre.wfv;
+      } else {
+        d = a.p.done[v];
+        o0 = a.p.dep_off[v];
+        o1 = a.p.dep_off[v + 1];
+        t = a.p.type[v];
+        l = a.p.loc[v];
+        e = a.p.est[v];
+        if (kFused) wfv = a.p.wf[v];
+      }
       if (kFused) {  // the rules of nalar_problem for this future
-        const bool bad = (a.p.wf[v] != w) | (t < 0) | (l < -1) | (int64_t(l) >= a.p.M) | (e < 0) |
+        const bool bad = (wfv != w) | (t < 0) | (l < -1) | (int64_t(l) >= a.p.M) | (e < 0) |
                          (e > NALAR_EST_MAX) | (d > 1) | (o0 < 0) | (o1 < o0) | (int64_t(o1) > a.p.E);
         if (bad) {  // reported; neutralised so that no access leaves its array
           flag_sweep(ctrl, kStInval);
@@ -1380,7 +1402,7 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
   int64_t b0 = 0, dl0 = 0, raw0 = 0;
   int n0 = 0;
   int32_t it_t = 0, it_sp = 1, spec_before = INT32_MIN, spec_at = INT32_MAX;
-  int64_t it_ld = 0, spec_g = 0;
+  int64_t it_ld = 0, spec_g = 0, spec_lo = 0, spec_hi = 0;
   int32_t off_first = 0, off_last = 0;
   if (kFused) {
     const int ie = wave_itab ? ln : tid;  // the instance this thread loads
@@ -1391,8 +1413,11 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
     }
     if (gw < h.W) {
       raw0 = h.deadline[gw];
+      // bounds that equal workflow sizes would give (the same on every lane)
+      spec_lo = (gw * h.N) / h.W;
+      spec_hi = ((gw + 1) * h.N) / h.W;
       if (ln < 2) {  // speculative lower bounds of gw and gw + 1 (lanes 0 and 1)
-        spec_g = ((gw + ln) * h.N) / h.W;
+        spec_g = ln == 0 ? spec_lo : spec_hi;
         if (spec_g >= 1) spec_before = h.wf[spec_g - 1];
         if (spec_g < h.N) spec_at = h.wf[spec_g];
       }
@@ -1401,6 +1426,19 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
   const WaveKernArgs* kargs = warm_kernargs_wait(warm);  // the rest, read after the warm-up
   const SweepArgs& a = kargs->a;
   const int wcap = kargs->wcap;
+  // one future per lane: the first workflow's attributes at the guessed
+  // bound, in flight with the bound checks instead of after them
+  PreAttr pre;
+  if (kFused && NPTW == 1 && gw < h.W && spec_lo + ln < h.N) {
+    const int64_t v = spec_lo + ln;
+    pre.d = a.p.done[v];
+    pre.o0 = a.p.dep_off[v];
+    pre.o1 = a.p.dep_off[v + 1];
+    pre.t = a.p.type[v];
+    pre.l = a.p.loc[v];
+    pre.e = a.p.est[v];
+    pre.wfv = a.p.wf[v];
+  }
   // the offsets' first and last entries (checked at the end: every future's
   // own offsets are checked where they are used, so nothing waits for these)
   if (kFused && gw == 0 && ln == 0) {
@@ -1507,7 +1545,7 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
       big = true;
       continue;
     }
-    sweep_wave<NPTW, kFused>(a, L, it, Wv, w, b, n, dl, kofs, acc, st);
+    sweep_wave<NPTW, kFused>(a, L, it, Wv, w, b, n, dl, kofs, acc, st, pre, w == gw && b == spec_lo);
   }
   if (ln == 0) s_big[wv] = big ? 1 : 0;
   __syncthreads();
