@@ -163,6 +163,7 @@ struct SweepShape {
   size_t lds_bytes;
   int blocks;
   int wave_path;      // one wave per workflow (k_sweep_wave)
+  int group = 1;      // wave path: consecutive workflows swept together by one wave
 };
 SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t lds_limit);
 hipError_t prepare_sweep_kernels(size_t lds_limit);

@@ -81,6 +81,19 @@ __device__ inline int32_t checked_dep(const Layout& L, int32_t p, int64_t b, int
   return lp;
 }
 
+// A dependency that must also lie in the workflow's own part [lo, hi) of a
+// slice holding several workflows (a dependency on another workflow of the
+// slice is one outside the future's workflow).
+__device__ inline int32_t checked_dep_seg(const Layout& L, int32_t p, int64_t b, int n, int lo, int hi,
+                                          int k, Ctrl* ctrl) {
+  const int32_t lp = checked_dep(L, p, b, n, k, ctrl);
+  if (lp >= 0 && (lp < lo || lp >= hi)) {
+    flag_sweep(ctrl, kStInval);
+    return -1;
+  }
+  return lp;
+}
+
 // ---------------------------------------------------------------- LDS atomics
 
 __device__ inline void agg_count_lds(int32_t* cnt, int lp) {
@@ -924,6 +937,28 @@ __device__ __attribute__((always_inline)) inline void rounds(
   }
 }
 
+// The workflows one wave sweeps together: ns consecutive workflows w[0] ..
+// occupying positions [b, b + n), workflow i at local indices [c[i], c[i+1])
+// (c[0] = 0, c[ns] = n), with their deadlines (less now) and key offsets.
+// Every field is the same on every lane.
+template <int G>
+struct Seg {
+  int64_t b;
+  int n;
+  int ns;
+  int c[G + 1];
+  int64_t w[G];
+  int64_t dl[G];
+  int64_t kofs[G];
+  // the part of local index k
+  __device__ int part(int k) const {
+    int s = 0;
+#pragma unroll
+    for (int i = 1; i < G; ++i) s += (i < ns && k >= c[i]) ? 1 : 0;
+    return s;
+  }
+};
+
 // Attributes of future spec + lane loaded before the workflow's bounds are
 // known, spec being the bound that equal workflow sizes would give (the
 // fused one-future-per-lane wave sweep; valid when the bound turns out so).
@@ -941,10 +976,12 @@ struct PreAttr {
 // nothing, so a round costs one LDS round trip (the counter and running-max
 // reads) however many futures it finalises.  Futures with more dependencies
 // are pushed by the whole wave from the dependency list.
-template <int NPTW, bool kFused>
+template <int NPTW, bool kFused, int G>
 __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, const Layout& L, const ITabLds& it,
-                           const WaveSlice& W, int64_t w, int64_t b, int n, int64_t dl, int64_t kofs,
-                           Acc& acc, ItabStage& st, const PreAttr& pre, bool use_pre) {
+                           const WaveSlice& W, const Seg<G>& sg, Acc& acc, ItabStage& st,
+                           const PreAttr& pre, bool use_pre) {
+  const int64_t b = sg.b;
+  const int n = sg.n;
   const int ln = lane_id();
   Ctrl* ctrl = a.ctrl;
   int32_t vv[NPTW], ty[NPTW], lc[NPTW], off[NPTW], deg[NPTW];
@@ -982,7 +1019,7 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
         if (kFused) wfv = a.p.wf[v];
       }
       if (kFused) {  // the rules of nalar_problem for this future
-        const bool bad = (wfv != w) | (t < 0) | (l < -1) | (int64_t(l) >= a.p.M) | (e < 0) |
+        const bool bad = (wfv != sg.w[sg.part(k)]) | (t < 0) | (l < -1) | (int64_t(l) >= a.p.M) | (e < 0) |
                          (e > NALAR_EST_MAX) | (d > 1) | (o0 < 0) | (o1 < o0) | (int64_t(o1) > a.p.E);
         if (bad) {  // reported; neutralised so that no access leaves its array
           flag_sweep(ctrl, kStInval);
@@ -1017,7 +1054,14 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
 #pragma unroll
     for (int q = 0; q < kPmax; ++q) {
       int32_t lp = -1;
-      if (light && q < deg[j]) lp = checked_dep(L, a.p.dep_idx[off[j] + q], b, n, k, ctrl);
+      if (light && q < deg[j]) {
+        if (G == 1) {
+          lp = checked_dep(L, a.p.dep_idx[off[j] + q], b, n, k, ctrl);
+        } else {
+          const int pk = sg.part(k);
+          lp = checked_dep_seg(L, a.p.dep_idx[off[j] + q], b, n, sg.c[pk], sg.c[pk + 1], k, ctrl);
+        }
+      }
       packed[q] = lp >= 0 ? uint32_t(lp) : kNoDep;
       if (lp >= 0) {
         atomicAdd(&W.cnt[lp], 1);
@@ -1035,11 +1079,13 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
       const int kh = j * kWave + src;
       const int o = readlane_i32(off[j], src);
       const int d = readlane_i32(deg[j], src);
+      const int ph = sg.part(kh);
       bool blk = false;
       for (int e0 = 0; e0 < d; e0 += kWave) {
         const int e = e0 + ln;
         if (e < d) {
-          const int32_t lp = checked_dep(L, a.p.dep_idx[o + e], b, n, kh, ctrl);
+          const int32_t lp = G == 1 ? checked_dep(L, a.p.dep_idx[o + e], b, n, kh, ctrl)
+                                    : checked_dep_seg(L, a.p.dep_idx[o + e], b, n, sg.c[ph], sg.c[ph + 1], kh, ctrl);
           if (lp >= 0) {
             atomicAdd(&W.cnt[lp], 1);
             blk |= W.dn[lp] == 0;
@@ -1090,7 +1136,8 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
     bkt[j] = 0;
     slot[j] = 0;
     if (bk.nb > 0 && ((ready >> j) & 1u)) {
-      bkt[j] = bucket_of<true>(bk, order_key(a, rr[j], dl, kofs), kofs);
+      const int pk = sg.part(j * kWave + ln);
+      bkt[j] = bucket_of<true>(bk, order_key(a, rr[j], sg.dl[pk], sg.kofs[pk]), sg.kofs[pk]);
       slot[j] = add_agent(bk.cnt + bkt[j], 1u);
     }
   }
@@ -1113,9 +1160,12 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
     const int64_t pos = b + j * kWave + ln;
     if (bk.nb == 0) a.stg_ready[pos] = uint8_t((ready >> j) & 1u);
     if (a.rem_out) a.rem_out[vv[j]] = rr[j];
-    if ((ready >> j) & 1u)
+    if ((ready >> j) & 1u) {
+      const int pk = sg.part(j * kWave + ln);
+      const int64_t dl = sg.dl[pk], kofs = sg.kofs[pk];
       store_ready(a, bkt[j], slot[j], order_key(a, rr[j], dl, kofs), kofs, dl - rr[j], pos, route[j],
                   cost[j], acc);
+    }
   }
   wave_order();
 }
@@ -1369,12 +1419,74 @@ __device__ inline void clear_for_next_pass(const SweepArgs& a) {
   if (kFused) reset_ctrl_spread(a.next_ctrl, gi, gstride);
 }
 
+// Bounds of group pw (workflows pw*G .. pw*G + G - 1): lane i <= G gets the
+// first position of workflow pw*G + i (N past the last workflow), lane i < G
+// that workflow's raw deadline.
+template <int G>
+__device__ inline void group_bounds(const SweepArgs& a, int64_t pw, int32_t& lbv, int64_t& rawv) {
+  const int ln = lane_id();
+  const int64_t W = a.p.W, N = a.p.N;
+  const int64_t key = pw * G + ln < W ? pw * G + ln : W;
+  lbv = 0;
+  rawv = 0;
+  if (ln <= G) {
+    if (a.fused)
+      lbv = key >= W ? int32_t(N) : int32_t(lower_bound_from(a.p.wf, N, key, (key * N) / W));
+    else
+      lbv = a.wf_off[key];
+  }
+  if (ln < G && pw * G + ln < W) rawv = a.p.deadline[pw * G + ln];
+}
+
+// The group's segment description from the per-lane bounds and deadlines, and
+// (fused mode) the rules of nalar_problem for its workflows: the ranges tile
+// [0, N) in workflow order, deadlines within the horizon, levels up to 15.
+template <int G, bool kFused>
+__device__ inline Seg<G> make_seg(const SweepArgs& a, int64_t pw, int32_t lbv, int64_t rawv, Ctrl* ctrl) {
+  const int ln = lane_id();
+  const int64_t W = a.p.W;
+  Seg<G> sg;
+  const int64_t w0 = pw * G;
+  sg.ns = int(W - w0 < G ? W - w0 : G);
+  int32_t lb[G + 1];
+#pragma unroll
+  for (int i = 0; i <= G; ++i) lb[i] = readlane_i32(lbv, i);
+  sg.b = lb[0];
+  sg.n = lb[sg.ns] - lb[0];
+#pragma unroll
+  for (int i = 0; i <= G; ++i) sg.c[i] = (i <= sg.ns ? lb[i] : lb[sg.ns]) - lb[0];
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    sg.w[i] = w0 + i;
+    sg.dl[i] = readlane_i64(rawv, i) - a.p.now;
+    sg.kofs[i] = i < sg.ns ? prio_offset(a, w0 + i) : 0;
+  }
+  if (kFused && ln < sg.ns) {
+    const int64_t w = w0 + ln;
+    int32_t lo = 0, hi = 0;
+#pragma unroll
+    for (int i = 0; i < G; ++i)
+      if (ln == i) {
+        lo = lb[i];
+        hi = lb[i + 1];
+      }
+    if ((hi < lo) | ((w == 0) & (lo != 0)) | ((w == W - 1) & (int64_t(hi) != a.p.N)) |
+        (rawv < a.p.now - NALAR_HORIZON_MAX) | (rawv > a.p.now + NALAR_HORIZON_MAX) |
+        (a.p.prio != nullptr && a.p.prio[w] > NALAR_PRIORITY_MAX))
+      flag_sweep(ctrl, kStInval);
+  }
+  return sg;
+}
+
 // Small workflows: one wave each, no workgroup barrier on the way (fused mode:
-// after the instance table is built).  Workflows larger than a wave's slice
-// (wcap futures) are swept at the end by whole workgroups with HBM state.
-// Each wave folds its slack range and ready count into one of the control
-// block's partial slots.
-template <int NPTW, bool kFused>
+// after the instance table is built).  With G > 1 a wave takes G consecutive
+// workflows and sweeps them together as one slice of at most wcap futures
+// (their DAGs are disjoint, so the rounds run side by side: half-empty waves
+// of 32-future workflows become full ones), else one at a time.  Workflows
+// larger than a wave's slice (wcap futures) are swept at the end by whole
+// workgroups with HBM state.  Each wave folds its slack range and ready count
+// into one of the control block's partial slots.
+template <int NPTW, bool kFused, int G>
 __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
     const int32_t* inst_type, const int32_t* inst_speed, const int64_t* inst_load, const int64_t* deadline,
     const int32_t* wf, int64_t N, int32_t W, int32_t M_, SweepArgs a_arg, int wcap_arg) {
@@ -1397,12 +1509,12 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
   const int64_t gw = int64_t(blockIdx.x) * kWavesPerBlock + wv;
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
 
-  // one round trip, from the preloaded arguments: this wave's first workflow
-  // (fused) and the instance table; every load is issued before any is used
-  int64_t b0 = 0, dl0 = 0, raw0 = 0;
-  int n0 = 0;
+  // one round trip, from the preloaded arguments: this wave's first group of
+  // workflows (fused) and the instance table; every load is issued before any
+  // is used
+  int64_t raw0 = 0;
   int32_t it_t = 0, it_sp = 1, spec_before = INT32_MIN, spec_at = INT32_MAX;
-  int64_t it_ld = 0, spec_g = 0, spec_lo = 0, spec_hi = 0;
+  int64_t it_ld = 0, spec_g = 0, spec_lo = 0;
   int32_t off_first = 0, off_last = 0;
   if (kFused) {
     const int ie = wave_itab ? ln : tid;  // the instance this thread loads
@@ -1411,16 +1523,17 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
       it_sp = h.inst_speed[ie];
       it_ld = h.inst_load[ie];
     }
-    if (gw < h.W) {
-      raw0 = h.deadline[gw];
-      // bounds that equal workflow sizes would give (the same on every lane)
-      spec_lo = (gw * h.N) / h.W;
-      spec_hi = ((gw + 1) * h.N) / h.W;
-      if (ln < 2) {  // speculative lower bounds of gw and gw + 1 (lanes 0 and 1)
-        spec_g = ln == 0 ? spec_lo : spec_hi;
+    if (gw * G < h.W) {
+      if (ln < G && gw * G + ln < h.W) raw0 = h.deadline[gw * G + ln];
+      // bounds that equal workflow sizes would give: lane i <= G guesses the
+      // first position of workflow gw*G + i and loads the ids around it
+      const int64_t key = gw * G + ln < h.W ? gw * G + ln : int64_t(h.W);
+      if (ln <= G) {
+        spec_g = (key * h.N) / h.W;
         if (spec_g >= 1) spec_before = h.wf[spec_g - 1];
         if (spec_g < h.N) spec_at = h.wf[spec_g];
       }
+      spec_lo = readlane_i64(spec_g, 0);
     }
   }
   const WaveKernArgs* kargs = warm_kernargs_wait(warm);  // the rest, read after the warm-up
@@ -1450,11 +1563,8 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
   // earlier kernels only, so a plain load sees it; an uncached load of one
   // word by every wave would queue at the memory controller)
   const uint32_t status = kFused ? 0u : ctrl->status;
-  if (!kFused && gw < a.p.W) {
-    wf_bounds(a, gw, b0, n0);
-    raw0 = a.p.deadline[gw];
-  }
-  dl0 = raw0 - a.p.now;
+  int32_t lb0 = 0;  // lane i <= G: first position of workflow gw*G + i
+  if (!kFused && gw * G < a.p.W) group_bounds<G>(a, gw, lb0, raw0);
   ItabStage st;
   st.pending = false;
   st.build = false;
@@ -1473,22 +1583,12 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
   if (kFused) {
     if ((wave_itab ? ln : tid) < M && ((it_t < 0) | (it_sp < 1) | (it_ld < 0) | (it_ld > NALAR_LOAD_MAX)))
       flag_sweep(ctrl, kStInval);
-    if (gw < a.p.W) {
-      // workflow bounds: the speculative guess, else a search (lanes 0 and 1)
-      int32_t lb = 0;
-      if (ln < 2) {
-        const int64_t key = gw + ln;
-        const bool ok = (spec_g == 0 || int64_t(spec_before) < key) &&
-                        (spec_g >= a.p.N || int64_t(spec_at) >= key);
-        lb = ok ? int32_t(spec_g) : int32_t(lower_bound_from(a.p.wf, a.p.N, key, spec_g));
-      }
-      const int32_t lo = readlane_i32(lb, 0), hi = readlane_i32(lb, 1);
-      b0 = lo;
-      n0 = hi - lo;
-      if (ln == 0 && ((n0 < 0) | ((gw == 0) & (lo != 0)) | ((gw == a.p.W - 1) & (int64_t(hi) != a.p.N)) |
-                      (raw0 < a.p.now - NALAR_HORIZON_MAX) | (raw0 > a.p.now + NALAR_HORIZON_MAX) |
-                      (a.p.prio != nullptr && a.p.prio[gw] > NALAR_PRIORITY_MAX)))
-        flag_sweep(ctrl, kStInval);
+    if (gw * G < a.p.W && ln <= G) {
+      // workflow bounds: the speculative guess, else a search (lanes 0 .. G)
+      const int64_t key = gw * G + ln < a.p.W ? gw * G + ln : a.p.W;
+      const bool ok = (spec_g == 0 || int64_t(spec_before) < key) &&
+                      (spec_g >= a.p.N || int64_t(spec_at) >= key);
+      lb0 = ok ? int32_t(spec_g) : int32_t(lower_bound_from(a.p.wf, a.p.N, key, spec_g));
     }
     if (wave_itab) {
       st.type[0] = it_t;
@@ -1525,35 +1625,52 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
   Acc acc;
   bool big = false;
   uint32_t lmask = 0;  // priority levels of the wave's workflows
-  for (int64_t w = gw; w < a.p.W; w += nwaves) {
-    int64_t b = b0;
-    int n = n0;
-    int64_t dl = dl0;
-    if (w != gw) {
-      wf_bounds(a, w, b, n);
-      const int64_t raw = a.p.deadline[w];
-      dl = raw - a.p.now;
-      if (kFused && ln == 0 &&
-          ((raw < a.p.now - NALAR_HORIZON_MAX) | (raw > a.p.now + NALAR_HORIZON_MAX) |
-           (a.p.prio != nullptr && a.p.prio[w] > NALAR_PRIORITY_MAX)))
-        flag_sweep(ctrl, kStInval);
+  for (int64_t pw = gw; pw * G < a.p.W; pw += nwaves) {
+    int32_t lbv = lb0;
+    int64_t rawv = raw0;
+    if (pw != gw) group_bounds<G>(a, pw, lbv, rawv);
+    Seg<G> sg = make_seg<G, kFused>(a, pw, lbv, rawv, ctrl);
+    bool any = false, gbig = false;  // a workflow of the group to sweep here / in HBM
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      const int ni = sg.c[i + 1] - sg.c[i];
+      if (i < sg.ns && ni > 0) {
+        lmask |= level_bit(sg.kofs[i]);
+        if (ni > wcap || a.force_global) gbig = true;
+        else any = true;
+      }
     }
-    if (n <= 0) continue;
-    const int64_t kofs = prio_offset(a, w);
-    lmask |= level_bit(kofs);
-    if (n > wcap || a.force_global) {
-      big = true;
+    big |= gbig;
+    if (!any) continue;
+    const bool use_pre = pw == gw && sg.b == spec_lo;
+    if (!gbig && sg.n <= wcap) {  // the whole group in one slice
+      sweep_wave<NPTW, kFused, G>(a, L, it, Wv, sg, acc, st, pre, use_pre);
       continue;
     }
-    sweep_wave<NPTW, kFused>(a, L, it, Wv, w, b, n, dl, kofs, acc, st, pre, w == gw && b == spec_lo);
+    // one workflow at a time (a group too large for one slice)
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      const int ni = sg.c[i + 1] - sg.c[i];
+      if (i >= sg.ns || ni <= 0 || ni > wcap || a.force_global) continue;
+      Seg<G> one = sg;
+      one.b = sg.b + sg.c[i];
+      one.n = ni;
+      one.ns = 1;
+      one.c[0] = 0;
+      one.c[1] = ni;
+      one.w[0] = sg.w[i];
+      one.dl[0] = sg.dl[i];
+      one.kofs[0] = sg.kofs[i];
+      sweep_wave<NPTW, kFused, G>(a, L, it, Wv, one, acc, st, pre, use_pre && i == 0);
+    }
   }
   if (ln == 0) s_big[wv] = big ? 1 : 0;
   __syncthreads();
   if (s_big[0] | s_big[1] | s_big[2] | s_big[3]) {  // the workgroup's large workflows (HBM state)
     itab_stage_store(st, it, M, ln);
     __syncthreads();
-    for (int64_t base = int64_t(blockIdx.x) * kWavesPerBlock; base < a.p.W; base += nwaves) {
-      for (int i = 0; i < kWavesPerBlock; ++i) {
+    for (int64_t base = int64_t(blockIdx.x) * kWavesPerBlock * G; base < a.p.W; base += nwaves * G) {
+      for (int i = 0; i < kWavesPerBlock * G; ++i) {
         const int64_t w = base + i;
         if (w >= a.p.W) break;
         int64_t b;
@@ -1600,7 +1717,9 @@ SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t ld
     s.lds_cap = int(wcap);
     s.lds_bytes = itab_lds_wave(M) + kWaveSliceBytesPerFuture * size_t(kWavesPerBlock) * size_t(wcap) + 16;
     s.wave_path = 1;
-    int64_t blocks = (W + kWavesPerBlock - 1) / kWavesPerBlock;
+    // workflows of up to 32 futures on average: two per wave, side by side
+    s.group = (wcap == kWave && 2 * avg <= kWave) ? 2 : 1;
+    int64_t blocks = (W + int64_t(kWavesPerBlock) * s.group - 1) / (int64_t(kWavesPerBlock) * s.group);
     const int64_t most = int64_t(device_cus) * 8;
     if (blocks > most) blocks = most;
     s.blocks = int(blocks < 1 ? 1 : blocks);
@@ -1629,14 +1748,16 @@ hipError_t prepare_sweep_kernels(size_t lds_limit) {
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sweep<kBlockT, kBlockNpt>),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(dyn));
   if (e != hipSuccess) return e;
-  for (const void* k : {reinterpret_cast<const void*>(&k_sweep_wave<1, false>),
-                        reinterpret_cast<const void*>(&k_sweep_wave<2, false>),
-                        reinterpret_cast<const void*>(&k_sweep_wave<4, false>),
-                        reinterpret_cast<const void*>(&k_sweep_wave<8, false>),
-                        reinterpret_cast<const void*>(&k_sweep_wave<1, true>),
-                        reinterpret_cast<const void*>(&k_sweep_wave<2, true>),
-                        reinterpret_cast<const void*>(&k_sweep_wave<4, true>),
-                        reinterpret_cast<const void*>(&k_sweep_wave<8, true>)}) {
+  for (const void* k : {reinterpret_cast<const void*>(&k_sweep_wave<1, false, 1>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<1, false, 2>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<2, false, 1>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<4, false, 1>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<8, false, 1>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<1, true, 1>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<1, true, 2>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<2, true, 1>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<4, true, 1>),
+                        reinterpret_cast<const void*>(&k_sweep_wave<8, true, 1>)}) {
     e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, int(dyn));
     if (e != hipSuccess) return e;
   }
@@ -1644,9 +1765,9 @@ hipError_t prepare_sweep_kernels(size_t lds_limit) {
 }
 
 // The wave kernel with its preloaded leading arguments taken from a.
-template <int NPTW, bool kFused>
+template <int NPTW, bool kFused, int G = 1>
 void launch_wave(hipStream_t s, dim3 g, dim3 t, size_t lds, const SweepArgs& a, int cap) {
-  hipLaunchKernelGGL((k_sweep_wave<NPTW, kFused>), g, t, lds, s, a.p.inst_type, a.p.inst_speed,
+  hipLaunchKernelGGL((k_sweep_wave<NPTW, kFused, G>), g, t, lds, s, a.p.inst_type, a.p.inst_speed,
                      a.p.inst_load, a.p.deadline, a.p.wf, a.p.N, int32_t(a.p.W), int32_t(a.p.M), a, cap);
 }
 
@@ -1658,14 +1779,20 @@ hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const SweepShape& sh)
     const int cap = sh.lds_cap;
     if (a.fused) {
       switch (sh.npt) {
-        case 1: launch_wave<1, true>(s, g, t, lds, a, cap); break;
+        case 1:
+          if (sh.group == 2) launch_wave<1, true, 2>(s, g, t, lds, a, cap);
+          else launch_wave<1, true>(s, g, t, lds, a, cap);
+          break;
         case 2: launch_wave<2, true>(s, g, t, lds, a, cap); break;
         case 4: launch_wave<4, true>(s, g, t, lds, a, cap); break;
         default: launch_wave<kWaveNpt, true>(s, g, t, lds, a, cap); break;
       }
     } else {
       switch (sh.npt) {
-        case 1: launch_wave<1, false>(s, g, t, lds, a, cap); break;
+        case 1:
+          if (sh.group == 2) launch_wave<1, false, 2>(s, g, t, lds, a, cap);
+          else launch_wave<1, false>(s, g, t, lds, a, cap);
+          break;
         case 2: launch_wave<2, false>(s, g, t, lds, a, cap); break;
         case 4: launch_wave<4, false>(s, g, t, lds, a, cap); break;
         default: launch_wave<kWaveNpt, false>(s, g, t, lds, a, cap); break;

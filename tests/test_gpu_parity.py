@@ -385,6 +385,64 @@ def test_greedy_candidate_counts(policy, n_inst):
     check(policy, q, f"greedy {n_inst} tied candidates", policy=G)
 
 
+def _sized_workflows(sizes, seed, heavy_every=7):
+    """Contiguous workflows of the given sizes; every future depends on up to
+    three earlier futures of its workflow, every heavy_every-th on up to six."""
+    rng = np.random.default_rng(seed)
+    W = len(sizes)
+    wf = np.repeat(np.arange(W, dtype=np.int32), sizes)
+    starts = np.concatenate([[0], np.cumsum(sizes)])
+    counts, flat = [], []
+    for w in range(W):
+        for i in range(sizes[w]):
+            cap = 6 if i % heavy_every == heavy_every - 1 else 3
+            k = int(rng.integers(0, min(i, cap) + 1))
+            par = rng.choice(i, size=k, replace=False) if k else []
+            counts.append(k)
+            flat.extend(int(starts[w] + q) for q in par)
+    N = int(starts[-1])
+    dep_off = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    M, K = 16, 4
+    now = 5_000
+    return wl.Problem("sized", now, 150_000, wf, rng.integers(0, K, N).astype(np.int32),
+                      rng.integers(0, 10**5, N).astype(np.int64), (rng.random(N) < 0.3).astype(np.uint8),
+                      np.where(rng.random(N) < 0.5, rng.integers(0, M, N), -1).astype(np.int32),
+                      dep_off, np.asarray(flat, np.int32),
+                      (now + rng.integers(-10**5, 10**7, W)).astype(np.int64),
+                      (np.arange(M) % K).astype(np.int32), rng.integers(0, 10**6, M).astype(np.int64),
+                      rng.integers(200, 3000, M).astype(np.int32), wf_contiguous=True)
+
+
+def test_grouped_waves(policy, policy_tiled, policy_hbm):
+    """Workflows of at most 32 futures on average are swept two per wave:
+    pairs that fill a slice exactly, pairs too large for one slice (swept one
+    by one), empty workflows, an odd count (a last group of one), relabelled
+    ids, every policy variant and levels; and a dependency on the other
+    workflow of a pair (light and heavy futures) is an error."""
+    sizes = [30, 34, 64, 1, 0, 63, 2, 33, 31, 5, 27, 3, 29, 20, 12, 32, 32]
+    p = _sized_workflows(sizes, 3)
+    check(policy, p, "grouped sizes")
+    check(policy_tiled, p, "grouped sizes tiled")
+    check(policy_hbm, p, "grouped sizes hbm")
+    q = wl.relabel(p, np.random.default_rng(2).permutation(p.n_nodes))
+    check(policy, q, "grouped sizes relabelled")
+    for bits in VARIANTS:
+        check(policy, p, f"grouped sizes policy {bits}", policy=bits)
+    lv = np.random.default_rng(4).integers(0, 5, len(sizes)).astype(np.uint8)
+    check(policy, p, "grouped sizes levels", priority=lv)
+    starts = np.concatenate([[0], np.cumsum(sizes)])
+    for label, w_from, w_to in (("wf1 -> wf0", 1, 0), ("wf0 -> wf1", 0, 1), ("wf8 -> wf7", 8, 7)):
+        bad = p.copy(dep_idx=p.dep_idx.copy())
+        v = int(starts[w_from]) + 10           # a future with dependencies
+        assert bad.dep_off[v + 1] > bad.dep_off[v], label
+        bad.dep_idx[bad.dep_off[v]] = int(starts[w_to]) + 1
+        check(policy, bad, f"cross-workflow dependency {label}")
+    hv = next(v for v in range(int(starts[1]), int(starts[2])) if p.dep_off[v + 1] - p.dep_off[v] > 3)
+    bad = p.copy(dep_idx=p.dep_idx.copy())
+    bad.dep_idx[bad.dep_off[hv + 1] - 1] = 2
+    check(policy, bad, "cross-workflow dependency of a heavy future")
+
+
 def test_other_seeds(policy):
     for s in (11, 12):
         check(policy, wl.paper_scale(seed=s), f"paper-scale seed {s}")
