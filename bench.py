@@ -80,8 +80,8 @@ def pass_alg_bytes(N: int, E: int, R: int, W: int, M: int) -> float:
 # copy of known size (`python3 bench.py --copy-calibration`).  Valid only for
 # the kernel sources it was taken on: a different source digest reports null.
 TRAFFIC = {
-    ("paper-scale", "sweep"): {"src_sha256": "fccd7efccde326fab98f0aa28c054569cbbf11d3f8bfd8f7d8ef932a0b3b4d00",
-                               "bytes_per_launch": 7657115},
+    ("paper-scale", "sweep"): {"src_sha256": "aaf21d1ae24da7fb03ec833e1968e0078ad49208fb9a5fc457394ba525de11e9",
+                               "bytes_per_launch": 7172709},
 }
 
 
