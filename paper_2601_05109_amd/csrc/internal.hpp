@@ -162,7 +162,7 @@ struct SweepShape {
   int lds_cap;    // largest workflow handled in LDS
   size_t lds_bytes;
   int blocks;
-  int wave_path;      // one wave per workflow (k_sweep_wave)
+  int wave_path;      // one wave per workflow or group of workflows (k_sweep_wave)
   int group = 1;      // wave path: consecutive workflows swept together by one wave
 };
 SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t lds_limit);

@@ -18,12 +18,14 @@
 // reduces first and one lane issues a single atomic.
 //
 // Three shapes:
-//  * k_sweep_wave: one wavefront per workflow of at most 512 futures (four
-//    independent waves per workgroup, no workgroup barrier in the sweep), the
-//    workflow's state in a 14-byte-per-future LDS slice, each lane owning up
-//    to eight futures with their dependencies in registers; the levels are
-//    rounds of LDS atomics.  In fused mode it also validates the snapshot,
-//    finds each workflow's bounds and builds the routing table itself.
+//  * k_sweep_wave: one wavefront per workflow of at most 512 futures, or per
+//    pair of consecutive workflows of at most 64 futures together when
+//    workflows average 32 or fewer (four independent waves per workgroup, no
+//    workgroup barrier in the sweep), the slice's state in a
+//    14-byte-per-future LDS slice, each lane owning up to eight futures with
+//    their dependencies in registers; the levels are rounds of LDS atomics.
+//    In fused mode it also validates the snapshot, finds each workflow's
+//    bounds and builds the routing table itself.
 //  * k_sweep: one workgroup per workflow of up to 5,120 futures (LDS state).
 //  * workflows larger than that (or all, under NALAR_FORCE_GLOBAL_SWEEP) keep
 //    their state in HBM by position and process explicit frontier lists,
@@ -1539,7 +1541,7 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
   const WaveKernArgs* kargs = warm_kernargs_wait(warm);  // the rest, read after the warm-up
   const SweepArgs& a = kargs->a;
   const int wcap = kargs->wcap;
-  // one future per lane: the first workflow's attributes at the guessed
+  // one future per lane: the first group's attributes at the guessed
   // bound, in flight with the bound checks instead of after them
   PreAttr pre;
   if (kFused && NPTW == 1 && gw < h.W && spec_lo + ln < h.N) {
@@ -1709,7 +1711,7 @@ SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t ld
   const int64_t avg = W > 0 ? (N + W - 1) / W : 0;
   const size_t itab = 32 * size_t(M) + 4 * kTypeDirect;
   SweepShape s;
-  if (avg <= kWaveCap) {  // one wave per workflow
+  if (avg <= kWaveCap) {  // one wave per workflow (or pair of workflows)
     int64_t wcap = 64;       // room for workflows up to twice the average size
     while (wcap < 2 * avg && wcap < kWaveCap) wcap *= 2;
     s.threads = kWaveBlock;
