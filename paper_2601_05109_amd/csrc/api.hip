@@ -91,7 +91,7 @@ struct nalar_policy {
   uint32_t hint_levels = 0;      // priority levels of the previous pass (bit l: level l)
   int bucket_skip = 0;           // passes left before the bucketed sort is tried again
   int bucket_backoff = 1;
-  int bucket_dense = 0;          // buckets doubled this many times after overflows
+  int bucket_dense = 0;          // buckets doubled this many times (overflows: up to 3, crowding: 4)
   int bucket_calm = 0;           // bucketed passes without overflow since the last change
   int bucket_relax = 64;         // calm passes before fewer buckets are tried again
   bool bucket_relaxed = false;   // the last pass tried fewer buckets
@@ -561,7 +561,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
       const bool crowded = __atomic_load_n(&h->host->max_bucket, __ATOMIC_ACQUIRE) > kBucketCrowded;
       const bool was_relaxed = h->bucket_relaxed;
       h->bucket_relaxed = false;
-      if (crowded && h->bucket_dense < 3 && bk.nb < kBucketMax) {
+      if (crowded && h->bucket_dense < 4 && bk.nb < kBucketMax) {
         // sorted, but a bucket is crowded (its futures rank one another one by
         // one, and its group of buckets outweighs the rest): add buckets, and
         // if fewer buckets were just tried, wait longer before trying again

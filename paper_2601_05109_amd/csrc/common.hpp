@@ -92,8 +92,9 @@ constexpr int kBucketLbGroup = 256;
 constexpr int kBucketLbGroups = kBucketMax / kBucketLbGroup;
 static_assert(kBucketLbGroup == 4 * kWave, "one uint4 of counters per lane and group");
 // A bucket with more futures than this after a large-bucket sort asks for a
-// denser plan next time (the sort still succeeded).
-constexpr uint32_t kBucketCrowded = 16;
+// denser plan next time (the sort still succeeded), up to sixteen times the
+// base bucket count.
+constexpr uint32_t kBucketCrowded = 8;
 static_assert(kBucketLbMin % kBucketLbGroup == 0, "whole groups");
 constexpr uint32_t kStatusTiled = 0x20000000u;
 
