@@ -82,27 +82,46 @@ __device__ inline uint32_t block_excl_scan(uint32_t x, uint32_t* s_tmp) {
 }
 
 // Digit histograms (all npass digits) of the first pass's items, added into
-// ghist.  H is a workgroup-private [kMaxSortPasses][256] array.
+// ghist.  H is a workgroup-private [kMaxSortPasses][256] array.  Each thread
+// takes kHistItems items per step, all loaded before any is used, so a
+// workgroup covers many items per memory round trip and few workgroups (few
+// flushes of 256 x npass global adds) cover the span.
+constexpr int kHistItems = 8;
+
 template <typename K>
 __device__ void histogram(const FirstSource& f, int npass, uint32_t (*H)[kRadixBuckets],
                           uint32_t* ghist) {
   for (int i = threadIdx.x; i < kMaxSortPasses * kRadixBuckets; i += kSortThreads) (&H[0][0])[i] = 0;
   __syncthreads();
-  const int64_t stride = int64_t(gridDim.x) * kSortThreads;
-  for (int64_t base = int64_t(blockIdx.x) * kSortThreads; base < f.span; base += stride) {
-    const int64_t i = base + threadIdx.x;
-    const bool valid = first_valid(f, i);
-    const K key = valid ? first_key<K>(f, i) : K(0);
-    for (int ps = 0; ps < npass; ++ps) {
-      const uint32_t dg = uint32_t(key >> (ps * kRadixBits)) & (kRadixBuckets - 1);
-      // most high digits are shared by the whole wave: one add instead of 64
-      const uint64_t act = ballot(valid);
-      const int first = readlane_i32(int(dg), act ? __builtin_ctzll(act) : 0);
-      const uint64_t same = ballot(valid && int(dg) == first);
-      if (same == act) {
-        if (act && lane_id() == __builtin_ctzll(act)) atomicAdd(&H[ps][dg], uint32_t(__popcll(act)));
-      } else if (valid) {
-        atomicAdd(&H[ps][dg], 1u);
+  const int64_t stride = int64_t(gridDim.x) * kSortThreads * kHistItems;
+  for (int64_t base = int64_t(blockIdx.x) * kSortThreads * kHistItems; base < f.span; base += stride) {
+    bool valid[kHistItems];
+    K key[kHistItems];
+#pragma unroll
+    for (int u = 0; u < kHistItems; ++u) {  // every load first (in bounds; stale keys are dropped)
+      const int64_t i = base + int64_t(u) * kSortThreads + threadIdx.x;
+      const bool in = i < f.span;
+      if (f.mode == kSrcStaged) {
+        valid[u] = in && f.stg_ready[in ? i : 0] != 0;
+        key[u] = K(uint64_t(f.stg_slack[in ? i : 0] - f.smin));
+      } else {
+        valid[u] = in;
+        key[u] = K(uint32_t(f.wf[in ? i : 0]));
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kHistItems; ++u) {
+      for (int ps = 0; ps < npass; ++ps) {
+        const uint32_t dg = uint32_t(key[u] >> (ps * kRadixBits)) & (kRadixBuckets - 1);
+        // most high digits are shared by the whole wave: one add instead of 64
+        const uint64_t act = ballot(valid[u]);
+        const int first = readlane_i32(int(dg), act ? __builtin_ctzll(act) : 0);
+        const uint64_t same = ballot(valid[u] && int(dg) == first);
+        if (same == act) {
+          if (act && lane_id() == __builtin_ctzll(act)) atomicAdd(&H[ps][dg], uint32_t(__popcll(act)));
+        } else if (valid[u]) {
+          atomicAdd(&H[ps][dg], 1u);
+        }
       }
     }
   }
@@ -739,7 +758,7 @@ hipError_t launch_slack_sort(hipStream_t s, const SortArgs& a, int first_pass, i
   hipError_t e;
   if (first_pass == 0) {
     mark(ctx, "sort_hist");
-    hipLaunchKernelGGL(k_slack_hist, dim3(grid_of(a.span, 4 * kSortThreads, 2048)),
+    hipLaunchKernelGGL(k_slack_hist, dim3(grid_of(a.span, kHistItems * kSortThreads, 256)),
                        dim3(kSortThreads), 0, s, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -759,7 +778,7 @@ hipError_t launch_slack_sort(hipStream_t s, const SortArgs& a, int first_pass, i
 hipError_t launch_group(hipStream_t s, const GroupArgs& a, void (*mark)(void*, const char*),
                         void* ctx) {
   mark(ctx, "group_hist");
-  hipLaunchKernelGGL(k_group_hist, dim3(grid_of(a.p.N, 4 * kSortThreads, 2048)), dim3(kSortThreads), 0, s,
+  hipLaunchKernelGGL(k_group_hist, dim3(grid_of(a.p.N, kHistItems * kSortThreads, 256)), dim3(kSortThreads), 0, s,
                      a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
