@@ -78,29 +78,31 @@ def pass_alg_bytes(N: int, E: int, R: int, W: int, M: int) -> float:
 # `python3 bench.py --no-cpu --steps 20 --warmup 5` (FETCH_SIZE, then
 # WRITE_SIZE, KiB per dispatch) scaled by the same counters read for a plain
 # copy of known size (`python3 bench.py --copy-calibration`).  Valid only for
-# the kernel sources it was taken on: a different source digest reports null.
+# the sources that kernel is built from (its own file and the shared headers):
+# a different digest of those reports null.
+KERNEL_SOURCES = {
+    "sweep": ("paper_2601_05109_amd/csrc/sweep.hip", "paper_2601_05109_amd/csrc/common.hpp",
+              "paper_2601_05109_amd/csrc/internal.hpp", "include/nalar_policy.h"),
+}
 TRAFFIC = {
-    ("paper-scale", "sweep"): {"src_sha256": "12ea0d18a9631721e862a8aaa488ed8f969949a0c8a8c6c1d12545b937a6277b",
+    ("paper-scale", "sweep"): {"src_sha256": "bddaafc52d4f1d876fea5738a0a8bbb3df86364a2927ed08efd6cdf35cb6a164",
                                "bytes_per_launch": 7172931},
 }
 
 
-def source_digest() -> str:
+def source_digest(kernel: str = "sweep") -> str:
     import hashlib
     h = hashlib.sha256()
-    for sub in ("paper_2601_05109_amd/csrc",):
-        d = os.path.join(ROOT, sub)
-        for f in sorted(os.listdir(d)):
-            if f.endswith((".hip", ".hpp", ".h")):
-                h.update(f.encode())
-                with open(os.path.join(d, f), "rb") as fh:
-                    h.update(fh.read())
+    for rel in KERNEL_SOURCES[kernel]:
+        h.update(rel.encode())
+        with open(os.path.join(ROOT, rel), "rb") as fh:
+            h.update(fh.read())
     return h.hexdigest()
 
 
 def measured_traffic(workload_name: str, kernel: str):
     t = TRAFFIC.get((workload_name, kernel))
-    if t is None or t["src_sha256"] != source_digest():
+    if t is None or kernel not in KERNEL_SOURCES or t["src_sha256"] != source_digest(kernel):
         return None
     return t["bytes_per_launch"]
 
