@@ -470,14 +470,16 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_totals(SortArgs a, Bu
   const int64_t t = int64_t((c.x < cap ? c.x : cap) + (c.y < cap ? c.y : cap) +
                             (c.z < cap ? c.z : cap) + (c.w < cap ? c.w : cap));
   const int64_t sum = wave_sum_i64(t);
+  if (lane_id() == 0) a.bagg[grp] = uint64_t(sum);
   // the fullest bucket (how crowded the plan is: the host adds buckets when
-  // it is), folded into one of kParts slots
-  const uint32_t m01 = c.x > c.y ? c.x : c.y, m23 = c.z > c.w ? c.z : c.w;
-  const int64_t mx = wave_max_i64(int64_t(m01 > m23 ? m01 : m23));
-  if (lane_id() == 0) {
-    a.bagg[grp] = uint64_t(sum);
-    __hip_atomic_fetch_max(&ctrl->part_crowd[grp & (kParts - 1)], uint32_t(mx), __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
+  // it is), folded into one of kParts slots; not needed once the plan has
+  // the most buckets it can have
+  if (bk.nb < kBucketMax) {
+    const uint32_t m01 = c.x > c.y ? c.x : c.y, m23 = c.z > c.w ? c.z : c.w;
+    const int64_t mx = wave_max_i64(int64_t(m01 > m23 ? m01 : m23));
+    if (lane_id() == 0)
+      __hip_atomic_fetch_max(&ctrl->part_crowd[grp & (kParts - 1)], uint32_t(mx), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
