@@ -75,7 +75,7 @@ def pass_alg_bytes(N: int, E: int, R: int, W: int, M: int) -> float:
 
 
 # HBM traffic of the dominant kernel, from two rocprofv3 --pmc runs of
-# `python3 bench.py --no-cpu --steps 20 --warmup 5` (FETCH_SIZE, then
+# `python3 bench.py --no-cpu --steps 20 --warmup 5 --cold 0` (FETCH_SIZE, then
 # WRITE_SIZE, KiB per dispatch) scaled by the same counters read for a plain
 # copy of known size (`python3 bench.py --copy-calibration`).  Valid only for
 # the sources that kernel is built from (its own file and the shared headers):
@@ -340,6 +340,8 @@ def main() -> int:
                          "routes in output order with running instance loads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cold", type=int, default=20,
+                    help="passes timed after evicting the L2 and the MALL (0: skip)")
     ap.add_argument("--priority-levels", type=int, default=0,
                     help="give every workflow a seeded priority level in [0, L) (set_priority); 0 = none")
     ap.add_argument("--dyn-steps", type=int, default=100, help="dynamic workload: steps after step 0")
@@ -410,6 +412,21 @@ def main() -> int:
     gpu_ms = ev0.elapsed_time(ev1)
     ms_per_step = 1e3 * wall / args.steps
 
+    # cold caches: before each of a few passes, overwrite a buffer larger than
+    # the L2 and the MALL (512 MiB), wait for it, then time the pass alone
+    cold = []
+    if args.cold > 0:
+        evict = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+        for _ in range(args.cold):
+            evict.fill_(1)
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            one_pass()
+            cold.append(time.perf_counter() - t)
+        del evict
+        torch.cuda.synchronize()
+    cold_us = sorted(1e6 * x for x in cold)
+
     # timed region 2: the same passes with per-kernel events on the library stream
     pol.set_timing(True)
     acc: dict[str, list[float]] = {}
@@ -447,6 +464,8 @@ def main() -> int:
                    "priority_levels": args.priority_levels},
         "latency_us": {"p50": lat_us[len(lat_us) // 2], "p99": lat_us[min(len(lat_us) - 1, int(0.99 * len(lat_us)))],
                        "min": lat_us[0], "gpu_event_mean": 1e3 * gpu_ms / args.steps},
+        "cold_latency_us": ({"p50": cold_us[len(cold_us) // 2], "max": cold_us[-1], "passes": len(cold_us),
+                             "evict_bytes": 512 << 20} if cold_us else None),
         "kernels_us": {k: round(1e3 * v, 2) for k, v in kern.items()},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
