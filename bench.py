@@ -86,7 +86,7 @@ KERNEL_SOURCES = {
 }
 TRAFFIC = {
     ("paper-scale", "sweep"): {"src_sha256": "bddaafc52d4f1d876fea5738a0a8bbb3df86364a2927ed08efd6cdf35cb6a164",
-                               "bytes_per_launch": 7172931},
+                               "bytes_per_launch": 7170451},
 }
 
 
