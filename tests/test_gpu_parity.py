@@ -443,6 +443,24 @@ def test_grouped_waves(policy, policy_tiled, policy_hbm):
     check(policy, bad, "cross-workflow dependency of a heavy future")
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_grouped_waves_random_sizes(policy, seed):
+    """Random workflow sizes around the pair boundary (a pair fills one
+    64-future slice, or spills and is swept one workflow at a time), averaging
+    at most 32 futures, with random levels and policy variants."""
+    rng = np.random.default_rng(500 + seed)
+    W = int(rng.integers(2, 90))
+    sizes = [int(x) for x in rng.choice([0, 1, 5, 16, 31, 32, 33, 40, 63, 64], size=W,
+                                        p=[.05, .05, .1, .15, .15, .2, .1, .1, .05, .05])]
+    while sum(sizes) > 32 * W:  # keep the pairs' plan (average at most 32)
+        sizes[int(np.argmax(sizes))] //= 2
+    p = _sized_workflows(sizes, 600 + seed, heavy_every=int(rng.integers(3, 9)))
+    bits = [0, nalar.NALAR_ORDER_LPT, nalar.NALAR_ROUTE_STATEFUL][seed % 3]
+    check(policy, p, f"random sizes seed {seed}", policy=bits)
+    lv = rng.integers(0, 4, W).astype(np.uint8)
+    check(policy, p, f"random sizes seed {seed} levels", policy=bits, priority=lv)
+
+
 def test_other_seeds(policy):
     for s in (11, 12):
         check(policy, wl.paper_scale(seed=s), f"paper-scale seed {s}")
