@@ -859,8 +859,19 @@ struct WaveSlice {
   int64_t* mx;      // running max of the consumers' rem, then rem
   int32_t* cnt;     // consumers not yet finalised
   uint8_t* dn;      // done
-  uint8_t* nr;      // some dependency not done
+  uint8_t* nr;      // some dependency not done (bit 0); finalised (bit 1, frontier rounds)
+  // frontier rounds only (kFrontierMinNpt futures per lane and more)
+  int64_t* est;     // est'
+  uint32_t* d01;    // dependency slots 0 and 1 (as p01)
+  uint32_t* d2;     // dependency slot 2 (as p2), or kHeavyMark
+  uint16_t* q0;     // frontier queues (ping-pong)
+  uint16_t* q1;
 };
+
+// From this many futures per lane the rounds follow a frontier (deep
+// workflows: many levels, few futures finalised per level).
+constexpr int kFrontierMinNpt = 4;
+constexpr uint32_t kHeavyMark = 0xFFFFFFFFu;
 
 // Rounds of the wave sweep: every owned future whose consumers are all
 // finalised (counter zero) is finalised, rem = est' + running max, and pushed
@@ -960,6 +971,121 @@ struct Seg {
     return s;
   }
 };
+
+// Rounds that follow a frontier instead of rescanning every owned future:
+// a future enters the next frontier when the push that drops its consumer
+// counter to zero (a returning LDS atomic) sees it, so each round touches
+// only the futures it finalises, processed by whichever lanes take the queue
+// entries (estimates and dependency slots are copied to LDS first).  Futures
+// with more than kPmax dependencies push their list with the whole wave.
+// Results as for rounds(): rem of every finalised future in rr, fin bits.
+template <int NPTW>
+__device__ __attribute__((always_inline)) inline void rounds_frontier(
+    const SweepArgs& a, const Layout& L, const WaveSlice& W, int64_t b, int n, uint32_t own,
+    uint32_t heavy, const int64_t* ee, const uint32_t* p01, const uint32_t* p2, int64_t* rr,
+    uint32_t& fin, bool& overflow) {
+  const int ln = lane_id();
+#pragma unroll
+  for (int j = 0; j < NPTW; ++j) {
+    if ((own >> j) & 1u) {
+      const int k = j * kWave + ln;
+      W.est[k] = ee[j];
+      W.d01[k] = p01[j];
+      W.d2[k] = ((heavy >> j) & 1u) ? kHeavyMark : p2[j];
+    }
+  }
+  // the first frontier: futures with no consumer left to wait for
+  int qn = 0;
+#pragma unroll
+  for (int j = 0; j < NPTW; ++j) {
+    const int k = j * kWave + ln;
+    const bool z = ((own >> j) & 1u) && W.cnt[k] == 0;
+    const uint64_t m = ballot(z);
+    if (z) W.q0[qn + int(lanes_below(m))] = uint16_t(k);
+    qn += int(__popcll(m));
+  }
+  wave_order();
+  uint16_t* cq = W.q0;
+  uint16_t* nq = W.q1;
+  while (qn > 0) {
+    int nn = 0;
+    for (int base = 0; base < qn; base += kWave) {
+      const int e = base + ln;
+      const bool act = e < qn;
+      int k = 0;
+      int64_t r = 0;
+      uint32_t d01 = 0xFFFFFFFFu, d2 = 0xFFFFFFFFu;
+      if (act) {
+        k = cq[e];
+        r = clamp_rem(W.est[k] + W.mx[k], overflow);
+        W.mx[k] = r;  // rem from here on
+        W.nr[k] |= 2u;
+        d01 = W.d01[k];
+        d2 = W.d2[k];
+      }
+      const bool hv = act && d2 == kHeavyMark;
+      int32_t lps[kPmax];
+      bool nw[kPmax];
+#pragma unroll
+      for (int q = 0; q < kPmax; ++q) {
+        const int lp = (act && !hv) ? dep_at(d01, d2, q) : -1;
+        lps[q] = lp;
+        nw[q] = false;
+        if (lp >= 0) {
+          atomicMax(reinterpret_cast<long long*>(&W.mx[lp]), (long long)r);
+          nw[q] = atomicSub(&W.cnt[lp], 1) == 1;
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < kPmax; ++q) {
+        const uint64_t m = ballot(nw[q]);
+        if (nw[q]) nq[nn + int(lanes_below(m))] = uint16_t(lps[q]);
+        nn += int(__popcll(m));
+      }
+      for (uint64_t hs = ballot(hv); hs; hs &= hs - 1) {
+        const int src = __builtin_ctzll(hs);
+        const int kh = readlane_i32(k, src);
+        const int64_t rh = readlane_i64(r, src);
+        const int32_t vh = node_at(L, b + kh);
+        const int o = a.p.dep_off[vh];
+        const int d = a.p.dep_off[vh + 1] - o;
+        for (int e0 = 0; e0 < d; e0 += kWave) {
+          const int ex = e0 + ln;
+          bool nwh = false;
+          int32_t lp = -1;
+          if (ex < d) {
+            lp = local_of(L, a.p.dep_idx[o + ex], b, n);
+            if (lp >= 0 && lp != kh) {
+              atomicMax(reinterpret_cast<long long*>(&W.mx[lp]), (long long)rh);
+              nwh = atomicSub(&W.cnt[lp], 1) == 1;
+            }
+          }
+          const uint64_t m = ballot(nwh);
+          if (nwh) nq[nn + int(lanes_below(m))] = uint16_t(lp);
+          nn += int(__popcll(m));
+        }
+      }
+    }
+    wave_order();
+    uint16_t* t = cq;
+    cq = nq;
+    nq = t;
+    qn = nn;
+  }
+  fin = 0;
+#pragma unroll
+  for (int j = 0; j < NPTW; ++j) {
+    rr[j] = 0;
+    if ((own >> j) & 1u) {
+      const int k = j * kWave + ln;
+      if (W.nr[k] & 2u) {
+        fin |= 1u << j;
+        rr[j] = W.mx[k];
+      }
+    }
+  }
+  wave_order();
+}
 
 // Attributes of future spec + lane loaded before the workflow's bounds are
 // known, spec being the bound that equal workflow sizes would give (the
@@ -1120,7 +1246,9 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
   bool overflow = false;
   uint32_t fin = 0;
   int64_t rr[NPTW];
-  if (ballot(heavy != 0) != 0)  // a future with many dependencies: the variant that pushes it
+  if constexpr (NPTW >= kFrontierMinNpt)
+    rounds_frontier<NPTW>(a, L, W, b, n, own, heavy, ee, p01, p2, rr, fin, overflow);
+  else if (ballot(heavy != 0) != 0)  // a future with many dependencies: the variant that pushes it
     rounds<NPTW, true>(a, L, W, b, n, own, heavy, ee, p01, p2, rr, fin, overflow);
   else
     rounds<NPTW, false>(a, L, W, b, n, own, heavy, ee, p01, p2, rr, fin, overflow);
@@ -1257,6 +1385,7 @@ constexpr int kWaveBlock = 256;                // four independent waves per wor
 constexpr int kWavesPerBlock = kWaveBlock / kWave;
 static_assert(kWavesPerBlock == 4, "the wave kernel's flags assume four waves");
 constexpr size_t kWaveSliceBytesPerFuture = 8 + 4 + 1 + 1;
+constexpr size_t kWaveFrontierBytesPerFuture = 8 + 4 + 4 + 2 + 2;  // est', slots, two queues
 
 // Instance table of the fused mode, built by the whole workgroup into its LDS
 // (M <= kWaveItabMax, entry i held by thread i, loaded by the caller): rank by
@@ -1577,11 +1706,18 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
   unsigned char* sp = smem;
   const ITabLds it = carve_itab(sp + (per_wave ? size_t(wv) * itab_one : 0), M);
   sp += itab_lds_wave(M);
-  WaveSlice Wv;
+  WaveSlice Wv{};
   Wv.mx = reinterpret_cast<int64_t*>(sp) + size_t(wv) * wcap; sp += 8 * nw;
   Wv.cnt = reinterpret_cast<int32_t*>(sp) + size_t(wv) * wcap; sp += 4 * nw;
   Wv.dn = sp + size_t(wv) * wcap; sp += nw;
-  Wv.nr = sp + size_t(wv) * wcap;
+  Wv.nr = sp + size_t(wv) * wcap; sp += nw;
+  if (NPTW >= kFrontierMinNpt) {
+    Wv.est = reinterpret_cast<int64_t*>(sp) + size_t(wv) * wcap; sp += 8 * nw;
+    Wv.d01 = reinterpret_cast<uint32_t*>(sp) + size_t(wv) * wcap; sp += 4 * nw;
+    Wv.d2 = reinterpret_cast<uint32_t*>(sp) + size_t(wv) * wcap; sp += 4 * nw;
+    Wv.q0 = reinterpret_cast<uint16_t*>(sp) + size_t(wv) * wcap; sp += 2 * nw;
+    Wv.q1 = reinterpret_cast<uint16_t*>(sp) + size_t(wv) * wcap;
+  }
   if (kFused) {
     if ((wave_itab ? ln : tid) < M && ((it_t < 0) | (it_sp < 1) | (it_ld < 0) | (it_ld > NALAR_LOAD_MAX)))
       flag_sweep(ctrl, kStInval);
@@ -1717,7 +1853,9 @@ SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t ld
     s.threads = kWaveBlock;
     s.npt = int(wcap / kWave);
     s.lds_cap = int(wcap);
-    s.lds_bytes = itab_lds_wave(M) + kWaveSliceBytesPerFuture * size_t(kWavesPerBlock) * size_t(wcap) + 16;
+    const size_t per = kWaveSliceBytesPerFuture +
+                       (wcap / kWave >= kFrontierMinNpt ? kWaveFrontierBytesPerFuture : 0);
+    s.lds_bytes = itab_lds_wave(M) + per * size_t(kWavesPerBlock) * size_t(wcap) + 16;
     s.wave_path = 1;
     // workflows of up to 32 futures on average: two per wave, side by side
     s.group = (wcap == kWave && 2 * avg <= kWave) ? 2 : 1;

@@ -461,6 +461,29 @@ def test_grouped_waves_random_sizes(policy, seed):
     check(policy, p, f"random sizes seed {seed} levels", policy=bits, priority=lv)
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_frontier_rounds(policy, policy_tiled, seed):
+    """Workflows of 70-512 futures (four or eight futures per lane, whose
+    rounds follow a frontier), with futures of up to six dependencies pushed
+    by the whole wave, duplicate-free random DAGs, and cycle / cross-workflow
+    errors planted in them."""
+    rng = np.random.default_rng(900 + seed)
+    W = int(rng.integers(3, 40))
+    lo, hi = ((70, 180), (257, 512), (130, 512))[seed % 3]
+    sizes = [int(x) for x in rng.integers(lo, hi + 1, W)]
+    p = _sized_workflows(sizes, 1000 + seed, heavy_every=int(rng.integers(2, 6)))
+    check(policy, p, f"frontier seed {seed}")
+    check(policy_tiled, p, f"frontier seed {seed} tiled", policy=nalar.NALAR_ORDER_LPT)
+    starts = np.concatenate([[0], np.cumsum(sizes)])
+    v = int(starts[1]) + 5  # a cycle: future v depends on a later future of its workflow that depends on v
+    later = int(starts[1]) + 100
+    bad = p.copy(dep_idx=p.dep_idx.copy())
+    if bad.dep_off[v + 1] > bad.dep_off[v] and bad.dep_off[later + 1] > bad.dep_off[later]:
+        bad.dep_idx[bad.dep_off[v]] = later
+        bad.dep_idx[bad.dep_off[later]] = v
+        check(policy, bad, f"frontier seed {seed} cycle")
+
+
 def test_other_seeds(policy):
     for s in (11, 12):
         check(policy, wl.paper_scale(seed=s), f"paper-scale seed {s}")
