@@ -85,8 +85,8 @@ KERNEL_SOURCES = {
               "paper_2601_05109_amd/csrc/internal.hpp", "include/nalar_policy.h"),
 }
 TRAFFIC = {
-    ("paper-scale", "sweep"): {"src_sha256": "bddaafc52d4f1d876fea5738a0a8bbb3df86364a2927ed08efd6cdf35cb6a164",
-                               "bytes_per_launch": 7170451},
+    ("paper-scale", "sweep"): {"src_sha256": "8f52b2861f1e8214e5818b479310bc8770b561d8546aa12066072a6b4c9b89bc",
+                               "bytes_per_launch": 7170591},
 }
 
 
