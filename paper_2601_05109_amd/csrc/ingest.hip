@@ -9,23 +9,35 @@ namespace nalar {
 namespace {
 
 constexpr int kNodeThreads = 256;
+constexpr int kNodeItems = 4;
 
 // Instance table sorted by (type, original index) and the run of each small
 // type; resets the next pass's control block (one workgroup).
 __device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl) {
   const int64_t M = p.M;
   reset_ctrl(next_ctrl);  // unused by this pass; ready for the next one
-  __shared__ int32_t s_type[NALAR_MAX_INSTANCES];
+  __shared__ __align__(16) int32_t s_type[NALAR_MAX_INSTANCES];
   __shared__ int32_t s_sorted[NALAR_MAX_INSTANCES];
-  for (int i = threadIdx.x; i < M; i += kNodeThreads) s_type[i] = p.inst_type[i];
-  for (int t = threadIdx.x; t < kTypeDirect; t += kNodeThreads) it.run[t] = 0;
+  __shared__ uint32_t s_run[kTypeDirect];
+  const int M4 = int((M + 3) & ~int64_t(3));
+  // padding past M compares as neither below nor equal to any entry's rank
+  for (int i = threadIdx.x; i < M4; i += kNodeThreads) s_type[i] = i < M ? p.inst_type[i] : INT32_MAX;
+  for (int t = threadIdx.x; t < kTypeDirect; t += kNodeThreads) s_run[t] = 0;
   __syncthreads();
+  const int4* s_type4 = reinterpret_cast<const int4*>(s_type);
   for (int i = threadIdx.x; i < M; i += kNodeThreads) {
     const int32_t t = s_type[i];
+    // rank = entries of a smaller type, plus entries of this type before i;
+    // four entries per LDS read, unrolled so that the reads overlap
     int rank = 0;
-    for (int j = 0; j < M; ++j) {
-      const int32_t u = s_type[j];
-      rank += (u < t) | ((u == t) & (j < i));
+#pragma unroll 4
+    for (int q = 0; q < M4 / 4; ++q) {
+      const int4 u = s_type4[q];
+      const int j = 4 * q;
+      rank += (u.x < t) | ((u.x == t) & (j < i));
+      rank += (u.y < t) | ((u.y == t) & (j + 1 < i));
+      rank += (u.z < t) | ((u.z == t) & (j + 2 < i));
+      rank += (u.w < t) | ((u.w == t) & (j + 3 < i));
     }
     const int32_t sp = p.inst_speed[i];
     it.type[rank] = t;
@@ -37,16 +49,17 @@ __device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl) {
     s_sorted[rank] = t;
   }
   __syncthreads();
-  // run of sorted positions per small type: from where the type starts to
-  // where the next one does (or M)
+  // run of sorted positions per small type: its first position, from the
+  // entry that starts it, and the end, from the entry that ends it
   for (int r = threadIdx.x; r < M; r += kNodeThreads) {
     const int32_t t = s_sorted[r];
-    if (t >= 0 && t < kTypeDirect && (r == 0 || s_sorted[r - 1] != t)) {
-      int e = r + 1;
-      while (e < M && s_sorted[e] == t) ++e;
-      it.run[t] = uint32_t(r) | (uint32_t(e) << 16);
+    if (t >= 0 && t < kTypeDirect) {
+      if (r == 0 || s_sorted[r - 1] != t) atomicOr(&s_run[t], uint32_t(r));
+      if (r == M - 1 || s_sorted[r + 1] != t) atomicOr(&s_run[t], uint32_t(r + 1) << 16);
     }
   }
+  __syncthreads();
+  for (int t = threadIdx.x; t < kTypeDirect; t += kNodeThreads) it.run[t] = s_run[t];
 }
 
 // Grid-stride over nodes, workflows and instances.  The last workgroup only
@@ -62,19 +75,35 @@ __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl
   const int64_t stride = int64_t(gridDim.x - 1) * kNodeThreads;
   const int64_t g0 = int64_t(blockIdx.x) * kNodeThreads + threadIdx.x;
   bool bad = false;
-  for (int64_t v = g0; v < N; v += stride) {
-    const int32_t w = p.wf[v];
-    const int32_t t = p.type[v];
-    const int32_t l = p.loc[v];
-    const int64_t e = p.est[v];
-    const uint8_t d = p.done[v];
-    const int32_t o0 = p.dep_off[v];
-    const int32_t o1 = p.dep_off[v + 1];
-    bad |= (w < 0) | (int64_t(w) >= W) | (t < 0) | (l < -1) | (int64_t(l) >= M) | (e < 0) |
-           (e > NALAR_EST_MAX) | (d > 1) | (o0 > o1);
-    if (v == 0) bad |= (o0 != 0);
-    if (v == N - 1) bad |= (int64_t(o1) != p.E);
-    if (contiguous && v + 1 < N) bad |= (p.wf[v + 1] < w);
+  // kNodeItems nodes a stride apart per thread, every load issued before the
+  // first check, so that each thread keeps that many lines in flight
+  for (int64_t v0 = g0; v0 < N; v0 += kNodeItems * stride) {
+    int32_t w[kNodeItems], t[kNodeItems], l[kNodeItems], o0[kNodeItems], o1[kNodeItems], wn[kNodeItems];
+    int64_t e[kNodeItems];
+    uint8_t d[kNodeItems];
+#pragma unroll
+    for (int u = 0; u < kNodeItems; ++u) {
+      const int64_t v = v0 + u * stride;
+      const bool in = v < N;
+      const int64_t vs = in ? v : v0;
+      w[u] = p.wf[vs];
+      t[u] = p.type[vs];
+      l[u] = p.loc[vs];
+      e[u] = p.est[vs];
+      d[u] = p.done[vs];
+      o0[u] = p.dep_off[vs];
+      o1[u] = p.dep_off[vs + 1];
+      wn[u] = contiguous && vs + 1 < N ? p.wf[vs + 1] : INT32_MAX;
+    }
+#pragma unroll
+    for (int u = 0; u < kNodeItems; ++u) {
+      const int64_t v = v0 + u * stride;
+      if (v >= N) continue;
+      bad |= (w[u] < 0) | (int64_t(w[u]) >= W) | (t[u] < 0) | (l[u] < -1) | (int64_t(l[u]) >= M) |
+             (e[u] < 0) | (e[u] > NALAR_EST_MAX) | (d[u] > 1) | (o0[u] > o1[u]) | (wn[u] < w[u]);
+      if (v == 0) bad |= (o0[u] != 0);
+      if (v == N - 1) bad |= (int64_t(o1[u]) != p.E);
+    }
   }
   for (int64_t w = g0; w < W; w += stride) {
     const int64_t dl = p.deadline[w];
@@ -108,7 +137,8 @@ int grid_for(int64_t n, int threads, int cap) {
 
 hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
                         int32_t* wf_off, int contiguous) {
-  int64_t n = p.N > p.W + 1 ? p.N : p.W + 1;
+  const int64_t nv = (p.N + kNodeItems - 1) / kNodeItems;
+  int64_t n = nv > p.W + 1 ? nv : p.W + 1;
   hipLaunchKernelGGL(k_nodes, dim3(grid_for(n, kNodeThreads, 4096) + 1), dim3(kNodeThreads), 0, s, p,
                      ctrl, next_ctrl, itab, wf_off, contiguous);
   return hipGetLastError();
