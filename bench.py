@@ -87,6 +87,8 @@ KERNEL_SOURCES = {
 TRAFFIC = {
     ("paper-scale", "sweep"): {"src_sha256": "8f52b2861f1e8214e5818b479310bc8770b561d8546aa12066072a6b4c9b89bc",
                                "bytes_per_launch": 7170591},
+    ("wide-mapreduce", "sweep"): {"src_sha256": "8f52b2861f1e8214e5818b479310bc8770b561d8546aa12066072a6b4c9b89bc",
+                                  "bytes_per_launch": 145231234},
 }
 
 
