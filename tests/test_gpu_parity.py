@@ -804,3 +804,18 @@ def test_store_small_graphs_and_errors():
                 del z
             finally:
                 st.close()
+
+
+# ------------------------------------------------------- large instance tables
+
+@pytest.mark.parametrize("n_inst,n_types", [(255, 3), (257, 70), (1021, 200), (1024, 5), (1024, 1)])
+@pytest.mark.parametrize("shuffle", [False, True])
+def test_large_instance_tables(policy, n_inst, n_types, shuffle):
+    """Instance tables past one workgroup's threads and past the directly
+    indexed types, sizes not a multiple of four: the (type, index) ranking and
+    the per-type runs, under plain, stateful and greedy routing."""
+    p = wl.random_dag(900 + n_inst + n_types, n_nodes=500, n_workflows=3, n_instances=n_inst,
+                      n_types=n_types, p_edge=0.02, est_max=10**6, load_max=10**9,
+                      shuffle_ids=shuffle)
+    for pol_bits in (0, nalar.NALAR_ROUTE_STATEFUL, nalar.NALAR_ROUTE_GREEDY):
+        check(policy, p, f"instances={n_inst} types={n_types} shuffle={shuffle}", policy=pol_bits)
