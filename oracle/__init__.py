@@ -28,6 +28,8 @@ OK, EINVAL, ECYCLE, ERANGE = 0, -1, -2, -3
 POLICY_LPT = 2        # order by remaining critical path, longest first
 POLICY_STATEFUL = 4   # a future whose state lives on an instance of its type runs there
 POLICY_GREEDY = 8     # route in output order, each future adding its service time to its instance
+POLICY_SRTF = 16      # order by remaining critical path, shortest first
+POLICY_WEIGHTED = 32  # deal each type's futures to its instances by weight, in output order
 
 _lock = threading.Lock()
 _lib: Optional[ctypes.CDLL] = None
@@ -54,7 +56,7 @@ def _load() -> ctypes.CDLL:
         lib.nalar_oracle_pass.restype = ctypes.c_int
         lib.nalar_oracle_pass.argtypes = [I64] * 6 + [P] * 17
         lib.nalar_oracle_pass_policy.restype = ctypes.c_int
-        lib.nalar_oracle_pass_policy.argtypes = [I64] * 6 + [ctypes.c_uint32] + [P] * 18
+        lib.nalar_oracle_pass_policy.argtypes = [I64] * 6 + [ctypes.c_uint32] + [P] * 19
         _lib = lib
     return _lib
 
@@ -75,11 +77,13 @@ def _ptr(a: Optional[np.ndarray]):
 
 
 def run(p, *, want_rem: bool = True, override: Optional[dict] = None,
-        policy: int = 0, priority: Optional[np.ndarray] = None) -> OracleResult:
+        policy: int = 0, priority: Optional[np.ndarray] = None,
+        weights: Optional[np.ndarray] = None) -> OracleResult:
     """Run the oracle on a problem (any object with the workloads.Problem
     fields).  ``override`` may replace scalar sizes or set arrays to None, to
-    exercise validation; ``policy`` selects the variants (POLICY_* bits) and
-    ``priority`` (uint8 per workflow, or None) the priority levels."""
+    exercise validation; ``policy`` selects the variants (POLICY_* bits),
+    ``priority`` (uint8 per workflow, or None) the priority levels and
+    ``weights`` (uint32 per instance, or None) the weights of POLICY_WEIGHTED."""
     lib = _load()
     o = dict(N=p.n_nodes, E=p.n_edges, W=p.n_workflows, M=p.n_instances,
              now=p.now_us, mig=p.migration_cost_us)
@@ -100,8 +104,9 @@ def run(p, *, want_rem: bool = True, override: Optional[dict] = None,
     cost = np.zeros(n_out, np.int64)
     n_ready = ctypes.c_int64(0)
     prio = None if priority is None else np.ascontiguousarray(priority, dtype=np.uint8)
+    wts = None if weights is None else np.ascontiguousarray(weights, dtype=np.uint32)
     rc = lib.nalar_oracle_pass_policy(
-        o["N"], o["E"], o["W"], o["M"], o["now"], o["mig"], policy, _ptr(prio),
+        o["N"], o["E"], o["W"], o["M"], o["now"], o["mig"], policy, _ptr(prio), _ptr(wts),
         *[_ptr(arrays[f]) for f in ("wf", "type", "est_us", "done", "loc", "dep_off",
                                     "dep_idx", "deadline_us", "inst_type", "inst_load_us",
                                     "inst_speed_permille")],

@@ -47,15 +47,32 @@
 //              it, then adds its service time on that instance,
 //              est*1000/speed, to that instance's load (routing that balances
 //              load across instances, Section 6.1); a load above 2^62 -> -3
+//   kSrtf      O9 sorts by (rem, wf, v) instead: the future with the least
+//              remaining work first (shortest remaining time first, the
+//              policy that minimises job completion time, Section 6.2); slack
+//              is still reported as in O7.  kLpt and kSrtf together -> -1
+//   kWeighted  after O9, the ready futures of each type that has instances of
+//              positive weight are dealt to those instances in proportion to
+//              their weights (route with a list of instances and weights,
+//              Table 2): the futures of type t, taken in output order, get
+//              sequence numbers j = 0, 1, 2, ...; with the instances of type t
+//              and positive weight listed by ascending index and S their total
+//              weight, future j goes to the instance whose run of w[i]
+//              consecutive numbers in 0..S-1 holds j mod S (the first w[0]
+//              numbers to the first instance, the next w[1] to the second,
+//              ...).  Its cost is that instance's O8 cost.  A future pinned by
+//              kStateful keeps its pin and takes no number; a type without a
+//              positive weight keeps the O8 route.  Weights above 2^20 -> -1;
+//              kWeighted with kGreedy -> -1
 //   priorities (a per-workflow level 0..15, set_priority of Table 2): O9
-//              sorts by (-priority[wf], key, wf, v), the higher level first;
-//              a level above 15 -> -1, and a ready future whose key (slack,
-//              or -rem under kLpt) lies outside (-2^58, 2^58) -> -3
+//              sorts by (-priority[wf], key, wf, v), the higher level first,
+//              for any key; a level above 15 -> -1
 //
 // Precedence of errors: EINVAL, then ECYCLE, then ERANGE.
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <map>
 #include <vector>
 
 namespace {
@@ -68,8 +85,10 @@ constexpr int kErange = -3;
 constexpr uint32_t kLpt = 2u;
 constexpr uint32_t kStateful = 4u;
 constexpr uint32_t kGreedy = 8u;
+constexpr uint32_t kSrtf = 16u;
+constexpr uint32_t kWeighted = 32u;
 constexpr int kMaxPriority = 15;
-constexpr int64_t kPrioKeyBound = int64_t(1) << 58;
+constexpr uint32_t kMaxWeight = 1u << 20;
 
 constexpr int64_t kMaxNodes = int64_t(1) << 30;
 constexpr int64_t kMaxEdges = (int64_t(1) << 31) - 1;
@@ -132,15 +151,22 @@ extern "C" {
 // must hold n_nodes entries (rem) and n_nodes entries (order, slack, route,
 // cost); rem_out and cost_out may be NULL.  Returns 0 or a negative error code.
 int nalar_oracle_pass_policy(int64_t N, int64_t E, int64_t W, int64_t M, int64_t now, int64_t mig,
-                             uint32_t policy, const uint8_t* priority, const int32_t* wf,
-                             const int32_t* type,
+                             uint32_t policy, const uint8_t* priority,
+                             const uint32_t* inst_weight, const int32_t* wf, const int32_t* type,
                              const int64_t* est, const uint8_t* done, const int32_t* loc,
                              const int32_t* dep_off, const int32_t* dep_idx,
                              const int64_t* deadline, const int32_t* inst_type,
                              const int64_t* inst_load, const int32_t* inst_speed, int64_t* rem_out,
                              int32_t* order_out, int64_t* slack_out, int32_t* route_out,
                              int64_t* cost_out, int64_t* n_ready_out) {
-  if ((policy & ~(kLpt | kStateful | kGreedy)) != 0) return kEinval;
+  if ((policy & ~(kLpt | kStateful | kGreedy | kSrtf | kWeighted)) != 0) return kEinval;
+  if ((policy & kLpt) && (policy & kSrtf)) return kEinval;
+  if ((policy & kGreedy) && (policy & kWeighted)) return kEinval;
+  if ((policy & kWeighted) && M > 0) {
+    if (!inst_weight) return kEinval;
+    for (int64_t i = 0; i < M; ++i)
+      if (inst_weight[i] > kMaxWeight) return kEinval;
+  }
   if (priority)
     for (int64_t w = 0; w < W; ++w)
       if (priority[w] > kMaxPriority) return kEinval;
@@ -237,20 +263,17 @@ int nalar_oracle_pass_policy(int64_t N, int64_t E, int64_t W, int64_t M, int64_t
     cost[v] = best;
   }
 
-  // O9: the full key (slack, wf, v), or (-rem, wf, v) under kLpt, behind the
-  // workflow's priority level when given, is a total order, so the result is
-  // unique.
+  // O9: the full key (slack, wf, v), or (-rem, wf, v) under kLpt, or
+  // (rem, wf, v) under kSrtf, behind the workflow's priority level when given,
+  // is a total order, so the result is unique.
   const bool lpt = (policy & kLpt) != 0;
-  if (priority)
-    for (int32_t v : ready_ids) {
-      const int64_t k = lpt ? -rem[v] : slack[v];
-      if (k <= -kPrioKeyBound || k >= kPrioKeyBound) return kErange;
-    }
+  const bool srtf = (policy & kSrtf) != 0;
+  auto key_of = [&](int32_t v) { return lpt ? -rem[v] : (srtf ? rem[v] : slack[v]); };
   std::vector<int32_t> order(ready_ids);
   std::sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
     if (priority && priority[wf[a]] != priority[wf[b]]) return priority[wf[a]] > priority[wf[b]];
-    const int64_t ka = lpt ? -rem[a] : slack[a];
-    const int64_t kb = lpt ? -rem[b] : slack[b];
+    const int64_t ka = key_of(a);
+    const int64_t kb = key_of(b);
     if (ka != kb) return ka < kb;
     if (wf[a] != wf[b]) return wf[a] < wf[b];
     return a < b;
@@ -282,6 +305,29 @@ int nalar_oracle_pass_policy(int64_t N, int64_t E, int64_t W, int64_t M, int64_t
     }
   }
 
+  // O9c (kWeighted): deal each weighted type's futures, in output order, to
+  // its instances by their weights.
+  if ((policy & kWeighted) && M > 0) {
+    std::map<int32_t, int64_t> next_seq;  // next sequence number of each type
+    for (int32_t v : order) {
+      if ((policy & kStateful) && loc[v] >= 0 && inst_type[loc[v]] == type[v]) continue;
+      int64_t total = 0;
+      for (int64_t i = 0; i < M; ++i)
+        if (inst_type[i] == type[v]) total += inst_weight[i];
+      if (total == 0) continue;
+      int64_t r = next_seq[type[v]]++ % total;
+      int32_t pick = -1;
+      for (int64_t i = 0; i < M && pick < 0; ++i) {
+        if (inst_type[i] != type[v]) continue;
+        if (r < int64_t(inst_weight[i])) pick = int32_t(i);
+        else r -= inst_weight[i];
+      }
+      route[v] = pick;
+      cost[v] = inst_load[pick] + (est[v] * 1000) / inst_speed[pick] +
+                ((loc[v] >= 0 && loc[v] != pick) ? mig : 0);
+    }
+  }
+
   // O10
   if (rem_out) std::memcpy(rem_out, rem.data(), sizeof(int64_t) * N);
   for (int64_t k = 0; k < R; ++k) {
@@ -295,7 +341,7 @@ int nalar_oracle_pass_policy(int64_t N, int64_t E, int64_t W, int64_t M, int64_t
   return kOk;
 }
 
-// The default policy (SRTF order by slack, load-and-locality routing).
+// The default policy (least slack first, load-and-locality routing).
 int nalar_oracle_pass(int64_t N, int64_t E, int64_t W, int64_t M, int64_t now, int64_t mig,
                       const int32_t* wf, const int32_t* type, const int64_t* est,
                       const uint8_t* done, const int32_t* loc, const int32_t* dep_off,
@@ -304,7 +350,7 @@ int nalar_oracle_pass(int64_t N, int64_t E, int64_t W, int64_t M, int64_t now, i
                       const int32_t* inst_speed, int64_t* rem_out, int32_t* order_out,
                       int64_t* slack_out, int32_t* route_out, int64_t* cost_out,
                       int64_t* n_ready_out) {
-  return nalar_oracle_pass_policy(N, E, W, M, now, mig, 0u, nullptr, wf, type, est, done, loc, dep_off,
+  return nalar_oracle_pass_policy(N, E, W, M, now, mig, 0u, nullptr, nullptr, wf, type, est, done, loc, dep_off,
                                   dep_idx, deadline, inst_type, inst_load, inst_speed, rem_out,
                                   order_out, slack_out, route_out, cost_out, n_ready_out);
 }

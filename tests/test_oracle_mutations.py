@@ -17,11 +17,15 @@ import oracle
 from golden_io import load as load_golden, names as golden_names
 from paper_2601_05109_amd import workloads as wl
 from test_oracle_pins import (brute_force_rem, push_replay_ready, rem_certificate,
+                              assert_routes_exhaustive, wide_range,
                               test_lpt_equals_srtf_when_deadlines_are_equal,
                               test_lpt_independent_futures_closed_form, test_stateful_routing_pins,
                               test_greedy_single_instance_prefix_sums,
                               test_greedy_identical_instances_round_robin,
-                              test_priority_levels_partition_the_order)
+                              test_priority_levels_partition_the_order,
+                              test_srtf_independent_futures_closed_form,
+                              test_weighted_against_quota_walk, test_weighted_rules,
+                              test_weighted_whole_periods_are_proportional)
 
 MUTATIONS = {
     "drop_est_term": ("if (__builtin_add_overflow(est_eff[v], best, &r)",
@@ -43,8 +47,22 @@ MUTATIONS = {
     "order_wf_desc": ("if (wf[a] != wf[b]) return wf[a] < wf[b];",
                       "if (wf[a] != wf[b]) return wf[a] > wf[b];"),
     "order_slack_desc": ("if (ka != kb) return ka < kb;", "if (ka != kb) return ka > kb;"),
-    "lpt_shortest_first": ("const int64_t ka = lpt ? -rem[a] : slack[a];",
-                           "const int64_t ka = lpt ? rem[a] : slack[a];"),
+    "lpt_shortest_first": ("return lpt ? -rem[v] : (srtf ? rem[v] : slack[v]);",
+                           "return lpt ? rem[v] : (srtf ? rem[v] : slack[v]);"),
+    "srtf_longest_first": ("return lpt ? -rem[v] : (srtf ? rem[v] : slack[v]);",
+                           "return lpt ? -rem[v] : (srtf ? -rem[v] : slack[v]);"),
+    "route_load_and_service_swapped": ("int64_t c = inst_load[i] + (est[v] * 1000) / inst_speed[i];",
+                                       "int64_t c = est[v] + (inst_load[i] * 1000) / inst_speed[i];"),
+    "route_penalty_without_loc_test": ("inst_speed[i];\n      if (loc[v] >= 0 && loc[v] != i) c += mig;",
+                                       "inst_speed[i];\n      if (loc[v] >= 0) c += mig;"),
+    "weighted_interval_off_by_one": ("if (r < int64_t(inst_weight[i])) pick = int32_t(i);",
+                                     "if (r <= int64_t(inst_weight[i])) pick = int32_t(i);"),
+    "weighted_one_sequence_for_all_types": ("int64_t r = next_seq[type[v]]++ % total;",
+                                            "int64_t r = next_seq[0]++ % total;"),
+    "weighted_pin_takes_a_number": ("if ((policy & kStateful) && loc[v] >= 0 && inst_type[loc[v]] == type[v]) continue;",
+                                    "if ((policy & kStateful) && loc[v] >= 0 && inst_type[loc[v]] == type[v]) { next_seq[type[v]]++; continue; }"),
+    "weighted_cost_without_penalty": ("(est[v] * 1000) / inst_speed[pick] +\n                ((loc[v] >= 0 && loc[v] != pick) ? mig : 0);",
+                                      "(est[v] * 1000) / inst_speed[pick];"),
     "stateful_pays_penalty": ("cost[v] = inst_load[i] + (est[v] * 1000) / inst_speed[i];",
                               "cost[v] = inst_load[i] + (est[v] * 1000) / inst_speed[i] + mig;"),
     "greedy_no_load_update": ("        load[arg] += (est[v] * 1000) / inst_speed[arg];\n", ""),
@@ -78,7 +96,7 @@ def _pins_pass(lib_path):
     lib.nalar_oracle_pass.restype = ctypes.c_int
     lib.nalar_oracle_pass.argtypes = [ctypes.c_int64] * 6 + [ctypes.c_void_p] * 17
     lib.nalar_oracle_pass_policy.restype = ctypes.c_int
-    lib.nalar_oracle_pass_policy.argtypes = [ctypes.c_int64] * 6 + [ctypes.c_uint32] + [ctypes.c_void_p] * 18
+    lib.nalar_oracle_pass_policy.argtypes = [ctypes.c_int64] * 6 + [ctypes.c_uint32] + [ctypes.c_void_p] * 19
     oracle._lib = lib
     try:
         for g in golden_names():
@@ -100,6 +118,10 @@ def _pins_pass(lib_path):
                 return False
             try:
                 rem_certificate(p, r.rem)
+                assert_routes_exhaustive(p, r)
+                if seed % 4 == 0 and p.n_instances > 0:
+                    q = wide_range(p, seed)
+                    assert_routes_exhaustive(q, oracle.run(q))
             except AssertionError:
                 return False
         for pin in (test_lpt_equals_srtf_when_deadlines_are_equal,
@@ -110,9 +132,15 @@ def _pins_pass(lib_path):
                 pin()
             except AssertionError:
                 return False
-        for pin in (test_priority_levels_partition_the_order,):
+        for pin in (test_priority_levels_partition_the_order, test_weighted_against_quota_walk):
             try:
                 pin(0)
+            except AssertionError:
+                return False
+        for pin in (test_srtf_independent_futures_closed_form, test_weighted_rules,
+                    test_weighted_whole_periods_are_proportional):
+            try:
+                pin()
             except AssertionError:
                 return False
         return True

@@ -266,6 +266,88 @@ def test_relabelled_ids_give_relabelled_result():
 
 # ---------------------------------------------------------------- routing
 
+def brute_route(p, v, mig=None):
+    """Exhaustive minimum of (cost, index) over every instance of the
+    future's type, in Python integers (no overflow, no rounding):
+    cost = load + floor(est * 1000 / speed) + migration penalty unless the
+    instance holds the future's state.  (INT64_MAX, -1) when none has the type."""
+    mig = int(p.migration_cost_us) if mig is None else mig
+    t, l, est = int(p.type[v]), int(p.loc[v]), int(p.est_us[v])
+    cands = [(int(p.inst_load_us[i]) + (est * 1000) // int(p.inst_speed_permille[i])
+              + (mig if (l >= 0 and l != i) else 0), i)
+             for i in range(p.n_instances) if int(p.inst_type[i]) == t]
+    if not cands:
+        return INT64_MAX, -1
+    return min(cands)
+
+
+def assert_routes_exhaustive(p, r):
+    for k, v in enumerate(r.order.tolist()):
+        c, i = brute_route(p, v)
+        assert (int(r.cost[k]), int(r.route[k])) == (c, i), (p.name, v)
+
+
+def wide_range(p, seed):
+    """The same graph with estimates, loads, speeds and migration cost drawn
+    over the whole range the boundary accepts (est up to 2^40, load and
+    migration up to 2^60, speed up to 2^31 - 1), loads often tied."""
+    rng = np.random.default_rng(seed)
+    N, M = p.n_nodes, p.n_instances
+    est = rng.integers(0, 1 << 40, N, dtype=np.int64, endpoint=True)
+    est[rng.random(N) < 0.2] = 0
+    load = rng.choice([0, 7, 1 << 60, int(rng.integers(0, 1 << 60))], M).astype(np.int64)
+    speed = rng.choice([1, 1000, (1 << 31) - 1, int(rng.integers(1, 1 << 31))], M).astype(np.int32)
+    return p.copy(est_us=est, inst_load_us=load, inst_speed_permille=speed,
+                  migration_cost_us=int(rng.choice([0, 200_000, 1 << 60])))
+
+
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_route_exhaustive_configs(cfg):
+    """Every ready future of the tiny and paper-scale snapshots is routed to
+    the exhaustive big-integer minimum of (cost, index)."""
+    p = wl.CONFIGS[cfg]()
+    r = oracle.run(p)
+    assert r.status == oracle.OK and r.n_ready > 0
+    assert_routes_exhaustive(p, r)
+
+
+@pytest.mark.parametrize("seed", range(150))
+def test_route_exhaustive_random(seed):
+    """Small DAGs with unequal loads and speeds, migration penalties, state on
+    instances of other types, ties and futures of types no instance has; every
+    fifth over the full value range of the boundary."""
+    rng = np.random.default_rng(1000 + seed)
+    p = wl.random_dag(500 + seed, n_nodes=int(rng.integers(1, 40)), n_workflows=int(rng.integers(1, 4)),
+                      n_instances=int(rng.integers(0, 12)), n_types=int(rng.integers(1, 5)),
+                      load_max=int(rng.choice([3, 100, 10**6])), speed_hi=int(rng.choice([2, 3000])))
+    if seed % 5 == 0 and p.n_instances > 0:
+        p = wide_range(p, seed)
+    r = oracle.run(p)
+    assert r.status == oracle.OK
+    assert_routes_exhaustive(p, r)
+
+
+def test_route_exhaustive_catches_planted_mistakes():
+    """The exhaustive pin rejects a swapped load and service term, a penalty
+    charged on the state's own instance, and ties to the higher index."""
+    p = wl.tiny()
+    r = oracle.run(p)
+    bad_swap = r.cost.copy()
+    v0 = int(r.order[0])
+    c, i = brute_route(p, v0)
+    for k, v in enumerate(r.order.tolist()):
+        l = int(p.loc[v])
+        if l >= 0 and int(p.inst_type[l]) == int(p.type[v]):
+            bad = r.cost.copy()
+            bad[k] += int(p.migration_cost_us)
+            with pytest.raises(AssertionError):
+                assert_routes_exhaustive(p, oracle.OracleResult(0, r.n_ready, r.rem, r.order, r.slack, r.route, bad))
+            break
+    bad_swap[0] = int(p.est_us[v0]) + int(p.inst_load_us[i]) * 1000 // int(p.inst_speed_permille[i])
+    with pytest.raises(AssertionError):
+        assert_routes_exhaustive(p, oracle.OracleResult(0, r.n_ready, r.rem, r.order, r.slack, r.route, bad_swap))
+
+
 def test_route_equal_loads_closed_form():
     """Equal loads and speed 1000 everywhere: the future goes where its state
     is when that instance has its type, otherwise to the lowest-index instance
@@ -392,7 +474,157 @@ def test_stateful_without_state_is_default():
 
 
 def test_unknown_policy_bits_rejected():
-    assert oracle.run(wl.tiny(), policy=16).status == oracle.EINVAL
+    assert oracle.run(wl.tiny(), policy=64).status == oracle.EINVAL
+    assert oracle.run(wl.tiny(), policy=LPT | oracle.POLICY_SRTF).status == oracle.EINVAL
+
+
+SRTF = oracle.POLICY_SRTF
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
+def test_srtf_order_certificate(cfg):
+    """SRTF (least remaining work first, Section 6.2): the ready set of the
+    default pass, strictly increasing in (rem, wf, v), which is unique under
+    that total order; slack, route and cost are the default pass's, permuted."""
+    p = wl.CONFIGS[cfg]()
+    a, b = oracle.run(p), oracle.run(p, policy=SRTF)
+    assert b.n_ready == a.n_ready
+    assert sorted(b.order.tolist()) == sorted(a.order.tolist())
+    keys = [(int(b.rem[v]), int(p.wf[v]), int(v)) for v in b.order.tolist()]
+    assert all(x < y for x, y in zip(keys, keys[1:]))
+    by_v = {int(v): i for i, v in enumerate(a.order.tolist())}
+    idx = np.array([by_v[int(v)] for v in b.order.tolist()], np.int64)
+    for f in ("slack", "route", "cost"):
+        np.testing.assert_array_equal(getattr(b, f), getattr(a, f)[idx])
+
+
+def test_srtf_is_lpt_reversed_for_distinct_work():
+    """With pairwise distinct remaining work, least-remaining-first is exactly
+    longest-remaining-first read backwards.  Estimates are distinct powers of
+    two, so each rem (a sum over the set of futures on one path) is distinct:
+    two start nodes with the same path set would reach each other."""
+    rng = np.random.default_rng(3)
+    p = wl.random_dag(21, n_nodes=40, n_workflows=4, p_edge=0.1)
+    p = p.copy(est_us=(np.int64(1) << rng.permutation(40).astype(np.int64)), done=np.zeros(40, np.uint8))
+    a, b = oracle.run(p, policy=SRTF), oracle.run(p, policy=LPT)
+    ready_rem = a.rem[a.order]
+    assert len(set(ready_rem.tolist())) == len(ready_rem)
+    assert a.order.tolist() == b.order.tolist()[::-1]
+
+
+def test_srtf_independent_futures_closed_form():
+    """Independent futures, none done: rem = est, so SRTF lists them by est
+    ascending, ties by workflow then id."""
+    N, W = 40, 3
+    rng = np.random.default_rng(6)
+    p = wl.random_dag(4, n_nodes=N, n_workflows=W, p_edge=0.0)
+    p = p.copy(done=np.zeros(N, np.uint8), est_us=rng.integers(0, 6, N).astype(np.int64))
+    r = oracle.run(p, policy=SRTF)
+    assert r.order.tolist() == sorted(range(N), key=lambda v: (int(p.est_us[v]), int(p.wf[v]), v))
+
+
+WEIGHTED = oracle.POLICY_WEIGHTED
+
+
+def quota_dispatch(p, order, weights, skip=()):
+    """A weighted dispatcher written as a stateful quota walk (a different
+    formulation from the oracle's modular arithmetic): per type, a pointer to
+    the current instance and its remaining quota; a future takes the current
+    instance and uses one unit of its quota; an exhausted quota moves the
+    pointer to the next instance of the type with a positive weight (cyclic,
+    by index) and refills it with that instance's weight.  Futures in ``skip``
+    are passed over.  Returns {future: instance} for weighted types only."""
+    state = {}
+    out = {}
+    for v in order:
+        if v in skip:
+            continue
+        t = int(p.type[v])
+        insts = [i for i in range(p.n_instances) if int(p.inst_type[i]) == t and int(weights[i]) > 0]
+        if not insts:
+            continue
+        ptr, quota = state.get(t, (0, int(weights[insts[0]])))
+        while quota == 0:
+            ptr = (ptr + 1) % len(insts)
+            quota = int(weights[insts[ptr]])
+        out[v] = insts[ptr]
+        state[t] = (ptr, quota - 1)
+    return out
+
+
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_weighted_against_quota_walk(cfg):
+    """Weighted routing (Table 2's route by a list of instances and weights):
+    every weighted future goes where the quota walk sends it, at the
+    exhaustive cost of that instance; unweighted types keep the default route;
+    the order is untouched."""
+    p = wl.CONFIGS[cfg]()
+    rng = np.random.default_rng(40 + cfg)
+    w = rng.integers(0, 5, p.n_instances).astype(np.uint32)
+    w[p.inst_type == 1] = 0            # one type without weights: default routing
+    a, r = oracle.run(p), oracle.run(p, policy=WEIGHTED, weights=w)
+    assert r.status == oracle.OK
+    for f in ("order", "slack", "rem"):
+        np.testing.assert_array_equal(getattr(a, f), getattr(r, f))
+    want = quota_dispatch(p, r.order.tolist(), w)
+    assert len(want) > r.n_ready // 4
+    mig = int(p.migration_cost_us)
+    for k, v in enumerate(r.order.tolist()):
+        if v in want:
+            i = want[v]
+            assert int(r.route[k]) == i
+            l = int(p.loc[v])
+            assert int(r.cost[k]) == (int(p.inst_load_us[i]) + int(p.est_us[v]) * 1000 // int(p.inst_speed_permille[i])
+                                      + (mig if l >= 0 and l != i else 0))
+        else:
+            assert (int(r.route[k]), int(r.cost[k])) == (int(a.route[k]), int(a.cost[k]))
+
+
+def test_weighted_unit_weights_round_robin():
+    """Weight one on every instance of a single type: plain round-robin in
+    index order, the k-th future (in output order) on instance k mod m."""
+    m, n = 5, 23
+    p = _one_type_problem(m, [0] * m, [1000] * m, [10] * n)
+    r = oracle.run(p, policy=WEIGHTED, weights=np.ones(m, np.uint32))
+    np.testing.assert_array_equal(r.route, np.arange(n) % m)
+
+
+def test_weighted_whole_periods_are_proportional():
+    """After a whole number of periods (futures = a multiple of the total
+    weight) every instance has received exactly its weight times the number
+    of periods; instances of weight zero receive nothing."""
+    w = np.array([3, 0, 1, 4, 2], np.uint32)
+    n = 4 * int(w.sum())
+    p = _one_type_problem(len(w), [9] * len(w), [1000] * len(w), [10] * n)
+    r = oracle.run(p, policy=WEIGHTED, weights=w)
+    np.testing.assert_array_equal(np.bincount(r.route, minlength=len(w)), 4 * w)
+
+
+def test_weighted_rules():
+    """Weights above 2^20, missing weights and weighted with greedy routing are
+    EINVAL; all-zero weights give the default routing; a stateful pin keeps
+    its instance and takes no place in its type's sequence."""
+    p = wl.tiny()
+    M = p.n_instances
+    assert oracle.run(p, policy=WEIGHTED).status == oracle.EINVAL
+    big = np.ones(M, np.uint32)
+    big[2] = (1 << 20) + 1
+    assert oracle.run(p, policy=WEIGHTED, weights=big).status == oracle.EINVAL
+    assert oracle.run(p, policy=WEIGHTED | GREEDY, weights=np.ones(M, np.uint32)).status == oracle.EINVAL
+    a, z = oracle.run(p), oracle.run(p, policy=WEIGHTED, weights=np.zeros(M, np.uint32))
+    for f in ("order", "route", "cost"):
+        np.testing.assert_array_equal(getattr(a, f), getattr(z, f))
+    w = np.arange(1, M + 1).astype(np.uint32) % 3
+    s = oracle.run(p, policy=WEIGHTED | STATEFUL, weights=w)
+    pinned = {int(v) for v in s.order.tolist()
+              if int(p.loc[v]) >= 0 and int(p.inst_type[int(p.loc[v])]) == int(p.type[v])}
+    assert pinned
+    want = quota_dispatch(p, s.order.tolist(), w, skip=pinned)
+    for k, v in enumerate(s.order.tolist()):
+        if v in pinned:
+            assert int(s.route[k]) == int(p.loc[v])
+        elif v in want:
+            assert int(s.route[k]) == want[v]
 
 
 GREEDY = oracle.POLICY_GREEDY
@@ -500,14 +732,26 @@ def test_priority_levels_partition_the_order(cfg):
 
 
 def test_priority_level_and_key_rules():
+    """A level above 15 is EINVAL; any key is ordered by the plain rule
+    (level first, then key, workflow, id), also keys far outside any clock
+    range: slacks near +-2^61 split by level exactly as small ones do."""
     p = wl.tiny()
     pr = np.zeros(p.n_workflows, np.uint8)
     pr[3] = 16
     assert oracle.run(p, priority=pr).status == oracle.EINVAL
-    far = p.copy(deadline_us=p.deadline_us.copy())
-    far.deadline_us[0] = p.now_us + (1 << 60)   # slack beyond 2^58
-    assert oracle.run(far).status == oracle.OK
-    assert oracle.run(far, priority=np.zeros(p.n_workflows, np.uint8)).status == oracle.ERANGE
+    rng = np.random.default_rng(11)
+    dl = p.now_us + rng.choice([-(1 << 61), (1 << 61) - (1 << 40), 0, 1 << 58], p.n_workflows)
+    far = p.copy(deadline_us=dl.astype(np.int64))
+    base = oracle.run(far)
+    assert base.status == oracle.OK
+    assert base.slack.min() < -(1 << 60) and base.slack.max() > (1 << 60)
+    for bits in (0, LPT, oracle.POLICY_SRTF):
+        pr = rng.integers(0, 16, p.n_workflows).astype(np.uint8)
+        a, b = oracle.run(far, policy=bits), oracle.run(far, policy=bits, priority=pr)
+        assert b.status == oracle.OK
+        lv = pr[p.wf[a.order]]
+        want = np.concatenate([a.order[lv == x] for x in range(15, -1, -1)])
+        np.testing.assert_array_equal(b.order, want)
 
 
 # ---------------------------------------------------------------- degenerate
