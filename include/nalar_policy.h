@@ -11,8 +11,9 @@
  *      of the SRTF policy, Section 6.2, taken over the whole DAG);
  *   2. readiness: a future is runnable once it is not done and every future it
  *      depends on is done (push-based readiness, Section 4.3.1, property 3);
- *   3. priority: ready futures ranked by deadline slack, most urgent first
- *      (set_priority, Table 2);
+ *   3. priority: ready futures ranked by deadline slack, least slack first
+ *      (set_priority, Table 2; the remaining-work orders of Section 6.2 are
+ *      policy variants);
  *   4. routing: each ready future sent to the instance of its component type
  *      with the least load plus speed-scaled service time plus a migration
  *      penalty when its managed state lives on another instance (route and
@@ -58,7 +59,7 @@ enum {
 #define NALAR_HORIZON_MAX    (INT64_C(1) << 61)  /* |now|, |deadline - now|      */
 #define NALAR_REM_MAX        (INT64_C(1) << 62)  /* remaining critical path, us  */
 #define NALAR_PRIORITY_MAX   15                  /* highest priority level       */
-#define NALAR_PRIORITY_KEY   (INT64_C(1) << 58)  /* |order key| bound with levels */
+#define NALAR_WEIGHT_MAX     (1u << 20)          /* routing weight of an instance */
 
 /* nalar_problem.flags */
 #define NALAR_WF_CONTIGUOUS  1u  /* the nodes of workflow w are exactly the ids
@@ -68,11 +69,17 @@ enum {
                                     Without it the library groups nodes by
                                     workflow itself (one extra sort).           */
 /* Policy variants of the same pass (nalar_problem.flags; 0 = the default
- * SRTF-by-slack order and load-and-locality routing): */
+ * least-slack-first order and load-and-locality routing): */
 #define NALAR_ORDER_LPT      2u  /* order = ready futures by (-rem, wf, id)
                                     ascending: longest remaining processing
                                     first (the LPT policy, Section 6.2); the
                                     slack output is unchanged                   */
+#define NALAR_ORDER_SRTF    16u  /* order = ready futures by (rem, wf, id)
+                                    ascending: least remaining work first
+                                    (shortest remaining time first, the policy
+                                    that minimises job completion time, Section
+                                    6.2); the slack output is unchanged; with
+                                    NALAR_ORDER_LPT it is NALAR_EINVAL          */
 #define NALAR_ROUTE_STATEFUL 4u  /* a ready future whose state lives on an
                                     instance of its own type (loc[v] >= 0 and
                                     inst_type[loc[v]] == type[v]) is routed there
@@ -92,6 +99,25 @@ enum {
                                     of different types are independent
                                     sequences, so this runs one wavefront per
                                     component type                              */
+#define NALAR_ROUTE_WEIGHTED 32u /* weighted routing (route with a list of
+                                    instances and weights, Table 2): after
+                                    ordering, the ready futures of each type
+                                    that has instances of positive weight
+                                    (inst_weight) are dealt to those instances
+                                    in proportion to their weights.  The futures
+                                    of type t, in output order, take sequence
+                                    numbers j = 0, 1, 2, ...; with the instances
+                                    of type t and positive weight listed by
+                                    ascending index and S their total weight,
+                                    future j goes to the instance whose run of
+                                    w[i] consecutive numbers in 0..S-1 holds
+                                    j mod S (the first w[0] numbers to the first
+                                    instance, the next w[1] to the second, ...),
+                                    at that instance's cost.  A future pinned by
+                                    NALAR_ROUTE_STATEFUL keeps its pin and takes
+                                    no number; a type without a positive weight
+                                    keeps its default route.  With
+                                    NALAR_ROUTE_GREEDY it is NALAR_EINVAL       */
 
 /* nalar_policy_config.flags (tuning and testing; 0 is the normal setting) */
 #define NALAR_FORCE_GLOBAL_SWEEP 1u  /* keep every workflow's sweep state in HBM
@@ -128,9 +154,8 @@ typedef struct {
   int64_t now_us;             /* |now_us| <= NALAR_HORIZON_MAX                    */
   int64_t migration_cost_us;  /* penalty for running a future away from the
                                  instance holding its state, [0, NALAR_MIG_MAX]   */
-  uint32_t flags;             /* NALAR_WF_CONTIGUOUS, NALAR_ORDER_LPT,
-                                 NALAR_ROUTE_STATEFUL, NALAR_ROUTE_GREEDY bits,
-                                 or 0                                             */
+  uint32_t flags;             /* NALAR_WF_CONTIGUOUS, NALAR_ORDER_* and
+                                 NALAR_ROUTE_* bits, or 0                         */
   uint32_t reserved;          /* must be 0                                        */
   const int32_t* wf;          /* [N] workflow (session) of each future, [0, W)    */
   const int32_t* type;        /* [N] component type, >= 0                         */
@@ -152,10 +177,11 @@ typedef struct {
                                  0..NALAR_PRIORITY_MAX, or NULL for none: the
                                  ready futures of a higher level come first in
                                  the order, whatever their key (set_priority,
-                                 Table 2).  With levels, every ready future's
-                                 order key (the slack, or -rem under
-                                 NALAR_ORDER_LPT) must lie strictly inside
-                                 +-NALAR_PRIORITY_KEY, else NALAR_ERANGE         */
+                                 Table 2): the order is by (-level, key, wf, id) */
+  const uint32_t* inst_weight;/* [M] routing weight of each instance,
+                                 0..NALAR_WEIGHT_MAX; read only under
+                                 NALAR_ROUTE_WEIGHTED (then required when M > 0),
+                                 else may be NULL                                 */
 } nalar_problem;
 
 /* Outputs.  Struct in host memory; array pointers are DEVICE pointers, owned by
@@ -197,14 +223,53 @@ int nalar_policy_create(const nalar_policy_config* cfg, nalar_policy** out);
  *   order    = the ready futures sorted by (slack, wf, id) ascending (behind
  *              the priority level of their workflow, highest first, when
  *              wf_priority is given)
- * (the NALAR_ORDER_LPT, NALAR_ROUTE_STATEFUL and NALAR_ROUTE_GREEDY bits change
- * order and route as described at their definitions).
+ * (the NALAR_ORDER_* and NALAR_ROUTE_* bits change order and route as
+ * described at their definitions).
  * Synchronous.  NULL p, r, or a required array (a node array when N > 0,
  * dep_idx when E > 0, deadline_us when W > 0, an instance array when M > 0,
  * order/slack_us/route when N > 0) is NALAR_EINVAL.  Error precedence and the
  * state of the outputs after an error are as described at the return codes.
  */
 int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r);
+
+/*
+ * One-level decisions (the central, per-future control that Section 6.3 and
+ * Table 4 contrast with installed policies): decide events one at a time (or
+ * a batch of them) against the view the last pass left, instead of running a
+ * pass.  The view is that pass's rem_us for every future and its order with
+ * the slack of each entry (device pointers, read only).  For each event future
+ * v = events[k]:
+ *   slack_us[k] = deadline_us[wf[v]] - now_us - rem_us[v]
+ *   route[k], cost_us[k] = v's route and cost under the routing rule of
+ *              nalar_policy_pass (NALAR_ROUTE_STATEFUL honoured)
+ *   rank[k]    = the number of entries of the view's order that come before v
+ *              in the pass's order ((-level, key, wf, id) with the key of the
+ *              NALAR_ORDER_* bits), i.e. where v enters the current order; a
+ *              future already in the order gets its own index.
+ * A future's rem does not change when it becomes ready, so the last pass's
+ * rem is the one the decision needs.  p must be the snapshot the view came
+ * from (its contents are not validated again); NALAR_ROUTE_GREEDY and
+ * NALAR_ROUTE_WEIGHTED (which route by position in a whole order) are
+ * NALAR_EINVAL.  Synchronous.  NALAR_EINVAL also for NULL or inconsistent
+ * arguments (n_order outside [0, N], a NULL view array with entries, NULL
+ * slack_us or route with events) and for an event id outside [0, N).
+ */
+typedef struct {
+  const int64_t* rem_us;      /* [N] remaining critical path of every future     */
+  const int32_t* order;       /* [n_order] ready futures in the pass's order      */
+  const int64_t* slack_us;    /* [n_order] aligned with order                     */
+  int64_t n_order;
+} nalar_view;
+
+typedef struct {              /* DEVICE arrays of n_events entries, caller-owned */
+  int64_t* slack_us;
+  int32_t* route;
+  int64_t* cost_us;           /* or NULL                                          */
+  int64_t* rank;              /* or NULL                                          */
+} nalar_decisions;
+
+int nalar_policy_decide(nalar_policy* h, const nalar_problem* p, const nalar_view* view,
+                        int64_t n_events, const int32_t* events, nalar_decisions* out);
 
 /* Release the handle and its scratch.  NULL-safe.  Waits for the handle's
  * stream first. */

@@ -71,8 +71,10 @@ int64_t nalar_store_n_nodes(const nalar_store* s);
 
 /* One pass over the stored snapshot, as nalar_policy_pass on the policy
  * handle the store is bound to: now_us and migration_cost_us as in
- * nalar_problem, policy the NALAR_ORDER_LPT / NALAR_ROUTE_STATEFUL /
- * NALAR_ROUTE_GREEDY bits; r as in nalar_policy_pass.  Synchronous. */
+ * nalar_problem, policy the NALAR_ORDER_LPT / NALAR_ORDER_SRTF /
+ * NALAR_ROUTE_STATEFUL / NALAR_ROUTE_GREEDY bits (the store keeps no routing
+ * weights: NALAR_ROUTE_WEIGHTED is NALAR_EINVAL); r as in nalar_policy_pass.
+ * Synchronous. */
 int nalar_store_pass(nalar_store* s, int64_t now_us, int64_t migration_cost_us, uint32_t policy,
                      nalar_result* r);
 

@@ -18,8 +18,11 @@
 //               four digit passes.  The last kernel writes the caller's arrays
 //               and the status into pinned host memory
 //   [greedy] -> NALAR_ROUTE_GREEDY only: routing again in output order
-// with one stream synchronisation after the sort (and one after greedy
-// routing).  The bucketed sort is used once a previous pass has given a key
+//   [weighted] -> NALAR_ROUTE_WEIGHTED only: the weighted instances are
+//               tabulated before the sweep (their weights validated), and the
+//               weighted types' futures are dealt out after the sort
+// with one stream synchronisation after the sort (and one after greedy or
+// weighted routing).  The bucketed sort is used once a previous pass has given a key
 // range and at most kBucketMaxReady futures were ready; if a bucket
 // overflows, the kernel reports "tiled", and after the synchronisation the
 // host resets the control block, sweeps again without buckets and runs the
@@ -62,6 +65,9 @@ struct Arena {
   uint32_t* gpay[2] = {nullptr, nullptr};
   uint64_t* glb = nullptr;
   uint64_t* bagg = nullptr;  // bucket-group totals of the look-back bucket kernel
+  int32_t* wt_i32 = nullptr;   // weighted routing: type, idx, first, cnt tables and the entry count
+  uint32_t* wt_u32 = nullptr;  // weighted routing: cum, tot tables
+  uint32_t* wcounts = nullptr; // weighted routing: per-tile counts
   int32_t* pos_of_node = nullptr;
   int32_t* g_cnt = nullptr;
   int64_t* g_mx = nullptr;
@@ -166,6 +172,9 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B) {
   a.glb = reinterpret_cast<uint64_t*>(take(8 * size_t(kMaxGroupPasses) * tiles * kRadixBuckets));
   a.bagg = reinterpret_cast<uint64_t*>(take(8 * size_t(kBucketLbGroups)));
   a.lookback_bytes = off - a.lookback_off;
+  a.wt_i32 = reinterpret_cast<int32_t*>(take(4 * size_t(4 * NALAR_MAX_INSTANCES + 1)));
+  a.wt_u32 = reinterpret_cast<uint32_t*>(take(4 * size_t(2 * NALAR_MAX_INSTANCES)));
+  a.wcounts = reinterpret_cast<uint32_t*>(take(4 * size_t(weighted_tiles(n1)) * NALAR_MAX_INSTANCES));
   return align_up(off, 256);
 }
 
@@ -255,8 +264,8 @@ BucketArgs plan_buckets(const nalar_policy* h, int64_t N, bool levels, bool wave
 
 bool in_range(int64_t v, int64_t lo, int64_t hi) { return v >= lo && v <= hi; }
 
-int check_problem(nalar_policy* h, const nalar_problem* p, const nalar_result* r) {
-  if (!p || !r) return fail(h, NALAR_EINVAL, "NULL problem or result");
+int check_snapshot(nalar_policy* h, const nalar_problem* p) {
+  if (!p) return fail(h, NALAR_EINVAL, "NULL problem");
   const int64_t N = p->n_nodes, E = p->n_edges, W = p->n_workflows, M = p->n_instances;
   if (!in_range(N, 0, NALAR_MAX_NODES)) return fail(h, NALAR_EINVAL, "n_nodes out of range");
   if (!in_range(E, 0, NALAR_MAX_EDGES)) return fail(h, NALAR_EINVAL, "n_edges out of range");
@@ -266,10 +275,16 @@ int check_problem(nalar_policy* h, const nalar_problem* p, const nalar_result* r
     return fail(h, NALAR_EINVAL, "now_us out of range");
   if (!in_range(p->migration_cost_us, 0, NALAR_MIG_MAX))
     return fail(h, NALAR_EINVAL, "migration_cost_us out of range");
-  if ((p->flags & ~(NALAR_WF_CONTIGUOUS | NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL |
-                    NALAR_ROUTE_GREEDY)) != 0 ||
+  if ((p->flags & ~(NALAR_WF_CONTIGUOUS | NALAR_ORDER_LPT | NALAR_ORDER_SRTF | NALAR_ROUTE_STATEFUL |
+                    NALAR_ROUTE_GREEDY | NALAR_ROUTE_WEIGHTED)) != 0 ||
       p->reserved != 0)
     return fail(h, NALAR_EINVAL, "unknown problem flags");
+  if ((p->flags & NALAR_ORDER_LPT) && (p->flags & NALAR_ORDER_SRTF))
+    return fail(h, NALAR_EINVAL, "NALAR_ORDER_LPT and NALAR_ORDER_SRTF together");
+  if ((p->flags & NALAR_ROUTE_GREEDY) && (p->flags & NALAR_ROUTE_WEIGHTED))
+    return fail(h, NALAR_EINVAL, "NALAR_ROUTE_GREEDY and NALAR_ROUTE_WEIGHTED together");
+  if ((p->flags & NALAR_ROUTE_WEIGHTED) && M > 0 && !p->inst_weight)
+    return fail(h, NALAR_EINVAL, "NALAR_ROUTE_WEIGHTED without inst_weight");
   if (N == 0 && E != 0) return fail(h, NALAR_EINVAL, "edges without nodes");
   if (N > 0 && (!p->wf || !p->type || !p->est_us || !p->done || !p->loc || !p->dep_off))
     return fail(h, NALAR_EINVAL, "NULL node array");
@@ -278,9 +293,23 @@ int check_problem(nalar_policy* h, const nalar_problem* p, const nalar_result* r
   if (W == 0 && p->wf_priority) return fail(h, NALAR_EINVAL, "wf_priority without workflows");
   if (M > 0 && (!p->inst_type || !p->inst_load_us || !p->inst_speed_permille))
     return fail(h, NALAR_EINVAL, "NULL instance array");
-  if (N > 0 && (!r->order || !r->slack_us || !r->route))
+  return NALAR_OK;
+}
+
+int check_problem(nalar_policy* h, const nalar_problem* p, const nalar_result* r) {
+  if (!p || !r) return fail(h, NALAR_EINVAL, "NULL problem or result");
+  const int rc = check_snapshot(h, p);
+  if (rc != NALAR_OK) return rc;
+  if (p->n_nodes > 0 && (!r->order || !r->slack_us || !r->route))
     return fail(h, NALAR_EINVAL, "NULL output array");
   return NALAR_OK;
+}
+
+ProblemDev device_view(const nalar_problem* p, uint32_t policy) {
+  return ProblemDev{p->n_nodes, p->n_edges, p->n_workflows, p->n_instances, p->now_us,
+                    p->migration_cost_us, policy, 0u, p->wf, p->type, p->est_us, p->done, p->loc,
+                    p->dep_off, p->dep_idx, p->deadline_us, p->inst_type, p->inst_load_us,
+                    p->inst_speed_permille, p->wf_priority, p->inst_weight};
 }
 
 struct Timer {
@@ -391,6 +420,38 @@ int nalar_policy_get_timing(const nalar_policy* h, const char** names, float* ms
   return NALAR_OK;
 }
 
+int nalar_policy_decide(nalar_policy* h, const nalar_problem* p, const nalar_view* view,
+                        int64_t n_events, const int32_t* events, nalar_decisions* out) {
+  if (!h) return NALAR_EINVAL;
+  h->err.clear();
+  h->timed_valid = false;
+  int rc = check_snapshot(h, p);
+  if (rc != NALAR_OK) return rc;
+  if (p->flags & (NALAR_ROUTE_GREEDY | NALAR_ROUTE_WEIGHTED))
+    return fail(h, NALAR_EINVAL, "decide: greedy and weighted routing need a whole order");
+  if (!view || !out || n_events < 0) return fail(h, NALAR_EINVAL, "decide: NULL view or output");
+  if (n_events == 0) return NALAR_OK;
+  const int64_t N = p->n_nodes;
+  if (view->n_order < 0 || view->n_order > N) return fail(h, NALAR_EINVAL, "decide: n_order out of range");
+  if (!events || !out->slack_us || !out->route || !view->rem_us ||
+      (view->n_order > 0 && (!view->order || !view->slack_us)))
+    return fail(h, NALAR_EINVAL, "decide: NULL array");
+  if (n_events > INT32_MAX) return fail(h, NALAR_EINVAL, "decide: too many events");
+  hipError_t e = hipSetDevice(h->device);
+  if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+  const uint32_t policy = p->flags & (NALAR_ORDER_LPT | NALAR_ORDER_SRTF | NALAR_ROUTE_STATEFUL);
+  DecideArgs a{device_view(p, policy), view->rem_us, view->order, view->slack_us, view->n_order,
+               events, n_events, out->slack_us, out->route, out->cost_us, out->rank, h->host};
+  __atomic_store_n(&h->host->aux_status, 0u, __ATOMIC_RELEASE);
+  e = launch_decide(h->stream, a);
+  if (e != hipSuccess) return hip_fail(h, e, "decide");
+  e = hipStreamSynchronize(h->stream);
+  if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
+  if (__atomic_load_n(&h->host->aux_status, __ATOMIC_ACQUIRE) & kStInval)
+    return fail(h, NALAR_EINVAL, "decide: an event id is out of range");
+  return NALAR_OK;
+}
+
 int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) {
   if (!h) return NALAR_EINVAL;
   h->err.clear();
@@ -426,11 +487,9 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   h->ctrl_dirty[cur] = true;
   h->ctrl_dirty[nxt] = true;
 
-  const uint32_t policy = p->flags & (NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL | NALAR_ROUTE_GREEDY);
-  ProblemDev pd{N, p->n_edges, W, M, p->now_us, p->migration_cost_us, policy, 0u,
-                p->wf, p->type, p->est_us, p->done, p->loc, p->dep_off, p->dep_idx,
-                p->deadline_us, p->inst_type, p->inst_load_us, p->inst_speed_permille,
-                p->wf_priority};
+  const uint32_t policy = p->flags & (NALAR_ORDER_LPT | NALAR_ORDER_SRTF | NALAR_ROUTE_STATEFUL |
+                                      NALAR_ROUTE_GREEDY | NALAR_ROUTE_WEIGHTED);
+  const ProblemDev pd = device_view(p, policy);
   const bool contiguous = (p->flags & NALAR_WF_CONTIGUOUS) != 0 || W <= 1;
 
   Timer tm{h};
@@ -446,6 +505,31 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   if (need_reset || need_clear)
     NALAR_LAUNCH("reset", launch_reset(s, need_reset ? ctrl : nullptr, bk.cnt, need_clear ? bk.nb : 0));
   if (bk.nb > 0) h->bcnt_clean[cur] = false;
+  WeightedArgs wa{};
+  if (policy & NALAR_ROUTE_WEIGHTED) {
+    wa.type = p->type;
+    wa.est = p->est_us;
+    wa.loc = p->loc;
+    wa.inst_type = p->inst_type;
+    wa.inst_load = p->inst_load_us;
+    wa.inst_speed = p->inst_speed_permille;
+    wa.inst_weight = p->inst_weight;
+    wa.M = int32_t(M);
+    wa.stateful = (policy & NALAR_ROUTE_STATEFUL) ? 1 : 0;
+    wa.mig = p->migration_cost_us;
+    wa.route = r->route;
+    wa.cost = r->cost_us;
+    wa.ctrl = ctrl;
+    wa.wt_type = A.wt_i32;
+    wa.wt_idx = A.wt_i32 + NALAR_MAX_INSTANCES;
+    wa.wt_first = A.wt_i32 + 2 * NALAR_MAX_INSTANCES;
+    wa.wt_cnt = A.wt_i32 + 3 * NALAR_MAX_INSTANCES;
+    wa.n_wt = A.wt_i32 + 4 * NALAR_MAX_INSTANCES;
+    wa.wt_cum = A.wt_u32;
+    wa.wt_tot = A.wt_u32 + NALAR_MAX_INSTANCES;
+    wa.counts = A.wcounts;
+    NALAR_LAUNCH("weighted_table", launch_weighted_table(s, wa));
+  }
   const bool fused = N > 0 && sweep_can_fuse(sh, M, contiguous);
   if (!fused)
     NALAR_LAUNCH("nodes", launch_nodes(s, pd, ctrl, A.ctrl[nxt], A.itab, A.wf_off, contiguous ? 1 : 0));
@@ -513,7 +597,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   sa.stg_route = A.stg_route;
   sa.stg_cost = A.stg_cost;
   sa.node_of_pos = node_of_pos;
-  sa.out_slack = ((policy & NALAR_ORDER_LPT) || p->wf_priority) ? A.stg_oslack : nullptr;
+  sa.out_slack = ((policy & (NALAR_ORDER_LPT | NALAR_ORDER_SRTF)) || p->wf_priority) ? A.stg_oslack : nullptr;
   sa.span = N;
   for (int i = 0; i < 2; ++i) {
     sa.key[i] = A.skey[i];
@@ -554,6 +638,8 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
         h->bucket_backoff = h->bucket_backoff < 64 ? 2 * h->bucket_backoff : 64;
       }
       NALAR_LAUNCH("reset", launch_reset(s, ctrl, nullptr, 0));
+      if (policy & NALAR_ROUTE_WEIGHTED)  // its weight check reports into the block just reset
+        NALAR_LAUNCH("weighted_table", launch_weighted_table(s, wa));
       sw.bk = BucketArgs{};
       NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
     } else {
@@ -610,6 +696,16 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
     if (__atomic_load_n(&h->host->aux_status, __ATOMIC_ACQUIRE) & kStRange)
       return fail(h, NALAR_ERANGE, "an instance load exceeds 2^62 us under load-aware routing");
+  }
+  if ((policy & NALAR_ROUTE_WEIGHTED) && r->n_ready > 0 && M > 0) {
+    wa.order = r->order;
+    wa.R = r->n_ready;
+    wa.tiles = weighted_tiles(r->n_ready);
+    e = launch_route_weighted(s, wa, Timer::cb, &tm);
+    if (e != hipSuccess) return hip_fail(h, e, "weighted");
+    tm.end();
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
   }
 #undef NALAR_LAUNCH
   if (h->timing) {

@@ -9,11 +9,6 @@
 namespace nalar {
 
 // Status word bits (ORed by any kernel that finds a problem).
-// Priority levels shift the order key by level * 2^kPrioShift; keys must stay
-// inside (-kPrioKeyBound, kPrioKeyBound) so that levels never interleave.
-constexpr int kPrioShift = 59;
-constexpr int64_t kPrioKeyBound = int64_t(1) << 58;
-
 constexpr uint32_t kStInval = 1u;
 constexpr uint32_t kStCycle = 2u;
 constexpr uint32_t kStRange = 4u;
@@ -21,7 +16,8 @@ constexpr uint32_t kStRange = 4u;
 constexpr int kWave = 64;
 constexpr int kRadixBits = 8;
 constexpr int kRadixBuckets = 1 << kRadixBits;
-constexpr int kMaxSortPasses = 8;    // 64-bit keys
+constexpr int kMaxKeyPasses = 8;     // 64-bit keys
+constexpr int kMaxSortPasses = 9;    // key passes, then one priority-level pass
 constexpr int kMaxGroupPasses = 4;   // workflow ids < 2^30
 constexpr int kSortThreads = 256;
 constexpr int kSortItems = 16;
@@ -42,8 +38,8 @@ __host__ __device__ inline uint64_t lb_pack(uint32_t epoch, uint64_t flag, uint6
 // passes: the last kernel of a pass resets the block the next pass will use.
 // The sweep folds each workgroup's slack range and ready count into one of
 // kParts slots (spreading the atomics over many addresses); the sort reduces
-// the slots with one wave.  With priority levels the slots hold the range of
-// the key within its level (key + level * 2^59) and a mask of the levels seen.
+// the slots with one wave.  With priority levels the slots also hold a mask of
+// the levels seen.
 constexpr int kParts = 64;
 
 struct Ctrl {
@@ -52,13 +48,13 @@ struct Ctrl {
   uint32_t sort_npass;           // digit passes the slack sort runs
   uint32_t bucket_overflow;      // a bucket of the bucketed sort overflowed
   uint32_t level_mask;           // priority levels seen (the next pass's bucket hint)
-  uint32_t pad;
+  uint32_t sort_level_pass;      // the last digit pass orders by priority level
   int64_t n_ready;
   int64_t slack_min;             // key range of the ready futures (all keys lie inside)
   int64_t slack_max;
-  int64_t hint_min;              // the range the host plans the next buckets from:
-  int64_t hint_max;              //   the key range, or with levels the in-level range
-  uint32_t tile_ticket[16];      // per radix pass: [0,8) slack sort, [8,12) grouping
+  int64_t hint_min;              // the range the host plans the next buckets from
+  int64_t hint_max;              //   (the key range)
+  uint32_t tile_ticket[16];      // per radix pass: [0,9) slack sort, [9,13) grouping
   int64_t part_min[kParts];
   int64_t part_max[kParts];
   int64_t part_cnt[kParts];
@@ -99,11 +95,20 @@ static_assert(kBucketLbMin % kBucketLbGroup == 0, "whole groups");
 constexpr uint32_t kStatusTiled = 0x20000000u;
 
 struct BucketSlot {
-  int64_t key;      // the order key: the slack, or -rem under NALAR_ORDER_LPT
+  int64_t key;      // the order key: the slack, or -rem / rem under NALAR_ORDER_LPT / _SRTF
   int64_t cost;
   int32_t pos;
-  int32_t route;
+  int32_t route;    // slot_pack(route, priority level)
 };
+
+// A slot's route field holds the route (-1 .. 1023) in its low 16 bits and
+// the future's priority level above them, so that a bucket holding futures of
+// several levels ranks them by (level descending, key, position).
+__host__ __device__ inline int32_t slot_pack(int32_t route, int lvl) {
+  return int32_t((uint32_t(route) & 0xFFFFu) | (uint32_t(lvl) << 16));
+}
+__host__ __device__ inline int32_t slot_route(int32_t packed) { return int32_t(int16_t(packed & 0xFFFF)); }
+__host__ __device__ inline int slot_level(int32_t packed) { return int((uint32_t(packed) >> 16) & 0xFFu); }
 
 // Written by the last kernel of a pass into pinned host memory.
 struct HostStatus {
@@ -125,6 +130,7 @@ __device__ inline void reset_ctrl(Ctrl* c) {
     c->status = 0;
     c->status_sweep = 0;
     c->sort_npass = 0;
+    c->sort_level_pass = 0;
     c->bucket_overflow = 0;
     c->n_ready = 0;
     c->slack_min = INT64_MAX;
@@ -149,6 +155,7 @@ __device__ inline void reset_ctrl_spread(Ctrl* c, int64_t gi, int64_t gstride) {
     c->status = 0;
     c->status_sweep = 0;
     c->sort_npass = 0;
+    c->sort_level_pass = 0;
     c->bucket_overflow = 0;
     c->n_ready = 0;
     c->slack_min = INT64_MAX;

@@ -12,7 +12,7 @@ namespace nalar {
 struct ProblemDev {
   int64_t N, E, W, M;
   int64_t now, mig;
-  uint32_t policy;              // NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL bits
+  uint32_t policy;              // NALAR_ORDER_* and NALAR_ROUTE_* bits
   uint32_t pad_;
   const int32_t* wf;
   const int32_t* type;
@@ -26,6 +26,7 @@ struct ProblemDev {
   const int64_t* inst_load;
   const int32_t* inst_speed;
   const uint8_t* prio;          // [W] priority level per workflow, or NULL
+  const uint32_t* inst_weight;  // [M] routing weights (NALAR_ROUTE_WEIGHTED), or NULL
 };
 
 enum RadixSource : int {
@@ -38,7 +39,7 @@ struct SortArgs {
   Ctrl* next_ctrl;              // reset here for the following pass
   HostStatus* host;             // pinned: status and ready count for the host
   const int64_t* stg_slack;     // [N] by position
-  const uint8_t* stg_ready;
+  const uint8_t* stg_ready;     // [N] by position: 1 + priority level if ready, else 0
   const int32_t* stg_route;
   const int64_t* stg_cost;
   const int32_t* node_of_pos;   // NULL: position == node id
@@ -73,10 +74,10 @@ struct GroupArgs {
 // Buckets of the bucketed slack sort (nb == 0: not used this pass).  Bucket of
 // a key k: min((k - lo) >> shift, nb - 1), 0 below lo.  With priority levels
 // (ngroups > 0) the buckets form ngroups groups of 2^lshift, one per level from
-// lvl_hi down; a key of level l falls into group lvl_hi - l by its in-level
-// value k + l * 2^59 (same mapping, 2^lshift buckets); a level above lvl_hi
-// takes bucket 0 and one below the last group bucket nb - 1, so buckets still
-// ascend with the key.
+// lvl_hi down; a key of level l falls into group lvl_hi - l (same mapping,
+// 2^lshift buckets); a level above lvl_hi takes bucket 0 and one below the
+// last group bucket nb - 1, so buckets still ascend in (-level, key), and the
+// ranking inside a bucket compares levels first.
 struct BucketArgs {
   int64_t lo;
   int32_t shift;
@@ -95,9 +96,10 @@ struct SweepArgs {
   const int32_t* node_of_pos;   // NULL: position == node id
   const int32_t* pos_of_node;   // NULL: position == node id
   int64_t* rem_out;             // [N] or NULL
-  uint8_t* stg_ready;           // [N] by position: 1 = ready
+  uint8_t* stg_ready;           // [N] by position: 1 + priority level if ready, else 0
   int64_t* stg_oslack;          // [N] by position: slack of ready futures when the
-                                //   sort key is not the slack (NALAR_ORDER_LPT)
+                                //   sort key is not the slack (NALAR_ORDER_LPT or
+                                //   _SRTF, or priority levels)
   int64_t* stg_slack;           // [N] by position, written for ready futures
   int32_t* stg_route;
   int64_t* stg_cost;
@@ -137,6 +139,59 @@ struct GreedyArgs {
   HostStatus* host;             // aux_status receives kStRange on a load overflow
 };
 hipError_t launch_route_greedy(hipStream_t s, const GreedyArgs& g);
+
+// Weighted routing over the ordered ready futures (weighted.hip).  The table
+// kernel also checks every weight against NALAR_WEIGHT_MAX (kStInval into
+// ctrl->status, so it runs before the sweep and the error keeps its
+// precedence); the other kernels run after a successful pass.
+struct WeightedArgs {
+  const int32_t* order;         // [R] the pass's output order
+  int64_t R;
+  const int32_t* type;
+  const int64_t* est;
+  const int32_t* loc;
+  const int32_t* inst_type;
+  const int64_t* inst_load;
+  const int32_t* inst_speed;
+  const uint32_t* inst_weight;
+  int32_t M;
+  int32_t stateful;             // NALAR_ROUTE_STATEFUL pins apply
+  int64_t mig;
+  int32_t* route;               // [R] overwritten for weighted futures
+  int64_t* cost;                // [R] or NULL
+  Ctrl* ctrl;                   // validation status of the pass
+  // scratch: the weighted instances sorted by (type, index)
+  int32_t* wt_type;
+  int32_t* wt_idx;
+  uint32_t* wt_cum;
+  uint32_t* wt_tot;
+  int32_t* wt_first;
+  int32_t* wt_cnt;
+  int32_t* n_wt;
+  uint32_t* counts;             // [tiles][NALAR_MAX_INSTANCES]
+  int64_t tiles;                // weighted_tiles(R)
+};
+int64_t weighted_tiles(int64_t R);
+hipError_t launch_weighted_table(hipStream_t s, const WeightedArgs& g);
+hipError_t launch_route_weighted(hipStream_t s, const WeightedArgs& g, void (*mark)(void*, const char*),
+                                 void* ctx);
+
+// Per-event decisions (decide.hip): one wavefront per event.
+struct DecideArgs {
+  ProblemDev p;
+  const int64_t* rem;           // [N] remaining critical path (the last pass's)
+  const int32_t* order;         // [n_order] the current order
+  const int64_t* slack;         // [n_order] aligned with order
+  int64_t n_order;
+  const int32_t* events;        // [n_events] future ids
+  int64_t n_events;
+  int64_t* slack_out;           // [n_events]
+  int32_t* route_out;
+  int64_t* cost_out;            // or NULL
+  int64_t* rank_out;            // or NULL
+  HostStatus* host;             // aux_status receives kStInval for an id out of range
+};
+hipError_t launch_decide(hipStream_t s, const DecideArgs& a);
 
 // Handle accessors for the graph store (store.hip), defined in api.hip.
 hipStream_t policy_stream(const nalar_policy* h);

@@ -19,9 +19,12 @@
 //    position of the ready future.  Its first pass reads the futures staged by
 //    position and skips positions that are not ready, so it also compacts them;
 //    the passes are stable, so equal slacks keep (wf, id) order, which makes the
-//    order exactly ascending (slack, wf, id).  Its last pass gathers each
-//    ready future's id, slack, route and cost straight into the caller's
-//    arrays;
+//    order exactly ascending (slack, wf, id).  With priority levels of more
+//    than one value, one more pass follows the key passes, whose digit is
+//    15 - level (read from the staged ready byte of the item's position), so
+//    that a higher level comes first and each level keeps its key order.  Its
+//    last pass gathers each ready future's id, slack, route and cost straight
+//    into the caller's arrays;
 //  * grouping futures by workflow when the caller's ids are not grouped:
 //    key = wf, payload = id; it ends by recording each node's position and
 //    each workflow's first position.
@@ -81,7 +84,8 @@ __device__ inline uint32_t block_excl_scan(uint32_t x, uint32_t* s_tmp) {
   return off + inc - x;
 }
 
-// Digit histograms (all npass digits) of the first pass's items, added into
+// Digit histograms (the npass key digits, and the level digit in row
+// level_row when it is not negative) of the first pass's items, added into
 // ghist.  H is a workgroup-private [kMaxSortPasses][256] array.  Each thread
 // takes kHistItems items per step, all loaded before any is used, so a
 // workgroup covers many items per memory round trip and few workgroups (few
@@ -89,7 +93,7 @@ __device__ inline uint32_t block_excl_scan(uint32_t x, uint32_t* s_tmp) {
 constexpr int kHistItems = 8;
 
 template <typename K>
-__device__ void histogram(const FirstSource& f, int npass, uint32_t (*H)[kRadixBuckets],
+__device__ void histogram(const FirstSource& f, int npass, int level_row, uint32_t (*H)[kRadixBuckets],
                           uint32_t* ghist) {
   for (int i = threadIdx.x; i < kMaxSortPasses * kRadixBuckets; i += kSortThreads) (&H[0][0])[i] = 0;
   __syncthreads();
@@ -97,12 +101,16 @@ __device__ void histogram(const FirstSource& f, int npass, uint32_t (*H)[kRadixB
   for (int64_t base = int64_t(blockIdx.x) * kSortThreads * kHistItems; base < f.span; base += stride) {
     bool valid[kHistItems];
     K key[kHistItems];
+    uint32_t ldg[kHistItems];  // level digit: 15 - level
 #pragma unroll
     for (int u = 0; u < kHistItems; ++u) {  // every load first (in bounds; stale keys are dropped)
       const int64_t i = base + int64_t(u) * kSortThreads + threadIdx.x;
       const bool in = i < f.span;
+      ldg[u] = 0;
       if (f.mode == kSrcStaged) {
-        valid[u] = in && f.stg_ready[in ? i : 0] != 0;
+        const uint32_t rd = f.stg_ready[in ? i : 0];
+        valid[u] = in && rd != 0;
+        ldg[u] = (16u - rd) & 15u;
         key[u] = K(uint64_t(f.stg_slack[in ? i : 0] - f.smin));
       } else {
         valid[u] = in;
@@ -123,9 +131,13 @@ __device__ void histogram(const FirstSource& f, int npass, uint32_t (*H)[kRadixB
           atomicAdd(&H[ps][dg], 1u);
         }
       }
+      if (level_row >= 0 && valid[u]) atomicAdd(&H[level_row][ldg[u]], 1u);
     }
   }
   __syncthreads();
+  if (level_row >= 0)
+    for (int b = threadIdx.x; b < 16; b += kSortThreads)
+      if (H[level_row][b]) atomicAdd(&ghist[level_row * kRadixBuckets + b], H[level_row][b]);
   for (int ps = 0; ps < npass; ++ps)
     for (int b = threadIdx.x; b < kRadixBuckets; b += kSortThreads)
       if (H[ps][b]) atomicAdd(&ghist[ps * kRadixBuckets + b], H[ps][b]);
@@ -146,15 +158,17 @@ struct FinalOut {
   int64_t* cost;
 };
 
+// level_of: non-NULL in the priority-level pass, whose digit is 15 - level
+// read from level_of[payload] (1 + level), instead of a digit of the key.
 template <typename K>
 __device__ void radix_tile(TileSmem<K>& S, const FirstSource& f, bool first, int pass, int64_t tile,
                            int64_t span, int64_t R, const K* kin, const uint32_t* pin, K* kout,
                            uint32_t* pout, const uint32_t* ghist_row, uint64_t* lb_pass,
-                           uint32_t epoch, const FinalOut& fo) {
+                           uint32_t epoch, const FinalOut& fo, const uint8_t* level_of = nullptr) {
   const int tid = threadIdx.x;
   const int wv = tid / kWave;
   const int ln = lane_id();
-  const int shift = pass * kRadixBits;
+  const int shift = level_of ? 0 : pass * kRadixBits;
   for (int i = tid; i < kWavesPerTile * kRadixBuckets; i += kSortThreads) (&S.whist[0][0])[i] = 0;
   __syncthreads();
   const int64_t seg = tile * kSortTile + int64_t(wv) * (kWave * kSortItems);
@@ -179,6 +193,11 @@ __device__ void radix_tile(TileSmem<K>& S, const FirstSource& f, bool first, int
       pay[j] = pin[i];
       validm |= 1u << j;
     }
+  }
+  if (level_of) {  // the key's digits are done: the level decides this pass
+#pragma unroll
+    for (int j = 0; j < kSortItems; ++j)
+      if ((validm >> j) & 1u) key[j] = K((16u - uint32_t(level_of[pay[j]])) & 15u);
   }
 
   // In-wave stable ranking: lanes with equal digits found by 8 ballots; the
@@ -286,30 +305,28 @@ __device__ inline RangeLanes load_range_lanes(const Ctrl* ctrl, bool levels) {
 // Slack range, ready count and pass count from the sweep's slots (one wave;
 // every thread of the workgroup calls it).  s_range = {min key, ready count,
 // digit passes, significant key bits, max key, hint min, hint max, level
-// mask}.  Without levels the hint is the key range.  With levels the slots
-// hold the in-level range [lo, hi] and the levels seen [l0, l1]: every key
-// lies in [lo - l1 * 2^59, hi - l0 * 2^59], the range the radix passes cover,
-// and the hint is [lo, hi] with the mask.
+// mask, level pass}.  The hint is the key range; with levels the mask of the
+// levels seen goes with it, and when more than one level is present the
+// passes end with the level pass.
+constexpr int kRangeWords = 9;
+
 __device__ void settle_range(const RangeLanes& rl, Ctrl* ctrl, int64_t* s_range, bool write,
                              bool levels) {
   if (threadIdx.x < kWave) {
-    int64_t mn = wave_min_i64(rl.mn);
-    int64_t mx = wave_max_i64(rl.mx);
+    const int64_t mn = wave_min_i64(rl.mn);
+    const int64_t mx = wave_max_i64(rl.mx);
     const int64_t ct = wave_sum_i64(rl.ct);
     const uint32_t lm = levels ? wave_or_u32(rl.lm) : 0u;
     if (threadIdx.x == 0) {
       const int64_t hmin = mn, hmax = mx;
-      if (levels && ct > 0 && lm != 0) {
-        const int l0 = __builtin_ctz(lm), l1 = 31 - __builtin_clz(lm);
-        mn -= int64_t(l1) << kPrioShift;
-        mx -= int64_t(l0) << kPrioShift;
-      }
-      int npass = 0, nbits = 0;
+      int npass = 0, nbits = 0, lpass = 0;
       if (ct > 0) {
-        const uint64_t range = uint64_t(mx - mn);
+        const uint64_t range = uint64_t(mx) - uint64_t(mn);
         nbits = range ? 64 - __builtin_clzll(range) : 0;
         npass = (nbits + kRadixBits - 1) / kRadixBits;
         if (npass == 0) npass = 1;  // the first pass also compacts
+        lpass = (lm & (lm - 1)) != 0 ? 1 : 0;
+        npass += lpass;
       }
       s_range[0] = mn;
       s_range[1] = ct;
@@ -319,6 +336,7 @@ __device__ void settle_range(const RangeLanes& rl, Ctrl* ctrl, int64_t* s_range,
       s_range[5] = hmin;
       s_range[6] = hmax;
       s_range[7] = int64_t(lm);
+      s_range[8] = lpass;
       if (write) {
         ctrl->n_ready = ct;
         ctrl->slack_min = mn;
@@ -327,6 +345,7 @@ __device__ void settle_range(const RangeLanes& rl, Ctrl* ctrl, int64_t* s_range,
         ctrl->hint_max = hmax;
         ctrl->level_mask = lm;
         ctrl->sort_npass = uint32_t(npass);
+        ctrl->sort_level_pass = uint32_t(lpass);
       }
     }
   }
@@ -365,7 +384,7 @@ constexpr int kGroupSlots = kBucketGroup * kBucketCap;
 // its bucket-mates by (slack, position).  Positions ascend in (workflow, id),
 // so that is the rank by (slack, workflow, id).
 __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, BucketArgs bk) {
-  __shared__ int64_t s_range[8];
+  __shared__ int64_t s_range[kRangeWords];
   __shared__ uint32_t s_off[kBucketGroup + 1];
   __shared__ uint32_t s_red[kBucketThreads / kWave];
   __shared__ int64_t s_slack[kGroupSlots];
@@ -438,15 +457,25 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket_sort(SortArgs a, Buck
     const int64_t sk = s_slack[i];
     const int32_t ps = s_pos[i];
     int rank = 0;
+    if (a.levels) {  // a bucket may hold several levels: (level desc, key, position)
+      const int sl = slot_level(s_route[i]);
+#pragma unroll 4
+      for (int j = lo; j < hi; ++j) {
+        const int64_t o = s_slack[j];
+        const int ol = slot_level(s_route[j]);
+        rank += (ol > sl) | ((ol == sl) & ((o < sk) | ((o == sk) & (s_pos[j] < ps))));
+      }
+    } else {
 #pragma unroll 8
-    for (int j = lo; j < hi; ++j) {  // independent LDS loads: unrolled, they overlap
-      const int64_t o = s_slack[j];
-      rank += (o < sk) | ((o == sk) & (s_pos[j] < ps));
+      for (int j = lo; j < hi; ++j) {  // independent LDS loads: unrolled, they overlap
+        const int64_t o = s_slack[j];
+        rank += (o < sk) | ((o == sk) & (s_pos[j] < ps));
+      }
     }
     const int64_t out = base + lo + rank;
     a.order[out] = a.node_of_pos ? a.node_of_pos[ps] : ps;
     a.slack[out] = a.out_slack ? a.out_slack[ps] : sk;
-    a.route[out] = s_route[i];
+    a.route[out] = slot_route(s_route[i]);
     if (a.cost) a.cost[out] = s_cost[i];
   }
 }
@@ -487,13 +516,14 @@ constexpr int kLbStage = 2048;  // futures of a bucket group staged in LDS at on
 static_assert(kLbStage % kBucketLbGroup == 0, "whole rows of the workgroup");
 
 __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, BucketArgs bk) {
-  __shared__ int64_t s_range[8];
+  __shared__ int64_t s_range[kRangeWords];
   __shared__ uint32_t s_off[kBucketLbGroup + 1];
   __shared__ uint32_t s_red[kBucketLbGroup / kWave];
   __shared__ int64_t s_base[kBucketLbGroup / kWave];
   __shared__ int64_t s_slack[kLbStage];
   __shared__ int32_t s_pos[kLbStage];
   __shared__ uint8_t s_b[kLbStage];
+  __shared__ uint8_t s_lv[kLbStage];  // priority level (with levels only)
   const int tid = threadIdx.x;
   const int wv = tid / kWave;
   const int g = blockIdx.x;
@@ -601,6 +631,7 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
       if (i < ce) {
         s_slack[i - cs] = v[u].key;
         s_pos[i - cs] = v[u].pos;
+        if (a.levels) s_lv[i - cs] = uint8_t(slot_level(v[u].route));
       }
     }
     __syncthreads();
@@ -612,15 +643,25 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
       const int k0 = int(s_off[lb]);
       const int k1 = int(s_off[lb + 1]);  // inside [cs, ce]: chunks end at bucket boundaries
       int rank = 0;
+      if (a.levels) {  // a bucket may hold several levels: (level desc, key, position)
+        const int sl = slot_level(v[u].route);
+#pragma unroll 4
+        for (int j = k0 - cs; j < k1 - cs; ++j) {
+          const int64_t o = s_slack[j];
+          const int ol = s_lv[j];
+          rank += (ol > sl) | ((ol == sl) & ((o < v[u].key) | ((o == v[u].key) & (s_pos[j] < v[u].pos))));
+        }
+      } else {
 #pragma unroll 8
-      for (int j = k0 - cs; j < k1 - cs; ++j) {  // independent LDS loads: unrolled, they overlap
-        const int64_t o = s_slack[j];
-        rank += (o < v[u].key) | ((o == v[u].key) & (s_pos[j] < v[u].pos));
+        for (int j = k0 - cs; j < k1 - cs; ++j) {  // independent LDS loads: unrolled, they overlap
+          const int64_t o = s_slack[j];
+          rank += (o < v[u].key) | ((o == v[u].key) & (s_pos[j] < v[u].pos));
+        }
       }
       const int64_t out = base + k0 + rank;
       a.order[out] = on[u];
       a.slack[out] = os[u];
-      a.route[out] = v[u].route;
+      a.route[out] = slot_route(v[u].route);
       if (a.cost) a.cost[out] = v[u].cost;
     }
     __syncthreads();
@@ -629,7 +670,7 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
 
 __global__ __launch_bounds__(kSortThreads) void k_slack_hist(SortArgs a) {
   __shared__ uint32_t H[kMaxSortPasses][kRadixBuckets];
-  __shared__ int64_t s_range[8];
+  __shared__ int64_t s_range[kRangeWords];
   Ctrl* ctrl = a.ctrl;
   const uint32_t status = ctrl->status | ctrl->status_sweep;
   if (status) {
@@ -643,7 +684,8 @@ __global__ __launch_bounds__(kSortThreads) void k_slack_hist(SortArgs a) {
     return;
   }
   const FirstSource f{kSrcStaged, a.stg_slack, a.stg_ready, nullptr, a.span, s_range[0]};
-  histogram<uint64_t>(f, npass, H, ctrl->ghist_slack);
+  const int lpass = int(s_range[8]);
+  histogram<uint64_t>(f, npass - lpass, lpass ? npass - 1 : -1, H, ctrl->ghist_slack);
 }
 
 // One digit pass of the slack sort.  The last pass the key range needs writes
@@ -658,6 +700,7 @@ __global__ __launch_bounds__(kSortThreads) void k_slack_pass(SortArgs a, int pas
   const int64_t R = ctrl->n_ready;
   const bool first = pass == 0;
   const bool last = pass == npass - 1;
+  const bool level_pass = last && ctrl->sort_level_pass != 0;
   const int64_t span = first ? a.span : R;
   const int64_t ntiles = (span + kSortTile - 1) / kSortTile;
   if (threadIdx.x == 0) S.tile = atomicAdd(&ctrl->tile_ticket[pass], 1u);
@@ -671,7 +714,8 @@ __global__ __launch_bounds__(kSortThreads) void k_slack_pass(SortArgs a, int pas
   radix_tile<uint64_t>(S, f, first, pass, tile, span, R, a.key[(pass + 1) & 1],
                        a.pay[(pass + 1) & 1], a.key[pass & 1], a.pay[pass & 1],
                        ctrl->ghist_slack + pass * kRadixBuckets,
-                       a.lookback + int64_t(pass) * a.tiles_cap * kRadixBuckets, a.epoch, fo);
+                       a.lookback + int64_t(pass) * a.tiles_cap * kRadixBuckets, a.epoch, fo,
+                       level_pass ? a.stg_ready : nullptr);
   if (tile == 0 && threadIdx.x == 0) {
     const int64_t smax = ctrl->slack_max;
     const int nbits = 64 - __builtin_clzll(uint64_t(smax - smin) | 1);
@@ -685,7 +729,7 @@ __global__ __launch_bounds__(kSortThreads) void k_group_hist(GroupArgs a) {
   __shared__ uint32_t H[kMaxSortPasses][kRadixBuckets];
   if (a.ctrl->status) return;
   const FirstSource f{kSrcWf, nullptr, nullptr, a.p.wf, a.p.N, 0};
-  histogram<uint32_t>(f, a.npass, H, a.ctrl->ghist_group);
+  histogram<uint32_t>(f, a.npass, -1, H, a.ctrl->ghist_group);
 }
 
 __global__ __launch_bounds__(kSortThreads) void k_group_pass(GroupArgs a, int pass) {
@@ -694,7 +738,7 @@ __global__ __launch_bounds__(kSortThreads) void k_group_pass(GroupArgs a, int pa
   if (ctrl->status) return;
   const int64_t N = a.p.N;
   const int64_t ntiles = (N + kSortTile - 1) / kSortTile;
-  if (threadIdx.x == 0) S.tile = atomicAdd(&ctrl->tile_ticket[8 + pass], 1u);
+  if (threadIdx.x == 0) S.tile = atomicAdd(&ctrl->tile_ticket[kMaxSortPasses + pass], 1u);
   __syncthreads();
   const int64_t tile = S.tile;
   if (tile >= ntiles) return;
@@ -765,8 +809,9 @@ hipError_t launch_slack_sort(hipStream_t s, const SortArgs& a, int first_pass, i
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  static const char* names[kMaxSortPasses] = {"sort_pass0", "sort_pass1", "sort_pass2", "sort_pass3",
-                                              "sort_pass4", "sort_pass5", "sort_pass6", "sort_pass7"};
+  static const char* names[kMaxSortPasses] = {"sort_pass0", "sort_pass1", "sort_pass2",
+                                              "sort_pass3", "sort_pass4", "sort_pass5",
+                                              "sort_pass6", "sort_pass7", "sort_pass8"};
   for (int ps = first_pass; ps <= last_pass; ++ps) {
     mark(ctx, names[ps]);
     hipLaunchKernelGGL(k_slack_pass, dim3(grid_of(a.span, kSortTile, INT32_MAX)), dim3(kSortThreads),

@@ -237,7 +237,7 @@ int64_t nalar_store_n_nodes(const nalar_store* st) { return st ? st->N : -1; }
 int nalar_store_pass(nalar_store* st, int64_t now_us, int64_t migration_cost_us, uint32_t policy,
                      nalar_result* r) {
   if (!st) return NALAR_EINVAL;
-  if ((policy & ~(NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL | NALAR_ROUTE_GREEDY)) != 0)
+  if ((policy & ~(NALAR_ORDER_LPT | NALAR_ORDER_SRTF | NALAR_ROUTE_STATEFUL | NALAR_ROUTE_GREEDY)) != 0)
     return policy_fail(st->h, NALAR_EINVAL, "store pass: unknown policy bits");
   nalar_problem p;
   std::memset(&p, 0, sizeof(p));

@@ -222,98 +222,93 @@ struct Acc {
   int64_t tready = 0;
 };
 
-// Bucket of a key under this pass's bucket boundaries (kofs: the key offset of
-// its priority level), and a slot in it (one returning atomic; claim early so
-// that its latency overlaps other work).  Every result lies in [0, nb).
+// Bucket of a key under this pass's bucket boundaries (lvl: the priority
+// level of its workflow), and a slot in it (one returning atomic; claim early
+// so that its latency overlaps other work).  Every result lies in [0, nb).
 // kLevels: the mapping may have level groups (the block kernel takes none,
 // which keeps it within its registers; the host then plans no buckets).
 template <bool kLevels>
-__device__ inline uint32_t bucket_of(const BucketArgs& bk, int64_t key, int64_t kofs) {
+__device__ inline uint32_t bucket_of(const BucketArgs& bk, int64_t key, int lvl) {
   // the workflow's part (the same on every lane): its level's group of
-  // buckets [base, base + last] and the lower bound shifted by the key offset
-  int64_t lo = bk.lo;
+  // buckets [base, base + last]
   uint32_t base = 0, last = uint32_t(bk.nb - 1);
   if (kLevels && bk.ngroups > 0) {
-    const int32_t g = bk.lvl_hi - int32_t(uint32_t(uint64_t(-kofs) >> kPrioShift) & 31u);
+    const int32_t g = bk.lvl_hi - int32_t(lvl);
     const bool in = g >= 0 && g < bk.ngroups;
     base = g < 0 ? 0u : (in ? uint32_t(g) << bk.lshift : last);
     last = in ? (1u << bk.lshift) - 1u : 0u;
-    lo = int64_t(uint64_t(lo) + uint64_t(kofs));
   }
-  const uint64_t d = key > lo ? uint64_t(key) - uint64_t(lo) : 0;
+  const uint64_t d = key > bk.lo ? uint64_t(key) - uint64_t(bk.lo) : 0;
   const uint64_t q = d >> bk.shift;
   return base + (q < uint64_t(last) ? uint32_t(q) : last);
 }
 
 __device__ inline void bucket_put(const SweepArgs& a, uint32_t bkt, uint32_t slot, int64_t key,
-                                  int64_t pos, int32_t route, int64_t cost) {
+                                  int64_t pos, int32_t route, int lvl, int64_t cost) {
   if (slot < uint32_t(kBucketCap)) {
     BucketSlot* sl = a.bk.slot + int64_t(bkt) * kBucketCap + slot;
     sl->key = key;
     sl->cost = cost;
     sl->pos = int32_t(pos);
-    sl->route = route;
+    sl->route = slot_pack(route, lvl);
   } else {
     st_relaxed_agent(&a.ctrl->bucket_overflow, 1u);
   }
 }
 
-// The key the ready futures are ordered by: the slack, or under
-// NALAR_ORDER_LPT the negated remaining critical path (longest first); with
-// priority levels, minus level * 2^59 (kofs), so that a higher level comes
-// first while keys stay inside (-2^58, 2^58) (checked in store_ready).
-__device__ inline int64_t order_key(const SweepArgs& a, int64_t rem, int64_t dl, int64_t kofs) {
-  return ((a.p.policy & NALAR_ORDER_LPT) ? -rem : dl - rem) + kofs;
+// The key the ready futures are ordered by (behind their workflow's priority
+// level): the slack, or the remaining critical path negated under
+// NALAR_ORDER_LPT (longest first) or as it is under NALAR_ORDER_SRTF
+// (shortest first).
+__device__ inline int64_t order_key(const SweepArgs& a, int64_t rem, int64_t dl) {
+  if (a.p.policy & NALAR_ORDER_LPT) return -rem;
+  if (a.p.policy & NALAR_ORDER_SRTF) return rem;
+  return dl - rem;
 }
 
-// The key offset of workflow w's priority level (0 without levels); w is the
-// same on every lane, so the level goes to a scalar register.
-__device__ inline int64_t prio_offset(const SweepArgs& a, int64_t w) {
-  return a.p.prio ? -(int64_t(__builtin_amdgcn_readfirstlane(int(a.p.prio[w]))) << kPrioShift) : 0;
+// Workflow w's priority level (0 without levels); w is the same on every
+// lane, so the level goes to a scalar register.
+__device__ inline int prio_level(const SweepArgs& a, int64_t w) {
+  return a.p.prio ? __builtin_amdgcn_readfirstlane(int(a.p.prio[w])) : 0;
 }
 
-// The mask bit of the level a key offset stands for.
-__device__ inline uint32_t level_bit(int64_t kofs) {
-  return 1u << (uint32_t(uint64_t(-kofs) >> kPrioShift) & 31u);
-}
+__device__ inline uint32_t level_bit(int lvl) { return 1u << (uint32_t(lvl) & 31u); }
 
 // Stores of one ready future: its bucket slot (bucketed sort) or its staged
 // values by position (tiled sort), and its slack by position when the key is
 // not the slack.
 __device__ inline void store_ready(const SweepArgs& a, uint32_t bkt, uint32_t slot, int64_t key,
-                                   int64_t kofs, int64_t slack, int64_t pos, int32_t route, int64_t cost,
+                                   int lvl, int64_t slack, int64_t pos, int32_t route, int64_t cost,
                                    Acc& acc) {
-  const int64_t kr = a.p.prio ? key - kofs : key;  // the key within its level
-  if (a.p.prio && (kr <= -kPrioKeyBound || kr >= kPrioKeyBound)) flag_sweep(a.ctrl, kStRange);
   if (a.bk.nb > 0) {
-    bucket_put(a, bkt, slot, key, pos, route, cost);
+    bucket_put(a, bkt, slot, key, pos, route, lvl, cost);
   } else {
     a.stg_slack[pos] = key;
     a.stg_route[pos] = route;
     a.stg_cost[pos] = cost;
   }
-  if ((a.p.policy & NALAR_ORDER_LPT) || a.p.prio) a.stg_oslack[pos] = slack;
-  acc.tmin = kr < acc.tmin ? kr : acc.tmin;
-  acc.tmax = kr > acc.tmax ? kr : acc.tmax;
+  if ((a.p.policy & (NALAR_ORDER_LPT | NALAR_ORDER_SRTF)) || a.p.prio) a.stg_oslack[pos] = slack;
+  acc.tmin = key < acc.tmin ? key : acc.tmin;
+  acc.tmax = key > acc.tmax ? key : acc.tmax;
   acc.tready += 1;
 }
 
 template <bool kLevels>
 __device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_t pos, int32_t type,
-                                   int32_t loc, int64_t rem, int64_t est, int64_t dl, int64_t kofs,
+                                   int32_t loc, int64_t rem, int64_t est, int64_t dl, int lvl,
                                    Acc& acc) {
-  const int64_t key = order_key(a, rem, dl, kofs);
+  const int64_t key = order_key(a, rem, dl);
   const BucketArgs& bk = a.bk;
   uint32_t bkt = 0, slot = 0;
   if (bk.nb > 0) {
-    bkt = bucket_of<kLevels>(bk, key, kofs);
+    bkt = bucket_of<kLevels>(bk, key, lvl);
     slot = add_agent(bk.cnt + bkt, 1u);
   }
   int32_t route;
   int64_t cost;
   route_future(type, est, loc, int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load, it.speed,
                it.inv, it.pos, it.run, (a.p.policy & NALAR_ROUTE_STATEFUL) != 0, route, cost);
-  store_ready(a, bkt, slot, key, kofs, dl - rem, pos, route, cost, acc);
+  store_ready(a, bkt, slot, key, lvl, dl - rem, pos, route, cost, acc);
 }
 
 // ------------------------------------------------------------ LDS workflow
@@ -332,7 +327,7 @@ __device__ inline int dep_at(uint32_t p01, uint32_t p2, int q) {
 template <int T, int NPT>
 __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
                           int64_t* mx, int32_t* cnt, uint8_t* dn, uint8_t* nr, int lds_cap, int64_t b,
-                          int n, int64_t dl, int64_t kofs, Acc& acc) {
+                          int n, int64_t dl, int lvl, Acc& acc) {
   const int tid = threadIdx.x;
   Ctrl* ctrl = a.ctrl;
 
@@ -432,7 +427,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
       const int k = j * T + tid;
       const bool rd = dn[k] == 0 && nr[k] == 0;
       if (rd) ready |= 1u << j;
-      if (a.bk.nb == 0) a.stg_ready[b + k] = rd ? 1 : 0;
+      if (a.bk.nb == 0) a.stg_ready[b + k] = rd ? uint8_t(1 + lvl) : 0;
     }
   }
   if (tid == 0) S.hcount = 0;
@@ -517,7 +512,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
     bkt[j] = 0;
     slot[j] = 0;
     if (bk.nb > 0 && ((ready >> j) & 1u)) {
-      bkt[j] = bucket_of<false>(bk, order_key(a, mx[j * T + tid], dl, kofs), kofs);
+      bkt[j] = bucket_of<false>(bk, order_key(a, mx[j * T + tid], dl), lvl);
       slot[j] = add_agent(bk.cnt + bkt[j], 1u);
     }
   }
@@ -543,7 +538,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
   for (int j = 0; j < NPT; ++j) {
     if (!((ready >> j) & 1u)) continue;
     const int k = j * T + tid;
-    store_ready(a, bkt[j], slot[j], order_key(a, mx[k], dl, kofs), kofs, dl - mx[k], b + k, route[j],
+    store_ready(a, bkt[j], slot[j], order_key(a, mx[k], dl), lvl, dl - mx[k], b + k, route[j],
                 cost[j], acc);
   }
 }
@@ -552,7 +547,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
 
 template <int T, bool kFused, bool kLevels>
 __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
-                          int w, int64_t b, int n, int64_t dl, int64_t kofs, Acc& acc) {
+                          int w, int64_t b, int n, int64_t dl, int lvl, Acc& acc) {
   const int tid = threadIdx.x;
   Ctrl* ctrl = a.ctrl;
   int32_t* cnt = a.g_cnt + b;
@@ -641,7 +636,7 @@ __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, con
   __syncthreads();
 
   if (a.bk.nb == 0)
-    for (int k = tid; k < n; k += T) a.stg_ready[b + k] = (dn[k] == 0 && nr[k] == 0) ? 1 : 0;
+    for (int k = tid; k < n; k += T) a.stg_ready[b + k] = (dn[k] == 0 && nr[k] == 0) ? uint8_t(1 + lvl) : 0;
   if (tid == 0) S.hcount = 0;
 
   // frontier 0: futures without consumers
@@ -728,7 +723,7 @@ __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, con
   for (int k = tid; k < n; k += T) {
     if (dn[k] == 0 && nr[k] == 0) {
       const int32_t v = node_at(L, b + k);
-      write_ready<kLevels>(a, it, b + k, a.p.type[v], a.p.loc[v], ld_wg(&mx[k]), a.p.est[v], dl, kofs, acc);
+      write_ready<kLevels>(a, it, b + k, a.p.type[v], a.p.loc[v], ld_wg(&mx[k]), a.p.est[v], dl, lvl, acc);
     }
   }
   __syncthreads();
@@ -962,7 +957,7 @@ struct Seg {
   int c[G + 1];
   int64_t w[G];
   int64_t dl[G];
-  int64_t kofs[G];
+  int lvl[G];
   // the part of local index k
   __device__ int part(int k) const {
     int s = 0;
@@ -1267,7 +1262,7 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
     slot[j] = 0;
     if (bk.nb > 0 && ((ready >> j) & 1u)) {
       const int pk = sg.part(j * kWave + ln);
-      bkt[j] = bucket_of<true>(bk, order_key(a, rr[j], sg.dl[pk], sg.kofs[pk]), sg.kofs[pk]);
+      bkt[j] = bucket_of<true>(bk, order_key(a, rr[j], sg.dl[pk]), sg.lvl[pk]);
       slot[j] = add_agent(bk.cnt + bkt[j], 1u);
     }
   }
@@ -1288,12 +1283,12 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
   for (int j = 0; j < NPTW; ++j) {
     if (!((own >> j) & 1u)) continue;
     const int64_t pos = b + j * kWave + ln;
-    if (bk.nb == 0) a.stg_ready[pos] = uint8_t((ready >> j) & 1u);
+    if (bk.nb == 0) a.stg_ready[pos] = ((ready >> j) & 1u) ? uint8_t(1 + sg.lvl[sg.part(j * kWave + ln)]) : uint8_t(0);
     if (a.rem_out) a.rem_out[vv[j]] = rr[j];
     if ((ready >> j) & 1u) {
       const int pk = sg.part(j * kWave + ln);
-      const int64_t dl = sg.dl[pk], kofs = sg.kofs[pk];
-      store_ready(a, bkt[j], slot[j], order_key(a, rr[j], dl, kofs), kofs, dl - rr[j], pos, route[j],
+      const int64_t dl = sg.dl[pk];
+      store_ready(a, bkt[j], slot[j], order_key(a, rr[j], dl), sg.lvl[pk], dl - rr[j], pos, route[j],
                   cost[j], acc);
     }
   }
@@ -1346,12 +1341,12 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
     const int n = a.wf_off[w + 1] - int32_t(b);
     if (n <= 0) continue;
     const int64_t dl = a.p.deadline[w] - a.p.now;
-    const int64_t kofs = prio_offset(a, w);
-    lmask |= level_bit(kofs);
+    const int lvl = prio_level(a, w);
+    lmask |= level_bit(lvl);
     if (!a.force_global && n <= lds_cap)
-      sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, lds_cap, b, n, dl, kofs, acc);
+      sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, lds_cap, b, n, dl, lvl, acc);
     else
-      sweep_hbm<T, false, false>(a, L, it, S, int(w), b, n, dl, kofs, acc);
+      sweep_hbm<T, false, false>(a, L, it, S, int(w), b, n, dl, lvl, acc);
   }
 
   // fold the block's slack range and ready count into the control block
@@ -1590,7 +1585,7 @@ __device__ inline Seg<G> make_seg(const SweepArgs& a, int64_t pw, int32_t lbv, i
   for (int i = 0; i < G; ++i) {
     sg.w[i] = w0 + i;
     sg.dl[i] = readlane_i64(rawv, i) - a.p.now;
-    sg.kofs[i] = i < sg.ns ? prio_offset(a, w0 + i) : 0;
+    sg.lvl[i] = i < sg.ns ? prio_level(a, w0 + i) : 0;
   }
   if (kFused && ln < sg.ns) {
     const int64_t w = w0 + ln;
@@ -1773,7 +1768,7 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
     for (int i = 0; i < G; ++i) {
       const int ni = sg.c[i + 1] - sg.c[i];
       if (i < sg.ns && ni > 0) {
-        lmask |= level_bit(sg.kofs[i]);
+        lmask |= level_bit(sg.lvl[i]);
         if (ni > wcap || a.force_global) gbig = true;
         else any = true;
       }
@@ -1798,7 +1793,7 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
       one.c[1] = ni;
       one.w[0] = sg.w[i];
       one.dl[0] = sg.dl[i];
-      one.kofs[0] = sg.kofs[i];
+      one.lvl[0] = sg.lvl[i];
       sweep_wave<NPTW, kFused, G>(a, L, it, Wv, one, acc, st, pre, use_pre && i == 0);
     }
   }
@@ -1815,9 +1810,9 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
         int n;
         wf_bounds(a, w, b, n);
         if (n <= 0 || (n <= wcap && !a.force_global)) continue;
-        const int64_t kofs = prio_offset(a, w);
-        lmask |= level_bit(kofs);
-        sweep_hbm<kWaveBlock, kFused, true>(a, L, it, S, int(w), b, n, a.p.deadline[w] - a.p.now, kofs, acc);
+        const int lvl = prio_level(a, w);
+        lmask |= level_bit(lvl);
+        sweep_hbm<kWaveBlock, kFused, true>(a, L, it, S, int(w), b, n, a.p.deadline[w] - a.p.now, lvl, acc);
       }
     }
   }

@@ -12,8 +12,11 @@ device tensors.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
+import sys
+import weakref
 from dataclasses import dataclass
 from typing import Optional
 
@@ -25,11 +28,13 @@ NALAR_WF_CONTIGUOUS = 1
 NALAR_ORDER_LPT = 2          # problem flag: order by remaining critical path, longest first
 NALAR_ROUTE_STATEFUL = 4     # problem flag: route a future to the instance of its type holding its state
 NALAR_ROUTE_GREEDY = 8       # problem flag: route in output order with running instance loads
+NALAR_ORDER_SRTF = 16        # problem flag: order by remaining critical path, shortest first
+NALAR_ROUTE_WEIGHTED = 32    # problem flag: deal each type's futures to its instances by weight
 NALAR_FORCE_GLOBAL_SWEEP = 1
 NALAR_FORCE_TILED_SORT = 2
 NALAR_MAX_INSTANCES = 1024
 
-EXPORTED = ("nalar_policy_create", "nalar_policy_pass", "nalar_policy_destroy",
+EXPORTED = ("nalar_policy_create", "nalar_policy_pass", "nalar_policy_destroy", "nalar_policy_decide",
             "nalar_policy_last_error", "nalar_policy_set_timing", "nalar_policy_get_timing",
             "nalar_store_create", "nalar_store_destroy", "nalar_store_append", "nalar_store_complete",
             "nalar_store_set_workflows", "nalar_store_set_instances", "nalar_store_n_nodes",
@@ -51,13 +56,24 @@ class NalarProblem(ctypes.Structure):
                 ("done", ctypes.c_void_p), ("loc", ctypes.c_void_p), ("dep_off", ctypes.c_void_p),
                 ("dep_idx", ctypes.c_void_p), ("deadline_us", ctypes.c_void_p),
                 ("inst_type", ctypes.c_void_p), ("inst_load_us", ctypes.c_void_p),
-                ("inst_speed_permille", ctypes.c_void_p), ("wf_priority", ctypes.c_void_p)]
+                ("inst_speed_permille", ctypes.c_void_p), ("wf_priority", ctypes.c_void_p),
+                ("inst_weight", ctypes.c_void_p)]
 
 
 class NalarResult(ctypes.Structure):
     _fields_ = [("rem_us", ctypes.c_void_p), ("order", ctypes.c_void_p),
                 ("slack_us", ctypes.c_void_p), ("route", ctypes.c_void_p),
                 ("cost_us", ctypes.c_void_p), ("n_ready", ctypes.c_int64)]
+
+
+class NalarView(ctypes.Structure):
+    _fields_ = [("rem_us", ctypes.c_void_p), ("order", ctypes.c_void_p),
+                ("slack_us", ctypes.c_void_p), ("n_order", ctypes.c_int64)]
+
+
+class NalarDecisions(ctypes.Structure):
+    _fields_ = [("slack_us", ctypes.c_void_p), ("route", ctypes.c_void_p),
+                ("cost_us", ctypes.c_void_p), ("rank", ctypes.c_void_p)]
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -77,6 +93,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.nalar_policy_create.restype = ctypes.c_int
     lib.nalar_policy_pass.argtypes = [H, ctypes.POINTER(NalarProblem), ctypes.POINTER(NalarResult)]
     lib.nalar_policy_pass.restype = ctypes.c_int
+    lib.nalar_policy_decide.argtypes = [H, ctypes.POINTER(NalarProblem), ctypes.POINTER(NalarView),
+                                        ctypes.c_int64, ctypes.c_void_p, ctypes.POINTER(NalarDecisions)]
+    lib.nalar_policy_decide.restype = ctypes.c_int
     lib.nalar_policy_destroy.argtypes = [H]
     lib.nalar_policy_destroy.restype = None
     lib.nalar_policy_last_error.argtypes = [H]
@@ -118,6 +137,12 @@ def nalar_policy_create(cfg: NalarPolicyConfig) -> tuple[int, Optional[int]]:
 
 def nalar_policy_pass(h: int, prob: NalarProblem, res: NalarResult) -> int:
     return load_library().nalar_policy_pass(h, ctypes.byref(prob), ctypes.byref(res))
+
+
+def nalar_policy_decide(h: int, prob: NalarProblem, view: NalarView, n_events: int, events,
+                        out: NalarDecisions) -> int:
+    return load_library().nalar_policy_decide(h, ctypes.byref(prob), ctypes.byref(view), n_events,
+                                              events, ctypes.byref(out))
 
 
 def nalar_policy_destroy(h: Optional[int]) -> None:
@@ -212,12 +237,14 @@ class DeviceProblem:
     def n_nodes(self) -> int:
         return int(self.tensors["wf"].shape[0])
 
-    def c_struct(self, flags: Optional[int] = None, policy: int = 0, priority=None) -> NalarProblem:
+    def c_struct(self, flags: Optional[int] = None, policy: int = 0, priority=None,
+                 weights=None) -> NalarProblem:
         """The C struct of this problem.  ``flags`` replaces the default
         problem flags (the contiguity bit when the ids are workflow-contiguous);
-        ``policy`` (NALAR_ORDER_LPT | NALAR_ROUTE_STATEFUL | NALAR_ROUTE_GREEDY
-        bits) is ORed in; ``priority`` is a uint8 device tensor of one level per
-        workflow, or None."""
+        ``policy`` (NALAR_ORDER_* and NALAR_ROUTE_* bits) is ORed in;
+        ``priority`` is a uint8 device tensor of one level per workflow, or
+        None; ``weights`` a uint32 (or int32) device tensor of one routing
+        weight per instance, or None."""
         t = self.tensors
         ptr = lambda x: x.data_ptr() if x.numel() > 0 else None
         return NalarProblem(
@@ -230,7 +257,8 @@ class DeviceProblem:
             dep_idx=ptr(t["dep_idx"]), deadline_us=ptr(t["deadline_us"]),
             inst_type=ptr(t["inst_type"]), inst_load_us=ptr(t["inst_load_us"]),
             inst_speed_permille=ptr(t["inst_speed_permille"]),
-            wf_priority=None if priority is None else priority.data_ptr())
+            wf_priority=None if priority is None else priority.data_ptr(),
+            inst_weight=None if weights is None else weights.data_ptr())
 
 
 @dataclass
@@ -258,6 +286,47 @@ class DeviceResult:
                            route=p(self.route), cost_us=p(self.cost), n_ready=0)
 
 
+# Handles still open when the interpreter exits are closed by an atexit hook,
+# which runs before modules are torn down: the library's device and pinned
+# memory is then released while the HIP runtime (and a profiler attached to
+# it) is fully alive, and no library call is left for interpreter
+# finalization or the C exit handlers.  Objects collected during
+# finalization do not call the library at all.
+_open_handles: "weakref.WeakSet" = weakref.WeakSet()
+
+
+@atexit.register
+def _close_open_handles() -> None:
+    for obj in sorted(list(_open_handles), key=lambda o: 0 if isinstance(o, Store) else 1):
+        try:
+            obj.close()
+        except Exception:
+            pass
+
+
+@dataclass
+class DeviceDecisions:
+    """Outputs of per-event decisions: one entry per event."""
+    slack: object
+    route: object
+    cost: object
+    rank: object
+
+    @classmethod
+    def alloc(cls, n: int, device="cuda") -> "DeviceDecisions":
+        import torch
+        n1 = max(n, 1)
+        return cls(torch.empty(n1, dtype=torch.int64, device=device),
+                   torch.empty(n1, dtype=torch.int32, device=device),
+                   torch.empty(n1, dtype=torch.int64, device=device),
+                   torch.empty(n1, dtype=torch.int64, device=device))
+
+    def c_struct(self) -> NalarDecisions:
+        p = lambda x: None if x is None else x.data_ptr()
+        return NalarDecisions(slack_us=p(self.slack), route=p(self.route), cost_us=p(self.cost),
+                              rank=p(self.rank))
+
+
 class Policy:
     """Owns one handle bound to a device and a stream."""
 
@@ -274,11 +343,13 @@ class Policy:
         if rc != NALAR_OK:
             raise NalarError(rc, nalar_policy_last_error(None))
         self.handle = h
+        _open_handles.add(self)
 
     def close(self) -> None:
         if self.handle:
             nalar_policy_destroy(self.handle)
             self.handle = None
+        _open_handles.discard(self)
 
     def __enter__(self):
         return self
@@ -287,6 +358,8 @@ class Policy:
         self.close()
 
     def __del__(self):
+        if sys.is_finalizing():  # the runtime may be going away: leave it to process exit
+            return
         try:
             self.close()
         except Exception:
@@ -300,6 +373,19 @@ class Policy:
         rc = nalar_policy_pass(self.handle, cp, cr)
         out.n_ready = int(cr.n_ready) if rc == NALAR_OK else 0
         return rc
+
+    def decide(self, prob: DeviceProblem, view: "DeviceResult", events, out: "DeviceDecisions",
+               flags: Optional[int] = None, policy: int = 0, priority=None,
+               raw: Optional[NalarProblem] = None) -> int:
+        """Decide the futures of ``events`` (an int32 device tensor) against the
+        view a pass left in ``view`` (its rem, order and slack, n_ready
+        entries); fills ``out`` (one entry per event).  Synchronous."""
+        cp = raw if raw is not None else prob.c_struct(flags, policy, priority)
+        cv = NalarView(rem_us=view.rem.data_ptr(), order=view.order.data_ptr(),
+                       slack_us=view.slack.data_ptr(), n_order=view.n_ready)
+        n = int(events.shape[0])
+        return nalar_policy_decide(self.handle, cp, cv, n, events.data_ptr() if n else None,
+                                   out.c_struct())
 
     def last_error(self) -> str:
         return nalar_policy_last_error(self.handle)
@@ -324,6 +410,7 @@ class Store:
             raise NalarError(rc, policy.last_error())
         self.policy = policy
         self.handle = h
+        _open_handles.add(self)
 
     @staticmethod
     def _dev(a, dtype, device="cuda"):
@@ -376,12 +463,21 @@ class Store:
         if self.handle:
             nalar_store_destroy(self.handle)
             self.handle = None
+        _open_handles.discard(self)
 
     def __enter__(self):
         return self
 
     def __exit__(self, *exc):
         self.close()
+
+    def __del__(self):
+        if sys.is_finalizing():
+            return
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def run(p, device: str = "cuda", policy: Optional[Policy] = None, flags: int = 0):

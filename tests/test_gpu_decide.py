@@ -1,0 +1,160 @@
+"""GPU parity of per-event decisions (nalar_policy_decide): the one-level
+design of Section 6.3 (Table 4), one decision per future event against the
+view the last pass left.
+
+For a future that is ready, its decision must reproduce the oracle's pass:
+its rank is its index in the oracle's order, and slack, route and cost are the
+oracle's.  For a future that is not ready, slack comes from the oracle's rem,
+route and cost from the exhaustive big-integer minimum (the pin the oracle's
+routing is checked against), and rank from bisecting the oracle's order keys.
+Decisions are made in one batch and one event per call.
+"""
+import bisect
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2601_05109_amd import workloads as wl
+from test_oracle_pins import brute_route
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover - collected on CPU hosts too
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2601_05109_amd import nalar  # noqa: E402
+
+
+def say(msg):
+    sys.stdout.write(msg + "\n")
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def policy():
+    with nalar.Policy() as p:
+        yield p
+
+
+def _key(p, r_rem, slack_of, bits, prio, v):
+    lv = int(prio[p.wf[v]]) if prio is not None else 0
+    if bits & nalar.NALAR_ORDER_LPT:
+        k = -int(r_rem[v])
+    elif bits & nalar.NALAR_ORDER_SRTF:
+        k = int(r_rem[v])
+    else:
+        k = slack_of(v)
+    return (-lv, k, int(p.wf[v]), int(v))
+
+
+def run_case(pol, p, bits=0, prio=None, n_other=300, singles=40, seed=0):
+    say(f"[gpu] decide {p.name} policy={bits} levels={prio is not None}")
+    ref = oracle.run(p, policy=bits, priority=prio)
+    assert ref.status == oracle.OK
+    dp = nalar.DeviceProblem.from_host(p)
+    view = nalar.DeviceResult.alloc(p.n_nodes)
+    pr = None if prio is None else torch.from_numpy(np.ascontiguousarray(prio, np.uint8)).cuda()
+    cp = dp.c_struct(policy=bits, priority=pr)
+    assert pol.run_pass(dp, view, raw=cp) == nalar.NALAR_OK, pol.last_error()
+    R = view.n_ready
+    assert R == ref.n_ready
+
+    # ready futures: every one, in a shuffled batch
+    rng = np.random.default_rng(seed)
+    ready = ref.order.astype(np.int32)
+    perm = rng.permutation(R)
+    ev = torch.from_numpy(ready[perm].copy()).cuda()
+    out = nalar.DeviceDecisions.alloc(R)
+    assert pol.decide(dp, view, ev, out, raw=cp) == nalar.NALAR_OK, pol.last_error()
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(out.rank[:R].cpu().numpy(), perm)
+    np.testing.assert_array_equal(out.slack[:R].cpu().numpy(), ref.slack[perm])
+    np.testing.assert_array_equal(out.route[:R].cpu().numpy(), ref.route[perm])
+    np.testing.assert_array_equal(out.cost[:R].cpu().numpy(), ref.cost[perm])
+
+    # futures that are not ready: where they would enter the order
+    others = np.setdiff1d(np.arange(p.n_nodes), ready)
+    if others.size:
+        pick = rng.choice(others, size=min(n_other, others.size), replace=False).astype(np.int32)
+        ev = torch.from_numpy(pick).cuda()
+        out = nalar.DeviceDecisions.alloc(pick.size)
+        assert pol.decide(dp, view, ev, out, raw=cp) == nalar.NALAR_OK, pol.last_error()
+        torch.cuda.synchronize()
+        deadline = {w: int(p.deadline_us[w]) - int(p.now_us) for w in range(p.n_workflows)}
+        slack_of = lambda v: deadline[int(p.wf[v])] - int(ref.rem[v])
+        keys = [_key(p, ref.rem, slack_of, bits, prio, int(u)) for u in ref.order.tolist()]
+        got = {f: getattr(out, f)[:pick.size].cpu().numpy() for f in ("rank", "slack", "route", "cost")}
+        for k, v in enumerate(pick.tolist()):
+            assert got["slack"][k] == slack_of(v)
+            assert got["rank"][k] == bisect.bisect_left(keys, _key(p, ref.rem, slack_of, bits, prio, v))
+            if bits & nalar.NALAR_ROUTE_STATEFUL and int(p.loc[v]) >= 0 and \
+                    int(p.inst_type[int(p.loc[v])]) == int(p.type[v]):
+                l = int(p.loc[v])
+                want = (int(p.inst_load_us[l]) + int(p.est_us[v]) * 1000 // int(p.inst_speed_permille[l]), l)
+            else:
+                want = brute_route(p, v)
+            assert (int(got["cost"][k]), int(got["route"][k])) == want, v
+
+    # one event per call, as a one-level controller takes them
+    one = nalar.DeviceDecisions.alloc(1)
+    for k in rng.choice(R, size=min(singles, R), replace=False).tolist():
+        ev = torch.tensor([int(ready[k])], dtype=torch.int32, device="cuda")
+        assert pol.decide(dp, view, ev, one, raw=cp) == nalar.NALAR_OK
+        assert int(one.rank[0]) == k and int(one.route[0]) == int(ref.route[k])
+        assert int(one.slack[0]) == int(ref.slack[k]) and int(one.cost[0]) == int(ref.cost[k])
+
+
+@pytest.mark.parametrize("cfg", [0, 1])
+@pytest.mark.parametrize("bits", [0, nalar.NALAR_ORDER_LPT, nalar.NALAR_ORDER_SRTF, nalar.NALAR_ROUTE_STATEFUL])
+def test_decide_configs(policy, cfg, bits):
+    run_case(policy, wl.CONFIGS[cfg](), bits, seed=cfg * 10 + bits)
+
+
+def test_decide_levels_and_large_tables(policy):
+    p = wl.tiny()
+    prio = np.random.default_rng(4).integers(0, 16, p.n_workflows).astype(np.uint8)
+    run_case(policy, p, 0, prio)
+    run_case(policy, p, nalar.NALAR_ORDER_SRTF, prio)
+    rng = np.random.default_rng(8)
+    m = 1024
+    q = p.copy(inst_type=rng.integers(0, 5, m).astype(np.int32),
+               inst_load_us=rng.choice([0, 5, 1 << 60], m).astype(np.int64),
+               inst_speed_permille=rng.integers(1, 3000, m).astype(np.int32),
+               loc=np.where(rng.random(p.n_nodes) < 0.5, rng.integers(0, m, p.n_nodes), -1).astype(np.int32))
+    run_case(policy, q, 0)
+
+
+def test_decide_map_reduce(policy):
+    """A million ready futures in the view: the search runs five rounds."""
+    run_case(policy, wl.wide_mapreduce(), 0, n_other=64, singles=10)
+
+
+def test_decide_random_dags(policy):
+    for seed in range(20):
+        p = wl.random_dag(1300 + seed, n_nodes=60, n_workflows=3, n_instances=7, n_types=3,
+                          shuffle_ids=bool(seed % 2))
+        run_case(policy, p, [0, nalar.NALAR_ORDER_LPT, nalar.NALAR_ORDER_SRTF][seed % 3], seed=seed)
+
+
+def test_decide_errors(policy):
+    p = wl.tiny()
+    dp = nalar.DeviceProblem.from_host(p)
+    view = nalar.DeviceResult.alloc(p.n_nodes)
+    assert policy.run_pass(dp, view) == nalar.NALAR_OK
+    out = nalar.DeviceDecisions.alloc(4)
+    bad = torch.tensor([0, p.n_nodes, 3, -1], dtype=torch.int32, device="cuda")
+    assert policy.decide(dp, view, bad, out) == nalar.NALAR_EINVAL
+    ev = torch.tensor([0, 1], dtype=torch.int32, device="cuda")
+    assert policy.decide(dp, view, ev, out, policy=nalar.NALAR_ROUTE_GREEDY) == nalar.NALAR_EINVAL
+    assert policy.decide(dp, view, ev, out, policy=nalar.NALAR_ROUTE_WEIGHTED) == nalar.NALAR_EINVAL
+    cv = nalar.NalarView(rem_us=view.rem.data_ptr(), order=view.order.data_ptr(),
+                         slack_us=view.slack.data_ptr(), n_order=p.n_nodes + 1)
+    assert nalar.nalar_policy_decide(policy.handle, dp.c_struct(), cv, 2, ev.data_ptr(),
+                                     out.c_struct()) == nalar.NALAR_EINVAL
+    # order entries that are no futures of the snapshot (every probe meets one)
+    view.order.fill_(p.n_nodes + 7)
+    assert policy.decide(dp, view, ev, out) == nalar.NALAR_EINVAL
+    assert policy.decide(dp, view, ev[:0], out) == nalar.NALAR_OK  # no events

@@ -51,11 +51,22 @@ def policy_tiled():
         yield p
 
 
-def gpu_run(pol, p, flags=None, policy=0, priority=None):
+def seeded_weights(p):
+    """Routing weights for NALAR_ROUTE_WEIGHTED cases: 0..4 per instance,
+    seeded by the problem's size, with one type left unweighted."""
+    w = np.random.default_rng(p.n_instances * 7 + p.n_nodes).integers(0, 5, p.n_instances).astype(np.uint32)
+    if p.n_instances:
+        w[p.inst_type == p.inst_type[0]] = 0
+    return w
+
+
+def gpu_run(pol, p, flags=None, policy=0, priority=None, weights=None):
     dp = nalar.DeviceProblem.from_host(p)
     out = nalar.DeviceResult.alloc(dp.n_nodes)
     pr = None if priority is None else torch.from_numpy(np.ascontiguousarray(priority, np.uint8)).cuda()
-    rc = pol.run_pass(dp, out, flags=flags, policy=policy, priority=pr)
+    wt = None if weights is None else torch.from_numpy(np.ascontiguousarray(weights, np.uint32).view(np.int32)).cuda()
+    cp = dp.c_struct(flags, policy, pr, wt)
+    rc = pol.run_pass(dp, out, raw=cp)
     torch.cuda.synchronize()
     R = out.n_ready
     N = dp.n_nodes
@@ -79,10 +90,12 @@ def assert_parity(g, o, label=""):
                                  f"gpu {got[bad[:5]]} oracle {ref[bad[:5]]}")
 
 
-def check(pol, p, label, flags=None, policy=0, priority=None):
+def check(pol, p, label, flags=None, policy=0, priority=None, weights=None):
     say(f"[gpu] {label}: N={p.n_nodes} E={p.n_edges} W={p.n_workflows} M={p.n_instances} policy={policy}")
-    assert_parity(gpu_run(pol, p, flags, policy, priority), oracle.run(p, policy=policy, priority=priority),
-                  label)
+    if (policy & nalar.NALAR_ROUTE_WEIGHTED) and weights is None:
+        weights = seeded_weights(p)
+    assert_parity(gpu_run(pol, p, flags, policy, priority, weights),
+                  oracle.run(p, policy=policy, priority=priority, weights=weights), label)
 
 
 # ---------------------------------------------------------------- small cases
@@ -146,6 +159,12 @@ def test_configs_hbm_sweep(policy_hbm, cfg):
 
 def test_deep_chains_hbm_small(policy_hbm):
     check(policy_hbm, wl.deep_chains(W=64), "deep chains W=64 hbm")
+
+
+def test_deep_chains_hbm_full(policy_hbm):
+    """The HBM sweep (state by position in global memory) on the full deep
+    chains: 1,024 workflows of 128 levels each."""
+    check(policy_hbm, wl.deep_chains(), "deep chains hbm")
 
 
 @pytest.mark.parametrize("cfg", [0, 1, 2])
@@ -229,7 +248,10 @@ def test_large_ready_set_bucketed():
 VARIANTS = [nalar.NALAR_ORDER_LPT, nalar.NALAR_ROUTE_STATEFUL,
             nalar.NALAR_ORDER_LPT | nalar.NALAR_ROUTE_STATEFUL, nalar.NALAR_ROUTE_GREEDY,
             nalar.NALAR_ROUTE_GREEDY | nalar.NALAR_ROUTE_STATEFUL,
-            nalar.NALAR_ROUTE_GREEDY | nalar.NALAR_ORDER_LPT]
+            nalar.NALAR_ROUTE_GREEDY | nalar.NALAR_ORDER_LPT,
+            nalar.NALAR_ORDER_SRTF, nalar.NALAR_ORDER_SRTF | nalar.NALAR_ROUTE_STATEFUL,
+            nalar.NALAR_ROUTE_WEIGHTED, nalar.NALAR_ROUTE_WEIGHTED | nalar.NALAR_ROUTE_STATEFUL,
+            nalar.NALAR_ROUTE_WEIGHTED | nalar.NALAR_ORDER_SRTF]
 
 
 @pytest.mark.parametrize("bits", VARIANTS)
@@ -265,10 +287,10 @@ def test_policy_switch_on_one_handle():
             check(pol, p, f"switch policy {bits}", policy=bits)
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 3])
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
 def test_priority_levels(policy, policy_tiled, policy_hbm, cfg):
     """Per-workflow priority levels (set_priority) with and without LPT, on
-    every sort and sweep path, plus the level and key-range rules."""
+    every sort and sweep path, plus the level rule and keys near +-2^61."""
     p = wl.CONFIGS[cfg]()
     rng = np.random.default_rng(20 + cfg)
     for levels in (rng.integers(0, 16, p.n_workflows), rng.integers(0, 2, p.n_workflows),
@@ -284,10 +306,15 @@ def test_priority_levels(policy, policy_tiled, policy_hbm, cfg):
         bad = pr.copy()
         bad[7] = 16
         check(policy, p, "level 16", priority=bad)
-        far = p.copy(deadline_us=p.deadline_us.copy())
-        far.deadline_us[0] = p.now_us + (1 << 60)
-        check(policy, far, "key beyond 2^58 with levels", priority=pr)
-        check(policy, far, "same without levels")
+        # slacks near -2^61 - rem and +2^61: the order by (-level, key, wf, id)
+        # needs no bound on the key
+        dl = p.now_us + rng.choice([-(1 << 61), (1 << 61) - (1 << 40), 0, 1 << 58], p.n_workflows)
+        far = p.copy(deadline_us=dl.astype(np.int64))
+        for pol, name in ((policy, "default"), (policy_tiled, "tiled"), (policy_hbm, "hbm")):
+            for bits in (0, nalar.NALAR_ORDER_SRTF):
+                check(pol, far, f"keys near 2^61 with levels {name} {bits}", policy=bits, priority=pr)
+                check(pol, far, f"keys near 2^61 with levels {name} {bits} again", policy=bits, priority=pr)
+            check(pol, far, f"keys near 2^61 without levels {name}")
 
 
 def test_priority_levels_bucketed():
@@ -336,7 +363,49 @@ def test_lpt_repeated_bucketed():
 def test_policy_unknown_bits_rejected(policy):
     dp = nalar.DeviceProblem.from_host(wl.tiny())
     out = nalar.DeviceResult.alloc(dp.n_nodes)
-    assert policy.run_pass(dp, out, policy=16) == nalar.NALAR_EINVAL
+    assert policy.run_pass(dp, out, policy=64) == nalar.NALAR_EINVAL
+    assert policy.run_pass(dp, out, policy=nalar.NALAR_ORDER_LPT | nalar.NALAR_ORDER_SRTF) == nalar.NALAR_EINVAL
+    assert policy.run_pass(dp, out, policy=nalar.NALAR_ROUTE_WEIGHTED) == nalar.NALAR_EINVAL  # no weights
+
+
+def test_weighted_rules_and_precedence(policy, policy_tiled):
+    """Weights above NALAR_WEIGHT_MAX and weighted with greedy routing are
+    EINVAL, and a bad weight wins over a cycle (EINVAL before ECYCLE); all-zero
+    weights give the default routes; repeated weighted passes on one handle
+    (the bucketed sort after the first) match the oracle."""
+    p = wl.tiny()
+    W = nalar.NALAR_ROUTE_WEIGHTED
+    big = seeded_weights(p)
+    big[3] = (1 << 20) + 1
+    check(policy, p, "weight above max", policy=W, weights=big)
+    check(policy_tiled, p, "weight above max tiled", policy=W, weights=big)
+    check(policy, p, "weighted with greedy", policy=W | nalar.NALAR_ROUTE_GREEDY, weights=seeded_weights(p))
+    cyc = p.copy(dep_idx=p.dep_idx.copy())
+    v = int(np.flatnonzero(np.diff(p.dep_off) > 0)[0])
+    cyc.dep_idx[p.dep_off[v]] = v  # a self-dependency
+    check(policy, cyc, "cycle without weights")
+    check(policy, cyc, "cycle and bad weight", policy=W, weights=big)
+    check(policy, p, "zero weights", policy=W, weights=np.zeros(p.n_instances, np.uint32))
+    q = wl.paper_scale()
+    for i in range(4):
+        check(policy, q, f"weighted paper scale pass {i}", policy=W)
+    r = wl.relabel(p, np.random.default_rng(3).permutation(p.n_nodes))
+    check(policy_tiled, r, "weighted relabelled tiled", policy=W | nalar.NALAR_ROUTE_STATEFUL)
+
+
+@pytest.mark.parametrize("m,n_types", [(1, 1), (63, 2), (1024, 1), (1024, 300)])
+def test_weighted_instance_tables(policy, m, n_types):
+    """Weighted routing with one instance, many types, and the largest tables
+    (one type of 1024 instances, 300 types), weights up to the maximum."""
+    p = wl.windowed(64)
+    rng = np.random.default_rng(m + n_types)
+    q = p.copy(inst_type=rng.integers(0, n_types, m).astype(np.int32),
+               inst_load_us=rng.integers(0, 2_000_000, m).astype(np.int64),
+               inst_speed_permille=rng.integers(500, 2001, m).astype(np.int32),
+               type=rng.integers(0, n_types + 1, p.n_nodes).astype(np.int32),
+               loc=np.where(rng.random(p.n_nodes) < 0.5, rng.integers(0, m, p.n_nodes), -1).astype(np.int32))
+    w = rng.choice([0, 1, 7, 1 << 20], m).astype(np.uint32)
+    check(policy, q, f"weighted M={m} types={n_types}", policy=nalar.NALAR_ROUTE_WEIGHTED, weights=w)
 
 
 def _one_type(n_inst, loads, speeds, est, loc=None, mig=200_000):
@@ -800,7 +869,9 @@ def test_store_small_graphs_and_errors():
                 assert nalar.nalar_store_append(st.handle, 1, 0, None, None, None, None, None, None,
                                                 None, 0) == nalar.NALAR_EINVAL
                 assert nalar.nalar_store_complete(st.handle, -1, None) == nalar.NALAR_EINVAL
-                assert nalar.nalar_store_pass(st.handle, 0, 0, 16, out.c_struct()) == nalar.NALAR_EINVAL
+                assert nalar.nalar_store_pass(st.handle, 0, 0, 64, out.c_struct()) == nalar.NALAR_EINVAL
+                assert nalar.nalar_store_pass(st.handle, 0, 0, nalar.NALAR_ROUTE_WEIGHTED,
+                                              out.c_struct()) == nalar.NALAR_EINVAL
                 del z
             finally:
                 st.close()

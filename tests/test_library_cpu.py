@@ -66,6 +66,8 @@ int main(void) {
          offsetof(nalar_problem, inst_speed_permille), offsetof(nalar_problem, wf_priority),
          offsetof(nalar_result, n_ready));
   printf("%zu\n", offsetof(nalar_policy_config, reserve_workflows));
+  printf("%zu %zu %zu %zu %zu\n", offsetof(nalar_problem, inst_weight), sizeof(nalar_view),
+         offsetof(nalar_view, n_order), sizeof(nalar_decisions), offsetof(nalar_decisions, rank));
   return 0;
 }
 '''
@@ -78,9 +80,11 @@ int main(void) {
         out = subprocess.run([exe], capture_output=True, text=True, check=True).stdout.split()
     got = list(map(int, out))
     P, C, R = nalar.NalarProblem, nalar.NalarPolicyConfig, nalar.NalarResult
+    V, D = nalar.NalarView, nalar.NalarDecisions
     assert got == [ctypes.sizeof(C), ctypes.sizeof(P), ctypes.sizeof(R), P.flags.offset,
                    P.wf.offset, P.inst_speed_permille.offset, P.wf_priority.offset, R.n_ready.offset,
-                   C.reserve_workflows.offset]
+                   C.reserve_workflows.offset, P.inst_weight.offset, ctypes.sizeof(V),
+                   V.n_order.offset, ctypes.sizeof(D), D.rank.offset]
 
 
 def test_binding_fails_loudly_without_library(tmp_path):
