@@ -271,6 +271,25 @@ typedef struct {              /* DEVICE arrays of n_events entries, caller-owned
 int nalar_policy_decide(nalar_policy* h, const nalar_problem* p, const nalar_view* view,
                         int64_t n_events, const int32_t* events, nalar_decisions* out);
 
+/*
+ * For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): nalar_policy_pass without
+ * any allocation.  Same arguments, results and return codes, but the scratch
+ * is a fixed array of NALAR_STATIC_SCRATCH_BYTES of device memory that the
+ * library holds on each device from the first handle created there until the
+ * process ends, instead of memory allocated for the handle.  Limits:
+ * n_nodes <= NALAR_STATIC_MAX_NODES and n_workflows <=
+ * NALAR_STATIC_MAX_WORKFLOWS, else NALAR_EINVAL (the bucketed sort is skipped
+ * for a ready set too large for the array's buckets).  Every call on one
+ * device shares that device's array, which keeps the last call's contents;
+ * the library serialises the calls on a device with a lock, so concurrent
+ * callers wait for each other (calls are synchronous).
+ */
+#define NALAR_STATIC_SCRATCH_BYTES (64u << 20)
+#define NALAR_STATIC_MAX_NODES     (INT64_C(1) << 18)
+#define NALAR_STATIC_MAX_WORKFLOWS (INT64_C(1) << 18)
+int nalar_policy_pass_static(nalar_policy* h, const nalar_problem* p, nalar_result* r);
+
 /* Release the handle and its scratch.  NULL-safe.  Waits for the handle's
  * stream first. */
 void nalar_policy_destroy(nalar_policy* h);

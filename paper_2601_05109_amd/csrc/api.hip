@@ -31,11 +31,16 @@
 // passes follow after another synchronisation.
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "internal.hpp"
 
 using namespace nalar;
+
+// The static scratch array of nalar_policy_pass_static (NALAR_STATIC_SCRATCH_BYTES
+// per device; see below for how host code reaches it).
+static __device__ __align__(256) char scratch[NALAR_STATIC_SCRATCH_BYTES];
 
 namespace {
 
@@ -79,6 +84,34 @@ struct Arena {
   int64_t capN = -1, capW = -1, capB = -1;
 };
 
+// The scratch a pass runs in: an arena and the state of what it holds (the
+// look-back tag of the last pass, the control block the next pass uses, and
+// which control blocks and bucket counters are stale).
+struct ArenaState {
+  Arena ar;
+  uint32_t epoch = 0;
+  uint64_t passes = 0;                 // selects the control block of the next pass
+  bool ctrl_dirty[2] = {true, true};
+  bool bcnt_clean[2] = {true, true};   // bucket counters known to be zero
+};
+
+// Scratch of nalar_policy_pass_static: one fixed array per device, laid out
+// once for the largest snapshot it takes.  `scratch` names the array only in
+// device code; host code uses the address hipGetSymbolAddress returns for it
+// on each device (kept in g_static), never the name.
+constexpr size_t kStaticScratchBytes = size_t(NALAR_STATIC_SCRATCH_BYTES);
+constexpr int64_t kStaticBuckets = 16384;
+constexpr int kMaxDevices = 64;
+
+struct StaticScratch {
+  std::mutex mu;          // serialises the calls on this device
+  bool ready = false;     // address resolved and arena laid out
+  bool cleared = false;   // look-back words untagged
+  ArenaState st;
+};
+
+StaticScratch g_static[kMaxDevices];
+
 }  // namespace
 
 struct nalar_policy {
@@ -87,10 +120,6 @@ struct nalar_policy {
   hipStream_t stream = nullptr;
   int cus = 0;
   size_t lds_limit = 0;
-  uint32_t epoch = 0;
-  uint64_t passes = 0;           // selects the control block of the next pass
-  bool ctrl_dirty[2] = {true, true};
-  bool bcnt_clean[2] = {true, true};  // bucket counters known to be zero
   // slack range and ready count of the last successful pass (bucket hint)
   bool hint_valid = false;
   int64_t hint_ready = 0, hint_min = 0, hint_max = 0;
@@ -102,7 +131,7 @@ struct nalar_policy {
   int bucket_relax = 64;         // calm passes before fewer buckets are tried again
   bool bucket_relaxed = false;   // the last pass tried fewer buckets
   std::string err;
-  Arena ar;
+  ArenaState own;                // scratch allocated by the library for this handle
   HostStatus* host = nullptr;    // pinned, written by the sort kernel
   bool timing = false;
   int n_timed = 0;
@@ -179,7 +208,7 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B) {
 }
 
 int ensure_capacity(nalar_policy* h, int64_t N, int64_t W, int64_t B) {
-  Arena& a = h->ar;
+  Arena& a = h->own.ar;
   if (a.base && N <= a.capN && W <= a.capW && B <= a.capB) return NALAR_OK;
   int64_t newN = a.capN > N ? a.capN : N;
   int64_t newW = a.capW > W ? a.capW : W;
@@ -211,10 +240,10 @@ int ensure_capacity(nalar_policy* h, int64_t N, int64_t W, int64_t B) {
   fresh.capN = newN;
   fresh.capW = newW;
   fresh.capB = newB;
-  h->ar = fresh;
-  h->epoch = 0;
-  h->ctrl_dirty[0] = h->ctrl_dirty[1] = true;
-  h->bcnt_clean[0] = h->bcnt_clean[1] = true;
+  h->own.ar = fresh;
+  h->own.epoch = 0;
+  h->own.ctrl_dirty[0] = h->own.ctrl_dirty[1] = true;
+  h->own.bcnt_clean[0] = h->own.bcnt_clean[1] = true;
   return NALAR_OK;
 }
 
@@ -369,6 +398,35 @@ int nalar_policy_create(const nalar_policy_config* cfg, nalar_policy** out) {
   if (e != hipSuccess) return bail(e, "hipGetDeviceProperties");
   h->cus = prop.multiProcessorCount;
   h->lds_limit = prop.sharedMemPerBlock;
+  if (h->device < 0 || h->device >= kMaxDevices) {
+    g_create_error = "device ordinal beyond the library's limit";
+    nalar_policy_destroy(h);
+    return NALAR_EINVAL;
+  }
+  {  // the static scratch of this device: resolve its address once
+    StaticScratch& ss = g_static[h->device];
+    std::lock_guard<std::mutex> lock(ss.mu);
+    if (!ss.ready) {
+      void* ptr = nullptr;
+      e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+      if (e != hipSuccess) return bail(e, "hipGetSymbolAddress(scratch)");
+      Arena& a = ss.st.ar;
+      const size_t need = carve(a, nullptr, NALAR_STATIC_MAX_NODES, NALAR_STATIC_MAX_WORKFLOWS, kStaticBuckets);
+      if (need > kStaticScratchBytes) {
+        g_create_error = "static scratch layout exceeds its array";
+        nalar_policy_destroy(h);
+        return NALAR_EDEVICE;
+      }
+      carve(a, static_cast<char*>(ptr), NALAR_STATIC_MAX_NODES, NALAR_STATIC_MAX_WORKFLOWS, kStaticBuckets);
+      a.base = ptr;
+      a.bytes = need;
+      a.capN = NALAR_STATIC_MAX_NODES;
+      a.capW = NALAR_STATIC_MAX_WORKFLOWS;
+      a.capB = kStaticBuckets;
+      ss.st.bcnt_clean[0] = ss.st.bcnt_clean[1] = false;  // cleared by the first pass
+      ss.ready = true;
+    }
+  }
   e = prepare_sweep_kernels(h->lds_limit);
   if (e != hipSuccess) return bail(e, "hipFuncSetAttribute");
   e = hipHostMalloc(reinterpret_cast<void**>(&h->host), sizeof(HostStatus), hipHostMallocCoherent);
@@ -391,7 +449,7 @@ void nalar_policy_destroy(nalar_policy* h) {
   if (!h) return;
   (void)hipSetDevice(h->device);
   (void)hipStreamSynchronize(h->stream);
-  if (h->ar.base) (void)hipFree(h->ar.base);
+  if (h->own.ar.base) (void)hipFree(h->own.ar.base);
   if (h->host) (void)hipHostFree(h->host);
   for (int i = 0; i <= kMaxTimed; ++i)
     if (h->ev[i]) (void)hipEventDestroy(h->ev[i]);
@@ -452,40 +510,43 @@ int nalar_policy_decide(nalar_policy* h, const nalar_problem* p, const nalar_vie
   return NALAR_OK;
 }
 
-int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) {
-  if (!h) return NALAR_EINVAL;
-  h->err.clear();
-  h->timed_valid = false;
-  int rc = check_problem(h, p, r);
-  if (rc != NALAR_OK) return rc;
-  hipError_t e = hipSetDevice(h->device);
-  if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+}  // extern "C"
+
+namespace {
+
+// Zero the look-back words of an arena (a fill kernel rather than a memset, so
+// that a caller may capture the pass into a graph).
+hipError_t clear_lookback(hipStream_t s, const Arena& A) {
+  return launch_reset(s, nullptr, reinterpret_cast<uint32_t*>(static_cast<char*>(A.base) + A.lookback_off),
+                      int64_t(A.lookback_bytes / 4));
+}
+
+// The pass proper, in the scratch of `as` (sized for the snapshot and for the
+// buckets of bk), after the checks of the entry point.
+int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaState& as, BucketArgs bk,
+             const SweepShape& sh) {
+  hipError_t e;
   const int64_t N = p->n_nodes, W = p->n_workflows, M = p->n_instances;
-  const SweepShape sh = plan_sweep(N, W, M, h->cus, h->lds_limit);
-  BucketArgs bk = plan_buckets(h, N, p->wf_priority != nullptr, sh.wave_path != 0);
-  if (h->bucket_skip > 0) --h->bucket_skip;
-  rc = ensure_capacity(h, N, W, bk.nb);
-  if (rc != NALAR_OK) return rc;
-  Arena& A = h->ar;
+  Arena& A = as.ar;
   hipStream_t s = h->stream;
-  const int cur = int(h->passes & 1);
+  const int cur = int(as.passes & 1);
   const int nxt = cur ^ 1;
   bk.cnt = A.bcnt[cur];
   bk.slot = A.bslot;
   Ctrl* ctrl = A.ctrl[cur];
 
-  h->epoch = (h->epoch + 1) & kEpochMask;
-  if (h->epoch == 0) {  // tags wrapped: forget every old look-back word
-    e = hipMemsetAsync(static_cast<char*>(A.base) + A.lookback_off, 0, A.lookback_bytes, s);
-    if (e != hipSuccess) return hip_fail(h, e, "hipMemsetAsync(look-back)");
-    h->epoch = 1;
+  as.epoch = (as.epoch + 1) & kEpochMask;
+  if (as.epoch == 0) {  // tags wrapped: forget every old look-back word
+    e = clear_lookback(s, A);
+    if (e != hipSuccess) return hip_fail(h, e, "clear look-back");
+    as.epoch = 1;
   }
-  const uint32_t epoch = h->epoch;
+  const uint32_t epoch = as.epoch;
   // This pass uses block `cur` (reset first if an earlier pass left it stale)
   // and its sort kernel resets block `nxt`; until that has run, both are stale.
-  const bool need_reset = h->ctrl_dirty[cur];
-  h->ctrl_dirty[cur] = true;
-  h->ctrl_dirty[nxt] = true;
+  const bool need_reset = as.ctrl_dirty[cur];
+  as.ctrl_dirty[cur] = true;
+  as.ctrl_dirty[nxt] = true;
 
   const uint32_t policy = p->flags & (NALAR_ORDER_LPT | NALAR_ORDER_SRTF | NALAR_ROUTE_STATEFUL |
                                       NALAR_ROUTE_GREEDY | NALAR_ROUTE_WEIGHTED);
@@ -501,10 +562,10 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   } while (0)
 
   // bucket counters of this pass: zeroed by the previous pass's sweep, else here
-  const bool need_clear = bk.nb > 0 && !h->bcnt_clean[cur];
+  const bool need_clear = bk.nb > 0 && !as.bcnt_clean[cur];
   if (need_reset || need_clear)
     NALAR_LAUNCH("reset", launch_reset(s, need_reset ? ctrl : nullptr, bk.cnt, need_clear ? bk.nb : 0));
-  if (bk.nb > 0) h->bcnt_clean[cur] = false;
+  if (bk.nb > 0) as.bcnt_clean[cur] = false;
   WeightedArgs wa{};
   if (policy & NALAR_ROUTE_WEIGHTED) {
     wa.type = p->type;
@@ -585,7 +646,7 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
     sw.bk_clear_n = A.capB > 0 ? A.capB : 0;
     sw.force_global = (h->flags & NALAR_FORCE_GLOBAL_SWEEP) ? 1 : 0;
     NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
-    h->bcnt_clean[nxt] = true;  // the sweep cleared them for the next pass
+    as.bcnt_clean[nxt] = true;  // the sweep cleared them for the next pass
   }
 
   SortArgs sa{};
@@ -676,8 +737,8 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
       if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
     }
   }
-  h->passes += 1;
-  h->ctrl_dirty[nxt] = false;
+  as.passes += 1;
+  as.ctrl_dirty[nxt] = false;
   const uint32_t st = __atomic_load_n(&h->host->status, __ATOMIC_ACQUIRE);
   if (st == 0xFFFFFFFFu) return fail(h, NALAR_EDEVICE, "status was not written");
   if (st & kStInval) return fail(h, NALAR_EINVAL, "invalid problem data");
@@ -719,6 +780,54 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   h->hint_max = r->n_ready ? __atomic_load_n(&h->host->slack_max, __ATOMIC_ACQUIRE) : 0;
   h->hint_levels = r->n_ready && p->wf_priority ? __atomic_load_n(&h->host->level_mask, __ATOMIC_ACQUIRE) : 0u;
   return NALAR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) {
+  if (!h) return NALAR_EINVAL;
+  h->err.clear();
+  h->timed_valid = false;
+  int rc = check_problem(h, p, r);
+  if (rc != NALAR_OK) return rc;
+  hipError_t e = hipSetDevice(h->device);
+  if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+  const int64_t N = p->n_nodes, W = p->n_workflows, M = p->n_instances;
+  const SweepShape sh = plan_sweep(N, W, M, h->cus, h->lds_limit);
+  const BucketArgs bk = plan_buckets(h, N, p->wf_priority != nullptr, sh.wave_path != 0);
+  if (h->bucket_skip > 0) --h->bucket_skip;
+  rc = ensure_capacity(h, N, W, bk.nb);
+  if (rc != NALAR_OK) return rc;
+  return run_pass(h, p, r, h->own, bk, sh);
+}
+
+int nalar_policy_pass_static(nalar_policy* h, const nalar_problem* p, nalar_result* r) {
+  if (!h) return NALAR_EINVAL;
+  h->err.clear();
+  h->timed_valid = false;
+  int rc = check_problem(h, p, r);
+  if (rc != NALAR_OK) return rc;
+  if (p->n_nodes > NALAR_STATIC_MAX_NODES || p->n_workflows > NALAR_STATIC_MAX_WORKFLOWS)
+    return fail(h, NALAR_EINVAL, "snapshot larger than the static scratch allows (n_nodes and n_workflows "
+                                 "<= NALAR_STATIC_MAX_NODES / _WORKFLOWS)");
+  hipError_t e = hipSetDevice(h->device);
+  if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+  StaticScratch& ss = g_static[h->device];
+  std::lock_guard<std::mutex> lock(ss.mu);
+  if (!ss.ready) return fail(h, NALAR_EDEVICE, "static scratch not set up on this device");
+  const int64_t N = p->n_nodes, W = p->n_workflows, M = p->n_instances;
+  const SweepShape sh = plan_sweep(N, W, M, h->cus, h->lds_limit);
+  BucketArgs bk = plan_buckets(h, N, p->wf_priority != nullptr, sh.wave_path != 0);
+  if (h->bucket_skip > 0) --h->bucket_skip;
+  if (bk.nb > kStaticBuckets) bk = BucketArgs{};  // more buckets than the array holds: tiled sort
+  if (!ss.cleared) {  // first use on this device: untag every look-back word
+    e = clear_lookback(h->stream, ss.st.ar);
+    if (e != hipSuccess) return hip_fail(h, e, "clear look-back");
+    ss.cleared = true;
+  }
+  return run_pass(h, p, r, ss.st, bk, sh);
 }
 
 }  // extern "C"

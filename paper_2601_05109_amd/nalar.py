@@ -33,8 +33,11 @@ NALAR_ROUTE_WEIGHTED = 32    # problem flag: deal each type's futures to its ins
 NALAR_FORCE_GLOBAL_SWEEP = 1
 NALAR_FORCE_TILED_SORT = 2
 NALAR_MAX_INSTANCES = 1024
+NALAR_STATIC_MAX_NODES = 1 << 18       # largest snapshot of nalar_policy_pass_static
+NALAR_STATIC_MAX_WORKFLOWS = 1 << 18
 
 EXPORTED = ("nalar_policy_create", "nalar_policy_pass", "nalar_policy_destroy", "nalar_policy_decide",
+            "nalar_policy_pass_static",
             "nalar_policy_last_error", "nalar_policy_set_timing", "nalar_policy_get_timing",
             "nalar_store_create", "nalar_store_destroy", "nalar_store_append", "nalar_store_complete",
             "nalar_store_set_workflows", "nalar_store_set_instances", "nalar_store_n_nodes",
@@ -93,6 +96,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.nalar_policy_create.restype = ctypes.c_int
     lib.nalar_policy_pass.argtypes = [H, ctypes.POINTER(NalarProblem), ctypes.POINTER(NalarResult)]
     lib.nalar_policy_pass.restype = ctypes.c_int
+    lib.nalar_policy_pass_static.argtypes = [H, ctypes.POINTER(NalarProblem), ctypes.POINTER(NalarResult)]
+    lib.nalar_policy_pass_static.restype = ctypes.c_int
     lib.nalar_policy_decide.argtypes = [H, ctypes.POINTER(NalarProblem), ctypes.POINTER(NalarView),
                                         ctypes.c_int64, ctypes.c_void_p, ctypes.POINTER(NalarDecisions)]
     lib.nalar_policy_decide.restype = ctypes.c_int
@@ -137,6 +142,10 @@ def nalar_policy_create(cfg: NalarPolicyConfig) -> tuple[int, Optional[int]]:
 
 def nalar_policy_pass(h: int, prob: NalarProblem, res: NalarResult) -> int:
     return load_library().nalar_policy_pass(h, ctypes.byref(prob), ctypes.byref(res))
+
+
+def nalar_policy_pass_static(h: int, prob: NalarProblem, res: NalarResult) -> int:
+    return load_library().nalar_policy_pass_static(h, ctypes.byref(prob), ctypes.byref(res))
 
 
 def nalar_policy_decide(h: int, prob: NalarProblem, view: NalarView, n_events: int, events,
