@@ -260,10 +260,12 @@ __device__ inline void bucket_put(const SweepArgs& a, uint32_t bkt, uint32_t slo
 // level): the slack, or the remaining critical path negated under
 // NALAR_ORDER_LPT (longest first) or as it is under NALAR_ORDER_SRTF
 // (shortest first).
+// Written as base - (+-rem) with both chosen by the policy word (the same on
+// every lane), which keeps the block sweep within its registers.
 __device__ inline int64_t order_key(const SweepArgs& a, int64_t rem, int64_t dl) {
-  if (a.p.policy & NALAR_ORDER_LPT) return -rem;
-  if (a.p.policy & NALAR_ORDER_SRTF) return rem;
-  return dl - rem;
+  const int64_t base = (a.p.policy & (NALAR_ORDER_LPT | NALAR_ORDER_SRTF)) ? 0 : dl;
+  const int64_t r = (a.p.policy & NALAR_ORDER_SRTF) ? -rem : rem;
+  return base - r;
 }
 
 // Workflow w's priority level (0 without levels); w is the same on every

@@ -18,6 +18,8 @@ Generators
 ``deep_chains(seed)``   1,024 x 512 futures, 128 layers of width 4, K=8, 128 inst.
 ``wide_mapreduce(seed)`` 256 x (1 root + 4,096 tools + 1 reduce), K=8, 256 inst.
 ``dynamic_stream(...)``  the wide map/reduce graph evolved over 100 steps.
+``churned(p, seed)``    p with 1 % of its in-flight futures completed.
+``deadline_shifted(p, seed)`` p with every deadline moved by up to 1 s.
 ``random_dag(seed,...)`` small arbitrary DAGs for brute-force checks.
 ``relabel(p, perm)``    the same problem under a permutation of node ids.
 """
@@ -389,6 +391,27 @@ def dynamic_stream(steps: int = 100, seed: Optional[int] = None, W: int = 256,
             app_parent.extend(par)
             running.extend(pend == 0)
         yield snapshot(step)
+
+
+def churned(p: Problem, seed: int, frac: float = 0.01) -> Problem:
+    """p with ``frac`` of its not-done futures (uniform, without replacement)
+    marked done: the values of 1 % of the in-flight futures materialised
+    since the last snapshot."""
+    rng = _rng(seed)
+    live = np.flatnonzero(p.done == 0)
+    k = int(live.shape[0] * frac)
+    done = p.done.copy()
+    if k > 0:
+        done[rng.choice(live, size=k, replace=False)] = 1
+    return p.copy(done=done)
+
+
+def deadline_shifted(p: Problem, seed: int, max_shift_us: int = 1_000_000) -> Problem:
+    """p with every workflow deadline moved by its own uniform shift in
+    [-max_shift_us, max_shift_us] (deadlines renegotiated, clocks adjusted)."""
+    rng = _rng(seed)
+    shift = rng.integers(-max_shift_us, max_shift_us, size=p.n_workflows, endpoint=True)
+    return p.copy(deadline_us=(p.deadline_us + shift).astype(np.int64))
 
 
 # ---------------------------------------------------------------------------

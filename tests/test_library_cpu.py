@@ -123,3 +123,30 @@ def test_routing_scorer(tmp_path):
     r = subprocess.run([str(exe)], capture_output=True, text=True)
     assert r.returncode == 0, r.stdout
     assert "mismatches 0" in r.stdout
+
+
+def test_kernels_keep_their_registers(tmp_path):
+    """No kernel spills to scratch memory beyond a small bound: a spill that
+    grows (the block sweep runs at the 128-register limit of 1024-thread
+    workgroups) turns into per-lane scratch traffic to HBM and slows the pass
+    several times over.  Resource usage as the compiler reports it for the
+    library's own build flags."""
+    from paper_2601_05109_amd import build
+    csrc = os.path.join(ROOT, "paper_2601_05109_amd", "csrc")
+    worst = {}
+    for src in sorted(f for f in os.listdir(csrc) if f.endswith(".hip")):
+        r = subprocess.run([build.HIPCC, *build.FLAGS, "-c", os.path.join(csrc, src), "-o",
+                            str(tmp_path / (src + ".o")), "-Rpass-analysis=kernel-resource-usage"],
+                           capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr[-2000:]
+        name = None
+        for line in r.stderr.splitlines():
+            m = re.search(r"Function Name: (\S+)", line)
+            if m:
+                name = m.group(1)
+            m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+            if m and name:
+                worst[name] = int(m.group(1))
+    assert worst, "no kernel resource remarks"
+    over = {k: v for k, v in worst.items() if v > 96}
+    assert not over, f"kernels spilling to scratch: {over}"
