@@ -81,7 +81,8 @@ struct Arena {
   int32_t* g_front[2] = {nullptr, nullptr};
   uint32_t* bcnt[2] = {nullptr, nullptr};  // bucket counters, by pass parity
   BucketSlot* bslot = nullptr;
-  int64_t capN = -1, capW = -1, capB = -1;
+  int64_t* split[2] = {nullptr, nullptr};   // bin splitters: read by one pass, written for the next
+  int64_t capN = -1, capW = -1, capB = -1, capRec = -1;
 };
 
 // The scratch a pass runs in: an arena and the state of what it holds (the
@@ -130,6 +131,10 @@ struct nalar_policy {
   int bucket_calm = 0;           // bucketed passes without overflow since the last change
   int bucket_relax = 64;         // calm passes before fewer buckets are tried again
   bool bucket_relaxed = false;   // the last pass tried fewer buckets
+  int split_nb = 0;              // bins the current splitters are for (0: none)
+  int split_cur = 0;             // the splitter buffer the next pass reads
+  int bin_skip = 0;              // passes left before bins are tried again
+  int bin_backoff = 1;
   std::string err;
   ArenaState own;                // scratch allocated by the library for this handle
   HostStatus* host = nullptr;    // pinned, written by the sort kernel
@@ -156,7 +161,7 @@ int hip_fail(nalar_policy* h, hipError_t e, const char* what) {
 }
 
 // Lay out (or measure, when base is null) the arena for the given capacities.
-size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B) {
+size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B, int64_t Rec) {
   size_t off = 0;
   auto take = [&](size_t bytes) {
     off = align_up(off, 256);
@@ -176,6 +181,7 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B) {
   a.itab.speed = reinterpret_cast<int32_t*>(take(4 * NALAR_MAX_INSTANCES));
   a.itab.pos_of = reinterpret_cast<int32_t*>(take(4 * NALAR_MAX_INSTANCES));
   a.itab.run = reinterpret_cast<uint32_t*>(take(4 * kTypeDirect));
+  a.itab.prun = reinterpret_cast<uint32_t*>(take(4 * kTypeDirect));
   a.wf_off = reinterpret_cast<int32_t*>(take(4 * size_t(w1 + 1)));
   a.stg_slack = reinterpret_cast<int64_t*>(take(8 * size_t(n1)));
   a.stg_cost = reinterpret_cast<int64_t*>(take(8 * size_t(n1)));
@@ -194,7 +200,9 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B) {
   a.g_nr = reinterpret_cast<uint8_t*>(take(size_t(n1)));
   const int64_t b1 = B > 0 ? B : 0;
   for (int i = 0; i < 2; ++i) a.bcnt[i] = reinterpret_cast<uint32_t*>(take(4 * size_t(b1 + 1)));
-  a.bslot = reinterpret_cast<BucketSlot*>(take(sizeof(BucketSlot) * size_t(b1) * kBucketCap));
+  const int64_t r1 = Rec > b1 * kBucketCap ? Rec : b1 * kBucketCap;
+  a.bslot = reinterpret_cast<BucketSlot*>(take(sizeof(BucketSlot) * size_t(r1)));
+  for (int i = 0; i < 2; ++i) a.split[i] = reinterpret_cast<int64_t*>(take(8 * size_t(kBinMax)));
   off = align_up(off, 256);
   a.lookback_off = off;
   a.slb = reinterpret_cast<uint64_t*>(take(8 * size_t(kMaxSortPasses) * tiles * kRadixBuckets));
@@ -207,22 +215,31 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B) {
   return align_up(off, 256);
 }
 
-int ensure_capacity(nalar_policy* h, int64_t N, int64_t W, int64_t B) {
+int ensure_capacity(nalar_policy* h, int64_t N, int64_t W, int64_t B, int64_t Rec) {
   Arena& a = h->own.ar;
-  if (a.base && N <= a.capN && W <= a.capW && B <= a.capB) return NALAR_OK;
+  if (a.base && N <= a.capN && W <= a.capW && B <= a.capB && Rec <= a.capRec) return NALAR_OK;
   int64_t newN = a.capN > N ? a.capN : N;
   int64_t newW = a.capW > W ? a.capW : W;
   int64_t newB = a.capB > B ? a.capB : B;
+  int64_t newRec = a.capRec > Rec ? a.capRec : Rec;
+  int64_t keep_split[kBinMax];  // the current splitters move to the new arena
   if (a.base) {  // grow geometrically so a slowly growing graph reallocates rarely
     if (N > a.capN) newN = N + N / 4;
     if (W > a.capW) newW = W + W / 4;
     hipError_t e = hipStreamSynchronize(h->stream);
     if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
+    if (h->split_nb > 0) {
+      e = hipMemcpy(keep_split, a.split[h->split_cur], sizeof(int64_t) * size_t(h->split_nb - 1),
+                    hipMemcpyDeviceToHost);
+      if (e != hipSuccess) h->split_nb = 0;
+    }
     (void)hipFree(a.base);
     a.base = nullptr;
+  } else {
+    h->split_nb = 0;
   }
   Arena fresh;
-  const size_t bytes = carve(fresh, nullptr, newN, newW, newB);
+  const size_t bytes = carve(fresh, nullptr, newN, newW, newB, newRec);
   void* p = nullptr;
   hipError_t e = hipMalloc(&p, bytes);
   if (e != hipSuccess) {
@@ -234,12 +251,18 @@ int ensure_capacity(nalar_policy* h, int64_t N, int64_t W, int64_t B) {
     (void)hipFree(p);
     return hip_fail(h, e, "hipMemset(scratch)");
   }
-  carve(fresh, static_cast<char*>(p), newN, newW, newB);
+  carve(fresh, static_cast<char*>(p), newN, newW, newB, newRec);
   fresh.base = p;
   fresh.bytes = bytes;
   fresh.capN = newN;
   fresh.capW = newW;
   fresh.capB = newB;
+  fresh.capRec = newRec;
+  if (h->split_nb > 0) {
+    e = hipMemcpy(fresh.split[h->split_cur], keep_split, sizeof(int64_t) * size_t(h->split_nb - 1),
+                  hipMemcpyHostToDevice);
+    if (e != hipSuccess) h->split_nb = 0;
+  }
   h->own.ar = fresh;
   h->own.epoch = 0;
   h->own.ctrl_dirty[0] = h->own.ctrl_dirty[1] = true;
@@ -289,6 +312,23 @@ BucketArgs plan_buckets(const nalar_policy* h, int64_t N, bool levels, bool wave
     bk.lshift = int16_t(lognb);
   }
   return bk;
+}
+
+// Bins for this pass (the block sweep of a large ready set, splitters from the
+// previous pass of this handle; bins == 0: not used).
+BucketArgs plan_bins(const nalar_policy* h, const SweepShape& sh, bool levels) {
+  BucketArgs bk{};
+  if ((h->flags & NALAR_FORCE_TILED_SORT) || sh.wave_path || levels || h->split_nb <= 0 ||
+      !h->hint_valid || h->hint_ready < kBinMinReady || h->bin_skip > 0)
+    return bk;
+  bk.bins = 1;
+  bk.nb = h->split_nb;
+  bk.cap = bin_cap_for(h->hint_ready, bk.nb);
+  return bk;
+}
+
+int64_t records_of(const BucketArgs& bk) {
+  return bk.bins ? int64_t(bk.nb) * bk.cap : int64_t(bk.nb) * kBucketCap;
 }
 
 bool in_range(int64_t v, int64_t lo, int64_t hi) { return v >= lo && v <= hi; }
@@ -411,31 +451,34 @@ int nalar_policy_create(const nalar_policy_config* cfg, nalar_policy** out) {
       e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
       if (e != hipSuccess) return bail(e, "hipGetSymbolAddress(scratch)");
       Arena& a = ss.st.ar;
-      const size_t need = carve(a, nullptr, NALAR_STATIC_MAX_NODES, NALAR_STATIC_MAX_WORKFLOWS, kStaticBuckets);
+      const size_t need = carve(a, nullptr, NALAR_STATIC_MAX_NODES, NALAR_STATIC_MAX_WORKFLOWS, kStaticBuckets, 0);
       if (need > kStaticScratchBytes) {
         g_create_error = "static scratch layout exceeds its array";
         nalar_policy_destroy(h);
         return NALAR_EDEVICE;
       }
-      carve(a, static_cast<char*>(ptr), NALAR_STATIC_MAX_NODES, NALAR_STATIC_MAX_WORKFLOWS, kStaticBuckets);
+      carve(a, static_cast<char*>(ptr), NALAR_STATIC_MAX_NODES, NALAR_STATIC_MAX_WORKFLOWS, kStaticBuckets, 0);
       a.base = ptr;
       a.bytes = need;
       a.capN = NALAR_STATIC_MAX_NODES;
       a.capW = NALAR_STATIC_MAX_WORKFLOWS;
       a.capB = kStaticBuckets;
+      a.capRec = int64_t(kStaticBuckets) * kBucketCap;
       ss.st.bcnt_clean[0] = ss.st.bcnt_clean[1] = false;  // cleared by the first pass
       ss.ready = true;
     }
   }
   e = prepare_sweep_kernels(h->lds_limit);
   if (e != hipSuccess) return bail(e, "hipFuncSetAttribute");
+  e = prepare_sort_kernels();
+  if (e != hipSuccess) return bail(e, "hipFuncSetAttribute(sort)");
   e = hipHostMalloc(reinterpret_cast<void**>(&h->host), sizeof(HostStatus), hipHostMallocCoherent);
   if (e != hipSuccess) return bail(e, "hipHostMalloc");
   for (int i = 0; i <= kMaxTimed; ++i) {
     e = hipEventCreate(&h->ev[i]);
     if (e != hipSuccess) return bail(e, "hipEventCreate");
   }
-  int rc = ensure_capacity(h, cfg->reserve_nodes, cfg->reserve_workflows, 0);
+  int rc = ensure_capacity(h, cfg->reserve_nodes, cfg->reserve_workflows, 0, 0);
   if (rc != NALAR_OK) {
     g_create_error = h->err;
     nalar_policy_destroy(h);
@@ -523,8 +566,10 @@ hipError_t clear_lookback(hipStream_t s, const Arena& A) {
 
 // The pass proper, in the scratch of `as` (sized for the snapshot and for the
 // buckets of bk), after the checks of the entry point.
+// own_splitters: the arena belongs to the handle, so the bin splitters it
+// holds are this handle's (bins and their splitters are used only then).
 int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaState& as, BucketArgs bk,
-             const SweepShape& sh) {
+             const SweepShape& sh, bool own_splitters) {
   hipError_t e;
   const int64_t N = p->n_nodes, W = p->n_workflows, M = p->n_instances;
   Arena& A = as.ar;
@@ -533,7 +578,11 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
   const int nxt = cur ^ 1;
   bk.cnt = A.bcnt[cur];
   bk.slot = A.bslot;
+  if (bk.bins) bk.split = A.split[h->split_cur];
   Ctrl* ctrl = A.ctrl[cur];
+  // the next pass's splitters: after the sort, from its output (block sweep,
+  // no priority levels, the handle's own arena)
+  const bool want_split = own_splitters && !sh.wave_path && !p->wf_priority;
 
   as.epoch = (as.epoch + 1) & kEpochMask;
   if (as.epoch == 0) {  // tags wrapped: forget every old look-back word
@@ -673,11 +722,20 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
   sa.slack = r->slack_us;
   sa.route = r->route;
   sa.cost = r->cost_us;
+  sa.split_next = A.split[h->split_cur ^ 1];
+  sa.p = pd;
+  sa.passes_launched = kMaxSortPasses;  // the bucketed and bin sorts finish in one launch
   __atomic_store_n(&h->host->max_bucket, 0u, __ATOMIC_RELAXED);       // written by the large-bucket sort
+  __atomic_store_n(&h->host->split_nb, 0u, __ATOMIC_RELAXED);         // written with new splitters
   __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);  // the kernels overwrite it
   bool tiled = bk.nb == 0;
   if (!tiled) {
-    NALAR_LAUNCH("sort_bucket", launch_bucket_sort(s, sa, bk));
+    if (bk.bins) {
+      NALAR_LAUNCH("sort_bin", launch_bin_sort(s, sa, bk));
+    } else {
+      NALAR_LAUNCH("sort_bucket", launch_bucket_sort(s, sa, bk));
+      if (want_split) NALAR_LAUNCH("splitters", launch_splitters(s, sa));
+    }
     tm.end();
     e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
@@ -688,21 +746,28 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
       // into; the next pass's control block and counters are reset again too.
       __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);
       tiled = true;
-      h->bucket_calm = 0;
-      // fewer buckets overflowed at once: wait twice as long before trying again
-      if (h->bucket_relaxed && h->bucket_relax < 4096) h->bucket_relax *= 2;
-      h->bucket_relaxed = false;
-      if (h->bucket_dense < 3) {  // retry at once with more buckets
-        ++h->bucket_dense;
-      } else {                    // then back off
-        h->bucket_skip = h->bucket_backoff;
-        h->bucket_backoff = h->bucket_backoff < 64 ? 2 * h->bucket_backoff : 64;
+      if (bk.bins) {  // a bin overflowed: new splitters come from the tiled sort; back off
+        h->bin_skip = h->bin_backoff;
+        h->bin_backoff = h->bin_backoff < 64 ? 2 * h->bin_backoff : 64;
+      } else {
+        h->bucket_calm = 0;
+        // fewer buckets overflowed at once: wait twice as long before trying again
+        if (h->bucket_relaxed && h->bucket_relax < 4096) h->bucket_relax *= 2;
+        h->bucket_relaxed = false;
+        if (h->bucket_dense < 3) {  // retry at once with more buckets
+          ++h->bucket_dense;
+        } else {                    // then back off
+          h->bucket_skip = h->bucket_backoff;
+          h->bucket_backoff = h->bucket_backoff < 64 ? 2 * h->bucket_backoff : 64;
+        }
       }
       NALAR_LAUNCH("reset", launch_reset(s, ctrl, nullptr, 0));
       if (policy & NALAR_ROUTE_WEIGHTED)  // its weight check reports into the block just reset
         NALAR_LAUNCH("weighted_table", launch_weighted_table(s, wa));
       sw.bk = BucketArgs{};
       NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
+    } else if (bk.bins) {
+      h->bin_backoff = 1;
     } else {
       h->bucket_backoff = 1;
       const bool crowded = __atomic_load_n(&h->host->max_bucket, __ATOMIC_ACQUIRE) > kBucketCrowded;
@@ -723,15 +788,19 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
     }
   }
   if (tiled) {
+    sa.passes_launched = kSortLaunched;
     e = launch_slack_sort(s, sa, 0, kSortLaunched - 1, Timer::cb, &tm);
     if (e != hipSuccess) return hip_fail(h, e, "sort");
+    if (want_split) NALAR_LAUNCH("splitters", launch_splitters(s, sa));
     tm.end();
     e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
     if (__atomic_load_n(&h->host->status, __ATOMIC_ACQUIRE) == kStatusContinue) {
       __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);
+      sa.passes_launched = kMaxSortPasses;
       e = launch_slack_sort(s, sa, kSortLaunched, kMaxSortPasses - 1, Timer::cb, &tm);
       if (e != hipSuccess) return hip_fail(h, e, "sort");
+      if (want_split) NALAR_LAUNCH("splitters", launch_splitters(s, sa));
       tm.end();
       e = hipStreamSynchronize(s);
       if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
@@ -745,6 +814,11 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
   if (st & kStCycle) return fail(h, NALAR_ECYCLE, "dependency cycle");
   if (st & kStRange) return fail(h, NALAR_ERANGE, "remaining critical path exceeds 2^62 us");
   r->n_ready = __atomic_load_n(&h->host->n_ready, __ATOMIC_ACQUIRE);
+  if (want_split || bk.bins) {  // splitters written for the next pass: read them from now on
+    const uint32_t snb = __atomic_load_n(&h->host->split_nb, __ATOMIC_ACQUIRE);
+    h->split_nb = int(snb);
+    if (snb > 0) h->split_cur ^= 1;
+  }
   if ((policy & NALAR_ROUTE_GREEDY) && r->n_ready > 0 && M > 0) {
     // route again in output order with running loads (one wavefront per type)
     __atomic_store_n(&h->host->aux_status, 0u, __ATOMIC_RELEASE);
@@ -796,11 +870,13 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
   const int64_t N = p->n_nodes, W = p->n_workflows, M = p->n_instances;
   const SweepShape sh = plan_sweep(N, W, M, h->cus, h->lds_limit);
-  const BucketArgs bk = plan_buckets(h, N, p->wf_priority != nullptr, sh.wave_path != 0);
+  BucketArgs bk = plan_bins(h, sh, p->wf_priority != nullptr);
+  if (!bk.bins) bk = plan_buckets(h, N, p->wf_priority != nullptr, sh.wave_path != 0);
   if (h->bucket_skip > 0) --h->bucket_skip;
-  rc = ensure_capacity(h, N, W, bk.nb);
+  if (h->bin_skip > 0) --h->bin_skip;
+  rc = ensure_capacity(h, N, W, bk.nb, records_of(bk));
   if (rc != NALAR_OK) return rc;
-  return run_pass(h, p, r, h->own, bk, sh);
+  return run_pass(h, p, r, h->own, bk, sh, true);
 }
 
 int nalar_policy_pass_static(nalar_policy* h, const nalar_problem* p, nalar_result* r) {
@@ -827,7 +903,7 @@ int nalar_policy_pass_static(nalar_policy* h, const nalar_problem* p, nalar_resu
     if (e != hipSuccess) return hip_fail(h, e, "clear look-back");
     ss.cleared = true;
   }
-  return run_pass(h, p, r, ss.st, bk, sh);
+  return run_pass(h, p, r, ss.st, bk, sh, false);
 }
 
 }  // extern "C"

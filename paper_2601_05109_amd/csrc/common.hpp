@@ -94,6 +94,29 @@ constexpr uint32_t kBucketCrowded = 8;
 static_assert(kBucketLbMin % kBucketLbGroup == 0, "whole groups");
 constexpr uint32_t kStatusTiled = 0x20000000u;
 
+// Partition sort of large ready sets (the block sweep): the previous pass's
+// key quantiles split the keys into nb bins (a power of two with at most
+// kBinTarget ready futures each on average); every workgroup of the sweep
+// counts its ready futures per bin in LDS, claims one segment of each bin with
+// one atomic, and writes them there; k_bin_sort then orders each bin in LDS
+// (at most kBinCap futures; more is an overflow, like a full bucket) and writes
+// the outputs at the bin's offset.
+constexpr int64_t kBinMinReady = 65536;   // smaller ready sets keep the buckets
+constexpr int kBinTarget = 1024;          // futures per bin on average
+constexpr int kBinCap = 2560;             // records per bin (LDS of k_bin_sort)
+constexpr int kBinMin = 64;               // bins: a power of two in [kBinMin, kBinMax]
+constexpr int kBinMax = 2048;
+// bins for a ready count (the same rule on the host and on the device)
+__host__ __device__ inline int bins_for(int64_t R) {
+  int nb = kBinMin;
+  while (nb < kBinMax && int64_t(nb) * kBinTarget < R) nb *= 2;
+  return nb;
+}
+__host__ __device__ inline int bin_cap_for(int64_t R, int nb) {
+  const int64_t c = 2 * ((R + nb - 1) / nb) + 256;
+  return int(c < kBinCap ? c : kBinCap);
+}
+
 struct BucketSlot {
   int64_t key;      // the order key: the slack, or -rem / rem under NALAR_ORDER_LPT / _SRTF
   int64_t cost;
@@ -120,7 +143,7 @@ struct HostStatus {
   uint32_t aux_status; // status bits of the load-aware routing kernel
   uint32_t level_mask; // priority levels of this pass (bit l: level l; with levels only)
   uint32_t max_bucket; // futures in the fullest bucket (large-bucket sort only, else 0)
-  uint32_t pad_;
+  uint32_t split_nb;   // bins the splitters written by this pass are for (0: none)
 };
 
 // Resets a control block for a later pass (run by one workgroup).
@@ -186,6 +209,8 @@ struct ITab {
   int32_t* speed;     // [M]
   int32_t* pos_of;    // [M] sorted position of original index i
   uint32_t* run;      // [kTypeDirect] first | end << 16 (0: no instance)
+  uint32_t* prun;     // [kTypeDirect] end of the type's undominated instances,
+                      //   which open its run (see route_future)
 };
 
 // ----------------------------------------------------------------- wave ops
@@ -396,12 +421,20 @@ __host__ __device__ inline int64_t floordiv_exact(double a, int32_t d, double in
 // best candidate overall plus the penalty (ties broken by index).  With
 // `stateful`, a future whose state lives on an instance of its own type runs
 // there, at that instance's cost and with no other candidate.
+//
+// With s_prun, the run of a small type opens with its undominated instances
+// (ascending index) and only those are scanned: instance j of the type is
+// dominated when another instance i of it has load_i <= load_j and speed_i >=
+// speed_j, with i < j or load_i < load_j.  Then for every estimate i's service
+// time is at most j's, so i's cost is at most j's and i wins every tie on
+// index, or its cost is strictly lower: j can never be the lexicographic
+// minimum of (cost, index), and leaving it out changes no result.
 __host__ __device__ inline void route_future(int32_t t, int64_t est, int32_t loc, int32_t M, int64_t mig,
                                     const int32_t* s_type, const int32_t* s_idx,
                                     const int64_t* s_load, const int32_t* s_speed,
                                     const double* s_inv, const int32_t* s_pos,
                                     const uint32_t* s_run, bool stateful, int32_t& route,
-                                    int64_t& cost) {
+                                    int64_t& cost, const uint32_t* s_prun = nullptr) {
   if (stateful && loc >= 0) {
     const int pl = s_pos[loc];
     if (s_type[pl] == t) {
@@ -414,7 +447,7 @@ __host__ __device__ inline void route_future(int32_t t, int64_t est, int32_t loc
   if (uint32_t(t) < uint32_t(kTypeDirect)) {
     const uint32_t rn = s_run[t];
     lo = int(rn & 0xFFFFu);
-    hi = int(rn >> 16);
+    hi = s_prun ? int(s_prun[t]) : int(rn >> 16);
   } else {
     lo = 0;
     hi = M;

@@ -52,6 +52,10 @@ struct SortArgs {
   uint64_t* bagg;               // [kBucketLbGroups] futures per group of buckets
   uint32_t epoch;
   uint32_t levels;              // nonzero: the keys carry priority levels
+  int64_t* split_next;          // [kBinMax - 1] this pass's key quantiles, for the next pass
+  int32_t passes_launched;      // tiled sort: digit passes launched so far (the
+                                //   splitters wait for the last one)
+  ProblemDev p;                 // the snapshot (deadline, wf and the key's policy for the splitters)
   int32_t* order;
   int64_t* slack;
   int32_t* route;
@@ -78,15 +82,23 @@ struct GroupArgs {
 // 2^lshift buckets); a level above lvl_hi takes bucket 0 and one below the
 // last group bucket nb - 1, so buckets still ascend in (-level, key), and the
 // ranking inside a bucket compares levels first.
+//
+// Bins (bins != 0, the partition sort of large ready sets, block sweep only):
+// nb bins of `cap` records, the bin of a key being the number of splitters
+// (split, nb - 1 ascending keys: the previous pass's key quantiles) at or below
+// it; cnt holds each bin's claimed records and slot its records.
 struct BucketArgs {
   int64_t lo;
   int32_t shift;
   int32_t nb;
   uint32_t* cnt;                // [nb] futures dropped into each bucket (16-byte aligned)
-  BucketSlot* slot;             // [nb * kBucketCap]
+  BucketSlot* slot;             // [nb * kBucketCap], or [nb * cap] with bins
   int32_t lvl_hi;
   int16_t ngroups;
   int16_t lshift;
+  int32_t bins;                 // nonzero: key bins
+  int32_t cap;                  // records per bin
+  const int64_t* split;         // [nb - 1] splitters
 };
 
 struct SweepArgs {
@@ -205,6 +217,11 @@ hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* ne
 // sort.hip (mark(ctx, name) is called before each launch, for timing)
 hipError_t launch_reset(hipStream_t s, Ctrl* c, uint32_t* clear, int64_t n_clear);
 hipError_t launch_bucket_sort(hipStream_t s, const SortArgs& a, const BucketArgs& bk);
+hipError_t launch_bin_sort(hipStream_t s, const SortArgs& a, const BucketArgs& bk);
+hipError_t prepare_sort_kernels();  // LDS limits of the sort kernels (at handle creation)
+// The next pass's splitters from this pass's output (after the tiled or the
+// bucketed sort of a large ready set).
+hipError_t launch_splitters(hipStream_t s, const SortArgs& a);
 hipError_t launch_slack_sort(hipStream_t s, const SortArgs& a, int first_pass, int last_pass,
                              void (*mark)(void*, const char*), void* ctx);
 hipError_t launch_group(hipStream_t s, const GroupArgs& a, void (*mark)(void*, const char*),

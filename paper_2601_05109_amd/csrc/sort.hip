@@ -668,6 +668,254 @@ __global__ __launch_bounds__(kBucketLbGroup) void k_bucket_sort_lb(SortArgs a, B
   }
 }
 
+// ------------------------------------------------------------ bin sort
+
+constexpr int kBinThreads = 256;
+
+// The key a pass orders by, recovered from its output at rank g: the slack,
+// or the remaining critical path (deadline - now - slack) negated under LPT or
+// as it is under SRTF.
+__device__ inline int64_t output_key(const SortArgs& a, int64_t g) {
+  const int64_t sl = a.slack[g];
+  if (!(a.p.policy & (NALAR_ORDER_LPT | NALAR_ORDER_SRTF))) return sl;
+  const int32_t v = a.order[g];
+  const int64_t rem = (a.p.deadline[a.p.wf[v]] - a.p.now) - sl;
+  return (a.p.policy & NALAR_ORDER_LPT) ? -rem : rem;
+}
+
+// One workgroup per bin: its records (claimed by the sweep in any order) are
+// sorted in LDS by (key, position) with a stable LSD radix sort: 8-bit digits
+// of the position (relative to the bin's lowest) first, then of the key
+// (relative to the bin's lowest key), so that the last passes order by key
+// and equal keys keep their position order; only as many digits as the
+// bin's ranges need.  Each pass ranks its items as the tiled sort's digit
+// passes do (wave w owns a contiguous run of items, lanes of equal digit found
+// by ballots, per-wave digit counts in LDS) and scatters them to the other
+// buffer.  The sorted bin is written at its offset (the records of all lower
+// bins).  Keys are unique with their positions, so this is the (key, wf, id)
+// order.  The workgroups also write the next pass's splitters (this pass's key
+// quantiles: the key at rank (q + 1) * R / nb' for nb' = bins_for(R)), each
+// those that fall into its bin, and workgroup 0 publishes the status.
+constexpr int kBinWaves = kBinThreads / kWave;
+constexpr int kBinJ = (kBinCap + kBinThreads - 1) / kBinThreads;  // items per lane
+
+struct BinSmem {
+  int64_t key[2][kBinCap];
+  int32_t pos[2][kBinCap];
+  uint16_t idx[2][kBinCap];
+  uint32_t whist[kBinWaves][kRadixBuckets];
+  uint32_t dstart[kRadixBuckets];
+  uint32_t tmp[kBinWaves];
+  int64_t range[kRangeWords];
+  int64_t red[4][kBinWaves];
+};
+
+__device__ inline uint32_t bin_digit(int64_t key, int32_t pos, int pass, int ppass, int64_t kmin,
+                                     int32_t pmin) {
+  return pass < ppass ? (uint32_t(pos - pmin) >> (8 * pass)) & 0xFFu
+                      : uint32_t((uint64_t(key) - uint64_t(kmin)) >> (8 * (pass - ppass))) & 0xFFu;
+}
+
+__global__ __launch_bounds__(kBinThreads) void k_bin_sort(SortArgs a, BucketArgs bk) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  BinSmem& S = *reinterpret_cast<BinSmem*>(smem);
+  const int tid = threadIdx.x;
+  const int wv = tid / kWave;
+  const int ln = lane_id();
+  const int b = blockIdx.x;
+  Ctrl* ctrl = a.ctrl;
+  const uint32_t status = ctrl->status | ctrl->status_sweep;
+  const uint32_t overflow = ctrl->bucket_overflow;
+  RangeLanes rl;
+  if (b == 0) rl = load_range_lanes(ctrl, a.levels != 0);
+  const uint32_t cap = uint32_t(bk.cap);
+  uint32_t before = 0, total = 0;
+  for (int i = tid; i < bk.nb; i += kBinThreads) {
+    uint32_t c = bk.cnt[i];
+    c = c < cap ? c : cap;
+    total += c;
+    before += i < b ? c : 0u;
+  }
+  if (status) {
+    if (b == 0 && tid == 0) publish_status(a.host, status, 0, 0, 0, 0, 0u);
+    return;
+  }
+  if (b == 0) {
+    settle_range(rl, ctrl, S.range, true, a.levels != 0);
+    if (tid == 0) publish_range(a.host, overflow ? kStatusTiled : 0u, S.range);
+  }
+  if (overflow) return;
+  uint32_t n = bk.cnt[b];
+  n = n < cap ? n : cap;
+  const BucketSlot* rec = bk.slot + int64_t(b) * cap;
+  // wave w owns items [w * C, (w + 1) * C), item j of lane l at w * C + j * 64 + l
+  const int J = int((n + kBinThreads - 1) / kBinThreads);
+  const int C = J * kWave;
+  int64_t key[kBinJ];
+  int32_t pos[kBinJ];
+  uint16_t idx[kBinJ];
+  int64_t kmin = INT64_MAX, kmax = INT64_MIN;
+  int32_t pmin = INT32_MAX, pmax = INT32_MIN;
+#pragma unroll
+  for (int j = 0; j < kBinJ; ++j) {
+    const int i = wv * C + j * kWave + ln;
+    key[j] = 0;
+    pos[j] = 0;
+    idx[j] = 0;
+    if (j < J && i < int(n)) {
+      key[j] = rec[i].key;
+      pos[j] = rec[i].pos;
+      idx[j] = uint16_t(i);
+      kmin = key[j] < kmin ? key[j] : kmin;
+      kmax = key[j] > kmax ? key[j] : kmax;
+      pmin = pos[j] < pmin ? pos[j] : pmin;
+      pmax = pos[j] > pmax ? pos[j] : pmax;
+    }
+  }
+  // block sums: records before this bin and in total; the bin's ranges
+  {
+    const int64_t s0 = wave_sum_i64(int64_t(before)), s1 = wave_sum_i64(int64_t(total));
+    const int64_t m0 = wave_min_i64(kmin), m1 = wave_max_i64(kmax);
+    const int64_t q0 = wave_min_i64(pmin), q1 = wave_max_i64(pmax);
+    if (ln == 0) {
+      S.red[0][wv] = s0;
+      S.red[1][wv] = s1;
+      S.red[2][wv] = m0;
+      S.red[3][wv] = m1;
+      S.key[0][wv] = q0;  // scratch for the position range, overwritten below
+      S.key[1][wv] = q1;
+    }
+    __syncthreads();
+    before = 0;
+    total = 0;
+    kmin = INT64_MAX;
+    kmax = INT64_MIN;
+    int64_t pm0 = INT64_MAX, pm1 = INT64_MIN;
+    for (int w = 0; w < kBinWaves; ++w) {
+      before += uint32_t(S.red[0][w]);
+      total += uint32_t(S.red[1][w]);
+      kmin = S.red[2][w] < kmin ? S.red[2][w] : kmin;
+      kmax = S.red[3][w] > kmax ? S.red[3][w] : kmax;
+      pm0 = S.key[0][w] < pm0 ? S.key[0][w] : pm0;
+      pm1 = S.key[1][w] > pm1 ? S.key[1][w] : pm1;
+    }
+    pmin = int32_t(pm0);
+    pmax = int32_t(pm1);
+    __syncthreads();
+  }
+  const int64_t R = total;
+  int ppass = 0, kpass = 0;
+  if (n > 1) {
+    const uint32_t pr = uint32_t(pmax - pmin);
+    const uint64_t kr = uint64_t(kmax) - uint64_t(kmin);
+    ppass = pr ? (32 - __builtin_clz(pr) + 7) / 8 : 0;
+    kpass = kr ? (64 - __builtin_clzll(kr) + 7) / 8 : 0;
+  }
+  const int npass = ppass + kpass;
+  int cur = 0;
+  for (int pass = 0; pass < npass; ++pass) {
+    for (int i = tid; i < kBinWaves * kRadixBuckets; i += kBinThreads) (&S.whist[0][0])[i] = 0;
+    __syncthreads();
+    uint32_t rank[kBinJ];
+    uint32_t* wh = S.whist[wv];
+#pragma unroll
+    for (int j = 0; j < kBinJ; ++j) {
+      rank[j] = 0;
+      if (j >= J) continue;  // the same on every lane
+      const bool valid = wv * C + j * kWave + ln < int(n);
+      const uint32_t dg = bin_digit(key[j], pos[j], pass, ppass, kmin, pmin);
+      uint64_t peers = ballot(valid);
+#pragma unroll
+      for (int bit = 0; bit < kRadixBits; ++bit) {
+        const bool on = (dg >> bit) & 1u;
+        const uint64_t m = ballot(on);
+        peers &= on ? m : ~m;
+      }
+      const uint64_t below = peers & lanemask_lt();
+      uint32_t c = 0;
+      if (valid) c = wh[dg];
+      rank[j] = c + uint32_t(__popcll(below));
+      if (valid && below == 0) wh[dg] = c + uint32_t(__popcll(peers));
+    }
+    __syncthreads();
+    // digit totals; per-wave counts become exclusive offsets inside the digit
+    uint32_t tot = 0;
+    if (tid < kRadixBuckets) {
+      for (int w = 0; w < kBinWaves; ++w) {
+        const uint32_t c = S.whist[w][tid];
+        S.whist[w][tid] = tot;
+        tot += c;
+      }
+    }
+    const uint32_t excl = block_excl_scan(tid < kRadixBuckets ? tot : 0u, S.tmp);
+    if (tid < kRadixBuckets) S.dstart[tid] = excl;
+    __syncthreads();
+    const int nxt = cur ^ 1;
+#pragma unroll
+    for (int j = 0; j < kBinJ; ++j) {
+      if (j >= J || wv * C + j * kWave + ln >= int(n)) continue;
+      const uint32_t dg = bin_digit(key[j], pos[j], pass, ppass, kmin, pmin);
+      const uint32_t o = S.dstart[dg] + S.whist[wv][dg] + rank[j];
+      S.key[nxt][o] = key[j];
+      S.pos[nxt][o] = pos[j];
+      S.idx[nxt][o] = idx[j];
+    }
+    __syncthreads();
+    cur = nxt;
+    // the next pass reads its items back in the same (wave, item, lane) order
+#pragma unroll
+    for (int j = 0; j < kBinJ; ++j) {
+      const int i = wv * C + j * kWave + ln;
+      if (j < J && i < int(n)) {
+        key[j] = S.key[cur][i];
+        pos[j] = S.pos[cur][i];
+        idx[j] = S.idx[cur][i];
+      }
+    }
+  }
+  // write the sorted bin: rank r holds (key[j], pos[j]) of item i = r
+#pragma unroll
+  for (int j = 0; j < kBinJ; ++j) {
+    const int r = wv * C + j * kWave + ln;
+    if (j >= J || r >= int(n)) continue;
+    const int64_t g = int64_t(before) + r;
+    const int32_t ps = pos[j];
+    const BucketSlot& src = rec[idx[j]];
+    a.order[g] = a.node_of_pos ? a.node_of_pos[ps] : ps;
+    a.slack[g] = a.out_slack ? a.out_slack[ps] : key[j];
+    a.route[g] = slot_route(src.route);
+    if (a.cost) a.cost[g] = src.cost;
+  }
+  // the next pass's splitters that fall into this bin
+  // (with no pass the bin holds at most one record, in place)
+  const int nbn = R >= kBinMinReady ? bins_for(R) : 0;
+  for (int q = tid; q < nbn - 1; q += kBinThreads) {
+    const int64_t g = (int64_t(q) + 1) * R / nbn;
+    if (g >= int64_t(before) && g < int64_t(before) + int64_t(n)) {
+      const int r = int(g - before);
+      a.split_next[q] = npass ? S.key[cur][r] : rec[r].key;
+    }
+  }
+  if (b == 0 && tid == 0)
+    __hip_atomic_store(&a.host->split_nb, uint32_t(nbn), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// The next pass's splitters from the output of the tiled or bucketed sort
+// (one workgroup; R from the control block the sort settled).
+__global__ __launch_bounds__(kSortThreads) void k_splitters(SortArgs a) {
+  Ctrl* ctrl = a.ctrl;
+  // nothing when the pass failed, a bucket overflowed (the host sorts again),
+  // or the tiled sort has passes still to run
+  if (ctrl->bucket_overflow || int(ctrl->sort_npass) > a.passes_launched) return;
+  const uint32_t bad = ctrl->status | ctrl->status_sweep;
+  const int64_t R = ctrl->n_ready;
+  const int nbn = (bad == 0 && R >= kBinMinReady) ? bins_for(R) : 0;
+  for (int q = threadIdx.x; q < nbn - 1; q += kSortThreads)
+    a.split_next[q] = output_key(a, (int64_t(q) + 1) * R / nbn);
+  if (threadIdx.x == 0)
+    __hip_atomic_store(&a.host->split_nb, uint32_t(nbn), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 __global__ __launch_bounds__(kSortThreads) void k_slack_hist(SortArgs a) {
   __shared__ uint32_t H[kMaxSortPasses][kRadixBuckets];
   __shared__ int64_t s_range[kRangeWords];
@@ -796,6 +1044,21 @@ hipError_t launch_bucket_sort(hipStream_t s, const SortArgs& a, const BucketArgs
     hipLaunchKernelGGL(k_bucket_sort_lb, dim3(groups), dim3(kBucketLbGroup), 0, s, a, bk);
   } else
     hipLaunchKernelGGL(k_bucket_sort, dim3(bk.nb / kBucketGroup), dim3(kBucketThreads), 0, s, a, bk);
+  return hipGetLastError();
+}
+
+hipError_t launch_bin_sort(hipStream_t s, const SortArgs& a, const BucketArgs& bk) {
+  hipLaunchKernelGGL(k_bin_sort, dim3(bk.nb), dim3(kBinThreads), sizeof(BinSmem), s, a, bk);
+  return hipGetLastError();
+}
+
+hipError_t prepare_sort_kernels() {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bin_sort),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, int(sizeof(BinSmem)));
+}
+
+hipError_t launch_splitters(hipStream_t s, const SortArgs& a) {
+  hipLaunchKernelGGL(k_splitters, dim3(1), dim3(kSortThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -214,6 +214,7 @@ struct ITabLds {
   int32_t* speed;
   int32_t* pos;
   uint32_t* run;    // [kTypeDirect]
+  uint32_t* prun;   // [kTypeDirect] undominated ends (tables from the node kernel), or NULL
 };
 
 struct Acc {
@@ -243,10 +244,27 @@ __device__ inline uint32_t bucket_of(const BucketArgs& bk, int64_t key, int lvl)
   return base + (q < uint64_t(last) ? uint32_t(q) : last);
 }
 
+// Bin of a key: the number of splitters at or below it (splitters ascending,
+// in LDS), so bins ascend with the key and equal keys share a bin.
+__device__ inline uint32_t bin_of(const int64_t* split, int nb, int64_t key) {
+  int lo = 0, n = nb - 1;
+  while (n > 0) {
+    const int half = n >> 1;
+    if (split[lo + half] <= key) {
+      lo += half + 1;
+      n -= half + 1;
+    } else {
+      n = half;
+    }
+  }
+  return uint32_t(lo);
+}
+
 __device__ inline void bucket_put(const SweepArgs& a, uint32_t bkt, uint32_t slot, int64_t key,
                                   int64_t pos, int32_t route, int lvl, int64_t cost) {
-  if (slot < uint32_t(kBucketCap)) {
-    BucketSlot* sl = a.bk.slot + int64_t(bkt) * kBucketCap + slot;
+  const uint32_t cap = a.bk.bins ? uint32_t(a.bk.cap) : uint32_t(kBucketCap);
+  if (slot < cap) {
+    BucketSlot* sl = a.bk.slot + int64_t(bkt) * cap + slot;
     sl->key = key;
     sl->cost = cost;
     sl->pos = int32_t(pos);
@@ -295,21 +313,22 @@ __device__ inline void store_ready(const SweepArgs& a, uint32_t bkt, uint32_t sl
   acc.tready += 1;
 }
 
+// split_l: the splitters in LDS when the pass uses bins (block kernel only).
 template <bool kLevels>
 __device__ inline void write_ready(const SweepArgs& a, const ITabLds& it, int64_t pos, int32_t type,
                                    int32_t loc, int64_t rem, int64_t est, int64_t dl, int lvl,
-                                   Acc& acc) {
+                                   Acc& acc, const int64_t* split_l) {
   const int64_t key = order_key(a, rem, dl);
   const BucketArgs& bk = a.bk;
   uint32_t bkt = 0, slot = 0;
   if (bk.nb > 0) {
-    bkt = bucket_of<kLevels>(bk, key, lvl);
+    bkt = bk.bins ? bin_of(split_l, bk.nb, key) : bucket_of<kLevels>(bk, key, lvl);
     slot = add_agent(bk.cnt + bkt, 1u);
   }
   int32_t route;
   int64_t cost;
   route_future(type, est, loc, int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load, it.speed,
-               it.inv, it.pos, it.run, (a.p.policy & NALAR_ROUTE_STATEFUL) != 0, route, cost);
+               it.inv, it.pos, it.run, (a.p.policy & NALAR_ROUTE_STATEFUL) != 0, route, cost, it.prun);
   store_ready(a, bkt, slot, key, lvl, dl - rem, pos, route, cost, acc);
 }
 
@@ -326,10 +345,18 @@ __device__ inline int dep_at(uint32_t p01, uint32_t p2, int q) {
   return x == kNoDep ? -1 : int(x);
 }
 
+// With bins, bl holds the splitters and two per-bin counter arrays in LDS
+// (zero on entry, left zero on return).
+struct BinLds {
+  const int64_t* split;   // [nb - 1]
+  uint32_t* cnt;          // [nb] this workflow's ready futures in each bin
+  uint32_t* base;         // [nb] the segment each bin gave this workflow
+};
+
 template <int T, int NPT>
-__device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
+__device__ __attribute__((always_inline)) void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
                           int64_t* mx, int32_t* cnt, uint8_t* dn, uint8_t* nr, int lds_cap, int64_t b,
-                          int n, int64_t dl, int lvl, Acc& acc) {
+                          int n, int64_t dl, int lvl, Acc& acc, const BinLds& bl) {
   const int tid = threadIdx.x;
   Ctrl* ctrl = a.ctrl;
 
@@ -502,12 +529,55 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
   __syncthreads();  // nothing is in flight here, so this barrier waits for no store
   if (tid == 0 && S.proc != n) flag_sweep(ctrl, kStCycle);
 
-  // D: every bucket-slot atomic first, then the rem stores, then the routing
-  // (LDS and arithmetic only) while the atomics are in flight, then the
-  // stores of the ready futures.  No barrier follows: the next workflow of
-  // this workgroup touches only its own threads' LDS entries before its
-  // first barrier.
+  if (a.rem_out) {  // rem stayed in LDS during the levels; store it once
+#pragma unroll
+    for (int j = 0; j < NPT; ++j)
+      if ((fin >> j) & 1u) a.rem_out[vv[j]] = mx[j * T + tid];
+  }
   const BucketArgs& bk = a.bk;
+  if (bk.bins) {
+    // D (bins): the bin of each ready future and its rank inside this
+    // workflow's part of the bin (LDS counters), kept in the consumer
+    // counters, which the levels left at zero: bin | rank << 16 (rank <
+    // lds_cap < 2^16, bin < kBinMax).  Then one segment of each bin for the
+    // whole workflow (one atomic per bin), and each future is routed and
+    // stored into its segment.
+#pragma unroll 1
+    for (int j = 0; j < NPT; ++j) {
+      if (!((ready >> j) & 1u)) continue;
+      const int k = j * T + tid;
+      const uint32_t bn = bin_of(bl.split, bk.nb, order_key(a, mx[k], dl));
+      cnt[k] = int32_t(bn | (atomicAdd(&bl.cnt[bn], 1u) << 16));
+    }
+    __syncthreads();
+    for (int t = tid; t < bk.nb; t += T) {
+      const uint32_t c = bl.cnt[t];
+      bl.base[t] = c ? add_agent(bk.cnt + t, c) : 0u;
+      bl.cnt[t] = 0;  // clean for the next workflow
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+      if (!((ready >> j) & 1u)) continue;
+      const int k = j * T + tid;
+      int32_t route;
+      int64_t cost;
+      route_future(ty[j], ee[j], lc[j], int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load, it.speed,
+                   it.inv, it.pos, it.run, (a.p.policy & NALAR_ROUTE_STATEFUL) != 0, route, cost, it.prun);
+      const uint32_t pk = uint32_t(cnt[k]);
+      const uint32_t bn = pk & 0xFFFFu;
+      const int64_t r = mx[k];
+      store_ready(a, bn, (pk >> 16) + bl.base[bn], order_key(a, r, dl), lvl, dl - r, b + k, route, cost, acc);
+      cnt[k] = 0;  // the next workflow starts from zero counters
+    }
+    return;
+  }
+
+  // D (buckets or staging): every bucket-slot atomic first, then the
+  // routing (LDS and arithmetic only) while the atomics are in flight, then
+  // the stores of the ready futures.  No barrier follows: the next workflow of
+  // this workgroup touches only its own threads' LDS entries before its first
+  // barrier.
   uint32_t bkt[NPT], slot[NPT];
 #pragma unroll
   for (int j = 0; j < NPT; ++j) {
@@ -518,11 +588,6 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
       slot[j] = add_agent(bk.cnt + bkt[j], 1u);
     }
   }
-  if (a.rem_out) {  // rem stayed in LDS during the levels; store it once
-#pragma unroll
-    for (int j = 0; j < NPT; ++j)
-      if ((fin >> j) & 1u) a.rem_out[vv[j]] = mx[j * T + tid];
-  }
   int32_t route[NPT];
   int64_t cost[NPT];
 #pragma unroll
@@ -532,7 +597,7 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
     if ((ready >> j) & 1u)
       route_future(ty[j], ee[j], lc[j], int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load, it.speed,
                    it.inv, it.pos, it.run, (a.p.policy & NALAR_ROUTE_STATEFUL) != 0, route[j],
-                   cost[j]);
+                   cost[j], it.prun);
   }
 #pragma unroll
   for (int j = 0; j < NPT; ++j) __asm__ __volatile__("" : "+v"(slot[j]) :: "memory");
@@ -549,7 +614,8 @@ __device__ void sweep_lds(const SweepArgs& a, const Layout& L, const ITabLds& it
 
 template <int T, bool kFused, bool kLevels>
 __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, const Layout& L, const ITabLds& it, Shared& S,
-                          int w, int64_t b, int n, int64_t dl, int lvl, Acc& acc) {
+                          int w, int64_t b, int n, int64_t dl, int lvl, Acc& acc,
+                          const int64_t* split_l) {
   const int tid = threadIdx.x;
   Ctrl* ctrl = a.ctrl;
   int32_t* cnt = a.g_cnt + b;
@@ -725,7 +791,8 @@ __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, con
   for (int k = tid; k < n; k += T) {
     if (dn[k] == 0 && nr[k] == 0) {
       const int32_t v = node_at(L, b + k);
-      write_ready<kLevels>(a, it, b + k, a.p.type[v], a.p.loc[v], ld_wg(&mx[k]), a.p.est[v], dl, lvl, acc);
+      write_ready<kLevels>(a, it, b + k, a.p.type[v], a.p.loc[v], ld_wg(&mx[k]), a.p.est[v], dl, lvl, acc,
+                           split_l);
     }
   }
   __syncthreads();
@@ -1321,6 +1388,12 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
   it.speed = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
   it.pos = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
   it.run = reinterpret_cast<uint32_t*>(sp); sp += 4 * size_t(kTypeDirect);
+  it.prun = reinterpret_cast<uint32_t*>(sp); sp += 4 * size_t(kTypeDirect);
+  BinLds bl;
+  int64_t* split_l = reinterpret_cast<int64_t*>(sp); sp += 8 * size_t(kBinMax);
+  bl.split = split_l;
+  bl.cnt = reinterpret_cast<uint32_t*>(sp); sp += 4 * size_t(kBinMax);
+  bl.base = reinterpret_cast<uint32_t*>(sp); sp += 4 * size_t(kBinMax);
   int32_t* cnt = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(lds_cap);
   uint8_t* dn = sp; sp += lds_cap;
   uint8_t* nr = sp;
@@ -1333,7 +1406,14 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
     it.speed[i] = a.itab.speed[i];
     it.pos[i] = a.itab.pos_of[i];
   }
-  for (int t = tid; t < kTypeDirect; t += blockDim.x) it.run[t] = a.itab.run[t];
+  for (int t = tid; t < kTypeDirect; t += blockDim.x) {
+    it.run[t] = a.itab.run[t];
+    it.prun[t] = a.itab.prun[t];
+  }
+  if (a.bk.bins) {  // the splitters; the counters start at zero
+    for (int i = tid; i < a.bk.nb - 1; i += T) split_l[i] = a.bk.split[i];
+    for (int i = tid; i < a.bk.nb; i += T) bl.cnt[i] = 0;
+  }
 
   const Layout L{a.node_of_pos, a.pos_of_node, a.p.N};
   Acc acc;
@@ -1346,9 +1426,9 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
     const int lvl = prio_level(a, w);
     lmask |= level_bit(lvl);
     if (!a.force_global && n <= lds_cap)
-      sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, lds_cap, b, n, dl, lvl, acc);
+      sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, lds_cap, b, n, dl, lvl, acc, bl);
     else
-      sweep_hbm<T, false, false>(a, L, it, S, int(w), b, n, dl, lvl, acc);
+      sweep_hbm<T, false, false>(a, L, it, S, int(w), b, n, dl, lvl, acc, split_l);
   }
 
   // fold the block's slack range and ready count into the control block
@@ -1468,6 +1548,7 @@ __device__ inline ITabLds carve_itab(unsigned char* sp, int M) {
   it.speed = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
   it.pos = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
   it.run = reinterpret_cast<uint32_t*>(sp);
+  it.prun = nullptr;  // the wave tables scan whole runs
   return it;
 }
 
@@ -1814,7 +1895,8 @@ __global__ __launch_bounds__(kWaveBlock) void k_sweep_wave(
         if (n <= 0 || (n <= wcap && !a.force_global)) continue;
         const int lvl = prio_level(a, w);
         lmask |= level_bit(lvl);
-        sweep_hbm<kWaveBlock, kFused, true>(a, L, it, S, int(w), b, n, a.p.deadline[w] - a.p.now, lvl, acc);
+        sweep_hbm<kWaveBlock, kFused, true>(a, L, it, S, int(w), b, n, a.p.deadline[w] - a.p.now, lvl, acc,
+                                            nullptr);
       }
     }
   }
@@ -1864,11 +1946,13 @@ SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t ld
   }
   s.threads = kBlockT;
   s.npt = kBlockNpt;
-  const size_t avail = lds_limit > kStaticLdsReserve + itab ? lds_limit - kStaticLdsReserve - itab : 0;
+  // and the undominated ends, the splitters and two bin counter arrays
+  const size_t itab_b = itab + 4 * kTypeDirect + 16 * size_t(kBinMax);
+  const size_t avail = lds_limit > kStaticLdsReserve + itab_b ? lds_limit - kStaticLdsReserve - itab_b : 0;
   int64_t cap = int64_t(avail / 14);
   if (cap > int64_t(kBlockT) * kBlockNpt) cap = int64_t(kBlockT) * kBlockNpt;
   s.lds_cap = int(cap);
-  s.lds_bytes = itab + 14 * size_t(cap) + 16;
+  s.lds_bytes = itab_b + 14 * size_t(cap) + 16;
   s.wave_path = 0;
   int64_t blocks = int64_t(device_cus) * 2;
   if (blocks > W) blocks = W;

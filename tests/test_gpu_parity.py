@@ -226,10 +226,11 @@ def test_sort_path_switching():
             check(pol, p, label)
 
 
-def test_large_ready_set_bucketed():
+def test_large_ready_set_bins():
     """About a million ready futures on one handle: the first pass uses the
-    tiled sort, later passes the bucketed sort whose workgroups find their base
-    from the published totals of earlier workgroups; every pass matches."""
+    tiled sort and leaves splitters, later passes the bin partition sort
+    (the block sweep claims one segment per workflow and bin); every pass
+    matches."""
     p = wl.wide_mapreduce()
     o = oracle.run(p)
     with nalar.Policy() as pol:
@@ -240,7 +241,7 @@ def test_large_ready_set_bucketed():
             names = [n for n, _ in pol.timing()]
             say(f"[gpu] pass {i}: {names}")
             if i > 0:
-                assert "sort_bucket" in names
+                assert "sort_bin" in names and "sort_pass0" not in names
 
 
 # ---------------------------------------------------------------- policy variants
@@ -890,3 +891,65 @@ def test_large_instance_tables(policy, n_inst, n_types, shuffle):
                       shuffle_ids=shuffle)
     for pol_bits in (0, nalar.NALAR_ROUTE_STATEFUL, nalar.NALAR_ROUTE_GREEDY):
         check(policy, p, f"instances={n_inst} types={n_types} shuffle={shuffle}", policy=pol_bits)
+
+
+# ------------------------------------------------------------ bin partition sort
+
+def _independent(W, n, seed, spread=True):
+    """W workflows of n independent futures (no dependencies, none done): all
+    ready, keys from seeded service times and deadlines."""
+    rng = np.random.default_rng(seed)
+    N = W * n
+    p = wl.random_dag(seed, n_nodes=4, n_workflows=1, n_instances=24, n_types=5)
+    types = rng.integers(0, 6, N).astype(np.int32)
+    M = p.n_instances
+    return wl.Problem(f"independent-{W}x{n}", p.now_us, 200_000, np.repeat(np.arange(W), n).astype(np.int32),
+                      types, rng.integers(1, 10**7, N).astype(np.int64), np.zeros(N, np.uint8),
+                      np.where(rng.random(N) < 0.5, rng.integers(0, M, N), -1).astype(np.int32),
+                      np.zeros(N + 1, np.int32), np.zeros(0, np.int32),
+                      (p.now_us + (rng.integers(2_000_000, 20_000_000, W) if spread else
+                                   np.full(W, 5_000_000))).astype(np.int64),
+                      rng.integers(0, 5, M).astype(np.int32), rng.integers(0, 2_000_000, M).astype(np.int64),
+                      rng.integers(500, 2001, M).astype(np.int32), wf_contiguous=True)
+
+
+def _sort_kind(pol):
+    names = [n for n, _ in pol.timing()]
+    return "bin" if "sort_bin" in names else ("bucket" if "sort_bucket" in names and "sort_pass0" not in names
+                                                else "tiled")
+
+
+def test_bin_sort_wide_mapreduce():
+    """Repeated passes over the wide map/reduce snapshot on one handle: the
+    first pass takes the tiled sort and leaves splitters, the later ones the
+    bin partition sort; then a policy switch (other keys, overflowing bins,
+    fallback) and back."""
+    p = wl.wide_mapreduce()
+    ref = {b: oracle.run(p, policy=b) for b in (0, nalar.NALAR_ORDER_SRTF, nalar.NALAR_ORDER_LPT)}
+    kinds = []
+    with nalar.Policy() as pol:
+        pol.set_timing(True)
+        for i, bits in enumerate([0, 0, 0, nalar.NALAR_ORDER_SRTF, nalar.NALAR_ORDER_SRTF,
+                                  nalar.NALAR_ORDER_LPT, 0, 0]):
+            say(f"[gpu] wide map/reduce bins pass {i} policy {bits}")
+            assert_parity(gpu_run(pol, p, policy=bits), ref[bits], f"bins pass {i}")
+            kinds.append(_sort_kind(pol))
+    say(f"[gpu] sort kinds {kinds}")
+    assert kinds[0] == "tiled" and kinds.count("bin") >= 4, kinds
+
+
+def test_bin_sort_fallback_and_paths():
+    """Bins on the LDS block sweep (1,024-future workflows) and on its HBM
+    sweep (8,192-future workflows); a snapshot whose keys all lie past the
+    last splitter (every future in one bin: overflow, tiled fallback), then
+    equal keys everywhere."""
+    lds = _independent(256, 1024, 31)
+    hbm = _independent(16, 8192, 32)
+    far = lds.copy(deadline_us=lds.deadline_us + (1 << 50))
+    flat = _independent(256, 1024, 33, spread=False).copy(est_us=np.full(256 * 1024, 12345, np.int64))
+    with nalar.Policy() as pol:
+        pol.set_timing(True)
+        for i, q in enumerate([lds, lds, lds, far, far, far, lds, hbm, hbm, hbm, flat, flat, flat, lds]):
+            say(f"[gpu] bins case {i}: {q.name}")
+            check(pol, q, f"bins case {i}")
+            say(f"[gpu]   sort {_sort_kind(pol)}")
