@@ -319,7 +319,8 @@ BucketArgs plan_buckets(const nalar_policy* h, int64_t N, bool levels, bool wave
 BucketArgs plan_bins(const nalar_policy* h, const SweepShape& sh, bool levels) {
   BucketArgs bk{};
   if ((h->flags & NALAR_FORCE_TILED_SORT) || sh.wave_path || levels || h->split_nb <= 0 ||
-      !h->hint_valid || h->hint_ready < kBinMinReady || h->bin_skip > 0)
+      !h->hint_valid || h->hint_ready < kBinMinReady || h->bin_skip > 0 ||
+      (h->split_nb & (h->split_nb - 1)) != 0)  // bins_for gives powers of two
     return bk;
   bk.bins = 1;
   bk.nb = h->split_nb;

@@ -103,7 +103,7 @@ constexpr uint32_t kStatusTiled = 0x20000000u;
 // the outputs at the bin's offset.
 constexpr int64_t kBinMinReady = 65536;   // smaller ready sets keep the buckets
 constexpr int kBinTarget = 1024;          // futures per bin on average
-constexpr int kBinCap = 2560;             // records per bin (LDS of k_bin_sort)
+constexpr int kBinCap = 2048;             // records per bin (LDS of k_bin_sort)
 constexpr int kBinMin = 64;               // bins: a power of two in [kBinMin, kBinMax]
 constexpr int kBinMax = 2048;
 // bins for a ready count (the same rule on the host and on the device)
@@ -123,6 +123,9 @@ struct BucketSlot {
   int32_t pos;
   int32_t route;    // slot_pack(route, priority level)
 };
+static_assert(sizeof(BucketSlot) == 24 && offsetof(BucketSlot, cost) == 8 && offsetof(BucketSlot, pos) == 16 &&
+                  offsetof(BucketSlot, route) == 20,
+              "the sweep writes a slot as three 8-byte words");
 
 // A slot's route field holds the route (-1 .. 1023) in its low 16 bits and
 // the future's priority level above them, so that a bucket holding futures of

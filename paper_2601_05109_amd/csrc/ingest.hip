@@ -17,108 +17,220 @@ constexpr int kNodeItems = 4;
 // ascending index, then the dominated ones (see route_future); prun marks the
 // end of the first part.  Types with more than kPruneRun instances are not
 // pruned (their run is in ascending index and prun is its end).
+//
+// With every type below kTypeDirect (the usual case) the (type, index) order
+// is a counting sort: inside each group of 64 instances, ballots over the type
+// bits find the lanes of equal type and the rank among them; per-group type
+// counts, summed over earlier groups and earlier types, give the run starts.
+// Otherwise each instance counts the entries before it (O(M^2), any types).
+// The dominance checks then run per sorted position, so the lanes of one run
+// read the same LDS entries.
 constexpr int kPruneRun = 128;
+constexpr int kTabGroups = NALAR_MAX_INSTANCES / kWave;
 
-__device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl) {
-  const int64_t M = p.M;
+struct TabLds {
+  int32_t* type;    // by index
+  int32_t* sorted;  // by (type, index) position: the index
+  int64_t* sload;   // by position
+  int32_t* sspeed;  // by position
+  uint32_t* rng;    // by position: its run, lo | hi << 16
+  uint8_t* sdom;    // by position: dominated inside its run
+  uint32_t* wh;     // [groups][kTypeDirect]: per group type counts, then offsets
+};
+
+size_t tab_lds_bytes(int64_t M) {
+  const size_t m4 = size_t((M + 3) & ~int64_t(3));
+  const size_t groups = size_t((M + kWave - 1) / kWave);
+  return 8 * m4 + 4 * m4 * 4 + ((m4 + 15) & ~size_t(15)) + 4 * groups * kTypeDirect;
+}
+
+__device__ inline TabLds carve_tab(unsigned char* sp, int64_t M) {
+  const size_t m4 = size_t((M + 3) & ~int64_t(3));
+  TabLds t;
+  t.sload = reinterpret_cast<int64_t*>(sp); sp += 8 * m4;
+  t.type = reinterpret_cast<int32_t*>(sp); sp += 4 * m4;
+  t.sorted = reinterpret_cast<int32_t*>(sp); sp += 4 * m4;
+  t.sspeed = reinterpret_cast<int32_t*>(sp); sp += 4 * m4;
+  t.rng = reinterpret_cast<uint32_t*>(sp); sp += 4 * m4;
+  t.sdom = sp; sp += (m4 + 15) & ~size_t(15);
+  t.wh = reinterpret_cast<uint32_t*>(sp);
+  return t;
+}
+
+__device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl, unsigned char* smem) {
+  const int M = int(p.M);
+  const int tid = threadIdx.x;
   reset_ctrl(next_ctrl);  // unused by this pass; ready for the next one
-  __shared__ __align__(16) int32_t s_type[NALAR_MAX_INSTANCES];
-  __shared__ int64_t s_load[NALAR_MAX_INSTANCES];
-  __shared__ int32_t s_speed[NALAR_MAX_INSTANCES];
-  __shared__ int32_t s_sorted[NALAR_MAX_INSTANCES];  // position by (type, index) -> index
-  __shared__ uint8_t s_dom[NALAR_MAX_INSTANCES];     // by index: dominated in its type
-  const int M4 = int((M + 3) & ~int64_t(3));
-  // padding past M compares as neither below nor equal to any entry's rank
-  for (int i = threadIdx.x; i < M4; i += kNodeThreads) {
-    s_type[i] = i < M ? p.inst_type[i] : INT32_MAX;
-    if (i < M) {
-      s_load[i] = p.inst_load[i];
-      s_speed[i] = p.inst_speed[i];
-    }
-  }
-  __syncthreads();
-  const int4* s_type4 = reinterpret_cast<const int4*>(s_type);
-  // pass 1: rank by (type, index), the type's first position and its size
+  __shared__ uint32_t s_run[kTypeDirect], s_prun[kTypeDirect], s_tstart[kTypeDirect];
+  const TabLds S = carve_tab(smem, M);
+  const int M4 = (M + 3) & ~3;
+  const int groups = (M + kWave - 1) / kWave;
   constexpr int kPer = (NALAR_MAX_INSTANCES + kNodeThreads - 1) / kNodeThreads;
-  int below[kPer], same[kPer];
+  // padding past M compares as neither below nor equal to any entry's rank
+  bool general = false;
+  int32_t ty[kPer];
+  int64_t ld[kPer];
+  int32_t sp[kPer];
+#pragma unroll
   for (int u = 0; u < kPer; ++u) {
-    const int i = threadIdx.x + u * kNodeThreads;
-    below[u] = 0;
-    same[u] = 0;
-    if (i >= M) continue;
-    const int32_t t = s_type[i];
-    // four entries per LDS read, unrolled so that the reads overlap
-    int bl = 0, sm = 0, before = 0;
-#pragma unroll 4
-    for (int q = 0; q < M4 / 4; ++q) {
-      const int4 v = s_type4[q];
-      const int j = 4 * q;
-      bl += (v.x < t) + (v.y < t) + (v.z < t) + (v.w < t);
-      sm += (v.x == t) + (v.y == t) + (v.z == t) + (v.w == t);
-      before += ((v.x == t) & (j < i)) + ((v.y == t) & (j + 1 < i)) + ((v.z == t) & (j + 2 < i)) +
-                ((v.w == t) & (j + 3 < i));
+    const int i = tid + u * kNodeThreads;
+    ty[u] = INT32_MAX;
+    ld[u] = 0;
+    sp[u] = 0;
+    if (i < M) {
+      ty[u] = p.inst_type[i];
+      ld[u] = p.inst_load[i];
+      sp[u] = p.inst_speed[i];
+      general |= uint32_t(ty[u]) >= uint32_t(kTypeDirect);
     }
-    below[u] = bl;
-    same[u] = sm;
-    s_sorted[bl + before] = i;
+    if (i < M4) S.type[i] = ty[u];
+  }
+  for (int t = tid; t < kTypeDirect; t += kNodeThreads) {
+    s_run[t] = 0;  // types without an instance keep an empty run
+    s_prun[t] = 0;
+  }
+  for (int q = tid; q < groups * kTypeDirect; q += kNodeThreads) S.wh[q] = 0;
+  general = __syncthreads_or(general ? 1 : 0) != 0;
+
+  int at[kPer], lo[kPer], hi[kPer];
+  if (!general) {
+    // rank among the equal types of the group, and each group's type counts
+    uint32_t below[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int i = tid + u * kNodeThreads;
+      below[u] = 0;
+      if (u * kNodeThreads >= M) continue;  // the same on every lane
+      const bool in = i < M;
+      uint64_t peers = ballot(in);
+#pragma unroll
+      for (int bit = 0; bit < 6; ++bit) {
+        static_assert(kTypeDirect == 64, "six type bits");
+        const bool on = (ty[u] >> bit) & 1;
+        const uint64_t m = ballot(on);
+        peers &= on ? m : ~m;
+      }
+      below[u] = uint32_t(__popcll(peers & lanemask_lt()));
+      if (in && below[u] == 0) S.wh[(i / kWave) * kTypeDirect + ty[u]] = uint32_t(__popcll(peers));
+    }
+    __syncthreads();
+    // per type: offsets of the groups, then the run starts (one wave)
+    if (tid < kTypeDirect) {
+      uint32_t tot = 0;
+      for (int g = 0; g < groups; ++g) {
+        const uint32_t c = S.wh[g * kTypeDirect + tid];
+        S.wh[g * kTypeDirect + tid] = tot;
+        tot += c;
+      }
+      const uint32_t inc = wave_incl_scan_u32(tot);
+      s_tstart[tid] = inc - tot;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int i = tid + u * kNodeThreads;
+      at[u] = lo[u] = hi[u] = 0;
+      if (i >= M) continue;
+      lo[u] = int(s_tstart[ty[u]]);
+      hi[u] = ty[u] + 1 < kTypeDirect ? int(s_tstart[ty[u] + 1]) : M;
+      at[u] = lo[u] + int(S.wh[(i / kWave) * kTypeDirect + ty[u]] + below[u]);
+    }
+  } else {
+    const int4* type4 = reinterpret_cast<const int4*>(S.type);
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int i = tid + u * kNodeThreads;
+      at[u] = lo[u] = hi[u] = 0;
+      if (i >= M) continue;
+      const int32_t t = ty[u];
+      int bl = 0, sm = 0, before = 0;
+#pragma unroll 4
+      for (int q = 0; q < M4 / 4; ++q) {
+        const int4 v = type4[q];
+        const int j = 4 * q;
+        bl += (v.x < t) + (v.y < t) + (v.z < t) + (v.w < t);
+        sm += (v.x == t) + (v.y == t) + (v.z == t) + (v.w == t);
+        before += ((v.x == t) & (j < i)) + ((v.y == t) & (j + 1 < i)) + ((v.z == t) & (j + 2 < i)) +
+                  ((v.w == t) & (j + 3 < i));
+      }
+      lo[u] = bl;
+      hi[u] = bl + sm;
+      at[u] = bl + before;
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int i = tid + u * kNodeThreads;
+    if (i >= M) continue;
+    S.sorted[at[u]] = i;
+    S.sload[at[u]] = ld[u];
+    S.sspeed[at[u]] = sp[u];
+    S.rng[at[u]] = uint32_t(lo[u]) | (uint32_t(hi[u]) << 16);
   }
   __syncthreads();
-  // pass 2: dominated instances of small runs
+  // dominated instances of small runs, per sorted position r (j < i is q < r)
+#pragma unroll
   for (int u = 0; u < kPer; ++u) {
-    const int i = threadIdx.x + u * kNodeThreads;
-    if (i >= M) continue;
+    const int r = tid + u * kNodeThreads;
+    if (r >= M) continue;
+    const uint32_t rg = S.rng[r];
+    const int a = int(rg & 0xFFFFu), e = int(rg >> 16);
     bool dom = false;
-    if (same[u] <= kPruneRun) {
-      const int64_t li = s_load[i];
-      const int32_t si = s_speed[i];
-      for (int r = below[u]; r < below[u] + same[u]; ++r) {
-        const int j = s_sorted[r];
-        const int64_t lj = s_load[j];
-        const int32_t sj = s_speed[j];
-        dom |= sj >= si && (lj < li || (lj == li && j < i));
+    if (e - a <= kPruneRun) {
+      const int64_t li = S.sload[r];
+      const int32_t si = S.sspeed[r];
+      // eight entries per step, their LDS reads in flight together (a step
+      // past the run rereads its first entry and ignores it)
+      for (int q0 = a; q0 < e; q0 += 8) {
+#pragma unroll
+        for (int d = 0; d < 8; ++d) {
+          const int q = q0 + d < e ? q0 + d : a;
+          const int64_t lj = S.sload[q];
+          dom |= (q0 + d < e) & (S.sspeed[q] >= si) & ((lj < li) | ((lj == li) & (q < r)));
+        }
       }
     }
-    s_dom[i] = dom ? 1 : 0;
+    S.sdom[r] = dom ? 1 : 0;
   }
   __syncthreads();
-  // pass 3: undominated first, each part in ascending index
+  // undominated first, each part in ascending index
+#pragma unroll
   for (int u = 0; u < kPer; ++u) {
-    const int i = threadIdx.x + u * kNodeThreads;
-    if (i >= M) continue;
-    const int32_t t = s_type[i];
-    const bool dom = s_dom[i] != 0;
+    const int r = tid + u * kNodeThreads;
+    if (r >= M) continue;
+    const uint32_t rg = S.rng[r];
+    const int a = int(rg & 0xFFFFu), e = int(rg >> 16);
+    const int dom = S.sdom[r];
     int und = 0, rank = 0;
-    for (int r = below[u]; r < below[u] + same[u]; ++r) {
-      const int j = s_sorted[r];
-      const bool dj = s_dom[j] != 0;
-      und += dj ? 0 : 1;
-      rank += (dj == dom && j < i) ? 1 : 0;
+    for (int q0 = a; q0 < e; q0 += 8) {
+#pragma unroll
+      for (int d = 0; d < 8; ++d) {
+        const int q = q0 + d < e ? q0 + d : a;
+        const int in = q0 + d < e ? 1 : 0;
+        const int dq = S.sdom[q];
+        und += in & (1 - dq);
+        rank += in & (dq == dom) & (q < r);
+      }
     }
-    const int pos = below[u] + (dom ? und + rank : rank);
-    const int32_t sp = s_speed[i];
+    const int pos = a + (dom ? und + rank : rank);
+    const int32_t i = S.sorted[r];
+    const int32_t t = S.type[i];
+    const int32_t spd = S.sspeed[r];
     it.type[pos] = t;
     it.idx[pos] = i;
-    it.load[pos] = s_load[i];
-    it.speed[pos] = sp;
-    it.inv_speed[pos] = sp >= 1 ? 1.0 / double(sp) : 0.0;
+    it.load[pos] = S.sload[r];
+    it.speed[pos] = spd;
+    it.inv_speed[pos] = spd >= 1 ? 1.0 / double(spd) : 0.0;
     it.pos_of[i] = pos;
-    // the run of a small type, written by the type's lowest index
-    if (t >= 0 && t < kTypeDirect && s_sorted[below[u]] == i) {
-      it.run[t] = uint32_t(below[u]) | (uint32_t(below[u] + same[u]) << 16);
-      it.prun[t] = uint32_t(below[u] + und);
+    if (t >= 0 && t < kTypeDirect && r == a) {  // the run of a small type
+      s_run[t] = uint32_t(a) | (uint32_t(e) << 16);
+      s_prun[t] = uint32_t(a + und);
     }
   }
-  // types without an instance
-  for (int t = threadIdx.x; t < kTypeDirect; t += kNodeThreads) {
-    bool present = false;
-    for (int q = 0; q < M4 / 4 && !present; ++q) {
-      const int4 v = s_type4[q];
-      present = v.x == t || v.y == t || v.z == t || v.w == t;
-    }
-    if (!present) {
-      it.run[t] = 0;
-      it.prun[t] = 0;
-    }
+  __syncthreads();
+  for (int t = tid; t < kTypeDirect; t += kNodeThreads) {
+    it.run[t] = s_run[t];
+    it.prun[t] = s_prun[t];
   }
 }
 
@@ -130,7 +242,8 @@ __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl
                                                        ITab it, int32_t* wf_off, int contiguous) {
   const int64_t N = p.N, W = p.W, M = p.M;
   if (blockIdx.x == 0) {
-    instance_table(p, it, next_ctrl);
+    extern __shared__ __align__(16) unsigned char smem[];
+    instance_table(p, it, next_ctrl, smem);
     return;
   }
   const int64_t stride = int64_t(gridDim.x - 1) * kNodeThreads;
@@ -200,7 +313,7 @@ hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* ne
                         int32_t* wf_off, int contiguous) {
   const int64_t nv = (p.N + kNodeItems - 1) / kNodeItems;
   int64_t n = nv > p.W + 1 ? nv : p.W + 1;
-  hipLaunchKernelGGL(k_nodes, dim3(grid_for(n, kNodeThreads, 4096) + 1), dim3(kNodeThreads), 0, s, p,
+  hipLaunchKernelGGL(k_nodes, dim3(grid_for(n, kNodeThreads, 4096) + 1), dim3(kNodeThreads), tab_lds_bytes(p.M), s, p,
                      ctrl, next_ctrl, itab, wf_off, contiguous);
   return hipGetLastError();
 }

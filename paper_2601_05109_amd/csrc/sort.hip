@@ -684,41 +684,116 @@ __device__ inline int64_t output_key(const SortArgs& a, int64_t g) {
 }
 
 // One workgroup per bin: its records (claimed by the sweep in any order) are
-// sorted in LDS by (key, position) with a stable LSD radix sort: 8-bit digits
-// of the position (relative to the bin's lowest) first, then of the key
-// (relative to the bin's lowest key), so that the last passes order by key
-// and equal keys keep their position order; only as many digits as the
-// bin's ranges need.  Each pass ranks its items as the tiled sort's digit
-// passes do (wave w owns a contiguous run of items, lanes of equal digit found
-// by ballots, per-wave digit counts in LDS) and scatters them to the other
-// buffer.  The sorted bin is written at its offset (the records of all lower
-// bins).  Keys are unique with their positions, so this is the (key, wf, id)
-// order.  The workgroups also write the next pass's splitters (this pass's key
-// quantiles: the key at rank (q + 1) * R / nb' for nb' = bins_for(R)), each
-// those that fall into its bin, and workgroup 0 publishes the status.
+// put in (key, position) order, which is the (key, wf, id) order since
+// positions follow (wf, id), by a counting sort over kBinSub sub-buckets of
+// the bin's key range (the top bits of key minus the bin's lowest key; the
+// lowest and highest bins, whose keys may trail off away from their one
+// splitter, count again on a log-linear scale of the distance from that
+// splitter, 16 sub-buckets per octave, if the first count crowds): one
+// LDS counter per sub-bucket, their exclusive scan, and a scatter of (key,
+// position) to LDS; a future's rank is then its sub-bucket's start plus the
+// number of sub-bucket mates of smaller (key, position).  Sub-buckets hold
+// about one future each, since the bins are cut at quantiles; one holding
+// more than kBinRun (many equal keys, or a bin whose keys crowd at one end of
+// its range, as the lowest and highest bins' tails do) is sorted in place by
+// the whole workgroup with a bitonic network whose comparators all put the
+// smaller entry first, so that the missing entries of the padded size never
+// move (comparators reaching past the segment are skipped).  The futures are
+// then in LDS by rank, and the sorted bin is written at its offset (the
+// records of all lower bins) with consecutive lanes on consecutive ranks.  The workgroups also write the next pass's
+// splitters (this pass's key quantiles: the key at rank (q + 1) * R / nb' for
+// nb' = bins_for(R)): the future of that rank writes it.  Workgroup 0
+// publishes the status.
 constexpr int kBinWaves = kBinThreads / kWave;
 constexpr int kBinJ = (kBinCap + kBinThreads - 1) / kBinThreads;  // items per lane
+constexpr int kBinSub = 1024;
+constexpr int kBinSubLog = 10;
+static_assert(kBinSub == 1 << kBinSubLog && kBinSub % kBinThreads == 0, "sub-buckets");
 
-struct BinSmem {
-  int64_t key[2][kBinCap];
-  int32_t pos[2][kBinCap];
-  uint16_t idx[2][kBinCap];
-  uint32_t whist[kBinWaves][kRadixBuckets];
-  uint32_t dstart[kRadixBuckets];
+constexpr int kBinRun = 32;
+constexpr int kBinCrowdMax = kBinCap / (kBinRun + 1) + 1;  // crowded sub-buckets a bin can hold
+
+struct BinFixed {
+  uint32_t sub[kBinSub];  // sub-bucket counts, then starts
+  uint32_t crowd[kBinCrowdMax];  // crowded sub-buckets: start | end << 16
+  int ncrowd;
   uint32_t tmp[kBinWaves];
   int64_t range[kRangeWords];
   int64_t red[4][kBinWaves];
 };
 
-__device__ inline uint32_t bin_digit(int64_t key, int32_t pos, int pass, int ppass, int64_t kmin,
-                                     int32_t pmin) {
-  return pass < ppass ? (uint32_t(pos - pmin) >> (8 * pass)) & 0xFFu
-                      : uint32_t((uint64_t(key) - uint64_t(kmin)) >> (8 * (pass - ppass))) & 0xFFu;
+__host__ __device__ constexpr size_t bin_align(size_t b) { return (b + 15) & ~size_t(15); }
+
+__host__ __device__ constexpr size_t bin_lds_bytes(int cap) {
+  return bin_align(8 * size_t(cap)) + bin_align(4 * size_t(cap)) + bin_align(2 * size_t(cap)) + sizeof(BinFixed);
+}
+
+// Sub-bucket of a key: mode 0, (key - base) >> sshift (base the bin's lowest
+// key); mode 1 (lowest bin, base = its splitter - 1 >= key) and mode 2
+// (highest bin, base = its splitter <= key) a log-linear scale of the
+// distance d from base (d below 16 as it is, else 16 steps per octave),
+// reversed in mode 1 so that sub-buckets ascend with the key.
+__device__ inline uint32_t bin_sub(int64_t key, int mode, int64_t base, int sshift) {
+  if (mode == 0) return uint32_t((uint64_t(key) - uint64_t(base)) >> sshift);
+  const uint64_t d = mode == 1 ? uint64_t(base) - uint64_t(key) : uint64_t(key) - uint64_t(base);
+  uint32_t f = uint32_t(d);
+  if (d >= 16) {
+    const int e = 63 - __builtin_clzll(d);  // 4 .. 63, so f < 976
+    f = uint32_t(e - 3) * 16u + uint32_t((d >> (e - 4)) & 15u);
+  }
+  return mode == 1 ? uint32_t(kBinSub - 1) - f : f;
+}
+
+// Entries x < y of an LDS segment: (key, position) ascending, the record
+// index moving along.
+__device__ inline void bin_cmpx(int64_t* k, int32_t* p, uint16_t* r, int x, int y) {
+  const int64_t kx = k[x], ky = k[y];
+  const int32_t px = p[x], py = p[y];
+  if (ky < kx || (ky == kx && py < px)) {
+    k[x] = ky;
+    k[y] = kx;
+    p[x] = py;
+    p[y] = px;
+    const uint16_t rx = r[x];
+    r[x] = r[y];
+    r[y] = rx;
+  }
+}
+
+// Sorts the segment [0, L) of the three LDS arrays in place (every thread of
+// the workgroup takes part): sizes 2, 4, ..., P (P the power of two >= L),
+// each a mirror step (entry i of a block against the block's entry k - 1 - i)
+// and then half-cleaners at distances k/4 ... 1.
+__device__ void bin_bitonic(int64_t* k, int32_t* p, uint16_t* r, int L) {
+  int lp = 0;
+  while ((1 << lp) < L) ++lp;
+  const int P = 1 << lp;
+  for (int ls = 1; ls <= lp; ++ls) {  // size 2^ls, half 2^(ls - 1)
+    const int lh = ls - 1;
+    for (int c = threadIdx.x; c < P / 2; c += kBinThreads) {
+      const int base = (c >> lh) << ls, off = c & ((1 << lh) - 1);
+      const int x = base + off, y = base + (1 << ls) - 1 - off;
+      if (y < L) bin_cmpx(k, p, r, x, y);
+    }
+    __syncthreads();
+    for (int ld = lh - 1; ld >= 0; --ld) {  // distance 2^ld
+      for (int c = threadIdx.x; c < P / 2; c += kBinThreads) {
+        const int x = ((c >> ld) << (ld + 1)) + (c & ((1 << ld) - 1)), y = x + (1 << ld);
+        if (y < L) bin_cmpx(k, p, r, x, y);
+      }
+      __syncthreads();
+    }
+  }
 }
 
 __global__ __launch_bounds__(kBinThreads) void k_bin_sort(SortArgs a, BucketArgs bk) {
   extern __shared__ __align__(16) unsigned char smem[];
-  BinSmem& S = *reinterpret_cast<BinSmem*>(smem);
+  const int cap = bk.cap;
+  int64_t* s_key = reinterpret_cast<int64_t*>(smem);
+  int32_t* s_pos = reinterpret_cast<int32_t*>(smem + bin_align(8 * size_t(cap)));
+  uint16_t* s_rec = reinterpret_cast<uint16_t*>(smem + bin_align(8 * size_t(cap)) + bin_align(4 * size_t(cap)));
+  BinFixed* F = reinterpret_cast<BinFixed*>(smem + bin_align(8 * size_t(cap)) + bin_align(4 * size_t(cap)) +
+                                            bin_align(2 * size_t(cap)));
   const int tid = threadIdx.x;
   const int wv = tid / kWave;
   const int ln = lane_id();
@@ -728,11 +803,10 @@ __global__ __launch_bounds__(kBinThreads) void k_bin_sort(SortArgs a, BucketArgs
   const uint32_t overflow = ctrl->bucket_overflow;
   RangeLanes rl;
   if (b == 0) rl = load_range_lanes(ctrl, a.levels != 0);
-  const uint32_t cap = uint32_t(bk.cap);
   uint32_t before = 0, total = 0;
   for (int i = tid; i < bk.nb; i += kBinThreads) {
     uint32_t c = bk.cnt[i];
-    c = c < cap ? c : cap;
+    c = c < uint32_t(cap) ? c : uint32_t(cap);
     total += c;
     before += i < b ? c : 0u;
   }
@@ -741,159 +815,172 @@ __global__ __launch_bounds__(kBinThreads) void k_bin_sort(SortArgs a, BucketArgs
     return;
   }
   if (b == 0) {
-    settle_range(rl, ctrl, S.range, true, a.levels != 0);
-    if (tid == 0) publish_range(a.host, overflow ? kStatusTiled : 0u, S.range);
+    settle_range(rl, ctrl, F->range, true, a.levels != 0);
+    if (tid == 0) publish_range(a.host, overflow ? kStatusTiled : 0u, F->range);
   }
   if (overflow) return;
-  uint32_t n = bk.cnt[b];
-  n = n < cap ? n : cap;
+  const uint32_t nraw = bk.cnt[b];
+  const int n = int(nraw < uint32_t(cap) ? nraw : uint32_t(cap));
   const BucketSlot* rec = bk.slot + int64_t(b) * cap;
-  // wave w owns items [w * C, (w + 1) * C), item j of lane l at w * C + j * 64 + l
-  const int J = int((n + kBinThreads - 1) / kBinThreads);
+  // item j of lane l of wave w: record w * C + j * 64 + l
+  const int J = (n + kBinThreads - 1) / kBinThreads;
   const int C = J * kWave;
   int64_t key[kBinJ];
   int32_t pos[kBinJ];
-  uint16_t idx[kBinJ];
   int64_t kmin = INT64_MAX, kmax = INT64_MIN;
-  int32_t pmin = INT32_MAX, pmax = INT32_MIN;
 #pragma unroll
   for (int j = 0; j < kBinJ; ++j) {
     const int i = wv * C + j * kWave + ln;
     key[j] = 0;
     pos[j] = 0;
-    idx[j] = 0;
-    if (j < J && i < int(n)) {
+    if (j < J && i < n) {
       key[j] = rec[i].key;
       pos[j] = rec[i].pos;
-      idx[j] = uint16_t(i);
       kmin = key[j] < kmin ? key[j] : kmin;
       kmax = key[j] > kmax ? key[j] : kmax;
-      pmin = pos[j] < pmin ? pos[j] : pmin;
-      pmax = pos[j] > pmax ? pos[j] : pmax;
     }
   }
-  // block sums: records before this bin and in total; the bin's ranges
+  // for (for the sub-bucket counters) and block sums: records before this
+  // bin and in total, and the bin's key range
+  for (int i = tid; i < kBinSub; i += kBinThreads) F->sub[i] = 0;
   {
     const int64_t s0 = wave_sum_i64(int64_t(before)), s1 = wave_sum_i64(int64_t(total));
     const int64_t m0 = wave_min_i64(kmin), m1 = wave_max_i64(kmax);
-    const int64_t q0 = wave_min_i64(pmin), q1 = wave_max_i64(pmax);
     if (ln == 0) {
-      S.red[0][wv] = s0;
-      S.red[1][wv] = s1;
-      S.red[2][wv] = m0;
-      S.red[3][wv] = m1;
-      S.key[0][wv] = q0;  // scratch for the position range, overwritten below
-      S.key[1][wv] = q1;
+      F->red[0][wv] = s0;
+      F->red[1][wv] = s1;
+      F->red[2][wv] = m0;
+      F->red[3][wv] = m1;
     }
     __syncthreads();
     before = 0;
     total = 0;
     kmin = INT64_MAX;
     kmax = INT64_MIN;
-    int64_t pm0 = INT64_MAX, pm1 = INT64_MIN;
     for (int w = 0; w < kBinWaves; ++w) {
-      before += uint32_t(S.red[0][w]);
-      total += uint32_t(S.red[1][w]);
-      kmin = S.red[2][w] < kmin ? S.red[2][w] : kmin;
-      kmax = S.red[3][w] > kmax ? S.red[3][w] : kmax;
-      pm0 = S.key[0][w] < pm0 ? S.key[0][w] : pm0;
-      pm1 = S.key[1][w] > pm1 ? S.key[1][w] : pm1;
+      before += uint32_t(F->red[0][w]);
+      total += uint32_t(F->red[1][w]);
+      kmin = F->red[2][w] < kmin ? F->red[2][w] : kmin;
+      kmax = F->red[3][w] > kmax ? F->red[3][w] : kmax;
     }
-    pmin = int32_t(pm0);
-    pmax = int32_t(pm1);
-    __syncthreads();
   }
   const int64_t R = total;
-  int ppass = 0, kpass = 0;
-  if (n > 1) {
-    const uint32_t pr = uint32_t(pmax - pmin);
-    const uint64_t kr = uint64_t(kmax) - uint64_t(kmin);
-    ppass = pr ? (32 - __builtin_clz(pr) + 7) / 8 : 0;
-    kpass = kr ? (64 - __builtin_clzll(kr) + 7) / 8 : 0;
+  const uint64_t kr = n > 0 ? uint64_t(kmax) - uint64_t(kmin) : 0;
+  // sub-bucket scale: linear over [kmin, kmax], or log-linear from the one
+  // splitter of the lowest or highest bin (below)
+  const int kbits = kr ? 64 - __builtin_clzll(kr) : 0;
+  const int sshift = kbits > kBinSubLog ? kbits - kBinSubLog : 0;
+  int smode = 0;
+  int64_t sbase = kmin;
+  uint32_t at[kBinJ];  // slot inside the sub-bucket, then the rank in the bin
+  for (;;) {
+#pragma unroll
+    for (int j = 0; j < kBinJ; ++j) {
+      at[j] = 0;
+      if (j < J && wv * C + j * kWave + ln < n)
+        at[j] = atomicAdd(&F->sub[bin_sub(key[j], smode, sbase, sshift)], 1u);
+    }
+    __syncthreads();
+    if (smode != 0 || (b != 0 && b != bk.nb - 1)) break;
+    // the lowest or highest bin with a crowded sub-bucket counts again on
+    // the log-linear scale
+    bool crowded = false;
+    for (int i = tid; i < kBinSub; i += kBinThreads) crowded |= F->sub[i] > uint32_t(kBinRun);
+    if (!__syncthreads_or(crowded ? 1 : 0)) break;
+    smode = b == 0 ? 1 : 2;
+    sbase = b == 0 ? bk.split[0] - 1 : bk.split[bk.nb - 2];
+    for (int i = tid; i < kBinSub; i += kBinThreads) F->sub[i] = 0;
+    __syncthreads();
   }
-  const int npass = ppass + kpass;
-  int cur = 0;
-  for (int pass = 0; pass < npass; ++pass) {
-    for (int i = tid; i < kBinWaves * kRadixBuckets; i += kBinThreads) (&S.whist[0][0])[i] = 0;
-    __syncthreads();
-    uint32_t rank[kBinJ];
-    uint32_t* wh = S.whist[wv];
+  {
+    constexpr int kPerT = kBinSub / kBinThreads;
+    uint32_t c[kPerT], sum = 0;
 #pragma unroll
-    for (int j = 0; j < kBinJ; ++j) {
-      rank[j] = 0;
-      if (j >= J) continue;  // the same on every lane
-      const bool valid = wv * C + j * kWave + ln < int(n);
-      const uint32_t dg = bin_digit(key[j], pos[j], pass, ppass, kmin, pmin);
-      uint64_t peers = ballot(valid);
-#pragma unroll
-      for (int bit = 0; bit < kRadixBits; ++bit) {
-        const bool on = (dg >> bit) & 1u;
-        const uint64_t m = ballot(on);
-        peers &= on ? m : ~m;
-      }
-      const uint64_t below = peers & lanemask_lt();
-      uint32_t c = 0;
-      if (valid) c = wh[dg];
-      rank[j] = c + uint32_t(__popcll(below));
-      if (valid && below == 0) wh[dg] = c + uint32_t(__popcll(peers));
+    for (int u = 0; u < kPerT; ++u) {
+      c[u] = F->sub[tid * kPerT + u];
+      sum += c[u];
     }
-    __syncthreads();
-    // digit totals; per-wave counts become exclusive offsets inside the digit
-    uint32_t tot = 0;
-    if (tid < kRadixBuckets) {
-      for (int w = 0; w < kBinWaves; ++w) {
-        const uint32_t c = S.whist[w][tid];
-        S.whist[w][tid] = tot;
-        tot += c;
-      }
-    }
-    const uint32_t excl = block_excl_scan(tid < kRadixBuckets ? tot : 0u, S.tmp);
-    if (tid < kRadixBuckets) S.dstart[tid] = excl;
-    __syncthreads();
-    const int nxt = cur ^ 1;
+    uint32_t run = block_excl_scan(sum, F->tmp);  // every count is read before its barrier
 #pragma unroll
-    for (int j = 0; j < kBinJ; ++j) {
-      if (j >= J || wv * C + j * kWave + ln >= int(n)) continue;
-      const uint32_t dg = bin_digit(key[j], pos[j], pass, ppass, kmin, pmin);
-      const uint32_t o = S.dstart[dg] + S.whist[wv][dg] + rank[j];
-      S.key[nxt][o] = key[j];
-      S.pos[nxt][o] = pos[j];
-      S.idx[nxt][o] = idx[j];
-    }
-    __syncthreads();
-    cur = nxt;
-    // the next pass reads its items back in the same (wave, item, lane) order
-#pragma unroll
-    for (int j = 0; j < kBinJ; ++j) {
-      const int i = wv * C + j * kWave + ln;
-      if (j < J && i < int(n)) {
-        key[j] = S.key[cur][i];
-        pos[j] = S.pos[cur][i];
-        idx[j] = S.idx[cur][i];
-      }
+    for (int u = 0; u < kPerT; ++u) {
+      F->sub[tid * kPerT + u] = run;
+      run += c[u];
     }
   }
-  // write the sorted bin: rank r holds (key[j], pos[j]) of item i = r
+  __syncthreads();
+  uint32_t span[kBinJ];  // the sub-bucket's [start, end) as start | end << 16 (n < 2^16)
 #pragma unroll
   for (int j = 0; j < kBinJ; ++j) {
-    const int r = wv * C + j * kWave + ln;
-    if (j >= J || r >= int(n)) continue;
+    span[j] = 0;
+    if (j >= J || wv * C + j * kWave + ln >= n) continue;
+    const uint32_t sb = bin_sub(key[j], smode, sbase, sshift);
+    const uint32_t st = F->sub[sb];
+    const uint32_t en = sb + 1 < uint32_t(kBinSub) ? F->sub[sb + 1] : uint32_t(n);
+    span[j] = st | (en << 16);
+    s_key[st + at[j]] = key[j];
+    s_pos[st + at[j]] = pos[j];
+    s_rec[st + at[j]] = uint16_t(wv * C + j * kWave + ln);
+  }
+  if (tid == 0) F->ncrowd = 0;
+  __syncthreads();
+  {
+    constexpr int kPerT = kBinSub / kBinThreads;
+#pragma unroll
+    for (int u = 0; u < kPerT; ++u) {
+      const int sb = tid * kPerT + u;
+      const uint32_t st = F->sub[sb];
+      const uint32_t en = sb + 1 < kBinSub ? F->sub[sb + 1] : uint32_t(n);
+      if (en - st > uint32_t(kBinRun)) F->crowd[atomicAdd(&F->ncrowd, 1)] = st | (en << 16);
+    }
+  }
+  // rank: the sub-bucket's start plus its mates of smaller (key, position)
+  // (crowded sub-buckets are sorted below)
+#pragma unroll
+  for (int j = 0; j < kBinJ; ++j) {
+    at[j] = 0xFFFFFFFFu;
+    if (j >= J || wv * C + j * kWave + ln >= n) continue;
+    const int st = int(span[j] & 0xFFFFu), en = int(span[j] >> 16);
+    if (en - st > kBinRun) continue;
+    uint32_t r = uint32_t(st);
+    for (int q = st; q < en; ++q) {
+      const int64_t kq = s_key[q];
+      r += (kq < key[j]) | ((kq == key[j]) & (s_pos[q] < pos[j]));
+    }
+    at[j] = r;
+  }
+  // by rank in LDS (every mate has been read), then written rank by rank; the
+  // future at a splitter rank G = (q + 1) * R / nb' also writes splitter q
+  // (q + 1 = ceil(G nb' / R); at most one q per rank since R / nb' >= 1)
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kBinJ; ++j) {
+    const int i = wv * C + j * kWave + ln;
+    if (j >= J || i >= n || at[j] == 0xFFFFFFFFu) continue;
+    s_key[at[j]] = key[j];
+    s_pos[at[j]] = pos[j];
+    s_rec[at[j]] = uint16_t(i);
+  }
+  // the crowded sub-buckets (other ranges of LDS than the moves above)
+  const int ncrowd = F->ncrowd;
+  for (int c = 0; c < ncrowd; ++c) {
+    const uint32_t sp = F->crowd[c];
+    const int st = int(sp & 0xFFFFu);
+    bin_bitonic(s_key + st, s_pos + st, s_rec + st, int(sp >> 16) - st);
+  }
+  __syncthreads();
+  const int nbn = R >= kBinMinReady ? bins_for(R) : 0;
+  for (int r = tid; r < n; r += kBinThreads) {
     const int64_t g = int64_t(before) + r;
-    const int32_t ps = pos[j];
-    const BucketSlot& src = rec[idx[j]];
+    const int64_t k = s_key[r];
+    const int32_t ps = s_pos[r];
+    const BucketSlot& src = rec[s_rec[r]];
     a.order[g] = a.node_of_pos ? a.node_of_pos[ps] : ps;
-    a.slack[g] = a.out_slack ? a.out_slack[ps] : key[j];
+    a.slack[g] = a.out_slack ? a.out_slack[ps] : k;
     a.route[g] = slot_route(src.route);
     if (a.cost) a.cost[g] = src.cost;
-  }
-  // the next pass's splitters that fall into this bin
-  // (with no pass the bin holds at most one record, in place)
-  const int nbn = R >= kBinMinReady ? bins_for(R) : 0;
-  for (int q = tid; q < nbn - 1; q += kBinThreads) {
-    const int64_t g = (int64_t(q) + 1) * R / nbn;
-    if (g >= int64_t(before) && g < int64_t(before) + int64_t(n)) {
-      const int r = int(g - before);
-      a.split_next[q] = npass ? S.key[cur][r] : rec[r].key;
+    if (nbn > 0) {
+      const int64_t q1 = (g * nbn + R - 1) / R;
+      if (q1 >= 1 && q1 <= nbn - 1 && (q1 * R) / nbn == g) a.split_next[q1 - 1] = k;
     }
   }
   if (b == 0 && tid == 0)
@@ -1048,13 +1135,13 @@ hipError_t launch_bucket_sort(hipStream_t s, const SortArgs& a, const BucketArgs
 }
 
 hipError_t launch_bin_sort(hipStream_t s, const SortArgs& a, const BucketArgs& bk) {
-  hipLaunchKernelGGL(k_bin_sort, dim3(bk.nb), dim3(kBinThreads), sizeof(BinSmem), s, a, bk);
+  hipLaunchKernelGGL(k_bin_sort, dim3(bk.nb), dim3(kBinThreads), bin_lds_bytes(bk.cap), s, a, bk);
   return hipGetLastError();
 }
 
 hipError_t prepare_sort_kernels() {
   return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bin_sort),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, int(sizeof(BinSmem)));
+                             hipFuncAttributeMaxDynamicSharedMemorySize, int(bin_lds_bytes(kBinCap)));
 }
 
 hipError_t launch_splitters(hipStream_t s, const SortArgs& a) {

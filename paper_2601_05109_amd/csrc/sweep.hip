@@ -42,6 +42,7 @@ namespace {
 
 constexpr int kPmax = 3;          // dependencies held in registers per future
 constexpr int kHeavyCap = 64;     // cooperative list capacity per phase
+constexpr int kHeavyBatch = 2;    // cooperative dependency loads a thread keeps in flight
 constexpr int kHbmLight = 32;     // HBM path: more dependencies -> cooperative
 constexpr size_t kStaticLdsReserve = 4096;
 
@@ -131,6 +132,30 @@ __device__ inline void agg_push_lds(int64_t* mx, int32_t* cnt, int lp, int64_t r
   if (lp >= 0) {
     atomicMax(reinterpret_cast<long long*>(&mx[lp]), (long long)r);
     atomicSub(&cnt[lp], 1);
+  }
+}
+
+// A push of n merged contributions (max rem r) to dependency lp; called with
+// every lane of the wave active.
+__device__ inline void agg_push_lds_n(int64_t* mx, int32_t* cnt, int lp, int64_t r, int32_t n) {
+  const uint64_t act = ballot(lp >= 0);
+  if (act == 0) return;
+  if ((act & (act - 1)) != 0) {
+    const int lead = __builtin_ctzll(act);
+    const int first = readlane_i32(lp, lead);
+    if (ballot(lp >= 0 && lp != first) == 0) {  // fan-in: reduce, then one atomic
+      const int64_t m = wave_max_i64(lp >= 0 ? r : INT64_MIN);
+      const int64_t c = wave_sum_i64(lp >= 0 ? int64_t(n) : 0);
+      if (lane_id() == lead) {
+        atomicMax(reinterpret_cast<long long*>(&mx[first]), (long long)m);
+        atomicSub(&cnt[first], int(c));
+      }
+      return;
+    }
+  }
+  if (lp >= 0) {
+    atomicMax(reinterpret_cast<long long*>(&mx[lp]), (long long)r);
+    atomicSub(&cnt[lp], n);
   }
 }
 
@@ -246,29 +271,26 @@ __device__ inline uint32_t bucket_of(const BucketArgs& bk, int64_t key, int lvl)
 
 // Bin of a key: the number of splitters at or below it (splitters ascending,
 // in LDS), so bins ascend with the key and equal keys share a bin.
+// Bin of a key: the number of splitters <= key (nb - 1 ascending splitters,
+// nb a power of two), by binary lifting so that every lane takes the same
+// log2(nb) steps.
 __device__ inline uint32_t bin_of(const int64_t* split, int nb, int64_t key) {
-  int lo = 0, n = nb - 1;
-  while (n > 0) {
-    const int half = n >> 1;
-    if (split[lo + half] <= key) {
-      lo += half + 1;
-      n -= half + 1;
-    } else {
-      n = half;
-    }
-  }
-  return uint32_t(lo);
+  uint32_t at = 0;
+  for (int step = nb >> 1; step > 0; step >>= 1)
+    if (split[at + step - 1] <= key) at += step;
+  return at;
 }
 
 __device__ inline void bucket_put(const SweepArgs& a, uint32_t bkt, uint32_t slot, int64_t key,
                                   int64_t pos, int32_t route, int lvl, int64_t cost) {
   const uint32_t cap = a.bk.bins ? uint32_t(a.bk.cap) : uint32_t(kBucketCap);
   if (slot < cap) {
-    BucketSlot* sl = a.bk.slot + int64_t(bkt) * cap + slot;
-    sl->key = key;
-    sl->cost = cost;
-    sl->pos = int32_t(pos);
-    sl->route = slot_pack(route, lvl);
+    // three 8-byte stores: key, cost, and position | packed route (the
+    // struct's last two fields)
+    int64_t* sl = reinterpret_cast<int64_t*>(a.bk.slot + int64_t(bkt) * cap + slot);
+    sl[0] = key;
+    sl[1] = cost;
+    sl[2] = int64_t(uint64_t(uint32_t(pos)) | (uint64_t(uint32_t(slot_pack(route, lvl))) << 32));
   } else {
     st_relaxed_agent(&a.ctrl->bucket_overflow, 1u);
   }
@@ -437,12 +459,20 @@ __device__ __attribute__((always_inline)) void sweep_lds(const SweepArgs& a, con
     for (int h = 0; h < hc; ++h) {
       const int k = S.hk[h], o = S.ho[h], dg = S.hd[h];
       bool blocked = false;
-      for (int e0 = 0; e0 < dg; e0 += T) {
-        const int e = e0 + tid;
-        int32_t lp = -1;
-        if (e < dg) lp = checked_dep(L, a.p.dep_idx[o + e], b, n, k, ctrl);
-        agg_count_lds(cnt, lp);
-        if (lp >= 0 && dn[lp] == 0) blocked = true;
+      for (int e0 = 0; e0 < dg; e0 += kHeavyBatch * T) {
+        int32_t raw[kHeavyBatch];
+#pragma unroll
+        for (int u = 0; u < kHeavyBatch; ++u) {  // the batch's loads in flight together
+          const int e = e0 + u * T + tid;
+          raw[u] = e < dg ? a.p.dep_idx[o + e] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < kHeavyBatch; ++u) {
+          int32_t lp = -1;
+          if (e0 + u * T + tid < dg) lp = checked_dep(L, raw[u], b, n, k, ctrl);
+          agg_count_lds(cnt, lp);
+          if (lp >= 0 && dn[lp] == 0) blocked = true;
+        }
       }
       if (blocked) nr[k] = 1;
     }
@@ -473,6 +503,15 @@ __device__ __attribute__((always_inline)) void sweep_lds(const SweepArgs& a, con
     for (int j = 0; j < NPT; ++j)
       if ((((own & ~fin) >> j) & 1u) && cv[j] == 0) cand |= 1u << j;
     if (!__syncthreads_or(cand != 0)) break;
+    // A lane's pushes to one dependency are merged before they reach LDS
+    // (pending: target, max rem, count), so that a fan-in (every future of
+    // the wave feeding one future) costs one wave reduction per round, not
+    // one per slot.  A future finalised this round is no push target in it
+    // (its consumers were all finalised before), so the pushes may wait for
+    // the end of the round.
+    int32_t pend_lp = -1;
+    int64_t pend_r = INT64_MIN;
+    int32_t pend_n = 0;
 #pragma unroll
     for (int j = 0; j < NPT; ++j) {
       const bool c = (cand >> j) & 1u;
@@ -485,12 +524,16 @@ __device__ __attribute__((always_inline)) void sweep_lds(const SweepArgs& a, con
         mx[k] = r;
         fin |= 1u << j;
         if (hv) {
+          // the dependency list read again (phase B's registers for it are
+          // not kept through the levels)
+          const int32_t ho = a.p.dep_off[vv[j]];
+          const int32_t hd = a.p.dep_off[vv[j] + 1] - ho;
           const int hs = atomicAdd(&S.hcount, 1);
           if (hs < kHeavyCap) {
-            S.hk[hs] = k; S.ho[hs] = off[j]; S.hd[hs] = deg[j];
+            S.hk[hs] = k; S.ho[hs] = ho; S.hd[hs] = hd;
           } else {
-            for (int e = 0; e < deg[j]; ++e) {
-              const int32_t lp = local_of(L, a.p.dep_idx[off[j] + e], b, n);
+            for (int e = 0; e < hd; ++e) {
+              const int32_t lp = local_of(L, a.p.dep_idx[ho + e], b, n);
               if (lp >= 0 && lp != k) {
                 atomicMax(reinterpret_cast<long long*>(&mx[lp]), (long long)r);
                 atomicSub(&cnt[lp], 1);
@@ -499,24 +542,49 @@ __device__ __attribute__((always_inline)) void sweep_lds(const SweepArgs& a, con
           }
         }
       }
-      const bool lightc = c && !hv;
+      if (c && !hv) {
 #pragma unroll
-      for (int q = 0; q < kPmax; ++q) agg_push_lds(mx, cnt, lightc ? dep_at(p01[j], p2[j], q) : -1, r);
+        for (int q = 0; q < kPmax; ++q) {
+          const int lp = dep_at(p01[j], p2[j], q);
+          if (lp < 0) continue;
+          if (lp == pend_lp) {
+            pend_r = r > pend_r ? r : pend_r;
+            ++pend_n;
+          } else {
+            if (pend_lp >= 0) {
+              atomicMax(reinterpret_cast<long long*>(&mx[pend_lp]), (long long)pend_r);
+              atomicSub(&cnt[pend_lp], pend_n);
+            }
+            pend_lp = lp;
+            pend_r = r;
+            pend_n = 1;
+          }
+        }
+      }
     }
+    agg_push_lds_n(mx, cnt, pend_lp, pend_r, pend_n);
     if (any_heavy) {
       __syncthreads();
       const int hc = S.hcount < kHeavyCap ? S.hcount : kHeavyCap;
       for (int h = 0; h < hc; ++h) {
         const int k = S.hk[h], o = S.ho[h], dg = S.hd[h];
         const int64_t r = mx[k];
-        for (int e0 = 0; e0 < dg; e0 += T) {
-          const int e = e0 + tid;
-          int32_t lp = -1;
-          if (e < dg) {
-            lp = local_of(L, a.p.dep_idx[o + e], b, n);
-            if (lp == k) lp = -1;
+        for (int e0 = 0; e0 < dg; e0 += kHeavyBatch * T) {
+          int32_t raw[kHeavyBatch];
+#pragma unroll
+          for (int u = 0; u < kHeavyBatch; ++u) {
+            const int e = e0 + u * T + tid;
+            raw[u] = e < dg ? a.p.dep_idx[o + e] : 0;
           }
-          agg_push_lds(mx, cnt, lp, r);
+#pragma unroll
+          for (int u = 0; u < kHeavyBatch; ++u) {
+            int32_t lp = -1;
+            if (e0 + u * T + tid < dg) {
+              lp = local_of(L, raw[u], b, n);
+              if (lp == k) lp = -1;
+            }
+            agg_push_lds(mx, cnt, lp, r);
+          }
         }
       }
       __syncthreads();
@@ -525,7 +593,10 @@ __device__ __attribute__((always_inline)) void sweep_lds(const SweepArgs& a, con
     __syncthreads();
   }
   if (overflow) flag_sweep(ctrl, kStRange);
-  if (fin) atomicAdd(&S.proc, __popc(fin));
+  {  // one LDS atomic per wave
+    const int64_t nf = wave_sum_i64(int64_t(__popc(fin)));
+    if (lane_id() == 0 && nf != 0) atomicAdd(&S.proc, int(nf));
+  }
   __syncthreads();  // nothing is in flight here, so this barrier waits for no store
   if (tid == 0 && S.proc != n) flag_sweep(ctrl, kStCycle);
 
@@ -542,12 +613,23 @@ __device__ __attribute__((always_inline)) void sweep_lds(const SweepArgs& a, con
     // lds_cap < 2^16, bin < kBinMax).  Then one segment of each bin for the
     // whole workflow (one atomic per bin), and each future is routed and
     // stored into its segment.
-#pragma unroll 1
+    // the searches of all NPT futures in lockstep (independent LDS reads)
+    int64_t key[NPT];
+    uint32_t at[NPT];
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+      at[j] = 0;
+      key[j] = ((ready >> j) & 1u) ? order_key(a, mx[j * T + tid], dl) : 0;
+    }
+    for (int step = bk.nb >> 1; step > 0; step >>= 1) {
+#pragma unroll
+      for (int j = 0; j < NPT; ++j)
+        if (((ready >> j) & 1u) && bl.split[at[j] + step - 1] <= key[j]) at[j] += step;
+    }
+#pragma unroll
     for (int j = 0; j < NPT; ++j) {
       if (!((ready >> j) & 1u)) continue;
-      const int k = j * T + tid;
-      const uint32_t bn = bin_of(bl.split, bk.nb, order_key(a, mx[k], dl));
-      cnt[k] = int32_t(bn | (atomicAdd(&bl.cnt[bn], 1u) << 16));
+      cnt[j * T + tid] = int32_t(at[j] | (atomicAdd(&bl.cnt[at[j]], 1u) << 16));
     }
     __syncthreads();
     for (int t = tid; t < bk.nb; t += T) {
