@@ -74,9 +74,42 @@ int64_t nalar_store_n_nodes(const nalar_store* s);
  * nalar_problem, policy the NALAR_ORDER_LPT / NALAR_ORDER_SRTF /
  * NALAR_ROUTE_STATEFUL / NALAR_ROUTE_GREEDY bits (the store keeps no routing
  * weights: NALAR_ROUTE_WEIGHTED is NALAR_EINVAL); r as in nalar_policy_pass.
- * Synchronous. */
+ * Synchronous.
+ *
+ * The results are those of nalar_policy_pass over the snapshot, however they
+ * are computed.  After a successful pass the store keeps every future's
+ * remaining critical path (Section 4.3.1's dynamic graph: a future's remaining
+ * path depends only on it and on the futures that consume it, transitively),
+ * and the next pass is incremental: it recomputes the remaining path only for
+ * the futures appended or completed since and for the futures they depend on,
+ * transitively; readiness, keys, routes and the order are computed afresh
+ * for every ready future, ties broken by (workflow, id) without grouping the
+ * ids.  A pass falls back to a full one when there was no successful earlier
+ * pass, when the sort has no splitters from an earlier pass or its bins
+ * overflow, or when the incremental rounds leave work.  The first failing
+ * pass (any error code) also makes the next one full.  An appended
+ * dependency list must start at 0, end at n_new_edges and never decrease;
+ * otherwise the next pass returns NALAR_EINVAL. */
 int nalar_store_pass(nalar_store* s, int64_t now_us, int64_t migration_cost_us, uint32_t policy,
                      nalar_result* r);
+
+/* Incremental passes on (enable != 0, the default) or off (every pass a full
+ * one).  NALAR_EINVAL for a NULL store. */
+int nalar_store_set_incremental(nalar_store* s, int enable);
+
+/* 1 if the last nalar_store_pass was incremental, 0 if it was a full pass,
+ * -1 for a NULL store. */
+int nalar_store_last_pass_incremental(const nalar_store* s);
+
+/* Why the last pass was a full one: 0 (it was incremental) or one of the
+ * NALAR_STORE_FULL_* reasons; -1 for a NULL store. */
+#define NALAR_STORE_FULL_DISABLED      1  /* nalar_store_set_incremental(s, 0)                 */
+#define NALAR_STORE_FULL_NO_STATE      2  /* no successful pass since the first append or an error */
+#define NALAR_STORE_FULL_SHRUNK        3  /* fewer workflows or instances than at the last pass */
+#define NALAR_STORE_FULL_NO_SPLITTERS  4  /* the handle has no splitters from an earlier pass  */
+#define NALAR_STORE_FULL_OVERFLOW      5  /* a bin of the partition sort overflowed            */
+#define NALAR_STORE_FULL_ROUNDS        6  /* the incremental rounds left work                  */
+int nalar_store_last_fallback(const nalar_store* s);
 
 #ifdef __cplusplus
 }

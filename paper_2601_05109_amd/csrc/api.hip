@@ -135,6 +135,7 @@ struct nalar_policy {
   int split_cur = 0;             // the splitter buffer the next pass reads
   int bin_skip = 0;              // passes left before bins are tried again
   int bin_backoff = 1;
+  bool split_any = false;        // splitters for any ready count, any sweep (graph store)
   std::string err;
   ArenaState own;                // scratch allocated by the library for this handle
   HostStatus* host = nullptr;    // pinned, written by the sort kernel
@@ -473,6 +474,8 @@ int nalar_policy_create(const nalar_policy_config* cfg, nalar_policy** out) {
   if (e != hipSuccess) return bail(e, "hipFuncSetAttribute");
   e = prepare_sort_kernels();
   if (e != hipSuccess) return bail(e, "hipFuncSetAttribute(sort)");
+  e = prepare_inc_kernels();
+  if (e != hipSuccess) return bail(e, "hipFuncSetAttribute(incremental)");
   e = hipHostMalloc(reinterpret_cast<void**>(&h->host), sizeof(HostStatus), hipHostMallocCoherent);
   if (e != hipSuccess) return bail(e, "hipHostMalloc");
   for (int i = 0; i <= kMaxTimed; ++i) {
@@ -583,7 +586,7 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
   Ctrl* ctrl = A.ctrl[cur];
   // the next pass's splitters: after the sort, from its output (block sweep,
   // no priority levels, the handle's own arena)
-  const bool want_split = own_splitters && !sh.wave_path && !p->wf_priority;
+  const bool want_split = own_splitters && (!sh.wave_path || h->split_any) && !p->wf_priority;
 
   as.epoch = (as.epoch + 1) & kEpochMask;
   if (as.epoch == 0) {  // tags wrapped: forget every old look-back word
@@ -724,6 +727,7 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
   sa.route = r->route;
   sa.cost = r->cost_us;
   sa.split_next = A.split[h->split_cur ^ 1];
+  sa.split_min = h->split_any ? 1 : kBinMinReady;
   sa.p = pd;
   sa.passes_launched = kMaxSortPasses;  // the bucketed and bin sorts finish in one launch
   __atomic_store_n(&h->host->max_bucket, 0u, __ATOMIC_RELAXED);       // written by the large-bucket sort
@@ -858,6 +862,153 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
 }
 
 }  // namespace
+
+void nalar::policy_split_any(nalar_policy* h, bool on) { h->split_any = on; }
+
+// The incremental pass over the graph store (the kernels in incremental.hip):
+// the appended futures validated, the closure of the changed futures and its
+// sweep, readiness of every future, the ready futures binned by the previous
+// pass's splitters and sorted with ties by (wf, id).  Everything the store
+// keeps is its own; the rest is this handle's arena, as in a full pass.
+int nalar::policy_pass_incremental(nalar_policy* h, const nalar_problem* p, nalar_result* r,
+                                   const IncStore& st) {
+  h->err.clear();
+  h->timed_valid = false;
+  int rc = check_problem(h, p, r);
+  if (rc != NALAR_OK) return rc;
+  const int64_t N = p->n_nodes, W = p->n_workflows, M = p->n_instances;
+  if (N == 0 || h->split_nb <= 0 || (h->split_nb & (h->split_nb - 1)) != 0 || !h->hint_valid ||
+      (h->flags & NALAR_FORCE_TILED_SORT) || p->wf_priority ||
+      (p->flags & NALAR_ROUTE_WEIGHTED) || st.n_prev > N)
+    return kIncFallback;
+  hipError_t e = hipSetDevice(h->device);
+  if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+  BucketArgs bk{};
+  bk.bins = 1;
+  bk.nb = h->split_nb;
+  bk.cap = bin_cap_for(h->hint_ready, bk.nb);
+  rc = ensure_capacity(h, N, W, bk.nb, records_of(bk));
+  if (rc != NALAR_OK) return rc;
+  ArenaState& as = h->own;
+  Arena& A = as.ar;
+  hipStream_t s = h->stream;
+  const int cur = int(as.passes & 1);
+  const int nxt = cur ^ 1;
+  bk.cnt = A.bcnt[cur];
+  bk.slot = A.bslot;
+  bk.split = A.split[h->split_cur];
+  Ctrl* ctrl = A.ctrl[cur];
+  const bool need_reset = as.ctrl_dirty[cur];
+  as.ctrl_dirty[cur] = true;
+  as.ctrl_dirty[nxt] = true;
+  const uint32_t policy = p->flags & (NALAR_ORDER_LPT | NALAR_ORDER_SRTF | NALAR_ROUTE_STATEFUL | NALAR_ROUTE_GREEDY);
+  const ProblemDev pd = device_view(p, policy);
+  const bool contiguous = (p->flags & NALAR_WF_CONTIGUOUS) != 0 || W <= 1;
+
+  Timer tm{h};
+#define NALAR_LAUNCH(name, call)                            \
+  do {                                                      \
+    tm.mark(name);                                          \
+    hipError_t le_ = (call);                                \
+    if (le_ != hipSuccess) return hip_fail(h, le_, name);   \
+  } while (0)
+
+  const bool need_clear = !as.bcnt_clean[cur];
+  if (need_reset || need_clear)
+    NALAR_LAUNCH("reset", launch_reset(s, need_reset ? ctrl : nullptr, bk.cnt, need_clear ? bk.nb : 0));
+  as.bcnt_clean[cur] = false;
+  // the appended futures (and the one before them, for the contiguity rule)
+  NALAR_LAUNCH("nodes", launch_nodes(s, pd, ctrl, A.ctrl[nxt], A.itab, A.wf_off, contiguous ? 1 : 0,
+                                     st.n_prev > 0 ? st.n_prev - 1 : 0));
+  IncArgs ia{};
+  ia.p = pd;
+  ia.n_prev = st.n_prev;
+  ia.log = st.log;
+  ia.n_log = st.n_log;
+  ia.rem = st.rem;
+  ia.inA = st.inA;
+  ia.mxA = st.mxA;
+  ia.cntA = st.cntA;
+  ia.light = st.light;
+  ia.heavy = st.heavy;
+  ia.rlist = st.rlist;
+  ia.ic = st.ic;
+  ia.ctrl = ctrl;
+  ia.itab = A.itab;
+  ia.bk = bk;
+  ia.bk_clear = A.bcnt[nxt];
+  ia.bk_clear_n = A.capB > 0 ? A.capB : 0;
+  ia.stg_oslack = A.stg_oslack;
+  NALAR_LAUNCH("inc_clear", launch_inc_clear(s, st.inA, (N + 31) / 32));
+  NALAR_LAUNCH("inc_clear", launch_inc_clear(s, reinterpret_cast<uint32_t*>(st.ic), sizeof(IncCtrl) / 4));
+  NALAR_LAUNCH("inc_closure", launch_inc_closure(s, ia, h->cus));
+  NALAR_LAUNCH("inc_scan", launch_inc_scan(s, ia, h->cus));
+  NALAR_LAUNCH("inc_sweep", launch_inc_sweep(s, ia, h->cus));
+  NALAR_LAUNCH("inc_ready", launch_inc_ready(s, ia, h->cus));
+  as.bcnt_clean[nxt] = true;
+
+  SortArgs sa{};
+  sa.ctrl = ctrl;
+  sa.next_ctrl = A.ctrl[nxt];
+  sa.host = h->host;
+  sa.out_slack = (policy & (NALAR_ORDER_LPT | NALAR_ORDER_SRTF)) ? A.stg_oslack : nullptr;
+  sa.span = N;
+  sa.split_next = A.split[h->split_cur ^ 1];
+  sa.split_min = 1;
+  sa.tie_wf = p->wf;
+  sa.p = pd;
+  sa.passes_launched = kMaxSortPasses;
+  sa.order = r->order;
+  sa.slack = r->slack_us;
+  sa.route = r->route;
+  sa.cost = r->cost_us;
+  __atomic_store_n(&h->host->max_bucket, 0u, __ATOMIC_RELAXED);
+  __atomic_store_n(&h->host->split_nb, 0u, __ATOMIC_RELAXED);
+  __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);
+  NALAR_LAUNCH("sort_bin", launch_bin_sort(s, sa, bk));
+  if (r->rem_us) NALAR_LAUNCH("rem_copy", hipMemcpyAsync(r->rem_us, st.rem, sizeof(int64_t) * size_t(N),
+                                                         hipMemcpyDeviceToDevice, s));
+  tm.end();
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
+  const uint32_t sts = __atomic_load_n(&h->host->status, __ATOMIC_ACQUIRE);
+  if (sts == 0xFFFFFFFFu) return fail(h, NALAR_EDEVICE, "status was not written");
+  if (sts == kStatusTiled) return kIncFallbackOverflow;
+  if (sts & kStIncomplete) return kIncFallbackRounds;
+  as.passes += 1;
+  as.ctrl_dirty[nxt] = false;
+  if (sts & kStInval) return fail(h, NALAR_EINVAL, "invalid problem data");
+  if (sts & kStCycle) return fail(h, NALAR_ECYCLE, "dependency cycle");
+  if (sts & kStRange) return fail(h, NALAR_ERANGE, "remaining critical path exceeds 2^62 us");
+  r->n_ready = __atomic_load_n(&h->host->n_ready, __ATOMIC_ACQUIRE);
+  const uint32_t snb = __atomic_load_n(&h->host->split_nb, __ATOMIC_ACQUIRE);
+  h->split_nb = int(snb);
+  if (snb > 0) h->split_cur ^= 1;
+  if ((policy & NALAR_ROUTE_GREEDY) && r->n_ready > 0 && M > 0) {
+    __atomic_store_n(&h->host->aux_status, 0u, __ATOMIC_RELEASE);
+    GreedyArgs g{r->order, r->n_ready, p->type, p->est_us, p->loc, p->inst_type, p->inst_load_us,
+                 p->inst_speed_permille, int32_t(M), (policy & NALAR_ROUTE_STATEFUL) ? 1 : 0,
+                 p->migration_cost_us, r->route, r->cost_us, h->host};
+    NALAR_LAUNCH("route_greedy", launch_route_greedy(s, g));
+    tm.end();
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
+    if (__atomic_load_n(&h->host->aux_status, __ATOMIC_ACQUIRE) & kStRange)
+      return fail(h, NALAR_ERANGE, "an instance load exceeds 2^62 us under load-aware routing");
+  }
+#undef NALAR_LAUNCH
+  if (h->timing) {
+    h->n_timed = tm.n;
+    for (int i = 0; i < tm.n; ++i) (void)hipEventElapsedTime(&h->ms[i], h->ev[i], h->ev[i + 1]);
+    h->timed_valid = true;
+  }
+  h->hint_valid = true;
+  h->hint_ready = r->n_ready;
+  h->hint_min = r->n_ready ? __atomic_load_n(&h->host->slack_min, __ATOMIC_ACQUIRE) : 0;
+  h->hint_max = r->n_ready ? __atomic_load_n(&h->host->slack_max, __ATOMIC_ACQUIRE) : 0;
+  h->hint_levels = 0;
+  return NALAR_OK;
+}
 
 extern "C" {
 

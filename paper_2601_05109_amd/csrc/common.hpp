@@ -12,6 +12,7 @@ namespace nalar {
 constexpr uint32_t kStInval = 1u;
 constexpr uint32_t kStCycle = 2u;
 constexpr uint32_t kStRange = 4u;
+constexpr uint32_t kStIncomplete = 8u;  // incremental pass: work left after the last round (fall back)
 
 constexpr int kWave = 64;
 constexpr int kRadixBits = 8;
@@ -99,11 +100,13 @@ constexpr uint32_t kStatusTiled = 0x20000000u;
 // kBinTarget ready futures each on average); every workgroup of the sweep
 // counts its ready futures per bin in LDS, claims one segment of each bin with
 // one atomic, and writes them there; k_bin_sort then orders each bin in LDS
-// (at most kBinCap futures; more is an overflow, like a full bucket) and writes
+// (k_bin_sort_big the bins of more than kBinCap futures; more than the bins'
+// capacity, at most kBinAlloc, is an overflow, like a full bucket) and writes
 // the outputs at the bin's offset.
 constexpr int64_t kBinMinReady = 65536;   // smaller ready sets keep the buckets
 constexpr int kBinTarget = 1024;          // futures per bin on average
-constexpr int kBinCap = 2048;             // records per bin (LDS of k_bin_sort)
+constexpr int kBinCap = 2048;             // records per bin in one workgroup's LDS (k_bin_sort)
+constexpr int kBinAlloc = 8192;           // records per bin in HBM (more than kBinCap: k_bin_sort_big)
 constexpr int kBinMin = 64;               // bins: a power of two in [kBinMin, kBinMax]
 constexpr int kBinMax = 2048;
 // bins for a ready count (the same rule on the host and on the device)
@@ -113,8 +116,8 @@ __host__ __device__ inline int bins_for(int64_t R) {
   return nb;
 }
 __host__ __device__ inline int bin_cap_for(int64_t R, int nb) {
-  const int64_t c = 2 * ((R + nb - 1) / nb) + 256;
-  return int(c < kBinCap ? c : kBinCap);
+  const int64_t c = 8 * ((R + nb - 1) / nb) + 256;
+  return int(c < kBinAlloc ? c : kBinAlloc);
 }
 
 struct BucketSlot {

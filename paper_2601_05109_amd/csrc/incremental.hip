@@ -1,0 +1,676 @@
+// Incremental pass over the graph store.  Between two passes the store only
+// changes by deltas (Section 4.3.1: futures created with their dependencies,
+// values materialising): futures appended, futures marked done.  A future's
+// remaining critical path rem(v) = est'(v) + max over its consumers c of
+// rem(c) (est' = 0 once done) depends only on v and its descendants, so after
+// a delta it can change only for the changed futures (the seeds: appended or
+// completed since the last pass) and their ancestors (every future a seed
+// depends on, transitively): the closure.  Everything else keeps the rem of
+// the last pass, persisted in the store.
+//
+// The pass, after validating the appended futures (k_nodes over the appended
+// range):
+//   1. closure: from every seed, its dependencies are marked (one bit per
+//      future) and visited in turn;
+//   2. scan (every future, O(N + E)): readiness (not done, every dependency
+//      done) into a list of ready futures; for a closure member, one count per
+//      dependency (its consumers inside the closure); for a future outside
+//      the closure, its unchanged rem pushed to each dependency inside the
+//      closure (max);
+//   3. sweep of the closure: the members without closure consumers listed,
+//      then a member whose closure consumers are all finalised takes rem =
+//      est' + max, and pushes it to its dependencies;
+//   4. the ready futures keyed, routed and dropped into the bins of the
+//      partition sort (the splitters of the previous pass), which then orders
+//      them by (key, wf, id).
+// Steps 1 and 3 let a thread follow a chain of single dependencies itself (the
+// common shape: a future created as the child of one future), so a chain of
+// any length costs one launch; a future with several new dependencies hands
+// all but one to its workgroup's LDS queue, and a future with more than
+// kIncHeavy dependencies goes to a second LDS queue whose futures the whole
+// workgroup expands together; the workgroup drains both before it ends.  A
+// full queue spills into the next round's lists; the host launches kIncRounds
+// rounds, and work left after the last one makes the pass fall back to a
+// full pass (kStIncomplete).
+#include "internal.hpp"
+
+namespace nalar {
+
+namespace {
+
+constexpr int kIncThreads = 256;
+constexpr int kIncHeavy = 64;     // more dependencies: one workgroup expands the future
+constexpr int kScanPer = 4;       // consecutive futures per thread in the scan
+constexpr int kReadyPer = 4;      // ready futures per thread and chunk in the ready kernel
+
+__device__ inline bool bit_set_new(uint32_t* bits, int32_t v) {
+  const uint32_t m = 1u << (uint32_t(v) & 31u);
+  return (atomicOr(&bits[uint32_t(v) >> 5], m) & m) == 0u;
+}
+
+__device__ inline bool bit_get(const uint32_t* bits, int32_t v) {
+  return ((bits[uint32_t(v) >> 5] >> (uint32_t(v) & 31u)) & 1u) != 0u;
+}
+
+// Start of round r's items in a list whose rounds are appended one after the
+// other (counts of rounds 0 .. r-1, stable once round r runs).
+__device__ inline uint32_t round_base(const uint32_t* cnt, int r) {
+  uint32_t b = 0;
+  for (int i = 0; i < r; ++i) b += cnt[i];
+  return b;
+}
+
+__device__ inline void push_round(int32_t* list, uint32_t* cnt, int r, int32_t v) {
+  if (r > kIncRounds) return;  // cannot happen: rounds past the last are never appended to
+  const uint32_t at = round_base(cnt, r) + atomicAdd(&cnt[r], 1u);
+  list[at] = v;
+}
+
+__device__ inline void flag(Ctrl* c, uint32_t bits) {
+  __hip_atomic_fetch_or(&c->status_sweep, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// A dependency d of closure member u, checked: in range and not u itself;
+// for an appended future (u >= n_prev, never validated before) also of u's
+// workflow.
+__device__ inline bool dep_ok(const IncArgs& a, int32_t u, int32_t d) {
+  if (d < 0 || int64_t(d) >= a.p.N) {
+    flag(a.ctrl, kStInval);
+    return false;
+  }
+  if (d == u) {
+    flag(a.ctrl, kStCycle);
+    return false;
+  }
+  if (int64_t(u) >= a.n_prev && a.p.wf[d] != a.p.wf[u]) {
+    flag(a.ctrl, kStInval);
+    return false;
+  }
+  return true;
+}
+
+__device__ inline void join(const IncArgs& a, int32_t d) {
+  a.mxA[d] = 0;
+  a.cntA[d] = 0;
+}
+
+// A workgroup's queues of futures to continue from (LDS): single ones and
+// heavy ones; past a queue's capacity a future goes to the next round's list
+// instead.
+constexpr int kIncQueue = 2048;
+constexpr int kIncHeavyQueue = 64;
+
+struct WgQueue {
+  int32_t* q;       // [kIncQueue]
+  int* n;
+  int32_t* hq;      // [kIncHeavyQueue]
+  int* hn;
+};
+
+__device__ inline void wg_push(const WgQueue& wq, int32_t* list, uint32_t* cnt, int round, int32_t v) {
+  const int at = atomicAdd(wq.n, 1);
+  if (at < kIncQueue) wq.q[at] = v;
+  else push_round(list, cnt, round + 1, v);
+}
+
+__device__ inline void wg_push_heavy(const WgQueue& wq, int32_t* list, uint32_t* cnt, int round, int32_t v) {
+  const int at = atomicAdd(wq.hn, 1);
+  if (at < kIncHeavyQueue) wq.hq[at] = v;
+  else push_round(list, cnt, round + 1, v);
+}
+
+// ------------------------------------------------------------------ closure
+
+// u has just joined the closure: visit its dependencies, following the chain
+// while exactly one of them is new.
+__device__ void close_walk(const IncArgs& a, int32_t u, int round, const WgQueue& wq) {
+  while (u >= 0) {
+    const int32_t o0 = a.p.dep_off[u], o1 = a.p.dep_off[u + 1];
+    if (o1 - o0 > kIncHeavy) {
+      wg_push_heavy(wq, a.heavy, a.ic->ch, round, u);
+      return;
+    }
+    int32_t next = -1;
+    for (int32_t e = o0; e < o1; ++e) {
+      const int32_t d = a.p.dep_idx[e];
+      if (!dep_ok(a, u, d)) continue;
+      if (bit_set_new(a.inA, d)) {
+        join(a, d);
+        if (next < 0) next = d;
+        else wg_push(wq, a.light, a.ic->cl, round, d);
+      }
+    }
+    u = next;
+  }
+}
+
+// Drains the workgroup's queues (every thread of the workgroup calls): a heavy
+// future is expanded by the whole workgroup (expand(v) on every thread), else
+// up to one single future per thread is taken from the top, until both are
+// empty.
+template <typename Walk, typename Expand>
+__device__ void wg_drain(const WgQueue& wq, Walk walk, Expand expand) {
+  for (;;) {
+    __syncthreads();
+    const int hc = *wq.hn, c = *wq.n;
+    const int hn = hc < kIncHeavyQueue ? hc : kIncHeavyQueue;
+    const int n = c < kIncQueue ? c : kIncQueue;
+    if (hn == 0 && n == 0) break;  // the same on every thread
+    if (hn > 0) {
+      const int32_t h = wq.hq[hn - 1];
+      __syncthreads();
+      if (threadIdx.x == 0) *wq.hn = hn - 1;
+      __syncthreads();
+      expand(h);
+      continue;
+    }
+    int32_t mine = -1;
+    if (int(threadIdx.x) < n) mine = wq.q[n - 1 - int(threadIdx.x)];
+    __syncthreads();
+    if (threadIdx.x == 0) *wq.n = n > int(blockDim.x) ? n - int(blockDim.x) : 0;
+    __syncthreads();
+    if (mine >= 0) walk(mine);
+  }
+}
+
+// A heavy member's dependencies visited by the whole workgroup.
+__device__ inline void close_expand(const IncArgs& a, int32_t u, int round, const WgQueue& wq) {
+  const int32_t o0 = a.p.dep_off[u], o1 = a.p.dep_off[u + 1];
+  for (int32_t e = o0 + int32_t(threadIdx.x); e < o1; e += int32_t(blockDim.x)) {
+    const int32_t d = a.p.dep_idx[e];
+    if (!dep_ok(a, u, d)) continue;
+    if (bit_set_new(a.inA, d)) {
+      join(a, d);
+      close_walk(a, d, round, wq);
+    }
+  }
+}
+
+// Every kernel leaves the snapshot alone once validation has failed (the
+// dependency offsets of the appended futures are trusted only then).
+__device__ inline bool invalid(const IncArgs& a) { return a.ctrl->status != 0; }
+
+// Round 0 takes the seeds (completed ids of the log, then the appended
+// range); round r >= 1 the futures handed on: heavy ones expanded one per
+// workgroup, the others one per thread.  Then the workgroup drains its queue.
+__global__ __launch_bounds__(kIncThreads) void k_inc_close(IncArgs a, int r) {
+  if (invalid(a)) return;
+  const uint32_t nh = r ? a.ic->ch[r] : 0u, nl = r ? a.ic->cl[r] : 0u;
+  const int64_t n_app = a.p.N - a.n_prev;
+  const int64_t n_seed = r ? 0 : a.n_log + (n_app > 0 ? n_app : 0);
+  if (nh == 0 && nl == 0 && n_seed == 0) return;
+  __shared__ int32_t s_q[kIncQueue], s_hq[kIncHeavyQueue];
+  __shared__ int s_n, s_hn;
+  const WgQueue wq{s_q, &s_n, s_hq, &s_hn};
+  if (threadIdx.x == 0) {
+    s_n = 0;
+    s_hn = 0;
+  }
+  __syncthreads();
+  for (int64_t i = int64_t(blockIdx.x) * kIncThreads + threadIdx.x; i < n_seed;
+       i += int64_t(gridDim.x) * kIncThreads) {
+    const int32_t v = i < a.n_log ? a.log[i] : int32_t(a.n_prev + (i - a.n_log));
+    if (v < 0 || int64_t(v) >= a.p.N) continue;  // counted by the completion kernel
+    if (bit_set_new(a.inA, v)) {
+      join(a, v);
+      close_walk(a, v, r, wq);
+    }
+  }
+  const uint32_t bh = round_base(a.ic->ch, r), bl = round_base(a.ic->cl, r);
+  for (uint32_t h = blockIdx.x; h < nh; h += gridDim.x) close_expand(a, a.heavy[bh + h], r, wq);
+  for (uint32_t i = blockIdx.x * kIncThreads + threadIdx.x; i < nl; i += gridDim.x * kIncThreads)
+    close_walk(a, a.light[bl + i], r, wq);
+  wg_drain(wq, [&](int32_t v) { close_walk(a, v, r, wq); }, [&](int32_t v) { close_expand(a, v, r, wq); });
+}
+
+// --------------------------------------------------------------------- scan
+
+// Pending pushes of one lane to one dependency: merged while the target
+// repeats (children of one future are appended next to one another).
+struct Pend {
+  int32_t d = -1;
+  int64_t v = 0;
+};
+
+__device__ inline void flush_max(int64_t* mx, Pend& p) {
+  if (p.d >= 0) atomicMax(reinterpret_cast<long long*>(&mx[p.d]), (long long)p.v);
+  p.d = -1;
+}
+
+__device__ inline void flush_cnt(int32_t* cnt, Pend& p) {
+  if (p.d >= 0) atomicAdd(&cnt[p.d], int32_t(p.v));
+  p.d = -1;
+}
+
+// The last pushes of a wave: one atomic when every lane holds the same target.
+__device__ inline void flush_wave_max(int64_t* mx, Pend& p) {
+  const uint64_t act = ballot(p.d >= 0);
+  if (act == 0) return;
+  const int lead = __builtin_ctzll(act);
+  const int32_t first = readlane_i32(p.d, lead);
+  if ((act & (act - 1)) != 0 && ballot(p.d >= 0 && p.d != first) == 0) {
+    const int64_t m = wave_max_i64(p.d >= 0 ? p.v : INT64_MIN);
+    if (lane_id() == lead) atomicMax(reinterpret_cast<long long*>(&mx[first]), (long long)m);
+    p.d = -1;
+    return;
+  }
+  flush_max(mx, p);
+}
+
+__device__ inline void flush_wave_cnt(int32_t* cnt, Pend& p) {
+  const uint64_t act = ballot(p.d >= 0);
+  if (act == 0) return;
+  const int lead = __builtin_ctzll(act);
+  const int32_t first = readlane_i32(p.d, lead);
+  if ((act & (act - 1)) != 0 && ballot(p.d >= 0 && p.d != first) == 0) {
+    const int64_t s = wave_sum_i64(p.d >= 0 ? p.v : 0);
+    if (lane_id() == lead) atomicAdd(&cnt[first], int32_t(s));
+    p.d = -1;
+    return;
+  }
+  flush_cnt(cnt, p);
+}
+
+// Appends the lanes' values to a list with one atomic per wave (every lane of
+// the wave calls).
+__device__ inline void push_wave(bool in, int32_t v, int32_t* list, uint32_t* n) {
+  const uint64_t m = ballot(in);
+  if (m == 0) return;
+  const int lead = __builtin_ctzll(m);
+  uint32_t b = 0;
+  if (lane_id() == lead) b = atomicAdd(n, uint32_t(__popcll(m)));
+  b = uint32_t(readlane_i32(int32_t(b), lead));
+  if (in) list[b + lanes_below(m)] = v;
+}
+
+__global__ __launch_bounds__(kIncThreads) void k_inc_scan(IncArgs a) {
+  if (invalid(a)) return;
+  const int64_t N = a.p.N;
+  Pend pm, pc;
+  uint32_t members = 0;
+  const int64_t step = int64_t(gridDim.x) * kIncThreads * kScanPer;
+  for (int64_t g0 = int64_t(blockIdx.x) * kIncThreads * kScanPer; g0 < N; g0 += step) {
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+      const int64_t v = g0 + int64_t(threadIdx.x) * kScanPer + j;
+      bool ready = false, heavy = false;
+      if (v < N) {
+        const bool in = bit_get(a.inA, int32_t(v));
+        members += in ? 1u : 0u;
+        const int32_t o0 = a.p.dep_off[v], o1 = a.p.dep_off[v + 1];
+        if (o1 - o0 > kIncHeavy) {
+          heavy = true;
+        } else {
+          bool blocked = false;
+          int64_t rv = 0;
+          bool have_rv = false;
+          for (int32_t e = o0; e < o1; ++e) {
+            const int32_t d = a.p.dep_idx[e];
+            if (d < 0 || int64_t(d) >= N) continue;  // reported by the closure or an earlier pass
+            blocked |= a.p.done[d] == 0;
+            if (in) {
+              if (d != pc.d) {
+                flush_cnt(a.cntA, pc);
+                pc.d = d;
+                pc.v = 0;
+              }
+              pc.v += 1;
+            } else if (bit_get(a.inA, d)) {
+              if (!have_rv) {
+                rv = a.rem[v];
+                have_rv = true;
+              }
+              if (d != pm.d) {
+                flush_max(a.mxA, pm);
+                pm.d = d;
+                pm.v = rv;
+              }
+              pm.v = rv > pm.v ? rv : pm.v;
+            }
+          }
+          ready = a.p.done[v] == 0 && !blocked;
+        }
+      }
+      push_wave(ready, int32_t(v), a.rlist, &a.ic->r_n);
+      push_wave(heavy, int32_t(v), a.heavy, &a.ic->scan_heavy);
+    }
+  }
+  flush_wave_cnt(a.cntA, pc);
+  flush_wave_max(a.mxA, pm);
+  const int64_t mt = wave_sum_i64(int64_t(members));
+  if (lane_id() == 0 && mt) atomicAdd(&a.ic->a_n, uint32_t(mt));
+}
+
+// The futures with more than kIncHeavy dependencies, one per workgroup.
+__global__ __launch_bounds__(kIncThreads) void k_inc_scan_heavy(IncArgs a) {
+  if (invalid(a)) return;
+  __shared__ int s_blocked;
+  const uint32_t nh = a.ic->scan_heavy;
+  for (uint32_t h = blockIdx.x; h < nh; h += gridDim.x) {
+    const int32_t v = a.heavy[h];
+    if (threadIdx.x == 0) s_blocked = 0;
+    __syncthreads();
+    const bool in = bit_get(a.inA, v);
+    const int32_t o0 = a.p.dep_off[v], o1 = a.p.dep_off[v + 1];
+    bool blocked = false;
+    int64_t rv = 0;
+    if (!in && int64_t(v) < a.n_prev) rv = a.rem[v];
+    for (int32_t e = o0 + int32_t(threadIdx.x); e < o1; e += kIncThreads) {
+      const int32_t d = a.p.dep_idx[e];
+      if (d < 0 || int64_t(d) >= a.p.N) continue;
+      blocked |= a.p.done[d] == 0;
+      if (in) atomicAdd(&a.cntA[d], 1);
+      else if (bit_get(a.inA, d)) atomicMax(reinterpret_cast<long long*>(&a.mxA[d]), (long long)rv);
+    }
+    if (blocked) s_blocked = 1;
+    __syncthreads();
+    if (threadIdx.x == 0 && a.p.done[v] == 0 && s_blocked == 0) a.rlist[atomicAdd(&a.ic->r_n, 1u)] = v;
+    __syncthreads();
+  }
+}
+
+// -------------------------------------------------------------------- sweep
+
+// u's closure consumers are all finalised: rem(u) = est' + max, pushed to its
+// dependencies; a dependency whose count reaches zero is finalised next (by
+// this thread if it is the first, else in the next round).
+__device__ void sweep_walk(const IncArgs& a, int32_t u, int round, uint32_t& fin, const WgQueue& wq) {
+  while (u >= 0) {
+    const int64_t est = a.p.done[u] ? 0 : a.p.est[u];
+    const int64_t m = __hip_atomic_load(&a.mxA[u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int64_t r = est + m;
+    if (r > NALAR_REM_MAX) {
+      r = NALAR_REM_MAX + 1;
+      flag(a.ctrl, kStRange);
+    }
+    a.rem[u] = r;
+    ++fin;
+    const int32_t o0 = a.p.dep_off[u], o1 = a.p.dep_off[u + 1];
+    if (o1 - o0 > kIncHeavy) {
+      wg_push_heavy(wq, a.heavy, a.ic->sh, round, u);
+      return;
+    }
+    int32_t next = -1;
+    for (int32_t e = o0; e < o1; ++e) {
+      const int32_t d = a.p.dep_idx[e];
+      if (d < 0 || int64_t(d) >= a.p.N || d == u) continue;
+      atomicMax(reinterpret_cast<long long*>(&a.mxA[d]), (long long)r);
+      if (__hip_atomic_fetch_add(&a.cntA[d], -1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == 1) {
+        if (next < 0) next = d;
+        else wg_push(wq, a.light, a.ic->sl, round, d);
+      }
+    }
+    u = next;
+  }
+}
+
+__device__ inline void add_fin(const IncArgs& a, uint32_t fin) {
+  const int64_t t = wave_sum_i64(int64_t(fin));
+  if (lane_id() == 0 && t) atomicAdd(&a.ic->fin, uint32_t(t));
+}
+
+// The sweep's first round: every closure member without closure consumers,
+// listed before any member is finalised (a walk may bring another member's
+// count to zero while this list is taken, and that member is then the
+// walker's), one thread per word of the membership bits.
+__global__ __launch_bounds__(kIncThreads) void k_inc_front0(IncArgs a) {
+  if (invalid(a)) return;
+  const int64_t words = (a.p.N + 31) / 32;
+  for (int64_t w = int64_t(blockIdx.x) * kIncThreads + threadIdx.x; w < words;
+       w += int64_t(gridDim.x) * kIncThreads) {
+    uint32_t bits = a.inA[w];
+    while (bits) {
+      const int b = __builtin_ctz(bits);
+      bits &= bits - 1;
+      const int32_t v = int32_t(w * 32 + b);
+      if (a.cntA[v] == 0) push_round(a.light, a.ic->sl, 0, v);
+    }
+  }
+}
+
+// A finalised heavy member's rem pushed to its dependencies by the whole
+// workgroup.
+__device__ inline void sweep_expand(const IncArgs& a, int32_t u, int round, uint32_t& fin, const WgQueue& wq) {
+  const int64_t ru = a.rem[u];
+  const int32_t o0 = a.p.dep_off[u], o1 = a.p.dep_off[u + 1];
+  for (int32_t e = o0 + int32_t(threadIdx.x); e < o1; e += int32_t(blockDim.x)) {
+    const int32_t d = a.p.dep_idx[e];
+    if (d < 0 || int64_t(d) >= a.p.N || d == u) continue;
+    atomicMax(reinterpret_cast<long long*>(&a.mxA[d]), (long long)ru);
+    if (__hip_atomic_fetch_add(&a.cntA[d], -1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == 1)
+      sweep_walk(a, d, round, fin, wq);
+  }
+}
+
+__global__ __launch_bounds__(kIncThreads) void k_inc_sweep(IncArgs a, int r) {
+  if (invalid(a)) return;
+  const uint32_t nh = a.ic->sh[r], nl = a.ic->sl[r];
+  if (nh == 0 && nl == 0) return;
+  __shared__ int32_t s_q[kIncQueue], s_hq[kIncHeavyQueue];
+  __shared__ int s_n, s_hn;
+  const WgQueue wq{s_q, &s_n, s_hq, &s_hn};
+  if (threadIdx.x == 0) {
+    s_n = 0;
+    s_hn = 0;
+  }
+  __syncthreads();
+  const uint32_t bh = round_base(a.ic->sh, r), bl = round_base(a.ic->sl, r);
+  uint32_t fin = 0;
+  for (uint32_t h = blockIdx.x; h < nh; h += gridDim.x) sweep_expand(a, a.heavy[bh + h], r, fin, wq);
+  for (uint32_t i = blockIdx.x * kIncThreads + threadIdx.x; i < nl; i += gridDim.x * kIncThreads)
+    sweep_walk(a, a.light[bl + i], r, fin, wq);
+  wg_drain(wq, [&](int32_t v) { sweep_walk(a, v, r, fin, wq); },
+           [&](int32_t v) { sweep_expand(a, v, r, fin, wq); });
+  add_fin(a, fin);
+}
+
+// -------------------------------------------------------------------- ready
+
+// Incomplete rounds or an unfinished closure: status for the host.
+__device__ inline void check_rounds(const IncArgs& a) {
+  const IncCtrl* ic = a.ic;
+  if (ic->cl[kIncRounds] | ic->ch[kIncRounds] | ic->sl[kIncRounds] | ic->sh[kIncRounds])
+    flag(a.ctrl, kStIncomplete);
+  else if (ic->fin != ic->a_n)
+    flag(a.ctrl, kStCycle);  // some member's closure consumers never all finalised
+}
+
+__device__ inline int64_t key_of(uint32_t policy, int64_t rem, int64_t dl) {
+  if (policy & NALAR_ORDER_LPT) return -rem;
+  if (policy & NALAR_ORDER_SRTF) return rem;
+  return dl - rem;
+}
+
+// The ready futures: key, bin (splitters in LDS), route, slot.  Per chunk of
+// kReadyPer * T futures, the bins' LDS counts give each future its rank
+// inside the chunk's part of its bin, and one atomic per bin claims that part.
+__global__ __launch_bounds__(kIncThreads) void k_inc_ready(IncArgs a) {
+  constexpr int T = kIncThreads;
+  for (int64_t i = int64_t(blockIdx.x) * T + threadIdx.x; i < a.bk_clear_n; i += int64_t(gridDim.x) * T)
+    a.bk_clear[i] = 0;  // the next pass's bin counters
+  Ctrl* ctrl = a.ctrl;
+  if (ctrl->status != 0) return;
+  if (blockIdx.x == 0 && threadIdx.x == 0) check_rounds(a);
+  if ((ctrl->status | ctrl->status_sweep) != 0) return;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int M = int(a.p.M);
+  const int nb = a.bk.nb;
+  unsigned char* sp = smem;
+  int64_t* s_split = reinterpret_cast<int64_t*>(sp); sp += 8 * size_t(kBinMax);
+  int64_t* s_load = reinterpret_cast<int64_t*>(sp); sp += 8 * size_t(M);
+  double* s_inv = reinterpret_cast<double*>(sp); sp += 8 * size_t(M);
+  int32_t* s_type = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  int32_t* s_idx = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  int32_t* s_speed = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  int32_t* s_pos = reinterpret_cast<int32_t*>(sp); sp += 4 * size_t(M);
+  uint32_t* s_run = reinterpret_cast<uint32_t*>(sp); sp += 4 * size_t(kTypeDirect);
+  uint32_t* s_prun = reinterpret_cast<uint32_t*>(sp); sp += 4 * size_t(kTypeDirect);
+  uint32_t* s_cnt = reinterpret_cast<uint32_t*>(sp); sp += 4 * size_t(kBinMax);
+  uint32_t* s_base = reinterpret_cast<uint32_t*>(sp);
+  __shared__ int64_t s_red[3][T / kWave];
+  const int tid = threadIdx.x;
+  for (int i = tid; i < M; i += T) {
+    s_load[i] = a.itab.load[i];
+    s_inv[i] = a.itab.inv_speed[i];
+    s_type[i] = a.itab.type[i];
+    s_idx[i] = a.itab.idx[i];
+    s_speed[i] = a.itab.speed[i];
+    s_pos[i] = a.itab.pos_of[i];
+  }
+  for (int t = tid; t < kTypeDirect; t += T) {
+    s_run[t] = a.itab.run[t];
+    s_prun[t] = a.itab.prun[t];
+  }
+  for (int i = tid; i < nb - 1; i += T) s_split[i] = a.bk.split[i];
+  for (int i = tid; i < nb; i += T) s_cnt[i] = 0;
+  __syncthreads();
+  const uint32_t policy = a.p.policy;
+  const bool out_slack = (policy & (NALAR_ORDER_LPT | NALAR_ORDER_SRTF)) != 0;
+  const int64_t R = a.ic->r_n;
+  int64_t tmin = INT64_MAX, tmax = INT64_MIN, tready = 0;
+  constexpr int64_t kChunk = int64_t(kReadyPer) * T;
+  for (int64_t c0 = int64_t(blockIdx.x) * kChunk; c0 < R; c0 += int64_t(gridDim.x) * kChunk) {
+    int32_t v[kReadyPer];
+    int64_t key[kReadyPer], rem[kReadyPer], dl[kReadyPer];
+    uint32_t bin[kReadyPer], rk[kReadyPer];
+#pragma unroll
+    for (int j = 0; j < kReadyPer; ++j) {
+      const int64_t i = c0 + j * T + tid;
+      v[j] = -1;
+      key[j] = rem[j] = dl[j] = 0;
+      bin[j] = rk[j] = 0;
+      if (i < R) {
+        v[j] = a.rlist[i];
+        rem[j] = a.rem[v[j]];
+        dl[j] = a.p.deadline[a.p.wf[v[j]]] - a.p.now;
+        key[j] = key_of(policy, rem[j], dl[j]);
+      }
+    }
+    for (int st = nb >> 1; st > 0; st >>= 1) {
+#pragma unroll
+      for (int j = 0; j < kReadyPer; ++j)
+        if (v[j] >= 0 && s_split[bin[j] + st - 1] <= key[j]) bin[j] += st;
+    }
+#pragma unroll
+    for (int j = 0; j < kReadyPer; ++j)
+      if (v[j] >= 0) rk[j] = atomicAdd(&s_cnt[bin[j]], 1u);
+    __syncthreads();
+    for (int t = tid; t < nb; t += T) {
+      const uint32_t c = s_cnt[t];
+      s_base[t] = c ? add_agent(a.bk.cnt + t, c) : 0u;
+      s_cnt[t] = 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kReadyPer; ++j) {
+      if (v[j] < 0) continue;
+      const int32_t u = v[j];
+      int32_t route;
+      int64_t cost;
+      route_future(a.p.type[u], a.p.est[u], a.p.loc[u], int32_t(M), a.p.mig, s_type, s_idx, s_load, s_speed,
+                   s_inv, s_pos, s_run, (policy & NALAR_ROUTE_STATEFUL) != 0, route, cost, s_prun);
+      const uint32_t slot = rk[j] + s_base[bin[j]];
+      if (slot < uint32_t(a.bk.cap)) {
+        int64_t* sl = reinterpret_cast<int64_t*>(a.bk.slot + int64_t(bin[j]) * a.bk.cap + slot);
+        sl[0] = key[j];
+        sl[1] = cost;
+        sl[2] = int64_t(uint64_t(uint32_t(u)) | (uint64_t(uint32_t(slot_pack(route, 0))) << 32));
+      } else {
+        st_relaxed_agent(&ctrl->bucket_overflow, 1u);
+      }
+      if (out_slack) a.stg_oslack[u] = dl[j] - rem[j];
+      tmin = key[j] < tmin ? key[j] : tmin;
+      tmax = key[j] > tmax ? key[j] : tmax;
+      tready += 1;
+    }
+    __syncthreads();  // the counters are clean again before the next chunk
+  }
+  const int64_t mn = wave_min_i64(tmin), mx = wave_max_i64(tmax), rd = wave_sum_i64(tready);
+  const int wv = tid / kWave;
+  if (lane_id() == 0) {
+    s_red[0][wv] = mn;
+    s_red[1][wv] = mx;
+    s_red[2][wv] = rd;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int64_t a0 = INT64_MAX, a1 = INT64_MIN, a2 = 0;
+    for (int x = 0; x < T / kWave; ++x) {
+      a0 = s_red[0][x] < a0 ? s_red[0][x] : a0;
+      a1 = s_red[1][x] > a1 ? s_red[1][x] : a1;
+      a2 += s_red[2][x];
+    }
+    if (a2 > 0) {
+      const int slot = blockIdx.x & (kParts - 1);
+      __hip_atomic_fetch_min(&ctrl->part_min[slot], a0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_fetch_max(&ctrl->part_max[slot], a1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      add_agent(&ctrl->part_cnt[slot], a2);
+    }
+  }
+}
+
+__global__ __launch_bounds__(kIncThreads) void k_inc_clear(uint32_t* p, int64_t n) {
+  for (int64_t i = int64_t(blockIdx.x) * kIncThreads + threadIdx.x; i < n; i += int64_t(gridDim.x) * kIncThreads)
+    p[i] = 0;
+}
+
+int inc_grid(int64_t n, int cap) {
+  int64_t g = (n + kIncThreads - 1) / kIncThreads;
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return int(g);
+}
+
+}  // namespace
+
+size_t inc_ready_lds(int64_t M) {
+  return 8 * size_t(kBinMax) + 32 * size_t(M) + 8 * size_t(kTypeDirect) + 8 * size_t(kBinMax);
+}
+
+hipError_t prepare_inc_kernels() {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_inc_ready),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, int(inc_ready_lds(NALAR_MAX_INSTANCES)));
+}
+
+hipError_t launch_inc_clear(hipStream_t s, uint32_t* p, int64_t n) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_inc_clear, dim3(inc_grid(n, 2048)), dim3(kIncThreads), 0, s, p, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_inc_closure(hipStream_t s, const IncArgs& a, int cus) {
+  const int64_t seeds = a.n_log + (a.p.N - a.n_prev);
+  hipLaunchKernelGGL(k_inc_close, dim3(inc_grid(seeds, 4096)), dim3(kIncThreads), 0, s, a, 0);
+  hipError_t e = hipGetLastError();
+  for (int r = 1; r <= kIncRounds - 1 && e == hipSuccess; ++r) {
+    hipLaunchKernelGGL(k_inc_close, dim3(4 * cus), dim3(kIncThreads), 0, s, a, r);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
+hipError_t launch_inc_scan(hipStream_t s, const IncArgs& a, int cus) {
+  hipLaunchKernelGGL(k_inc_scan, dim3(inc_grid((a.p.N + kScanPer - 1) / kScanPer, 8 * cus)), dim3(kIncThreads),
+                     0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_inc_scan_heavy, dim3(2 * cus), dim3(kIncThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_inc_sweep(hipStream_t s, const IncArgs& a, int cus) {
+  hipLaunchKernelGGL(k_inc_front0, dim3(inc_grid((a.p.N + 31) / 32, 8 * cus)), dim3(kIncThreads), 0, s, a);
+  hipError_t e = hipGetLastError();
+  for (int r = 0; r <= kIncRounds - 1 && e == hipSuccess; ++r) {
+    hipLaunchKernelGGL(k_inc_sweep, dim3(4 * cus), dim3(kIncThreads), 0, s, a, r);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
+hipError_t launch_inc_ready(hipStream_t s, const IncArgs& a, int cus) {
+  hipLaunchKernelGGL(k_inc_ready, dim3(4 * cus), dim3(kIncThreads), inc_ready_lds(a.p.M), s, a);
+  return hipGetLastError();
+}
+
+}  // namespace nalar

@@ -26,7 +26,6 @@ constexpr int kNodeItems = 4;
 // The dominance checks then run per sorted position, so the lanes of one run
 // read the same LDS entries.
 constexpr int kPruneRun = 128;
-constexpr int kTabGroups = NALAR_MAX_INSTANCES / kWave;
 
 struct TabLds {
   int32_t* type;    // by index
@@ -239,7 +238,8 @@ __device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl, un
 // instance table sorted by type, so each future's candidates form one
 // contiguous run, and resets the control block of the next pass.
 __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl, Ctrl* next_ctrl,
-                                                       ITab it, int32_t* wf_off, int contiguous) {
+                                                       ITab it, int32_t* wf_off, int contiguous,
+                                                       int64_t v_begin) {
   const int64_t N = p.N, W = p.W, M = p.M;
   if (blockIdx.x == 0) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -251,7 +251,7 @@ __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl
   bool bad = false;
   // kNodeItems nodes a stride apart per thread, every load issued before the
   // first check, so that each thread keeps that many lines in flight
-  for (int64_t v0 = g0; v0 < N; v0 += kNodeItems * stride) {
+  for (int64_t v0 = v_begin + g0; v0 < N; v0 += kNodeItems * stride) {
     int32_t w[kNodeItems], t[kNodeItems], l[kNodeItems], o0[kNodeItems], o1[kNodeItems], wn[kNodeItems];
     int64_t e[kNodeItems];
     uint8_t d[kNodeItems];
@@ -310,11 +310,11 @@ int grid_for(int64_t n, int threads, int cap) {
 }  // namespace
 
 hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
-                        int32_t* wf_off, int contiguous) {
-  const int64_t nv = (p.N + kNodeItems - 1) / kNodeItems;
+                        int32_t* wf_off, int contiguous, int64_t v_begin) {
+  const int64_t nv = (p.N - v_begin + kNodeItems - 1) / kNodeItems;
   int64_t n = nv > p.W + 1 ? nv : p.W + 1;
   hipLaunchKernelGGL(k_nodes, dim3(grid_for(n, kNodeThreads, 4096) + 1), dim3(kNodeThreads), tab_lds_bytes(p.M), s, p,
-                     ctrl, next_ctrl, itab, wf_off, contiguous);
+                     ctrl, next_ctrl, itab, wf_off, contiguous, v_begin);
   return hipGetLastError();
 }
 

@@ -53,8 +53,11 @@ struct SortArgs {
   uint32_t epoch;
   uint32_t levels;              // nonzero: the keys carry priority levels
   int64_t* split_next;          // [kBinMax - 1] this pass's key quantiles, for the next pass
+  int64_t split_min;            // fewest ready futures that get splitters
   int32_t passes_launched;      // tiled sort: digit passes launched so far (the
                                 //   splitters wait for the last one)
+  const int32_t* tie_wf;        // bin sort: positions are node ids, equal keys ordered by
+                                //   (tie_wf[id], id); NULL: by position
   ProblemDev p;                 // the snapshot (deadline, wf and the key's policy for the splitters)
   int32_t* order;
   int64_t* slack;
@@ -205,14 +208,83 @@ struct DecideArgs {
 };
 hipError_t launch_decide(hipStream_t s, const DecideArgs& a);
 
+// Incremental pass over the graph store (incremental.hip).  Rounds of the
+// closure and of its sweep append to per-round lists (items of round r follow
+// those of rounds 0 .. r-1); the host launches kIncRounds rounds of each.
+constexpr int kIncRounds = 8;
+
+struct IncCtrl {
+  uint32_t a_n;                  // closure members
+  uint32_t r_n;                  // ready futures
+  uint32_t fin;                  // closure members finalised by the sweep
+  uint32_t scan_heavy;           // futures with many dependencies, for the scan
+  uint32_t cl[kIncRounds + 1];   // closure: single futures per round
+  uint32_t ch[kIncRounds + 1];   // closure: futures expanded by a workgroup
+  uint32_t sl[kIncRounds + 1];   // sweep: single futures per round
+  uint32_t sh[kIncRounds + 1];   // sweep: futures pushed by a workgroup
+};
+
+struct IncArgs {
+  ProblemDev p;                  // the store's snapshot
+  int64_t n_prev;                // futures rem covers from the last pass
+  const int32_t* log;            // [n_log] ids completed since the last pass
+  int64_t n_log;
+  int64_t* rem;                  // [N] remaining critical path, kept across passes
+  uint32_t* inA;                 // [ceil(N/32)] closure membership bits (zero on entry)
+  int64_t* mxA;                  // [N] max rem over consumers (closure members)
+  int32_t* cntA;                 // [N] closure consumers not yet finalised (members)
+  int32_t* light;                // [N] per-round lists
+  int32_t* heavy;                // [N]
+  int32_t* rlist;                // [N] ready futures
+  IncCtrl* ic;                   // zero on entry
+  Ctrl* ctrl;                    // the pass's control block
+  ITab itab;
+  BucketArgs bk;                 // bins (the previous pass's splitters)
+  uint32_t* bk_clear;            // the next pass's bin counters, zeroed here
+  int64_t bk_clear_n;
+  int64_t* stg_oslack;           // [N] slack by id when the key is not the slack
+};
+size_t inc_ready_lds(int64_t M);
+hipError_t prepare_inc_kernels();
+hipError_t launch_inc_clear(hipStream_t s, uint32_t* p, int64_t n_words);
+hipError_t launch_inc_closure(hipStream_t s, const IncArgs& a, int cus);
+hipError_t launch_inc_scan(hipStream_t s, const IncArgs& a, int cus);
+hipError_t launch_inc_sweep(hipStream_t s, const IncArgs& a, int cus);
+hipError_t launch_inc_ready(hipStream_t s, const IncArgs& a, int cus);
+
+// The store's side of an incremental pass (defined in api.hip): its buffers,
+// and the pass.  Returns a NALAR_* code, or one of the kIncFallback codes when
+// the pass must be a full one instead.
+constexpr int kIncFallback = 1000;          // no splitters or another precondition
+constexpr int kIncFallbackOverflow = 1001;  // a bin overflowed
+constexpr int kIncFallbackRounds = 1002;    // the rounds left work
+inline bool inc_fallback(int rc) { return rc >= kIncFallback && rc <= kIncFallbackRounds; }
+struct IncStore {
+  int64_t n_prev;
+  const int32_t* log;
+  int64_t n_log;
+  int64_t* rem;
+  uint32_t* inA;
+  int64_t* mxA;
+  int32_t* cntA;
+  int32_t* light;
+  int32_t* heavy;
+  int32_t* rlist;
+  IncCtrl* ic;
+};
+int policy_pass_incremental(nalar_policy* h, const nalar_problem* p, nalar_result* r, const IncStore& st);
+// Full passes of the store leave splitters for any number of ready futures.
+void policy_split_any(nalar_policy* h, bool on);
+
 // Handle accessors for the graph store (store.hip), defined in api.hip.
 hipStream_t policy_stream(const nalar_policy* h);
 int policy_device(const nalar_policy* h);
 int policy_fail(nalar_policy* h, int code, const char* msg);
 
 // ingest.hip
+// Validates the futures from v_begin on (and every deadline and instance).
 hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
-                        int32_t* wf_off, int contiguous);
+                        int32_t* wf_off, int contiguous, int64_t v_begin = 0);
 
 // sort.hip (mark(ctx, name) is called before each launch, for timing)
 hipError_t launch_reset(hipStream_t s, Ctrl* c, uint32_t* clear, int64_t n_clear);

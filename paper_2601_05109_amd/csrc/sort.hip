@@ -704,28 +704,65 @@ __device__ inline int64_t output_key(const SortArgs& a, int64_t g) {
 // splitters (this pass's key quantiles: the key at rank (q + 1) * R / nb' for
 // nb' = bins_for(R)): the future of that rank writes it.  Workgroup 0
 // publishes the status.
-constexpr int kBinWaves = kBinThreads / kWave;
-constexpr int kBinJ = (kBinCap + kBinThreads - 1) / kBinThreads;  // items per lane
+// Two kernels share the work: k_bin_sort (kBinThreads threads, a bin of up
+// to kBinCap futures in LDS, one workgroup per bin) and k_bin_sort_big (four
+// times the threads and the LDS) for the few bins holding more: the bins hold up to
+// kBinAlloc records, so that a ready set whose keys moved since the splitters
+// were taken (a whole workflow's futures shifting together) still fits.
+constexpr int kBinBigThreads = 4 * kBinThreads;
+constexpr int kBinBigCap = 4 * kBinCap;
+static_assert(kBinBigCap >= kBinAlloc, "the big-bin kernel holds a full bin");
+constexpr int kBinJ = (kBinCap + kBinThreads - 1) / kBinThreads;  // items per lane (both kernels)
+static_assert(kBinJ * kBinBigThreads >= kBinBigCap, "items per lane of the big-bin kernel");
 constexpr int kBinSub = 1024;
 constexpr int kBinSubLog = 10;
-static_assert(kBinSub == 1 << kBinSubLog && kBinSub % kBinThreads == 0, "sub-buckets");
+static_assert(kBinSub == 1 << kBinSubLog && kBinSub % kBinBigThreads == 0, "sub-buckets");
 
 constexpr int kBinRun = 32;
-constexpr int kBinCrowdMax = kBinCap / (kBinRun + 1) + 1;  // crowded sub-buckets a bin can hold
+constexpr int kBinCrowdMax = kBinBigCap / (kBinRun + 1) + 1;  // crowded sub-buckets a bin can hold
 
+template <int NW>
 struct BinFixed {
   uint32_t sub[kBinSub];  // sub-bucket counts, then starts
   uint32_t crowd[kBinCrowdMax];  // crowded sub-buckets: start | end << 16
   int ncrowd;
-  uint32_t tmp[kBinWaves];
+  uint32_t tmp[NW];
   int64_t range[kRangeWords];
-  int64_t red[4][kBinWaves];
+  int64_t red[4][NW];
 };
 
 __host__ __device__ constexpr size_t bin_align(size_t b) { return (b + 15) & ~size_t(15); }
 
-__host__ __device__ constexpr size_t bin_lds_bytes(int cap) {
-  return bin_align(8 * size_t(cap)) + bin_align(4 * size_t(cap)) + bin_align(2 * size_t(cap)) + sizeof(BinFixed);
+// LDS of a workgroup holding lc futures: keys, positions, record indices,
+// (with workflow ties) the positions' workflows, and the fixed part.
+template <int NW>
+__host__ __device__ constexpr size_t bin_lds_bytes(int lc, bool tie_wf) {
+  return bin_align(8 * size_t(lc)) + bin_align(4 * size_t(lc)) + bin_align(2 * size_t(lc)) +
+         (tie_wf ? bin_align(4 * size_t(lc)) : 0) + sizeof(BinFixed<NW>);
+}
+
+template <int NW>
+struct BinLds {
+  int64_t* key;
+  int32_t* pos;
+  uint16_t* rec;
+  int32_t* wf;
+  BinFixed<NW>* F;
+};
+
+template <int NW>
+__device__ inline BinLds<NW> carve_bin(unsigned char* sp, int lc, bool tie_wf) {
+  BinLds<NW> L;
+  L.key = reinterpret_cast<int64_t*>(sp); sp += bin_align(8 * size_t(lc));
+  L.pos = reinterpret_cast<int32_t*>(sp); sp += bin_align(4 * size_t(lc));
+  L.rec = reinterpret_cast<uint16_t*>(sp); sp += bin_align(2 * size_t(lc));
+  L.wf = nullptr;
+  if (tie_wf) {
+    L.wf = reinterpret_cast<int32_t*>(sp);
+    sp += bin_align(4 * size_t(lc));
+  }
+  L.F = reinterpret_cast<BinFixed<NW>*>(sp);
+  return L;
 }
 
 // Sub-bucket of a key: mode 0, (key - base) >> sshift (base the bin's lowest
@@ -744,16 +781,21 @@ __device__ inline uint32_t bin_sub(int64_t key, int mode, int64_t base, int sshi
   return mode == 1 ? uint32_t(kBinSub - 1) - f : f;
 }
 
-// Entries x < y of an LDS segment: (key, position) ascending, the record
-// index moving along.
-__device__ inline void bin_cmpx(int64_t* k, int32_t* p, uint16_t* r, int x, int y) {
+// Entries x < y of an LDS segment: (key, workflow, position) ascending (no
+// workflow array: (key, position)), the record index moving along.
+__device__ inline void bin_cmpx(int64_t* k, int32_t* p, uint16_t* r, int32_t* w, int x, int y) {
   const int64_t kx = k[x], ky = k[y];
   const int32_t px = p[x], py = p[y];
-  if (ky < kx || (ky == kx && py < px)) {
+  const int32_t wx = w ? w[x] : 0, wy = w ? w[y] : 0;
+  if (ky < kx || (ky == kx && (wy < wx || (wy == wx && py < px)))) {
     k[x] = ky;
     k[y] = kx;
     p[x] = py;
     p[y] = px;
+    if (w) {
+      w[x] = wy;
+      w[y] = wx;
+    }
     const uint16_t rx = r[x];
     r[x] = r[y];
     r[y] = rx;
@@ -764,45 +806,43 @@ __device__ inline void bin_cmpx(int64_t* k, int32_t* p, uint16_t* r, int x, int 
 // the workgroup takes part): sizes 2, 4, ..., P (P the power of two >= L),
 // each a mirror step (entry i of a block against the block's entry k - 1 - i)
 // and then half-cleaners at distances k/4 ... 1.
-__device__ void bin_bitonic(int64_t* k, int32_t* p, uint16_t* r, int L) {
+__device__ void bin_bitonic(int64_t* k, int32_t* p, uint16_t* r, int32_t* w, int L) {
   int lp = 0;
   while ((1 << lp) < L) ++lp;
   const int P = 1 << lp;
   for (int ls = 1; ls <= lp; ++ls) {  // size 2^ls, half 2^(ls - 1)
     const int lh = ls - 1;
-    for (int c = threadIdx.x; c < P / 2; c += kBinThreads) {
+    for (int c = threadIdx.x; c < P / 2; c += int(blockDim.x)) {
       const int base = (c >> lh) << ls, off = c & ((1 << lh) - 1);
       const int x = base + off, y = base + (1 << ls) - 1 - off;
-      if (y < L) bin_cmpx(k, p, r, x, y);
+      if (y < L) bin_cmpx(k, p, r, w, x, y);
     }
     __syncthreads();
     for (int ld = lh - 1; ld >= 0; --ld) {  // distance 2^ld
-      for (int c = threadIdx.x; c < P / 2; c += kBinThreads) {
+      for (int c = threadIdx.x; c < P / 2; c += int(blockDim.x)) {
         const int x = ((c >> ld) << (ld + 1)) + (c & ((1 << ld) - 1)), y = x + (1 << ld);
-        if (y < L) bin_cmpx(k, p, r, x, y);
+        if (y < L) bin_cmpx(k, p, r, w, x, y);
       }
       __syncthreads();
     }
   }
 }
 
-__global__ __launch_bounds__(kBinThreads) void k_bin_sort(SortArgs a, BucketArgs bk) {
-  extern __shared__ __align__(16) unsigned char smem[];
+// Sorts bin b (n records, n <= LC) with T threads and writes it out.
+template <int T, int LC>
+__device__ void bin_sort_one(const SortArgs& a, const BucketArgs& bk, int b, int n, const BinLds<T / kWave>& L) {
+  constexpr int kBinThreads = T;
+  constexpr int kBinWaves = T / kWave;
   const int cap = bk.cap;
-  int64_t* s_key = reinterpret_cast<int64_t*>(smem);
-  int32_t* s_pos = reinterpret_cast<int32_t*>(smem + bin_align(8 * size_t(cap)));
-  uint16_t* s_rec = reinterpret_cast<uint16_t*>(smem + bin_align(8 * size_t(cap)) + bin_align(4 * size_t(cap)));
-  BinFixed* F = reinterpret_cast<BinFixed*>(smem + bin_align(8 * size_t(cap)) + bin_align(4 * size_t(cap)) +
-                                            bin_align(2 * size_t(cap)));
+  const int32_t* tw = a.tie_wf;
+  int64_t* s_key = L.key;
+  int32_t* s_pos = L.pos;
+  uint16_t* s_rec = L.rec;
+  int32_t* s_wf = L.wf;
+  BinFixed<kBinWaves>* F = L.F;
   const int tid = threadIdx.x;
   const int wv = tid / kWave;
   const int ln = lane_id();
-  const int b = blockIdx.x;
-  Ctrl* ctrl = a.ctrl;
-  const uint32_t status = ctrl->status | ctrl->status_sweep;
-  const uint32_t overflow = ctrl->bucket_overflow;
-  RangeLanes rl;
-  if (b == 0) rl = load_range_lanes(ctrl, a.levels != 0);
   uint32_t before = 0, total = 0;
   for (int i = tid; i < bk.nb; i += kBinThreads) {
     uint32_t c = bk.cnt[i];
@@ -810,32 +850,23 @@ __global__ __launch_bounds__(kBinThreads) void k_bin_sort(SortArgs a, BucketArgs
     total += c;
     before += i < b ? c : 0u;
   }
-  if (status) {
-    if (b == 0 && tid == 0) publish_status(a.host, status, 0, 0, 0, 0, 0u);
-    return;
-  }
-  if (b == 0) {
-    settle_range(rl, ctrl, F->range, true, a.levels != 0);
-    if (tid == 0) publish_range(a.host, overflow ? kStatusTiled : 0u, F->range);
-  }
-  if (overflow) return;
-  const uint32_t nraw = bk.cnt[b];
-  const int n = int(nraw < uint32_t(cap) ? nraw : uint32_t(cap));
   const BucketSlot* rec = bk.slot + int64_t(b) * cap;
   // item j of lane l of wave w: record w * C + j * 64 + l
   const int J = (n + kBinThreads - 1) / kBinThreads;
   const int C = J * kWave;
   int64_t key[kBinJ];
-  int32_t pos[kBinJ];
+  int32_t pos[kBinJ], wfj[kBinJ];
   int64_t kmin = INT64_MAX, kmax = INT64_MIN;
 #pragma unroll
   for (int j = 0; j < kBinJ; ++j) {
     const int i = wv * C + j * kWave + ln;
     key[j] = 0;
     pos[j] = 0;
+    wfj[j] = 0;
     if (j < J && i < n) {
       key[j] = rec[i].key;
       pos[j] = rec[i].pos;
+      if (tw) wfj[j] = tw[pos[j]];
       kmin = key[j] < kmin ? key[j] : kmin;
       kmax = key[j] > kmax ? key[j] : kmax;
     }
@@ -920,6 +951,7 @@ __global__ __launch_bounds__(kBinThreads) void k_bin_sort(SortArgs a, BucketArgs
     s_key[st + at[j]] = key[j];
     s_pos[st + at[j]] = pos[j];
     s_rec[st + at[j]] = uint16_t(wv * C + j * kWave + ln);
+    if (tw) s_wf[st + at[j]] = wfj[j];
   }
   if (tid == 0) F->ncrowd = 0;
   __syncthreads();
@@ -942,9 +974,17 @@ __global__ __launch_bounds__(kBinThreads) void k_bin_sort(SortArgs a, BucketArgs
     const int st = int(span[j] & 0xFFFFu), en = int(span[j] >> 16);
     if (en - st > kBinRun) continue;
     uint32_t r = uint32_t(st);
-    for (int q = st; q < en; ++q) {
-      const int64_t kq = s_key[q];
-      r += (kq < key[j]) | ((kq == key[j]) & (s_pos[q] < pos[j]));
+    if (tw) {
+      for (int q = st; q < en; ++q) {
+        const int64_t kq = s_key[q];
+        const int32_t wq = s_wf[q];
+        r += (kq < key[j]) | ((kq == key[j]) & ((wq < wfj[j]) | ((wq == wfj[j]) & (s_pos[q] < pos[j]))));
+      }
+    } else {
+      for (int q = st; q < en; ++q) {
+        const int64_t kq = s_key[q];
+        r += (kq < key[j]) | ((kq == key[j]) & (s_pos[q] < pos[j]));
+      }
     }
     at[j] = r;
   }
@@ -963,12 +1003,12 @@ __global__ __launch_bounds__(kBinThreads) void k_bin_sort(SortArgs a, BucketArgs
   // the crowded sub-buckets (other ranges of LDS than the moves above)
   const int ncrowd = F->ncrowd;
   for (int c = 0; c < ncrowd; ++c) {
-    const uint32_t sp = F->crowd[c];
-    const int st = int(sp & 0xFFFFu);
-    bin_bitonic(s_key + st, s_pos + st, s_rec + st, int(sp >> 16) - st);
+    const uint32_t cs = F->crowd[c];
+    const int st = int(cs & 0xFFFFu);
+    bin_bitonic(s_key + st, s_pos + st, s_rec + st, s_wf ? s_wf + st : nullptr, int(cs >> 16) - st);
   }
   __syncthreads();
-  const int nbn = R >= kBinMinReady ? bins_for(R) : 0;
+  const int nbn = R >= a.split_min ? bins_for(R) : 0;
   for (int r = tid; r < n; r += kBinThreads) {
     const int64_t g = int64_t(before) + r;
     const int64_t k = s_key[r];
@@ -987,6 +1027,64 @@ __global__ __launch_bounds__(kBinThreads) void k_bin_sort(SortArgs a, BucketArgs
     __hip_atomic_store(&a.host->split_nb, uint32_t(nbn), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+// One workgroup per bin; bins of more than kBinCap records are left to
+// k_bin_sort_big.  Workgroup 0 settles and publishes the status and range.
+__global__ __launch_bounds__(kBinThreads) void k_bin_sort(SortArgs a, BucketArgs bk) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int NW = kBinThreads / kWave;
+  const BinLds<NW> L = carve_bin<NW>(smem, kBinCap, a.tie_wf != nullptr);
+  const int b = blockIdx.x;
+  Ctrl* ctrl = a.ctrl;
+  const uint32_t status = ctrl->status | ctrl->status_sweep;
+  const uint32_t overflow = ctrl->bucket_overflow;
+  RangeLanes rl;
+  if (b == 0) rl = load_range_lanes(ctrl, a.levels != 0);
+  if (status) {
+    if (b == 0 && threadIdx.x == 0) publish_status(a.host, status, 0, 0, 0, 0, 0u);
+    return;
+  }
+  if (b == 0) {
+    settle_range(rl, ctrl, L.F->range, true, a.levels != 0);
+    if (threadIdx.x == 0) publish_range(a.host, overflow ? kStatusTiled : 0u, L.F->range);
+  }
+  if (overflow) return;
+  const uint32_t nraw = bk.cnt[b];
+  const int n = int(nraw < uint32_t(bk.cap) ? nraw : uint32_t(bk.cap));
+  if (n > kBinCap) return;
+  bin_sort_one<kBinThreads, kBinCap>(a, bk, b, n, L);
+}
+
+// The bins of more than kBinCap records: every workgroup lists them in bin
+// order and takes every gridDim-th.
+constexpr int kBinBigGroups = 64;
+
+__global__ __launch_bounds__(kBinBigThreads) void k_bin_sort_big(SortArgs a, BucketArgs bk) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int NW = kBinBigThreads / kWave;
+  const BinLds<NW> L = carve_bin<NW>(smem, kBinBigCap, a.tie_wf != nullptr);
+  __shared__ int32_t s_big[kBinMax];
+  __shared__ int s_nbig;
+  Ctrl* ctrl = a.ctrl;
+  if ((ctrl->status | ctrl->status_sweep) != 0 || ctrl->bucket_overflow != 0) return;
+  int nbig = 0;
+  for (int i0 = 0; i0 < bk.nb; i0 += kBinBigThreads) {
+    const int i = i0 + int(threadIdx.x);
+    const uint32_t c = i < bk.nb ? bk.cnt[i] : 0u;
+    const bool big = c > uint32_t(kBinCap) && c <= uint32_t(bk.cap);
+    const uint32_t at = block_excl_scan(big ? 1u : 0u, L.F->tmp);
+    if (big) s_big[nbig + int(at)] = i;
+    if (threadIdx.x == kBinBigThreads - 1) s_nbig = nbig + int(at) + (big ? 1 : 0);
+    __syncthreads();
+    nbig = s_nbig;
+    __syncthreads();
+  }
+  for (int k = int(blockIdx.x); k < nbig; k += int(gridDim.x)) {
+    const int b = s_big[k];
+    bin_sort_one<kBinBigThreads, kBinBigCap>(a, bk, b, int(bk.cnt[b]), L);
+    __syncthreads();
+  }
+}
+
 // The next pass's splitters from the output of the tiled or bucketed sort
 // (one workgroup; R from the control block the sort settled).
 __global__ __launch_bounds__(kSortThreads) void k_splitters(SortArgs a) {
@@ -996,7 +1094,7 @@ __global__ __launch_bounds__(kSortThreads) void k_splitters(SortArgs a) {
   if (ctrl->bucket_overflow || int(ctrl->sort_npass) > a.passes_launched) return;
   const uint32_t bad = ctrl->status | ctrl->status_sweep;
   const int64_t R = ctrl->n_ready;
-  const int nbn = (bad == 0 && R >= kBinMinReady) ? bins_for(R) : 0;
+  const int nbn = (bad == 0 && R >= a.split_min) ? bins_for(R) : 0;
   for (int q = threadIdx.x; q < nbn - 1; q += kSortThreads)
     a.split_next[q] = output_key(a, (int64_t(q) + 1) * R / nbn);
   if (threadIdx.x == 0)
@@ -1135,13 +1233,23 @@ hipError_t launch_bucket_sort(hipStream_t s, const SortArgs& a, const BucketArgs
 }
 
 hipError_t launch_bin_sort(hipStream_t s, const SortArgs& a, const BucketArgs& bk) {
-  hipLaunchKernelGGL(k_bin_sort, dim3(bk.nb), dim3(kBinThreads), bin_lds_bytes(bk.cap), s, a, bk);
+  hipLaunchKernelGGL(k_bin_sort, dim3(bk.nb), dim3(kBinThreads),
+                     bin_lds_bytes<kBinThreads / kWave>(kBinCap, a.tie_wf != nullptr), s, a, bk);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || bk.cap <= kBinCap) return e;
+  hipLaunchKernelGGL(k_bin_sort_big, dim3(kBinBigGroups), dim3(kBinBigThreads),
+                     bin_lds_bytes<kBinBigThreads / kWave>(kBinBigCap, a.tie_wf != nullptr), s, a, bk);
   return hipGetLastError();
 }
 
 hipError_t prepare_sort_kernels() {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bin_sort),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, int(bin_lds_bytes(kBinCap)));
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bin_sort),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     int(bin_lds_bytes<kBinThreads / kWave>(kBinCap, true)));
+  if (e != hipSuccess) return e;
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bin_sort_big),
+                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                             int(bin_lds_bytes<kBinBigThreads / kWave>(kBinBigCap, true)));
 }
 
 hipError_t launch_splitters(hipStream_t s, const SortArgs& a) {

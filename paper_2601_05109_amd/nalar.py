@@ -36,12 +36,21 @@ NALAR_MAX_INSTANCES = 1024
 NALAR_STATIC_MAX_NODES = 1 << 18       # largest snapshot of nalar_policy_pass_static
 NALAR_STATIC_MAX_WORKFLOWS = 1 << 18
 
+# why a graph-store pass was a full one (nalar_store_last_fallback)
+NALAR_STORE_FULL_DISABLED = 1
+NALAR_STORE_FULL_NO_STATE = 2
+NALAR_STORE_FULL_SHRUNK = 3
+NALAR_STORE_FULL_NO_SPLITTERS = 4
+NALAR_STORE_FULL_OVERFLOW = 5
+NALAR_STORE_FULL_ROUNDS = 6
+
 EXPORTED = ("nalar_policy_create", "nalar_policy_pass", "nalar_policy_destroy", "nalar_policy_decide",
             "nalar_policy_pass_static",
             "nalar_policy_last_error", "nalar_policy_set_timing", "nalar_policy_get_timing",
             "nalar_store_create", "nalar_store_destroy", "nalar_store_append", "nalar_store_complete",
             "nalar_store_set_workflows", "nalar_store_set_instances", "nalar_store_n_nodes",
-            "nalar_store_pass")
+            "nalar_store_pass", "nalar_store_set_incremental", "nalar_store_last_pass_incremental",
+            "nalar_store_last_fallback")
 
 
 class NalarPolicyConfig(ctypes.Structure):
@@ -128,6 +137,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.nalar_store_n_nodes.restype = I64
     lib.nalar_store_pass.argtypes = [H, I64, I64, U32, ctypes.POINTER(NalarResult)]
     lib.nalar_store_pass.restype = ctypes.c_int
+    lib.nalar_store_set_incremental.argtypes = [H, ctypes.c_int]
+    lib.nalar_store_set_incremental.restype = ctypes.c_int
+    lib.nalar_store_last_pass_incremental.argtypes = [H]
+    lib.nalar_store_last_pass_incremental.restype = ctypes.c_int
+    lib.nalar_store_last_fallback.argtypes = [H]
+    lib.nalar_store_last_fallback.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -212,6 +227,18 @@ def nalar_store_n_nodes(s: Optional[int]) -> int:
 
 def nalar_store_pass(s: int, now_us: int, migration_cost_us: int, policy: int, res: NalarResult) -> int:
     return load_library().nalar_store_pass(s, now_us, migration_cost_us, policy, ctypes.byref(res))
+
+
+def nalar_store_set_incremental(s: Optional[int], enable: int) -> int:
+    return load_library().nalar_store_set_incremental(s, enable)
+
+
+def nalar_store_last_pass_incremental(s: Optional[int]) -> int:
+    return int(load_library().nalar_store_last_pass_incremental(s))
+
+
+def nalar_store_last_fallback(s: Optional[int]) -> int:
+    return int(load_library().nalar_store_last_fallback(s))
 
 
 # ---------------------------------------------------------------- torch helpers
@@ -461,6 +488,18 @@ class Store:
     @property
     def n_nodes(self) -> int:
         return nalar_store_n_nodes(self.handle)
+
+    def set_incremental(self, enable: bool) -> int:
+        return nalar_store_set_incremental(self.handle, 1 if enable else 0)
+
+    @property
+    def last_pass_incremental(self) -> bool:
+        return nalar_store_last_pass_incremental(self.handle) == 1
+
+    @property
+    def last_fallback(self) -> int:
+        """0 after an incremental pass, else a NALAR_STORE_FULL_* reason."""
+        return nalar_store_last_fallback(self.handle)
 
     def run_pass(self, out: "DeviceResult", now_us: int, migration_cost_us: int, policy: int = 0) -> int:
         cr = out.c_struct()
