@@ -319,7 +319,9 @@ def run_dynamic(steps: int, reps: int, use_store: bool, log=None) -> dict:
     """The evolving map/reduce graph: each snapshot is uploaded (timed apart,
     not part of a pass), then passed once (the first pass over it, timed) and
     ``reps`` more times (median).  With ``use_store`` the snapshot reaches the
-    device-resident graph store as the delta from the previous one."""
+    device-resident graph store as the delta from the previous one, the
+    passes are the store's incremental ones, and every 25 steps a full pass
+    over the same store is timed beside them."""
     import numpy as np
     import torch
     from paper_2601_05109_amd import nalar, workloads as wl
@@ -376,9 +378,16 @@ def run_dynamic(steps: int, reps: int, use_store: bool, log=None) -> dict:
                 return R, 1e3 * e0.elapsed_time(e1)
 
             R, first_us = timed_pass()
+            inc = store.last_pass_incremental if store is not None else False
             reps_us = [timed_pass()[1] for _ in range(reps)]
             row = {"step": step, "n": N, "e": p.n_edges, "ready": R, "first_us": first_us,
                    "us": statistics.median(reps_us) if reps_us else first_us, "upload_ms": up_ms}
+            if store is not None:
+                row["incremental"] = inc
+                if step % 25 == 0 and step > 0:  # a full pass over the same store, for comparison
+                    store.set_incremental(False)
+                    row["full_us"] = timed_pass()[1]
+                    store.set_incremental(True)
             if step % 25 == 0:  # per-kernel events on the library stream
                 pol.set_timing(True)
                 one_pass()
@@ -389,7 +398,8 @@ def run_dynamic(steps: int, reps: int, use_store: bool, log=None) -> dict:
             rows.append(row)
             if log and step % 10 == 0:
                 log(f"dynamic step {step}: N={N} R={R} first {first_us:.1f} us, repeat {row['us']:.1f} us "
-                    f"(upload {up_ms:.1f} ms)")
+                    f"(upload {up_ms:.1f} ms)" + (f", incremental {row['incremental']}" if store else "")
+                    + (f", full {row['full_us']:.1f} us" if "full_us" in row else ""))
     finally:
         if store is not None:
             store.close()
@@ -398,13 +408,23 @@ def run_dynamic(steps: int, reps: int, use_store: bool, log=None) -> dict:
     firsts = [r["first_us"] for r in later]
     reps_ = [r["us"] for r in later]
     last = rows[-1]
+    extra = {}
+    if use_store:
+        extra = {"passes": "incremental (the store recomputes the remaining path of the changed futures "
+                           "and their ancestors only)",
+                 "incremental_steps": sum(1 for r in later if r.get("incremental")),
+                 "full_pass_us": {str(r["step"]): round(r["full_us"], 1) for r in rows if "full_us" in r}}
+        if "full_us" in last:
+            extra["step_last_full_over_incremental"] = round(last["full_us"] / last["first_us"], 2)
     return {"workload": f"dynamic-stream: {rows[0]['n']} -> {last['n']} futures over {len(rows) - 1} steps, "
                         "ids not workflow-contiguous after step 0",
             "input": "device-resident graph store fed by deltas" if use_store else "whole snapshot uploaded every step",
             "steps": len(rows) - 1,
             "first_pass_us": {"p50": pct(firsts, 0.5), "p99": pct(firsts, 0.99)},
             "repeat_pass_us": {"p50": pct(reps_, 0.5), "p99": pct(reps_, 0.99)},
-            "step0_us": rows[0]["us"], "last_step": {k: last[k] for k in ("step", "n", "e", "ready", "first_us", "us")},
+            **extra,
+            "step0_us": rows[0]["us"],
+            "last_step": {k: last[k] for k in ("step", "n", "e", "ready", "first_us", "us", "full_us") if k in last},
             "last_step_kernels_us": next((r["kernels_us"] for r in reversed(rows) if "kernels_us" in r), None),
             "last_step_pass_roofline_frac": pass_alg_bytes(last["n"], last["e"], last["ready"], 256, 256)
             / (last["us"] * 1e-6) / 1e9 / HBM_PEAK_GBS,
@@ -689,7 +709,7 @@ def main() -> int:
         res["wide_mapreduce"] = leg_wide(args)
     if "dynamic" in legs:
         log_err("leg: dynamic stream")
-        dyn = run_dynamic(args.dyn_steps, args.dyn_reps, False, log_err)
+        dyn = run_dynamic(args.dyn_steps, args.dyn_reps, True, log_err)
         dyn.pop("per_step")
         res["dynamic"] = dyn
     if "traffic" in legs:

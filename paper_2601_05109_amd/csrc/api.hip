@@ -44,7 +44,7 @@ static __device__ __align__(256) char scratch[NALAR_STATIC_SCRATCH_BYTES];
 
 namespace {
 
-constexpr int kMaxTimed = 24;
+constexpr int kMaxTimed = 48;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -941,9 +941,11 @@ int nalar::policy_pass_incremental(nalar_policy* h, const nalar_problem* p, nala
   ia.stg_oslack = A.stg_oslack;
   NALAR_LAUNCH("inc_clear", launch_inc_clear(s, st.inA, (N + 31) / 32));
   NALAR_LAUNCH("inc_clear", launch_inc_clear(s, reinterpret_cast<uint32_t*>(st.ic), sizeof(IncCtrl) / 4));
-  NALAR_LAUNCH("inc_closure", launch_inc_closure(s, ia, h->cus));
+  e = launch_inc_closure(s, ia, h->cus, Timer::cb, &tm);
+  if (e != hipSuccess) return hip_fail(h, e, "inc_closure");
   NALAR_LAUNCH("inc_scan", launch_inc_scan(s, ia, h->cus));
-  NALAR_LAUNCH("inc_sweep", launch_inc_sweep(s, ia, h->cus));
+  e = launch_inc_sweep(s, ia, h->cus, Timer::cb, &tm);
+  if (e != hipSuccess) return hip_fail(h, e, "inc_sweep");
   NALAR_LAUNCH("inc_ready", launch_inc_ready(s, ia, h->cus));
   as.bcnt_clean[nxt] = true;
 

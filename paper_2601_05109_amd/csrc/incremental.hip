@@ -40,7 +40,7 @@ namespace {
 
 constexpr int kIncThreads = 256;
 constexpr int kIncHeavy = 64;     // more dependencies: one workgroup expands the future
-constexpr int kScanPer = 4;       // consecutive futures per thread in the scan
+constexpr int kScanPer = 8;       // consecutive futures per thread in the scan
 constexpr int kReadyPer = 4;      // ready futures per thread and chunk in the ready kernel
 
 __device__ inline bool bit_set_new(uint32_t* bits, int32_t v) {
@@ -64,6 +64,39 @@ __device__ inline void push_round(int32_t* list, uint32_t* cnt, int r, int32_t v
   if (r > kIncRounds) return;  // cannot happen: rounds past the last are never appended to
   const uint32_t at = round_base(cnt, r) + atomicAdd(&cnt[r], 1u);
   list[at] = v;
+}
+
+// Appends the lanes' futures with one atomic per workgroup: thread t holds the
+// futures first + j for the set bits j of mask (every thread of the
+// workgroup calls).  s_tmp holds one word per wave and two more.
+__device__ inline void push_block(uint32_t mask, int64_t first, int32_t* list, uint32_t* n, uint32_t base,
+                                  uint32_t* s_tmp) {
+  const int nw = int(blockDim.x) / kWave;
+  const int wv = int(threadIdx.x) / kWave;
+  const uint32_t k = uint32_t(__popc(mask));
+  const uint32_t inc = wave_incl_scan_u32(k);
+  if (lane_id() == kWave - 1) s_tmp[wv] = inc;
+  __syncthreads();
+  uint32_t off = 0, tot = 0;
+  for (int w = 0; w < nw; ++w) {
+    off += w < wv ? s_tmp[w] : 0u;
+    tot += s_tmp[w];
+  }
+  if (threadIdx.x == 0) s_tmp[nw] = tot ? atomicAdd(n, tot) : 0u;
+  __syncthreads();
+  uint32_t at = base + s_tmp[nw] + off + inc - k;
+  while (mask) {
+    const int j = __builtin_ctz(mask);
+    mask &= mask - 1;
+    list[at++] = int32_t(first + j);
+  }
+  __syncthreads();  // s_tmp is free again
+}
+
+// One future (or none) per thread, appended as push_block does.
+__device__ inline void push_block1(bool in, int32_t v, int32_t* list, uint32_t* n, uint32_t base,
+                                   uint32_t* s_tmp) {
+  push_block(in ? 1u : 0u, v, list, n, base, s_tmp);
 }
 
 __device__ inline void flag(Ctrl* c, uint32_t bits) {
@@ -105,6 +138,8 @@ struct WgQueue {
   int* n;
   int32_t* hq;      // [kIncHeavyQueue]
   int* hn;
+  uint32_t* tmp;    // [waves + 2] for push_block
+  int* htaken;      // heavy futures this workgroup kept (at most kIncHeavyKeep)
 };
 
 __device__ inline void wg_push(const WgQueue& wq, int32_t* list, uint32_t* cnt, int round, int32_t v) {
@@ -113,34 +148,80 @@ __device__ inline void wg_push(const WgQueue& wq, int32_t* list, uint32_t* cnt, 
   else push_round(list, cnt, round + 1, v);
 }
 
-__device__ inline void wg_push_heavy(const WgQueue& wq, int32_t* list, uint32_t* cnt, int round, int32_t v) {
-  const int at = atomicAdd(wq.hn, 1);
-  if (at < kIncHeavyQueue) wq.hq[at] = v;
-  else push_round(list, cnt, round + 1, v);
+// A workgroup expands heavy futures itself while its queue has room, but at
+// most kIncHeavyKeep of those with more than kIncHugeDeps dependencies (a
+// reduction over thousands of futures); the others go to the next round,
+// whose workgroups expand them side by side.
+constexpr int kIncHeavyKeep = 1;
+constexpr int kIncHugeDeps = 1024;
+
+__device__ inline void wg_push_heavy(const WgQueue& wq, int32_t* list, uint32_t* cnt, int round, int32_t v,
+                                     int32_t deg) {
+  if (deg <= kIncHugeDeps || atomicAdd(wq.htaken, 1) < kIncHeavyKeep) {
+    const int at = atomicAdd(wq.hn, 1);
+    if (at < kIncHeavyQueue) {
+      wq.hq[at] = v;
+      return;
+    }
+  }
+  push_round(list, cnt, round + 1, v);
 }
 
 // ------------------------------------------------------------------ closure
 
+// Marks the lanes' dependencies d (d < 0: none) with one atomic per group of
+// lanes holding the same d (a fan-in: many consumers of one future walking
+// at once), else one per lane; returns whether this lane made d a member
+// (one lane per d).  Every lane of the wave calls.
+__device__ inline bool wave_mark(uint32_t* bits, int32_t d) {
+  uint64_t pend = ballot(d >= 0);
+  bool fresh = false;
+  for (int it = 0; it < 2 && pend != 0; ++it) {
+    const int lead = __builtin_ctzll(pend);
+    const int32_t t = readlane_i32(d, lead);
+    const uint64_t grp = ballot(((pend >> lane_id()) & 1u) && d == t);
+    if (__popcll(grp) < 2) break;
+    if (lane_id() == lead) fresh = bit_set_new(bits, t);
+    pend &= ~grp;
+  }
+  if ((pend >> lane_id()) & 1u) fresh = bit_set_new(bits, d);
+  return fresh;
+}
+
 // u has just joined the closure: visit its dependencies, following the chain
-// while exactly one of them is new.
+// while exactly one of them is new.  Every lane of the wave calls (u = -1:
+// nothing), so that the lanes whose single dependency is one future mark it
+// together.
 __device__ void close_walk(const IncArgs& a, int32_t u, int round, const WgQueue& wq) {
-  while (u >= 0) {
-    const int32_t o0 = a.p.dep_off[u], o1 = a.p.dep_off[u + 1];
-    if (o1 - o0 > kIncHeavy) {
-      wg_push_heavy(wq, a.heavy, a.ic->ch, round, u);
-      return;
-    }
-    int32_t next = -1;
-    for (int32_t e = o0; e < o1; ++e) {
-      const int32_t d = a.p.dep_idx[e];
-      if (!dep_ok(a, u, d)) continue;
-      if (bit_set_new(a.inA, d)) {
-        join(a, d);
-        if (next < 0) next = d;
-        else wg_push(wq, a.light, a.ic->cl, round, d);
+  while (ballot(u >= 0) != 0) {
+    int32_t d1 = -1;  // the one dependency of a single-dependency future
+    if (u >= 0) {
+      const int32_t o0 = a.p.dep_off[u], o1 = a.p.dep_off[u + 1];
+      if (o1 - o0 > kIncHeavy) {
+        wg_push_heavy(wq, a.heavy, a.ic->ch, round, u, o1 - o0);
+        u = -1;
+      } else if (o1 - o0 == 1) {
+        const int32_t d = a.p.dep_idx[o0];
+        if (dep_ok(a, u, d)) d1 = d;
+        u = -1;
+      } else {
+        int32_t next = -1;
+        for (int32_t e = o0; e < o1; ++e) {
+          const int32_t d = a.p.dep_idx[e];
+          if (!dep_ok(a, u, d)) continue;
+          if (bit_set_new(a.inA, d)) {
+            join(a, d);
+            if (next < 0) next = d;
+            else wg_push(wq, a.light, a.ic->cl, round, d);
+          }
+        }
+        u = next;
       }
     }
-    u = next;
+    if (wave_mark(a.inA, d1)) {
+      join(a, d1);
+      u = d1;
+    }
   }
 }
 
@@ -169,26 +250,49 @@ __device__ void wg_drain(const WgQueue& wq, Walk walk, Expand expand) {
     __syncthreads();
     if (threadIdx.x == 0) *wq.n = n > int(blockDim.x) ? n - int(blockDim.x) : 0;
     __syncthreads();
-    if (mine >= 0) walk(mine);
+    walk(mine);  // every lane: the walks work wave by wave
   }
 }
 
-// A heavy member's dependencies visited by the whole workgroup.
+// A heavy member's dependencies visited by the whole workgroup; the new
+// members go to the next round, where every workgroup shares their walks.
 __device__ inline void close_expand(const IncArgs& a, int32_t u, int round, const WgQueue& wq) {
   const int32_t o0 = a.p.dep_off[u], o1 = a.p.dep_off[u + 1];
-  for (int32_t e = o0 + int32_t(threadIdx.x); e < o1; e += int32_t(blockDim.x)) {
-    const int32_t d = a.p.dep_idx[e];
-    if (!dep_ok(a, u, d)) continue;
-    if (bit_set_new(a.inA, d)) {
-      join(a, d);
-      close_walk(a, d, round, wq);
+  for (int32_t e0 = o0; e0 < o1; e0 += int32_t(blockDim.x)) {
+    const int32_t e = e0 + int32_t(threadIdx.x);
+    bool fresh = false;
+    int32_t d = -1;
+    if (e < o1) {
+      d = a.p.dep_idx[e];
+      if (dep_ok(a, u, d) && bit_set_new(a.inA, d)) {
+        join(a, d);
+        fresh = true;
+      }
     }
+    const int rn = round + 1 <= kIncRounds ? round + 1 : kIncRounds;
+    push_block1(fresh, d, a.light, &a.ic->cl[rn], round_base(a.ic->cl, rn), wq.tmp);
   }
 }
 
 // Every kernel leaves the snapshot alone once validation has failed (the
 // dependency offsets of the appended futures are trusted only then).
 __device__ inline bool invalid(const IncArgs& a) { return a.ctrl->status != 0; }
+
+// The appended futures' membership bits, one word per thread (every bit is
+// clear when this runs).
+__global__ __launch_bounds__(kIncThreads) void k_inc_mark(IncArgs a) {
+  if (invalid(a)) return;
+  const int64_t lo = a.n_prev, hi = a.p.N;
+  if (hi <= lo) return;
+  const int64_t w0 = lo >> 5, w1 = (hi - 1) >> 5;
+  for (int64_t w = w0 + int64_t(blockIdx.x) * kIncThreads + threadIdx.x; w <= w1;
+       w += int64_t(gridDim.x) * kIncThreads) {
+    const int64_t b0 = w * 32 > lo ? w * 32 : lo, b1 = w * 32 + 32 < hi ? w * 32 + 32 : hi;
+    const uint32_t hi_mask = b1 - w * 32 >= 32 ? 0xFFFFFFFFu : ((1u << uint32_t(b1 - w * 32)) - 1u);
+    const uint32_t lo_mask = ~((1u << uint32_t(b0 - w * 32)) - 1u);
+    a.inA[w] = hi_mask & lo_mask;
+  }
+}
 
 // Round 0 takes the seeds (completed ids of the log, then the appended
 // range); round r >= 1 the futures handed on: heavy ones expanded one per
@@ -200,26 +304,40 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_close(IncArgs a, int r) {
   const int64_t n_seed = r ? 0 : a.n_log + (n_app > 0 ? n_app : 0);
   if (nh == 0 && nl == 0 && n_seed == 0) return;
   __shared__ int32_t s_q[kIncQueue], s_hq[kIncHeavyQueue];
-  __shared__ int s_n, s_hn;
-  const WgQueue wq{s_q, &s_n, s_hq, &s_hn};
+  __shared__ int s_n, s_hn, s_htaken;
+  __shared__ uint32_t s_tmp[kIncThreads / kWave + 2];
+  const WgQueue wq{s_q, &s_n, s_hq, &s_hn, s_tmp, &s_htaken};
   if (threadIdx.x == 0) {
     s_n = 0;
     s_hn = 0;
+    s_htaken = 0;
   }
   __syncthreads();
-  for (int64_t i = int64_t(blockIdx.x) * kIncThreads + threadIdx.x; i < n_seed;
-       i += int64_t(gridDim.x) * kIncThreads) {
-    const int32_t v = i < a.n_log ? a.log[i] : int32_t(a.n_prev + (i - a.n_log));
-    if (v < 0 || int64_t(v) >= a.p.N) continue;  // counted by the completion kernel
-    if (bit_set_new(a.inA, v)) {
-      join(a, v);
-      close_walk(a, v, r, wq);
+  // every lane of a wave runs each iteration (the walks work wave by wave)
+  for (int64_t i0 = int64_t(blockIdx.x) * kIncThreads; i0 < n_seed; i0 += int64_t(gridDim.x) * kIncThreads) {
+    const int64_t i = i0 + threadIdx.x;
+    int32_t v = -1;
+    if (i < n_seed) {
+      if (i >= a.n_log) {  // appended: already members (k_inc_mark)
+        v = int32_t(a.n_prev + (i - a.n_log));
+        join(a, v);
+      } else {
+        const int32_t c = a.log[i];
+        // an id out of range is counted by the completion kernel
+        if (c >= 0 && int64_t(c) < a.p.N && bit_set_new(a.inA, c)) {
+          join(a, c);
+          v = c;
+        }
+      }
     }
+    close_walk(a, v, r, wq);
   }
   const uint32_t bh = round_base(a.ic->ch, r), bl = round_base(a.ic->cl, r);
   for (uint32_t h = blockIdx.x; h < nh; h += gridDim.x) close_expand(a, a.heavy[bh + h], r, wq);
-  for (uint32_t i = blockIdx.x * kIncThreads + threadIdx.x; i < nl; i += gridDim.x * kIncThreads)
-    close_walk(a, a.light[bl + i], r, wq);
+  for (uint32_t i0 = blockIdx.x * kIncThreads; i0 < nl; i0 += gridDim.x * kIncThreads) {
+    const uint32_t i = i0 + threadIdx.x;
+    close_walk(a, i < nl ? a.light[bl + i] : -1, r, wq);
+  }
   wg_drain(wq, [&](int32_t v) { close_walk(a, v, r, wq); }, [&](int32_t v) { close_expand(a, v, r, wq); });
 }
 
@@ -283,39 +401,78 @@ __device__ inline void push_wave(bool in, int32_t v, int32_t* list, uint32_t* n)
   if (in) list[b + lanes_below(m)] = v;
 }
 
+// Each thread takes kScanPer consecutive futures and issues the loads of all
+// of them together, stage by stage (offsets, membership and done flags; the
+// first dependency; its done flag and membership), so that the gathers of a
+// thread overlap; further dependencies (rare in the graphs this serves) are
+// visited one by one after.
 __global__ __launch_bounds__(kIncThreads) void k_inc_scan(IncArgs a) {
   if (invalid(a)) return;
+  __shared__ uint32_t s_tmp[kIncThreads / kWave + 2];
   const int64_t N = a.p.N;
   Pend pm, pc;
   uint32_t members = 0;
   const int64_t step = int64_t(gridDim.x) * kIncThreads * kScanPer;
   for (int64_t g0 = int64_t(blockIdx.x) * kIncThreads * kScanPer; g0 < N; g0 += step) {
+    const int64_t v0 = g0 + int64_t(threadIdx.x) * kScanPer;
+    int32_t o0[kScanPer], o1[kScanPer], d0[kScanPer];
+    bool in[kScanPer], dn[kScanPer], dd[kScanPer], din[kScanPer];
 #pragma unroll
     for (int j = 0; j < kScanPer; ++j) {
-      const int64_t v = g0 + int64_t(threadIdx.x) * kScanPer + j;
+      const int64_t v = v0 + j;
+      const bool ok = v < N;
+      o0[j] = ok ? a.p.dep_off[v] : 0;
+      o1[j] = ok ? a.p.dep_off[v + 1] : 0;
+      in[j] = ok && bit_get(a.inA, int32_t(v));
+      dn[j] = ok ? a.p.done[v] != 0 : true;
+    }
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+      const bool one = o1[j] > o0[j] && o1[j] - o0[j] <= kIncHeavy;
+      d0[j] = one ? a.p.dep_idx[o0[j]] : -1;
+    }
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+      const bool okd = d0[j] >= 0 && int64_t(d0[j]) < N;
+      dd[j] = okd ? a.p.done[d0[j]] != 0 : true;
+      din[j] = okd && bit_get(a.inA, d0[j]);
+    }
+    uint32_t rmask = 0;
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+      const int64_t v = v0 + j;
       bool ready = false, heavy = false;
       if (v < N) {
-        const bool in = bit_get(a.inA, int32_t(v));
-        members += in ? 1u : 0u;
-        const int32_t o0 = a.p.dep_off[v], o1 = a.p.dep_off[v + 1];
-        if (o1 - o0 > kIncHeavy) {
+        members += in[j] ? 1u : 0u;
+        if (o1[j] - o0[j] > kIncHeavy) {
           heavy = true;
         } else {
           bool blocked = false;
           int64_t rv = 0;
           bool have_rv = false;
-          for (int32_t e = o0; e < o1; ++e) {
-            const int32_t d = a.p.dep_idx[e];
+          for (int32_t e = o0[j]; e < o1[j]; ++e) {
+            int32_t d;
+            bool d_done, d_in;
+            if (e == o0[j]) {  // the first dependency, loaded above
+              d = d0[j];
+              d_done = dd[j];
+              d_in = din[j];
+            } else {
+              d = a.p.dep_idx[e];
+              const bool okd = d >= 0 && int64_t(d) < N;
+              d_done = okd ? a.p.done[d] != 0 : true;
+              d_in = okd && bit_get(a.inA, d);
+            }
             if (d < 0 || int64_t(d) >= N) continue;  // reported by the closure or an earlier pass
-            blocked |= a.p.done[d] == 0;
-            if (in) {
+            blocked |= !d_done;
+            if (in[j]) {
               if (d != pc.d) {
                 flush_cnt(a.cntA, pc);
                 pc.d = d;
                 pc.v = 0;
               }
               pc.v += 1;
-            } else if (bit_get(a.inA, d)) {
+            } else if (d_in) {
               if (!have_rv) {
                 rv = a.rem[v];
                 have_rv = true;
@@ -328,12 +485,13 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_scan(IncArgs a) {
               pm.v = rv > pm.v ? rv : pm.v;
             }
           }
-          ready = a.p.done[v] == 0 && !blocked;
+          ready = !dn[j] && !blocked;
         }
       }
-      push_wave(ready, int32_t(v), a.rlist, &a.ic->r_n);
-      push_wave(heavy, int32_t(v), a.heavy, &a.ic->scan_heavy);
+      if (ready) rmask |= 1u << j;
+      push_wave(heavy, int32_t(v), a.heavy, &a.ic->scan_heavy);  // rare
     }
+    push_block(rmask, v0, a.rlist, &a.ic->r_n, 0u, s_tmp);
   }
   flush_wave_cnt(a.cntA, pc);
   flush_wave_max(a.mxA, pm);
@@ -371,36 +529,82 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_scan_heavy(IncArgs a) {
 
 // -------------------------------------------------------------------- sweep
 
+// One push of a finalised member: its rem into d's max, then d's count down
+// by k; returns the count before.  Every access to the maxima and counts in
+// the sweep is a device-scope atomic, so their values meet where such
+// atomics are coherent, and the only order needed is the max before the
+// count: the wait makes the max complete there before the count is touched,
+// so the member that sees the count reach zero (and then loads the max
+// atomically) sees every push.  No cache write-back or invalidation is
+// needed, since nothing passes through plain loads and stores.
+__device__ inline int32_t push_count(const IncArgs& a, int32_t d, int64_t r, int32_t k) {
+  __hip_atomic_fetch_max(&a.mxA[d], r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __asm__ __volatile__("s_waitcnt vmcnt(0)" ::: "memory");
+  return __hip_atomic_fetch_add(&a.cntA[d], -k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Pushes the lanes' rem r to their dependencies d (d < 0: none) with one
+// pair of atomics per group of lanes holding the same d (a fan-in), else one
+// pair per lane; returns whether this lane brought d's count to zero (one
+// lane per d).  Every lane of the wave calls.
+__device__ inline bool wave_push(const IncArgs& a, int32_t d, int64_t r) {
+  uint64_t pend = ballot(d >= 0);
+  bool zero = false;
+  for (int it = 0; it < 2 && pend != 0; ++it) {
+    const int lead = __builtin_ctzll(pend);
+    const int32_t t = readlane_i32(d, lead);
+    const bool in = ((pend >> lane_id()) & 1u) && d == t;
+    const uint64_t grp = ballot(in);
+    const int n = __popcll(grp);
+    if (n < 2) break;
+    const int64_t m = wave_max_i64(in ? r : INT64_MIN);
+    if (lane_id() == lead) zero = push_count(a, t, m, n) == n;
+    pend &= ~grp;
+  }
+  if ((pend >> lane_id()) & 1u) zero = push_count(a, d, r, 1) == 1;
+  return zero;
+}
+
 // u's closure consumers are all finalised: rem(u) = est' + max, pushed to its
 // dependencies; a dependency whose count reaches zero is finalised next (by
-// this thread if it is the first, else in the next round).
+// this lane if it is the first, else through the workgroup's queue).  Every
+// lane of the wave calls (u = -1: nothing).
 __device__ void sweep_walk(const IncArgs& a, int32_t u, int round, uint32_t& fin, const WgQueue& wq) {
-  while (u >= 0) {
-    const int64_t est = a.p.done[u] ? 0 : a.p.est[u];
-    const int64_t m = __hip_atomic_load(&a.mxA[u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    int64_t r = est + m;
-    if (r > NALAR_REM_MAX) {
-      r = NALAR_REM_MAX + 1;
-      flag(a.ctrl, kStRange);
-    }
-    a.rem[u] = r;
-    ++fin;
-    const int32_t o0 = a.p.dep_off[u], o1 = a.p.dep_off[u + 1];
-    if (o1 - o0 > kIncHeavy) {
-      wg_push_heavy(wq, a.heavy, a.ic->sh, round, u);
-      return;
-    }
-    int32_t next = -1;
-    for (int32_t e = o0; e < o1; ++e) {
-      const int32_t d = a.p.dep_idx[e];
-      if (d < 0 || int64_t(d) >= a.p.N || d == u) continue;
-      atomicMax(reinterpret_cast<long long*>(&a.mxA[d]), (long long)r);
-      if (__hip_atomic_fetch_add(&a.cntA[d], -1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == 1) {
-        if (next < 0) next = d;
-        else wg_push(wq, a.light, a.ic->sl, round, d);
+  while (ballot(u >= 0) != 0) {
+    int32_t d1 = -1;  // the one dependency of a single-dependency future
+    int64_t r = 0;
+    if (u >= 0) {
+      const int64_t est = a.p.done[u] ? 0 : a.p.est[u];
+      const int64_t m = __hip_atomic_load(&a.mxA[u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      r = est + m;
+      if (r > NALAR_REM_MAX) {
+        r = NALAR_REM_MAX + 1;
+        flag(a.ctrl, kStRange);
+      }
+      a.rem[u] = r;
+      ++fin;
+      const int32_t o0 = a.p.dep_off[u], o1 = a.p.dep_off[u + 1];
+      if (o1 - o0 > kIncHeavy) {
+        wg_push_heavy(wq, a.heavy, a.ic->sh, round, u, o1 - o0);
+        u = -1;
+      } else if (o1 - o0 == 1) {
+        const int32_t d = a.p.dep_idx[o0];
+        if (d >= 0 && int64_t(d) < a.p.N && d != u) d1 = d;
+        u = -1;
+      } else {
+        int32_t next = -1;
+        for (int32_t e = o0; e < o1; ++e) {
+          const int32_t d = a.p.dep_idx[e];
+          if (d < 0 || int64_t(d) >= a.p.N || d == u) continue;
+          if (push_count(a, d, r, 1) == 1) {
+            if (next < 0) next = d;
+            else wg_push(wq, a.light, a.ic->sl, round, d);
+          }
+        }
+        u = next;
       }
     }
-    u = next;
+    if (wave_push(a, d1, r)) u = d1;
   }
 }
 
@@ -415,31 +619,41 @@ __device__ inline void add_fin(const IncArgs& a, uint32_t fin) {
 // walker's), one thread per word of the membership bits.
 __global__ __launch_bounds__(kIncThreads) void k_inc_front0(IncArgs a) {
   if (invalid(a)) return;
+  __shared__ uint32_t s_tmp[kIncThreads / kWave + 2];
   const int64_t words = (a.p.N + 31) / 32;
-  for (int64_t w = int64_t(blockIdx.x) * kIncThreads + threadIdx.x; w < words;
-       w += int64_t(gridDim.x) * kIncThreads) {
-    uint32_t bits = a.inA[w];
+  const int64_t step = int64_t(gridDim.x) * kIncThreads;
+  // the loop runs the same number of times on every thread of the workgroup
+  for (int64_t w0 = int64_t(blockIdx.x) * kIncThreads; w0 < words; w0 += step) {
+    const int64_t w = w0 + threadIdx.x;
+    uint32_t bits = w < words ? a.inA[w] : 0u;
+    uint32_t zmask = 0;
     while (bits) {
       const int b = __builtin_ctz(bits);
       bits &= bits - 1;
-      const int32_t v = int32_t(w * 32 + b);
-      if (a.cntA[v] == 0) push_round(a.light, a.ic->sl, 0, v);
+      if (a.cntA[w * 32 + b] == 0) zmask |= 1u << b;
     }
+    push_block(zmask, w * 32, a.light, &a.ic->sl[0], 0u, s_tmp);
   }
 }
 
 // A finalised heavy member's rem pushed to its dependencies by the whole
-// workgroup.
+// workgroup; the dependencies it finalises go to the next round, where every
+// workgroup shares their walks.
 __device__ inline void sweep_expand(const IncArgs& a, int32_t u, int round, uint32_t& fin, const WgQueue& wq) {
   const int64_t ru = a.rem[u];
   const int32_t o0 = a.p.dep_off[u], o1 = a.p.dep_off[u + 1];
-  for (int32_t e = o0 + int32_t(threadIdx.x); e < o1; e += int32_t(blockDim.x)) {
-    const int32_t d = a.p.dep_idx[e];
-    if (d < 0 || int64_t(d) >= a.p.N || d == u) continue;
-    atomicMax(reinterpret_cast<long long*>(&a.mxA[d]), (long long)ru);
-    if (__hip_atomic_fetch_add(&a.cntA[d], -1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == 1)
-      sweep_walk(a, d, round, fin, wq);
+  const int rn = round + 1 <= kIncRounds ? round + 1 : kIncRounds;
+  for (int32_t e0 = o0; e0 < o1; e0 += int32_t(blockDim.x)) {
+    const int32_t e = e0 + int32_t(threadIdx.x);
+    bool zero = false;
+    int32_t d = -1;
+    if (e < o1) {
+      d = a.p.dep_idx[e];
+      if (d >= 0 && int64_t(d) < a.p.N && d != u) zero = push_count(a, d, ru, 1) == 1;
+    }
+    push_block1(zero, d, a.light, &a.ic->sl[rn], round_base(a.ic->sl, rn), wq.tmp);
   }
+  (void)fin;
 }
 
 __global__ __launch_bounds__(kIncThreads) void k_inc_sweep(IncArgs a, int r) {
@@ -447,18 +661,22 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_sweep(IncArgs a, int r) {
   const uint32_t nh = a.ic->sh[r], nl = a.ic->sl[r];
   if (nh == 0 && nl == 0) return;
   __shared__ int32_t s_q[kIncQueue], s_hq[kIncHeavyQueue];
-  __shared__ int s_n, s_hn;
-  const WgQueue wq{s_q, &s_n, s_hq, &s_hn};
+  __shared__ int s_n, s_hn, s_htaken;
+  __shared__ uint32_t s_tmp[kIncThreads / kWave + 2];
+  const WgQueue wq{s_q, &s_n, s_hq, &s_hn, s_tmp, &s_htaken};
   if (threadIdx.x == 0) {
     s_n = 0;
     s_hn = 0;
+    s_htaken = 0;
   }
   __syncthreads();
   const uint32_t bh = round_base(a.ic->sh, r), bl = round_base(a.ic->sl, r);
   uint32_t fin = 0;
   for (uint32_t h = blockIdx.x; h < nh; h += gridDim.x) sweep_expand(a, a.heavy[bh + h], r, fin, wq);
-  for (uint32_t i = blockIdx.x * kIncThreads + threadIdx.x; i < nl; i += gridDim.x * kIncThreads)
-    sweep_walk(a, a.light[bl + i], r, fin, wq);
+  for (uint32_t i0 = blockIdx.x * kIncThreads; i0 < nl; i0 += gridDim.x * kIncThreads) {
+    const uint32_t i = i0 + threadIdx.x;
+    sweep_walk(a, i < nl ? a.light[bl + i] : -1, r, fin, wq);
+  }
   wg_drain(wq, [&](int32_t v) { sweep_walk(a, v, r, fin, wq); },
            [&](int32_t v) { sweep_expand(a, v, r, fin, wq); });
   add_fin(a, fin);
@@ -638,31 +856,47 @@ hipError_t launch_inc_clear(hipStream_t s, uint32_t* p, int64_t n) {
   return hipGetLastError();
 }
 
-hipError_t launch_inc_closure(hipStream_t s, const IncArgs& a, int cus) {
+constexpr const char* kCloseNames[kIncRounds] = {"inc_close_r0", "inc_close_r1", "inc_close_r2", "inc_close_r3",
+                                                  "inc_close_r4", "inc_close_r5", "inc_close_r6", "inc_close_r7"};
+constexpr const char* kSweepNames[kIncRounds] = {"inc_sweep_r0", "inc_sweep_r1", "inc_sweep_r2", "inc_sweep_r3",
+                                                  "inc_sweep_r4", "inc_sweep_r5", "inc_sweep_r6", "inc_sweep_r7"};
+static_assert(kIncRounds == 8, "one name per round");
+
+hipError_t launch_inc_closure(hipStream_t s, const IncArgs& a, int cus, void (*mark)(void*, const char*),
+                              void* ctx) {
   const int64_t seeds = a.n_log + (a.p.N - a.n_prev);
-  hipLaunchKernelGGL(k_inc_close, dim3(inc_grid(seeds, 4096)), dim3(kIncThreads), 0, s, a, 0);
+  mark(ctx, "inc_mark");
+  hipLaunchKernelGGL(k_inc_mark, dim3(inc_grid((a.p.N - a.n_prev) / 32 + 2, 1024)), dim3(kIncThreads), 0, s, a);
   hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  mark(ctx, kCloseNames[0]);
+  hipLaunchKernelGGL(k_inc_close, dim3(inc_grid(seeds, 4096)), dim3(kIncThreads), 0, s, a, 0);
+  e = hipGetLastError();
   for (int r = 1; r <= kIncRounds - 1 && e == hipSuccess; ++r) {
-    hipLaunchKernelGGL(k_inc_close, dim3(4 * cus), dim3(kIncThreads), 0, s, a, r);
+    mark(ctx, kCloseNames[r]);
+    hipLaunchKernelGGL(k_inc_close, dim3(r < 2 ? 4 * cus : cus), dim3(kIncThreads), 0, s, a, r);
     e = hipGetLastError();
   }
   return e;
 }
 
 hipError_t launch_inc_scan(hipStream_t s, const IncArgs& a, int cus) {
-  hipLaunchKernelGGL(k_inc_scan, dim3(inc_grid((a.p.N + kScanPer - 1) / kScanPer, 8 * cus)), dim3(kIncThreads),
-                     0, s, a);
+  hipLaunchKernelGGL(k_inc_scan, dim3(inc_grid((a.p.N + kScanPer - 1) / kScanPer, 16 * cus)),
+                     dim3(kIncThreads), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_inc_scan_heavy, dim3(2 * cus), dim3(kIncThreads), 0, s, a);
   return hipGetLastError();
 }
 
-hipError_t launch_inc_sweep(hipStream_t s, const IncArgs& a, int cus) {
+hipError_t launch_inc_sweep(hipStream_t s, const IncArgs& a, int cus, void (*mark)(void*, const char*),
+                            void* ctx) {
+  mark(ctx, "inc_front0");
   hipLaunchKernelGGL(k_inc_front0, dim3(inc_grid((a.p.N + 31) / 32, 8 * cus)), dim3(kIncThreads), 0, s, a);
   hipError_t e = hipGetLastError();
   for (int r = 0; r <= kIncRounds - 1 && e == hipSuccess; ++r) {
-    hipLaunchKernelGGL(k_inc_sweep, dim3(4 * cus), dim3(kIncThreads), 0, s, a, r);
+    mark(ctx, kSweepNames[r]);
+    hipLaunchKernelGGL(k_inc_sweep, dim3(r < 3 ? 4 * cus : cus), dim3(kIncThreads), 0, s, a, r);
     e = hipGetLastError();
   }
   return e;

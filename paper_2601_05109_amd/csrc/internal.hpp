@@ -247,9 +247,10 @@ struct IncArgs {
 size_t inc_ready_lds(int64_t M);
 hipError_t prepare_inc_kernels();
 hipError_t launch_inc_clear(hipStream_t s, uint32_t* p, int64_t n_words);
-hipError_t launch_inc_closure(hipStream_t s, const IncArgs& a, int cus);
+// (mark(ctx, name) before each launch, for timing)
+hipError_t launch_inc_closure(hipStream_t s, const IncArgs& a, int cus, void (*mark)(void*, const char*), void* ctx);
 hipError_t launch_inc_scan(hipStream_t s, const IncArgs& a, int cus);
-hipError_t launch_inc_sweep(hipStream_t s, const IncArgs& a, int cus);
+hipError_t launch_inc_sweep(hipStream_t s, const IncArgs& a, int cus, void (*mark)(void*, const char*), void* ctx);
 hipError_t launch_inc_ready(hipStream_t s, const IncArgs& a, int cus);
 
 // The store's side of an incremental pass (defined in api.hip): its buffers,

@@ -20,6 +20,8 @@ import weakref
 from dataclasses import dataclass
 from typing import Optional
 
+_is_finalizing = sys.is_finalizing  # kept: sys may be cleared before late finalizers run
+
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libnalar_policy.so")
 
@@ -394,7 +396,9 @@ class Policy:
         self.close()
 
     def __del__(self):
-        if sys.is_finalizing():  # the runtime may be going away: leave it to process exit
+        # closed already, or the interpreter (and maybe the runtime) going away:
+        # leave it to process exit (module globals such as sys may be gone)
+        if getattr(self, "handle", None) is None or _is_finalizing():
             return
         try:
             self.close()
@@ -520,7 +524,7 @@ class Store:
         self.close()
 
     def __del__(self):
-        if sys.is_finalizing():
+        if getattr(self, "handle", None) is None or _is_finalizing():
             return
         try:
             self.close()
