@@ -865,6 +865,22 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
 
 void nalar::policy_split_any(nalar_policy* h, bool on) { h->split_any = on; }
 
+int nalar::policy_reserve(nalar_policy* h, int64_t N, int64_t W) {
+  const Arena& a = h->own.ar;
+  if (!a.base || (N <= a.capN && W <= a.capW)) return NALAR_OK;  // the first pass sizes it
+  hipError_t e = hipSetDevice(h->device);
+  if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+  // the incremental pass's bins at the last pass's ready count, kept at least
+  BucketArgs bk{};
+  bk.bins = 1;
+  bk.nb = h->split_nb > 0 ? h->split_nb : 0;
+  bk.cap = bk.nb > 0 ? bin_cap_for(h->hint_ready, bk.nb) : 0;
+  const int64_t B = a.capB > bk.nb ? a.capB : bk.nb;
+  const int64_t rec = bk.nb > 0 ? records_of(bk) : 0;
+  const int64_t Rec = a.capRec > rec ? a.capRec : rec;
+  return ensure_capacity(h, N, W, B, Rec);
+}
+
 // The incremental pass over the graph store (the kernels in incremental.hip):
 // the appended futures validated, the closure of the changed futures and its
 // sweep, readiness of every future, the ready futures binned by the previous
@@ -927,6 +943,7 @@ int nalar::policy_pass_incremental(nalar_policy* h, const nalar_problem* p, nala
   ia.n_log = st.n_log;
   ia.rem = st.rem;
   ia.inA = st.inA;
+  ia.dnb = st.dnb;
   ia.mxA = st.mxA;
   ia.cntA = st.cntA;
   ia.light = st.light;
@@ -939,7 +956,7 @@ int nalar::policy_pass_incremental(nalar_policy* h, const nalar_problem* p, nala
   ia.bk_clear = A.bcnt[nxt];
   ia.bk_clear_n = A.capB > 0 ? A.capB : 0;
   ia.stg_oslack = A.stg_oslack;
-  NALAR_LAUNCH("inc_clear", launch_inc_clear(s, st.inA, (N + 31) / 32));
+  NALAR_LAUNCH("inc_pack", launch_inc_pack(s, ia));
   NALAR_LAUNCH("inc_clear", launch_inc_clear(s, reinterpret_cast<uint32_t*>(st.ic), sizeof(IncCtrl) / 4));
   e = launch_inc_closure(s, ia, h->cus, Timer::cb, &tm);
   if (e != hipSuccess) return hip_fail(h, e, "inc_closure");

@@ -434,7 +434,7 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_scan(IncArgs a) {
 #pragma unroll
     for (int j = 0; j < kScanPer; ++j) {
       const bool okd = d0[j] >= 0 && int64_t(d0[j]) < N;
-      dd[j] = okd ? a.p.done[d0[j]] != 0 : true;
+      dd[j] = okd ? bit_get(a.dnb, d0[j]) : true;
       din[j] = okd && bit_get(a.inA, d0[j]);
     }
     uint32_t rmask = 0;
@@ -460,7 +460,7 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_scan(IncArgs a) {
             } else {
               d = a.p.dep_idx[e];
               const bool okd = d >= 0 && int64_t(d) < N;
-              d_done = okd ? a.p.done[d] != 0 : true;
+              d_done = okd ? bit_get(a.dnb, d) : true;
               d_in = okd && bit_get(a.inA, d);
             }
             if (d < 0 || int64_t(d) >= N) continue;  // reported by the closure or an earlier pass
@@ -516,7 +516,7 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_scan_heavy(IncArgs a) {
     for (int32_t e = o0 + int32_t(threadIdx.x); e < o1; e += kIncThreads) {
       const int32_t d = a.p.dep_idx[e];
       if (d < 0 || int64_t(d) >= a.p.N) continue;
-      blocked |= a.p.done[d] == 0;
+      blocked |= !bit_get(a.dnb, d);
       if (in) atomicAdd(&a.cntA[d], 1);
       else if (bit_get(a.inA, d)) atomicMax(reinterpret_cast<long long*>(&a.mxA[d]), (long long)rv);
     }
@@ -574,7 +574,7 @@ __device__ void sweep_walk(const IncArgs& a, int32_t u, int round, uint32_t& fin
     int32_t d1 = -1;  // the one dependency of a single-dependency future
     int64_t r = 0;
     if (u >= 0) {
-      const int64_t est = a.p.done[u] ? 0 : a.p.est[u];
+      const int64_t est = bit_get(a.dnb, u) ? 0 : a.p.est[u];
       const int64_t m = __hip_atomic_load(&a.mxA[u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       r = est + m;
       if (r > NALAR_REM_MAX) {
@@ -827,6 +827,30 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_ready(IncArgs a) {
   }
 }
 
+// Word i of the membership bits cleared, and of the done bits packed from
+// the done flags of futures 32i .. 32i+31 (the gathers of dependencies' flags
+// then read 1/8 of the bytes, a bitmap that stays in the L2).
+__global__ __launch_bounds__(kIncThreads) void k_inc_pack(IncArgs a) {
+  const int64_t N = a.p.N, nw = (N + 31) / 32;
+  for (int64_t i = int64_t(blockIdx.x) * kIncThreads + threadIdx.x; i < nw; i += int64_t(gridDim.x) * kIncThreads) {
+    const int64_t v0 = 32 * i;
+    uint32_t bits = 0;
+    if (v0 + 32 <= N) {  // 32 flags in two aligned 16-byte loads (the array is 256-byte aligned)
+      const uint4* q = reinterpret_cast<const uint4*>(a.p.done + v0);
+      const uint4 x = q[0], y = q[1];
+      const uint32_t w[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) bits |= uint32_t(((w[k] >> (8 * b)) & 0xFFu) != 0u) << (4 * k + b);
+    } else {
+      for (int64_t v = v0; v < N; ++v) bits |= uint32_t(a.p.done[v] != 0) << uint32_t(v - v0);
+    }
+    a.inA[i] = 0;
+    a.dnb[i] = bits;
+  }
+}
+
 __global__ __launch_bounds__(kIncThreads) void k_inc_clear(uint32_t* p, int64_t n) {
   for (int64_t i = int64_t(blockIdx.x) * kIncThreads + threadIdx.x; i < n; i += int64_t(gridDim.x) * kIncThreads)
     p[i] = 0;
@@ -853,6 +877,13 @@ hipError_t prepare_inc_kernels() {
 hipError_t launch_inc_clear(hipStream_t s, uint32_t* p, int64_t n) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_inc_clear, dim3(inc_grid(n, 2048)), dim3(kIncThreads), 0, s, p, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_inc_pack(hipStream_t s, const IncArgs& a) {
+  const int64_t nw = (a.p.N + 31) / 32;
+  if (nw <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_inc_pack, dim3(inc_grid(nw, 2048)), dim3(kIncThreads), 0, s, a);
   return hipGetLastError();
 }
 

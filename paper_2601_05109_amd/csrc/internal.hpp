@@ -230,7 +230,8 @@ struct IncArgs {
   const int32_t* log;            // [n_log] ids completed since the last pass
   int64_t n_log;
   int64_t* rem;                  // [N] remaining critical path, kept across passes
-  uint32_t* inA;                 // [ceil(N/32)] closure membership bits (zero on entry)
+  uint32_t* inA;                 // [ceil(N/32)] closure membership bits (cleared by the pack)
+  uint32_t* dnb;                 // [ceil(N/32)] done flags as bits (written by the pack)
   int64_t* mxA;                  // [N] max rem over consumers (closure members)
   int32_t* cntA;                 // [N] closure consumers not yet finalised (members)
   int32_t* light;                // [N] per-round lists
@@ -247,6 +248,8 @@ struct IncArgs {
 size_t inc_ready_lds(int64_t M);
 hipError_t prepare_inc_kernels();
 hipError_t launch_inc_clear(hipStream_t s, uint32_t* p, int64_t n_words);
+// Clears the membership bits and packs the done flags into bits.
+hipError_t launch_inc_pack(hipStream_t s, const IncArgs& a);
 // (mark(ctx, name) before each launch, for timing)
 hipError_t launch_inc_closure(hipStream_t s, const IncArgs& a, int cus, void (*mark)(void*, const char*), void* ctx);
 hipError_t launch_inc_scan(hipStream_t s, const IncArgs& a, int cus);
@@ -266,6 +269,7 @@ struct IncStore {
   int64_t n_log;
   int64_t* rem;
   uint32_t* inA;
+  uint32_t* dnb;
   int64_t* mxA;
   int32_t* cntA;
   int32_t* light;
@@ -276,6 +280,10 @@ struct IncStore {
 int policy_pass_incremental(nalar_policy* h, const nalar_problem* p, nalar_result* r, const IncStore& st);
 // Full passes of the store leave splitters for any number of ready futures.
 void policy_split_any(nalar_policy* h, bool on);
+// Grows the handle's pass arena ahead of a pass over N futures of W
+// workflows (geometrically, like the pass itself), so that a store reallocates
+// while taking in its deltas rather than inside a pass.
+int policy_reserve(nalar_policy* h, int64_t N, int64_t W);
 
 // Handle accessors for the graph store (store.hip), defined in api.hip.
 hipStream_t policy_stream(const nalar_policy* h);

@@ -45,6 +45,7 @@ struct nalar_store {
   int64_t capI = 0;             // futures the incremental buffers hold
   int64_t* rem = nullptr;       // [capI]
   uint32_t* inA = nullptr;      // [capI / 32 + 1]
+  uint32_t* dnb = nullptr;      // [capI / 32 + 1] done flags as bits (pass scratch)
   int64_t* mxA = nullptr;
   int32_t* cntA = nullptr;
   int32_t* light = nullptr;
@@ -147,6 +148,7 @@ int ensure_incremental(nalar_store* st) {
   int64_t c;
   c = st->capI; e = grow(st->rem, c, nc, st->rem_valid ? st->n_prev : 0, s);
   if (e == hipSuccess) { c = st->capI / 32 + 1; e = grow(st->inA, c, nc / 32 + 1, 0, s); }
+  if (e == hipSuccess) { c = st->capI / 32 + 1; e = grow(st->dnb, c, nc / 32 + 1, 0, s); }
   if (e == hipSuccess) { c = st->capI; e = grow(st->mxA, c, nc, 0, s); }
   if (e == hipSuccess) { c = st->capI; e = grow(st->cntA, c, nc, 0, s); }
   if (e == hipSuccess) { c = st->capI; e = grow(st->light, c, nc, 0, s); }
@@ -190,7 +192,7 @@ void nalar_store_destroy(nalar_store* st) {
                   static_cast<void*>(st->done), static_cast<void*>(st->loc), static_cast<void*>(st->dep_off),
                   static_cast<void*>(st->dep_idx), static_cast<void*>(st->deadline),
                   static_cast<void*>(st->inst_type), static_cast<void*>(st->inst_load),
-                  static_cast<void*>(st->inst_speed), static_cast<void*>(st->rem), static_cast<void*>(st->inA),
+                  static_cast<void*>(st->inst_speed), static_cast<void*>(st->rem), static_cast<void*>(st->inA), static_cast<void*>(st->dnb),
                   static_cast<void*>(st->mxA), static_cast<void*>(st->cntA), static_cast<void*>(st->light),
                   static_cast<void*>(st->heavy), static_cast<void*>(st->rlist), static_cast<void*>(st->ic),
                   static_cast<void*>(st->log)})
@@ -254,7 +256,11 @@ int nalar_store_append(nalar_store* st, int64_t n_new, int64_t n_new_edges, cons
   st->N = need;
   st->E = E + n_new_edges;
   st->contiguous = st->contiguous && (flags & NALAR_WF_CONTIGUOUS);
-  return NALAR_OK;
+  // the per-future buffers of the next pass grow here, with the store, and
+  // not inside the pass
+  int rc = ensure_incremental(st);
+  if (rc == NALAR_OK) rc = policy_reserve(st->h, st->N, st->W);
+  return rc;
 }
 
 int nalar_store_complete(nalar_store* st, int64_t n, const int32_t* ids) {
@@ -357,7 +363,7 @@ int nalar_store_pass(nalar_store* st, int64_t now_us, int64_t migration_cost_us,
   else if (!st->rem_valid || !r) st->last_fallback = NALAR_STORE_FULL_NO_STATE;
   else if (st->W < st->W_prev || st->M < st->M_prev) st->last_fallback = NALAR_STORE_FULL_SHRUNK;
   else {
-    const IncStore is{st->n_prev, st->log, st->n_log, st->rem, st->inA, st->mxA, st->cntA,
+    const IncStore is{st->n_prev, st->log, st->n_log, st->rem, st->inA, st->dnb, st->mxA, st->cntA,
                       st->light, st->heavy, st->rlist, st->ic};
     rc = policy_pass_incremental(st->h, &p, r, is);
     if (!inc_fallback(rc)) st->last_incremental = 1;
