@@ -425,8 +425,12 @@ def run_dynamic(steps: int, reps: int, use_store: bool, log=None) -> dict:
             **extra,
             "step0_us": rows[0]["us"],
             "last_step": {k: last[k] for k in ("step", "n", "e", "ready", "first_us", "us", "full_us") if k in last},
-            "last_step_kernels_us": next((r["kernels_us"] for r in reversed(rows) if "kernels_us" in r), None),
+            # per-kernel events of a pass repeated over the last snapshot (no change since the
+            # pass before it: for the store, an empty closure)
+            "last_step_repeat_kernels_us": next((r["kernels_us"] for r in reversed(rows) if "kernels_us" in r), None),
             "last_step_pass_roofline_frac": pass_alg_bytes(last["n"], last["e"], last["ready"], 256, 256)
+            / (last["first_us"] * 1e-6) / 1e9 / HBM_PEAK_GBS,
+            "last_step_repeat_pass_roofline_frac": pass_alg_bytes(last["n"], last["e"], last["ready"], 256, 256)
             / (last["us"] * 1e-6) / 1e9 / HBM_PEAK_GBS,
             "per_step": [{k: (round(v, 2) if isinstance(v, float) else v) for k, v in r.items()} for r in rows],
             "wall_s": time.perf_counter() - t_all}
