@@ -70,7 +70,7 @@ __device__ inline void push_round(int32_t* list, uint32_t* cnt, int r, int32_t v
 // futures first + j for the set bits j of mask (every thread of the
 // workgroup calls).  s_tmp holds one word per wave and two more.
 __device__ inline void push_block(uint32_t mask, int64_t first, int32_t* list, uint32_t* n, uint32_t base,
-                                  uint32_t* s_tmp) {
+                                  uint32_t* s_tmp, int64_t stride = 1) {
   const int nw = int(blockDim.x) / kWave;
   const int wv = int(threadIdx.x) / kWave;
   const uint32_t k = uint32_t(__popc(mask));
@@ -88,7 +88,7 @@ __device__ inline void push_block(uint32_t mask, int64_t first, int32_t* list, u
   while (mask) {
     const int j = __builtin_ctz(mask);
     mask &= mask - 1;
-    list[at++] = int32_t(first + j);
+    list[at++] = int32_t(first + int64_t(j) * stride);
   }
   __syncthreads();  // s_tmp is free again
 }
@@ -401,11 +401,14 @@ __device__ inline void push_wave(bool in, int32_t v, int32_t* list, uint32_t* n)
   if (in) list[b + lanes_below(m)] = v;
 }
 
-// Each thread takes kScanPer consecutive futures and issues the loads of all
-// of them together, stage by stage (offsets, membership and done flags; the
-// first dependency; its done flag and membership), so that the gathers of a
-// thread overlap; further dependencies (rare in the graphs this serves) are
-// visited one by one after.
+// A workgroup takes kScanPer x kIncThreads consecutive futures, thread t the
+// futures t, t + kIncThreads, ... of them (so every load of a wave is
+// coalesced), and issues the loads of all of them together, stage by stage
+// (offsets, membership and done flags; the first dependency; its done flag
+// and membership), so that the gathers of a thread overlap; further
+// dependencies (rare in the graphs this serves) are visited one by one after.
+// A thread's futures lie kIncThreads apart, so a run of futures with one
+// common dependency (the children of a hub) still merges its pushes per lane.
 __global__ __launch_bounds__(kIncThreads) void k_inc_scan(IncArgs a) {
   if (invalid(a)) return;
   __shared__ uint32_t s_tmp[kIncThreads / kWave + 2];
@@ -414,12 +417,12 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_scan(IncArgs a) {
   uint32_t members = 0;
   const int64_t step = int64_t(gridDim.x) * kIncThreads * kScanPer;
   for (int64_t g0 = int64_t(blockIdx.x) * kIncThreads * kScanPer; g0 < N; g0 += step) {
-    const int64_t v0 = g0 + int64_t(threadIdx.x) * kScanPer;
+    const int64_t v0 = g0 + int64_t(threadIdx.x);
     int32_t o0[kScanPer], o1[kScanPer], d0[kScanPer];
     bool in[kScanPer], dn[kScanPer], dd[kScanPer], din[kScanPer];
 #pragma unroll
     for (int j = 0; j < kScanPer; ++j) {
-      const int64_t v = v0 + j;
+      const int64_t v = v0 + int64_t(j) * kIncThreads;
       const bool ok = v < N;
       o0[j] = ok ? a.p.dep_off[v] : 0;
       o1[j] = ok ? a.p.dep_off[v + 1] : 0;
@@ -440,7 +443,7 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_scan(IncArgs a) {
     uint32_t rmask = 0;
 #pragma unroll
     for (int j = 0; j < kScanPer; ++j) {
-      const int64_t v = v0 + j;
+      const int64_t v = v0 + int64_t(j) * kIncThreads;
       bool ready = false, heavy = false;
       if (v < N) {
         members += in[j] ? 1u : 0u;
@@ -491,7 +494,7 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_scan(IncArgs a) {
       if (ready) rmask |= 1u << j;
       push_wave(heavy, int32_t(v), a.heavy, &a.ic->scan_heavy);  // rare
     }
-    push_block(rmask, v0, a.rlist, &a.ic->r_n, 0u, s_tmp);
+    push_block(rmask, v0, a.rlist, &a.ic->r_n, 0u, s_tmp, kIncThreads);
   }
   flush_wave_cnt(a.cntA, pc);
   flush_wave_max(a.mxA, pm);
@@ -773,10 +776,24 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_ready(IncArgs a) {
     for (int j = 0; j < kReadyPer; ++j)
       if (v[j] >= 0) rk[j] = atomicAdd(&s_cnt[bin[j]], 1u);
     __syncthreads();
-    for (int t = tid; t < nb; t += T) {
-      const uint32_t c = s_cnt[t];
-      s_base[t] = c ? add_agent(a.bk.cnt + t, c) : 0u;
-      s_cnt[t] = 0;
+    {  // one segment per bin for the chunk: every thread's atomics in flight together
+      constexpr int kPerT = kBinMax / T;
+      uint32_t c[kPerT];
+#pragma unroll
+      for (int q = 0; q < kPerT; ++q) {
+        const int t = tid + q * T;
+        c[q] = t < nb ? s_cnt[t] : 0u;
+      }
+#pragma unroll
+      for (int q = 0; q < kPerT; ++q) c[q] = c[q] ? add_agent(a.bk.cnt + tid + q * T, c[q]) : 0u;
+#pragma unroll
+      for (int q = 0; q < kPerT; ++q) {
+        const int t = tid + q * T;
+        if (t < nb) {
+          s_base[t] = c[q];
+          s_cnt[t] = 0;
+        }
+      }
     }
     __syncthreads();
 #pragma unroll
