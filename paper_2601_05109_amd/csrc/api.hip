@@ -136,6 +136,7 @@ struct nalar_policy {
   int bin_skip = 0;              // passes left before bins are tried again
   int bin_backoff = 1;
   bool split_any = false;        // splitters for any ready count, any sweep (graph store)
+  uint32_t bin_max = 0;          // records in the largest bin of the last bin sort (0: unknown)
   std::string err;
   ArenaState own;                // scratch allocated by the library for this handle
   HostStatus* host = nullptr;    // pinned, written by the sort kernel
@@ -317,6 +318,18 @@ BucketArgs plan_buckets(const nalar_policy* h, int64_t N, bool levels, bool wave
 
 // Bins for this pass (the block sweep of a large ready set, splitters from the
 // previous pass of this handle; bins == 0: not used).
+// Records per bin for a full pass: one workgroup's LDS worth (kBinCap, one
+// sort launch) when the largest bin of the last bin sort left a third of that
+// to spare, else room for eight times the average bin (the large-bin kernel
+// sorts the bins above kBinCap).  A bin past its capacity is an overflow: the
+// pass sorts again another way, and the next plan is the roomy one.  (The
+// store's incremental passes always plan the roomy bins: the keys of the
+// futures they recompute move between passes.)
+int bin_cap_plan(const nalar_policy* h, int nb) {
+  if (h->bin_max > 0 && h->bin_max + h->bin_max / 2 + 128 <= uint32_t(kBinCap)) return kBinCap;
+  return bin_cap_for(h->hint_ready, nb);
+}
+
 BucketArgs plan_bins(const nalar_policy* h, const SweepShape& sh, bool levels) {
   BucketArgs bk{};
   if ((h->flags & NALAR_FORCE_TILED_SORT) || sh.wave_path || levels || h->split_nb <= 0 ||
@@ -325,7 +338,7 @@ BucketArgs plan_bins(const nalar_policy* h, const SweepShape& sh, bool levels) {
     return bk;
   bk.bins = 1;
   bk.nb = h->split_nb;
-  bk.cap = bin_cap_for(h->hint_ready, bk.nb);
+  bk.cap = bin_cap_plan(h, bk.nb);
   return bk;
 }
 
@@ -752,6 +765,7 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
       __atomic_store_n(&h->host->status, 0xFFFFFFFFu, __ATOMIC_RELEASE);
       tiled = true;
       if (bk.bins) {  // a bin overflowed: new splitters come from the tiled sort; back off
+        h->bin_max = 0;
         h->bin_skip = h->bin_backoff;
         h->bin_backoff = h->bin_backoff < 64 ? 2 * h->bin_backoff : 64;
       } else {
@@ -773,6 +787,7 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
       NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
     } else if (bk.bins) {
       h->bin_backoff = 1;
+      h->bin_max = __atomic_load_n(&h->host->max_bucket, __ATOMIC_ACQUIRE);
     } else {
       h->bucket_backoff = 1;
       const bool crowded = __atomic_load_n(&h->host->max_bucket, __ATOMIC_ACQUIRE) > kBucketCrowded;
@@ -992,7 +1007,11 @@ int nalar::policy_pass_incremental(nalar_policy* h, const nalar_problem* p, nala
   if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
   const uint32_t sts = __atomic_load_n(&h->host->status, __ATOMIC_ACQUIRE);
   if (sts == 0xFFFFFFFFu) return fail(h, NALAR_EDEVICE, "status was not written");
-  if (sts == kStatusTiled) return kIncFallbackOverflow;
+  if (sts == kStatusTiled) {
+    h->bin_max = 0;
+    return kIncFallbackOverflow;
+  }
+  h->bin_max = __atomic_load_n(&h->host->max_bucket, __ATOMIC_ACQUIRE);
   if (sts & kStIncomplete) return kIncFallbackRounds;
   as.passes += 1;
   as.ctrl_dirty[nxt] = false;

@@ -56,10 +56,16 @@ __device__ inline TabLds carve_tab(unsigned char* sp, int64_t M) {
   return t;
 }
 
-__device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl, unsigned char* smem) {
+// A workgroup barrier that orders LDS accesses only: it waits for this wave's
+// LDS operations, not for its global loads and stores in flight (which
+// __syncthreads also waits for).
+__device__ inline void lds_barrier() {
+  __asm__ __volatile__("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+__device__ void instance_table(const ProblemDev& p, ITab it, unsigned char* smem) {
   const int M = int(p.M);
   const int tid = threadIdx.x;
-  reset_ctrl(next_ctrl);  // unused by this pass; ready for the next one
   __shared__ uint32_t s_run[kTypeDirect], s_prun[kTypeDirect], s_tstart[kTypeDirect];
   const TabLds S = carve_tab(smem, M);
   const int M4 = (M + 3) & ~3;
@@ -112,7 +118,7 @@ __device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl, un
       below[u] = uint32_t(__popcll(peers & lanemask_lt()));
       if (in && below[u] == 0) S.wh[(i / kWave) * kTypeDirect + ty[u]] = uint32_t(__popcll(peers));
     }
-    __syncthreads();
+    lds_barrier();
     // per type: offsets of the groups, then the run starts (one wave)
     if (tid < kTypeDirect) {
       uint32_t tot = 0;
@@ -124,7 +130,7 @@ __device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl, un
       const uint32_t inc = wave_incl_scan_u32(tot);
       s_tstart[tid] = inc - tot;
     }
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
       const int i = tid + u * kNodeThreads;
@@ -166,7 +172,7 @@ __device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl, un
     S.sspeed[at[u]] = sp[u];
     S.rng[at[u]] = uint32_t(lo[u]) | (uint32_t(hi[u]) << 16);
   }
-  __syncthreads();
+  lds_barrier();
   // dominated instances of small runs, per sorted position r (j < i is q < r)
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
@@ -191,7 +197,7 @@ __device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl, un
     }
     S.sdom[r] = dom ? 1 : 0;
   }
-  __syncthreads();
+  lds_barrier();
   // undominated first, each part in ascending index
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
@@ -226,7 +232,7 @@ __device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl, un
       s_prun[t] = uint32_t(a + und);
     }
   }
-  __syncthreads();
+  lds_barrier();
   for (int t = tid; t < kTypeDirect; t += kNodeThreads) {
     it.run[t] = s_run[t];
     it.prun[t] = s_prun[t];
@@ -236,16 +242,18 @@ __device__ void instance_table(const ProblemDev& p, ITab it, Ctrl* next_ctrl, un
 // Grid-stride over nodes, workflows and instances.  Workgroup 0 (dispatched
 // first, so that its longer work overlaps the others) only builds the
 // instance table sorted by type, so each future's candidates form one
-// contiguous run, and resets the control block of the next pass.
+// contiguous run; workgroup 1 also resets the control block of the next pass
+// (the grid always has a second workgroup).
 __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl, Ctrl* next_ctrl,
                                                        ITab it, int32_t* wf_off, int contiguous,
                                                        int64_t v_begin) {
   const int64_t N = p.N, W = p.W, M = p.M;
   if (blockIdx.x == 0) {
     extern __shared__ __align__(16) unsigned char smem[];
-    instance_table(p, it, next_ctrl, smem);
+    instance_table(p, it, smem);
     return;
   }
+  if (blockIdx.x == 1) reset_ctrl(next_ctrl);  // unused by this pass; ready for the next one
   const int64_t stride = int64_t(gridDim.x - 1) * kNodeThreads;
   const int64_t g0 = int64_t(blockIdx.x - 1) * kNodeThreads + threadIdx.x;
   bool bad = false;

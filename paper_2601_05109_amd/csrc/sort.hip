@@ -1028,12 +1028,26 @@ __device__ void bin_sort_one(const SortArgs& a, const BucketArgs& bk, int b, int
 }
 
 // One workgroup per bin; bins of more than kBinCap records are left to
-// k_bin_sort_big.  Workgroup 0 settles and publishes the status and range.
+// k_bin_sort_big.  Workgroup 0 settles and publishes the status and range,
+// and the size of the largest bin (in max_bucket), from which the host plans
+// the next pass's bin capacity.
 __global__ __launch_bounds__(kBinThreads) void k_bin_sort(SortArgs a, BucketArgs bk) {
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int NW = kBinThreads / kWave;
   const BinLds<NW> L = carve_bin<NW>(smem, kBinCap, a.tie_wf != nullptr);
   const int b = blockIdx.x;
+  if (b == 0) {
+    __shared__ uint32_t s_mx[NW];
+    uint32_t mx = 0;
+    for (int i = int(threadIdx.x); i < bk.nb; i += kBinThreads) mx = bk.cnt[i] > mx ? bk.cnt[i] : mx;
+    mx = uint32_t(wave_max_i64(int64_t(mx)));
+    if (lane_id() == 0) s_mx[threadIdx.x / kWave] = mx;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      for (int w = 1; w < NW; ++w) mx = s_mx[w] > mx ? s_mx[w] : mx;
+      __hip_atomic_store(&a.host->max_bucket, mx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+  }
   Ctrl* ctrl = a.ctrl;
   const uint32_t status = ctrl->status | ctrl->status_sweep;
   const uint32_t overflow = ctrl->bucket_overflow;
