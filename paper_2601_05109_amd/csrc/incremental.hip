@@ -40,7 +40,7 @@ namespace {
 
 constexpr int kIncThreads = 256;
 constexpr int kIncHeavy = 64;     // more dependencies: one workgroup expands the future
-constexpr int kScanPer = 8;       // consecutive futures per thread in the scan
+constexpr int kScanPer = 8;       // futures per thread in the scan (kIncThreads apart)
 constexpr int kReadyPer = 4;      // ready futures per thread and chunk in the ready kernel
 
 __device__ inline bool bit_set_new(uint32_t* bits, int32_t v) {
@@ -67,7 +67,7 @@ __device__ inline void push_round(int32_t* list, uint32_t* cnt, int r, int32_t v
 }
 
 // Appends the lanes' futures with one atomic per workgroup: thread t holds the
-// futures first + j for the set bits j of mask (every thread of the
+// futures first + j * stride for the set bits j of mask (every thread of the
 // workgroup calls).  s_tmp holds one word per wave and two more.
 __device__ inline void push_block(uint32_t mask, int64_t first, int32_t* list, uint32_t* n, uint32_t base,
                                   uint32_t* s_tmp, int64_t stride = 1) {
