@@ -318,3 +318,41 @@ def test_store_incremental_errors():
             assert st.run_pass(out, p.now_us, p.migration_cost_us) == nalar.NALAR_EINVAL
         finally:
             st.close()
+
+
+def test_store_incremental_random_streams():
+    """Two hundred small random streams (workflows, instances and types of
+    random counts, heavy dependency lists in some, deadline and instance
+    changes at random steps) under every order and routing policy: every pass,
+    incremental or not, equals the oracle's pass over the snapshot."""
+    pols = [0, nalar.NALAR_ORDER_LPT, nalar.NALAR_ORDER_SRTF, nalar.NALAR_ROUTE_STATEFUL,
+            nalar.NALAR_ROUTE_GREEDY, nalar.NALAR_ORDER_SRTF | nalar.NALAR_ROUTE_STATEFUL,
+            nalar.NALAR_ORDER_LPT | nalar.NALAR_ROUTE_GREEDY]
+    n_pass = n_inc = 0
+    for seed in range(200):
+        rng = np.random.default_rng(90000 + seed)
+        gr = Grower(50000 + seed, W=int(rng.integers(1, 12)), M=int(rng.integers(1, 40)),
+                    K=int(rng.integers(1, 6)), heavy=bool(seed % 3))
+        bits = pols[seed % len(pols)]
+        with nalar.Policy() as pol:
+            st = nalar.Store(pol)
+            try:
+                prev = (0, None)
+                for step in range(int(rng.integers(5, 25))):
+                    gr.step(int(rng.integers(1, 120)) if step else int(rng.integers(1, 200)))
+                    if rng.random() < 0.15:
+                        gr.deadline = gr.deadline + rng.integers(-300, 300, gr.W)
+                        assert st.set_workflows(gr.deadline) == nalar.NALAR_OK
+                    if rng.random() < 0.1:
+                        gr.inst()
+                        assert st.set_instances(gr.inst_type, gr.inst_load, gr.inst_speed) == nalar.NALAR_OK
+                    p = gr.problem()
+                    prev = feed(st, p, *prev)
+                    g, inc = store_pass(pol, st, p, bits)
+                    n_pass += 1
+                    n_inc += inc
+                    assert_parity(g, oracle.run(p, policy=bits), f"stream seed {seed} step {step} policy {bits}")
+            finally:
+                st.close()
+    say(f"[gpu] random streams: {n_pass} passes, {n_inc} incremental")
+    assert n_inc * 2 > n_pass, (n_inc, n_pass)
