@@ -39,6 +39,7 @@ namespace nalar {
 namespace {
 
 constexpr int kIncThreads = 256;
+constexpr int kIncTail = 3;       // rounds from here on run in one workgroup (k_inc_*_tail)
 constexpr int kIncHeavy = 64;     // more dependencies: one workgroup expands the future
 constexpr int kScanPer = 8;       // futures per thread in the scan (kIncThreads apart)
 constexpr int kReadyPer = 4;      // ready futures per thread and chunk in the ready kernel
@@ -52,11 +53,17 @@ __device__ inline bool bit_get(const uint32_t* bits, int32_t v) {
   return ((bits[uint32_t(v) >> 5] >> (uint32_t(v) & 31u)) & 1u) != 0u;
 }
 
+// A round's count, read where the atomics that wrote it are coherent (the
+// tail kernel reads counts its own earlier rounds wrote).
+__device__ inline uint32_t ld_count(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Start of round r's items in a list whose rounds are appended one after the
 // other (counts of rounds 0 .. r-1, stable once round r runs).
 __device__ inline uint32_t round_base(const uint32_t* cnt, int r) {
   uint32_t b = 0;
-  for (int i = 0; i < r; ++i) b += cnt[i];
+  for (int i = 0; i < r; ++i) b += ld_count(&cnt[i]);
   return b;
 }
 
@@ -140,6 +147,7 @@ struct WgQueue {
   int* hn;
   uint32_t* tmp;    // [waves + 2] for push_block
   int* htaken;      // heavy futures this workgroup kept (at most kIncHeavyKeep)
+  bool keep_all;    // one workgroup for every round left: keep every heavy future
 };
 
 __device__ inline void wg_push(const WgQueue& wq, int32_t* list, uint32_t* cnt, int round, int32_t v) {
@@ -157,7 +165,7 @@ constexpr int kIncHugeDeps = 1024;
 
 __device__ inline void wg_push_heavy(const WgQueue& wq, int32_t* list, uint32_t* cnt, int round, int32_t v,
                                      int32_t deg) {
-  if (deg <= kIncHugeDeps || atomicAdd(wq.htaken, 1) < kIncHeavyKeep) {
+  if (wq.keep_all || deg <= kIncHugeDeps || atomicAdd(wq.htaken, 1) < kIncHeavyKeep) {
     const int at = atomicAdd(wq.hn, 1);
     if (at < kIncHeavyQueue) {
       wq.hq[at] = v;
@@ -297,20 +305,17 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_mark(IncArgs a) {
 // Round 0 takes the seeds (completed ids of the log, then the appended
 // range); round r >= 1 the futures handed on: heavy ones expanded one per
 // workgroup, the others one per thread.  Then the workgroup drains its queue.
-__global__ __launch_bounds__(kIncThreads) void k_inc_close(IncArgs a, int r) {
-  if (invalid(a)) return;
-  const uint32_t nh = r ? a.ic->ch[r] : 0u, nl = r ? a.ic->cl[r] : 0u;
+// One round of the closure, this workgroup's share of it (every thread of the
+// workgroup calls; the workgroup's queues are empty on entry and on return).
+__device__ void close_round(const IncArgs& a, int r, const WgQueue& wq) {
+  const uint32_t nh = r ? ld_count(&a.ic->ch[r]) : 0u, nl = r ? ld_count(&a.ic->cl[r]) : 0u;
   const int64_t n_app = a.p.N - a.n_prev;
   const int64_t n_seed = r ? 0 : a.n_log + (n_app > 0 ? n_app : 0);
-  if (nh == 0 && nl == 0 && n_seed == 0) return;
-  __shared__ int32_t s_q[kIncQueue], s_hq[kIncHeavyQueue];
-  __shared__ int s_n, s_hn, s_htaken;
-  __shared__ uint32_t s_tmp[kIncThreads / kWave + 2];
-  const WgQueue wq{s_q, &s_n, s_hq, &s_hn, s_tmp, &s_htaken};
+  if (nh == 0 && nl == 0 && n_seed == 0) return;  // the same on every thread
   if (threadIdx.x == 0) {
-    s_n = 0;
-    s_hn = 0;
-    s_htaken = 0;
+    *wq.n = 0;
+    *wq.hn = 0;
+    *wq.htaken = 0;
   }
   __syncthreads();
   // every lane of a wave runs each iteration (the walks work wave by wave)
@@ -339,6 +344,31 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_close(IncArgs a, int r) {
     close_walk(a, i < nl ? a.light[bl + i] : -1, r, wq);
   }
   wg_drain(wq, [&](int32_t v) { close_walk(a, v, r, wq); }, [&](int32_t v) { close_expand(a, v, r, wq); });
+}
+
+// The workgroup's LDS queues.
+#define NALAR_INC_QUEUES(keep)                                                  \
+  __shared__ int32_t s_q[kIncQueue], s_hq[kIncHeavyQueue];                      \
+  __shared__ int s_n, s_hn, s_htaken;                                           \
+  __shared__ uint32_t s_tmp[kIncThreads / kWave + 2];                           \
+  const WgQueue wq{s_q, &s_n, s_hq, &s_hn, s_tmp, &s_htaken, keep}
+
+__global__ __launch_bounds__(kIncThreads) void k_inc_close(IncArgs a, int r) {
+  if (invalid(a)) return;
+  NALAR_INC_QUEUES(false);
+  close_round(a, r, wq);
+}
+
+// Rounds kIncTail .. kIncRounds - 1 by one workgroup (they are usually empty,
+// and one launch costs less than one per round).  What a round hands on is
+// read by the same workgroup in the next one.
+__global__ __launch_bounds__(kIncThreads) void k_inc_close_tail(IncArgs a) {
+  if (invalid(a)) return;
+  NALAR_INC_QUEUES(true);
+  for (int r = kIncTail; r < kIncRounds; ++r) {
+    close_round(a, r, wq);
+    __syncthreads();
+  }
 }
 
 // --------------------------------------------------------------------- scan
@@ -659,22 +689,17 @@ __device__ inline void sweep_expand(const IncArgs& a, int32_t u, int round, uint
   (void)fin;
 }
 
-__global__ __launch_bounds__(kIncThreads) void k_inc_sweep(IncArgs a, int r) {
-  if (invalid(a)) return;
-  const uint32_t nh = a.ic->sh[r], nl = a.ic->sl[r];
-  if (nh == 0 && nl == 0) return;
-  __shared__ int32_t s_q[kIncQueue], s_hq[kIncHeavyQueue];
-  __shared__ int s_n, s_hn, s_htaken;
-  __shared__ uint32_t s_tmp[kIncThreads / kWave + 2];
-  const WgQueue wq{s_q, &s_n, s_hq, &s_hn, s_tmp, &s_htaken};
+// One round of the sweep, this workgroup's share of it (as close_round).
+__device__ void sweep_round(const IncArgs& a, int r, const WgQueue& wq, uint32_t& fin) {
+  const uint32_t nh = ld_count(&a.ic->sh[r]), nl = ld_count(&a.ic->sl[r]);
+  if (nh == 0 && nl == 0) return;  // the same on every thread
   if (threadIdx.x == 0) {
-    s_n = 0;
-    s_hn = 0;
-    s_htaken = 0;
+    *wq.n = 0;
+    *wq.hn = 0;
+    *wq.htaken = 0;
   }
   __syncthreads();
   const uint32_t bh = round_base(a.ic->sh, r), bl = round_base(a.ic->sl, r);
-  uint32_t fin = 0;
   for (uint32_t h = blockIdx.x; h < nh; h += gridDim.x) sweep_expand(a, a.heavy[bh + h], r, fin, wq);
   for (uint32_t i0 = blockIdx.x * kIncThreads; i0 < nl; i0 += gridDim.x * kIncThreads) {
     const uint32_t i = i0 + threadIdx.x;
@@ -682,6 +707,25 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_sweep(IncArgs a, int r) {
   }
   wg_drain(wq, [&](int32_t v) { sweep_walk(a, v, r, fin, wq); },
            [&](int32_t v) { sweep_expand(a, v, r, fin, wq); });
+}
+
+__global__ __launch_bounds__(kIncThreads) void k_inc_sweep(IncArgs a, int r) {
+  if (invalid(a)) return;
+  NALAR_INC_QUEUES(false);
+  uint32_t fin = 0;
+  sweep_round(a, r, wq, fin);
+  add_fin(a, fin);
+}
+
+// Rounds kIncTail .. kIncRounds - 1 of the sweep by one workgroup.
+__global__ __launch_bounds__(kIncThreads) void k_inc_sweep_tail(IncArgs a) {
+  if (invalid(a)) return;
+  NALAR_INC_QUEUES(true);
+  uint32_t fin = 0;
+  for (int r = kIncTail; r < kIncRounds; ++r) {
+    sweep_round(a, r, wq, fin);
+    __syncthreads();
+  }
   add_fin(a, fin);
 }
 
@@ -920,12 +964,15 @@ hipError_t launch_inc_closure(hipStream_t s, const IncArgs& a, int cus, void (*m
   mark(ctx, kCloseNames[0]);
   hipLaunchKernelGGL(k_inc_close, dim3(inc_grid(seeds, 4096)), dim3(kIncThreads), 0, s, a, 0);
   e = hipGetLastError();
-  for (int r = 1; r <= kIncRounds - 1 && e == hipSuccess; ++r) {
+  for (int r = 1; r < kIncTail && e == hipSuccess; ++r) {
     mark(ctx, kCloseNames[r]);
     hipLaunchKernelGGL(k_inc_close, dim3(r < 2 ? 4 * cus : cus), dim3(kIncThreads), 0, s, a, r);
     e = hipGetLastError();
   }
-  return e;
+  if (e != hipSuccess) return e;
+  mark(ctx, "inc_close_tail");
+  hipLaunchKernelGGL(k_inc_close_tail, dim3(1), dim3(kIncThreads), 0, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_inc_scan(hipStream_t s, const IncArgs& a, int cus) {
@@ -942,12 +989,15 @@ hipError_t launch_inc_sweep(hipStream_t s, const IncArgs& a, int cus, void (*mar
   mark(ctx, "inc_front0");
   hipLaunchKernelGGL(k_inc_front0, dim3(inc_grid((a.p.N + 31) / 32, 8 * cus)), dim3(kIncThreads), 0, s, a);
   hipError_t e = hipGetLastError();
-  for (int r = 0; r <= kIncRounds - 1 && e == hipSuccess; ++r) {
+  for (int r = 0; r < kIncTail && e == hipSuccess; ++r) {
     mark(ctx, kSweepNames[r]);
-    hipLaunchKernelGGL(k_inc_sweep, dim3(r < 3 ? 4 * cus : cus), dim3(kIncThreads), 0, s, a, r);
+    hipLaunchKernelGGL(k_inc_sweep, dim3(4 * cus), dim3(kIncThreads), 0, s, a, r);
     e = hipGetLastError();
   }
-  return e;
+  if (e != hipSuccess) return e;
+  mark(ctx, "inc_sweep_tail");
+  hipLaunchKernelGGL(k_inc_sweep_tail, dim3(1), dim3(kIncThreads), 0, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_inc_ready(hipStream_t s, const IncArgs& a, int cus) {
