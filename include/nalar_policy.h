@@ -128,6 +128,11 @@ enum {
                                         on a handle's first pass, above 131072
                                         ready futures and when a bucket of the
                                         bucketed sort overflows)                 */
+#define NALAR_FORCE_LEVEL_SWEEP  4u  /* sweep every workflow kept in HBM level
+                                        by level with out-degree counters, also
+                                        one whose dependencies all lie at lower
+                                        ids (which otherwise takes one pass over
+                                        its ids from the last to the first)      */
 
 typedef struct nalar_policy nalar_policy;   /* opaque handle */
 

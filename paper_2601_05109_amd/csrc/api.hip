@@ -79,6 +79,7 @@ struct Arena {
   uint8_t* g_dn = nullptr;
   uint8_t* g_nr = nullptr;
   int32_t* g_front[2] = {nullptr, nullptr};
+  uint64_t* done_bits = nullptr;  // [N / 64] the done flags, one bit per future
   uint32_t* bcnt[2] = {nullptr, nullptr};  // bucket counters, by pass parity
   BucketSlot* bslot = nullptr;
   int64_t* split[2] = {nullptr, nullptr};   // bin splitters: read by one pass, written for the next
@@ -200,6 +201,7 @@ size_t carve(Arena& a, char* base, int64_t N, int64_t W, int64_t B, int64_t Rec)
   for (int i = 0; i < 2; ++i) a.g_front[i] = reinterpret_cast<int32_t*>(take(4 * size_t(n1)));
   a.g_dn = reinterpret_cast<uint8_t*>(take(size_t(n1)));
   a.g_nr = reinterpret_cast<uint8_t*>(take(size_t(n1)));
+  a.done_bits = reinterpret_cast<uint64_t*>(take(8 * size_t((n1 + 63) / 64)));
   const int64_t b1 = B > 0 ? B : 0;
   for (int i = 0; i < 2; ++i) a.bcnt[i] = reinterpret_cast<uint32_t*>(take(4 * size_t(b1 + 1)));
   const int64_t r1 = Rec > b1 * kBucketCap ? Rec : b1 * kBucketCap;
@@ -427,7 +429,7 @@ int nalar_policy_create(const nalar_policy_config* cfg, nalar_policy** out) {
     g_create_error = "NULL config or output";
     return NALAR_EINVAL;
   }
-  if ((cfg->flags & ~(NALAR_FORCE_GLOBAL_SWEEP | NALAR_FORCE_TILED_SORT)) != 0 || cfg->reserve_nodes < 0 ||
+  if ((cfg->flags & ~(NALAR_FORCE_GLOBAL_SWEEP | NALAR_FORCE_TILED_SORT | NALAR_FORCE_LEVEL_SWEEP)) != 0 || cfg->reserve_nodes < 0 ||
       cfg->reserve_edges < 0 || cfg->reserve_workflows < 0 ||
       cfg->reserve_nodes > NALAR_MAX_NODES || cfg->reserve_workflows > NALAR_MAX_WORKFLOWS) {
     g_create_error = "invalid config";
@@ -659,7 +661,8 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
   }
   const bool fused = N > 0 && sweep_can_fuse(sh, M, contiguous);
   if (!fused)
-    NALAR_LAUNCH("nodes", launch_nodes(s, pd, ctrl, A.ctrl[nxt], A.itab, A.wf_off, contiguous ? 1 : 0));
+    NALAR_LAUNCH("nodes", launch_nodes(s, pd, ctrl, A.ctrl[nxt], A.itab, A.wf_off, contiguous ? 1 : 0, 0,
+                                       sh.wave_path ? nullptr : A.done_bits));
 
   const int32_t* node_of_pos = nullptr;
   const int32_t* pos_of_node = nullptr;
@@ -686,6 +689,7 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
   }
 
   SweepArgs sw{};
+  BlockSweepArgs ba{};
   if (N > 0) {
     sw.p = pd;
     sw.itab = A.itab;
@@ -711,7 +715,9 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
     sw.bk_clear = A.bcnt[nxt];
     sw.bk_clear_n = A.capB > 0 ? A.capB : 0;
     sw.force_global = (h->flags & NALAR_FORCE_GLOBAL_SWEEP) ? 1 : 0;
-    NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
+    ba.ordered = (h->flags & NALAR_FORCE_LEVEL_SWEEP) ? 0 : 1;
+    ba.done_bits = reinterpret_cast<const uint32_t*>(A.done_bits);
+    NALAR_LAUNCH("sweep", launch_sweep(s, sw, ba, sh));
     as.bcnt_clean[nxt] = true;  // the sweep cleared them for the next pass
   }
 
@@ -784,7 +790,7 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
       if (policy & NALAR_ROUTE_WEIGHTED)  // its weight check reports into the block just reset
         NALAR_LAUNCH("weighted_table", launch_weighted_table(s, wa));
       sw.bk = BucketArgs{};
-      NALAR_LAUNCH("sweep", launch_sweep(s, sw, sh));
+      NALAR_LAUNCH("sweep", launch_sweep(s, sw, ba, sh));
     } else if (bk.bins) {
       h->bin_backoff = 1;
       h->bin_max = __atomic_load_n(&h->host->max_bucket, __ATOMIC_ACQUIRE);

@@ -246,7 +246,7 @@ __device__ void instance_table(const ProblemDev& p, ITab it, unsigned char* smem
 // (the grid always has a second workgroup).
 __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl, Ctrl* next_ctrl,
                                                        ITab it, int32_t* wf_off, int contiguous,
-                                                       int64_t v_begin) {
+                                                       int64_t v_begin, uint64_t* done_bits) {
   const int64_t N = p.N, W = p.W, M = p.M;
   if (blockIdx.x == 0) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -286,6 +286,14 @@ __global__ __launch_bounds__(kNodeThreads) void k_nodes(ProblemDev p, Ctrl* ctrl
       if (v == 0) bad |= (o0[u] != 0);
       if (v == N - 1) bad |= (int64_t(o1[u]) != p.E);
     }
+    if (done_bits) {  // a wave holds 64 consecutive futures (lane 0's a multiple of 64)
+#pragma unroll
+      for (int u = 0; u < kNodeItems; ++u) {
+        const int64_t v = v0 + u * stride;
+        const uint64_t m = ballot(v < N && d[u] != 0);
+        if (lane_id() == 0 && v < N) done_bits[v >> 6] = m;
+      }
+    }
   }
   for (int64_t w = g0; w < W; w += stride) {
     const int64_t dl = p.deadline[w];
@@ -318,11 +326,12 @@ int grid_for(int64_t n, int threads, int cap) {
 }  // namespace
 
 hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
-                        int32_t* wf_off, int contiguous, int64_t v_begin) {
+                        int32_t* wf_off, int contiguous, int64_t v_begin, uint64_t* done_bits) {
+  if (v_begin % kWave != 0) done_bits = nullptr;  // a wave's futures must fill whole words
   const int64_t nv = (p.N - v_begin + kNodeItems - 1) / kNodeItems;
   int64_t n = nv > p.W + 1 ? nv : p.W + 1;
   hipLaunchKernelGGL(k_nodes, dim3(grid_for(n, kNodeThreads, 4096) + 1), dim3(kNodeThreads), tab_lds_bytes(p.M), s, p,
-                     ctrl, next_ctrl, itab, wf_off, contiguous, v_begin);
+                     ctrl, next_ctrl, itab, wf_off, contiguous, v_begin, done_bits);
   return hipGetLastError();
 }
 

@@ -136,6 +136,13 @@ struct SweepArgs {
   int64_t bk_clear_n;
 };
 
+// What the block sweep alone takes besides SweepArgs (the wave kernel's
+// arguments stay within eight 64-byte lines).
+struct BlockSweepArgs {
+  const uint32_t* done_bits;    // [N bits] done flags, one bit per future
+  int ordered;                  // workflows kept in HBM may take the ordered chunk pass
+};
+
 // Load-aware routing over the ordered ready futures (greedy.hip).
 struct GreedyArgs {
   const int32_t* order;         // [R] the pass's output order
@@ -292,8 +299,10 @@ int policy_fail(nalar_policy* h, int code, const char* msg);
 
 // ingest.hip
 // Validates the futures from v_begin on (and every deadline and instance).
+// done_bits (or null, and only with v_begin = 0): the done flags packed one
+// bit per future, bit v % 64 of word v / 64.
 hipError_t launch_nodes(hipStream_t s, const ProblemDev& p, Ctrl* ctrl, Ctrl* next_ctrl, ITab itab,
-                        int32_t* wf_off, int contiguous, int64_t v_begin = 0);
+                        int32_t* wf_off, int contiguous, int64_t v_begin = 0, uint64_t* done_bits = nullptr);
 
 // sort.hip (mark(ctx, name) is called before each launch, for timing)
 hipError_t launch_reset(hipStream_t s, Ctrl* c, uint32_t* clear, int64_t n_clear);
@@ -320,7 +329,7 @@ struct SweepShape {
 };
 SweepShape plan_sweep(int64_t N, int64_t W, int64_t M, int device_cus, size_t lds_limit);
 hipError_t prepare_sweep_kernels(size_t lds_limit);
-hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const SweepShape& shape);
+hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const BlockSweepArgs& ba, const SweepShape& shape);
 // Whether the sweep can do validation, workflow bounds and the instance table
 // itself (no node kernel): ids grouped by workflow, wave path, small table.
 bool sweep_can_fuse(const SweepShape& shape, int64_t M, bool contiguous);

@@ -28,8 +28,11 @@
 //    bounds and builds the routing table itself.
 //  * k_sweep: one workgroup per workflow of up to 5,120 futures (LDS state).
 //  * workflows larger than that (or all, under NALAR_FORCE_GLOBAL_SWEEP) keep
-//    their state in HBM by position and process explicit frontier lists,
-//    swept by the workgroup that met them.
+//    their state in HBM by position.  When every dependency of such a
+//    workflow lies at a lower position than its consumer, its positions are
+//    taken in chunks from the last to the first (sweep_hbm_ordered); else it
+//    processes explicit frontier lists (sweep_hbm).  Either way the workgroup
+//    that met the workflow sweeps it.
 //
 // Every ready future is routed against the pass-start instance table and then
 // either dropped into its order-key bucket (one returning atomic for a slot)
@@ -880,6 +883,274 @@ __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, con
   __syncthreads();
 }
 
+// ------------------------------------------------------------ ordered workflow
+
+// Future v's done flag from the packed copy the node kernel wrote (1.5 MB per
+// 12M futures, so that the random reads of dependencies' flags stay in L2).
+__device__ inline bool done_bit(const uint32_t* bits, int32_t v) {
+  return ((bits[uint32_t(v) >> 5] >> (uint32_t(v) & 31u)) & 1u) != 0u;
+}
+
+// A workflow in HBM whose every dependency lies at a lower position than its
+// consumer (ids in topological order within the workflow, as when futures are
+// appended after their dependencies) needs no out-degree counters and no
+// frontiers: taking its positions in chunks from the last chunk to the first,
+// every consumer of a future in an earlier chunk has already pushed its rem
+// when that chunk is reached.  Inside a chunk, a future waits until its
+// consumers in the same chunk (counted beforehand, in LDS) have pushed; these
+// rounds end because the pending future at the highest position never waits.
+// A workflow of n futures costs about n / (T x P) chunks of a few dependent
+// round trips each, instead of a counter pass plus one frontier round per
+// level with random accesses to per-position state.  A thread takes P
+// futures of each chunk (T x P positions), their loads issued together.
+// P = kOrdP = 1: the block kernel also holds the LDS sweep, whose registers
+// this path shares; with P = 4 it spills, and a kernel of its own (512
+// threads, P = 4, no spills) measured slower than P = 1 here.
+constexpr int kOrdP = 1;
+//
+// Returns false, having written only its own scratch (mx and the in-chunk
+// counters), when some dependency does not lie lower; the caller then runs
+// the level-synchronous sweep.  lc: T x P ints of LDS.
+template <int T, int P>
+__device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs& a, const Layout& L, const ITabLds& it,
+                                                                 const BlockSweepArgs& ba, Shared& S, int64_t b, int n,
+                                                                 int64_t dl, int lvl, Acc& acc, const int64_t* split_l,
+                                                                 int32_t* lc) {
+  constexpr int C = T * P;  // positions per chunk
+  const int tid = threadIdx.x;
+  Ctrl* ctrl = a.ctrl;
+  int32_t* cnt = a.g_cnt + b;  // consumers in the same chunk, by position
+  int64_t* mx = a.g_mx + b;
+  if (tid == 0) { S.bad = 0; S.hcount = 0; }
+
+  // 1: chunk by chunk, check the order, count in-chunk consumers, clear mx
+  for (int c0 = 0; c0 < n; c0 += C) {
+    int32_t v[P], off[P], deg[P];
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      const int k = c0 + j * T + tid;
+      v[j] = k < n ? node_at(L, b + k) : 0;
+      lc[j * T + tid] = 0;
+    }
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      const bool own = c0 + j * T + tid < n;
+      off[j] = own ? a.p.dep_off[v[j]] : 0;
+      deg[j] = own ? a.p.dep_off[v[j] + 1] - off[j] : 0;
+    }
+    __syncthreads();
+    bool up = false;
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      const int k = c0 + j * T + tid;
+      if (k >= n) continue;
+      if (deg[j] <= kHbmLight) {
+        for (int e = 0; e < deg[j]; ++e) {
+          const int32_t lp = checked_dep(L, a.p.dep_idx[off[j] + e], b, n, k, ctrl);
+          if (lp > k) up = true;
+          else if (lp >= c0) atomicAdd(&lc[lp - c0], 1);
+        }
+      } else {
+        const int slot = atomicAdd(&S.hcount, 1);
+        if (slot < kHeavyCap) {
+          S.hk[slot] = k; S.ho[slot] = off[j]; S.hd[slot] = deg[j];
+        } else {
+          up = true;  // more heavy futures in one chunk than the list holds
+        }
+      }
+    }
+    if (up) S.bad = 1;
+    __syncthreads();
+    const int hc = S.hcount < kHeavyCap ? S.hcount : kHeavyCap;
+    for (int h = 0; h < hc; ++h) {
+      const int hk = S.hk[h], ho = S.ho[h], hd = S.hd[h];
+      for (int e = tid; e < hd; e += T) {
+        const int32_t lp = checked_dep(L, a.p.dep_idx[ho + e], b, n, hk, ctrl);
+        if (lp > hk) S.bad = 1;
+        else if (lp >= c0) atomicAdd(&lc[lp - c0], 1);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      const int k = c0 + j * T + tid;
+      if (k < n) {
+        st_wg(&cnt[k], lc[j * T + tid]);
+        st_wg(&mx[k], int64_t(0));
+      }
+    }
+    if (tid == 0) S.hcount = 0;
+  }
+  __syncthreads();
+  const bool unordered = S.bad != 0;
+  __syncthreads();  // every thread has read the flag before the caller reuses it
+  if (unordered) return false;
+
+  // 2: the chunks from the last to the first.  Everything a future needs
+  // except its consumers' max is loaded when its chunk starts (its first two
+  // dependencies, their positions and done flags), so that a round waits on
+  // the loads of the maxima, then on those of the futures that turned out
+  // ready and on their bucket-slot atomics.
+  bool overflow = false;
+  for (int c0 = ((n - 1) / C) * C; c0 >= 0; c0 -= C) {
+    int32_t v[P], off[P], deg[P], p0[P], p1[P], lp0[P], lp1[P];
+    int64_t est[P];
+    uint32_t own = 0, light = 0, dn = 0, blocked = 0;
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      const int k = c0 + j * T + tid;
+      if (k < n) own |= 1u << j;
+      v[j] = k < n ? node_at(L, b + k) : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      const int k = c0 + j * T + tid;
+      const bool o = (own >> j) & 1u;
+      off[j] = o ? a.p.dep_off[v[j]] : 0;
+      deg[j] = o ? a.p.dep_off[v[j] + 1] - off[j] : 0;
+      if (!o || done_bit(ba.done_bits, v[j])) dn |= 1u << j;
+      est[j] = o ? a.p.est[v[j]] : 0;
+      if (o) lc[j * T + tid] = ld_wg(&cnt[k]);
+    }
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      if (((own >> j) & 1u) && deg[j] <= kHbmLight) light |= 1u << j;
+      const bool l = (light >> j) & 1u;
+      p0[j] = l && deg[j] > 0 ? a.p.dep_idx[off[j]] : 0;
+      p1[j] = l && deg[j] > 1 ? a.p.dep_idx[off[j] + 1] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      const int k = c0 + j * T + tid;
+      const bool l = (light >> j) & 1u;
+      lp0[j] = l && deg[j] > 0 ? local_of(L, p0[j], b, n) : -1;
+      lp1[j] = l && deg[j] > 1 ? local_of(L, p1[j], b, n) : -1;
+      if (lp0[j] == k) lp0[j] = -1;  // reported by the first step
+      if (lp1[j] == k) lp1[j] = -1;
+    }
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      const bool bl0 = lp0[j] >= 0 && !done_bit(ba.done_bits, p0[j]);
+      const bool bl1 = lp1[j] >= 0 && !done_bit(ba.done_bits, p1[j]);
+      if (bl0 || bl1) blocked |= 1u << j;
+    }
+    uint32_t pending = own;
+    if (tid == 0) { S.fcount = 0; S.hcount = 0; }
+    __syncthreads();
+    for (int round = 0;; ++round) {
+      uint32_t go = 0;
+#pragma unroll
+      for (int j = 0; j < P; ++j)
+        if (((pending >> j) & 1u) && lc[j * T + tid] == 0) go |= 1u << j;
+      __syncthreads();  // every count is read before this round's pushes
+      pending &= ~go;
+      int64_t r[P];
+#pragma unroll
+      for (int j = 0; j < P; ++j) r[j] = ((go >> j) & 1u) ? ld_wg(&mx[c0 + j * T + tid]) : 0;
+      uint32_t rd = 0;
+#pragma unroll
+      for (int j = 0; j < P; ++j) {
+        if (!((go >> j) & 1u)) continue;
+        const int k = c0 + j * T + tid;
+        r[j] = clamp_rem((((dn >> j) & 1u) ? 0 : est[j]) + r[j], overflow);
+        st_wg(&mx[k], r[j]);
+        if (a.rem_out) a.rem_out[v[j]] = r[j];
+        if (!((light >> j) & 1u)) {
+          const int slot = atomicAdd(&S.hcount, 1);  // below kHeavyCap: checked by the first step
+          S.hk[slot] = k; S.ho[slot] = off[j]; S.hd[slot] = deg[j];
+          continue;
+        }
+        if (lp0[j] >= 0) {
+          max_wg(&mx[lp0[j]], r[j]);
+          if (lp0[j] >= c0) atomicSub(&lc[lp0[j] - c0], 1);
+        }
+        if (lp1[j] >= 0) {
+          max_wg(&mx[lp1[j]], r[j]);
+          if (lp1[j] >= c0) atomicSub(&lc[lp1[j] - c0], 1);
+        }
+        for (int e = 2; e < deg[j]; ++e) {
+          const int32_t p = a.p.dep_idx[off[j] + e];
+          const int32_t lp = local_of(L, p, b, n);
+          if (lp < 0 || lp == k) continue;
+          if (!done_bit(ba.done_bits, p)) blocked |= 1u << j;
+          max_wg(&mx[lp], r[j]);
+          if (lp >= c0) atomicSub(&lc[lp - c0], 1);
+        }
+        const bool ready = !((dn >> j) & 1u) && !((blocked >> j) & 1u);
+        if (a.bk.nb == 0) a.stg_ready[b + k] = ready ? uint8_t(1 + lvl) : 0;
+        if (ready) rd |= 1u << j;
+      }
+      // the ready futures: their type and location, every bucket-slot atomic,
+      // the routing while they are in flight, then the stores
+      int64_t key[P];
+      uint32_t bkt[P], slot[P];
+      int32_t ty[P], lo[P];
+#pragma unroll
+      for (int j = 0; j < P; ++j) {
+        ty[j] = ((rd >> j) & 1u) ? a.p.type[v[j]] : 0;
+        lo[j] = ((rd >> j) & 1u) ? a.p.loc[v[j]] : -1;
+      }
+#pragma unroll
+      for (int j = 0; j < P; ++j) {
+        key[j] = order_key(a, r[j], dl);
+        bkt[j] = 0;
+        slot[j] = 0;
+        if (((rd >> j) & 1u) && a.bk.nb > 0) {
+          bkt[j] = a.bk.bins ? bin_of(split_l, a.bk.nb, key[j]) : bucket_of<false>(a.bk, key[j], lvl);
+          slot[j] = add_agent(a.bk.cnt + bkt[j], 1u);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < P; ++j) {
+        if (!((rd >> j) & 1u)) continue;
+        int32_t route;
+        int64_t cost;
+        route_future(ty[j], est[j], lo[j], int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load, it.speed,
+                     it.inv, it.pos, it.run, (a.p.policy & NALAR_ROUTE_STATEFUL) != 0, route, cost, it.prun);
+        store_ready(a, bkt[j], slot[j], key[j], lvl, dl - r[j], b + c0 + j * T + tid, route, cost, acc);
+      }
+      if (pending) atomicAdd(&S.fcount, 1);
+      __syncthreads();
+      const int hc = S.hcount;
+      for (int h = 0; h < hc; ++h) {  // heavy futures: the workgroup pushes together
+        const int hk = S.hk[h], ho = S.ho[h], hd = S.hd[h];
+        const int64_t hr = ld_wg(&mx[hk]);
+        if (tid == 0) S.proc = 0;
+        __syncthreads();
+        bool hb = false;
+        for (int e = tid; e < hd; e += T) {
+          const int32_t p = a.p.dep_idx[ho + e];
+          const int32_t lp = local_of(L, p, b, n);
+          if (lp < 0 || lp == hk) continue;
+          hb |= !done_bit(ba.done_bits, p);
+          max_wg(&mx[lp], hr);
+          if (lp >= c0) atomicSub(&lc[lp - c0], 1);
+        }
+        if (hb) S.proc = 1;
+        __syncthreads();
+        if (tid == 0) {
+          const int32_t hv = node_at(L, b + hk);
+          const bool ready = !done_bit(ba.done_bits, hv) && S.proc == 0;
+          if (a.bk.nb == 0) a.stg_ready[b + hk] = ready ? uint8_t(1 + lvl) : 0;
+          if (ready) write_ready<false>(a, it, b + hk, a.p.type[hv], a.p.loc[hv], hr, a.p.est[hv], dl, lvl, acc, split_l);
+        }
+      }
+      __syncthreads();
+      const int pend = S.fcount;
+      __syncthreads();  // every thread has read the counts before they are reset
+      if (pend == 0) break;
+      if (round > C) {  // cannot happen: some pending future never waits
+        if (tid == 0) flag_sweep(ctrl, kStCycle);
+        break;
+      }
+      if (tid == 0) { S.fcount = 0; S.hcount = 0; }
+    }
+  }
+  if (overflow) flag_sweep(ctrl, kStRange);
+  __syncthreads();
+  return true;
+}
+
 // ------------------------------------------------------------ wave workflow
 
 // The LDS operations of one wave complete in program order, so a wave working
@@ -1449,7 +1720,7 @@ __device__ __attribute__((always_inline)) void sweep_wave(const SweepArgs& a, co
 // ------------------------------------------------------------ kernel
 
 template <int T, int NPT>
-__global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
+__global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap, BlockSweepArgs ba) {
   constexpr int NW = T / kWave;
   Ctrl* ctrl = a.ctrl;
   for (int64_t i = int64_t(blockIdx.x) * T + threadIdx.x; i < a.bk_clear_n; i += int64_t(gridDim.x) * T)
@@ -1509,7 +1780,8 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap) {
     lmask |= level_bit(lvl);
     if (!a.force_global && n <= lds_cap)
       sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, lds_cap, b, n, dl, lvl, acc, bl);
-    else
+    else if (!(ba.ordered && lds_cap >= T * kOrdP &&
+               sweep_hbm_ordered<T, kOrdP>(a, L, it, ba, S, b, n, dl, lvl, acc, split_l, cnt)))
       sweep_hbm<T, false, false>(a, L, it, S, int(w), b, n, dl, lvl, acc, split_l);
   }
 
@@ -2048,10 +2320,8 @@ bool sweep_can_fuse(const SweepShape& shape, int64_t M, bool contiguous) {
 
 hipError_t prepare_sweep_kernels(size_t lds_limit) {
   const size_t dyn = lds_limit > kStaticLdsReserve ? lds_limit - kStaticLdsReserve : 0;
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sweep<kBlockT, kBlockNpt>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(dyn));
-  if (e != hipSuccess) return e;
-  for (const void* k : {reinterpret_cast<const void*>(&k_sweep_wave<1, false, 1>),
+  hipError_t e = hipSuccess;
+  for (const void* k : {reinterpret_cast<const void*>(&k_sweep<kBlockT, kBlockNpt>),reinterpret_cast<const void*>(&k_sweep_wave<1, false, 1>),
                         reinterpret_cast<const void*>(&k_sweep_wave<1, false, 2>),
                         reinterpret_cast<const void*>(&k_sweep_wave<2, false, 1>),
                         reinterpret_cast<const void*>(&k_sweep_wave<4, false, 1>),
@@ -2074,7 +2344,7 @@ void launch_wave(hipStream_t s, dim3 g, dim3 t, size_t lds, const SweepArgs& a, 
                      a.p.inst_load, a.p.deadline, a.p.wf, a.p.N, int32_t(a.p.W), int32_t(a.p.M), a, cap);
 }
 
-hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const SweepShape& sh) {
+hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const BlockSweepArgs& ba, const SweepShape& sh) {
   if (sh.threads == kWaveBlock) {
     // futures per lane = slice capacity / 64 (a power of two up to kWaveNpt)
     const dim3 g(sh.blocks), t(kWaveBlock);
@@ -2101,9 +2371,10 @@ hipError_t launch_sweep(hipStream_t s, const SweepArgs& a, const SweepShape& sh)
         default: launch_wave<kWaveNpt, false>(s, g, t, lds, a, cap); break;
       }
     }
-  } else
+  } else {
     hipLaunchKernelGGL((k_sweep<kBlockT, kBlockNpt>), dim3(sh.blocks), dim3(kBlockT), sh.lds_bytes, s,
-                       a, sh.lds_cap);
+                       a, sh.lds_cap, ba);
+  }
   return hipGetLastError();
 }
 

@@ -34,6 +34,7 @@ NALAR_ORDER_SRTF = 16        # problem flag: order by remaining critical path, s
 NALAR_ROUTE_WEIGHTED = 32    # problem flag: deal each type's futures to its instances by weight
 NALAR_FORCE_GLOBAL_SWEEP = 1
 NALAR_FORCE_TILED_SORT = 2
+NALAR_FORCE_LEVEL_SWEEP = 4
 NALAR_MAX_INSTANCES = 1024
 NALAR_STATIC_MAX_NODES = 1 << 18       # largest snapshot of nalar_policy_pass_static
 NALAR_STATIC_MAX_WORKFLOWS = 1 << 18

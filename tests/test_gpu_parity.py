@@ -46,6 +46,13 @@ def policy_hbm():
 
 
 @pytest.fixture(scope="module")
+def policy_hbm_levels():
+    """Every workflow in HBM, swept level by level (never the ordered chunk pass)."""
+    with nalar.Policy(flags=nalar.NALAR_FORCE_GLOBAL_SWEEP | nalar.NALAR_FORCE_LEVEL_SWEEP) as p:
+        yield p
+
+
+@pytest.fixture(scope="module")
 def policy_tiled():
     with nalar.Policy(flags=nalar.NALAR_FORCE_TILED_SORT) as p:
         yield p
@@ -122,14 +129,97 @@ def test_random_small_dags(policy, seed):
 
 
 @pytest.mark.parametrize("seed", range(12))
-def test_random_medium_dags(policy, policy_hbm, seed):
+def test_random_medium_dags(policy, policy_hbm, policy_hbm_levels, seed):
     """Several hundred futures per workflow, wide fan-in and fan-out (futures
-    with more dependencies than a thread keeps in registers), ids shuffled."""
+    with more dependencies than a thread keeps in registers), ids shuffled
+    (the HBM sweep then declines the ordered chunk pass) or in topological
+    order (it takes it, with many rounds inside the one chunk)."""
     p = wl.random_dag(500 + seed, n_nodes=600, n_workflows=3, n_instances=40, n_types=6,
                       p_edge=0.02 + 0.01 * (seed % 4), est_max=10**9, load_max=10**12,
                       speed_hi=1 << 30, shuffle_ids=seed % 3 != 0)
     check(policy, p, f"medium seed={seed}")
     check(policy_hbm, p, f"medium seed={seed} hbm")
+    check(policy_hbm_levels, p, f"medium seed={seed} hbm levels")
+
+
+def chunked_workflows(seed, W=3, n=3000, heavy_every=60, p_near=0.3, p_done=0.3, sizes=None):
+    """W workflows of n futures (or of the given sizes) with ids in
+    topological order: each future
+    depends on up to three earlier futures of its workflow, with probability
+    p_near on one of the eight just before it (chains inside a chunk of
+    positions), else anywhere earlier; about one in heavy_every depends on 40
+    to 300 earlier ones (expanded by the whole workgroup).  Workflows above
+    the LDS capacity take the HBM sweep without any flag."""
+    rng = np.random.default_rng(seed)
+    sizes = [n] * W if sizes is None else list(sizes)
+    W = len(sizes)
+    deps = []
+    base = 0
+    for w in range(W):
+        n = sizes[w]
+        if w:
+            base += sizes[w - 1]
+        for i in range(n):
+            if i == 0:
+                deps.append([])
+            elif rng.random() < 1.0 / heavy_every and i >= 40:
+                deps.append((base + rng.choice(i, size=int(rng.integers(40, min(300, i) + 1)),
+                                               replace=False)).tolist())
+            else:
+                k = int(rng.integers(0, 4))
+                near = rng.random(k) < p_near
+                lo = np.maximum(0, i - 1 - rng.integers(0, 8, size=k))
+                far = rng.integers(0, i, size=k)
+                deps.append((base + np.where(near, lo, far)).tolist())
+    N = sum(sizes)
+    counts = np.array([len(d) for d in deps], np.int64)
+    dep_off = np.zeros(N + 1, np.int32)
+    dep_off[1:] = np.cumsum(counts)
+    dep_idx = np.array([x for d in deps for x in d], np.int32)
+    M, K = 24, 5
+    return wl.Problem(f"chunked-{seed}", 1000, 150, np.repeat(np.arange(W), sizes).astype(np.int32),
+                      rng.integers(0, K, size=N).astype(np.int32),
+                      rng.integers(0, 10**6, size=N).astype(np.int64),
+                      (rng.random(N) < p_done).astype(np.uint8),
+                      np.where(rng.random(N) < 0.5, rng.integers(0, M, size=N), -1).astype(np.int32),
+                      dep_off, dep_idx, (1000 + rng.integers(-10**5, 10**7, size=W)).astype(np.int64),
+                      rng.integers(0, K, size=M).astype(np.int32),
+                      rng.integers(0, 10**6, size=M).astype(np.int64),
+                      rng.integers(500, 3000, size=M).astype(np.int32), wf_contiguous=True)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_hbm_ordered_chunks(policy, policy_hbm, policy_hbm_levels, seed):
+    """Workflows of 3,000 and 7,000 futures in topological id order: the
+    ordered chunk pass (in-chunk chains, heavy futures inside a chunk, the
+    last chunk ragged), against the level sweep and the LDS sweep; then the
+    same with ids shuffled, where the ordered pass must decline."""
+    p = chunked_workflows(seed, W=3, n=3000 if seed % 2 == 0 else 7000)
+    check(policy, p, f"chunked seed={seed}")
+    check(policy_hbm, p, f"chunked seed={seed} hbm")
+    check(policy_hbm_levels, p, f"chunked seed={seed} hbm levels")
+    q = wl.relabel(p, np.random.default_rng(seed).permutation(p.n_nodes))
+    check(policy_hbm, q, f"chunked seed={seed} shuffled hbm")
+
+
+def test_hbm_ordered_mixed_sizes(policy, policy_hbm_levels):
+    """Small workflows beside one above the LDS capacity: one launch sweeps
+    them all, the large one by the ordered pass with one future per thread
+    per chunk."""
+    for seed in range(3):
+        p = chunked_workflows(20 + seed, sizes=[50, 700, 9000 + 37 * seed, 1200, 3])
+        check(policy, p, f"mixed sizes seed={seed}")
+        check(policy_hbm_levels, p, f"mixed sizes seed={seed} hbm levels")
+        q = wl.relabel(p, np.random.default_rng(seed).permutation(p.n_nodes))
+        check(policy, q, f"mixed sizes seed={seed} shuffled")
+
+
+def test_hbm_ordered_declines_heavy_chunk(policy_hbm, policy_hbm_levels):
+    """More heavy futures in one chunk than the workgroup's list holds: the
+    ordered pass hands the workflow to the level sweep."""
+    p = chunked_workflows(11, W=2, n=2500, heavy_every=4)
+    check(policy_hbm, p, "heavy chunks hbm")
+    check(policy_hbm_levels, p, "heavy chunks hbm levels")
 
 
 # ---------------------------------------------------------------- workloads
@@ -153,12 +243,14 @@ def test_config_contiguous_flag_not_set(policy):
 
 
 @pytest.mark.parametrize("cfg", [0, 1, 3])
-def test_configs_hbm_sweep(policy_hbm, cfg):
+def test_configs_hbm_sweep(policy_hbm, policy_hbm_levels, cfg):
     check(policy_hbm, wl.CONFIGS[cfg](), f"config{cfg} hbm")
+    check(policy_hbm_levels, wl.CONFIGS[cfg](), f"config{cfg} hbm levels")
 
 
-def test_deep_chains_hbm_small(policy_hbm):
+def test_deep_chains_hbm_small(policy_hbm, policy_hbm_levels):
     check(policy_hbm, wl.deep_chains(W=64), "deep chains W=64 hbm")
+    check(policy_hbm_levels, wl.deep_chains(W=64), "deep chains W=64 hbm levels")
 
 
 def test_deep_chains_hbm_full(policy_hbm):
