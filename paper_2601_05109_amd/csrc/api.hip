@@ -91,6 +91,11 @@ struct Arena {
 // which control blocks and bucket counters are stale).
 struct ArenaState {
   Arena ar;
+  // the ordered HBM sweep's log of pushes into earlier chunks (one entry per
+  // dependency at most): allocated apart from the arena, for this handle's
+  // own passes only (null for the static scratch)
+  void* plog = nullptr;
+  int64_t plog_cap = 0;
   uint32_t epoch = 0;
   uint64_t passes = 0;                 // selects the control block of the next pass
   bool ctrl_dirty[2] = {true, true};
@@ -512,6 +517,7 @@ void nalar_policy_destroy(nalar_policy* h) {
   (void)hipSetDevice(h->device);
   (void)hipStreamSynchronize(h->stream);
   if (h->own.ar.base) (void)hipFree(h->own.ar.base);
+  if (h->own.plog) (void)hipFree(h->own.plog);
   if (h->host) (void)hipHostFree(h->host);
   for (int i = 0; i <= kMaxTimed; ++i)
     if (h->ev[i]) (void)hipEventDestroy(h->ev[i]);
@@ -587,6 +593,26 @@ hipError_t clear_lookback(hipStream_t s, const Arena& A) {
 // buckets of bk), after the checks of the entry point.
 // own_splitters: the arena belongs to the handle, so the bin splitters it
 // holds are this handle's (bins and their splitters are used only then).
+// The push log of the ordered HBM sweep, for E dependencies (grown by a
+// quarter beyond the need, like the arena).
+int ensure_push_log(nalar_policy* h, int64_t E) {
+  ArenaState& as = h->own;
+  if (E <= as.plog_cap) return NALAR_OK;
+  const int64_t cap = E + E / 4;
+  hipError_t e = hipStreamSynchronize(h->stream);
+  if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
+  if (as.plog) (void)hipFree(as.plog);
+  as.plog = nullptr;
+  as.plog_cap = 0;
+  e = hipMalloc(&as.plog, size_t(cap) * (sizeof(int32_t) + sizeof(int64_t)) + 256);
+  if (e != hipSuccess) {
+    as.plog = nullptr;
+    return hip_fail(h, e, "hipMalloc push log");
+  }
+  as.plog_cap = cap;
+  return NALAR_OK;
+}
+
 int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaState& as, BucketArgs bk,
              const SweepShape& sh, bool own_splitters) {
   hipError_t e;
@@ -717,6 +743,11 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
     sw.force_global = (h->flags & NALAR_FORCE_GLOBAL_SWEEP) ? 1 : 0;
     ba.ordered = (h->flags & NALAR_FORCE_LEVEL_SWEEP) ? 0 : 1;
     ba.done_bits = reinterpret_cast<const uint32_t*>(A.done_bits);
+    if (as.plog && as.plog_cap >= p->n_edges) {
+      ba.plog_r = static_cast<int64_t*>(as.plog);
+      ba.plog_lp = reinterpret_cast<int32_t*>(static_cast<char*>(as.plog) + align_up(size_t(as.plog_cap) * 8, 256));
+      ba.plog_cap = as.plog_cap;
+    }
     NALAR_LAUNCH("sweep", launch_sweep(s, sw, ba, sh));
     as.bcnt_clean[nxt] = true;  // the sweep cleared them for the next pass
   }
@@ -1072,6 +1103,10 @@ int nalar_policy_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r) 
   if (h->bin_skip > 0) --h->bin_skip;
   rc = ensure_capacity(h, N, W, bk.nb, records_of(bk));
   if (rc != NALAR_OK) return rc;
+  if (!sh.wave_path && !(h->flags & NALAR_FORCE_LEVEL_SWEEP)) {
+    rc = ensure_push_log(h, p->n_edges);
+    if (rc != NALAR_OK) return rc;
+  }
   return run_pass(h, p, r, h->own, bk, sh, true);
 }
 

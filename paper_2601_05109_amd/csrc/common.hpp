@@ -55,6 +55,7 @@ struct Ctrl {
   int64_t slack_max;
   int64_t hint_min;              // the range the host plans the next buckets from
   int64_t hint_max;              //   (the key range)
+  uint64_t plog_fill;            // entries of the push log taken by the ordered HBM sweep
   uint32_t tile_ticket[16];      // per radix pass: [0,9) slack sort, [9,13) grouping
   int64_t part_min[kParts];
   int64_t part_max[kParts];
@@ -164,6 +165,7 @@ __device__ inline void reset_ctrl(Ctrl* c) {
     c->n_ready = 0;
     c->slack_min = INT64_MAX;
     c->slack_max = INT64_MIN;
+    c->plog_fill = 0;
   }
   for (int i = tid; i < 16; i += blockDim.x) c->tile_ticket[i] = 0;
   for (int i = tid; i < kParts; i += blockDim.x) {
@@ -189,6 +191,7 @@ __device__ inline void reset_ctrl_spread(Ctrl* c, int64_t gi, int64_t gstride) {
     c->n_ready = 0;
     c->slack_min = INT64_MAX;
     c->slack_max = INT64_MIN;
+    c->plog_fill = 0;
   }
   for (int64_t i = gi; i < 16; i += gstride) c->tile_ticket[i] = 0;
   for (int64_t i = gi; i < kParts; i += gstride) {

@@ -141,6 +141,9 @@ struct SweepArgs {
 struct BlockSweepArgs {
   const uint32_t* done_bits;    // [N bits] done flags, one bit per future
   int ordered;                  // workflows kept in HBM may take the ordered chunk pass
+  int64_t* plog_r;              // [plog_cap] the ordered pass's pushes into earlier chunks:
+  int32_t* plog_lp;             //   value and target position (null: no log, no ordered pass)
+  int64_t plog_cap;
 };
 
 // Load-aware routing over the ordered ready futures (greedy.hip).

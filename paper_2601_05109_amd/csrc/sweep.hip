@@ -894,69 +894,68 @@ __device__ inline bool done_bit(const uint32_t* bits, int32_t v) {
 // A workflow in HBM whose every dependency lies at a lower position than its
 // consumer (ids in topological order within the workflow, as when futures are
 // appended after their dependencies) needs no out-degree counters and no
-// frontiers: taking its positions in chunks from the last chunk to the first,
-// every consumer of a future in an earlier chunk has already pushed its rem
-// when that chunk is reached.  Inside a chunk, a future waits until its
-// consumers in the same chunk (counted beforehand, in LDS) have pushed; these
-// rounds end because the pending future at the highest position never waits.
-// A workflow of n futures costs about n / (T x P) chunks of a few dependent
-// round trips each, instead of a counter pass plus one frontier round per
-// level with random accesses to per-position state.  A thread takes P
-// futures of each chunk (T x P positions), their loads issued together.
-// P = kOrdP = 1: the block kernel also holds the LDS sweep, whose registers
-// this path shares; with P = 4 it spills, and a kernel of its own (512
-// threads, P = 4, no spills) measured slower than P = 1 here.
-constexpr int kOrdP = 1;
+// frontiers: taking its positions in chunks of T from the last chunk to the
+// first, every consumer of a future in an earlier chunk has already pushed its
+// rem when that chunk is reached.  Inside a chunk, a future waits until its
+// consumers in the same chunk (counted beforehand) have pushed; these rounds
+// end because the pending future at the highest position never waits.
 //
-// Returns false, having written only its own scratch (mx and the in-chunk
-// counters), when some dependency does not lie lower; the caller then runs
-// the level-synchronous sweep.  lc: T x P ints of LDS.
-template <int T, int P>
+// The chunk being swept keeps its futures' running maxima in LDS.  A push
+// into an earlier chunk is not an atomic on a random line of HBM: it is
+// appended to that chunk's segment of a log (the segments sized by a count
+// taken with the order check), and the chunk folds its segment into LDS when
+// its turn comes.  A workflow of n futures costs about n / T chunks of a few
+// round trips each, plus one write and one read of 12 bytes per dependency.
+//
+// Returns false, having written only its own scratch (the in-chunk counters),
+// when some dependency does not lie lower, when there is no log, or when the
+// chunk table does not fit; the caller then runs the level-synchronous sweep.
+// lc: T ints of LDS; mxl: lds_cap int64 of LDS (T maxima, then the table).
+template <int T>
 __device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs& a, const Layout& L, const ITabLds& it,
                                                                  const BlockSweepArgs& ba, Shared& S, int64_t b, int n,
                                                                  int64_t dl, int lvl, Acc& acc, const int64_t* split_l,
-                                                                 int32_t* lc) {
-  constexpr int C = T * P;  // positions per chunk
+                                                                 int32_t* lc, int64_t* mxl, int lds_cap) {
   const int tid = threadIdx.x;
   Ctrl* ctrl = a.ctrl;
-  int32_t* cnt = a.g_cnt + b;  // consumers in the same chunk, by position
-  int64_t* mx = a.g_mx + b;
-  if (tid == 0) { S.bad = 0; S.hcount = 0; }
+  const int nc = (n + T - 1) / T;
+  if (ba.plog_lp == nullptr || T + nc > lds_cap || nc > 4 * T) return false;  // the same on every thread
+  uint32_t* cseg = reinterpret_cast<uint32_t*>(mxl + T);  // [nc] pushes into each chunk, then its segment's start
+  uint32_t* cfill = cseg + nc;                             // [nc] pushes appended to each segment so far
+  int32_t* cnt = a.g_cnt + b;                              // consumers in the same chunk, by position
+  __shared__ int64_t s_base;
+  __shared__ uint32_t s_total;
 
-  // 1: chunk by chunk, check the order, count in-chunk consumers, clear mx
-  for (int c0 = 0; c0 < n; c0 += C) {
-    int32_t v[P], off[P], deg[P];
-#pragma unroll
-    for (int j = 0; j < P; ++j) {
-      const int k = c0 + j * T + tid;
-      v[j] = k < n ? node_at(L, b + k) : 0;
-      lc[j * T + tid] = 0;
+  // 1: chunk by chunk, check the order and count each dependency's push: into
+  // its own chunk's counter if the consumer is in the same chunk, else into
+  // the count of its chunk's segment
+  if (tid == 0) { S.bad = 0; S.hcount = 0; }
+  for (int i = tid; i < nc; i += T) { cseg[i] = 0; cfill[i] = 0; }
+  for (int c0 = 0; c0 < n; c0 += T) {
+    const int k = c0 + tid;
+    const bool own = k < n;
+    int32_t v = 0, off = 0, deg = 0;
+    if (own) {
+      v = node_at(L, b + k);
+      off = a.p.dep_off[v];
+      deg = a.p.dep_off[v + 1] - off;
     }
-#pragma unroll
-    for (int j = 0; j < P; ++j) {
-      const bool own = c0 + j * T + tid < n;
-      off[j] = own ? a.p.dep_off[v[j]] : 0;
-      deg[j] = own ? a.p.dep_off[v[j] + 1] - off[j] : 0;
-    }
+    lc[tid] = 0;
     __syncthreads();
     bool up = false;
-#pragma unroll
-    for (int j = 0; j < P; ++j) {
-      const int k = c0 + j * T + tid;
-      if (k >= n) continue;
-      if (deg[j] <= kHbmLight) {
-        for (int e = 0; e < deg[j]; ++e) {
-          const int32_t lp = checked_dep(L, a.p.dep_idx[off[j] + e], b, n, k, ctrl);
-          if (lp > k) up = true;
-          else if (lp >= c0) atomicAdd(&lc[lp - c0], 1);
-        }
+    if (own && deg <= kHbmLight) {
+      for (int e = 0; e < deg; ++e) {
+        const int32_t lp = checked_dep(L, a.p.dep_idx[off + e], b, n, k, ctrl);
+        if (lp > k) up = true;
+        else if (lp >= c0) atomicAdd(&lc[lp - c0], 1);
+        else if (lp >= 0) atomicAdd(&cseg[lp / T], 1u);
+      }
+    } else if (own) {
+      const int slot = atomicAdd(&S.hcount, 1);
+      if (slot < kHeavyCap) {
+        S.hk[slot] = k; S.ho[slot] = off; S.hd[slot] = deg;
       } else {
-        const int slot = atomicAdd(&S.hcount, 1);
-        if (slot < kHeavyCap) {
-          S.hk[slot] = k; S.ho[slot] = off[j]; S.hd[slot] = deg[j];
-        } else {
-          up = true;  // more heavy futures in one chunk than the list holds
-        }
+        up = true;  // more heavy futures in one chunk than the list holds
       }
     }
     if (up) S.bad = 1;
@@ -968,153 +967,147 @@ __device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs
         const int32_t lp = checked_dep(L, a.p.dep_idx[ho + e], b, n, hk, ctrl);
         if (lp > hk) S.bad = 1;
         else if (lp >= c0) atomicAdd(&lc[lp - c0], 1);
+        else if (lp >= 0) atomicAdd(&cseg[lp / T], 1u);
       }
     }
     __syncthreads();
-#pragma unroll
-    for (int j = 0; j < P; ++j) {
-      const int k = c0 + j * T + tid;
-      if (k < n) {
-        st_wg(&cnt[k], lc[j * T + tid]);
-        st_wg(&mx[k], int64_t(0));
-      }
-    }
+    if (own) st_wg(&cnt[k], lc[tid]);
     if (tid == 0) S.hcount = 0;
   }
   __syncthreads();
   const bool unordered = S.bad != 0;
-  __syncthreads();  // every thread has read the flag before the caller reuses it
-  if (unordered) return false;
+
+  // the segments: an exclusive scan of the counts (up to four per thread),
+  // and one stretch of the log for the whole workflow
+  {
+    constexpr int Q = 4;
+    const int q = (nc + T - 1) / T;
+    uint32_t x[Q], sum = 0;
+#pragma unroll
+    for (int j = 0; j < Q; ++j) {
+      const int i = tid * q + j;
+      x[j] = j < q && i < nc ? cseg[i] : 0u;
+      sum += x[j];
+    }
+    const uint32_t inc = wave_incl_scan_u32(sum);
+    if (lane_id() == kWave - 1) S.hk[tid / kWave] = int32_t(inc);
+    __syncthreads();
+    uint32_t run = 0;
+    for (int w = 0; w < tid / kWave; ++w) run += uint32_t(S.hk[w]);
+    run += inc - sum;
+#pragma unroll
+    for (int j = 0; j < Q; ++j) {
+      const int i = tid * q + j;
+      if (j < q && i < nc) cseg[i] = run;
+      run += x[j];
+    }
+    if (tid == T - 1) {
+      s_total = run;
+      s_base = unordered ? 0 : int64_t(atomicAdd(reinterpret_cast<unsigned long long*>(&ctrl->plog_fill),
+                                                 (unsigned long long)run));
+    }
+    __syncthreads();
+  }
+  const uint32_t total = s_total;
+  const int64_t base = s_base;
+  __syncthreads();  // every thread has read the flags before the caller reuses them
+  if (unordered || base + int64_t(total) > ba.plog_cap) return false;
+  int64_t* pr = ba.plog_r + base;
+  int32_t* plp = ba.plog_lp + base;
+
+  // a push of r into the future at position lp (lp < the consumer's)
+  auto push = [&](int32_t lp, int64_t r, int c0) {
+    if (lp >= c0) {
+      atomicMax(reinterpret_cast<long long*>(&mxl[lp - c0]), (long long)r);
+      atomicSub(&lc[lp - c0], 1);
+    } else {
+      const int cj = lp / T;
+      const uint32_t at = cseg[cj] + atomicAdd(&cfill[cj], 1u);
+      const uint32_t end = cj + 1 < nc ? cseg[cj + 1] : total;
+      if (at < end) {
+        plp[at] = lp;
+        pr[at] = r;
+      } else {
+        flag_sweep(ctrl, kStCycle);  // cannot happen: the counts above are exact
+      }
+    }
+  };
 
   // 2: the chunks from the last to the first.  Everything a future needs
   // except its consumers' max is loaded when its chunk starts (its first two
-  // dependencies, their positions and done flags), so that a round waits on
-  // the loads of the maxima, then on those of the futures that turned out
-  // ready and on their bucket-slot atomics.
+  // dependencies, their positions and done flags), while the chunk folds in
+  // the pushes its futures received from later chunks.
   bool overflow = false;
-  for (int c0 = ((n - 1) / C) * C; c0 >= 0; c0 -= C) {
-    int32_t v[P], off[P], deg[P], p0[P], p1[P], lp0[P], lp1[P];
-    int64_t est[P];
-    uint32_t own = 0, light = 0, dn = 0, blocked = 0;
-#pragma unroll
-    for (int j = 0; j < P; ++j) {
-      const int k = c0 + j * T + tid;
-      if (k < n) own |= 1u << j;
-      v[j] = k < n ? node_at(L, b + k) : 0;
+  for (int c0 = ((n - 1) / T) * T; c0 >= 0; c0 -= T) {
+    const int k = c0 + tid;
+    const bool own = k < n;
+    int32_t v = 0, off = 0, deg = 0;
+    bool dnk = true;
+    int64_t est = 0;
+    if (own) {
+      v = node_at(L, b + k);
+      off = a.p.dep_off[v];
+      deg = a.p.dep_off[v + 1] - off;
+      dnk = done_bit(ba.done_bits, v);
+      est = a.p.est[v];
+      lc[tid] = ld_wg(&cnt[k]);
     }
-#pragma unroll
-    for (int j = 0; j < P; ++j) {
-      const int k = c0 + j * T + tid;
-      const bool o = (own >> j) & 1u;
-      off[j] = o ? a.p.dep_off[v[j]] : 0;
-      deg[j] = o ? a.p.dep_off[v[j] + 1] - off[j] : 0;
-      if (!o || done_bit(ba.done_bits, v[j])) dn |= 1u << j;
-      est[j] = o ? a.p.est[v[j]] : 0;
-      if (o) lc[j * T + tid] = ld_wg(&cnt[k]);
-    }
-#pragma unroll
-    for (int j = 0; j < P; ++j) {
-      if (((own >> j) & 1u) && deg[j] <= kHbmLight) light |= 1u << j;
-      const bool l = (light >> j) & 1u;
-      p0[j] = l && deg[j] > 0 ? a.p.dep_idx[off[j]] : 0;
-      p1[j] = l && deg[j] > 1 ? a.p.dep_idx[off[j] + 1] : 0;
-    }
-#pragma unroll
-    for (int j = 0; j < P; ++j) {
-      const int k = c0 + j * T + tid;
-      const bool l = (light >> j) & 1u;
-      lp0[j] = l && deg[j] > 0 ? local_of(L, p0[j], b, n) : -1;
-      lp1[j] = l && deg[j] > 1 ? local_of(L, p1[j], b, n) : -1;
-      if (lp0[j] == k) lp0[j] = -1;  // reported by the first step
-      if (lp1[j] == k) lp1[j] = -1;
-    }
-#pragma unroll
-    for (int j = 0; j < P; ++j) {
-      const bool bl0 = lp0[j] >= 0 && !done_bit(ba.done_bits, p0[j]);
-      const bool bl1 = lp1[j] >= 0 && !done_bit(ba.done_bits, p1[j]);
-      if (bl0 || bl1) blocked |= 1u << j;
-    }
-    uint32_t pending = own;
+    const bool light = own && deg <= kHbmLight;
+    int32_t p0 = 0, p1 = 0, lp0 = -1, lp1 = -1;
+    if (light && deg > 0) p0 = a.p.dep_idx[off];
+    if (light && deg > 1) p1 = a.p.dep_idx[off + 1];
+    if (light && deg > 0) lp0 = local_of(L, p0, b, n);
+    if (light && deg > 1) lp1 = local_of(L, p1, b, n);
+    if (lp0 == k) lp0 = -1;  // reported by the first step
+    if (lp1 == k) lp1 = -1;
+    bool blocked = false;
+    if (lp0 >= 0) blocked |= !done_bit(ba.done_bits, p0);
+    if (lp1 >= 0) blocked |= !done_bit(ba.done_bits, p1);
+    mxl[tid] = 0;
     if (tid == 0) { S.fcount = 0; S.hcount = 0; }
     __syncthreads();
+    {
+      const int ci = c0 / T;
+      const uint32_t s0 = cseg[ci], s1 = s0 + cfill[ci];
+      for (uint32_t i = s0 + uint32_t(tid); i < s1; i += T) {
+        const int32_t lp = plp[i];
+        atomicMax(reinterpret_cast<long long*>(&mxl[lp - c0]), (long long)pr[i]);
+      }
+    }
+    bool pending = own;
+    __syncthreads();
     for (int round = 0;; ++round) {
-      uint32_t go = 0;
-#pragma unroll
-      for (int j = 0; j < P; ++j)
-        if (((pending >> j) & 1u) && lc[j * T + tid] == 0) go |= 1u << j;
+      const bool go = pending && lc[tid] == 0;
       __syncthreads();  // every count is read before this round's pushes
-      pending &= ~go;
-      int64_t r[P];
-#pragma unroll
-      for (int j = 0; j < P; ++j) r[j] = ((go >> j) & 1u) ? ld_wg(&mx[c0 + j * T + tid]) : 0;
-      uint32_t rd = 0;
-#pragma unroll
-      for (int j = 0; j < P; ++j) {
-        if (!((go >> j) & 1u)) continue;
-        const int k = c0 + j * T + tid;
-        r[j] = clamp_rem((((dn >> j) & 1u) ? 0 : est[j]) + r[j], overflow);
-        st_wg(&mx[k], r[j]);
-        if (a.rem_out) a.rem_out[v[j]] = r[j];
-        if (!((light >> j) & 1u)) {
+      if (go) {
+        pending = false;
+        const int64_t r = clamp_rem((dnk ? 0 : est) + mxl[tid], overflow);
+        mxl[tid] = r;
+        if (a.rem_out) a.rem_out[v] = r;
+        if (light) {
+          if (lp0 >= 0) push(lp0, r, c0);
+          if (lp1 >= 0) push(lp1, r, c0);
+          for (int e = 2; e < deg; ++e) {
+            const int32_t p = a.p.dep_idx[off + e];
+            const int32_t lp = local_of(L, p, b, n);
+            if (lp < 0 || lp == k) continue;
+            blocked |= !done_bit(ba.done_bits, p);
+            push(lp, r, c0);
+          }
+          const bool rd = !dnk && !blocked;
+          if (a.bk.nb == 0) a.stg_ready[b + k] = rd ? uint8_t(1 + lvl) : 0;
+          if (rd) write_ready<false>(a, it, b + k, a.p.type[v], a.p.loc[v], r, est, dl, lvl, acc, split_l);
+        } else {
           const int slot = atomicAdd(&S.hcount, 1);  // below kHeavyCap: checked by the first step
-          S.hk[slot] = k; S.ho[slot] = off[j]; S.hd[slot] = deg[j];
-          continue;
+          S.hk[slot] = k; S.ho[slot] = off; S.hd[slot] = deg;
         }
-        if (lp0[j] >= 0) {
-          max_wg(&mx[lp0[j]], r[j]);
-          if (lp0[j] >= c0) atomicSub(&lc[lp0[j] - c0], 1);
-        }
-        if (lp1[j] >= 0) {
-          max_wg(&mx[lp1[j]], r[j]);
-          if (lp1[j] >= c0) atomicSub(&lc[lp1[j] - c0], 1);
-        }
-        for (int e = 2; e < deg[j]; ++e) {
-          const int32_t p = a.p.dep_idx[off[j] + e];
-          const int32_t lp = local_of(L, p, b, n);
-          if (lp < 0 || lp == k) continue;
-          if (!done_bit(ba.done_bits, p)) blocked |= 1u << j;
-          max_wg(&mx[lp], r[j]);
-          if (lp >= c0) atomicSub(&lc[lp - c0], 1);
-        }
-        const bool ready = !((dn >> j) & 1u) && !((blocked >> j) & 1u);
-        if (a.bk.nb == 0) a.stg_ready[b + k] = ready ? uint8_t(1 + lvl) : 0;
-        if (ready) rd |= 1u << j;
-      }
-      // the ready futures: their type and location, every bucket-slot atomic,
-      // the routing while they are in flight, then the stores
-      int64_t key[P];
-      uint32_t bkt[P], slot[P];
-      int32_t ty[P], lo[P];
-#pragma unroll
-      for (int j = 0; j < P; ++j) {
-        ty[j] = ((rd >> j) & 1u) ? a.p.type[v[j]] : 0;
-        lo[j] = ((rd >> j) & 1u) ? a.p.loc[v[j]] : -1;
-      }
-#pragma unroll
-      for (int j = 0; j < P; ++j) {
-        key[j] = order_key(a, r[j], dl);
-        bkt[j] = 0;
-        slot[j] = 0;
-        if (((rd >> j) & 1u) && a.bk.nb > 0) {
-          bkt[j] = a.bk.bins ? bin_of(split_l, a.bk.nb, key[j]) : bucket_of<false>(a.bk, key[j], lvl);
-          slot[j] = add_agent(a.bk.cnt + bkt[j], 1u);
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < P; ++j) {
-        if (!((rd >> j) & 1u)) continue;
-        int32_t route;
-        int64_t cost;
-        route_future(ty[j], est[j], lo[j], int32_t(a.p.M), a.p.mig, it.type, it.idx, it.load, it.speed,
-                     it.inv, it.pos, it.run, (a.p.policy & NALAR_ROUTE_STATEFUL) != 0, route, cost, it.prun);
-        store_ready(a, bkt[j], slot[j], key[j], lvl, dl - r[j], b + c0 + j * T + tid, route, cost, acc);
       }
       if (pending) atomicAdd(&S.fcount, 1);
       __syncthreads();
       const int hc = S.hcount;
       for (int h = 0; h < hc; ++h) {  // heavy futures: the workgroup pushes together
         const int hk = S.hk[h], ho = S.ho[h], hd = S.hd[h];
-        const int64_t hr = ld_wg(&mx[hk]);
+        const int64_t hr = mxl[hk - c0];
         if (tid == 0) S.proc = 0;
         __syncthreads();
         bool hb = false;
@@ -1123,23 +1116,22 @@ __device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs
           const int32_t lp = local_of(L, p, b, n);
           if (lp < 0 || lp == hk) continue;
           hb |= !done_bit(ba.done_bits, p);
-          max_wg(&mx[lp], hr);
-          if (lp >= c0) atomicSub(&lc[lp - c0], 1);
+          push(lp, hr, c0);
         }
         if (hb) S.proc = 1;
         __syncthreads();
         if (tid == 0) {
           const int32_t hv = node_at(L, b + hk);
-          const bool ready = !done_bit(ba.done_bits, hv) && S.proc == 0;
-          if (a.bk.nb == 0) a.stg_ready[b + hk] = ready ? uint8_t(1 + lvl) : 0;
-          if (ready) write_ready<false>(a, it, b + hk, a.p.type[hv], a.p.loc[hv], hr, a.p.est[hv], dl, lvl, acc, split_l);
+          const bool rd = !done_bit(ba.done_bits, hv) && S.proc == 0;
+          if (a.bk.nb == 0) a.stg_ready[b + hk] = rd ? uint8_t(1 + lvl) : 0;
+          if (rd) write_ready<false>(a, it, b + hk, a.p.type[hv], a.p.loc[hv], hr, a.p.est[hv], dl, lvl, acc, split_l);
         }
       }
       __syncthreads();
       const int pend = S.fcount;
       __syncthreads();  // every thread has read the counts before they are reset
       if (pend == 0) break;
-      if (round > C) {  // cannot happen: some pending future never waits
+      if (round > T) {  // cannot happen: some pending future never waits
         if (tid == 0) flag_sweep(ctrl, kStCycle);
         break;
       }
@@ -1780,8 +1772,7 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a, int lds_cap, BlockSwee
     lmask |= level_bit(lvl);
     if (!a.force_global && n <= lds_cap)
       sweep_lds<T, NPT>(a, L, it, S, mx, cnt, dn, nr, lds_cap, b, n, dl, lvl, acc, bl);
-    else if (!(ba.ordered && lds_cap >= T * kOrdP &&
-               sweep_hbm_ordered<T, kOrdP>(a, L, it, ba, S, b, n, dl, lvl, acc, split_l, cnt)))
+    else if (!(ba.ordered && sweep_hbm_ordered<T>(a, L, it, ba, S, b, n, dl, lvl, acc, split_l, cnt, mx, lds_cap)))
       sweep_hbm<T, false, false>(a, L, it, S, int(w), b, n, dl, lvl, acc, split_l);
   }
 
