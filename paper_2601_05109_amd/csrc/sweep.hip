@@ -1036,8 +1036,13 @@ __device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs
   // 2: the chunks from the last to the first.  Everything a future needs
   // except its consumers' max is loaded when its chunk starts (its first two
   // dependencies, their positions and done flags), while the chunk folds in
-  // the pushes its futures received from later chunks.
+  // the pushes its futures received from later chunks.  A thread's ready
+  // future is routed and stored while the loads of its next chunk are in
+  // flight, off the rounds' critical path.
   bool overflow = false;
+  bool prd = false;  // the thread's ready future of the previous chunk, not yet stored
+  int32_t pty = 0, plo = -1;
+  int64_t prem = 0, pest = 0, ppos = 0;
   for (int c0 = ((n - 1) / T) * T; c0 >= 0; c0 -= T) {
     const int k = c0 + tid;
     const bool own = k < n;
@@ -1063,6 +1068,10 @@ __device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs
     bool blocked = false;
     if (lp0 >= 0) blocked |= !done_bit(ba.done_bits, p0);
     if (lp1 >= 0) blocked |= !done_bit(ba.done_bits, p1);
+    if (prd) {
+      write_ready<false>(a, it, ppos, pty, plo, prem, pest, dl, lvl, acc, split_l);
+      prd = false;
+    }
     mxl[tid] = 0;
     if (tid == 0) { S.fcount = 0; S.hcount = 0; }
     __syncthreads();
@@ -1096,7 +1105,14 @@ __device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs
           }
           const bool rd = !dnk && !blocked;
           if (a.bk.nb == 0) a.stg_ready[b + k] = rd ? uint8_t(1 + lvl) : 0;
-          if (rd) write_ready<false>(a, it, b + k, a.p.type[v], a.p.loc[v], r, est, dl, lvl, acc, split_l);
+          if (rd) {  // stored at the next chunk's start
+            prd = true;
+            pty = a.p.type[v];
+            plo = a.p.loc[v];
+            prem = r;
+            pest = est;
+            ppos = b + k;
+          }
         } else {
           const int slot = atomicAdd(&S.hcount, 1);  // below kHeavyCap: checked by the first step
           S.hk[slot] = k; S.ho[slot] = off; S.hd[slot] = deg;
@@ -1138,6 +1154,7 @@ __device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs
       if (tid == 0) { S.fcount = 0; S.hcount = 0; }
     }
   }
+  if (prd) write_ready<false>(a, it, ppos, pty, plo, prem, pest, dl, lvl, acc, split_l);
   if (overflow) flag_sweep(ctrl, kStRange);
   __syncthreads();
   return true;
