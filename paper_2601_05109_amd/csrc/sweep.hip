@@ -885,6 +885,10 @@ __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, con
 
 // ------------------------------------------------------------ ordered workflow
 
+// Futures a thread carries through one step of the ordered pass's counting,
+// their loads issued together.
+constexpr int kHbmU = 4;
+
 // Future v's done flag from the packed copy the node kernel wrote (1.5 MB per
 // 12M futures, so that the random reads of dependencies' flags stay in L2).
 __device__ inline bool done_bit(const uint32_t* bits, int32_t v) {
@@ -926,53 +930,65 @@ __device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs
   __shared__ int64_t s_base;
   __shared__ uint32_t s_total;
 
-  // 1: chunk by chunk, check the order and count each dependency's push: into
-  // its own chunk's counter if the consumer is in the same chunk, else into
-  // the count of its chunk's segment
-  if (tid == 0) { S.bad = 0; S.hcount = 0; }
+  // 1: check the order and count each dependency's push: into its own
+  // counter (HBM, by position) if the consumer is in the same chunk, else into
+  // the count of its chunk's segment (LDS).  No chunk order is needed here:
+  // kHbmU futures per thread, their loads issued together.
+  for (int k = tid; k < n; k += T) st_wg(&cnt[k], int32_t(0));
   for (int i = tid; i < nc; i += T) { cseg[i] = 0; cfill[i] = 0; }
-  for (int c0 = 0; c0 < n; c0 += T) {
-    const int k = c0 + tid;
-    const bool own = k < n;
-    int32_t v = 0, off = 0, deg = 0;
-    if (own) {
-      v = node_at(L, b + k);
-      off = a.p.dep_off[v];
-      deg = a.p.dep_off[v + 1] - off;
+  if (tid == 0) { S.bad = 0; S.hcount = 0; }
+  __syncthreads();
+  // a dependency at position lp of the future at position k
+  auto count = [&](int32_t lp, int k) -> bool {
+    if (lp > k) return true;  // not below its consumer: not ordered
+    if (lp >= (k / T) * T) add_wg(&cnt[lp], int32_t(1));
+    else if (lp >= 0) atomicAdd(&cseg[lp / T], 1u);
+    return false;
+  };
+  bool up = false;
+  for (int k0 = 0; k0 < n; k0 += T * kHbmU) {
+    int32_t v[kHbmU], off[kHbmU], deg[kHbmU], d0[kHbmU];
+#pragma unroll
+    for (int j = 0; j < kHbmU; ++j) {
+      const int k = k0 + j * T + tid;
+      v[j] = k < n ? node_at(L, b + k) : 0;
     }
-    lc[tid] = 0;
-    __syncthreads();
-    bool up = false;
-    if (own && deg <= kHbmLight) {
-      for (int e = 0; e < deg; ++e) {
-        const int32_t lp = checked_dep(L, a.p.dep_idx[off + e], b, n, k, ctrl);
-        if (lp > k) up = true;
-        else if (lp >= c0) atomicAdd(&lc[lp - c0], 1);
-        else if (lp >= 0) atomicAdd(&cseg[lp / T], 1u);
+#pragma unroll
+    for (int j = 0; j < kHbmU; ++j) {
+      const bool own = k0 + j * T + tid < n;
+      off[j] = own ? a.p.dep_off[v[j]] : 0;
+      deg[j] = own ? a.p.dep_off[v[j] + 1] - off[j] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < kHbmU; ++j)
+      d0[j] = deg[j] > 0 && deg[j] <= kHbmLight ? a.p.dep_idx[off[j]] : 0;
+#pragma unroll
+    for (int j = 0; j < kHbmU; ++j) {
+      const int k = k0 + j * T + tid;
+      if (deg[j] <= 0) continue;
+      if (deg[j] <= kHbmLight) {
+        up |= count(checked_dep(L, d0[j], b, n, k, ctrl), k);
+        for (int e = 1; e < deg[j]; ++e) up |= count(checked_dep(L, a.p.dep_idx[off[j] + e], b, n, k, ctrl), k);
+        continue;
       }
-    } else if (own) {
       const int slot = atomicAdd(&S.hcount, 1);
       if (slot < kHeavyCap) {
-        S.hk[slot] = k; S.ho[slot] = off; S.hd[slot] = deg;
-      } else {
-        up = true;  // more heavy futures in one chunk than the list holds
+        S.hk[slot] = k; S.ho[slot] = off[j]; S.hd[slot] = deg[j];
+      } else {  // the list is full: this thread counts them itself
+        for (int e = 0; e < deg[j]; ++e) up |= count(checked_dep(L, a.p.dep_idx[off[j] + e], b, n, k, ctrl), k);
       }
     }
-    if (up) S.bad = 1;
-    __syncthreads();
+  }
+  if (up) S.bad = 1;
+  __syncthreads();
+  {
     const int hc = S.hcount < kHeavyCap ? S.hcount : kHeavyCap;
+    bool hup = false;
     for (int h = 0; h < hc; ++h) {
       const int hk = S.hk[h], ho = S.ho[h], hd = S.hd[h];
-      for (int e = tid; e < hd; e += T) {
-        const int32_t lp = checked_dep(L, a.p.dep_idx[ho + e], b, n, hk, ctrl);
-        if (lp > hk) S.bad = 1;
-        else if (lp >= c0) atomicAdd(&lc[lp - c0], 1);
-        else if (lp >= 0) atomicAdd(&cseg[lp / T], 1u);
-      }
+      for (int e = tid; e < hd; e += T) hup |= count(checked_dep(L, a.p.dep_idx[ho + e], b, n, hk, ctrl), hk);
     }
-    __syncthreads();
-    if (own) st_wg(&cnt[k], lc[tid]);
-    if (tid == 0) S.hcount = 0;
+    if (hup) S.bad = 1;
   }
   __syncthreads();
   const bool unordered = S.bad != 0;
@@ -1093,10 +1109,15 @@ __device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs
         const int64_t r = clamp_rem((dnk ? 0 : est) + mxl[tid], overflow);
         mxl[tid] = r;
         if (a.rem_out) a.rem_out[v] = r;
-        if (light) {
+        // a heavy future goes to the workgroup's list; when that is full, its
+        // thread pushes alone, as for a light one
+        const int slot = light ? -1 : atomicAdd(&S.hcount, 1);
+        if (slot >= 0 && slot < kHeavyCap) {
+          S.hk[slot] = k; S.ho[slot] = off; S.hd[slot] = deg;
+        } else {
           if (lp0 >= 0) push(lp0, r, c0);
           if (lp1 >= 0) push(lp1, r, c0);
-          for (int e = 2; e < deg; ++e) {
+          for (int e = light ? 2 : 0; e < deg; ++e) {
             const int32_t p = a.p.dep_idx[off + e];
             const int32_t lp = local_of(L, p, b, n);
             if (lp < 0 || lp == k) continue;
@@ -1113,14 +1134,11 @@ __device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs
             pest = est;
             ppos = b + k;
           }
-        } else {
-          const int slot = atomicAdd(&S.hcount, 1);  // below kHeavyCap: checked by the first step
-          S.hk[slot] = k; S.ho[slot] = off; S.hd[slot] = deg;
         }
       }
       if (pending) atomicAdd(&S.fcount, 1);
       __syncthreads();
-      const int hc = S.hcount;
+      const int hc = S.hcount < kHeavyCap ? S.hcount : kHeavyCap;
       for (int h = 0; h < hc; ++h) {  // heavy futures: the workgroup pushes together
         const int hk = S.hk[h], ho = S.ho[h], hd = S.hd[h];
         const int64_t hr = mxl[hk - c0];

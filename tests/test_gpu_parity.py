@@ -214,9 +214,9 @@ def test_hbm_ordered_mixed_sizes(policy, policy_hbm_levels):
         check(policy, q, f"mixed sizes seed={seed} shuffled")
 
 
-def test_hbm_ordered_declines_heavy_chunk(policy_hbm, policy_hbm_levels):
+def test_hbm_ordered_many_heavy(policy_hbm, policy_hbm_levels):
     """More heavy futures in one chunk than the workgroup's list holds: the
-    ordered pass hands the workflow to the level sweep."""
+    ones past it are pushed by their own threads."""
     p = chunked_workflows(11, W=2, n=2500, heavy_every=4)
     check(policy_hbm, p, "heavy chunks hbm")
     check(policy_hbm_levels, p, "heavy chunks hbm levels")
