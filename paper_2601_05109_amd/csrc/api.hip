@@ -917,8 +917,14 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
 
 void nalar::policy_split_any(nalar_policy* h, bool on) { h->split_any = on; }
 
-int nalar::policy_reserve(nalar_policy* h, int64_t N, int64_t W) {
+int nalar::policy_reserve(nalar_policy* h, int64_t N, int64_t E, int64_t W) {
   const Arena& a = h->own.ar;
+  if (h->own.plog && E > h->own.plog_cap) {  // once a pass has used it, the push log follows the graph
+    hipError_t e = hipSetDevice(h->device);
+    if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+    const int rc = ensure_push_log(h, E);
+    if (rc != NALAR_OK) return rc;
+  }
   if (!a.base || (N <= a.capN && W <= a.capW)) return NALAR_OK;  // the first pass sizes it
   hipError_t e = hipSetDevice(h->device);
   if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");

@@ -293,7 +293,7 @@ void policy_split_any(nalar_policy* h, bool on);
 // Grows the handle's pass arena ahead of a pass over N futures of W
 // workflows (geometrically, like the pass itself), so that a store reallocates
 // while taking in its deltas rather than inside a pass.
-int policy_reserve(nalar_policy* h, int64_t N, int64_t W);
+int policy_reserve(nalar_policy* h, int64_t N, int64_t E, int64_t W);
 
 // Handle accessors for the graph store (store.hip), defined in api.hip.
 hipStream_t policy_stream(const nalar_policy* h);

@@ -259,7 +259,7 @@ int nalar_store_append(nalar_store* st, int64_t n_new, int64_t n_new_edges, cons
   // the per-future buffers of the next pass grow here, with the store, and
   // not inside the pass
   int rc = ensure_incremental(st);
-  if (rc == NALAR_OK) rc = policy_reserve(st->h, st->N, st->W);
+  if (rc == NALAR_OK) rc = policy_reserve(st->h, st->N, st->E, st->W);
   return rc;
 }
 
