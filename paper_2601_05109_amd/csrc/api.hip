@@ -708,6 +708,7 @@ int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaStat
     g.epoch = epoch;
     g.pos_of_node = A.pos_of_node;
     g.wf_off = A.wf_off;
+    g.cap_n = A.capN > 0 ? A.capN : 1;
     e = launch_group(s, g, Timer::cb, &tm);
     if (e != hipSuccess) return hip_fail(h, e, "group");
     node_of_pos = reinterpret_cast<const int32_t*>(A.gpay[(g.npass - 1) & 1]);

@@ -76,6 +76,7 @@ struct GroupArgs {
   uint32_t epoch;
   int32_t* pos_of_node;
   int32_t* wf_off;
+  int64_t cap_n;                // entries each key and payload buffer holds
 };
 
 // Buckets of the bucketed slack sort (nb == 0: not used this pass).  Bucket of

@@ -1172,6 +1172,114 @@ __global__ __launch_bounds__(kSortThreads) void k_slack_pass(SortArgs a, int pas
   }
 }
 
+// Grouping by workflow in one digit (at most 256 workflows), without the
+// onesweep look-back: its tiles wait on each other in a chain, about 40 ns
+// each, which at 12M futures (3,000 tiles) costs more than the data does.
+// Three kernels instead, each parallel over tiles or workflows:
+//   count  per tile of kSortTile ids, the futures of each workflow
+//          (workflow-major, so that a workflow's counts are contiguous);
+//   scan   per workflow, its tiles' counts into offsets, and its total;
+//   place  per tile, the workflows' starts from the totals, then each
+//          future's stable rank in its tile by ballots, its position =
+//          start + tile offset + rank, and both maps.
+// The counts take the first key buffer, the totals the second.
+constexpr int kGroup1Items = kSortTile / kSortThreads;
+
+__global__ __launch_bounds__(kSortThreads) void k_group1_count(GroupArgs a) {
+  __shared__ uint32_t H[kRadixBuckets];
+  if (a.ctrl->status) return;
+  const int64_t N = a.p.N;
+  const int64_t ntiles = (N + kSortTile - 1) / kSortTile;
+  const int64_t tile = blockIdx.x;
+  H[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t t0 = tile * kSortTile;
+  uint32_t d[kGroup1Items];
+#pragma unroll
+  for (int j = 0; j < kGroup1Items; ++j) {
+    const int64_t i = t0 + j * kSortThreads + threadIdx.x;
+    d[j] = i < N ? uint32_t(a.p.wf[i]) & (kRadixBuckets - 1) : kRadixBuckets;
+  }
+#pragma unroll
+  for (int j = 0; j < kGroup1Items; ++j)
+    if (d[j] < kRadixBuckets) atomicAdd(&H[d[j]], 1u);
+  __syncthreads();
+  a.key[0][int64_t(threadIdx.x) * ntiles + tile] = H[threadIdx.x];
+}
+
+__global__ __launch_bounds__(kSortThreads) void k_group1_scan(GroupArgs a) {
+  __shared__ uint32_t s_tmp[kSortThreads / kWave + 2];
+  __shared__ uint32_t s_sum;
+  if (a.ctrl->status) return;
+  const int64_t ntiles = (a.p.N + kSortTile - 1) / kSortTile;
+  uint32_t* row = a.key[0] + int64_t(blockIdx.x) * ntiles;
+  uint32_t carry = 0;
+  for (int64_t t0 = 0; t0 < ntiles; t0 += kSortThreads) {
+    const int64_t t = t0 + threadIdx.x;
+    const uint32_t x = t < ntiles ? row[t] : 0u;
+    const uint32_t ex = block_excl_scan(x, s_tmp);
+    if (t < ntiles) row[t] = carry + ex;
+    if (threadIdx.x == kSortThreads - 1) s_sum = ex + x;
+    __syncthreads();
+    carry += s_sum;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) a.key[1][blockIdx.x] = carry;
+}
+
+__global__ __launch_bounds__(kSortThreads) void k_group1_place(GroupArgs a) {
+  __shared__ uint32_t s_tmp[kSortThreads / kWave + 2];
+  __shared__ uint32_t base[kRadixBuckets];   // first position of each workflow, then of its part of this tile
+  __shared__ uint32_t wcnt[kSortThreads / kWave][kRadixBuckets];  // this round's futures per wave and workflow
+  __shared__ uint32_t run[kRadixBuckets];    // this tile's futures per workflow in earlier rounds
+  if (a.ctrl->status) return;
+  const int64_t N = a.p.N;
+  const int64_t ntiles = (N + kSortTile - 1) / kSortTile;
+  const int64_t tile = blockIdx.x;
+  const int tid = threadIdx.x, wv = tid / kWave;
+  {
+    const uint32_t tot = a.key[1][tid];
+    const uint32_t start = block_excl_scan(tot, s_tmp);
+    if (tile == 0 && tid <= a.p.W) a.wf_off[tid] = int32_t(start);
+    if (tile == 0 && tid == kSortThreads - 1 && a.p.W == kRadixBuckets) a.wf_off[kRadixBuckets] = int32_t(N);
+    base[tid] = start + a.key[0][int64_t(tid) * ntiles + tile];
+    run[tid] = 0;
+    for (int w = 0; w < kSortThreads / kWave; ++w) wcnt[w][tid] = 0;
+  }
+  __syncthreads();
+  const int64_t t0 = tile * kSortTile;
+  for (int j = 0; j < kGroup1Items; ++j) {
+    const int64_t i = t0 + j * kSortThreads + tid;
+    const bool in = i < N;
+    const uint32_t d = in ? uint32_t(a.p.wf[i]) & (kRadixBuckets - 1) : 0u;
+    uint64_t m = ballot(in);  // the wave's lanes holding the same workflow
+#pragma unroll
+    for (int bit = 0; bit < kRadixBits; ++bit) {
+      const uint64_t b = ballot(in && ((d >> bit) & 1u));
+      m &= ((d >> bit) & 1u) ? b : ~b;
+    }
+    if (in && lanes_below(m) == 0) wcnt[wv][d] = uint32_t(__popcll(m));
+    __syncthreads();
+    if (in) {
+      uint32_t r = run[d] + lanes_below(m);
+      for (int w = 0; w < wv; ++w) r += wcnt[w][d];
+      const uint32_t q = base[d] + r;
+      a.pay[0][q] = uint32_t(i);
+      a.pos_of_node[i] = int32_t(q);
+    }
+    __syncthreads();
+    {
+      uint32_t s = 0;
+      for (int w = 0; w < kSortThreads / kWave; ++w) {
+        s += wcnt[w][tid];
+        wcnt[w][tid] = 0;
+      }
+      run[tid] += s;
+    }
+    __syncthreads();
+  }
+}
+
 __global__ __launch_bounds__(kSortThreads) void k_group_hist(GroupArgs a) {
   __shared__ uint32_t H[kMaxSortPasses][kRadixBuckets];
   if (a.ctrl->status) return;
@@ -1296,6 +1404,20 @@ hipError_t launch_slack_sort(hipStream_t s, const SortArgs& a, int first_pass, i
 
 hipError_t launch_group(hipStream_t s, const GroupArgs& a, void (*mark)(void*, const char*),
                         void* ctx) {
+  const int64_t ntiles = (a.p.N + kSortTile - 1) / kSortTile;
+  if (a.npass == 1 && int64_t(kRadixBuckets) * ntiles <= a.cap_n) {  // at most 256 workflows
+    mark(ctx, "group_count");
+    hipLaunchKernelGGL(k_group1_count, dim3(ntiles), dim3(kSortThreads), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    mark(ctx, "group_scan");
+    hipLaunchKernelGGL(k_group1_scan, dim3(kRadixBuckets), dim3(kSortThreads), 0, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    mark(ctx, "group_place");
+    hipLaunchKernelGGL(k_group1_place, dim3(ntiles), dim3(kSortThreads), 0, s, a);
+    return hipGetLastError();
+  }
   mark(ctx, "group_hist");
   hipLaunchKernelGGL(k_group_hist, dim3(grid_of(a.p.N, kHistItems * kSortThreads, 256)), dim3(kSortThreads), 0, s,
                      a);
