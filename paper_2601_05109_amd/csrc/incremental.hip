@@ -562,6 +562,17 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_scan_heavy(IncArgs a) {
 
 // -------------------------------------------------------------------- sweep
 
+// A device-scope max that is skipped when a plain read of the location
+// already shows a value at least as large.  Within the sweep a member's max
+// only grows (the closure zeroed it, the scan and the sweep only raise it),
+// so a stale read is never above the true value and skipping stays exact; it
+// saves a memory-side atomic whenever an earlier push was larger.  (In the
+// scan the extra reads cost more than the atomics they save.)
+__device__ inline void max_if_larger(int64_t* p, int64_t v) {
+  if (v > __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP))
+    __hip_atomic_fetch_max(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // One push of a finalised member: its rem into d's max, then d's count down
 // by k; returns the count before.  Every access to the maxima and counts in
 // the sweep is a device-scope atomic, so their values meet where such
@@ -569,9 +580,10 @@ __global__ __launch_bounds__(kIncThreads) void k_inc_scan_heavy(IncArgs a) {
 // count: the wait makes the max complete there before the count is touched,
 // so the member that sees the count reach zero (and then loads the max
 // atomically) sees every push.  No cache write-back or invalidation is
-// needed, since nothing passes through plain loads and stores.
+// needed: the only other access is the read that lets max_if_larger skip a
+// max, and a stale value there is never above the true one.
 __device__ inline int32_t push_count(const IncArgs& a, int32_t d, int64_t r, int32_t k) {
-  __hip_atomic_fetch_max(&a.mxA[d], r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  max_if_larger(&a.mxA[d], r);
   __asm__ __volatile__("s_waitcnt vmcnt(0)" ::: "memory");
   return __hip_atomic_fetch_add(&a.cntA[d], -k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
