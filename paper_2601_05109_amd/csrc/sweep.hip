@@ -888,6 +888,11 @@ __device__ __attribute__((always_inline)) void sweep_hbm(const SweepArgs& a, con
 // Futures a thread carries through one step of the ordered pass's counting,
 // their loads issued together.
 constexpr int kHbmU = 4;
+// The one-dependency summary the counting leaves by position (positions of a
+// workflow on this path stay below 2^22, the chunk table's limit).
+constexpr int32_t kOneNone = -1;
+constexpr int32_t kOneMany = -2;
+constexpr int32_t kOneBlocked = 1 << 30;
 
 // Future v's done flag from the packed copy the node kernel wrote (1.5 MB per
 // 12M futures, so that the random reads of dependencies' flags stay in L2).
@@ -927,13 +932,19 @@ __device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs
   uint32_t* cseg = reinterpret_cast<uint32_t*>(mxl + T);  // [nc] pushes into each chunk, then its segment's start
   uint32_t* cfill = cseg + nc;                             // [nc] pushes appended to each segment so far
   int32_t* cnt = a.g_cnt + b;                              // consumers in the same chunk, by position
+  // by position, what the second step needs of a future with one dependency:
+  // that dependency's position, and kOneBlocked if it is not done; else
+  // kOneNone (no valid dependency) or kOneMany (gather the list again)
+  int32_t* one = a.g_front0 + b;
   __shared__ int64_t s_base;
   __shared__ uint32_t s_total;
 
   // 1: check the order and count each dependency's push: into its own
   // counter (HBM, by position) if the consumer is in the same chunk, else into
   // the count of its chunk's segment (LDS).  No chunk order is needed here:
-  // kHbmU futures per thread, their loads issued together.
+  // kHbmU futures per thread, their loads issued together.  A future with a
+  // single dependency also leaves its summary in `one`, so that the second
+  // step reads one coalesced word instead of gathering the list again.
   for (int k = tid; k < n; k += T) st_wg(&cnt[k], int32_t(0));
   for (int i = tid; i < nc; i += T) { cseg[i] = 0; cfill[i] = 0; }
   if (tid == 0) { S.bad = 0; S.hcount = 0; }
@@ -965,9 +976,13 @@ __device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs
 #pragma unroll
     for (int j = 0; j < kHbmU; ++j) {
       const int k = k0 + j * T + tid;
+      if (k < n) one[k] = deg[j] == 0 ? kOneNone : kOneMany;
       if (deg[j] <= 0) continue;
       if (deg[j] <= kHbmLight) {
-        up |= count(checked_dep(L, d0[j], b, n, k, ctrl), k);
+        const int32_t lp = checked_dep(L, d0[j], b, n, k, ctrl);
+        up |= count(lp, k);
+        if (deg[j] == 1)
+          one[k] = lp < 0 || lp > k ? kOneNone : lp | (done_bit(ba.done_bits, d0[j]) ? 0 : kOneBlocked);
         for (int e = 1; e < deg[j]; ++e) up |= count(checked_dep(L, a.p.dep_idx[off[j] + e], b, n, k, ctrl), k);
         continue;
       }
@@ -1065,25 +1080,32 @@ __device__ __attribute__((always_inline)) bool sweep_hbm_ordered(const SweepArgs
     int32_t v = 0, off = 0, deg = 0;
     bool dnk = true;
     int64_t est = 0;
+    const int32_t o = own ? one[k] : kOneNone;
     if (own) {
       v = node_at(L, b + k);
-      off = a.p.dep_off[v];
-      deg = a.p.dep_off[v + 1] - off;
       dnk = done_bit(ba.done_bits, v);
       est = a.p.est[v];
       lc[tid] = ld_wg(&cnt[k]);
     }
+    if (o == kOneMany) {
+      off = a.p.dep_off[v];
+      deg = a.p.dep_off[v + 1] - off;
+    } else if (o >= 0) {
+      deg = 1;
+    }
     const bool light = own && deg <= kHbmLight;
-    int32_t p0 = 0, p1 = 0, lp0 = -1, lp1 = -1;
-    if (light && deg > 0) p0 = a.p.dep_idx[off];
-    if (light && deg > 1) p1 = a.p.dep_idx[off + 1];
-    if (light && deg > 0) lp0 = local_of(L, p0, b, n);
-    if (light && deg > 1) lp1 = local_of(L, p1, b, n);
-    if (lp0 == k) lp0 = -1;  // reported by the first step
-    if (lp1 == k) lp1 = -1;
-    bool blocked = false;
-    if (lp0 >= 0) blocked |= !done_bit(ba.done_bits, p0);
-    if (lp1 >= 0) blocked |= !done_bit(ba.done_bits, p1);
+    int32_t p0 = 0, p1 = 0, lp0 = o >= 0 ? o & ~kOneBlocked : -1, lp1 = -1;
+    bool blocked = o >= 0 && (o & kOneBlocked) != 0;
+    if (o == kOneMany && light) {
+      p0 = a.p.dep_idx[off];
+      p1 = a.p.dep_idx[off + 1];  // deg >= 2
+      lp0 = local_of(L, p0, b, n);
+      lp1 = local_of(L, p1, b, n);
+      if (lp0 == k) lp0 = -1;  // reported by the first step
+      if (lp1 == k) lp1 = -1;
+      if (lp0 >= 0) blocked |= !done_bit(ba.done_bits, p0);
+      if (lp1 >= 0) blocked |= !done_bit(ba.done_bits, p1);
+    }
     if (prd) {
       write_ready<false>(a, it, ppos, pty, plo, prem, pest, dl, lvl, acc, split_l);
       prd = false;
