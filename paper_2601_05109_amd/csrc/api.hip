@@ -232,9 +232,11 @@ int ensure_capacity(nalar_policy* h, int64_t N, int64_t W, int64_t B, int64_t Re
   int64_t newB = a.capB > B ? a.capB : B;
   int64_t newRec = a.capRec > Rec ? a.capRec : Rec;
   int64_t keep_split[kBinMax];  // the current splitters move to the new arena
-  if (a.base) {  // grow geometrically so a slowly growing graph reallocates rarely
+  if (a.base) {  // grow geometrically so a slowly growing graph (or ready set) reallocates rarely
     if (N > a.capN) newN = N + N / 4;
     if (W > a.capW) newW = W + W / 4;
+    if (B > a.capB) newB = B + B / 4;
+    if (Rec > a.capRec) newRec = Rec + Rec / 4;
     hipError_t e = hipStreamSynchronize(h->stream);
     if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
     if (h->split_nb > 0) {
@@ -926,9 +928,7 @@ int nalar::policy_reserve(nalar_policy* h, int64_t N, int64_t E, int64_t W) {
     const int rc = ensure_push_log(h, E);
     if (rc != NALAR_OK) return rc;
   }
-  if (!a.base || (N <= a.capN && W <= a.capW)) return NALAR_OK;  // the first pass sizes it
-  hipError_t e = hipSetDevice(h->device);
-  if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+  if (!a.base) return NALAR_OK;  // the first pass sizes it
   // the incremental pass's bins at the last pass's ready count, kept at least
   BucketArgs bk{};
   bk.bins = 1;
@@ -937,6 +937,11 @@ int nalar::policy_reserve(nalar_policy* h, int64_t N, int64_t E, int64_t W) {
   const int64_t B = a.capB > bk.nb ? a.capB : bk.nb;
   const int64_t rec = bk.nb > 0 ? records_of(bk) : 0;
   const int64_t Rec = a.capRec > rec ? a.capRec : rec;
+  // also when only the bins grew: a reallocation (and its clearing fill) inside
+  // the next pass costs more than the pass
+  if (N <= a.capN && W <= a.capW && B <= a.capB && Rec <= a.capRec) return NALAR_OK;
+  hipError_t e = hipSetDevice(h->device);
+  if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
   return ensure_capacity(h, N, W, B, Rec);
 }
 
