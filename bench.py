@@ -20,7 +20,10 @@ The same JSON line carries, from the same run:
                    kernels and roofline (the workload where the HBM roofline
                    is the fair yardstick);
   dynamic          the map/reduce graph evolving over 100 steps (1.05M ->
-                   12.4M futures): first-pass and repeat-pass latency per step;
+                   12.4M futures) in the graph store: first-pass and
+                   repeat-pass latency per step, full passes beside them
+                   every 25 steps, and (one_pass_per_change) the first passes
+                   again with no repeated pass in between;
   cpu_baseline     the CPU oracle timed on this host, one core.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload paper-scale]
@@ -715,6 +718,13 @@ def main() -> int:
         log_err("leg: dynamic stream")
         dyn = run_dynamic(args.dyn_steps, args.dyn_reps, True, log_err)
         dyn.pop("per_step")
+        if args.dyn_reps > 0:  # one pass per change, as a controller makes it (no repeats in between)
+            log_err("leg: dynamic stream, one pass per change")
+            one = run_dynamic(args.dyn_steps, 0, True, log_err)
+            dyn["one_pass_per_change"] = {"first_pass_us": one["first_pass_us"],
+                                          "incremental_steps": one["incremental_steps"],
+                                          "last_step_first_us": one["last_step"]["first_us"],
+                                          "full_pass_us": one.get("full_pass_us"), "wall_s": one["wall_s"]}
         res["dynamic"] = dyn
     if "traffic" in legs:
         log_err("leg: HBM traffic (rocprofv3 --pmc child runs)")
