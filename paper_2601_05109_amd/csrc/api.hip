@@ -591,10 +591,6 @@ hipError_t clear_lookback(hipStream_t s, const Arena& A) {
                       int64_t(A.lookback_bytes / 4));
 }
 
-// The pass proper, in the scratch of `as` (sized for the snapshot and for the
-// buckets of bk), after the checks of the entry point.
-// own_splitters: the arena belongs to the handle, so the bin splitters it
-// holds are this handle's (bins and their splitters are used only then).
 // The push log of the ordered HBM sweep, for E dependencies (grown by a
 // quarter beyond the need, like the arena).
 int ensure_push_log(nalar_policy* h, int64_t E) {
@@ -615,6 +611,10 @@ int ensure_push_log(nalar_policy* h, int64_t E) {
   return NALAR_OK;
 }
 
+// The pass proper, in the scratch of `as` (sized for the snapshot and for the
+// buckets of bk), after the checks of the entry point.
+// own_splitters: the arena belongs to the handle, so the bin splitters it
+// holds are this handle's (bins and their splitters are used only then).
 int run_pass(nalar_policy* h, const nalar_problem* p, nalar_result* r, ArenaState& as, BucketArgs bk,
              const SweepShape& sh, bool own_splitters) {
   hipError_t e;
