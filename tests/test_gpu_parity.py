@@ -5,8 +5,11 @@ path of every future, the ready order, slack, route and cost, and the return
 code.  Cases: hand-worked fixtures, small random DAGs (contiguous and shuffled
 ids, many instances/types, duplicate dependencies), the tiny / paper-scale /
 deep-chain / map-reduce workloads, relabelled ids (the library groups futures by
-workflow itself), the HBM sweep path forced on, every error rule, repeated
-passes, scratch reuse across sizes, and every step of the dynamic stream.
+workflow itself), the HBM sweep path forced on (with topological ids the
+ordered chunk pass, with shuffled ids or NALAR_FORCE_LEVEL_SWEEP the level
+sweep), workflows of several chunks with chains and heavy futures inside a
+chunk, every error rule, repeated passes, scratch reuse across sizes, and
+every step of the dynamic stream.
 """
 import concurrent.futures as cf
 import os
