@@ -435,6 +435,9 @@ def run_dynamic(steps: int, reps: int, use_store: bool, log=None) -> dict:
             / (last["first_us"] * 1e-6) / 1e9 / HBM_PEAK_GBS,
             "last_step_repeat_pass_roofline_frac": pass_alg_bytes(last["n"], last["e"], last["ready"], 256, 256)
             / (last["us"] * 1e-6) / 1e9 / HBM_PEAK_GBS,
+            "last_step_full_pass_roofline_frac": (pass_alg_bytes(last["n"], last["e"], last["ready"], 256, 256)
+                                                  / (last["full_us"] * 1e-6) / 1e9 / HBM_PEAK_GBS)
+            if "full_us" in last else None,
             "per_step": [{k: (round(v, 2) if isinstance(v, float) else v) for k, v in r.items()} for r in rows],
             "wall_s": time.perf_counter() - t_all}
 
