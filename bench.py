@@ -102,11 +102,9 @@ KERNEL_SYMBOL = {"sweep": "k_sweep", "sort_bucket": "k_bucket_sort", "nodes": "k
 
 def workload(name: str):
     from paper_2601_05109_amd import workloads as wl
-    table = {"paper-scale": wl.paper_scale, "tiny": wl.tiny, "deep-chains": wl.deep_chains,
-             "wide-mapreduce": wl.wide_mapreduce}
-    if name not in table:
+    if name not in wl.WORKLOADS:
         raise SystemExit(f"unknown workload {name}")
-    return table[name]()
+    return wl.WORKLOADS[name]()
 
 
 def pct(xs, f):

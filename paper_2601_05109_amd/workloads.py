@@ -497,9 +497,9 @@ def relabel(p: Problem, perm: np.ndarray) -> Problem:
                    wf_contiguous=contiguous)
 
 
-CONFIGS = {
-    0: tiny,
-    1: paper_scale,
-    2: deep_chains,
-    3: wide_mapreduce,
+WORKLOADS = {
+    "tiny": tiny,
+    "paper-scale": paper_scale,
+    "deep-chains": deep_chains,
+    "wide-mapreduce": wide_mapreduce,
 }

@@ -17,7 +17,7 @@ import pytest
 
 import oracle
 from paper_2601_05109_amd import workloads as wl
-from test_oracle_pins import brute_route
+from test_oracle_pins import brute_route, wl_index
 
 pytestmark = pytest.mark.gpu
 
@@ -107,10 +107,10 @@ def run_case(pol, p, bits=0, prio=None, n_other=300, singles=40, seed=0):
         assert int(one.slack[0]) == int(ref.slack[k]) and int(one.cost[0]) == int(ref.cost[k])
 
 
-@pytest.mark.parametrize("cfg", [0, 1])
+@pytest.mark.parametrize("name", ["tiny", "paper-scale"])
 @pytest.mark.parametrize("bits", [0, nalar.NALAR_ORDER_LPT, nalar.NALAR_ORDER_SRTF, nalar.NALAR_ROUTE_STATEFUL])
-def test_decide_configs(policy, cfg, bits):
-    run_case(policy, wl.CONFIGS[cfg](), bits, seed=cfg * 10 + bits)
+def test_decide_workloads(policy, name, bits):
+    run_case(policy, wl.WORKLOADS[name](), bits, seed=wl_index(name) * 10 + bits)
 
 
 def test_decide_levels_and_large_tables(policy):

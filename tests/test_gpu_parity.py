@@ -21,6 +21,7 @@ import pytest
 import oracle
 from golden_io import load as load_golden, names as golden_names
 from paper_2601_05109_amd import workloads as wl
+from test_oracle_pins import wl_index
 
 pytestmark = pytest.mark.gpu
 
@@ -227,28 +228,28 @@ def test_hbm_ordered_many_heavy(policy_hbm, policy_hbm_levels):
 
 # ---------------------------------------------------------------- workloads
 
-@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
-def test_configs(policy, cfg):
-    check(policy, wl.CONFIGS[cfg](), f"config{cfg}")
+@pytest.mark.parametrize("name", ["tiny", "paper-scale", "deep-chains", "wide-mapreduce"])
+def test_workloads(policy, name):
+    check(policy, wl.WORKLOADS[name](), name)
 
 
-@pytest.mark.parametrize("cfg", [0, 1])
-def test_configs_relabelled(policy, cfg):
-    p = wl.CONFIGS[cfg]()
-    q = wl.relabel(p, np.random.default_rng(cfg).permutation(p.n_nodes))
+@pytest.mark.parametrize("name", ["tiny", "paper-scale"])
+def test_workloads_relabelled(policy, name):
+    p = wl.WORKLOADS[name]()
+    q = wl.relabel(p, np.random.default_rng(wl_index(name)).permutation(p.n_nodes))
     assert not q.wf_contiguous
-    check(policy, q, f"config{cfg} relabelled")
+    check(policy, q, f"{name} relabelled")
 
 
-def test_config_contiguous_flag_not_set(policy):
+def test_contiguous_flag_not_set(policy):
     """The grouping path on ids that happen to be grouped already."""
-    check(policy, wl.paper_scale(), "config1 grouped by the library", flags=0)
+    check(policy, wl.paper_scale(), "paper-scale grouped by the library", flags=0)
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 3])
-def test_configs_hbm_sweep(policy_hbm, policy_hbm_levels, cfg):
-    check(policy_hbm, wl.CONFIGS[cfg](), f"config{cfg} hbm")
-    check(policy_hbm_levels, wl.CONFIGS[cfg](), f"config{cfg} hbm levels")
+@pytest.mark.parametrize("name", ["tiny", "paper-scale", "wide-mapreduce"])
+def test_workloads_hbm_sweep(policy_hbm, policy_hbm_levels, name):
+    check(policy_hbm, wl.WORKLOADS[name](), f"{name} hbm")
+    check(policy_hbm_levels, wl.WORKLOADS[name](), f"{name} hbm levels")
 
 
 def test_deep_chains_hbm_small(policy_hbm, policy_hbm_levels):
@@ -262,15 +263,15 @@ def test_deep_chains_hbm_full(policy_hbm):
     check(policy_hbm, wl.deep_chains(), "deep chains hbm")
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 2])
-def test_configs_tiled_sort(policy_tiled, cfg):
-    check(policy_tiled, wl.CONFIGS[cfg](), f"config{cfg} tiled sort")
+@pytest.mark.parametrize("name", ["tiny", "paper-scale", "deep-chains"])
+def test_workloads_tiled_sort(policy_tiled, name):
+    check(policy_tiled, wl.WORKLOADS[name](), f"{name} tiled sort")
 
 
-def test_configs_relabelled_tiled_sort(policy_tiled):
+def test_workloads_relabelled_tiled_sort(policy_tiled):
     p = wl.tiny()
     check(policy_tiled, wl.relabel(p, np.random.default_rng(7).permutation(p.n_nodes)),
-          "config0 relabelled tiled sort")
+          "tiny relabelled tiled sort")
 
 
 def _flat(deadline_offsets, per_wf=3):
@@ -351,11 +352,11 @@ VARIANTS = [nalar.NALAR_ORDER_LPT, nalar.NALAR_ROUTE_STATEFUL,
 
 
 @pytest.mark.parametrize("bits", VARIANTS)
-@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
-def test_policy_variants_configs(policy, cfg, bits):
-    p = wl.CONFIGS[cfg]()
-    check(policy, p, f"config{cfg} policy {bits}", policy=bits)
-    check(policy, p, f"config{cfg} policy {bits} again", policy=bits)
+@pytest.mark.parametrize("name", ["tiny", "paper-scale", "deep-chains", "wide-mapreduce"])
+def test_policy_variants_workloads(policy, name, bits):
+    p = wl.WORKLOADS[name]()
+    check(policy, p, f"{name} policy {bits}", policy=bits)
+    check(policy, p, f"{name} policy {bits} again", policy=bits)
 
 
 @pytest.mark.parametrize("bits", VARIANTS)
@@ -383,18 +384,18 @@ def test_policy_switch_on_one_handle():
             check(pol, p, f"switch policy {bits}", policy=bits)
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
-def test_priority_levels(policy, policy_tiled, policy_hbm, cfg):
+@pytest.mark.parametrize("name", ["tiny", "paper-scale", "deep-chains", "wide-mapreduce"])
+def test_priority_levels(policy, policy_tiled, policy_hbm, name):
     """Per-workflow priority levels (set_priority) with and without LPT, on
     every sort and sweep path, plus the level rule and keys near +-2^61."""
-    p = wl.CONFIGS[cfg]()
-    rng = np.random.default_rng(20 + cfg)
+    p = wl.WORKLOADS[name]()
+    rng = np.random.default_rng(20 + wl_index(name))
     for levels in (rng.integers(0, 16, p.n_workflows), rng.integers(0, 2, p.n_workflows),
                    np.full(p.n_workflows, 15)):
         pr = levels.astype(np.uint8)
-        check(policy, p, f"config{cfg} levels", priority=pr)
-        check(policy, p, f"config{cfg} levels lpt", policy=nalar.NALAR_ORDER_LPT, priority=pr)
-    if cfg == 0:
+        check(policy, p, f"{name} levels", priority=pr)
+        check(policy, p, f"{name} levels lpt", policy=nalar.NALAR_ORDER_LPT, priority=pr)
+    if name == "tiny":
         pr = rng.integers(0, 16, p.n_workflows).astype(np.uint8)
         q = wl.relabel(p, np.random.default_rng(5).permutation(p.n_nodes))
         check(policy_tiled, q, "relabelled levels", priority=pr)

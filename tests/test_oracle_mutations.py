@@ -134,7 +134,7 @@ def _pins_pass(lib_path):
                 return False
         for pin in (test_priority_levels_partition_the_order, test_weighted_against_quota_walk):
             try:
-                pin(0)
+                pin("tiny")
             except AssertionError:
                 return False
         for pin in (test_srtf_independent_futures_closed_form, test_weighted_rules,

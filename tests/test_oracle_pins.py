@@ -9,7 +9,7 @@ checked here against things other than itself:
 * a push-based replay of value deliveries for readiness (Section 4.3.1,
   property 3), a different formulation from the oracle's pull check;
 * the optimality certificate of longest paths (edge inequality, equality on
-  some consumer, sinks equal their own service time) on the full configs;
+  some consumer, sinks equal their own service time) on the full workloads;
 * closed forms (chains, unit service times, the map/reduce shape);
 * the routing special case with equal loads and speeds, and invariances;
 * uniqueness of a sorted permutation under a total order;
@@ -26,6 +26,12 @@ import pytest
 import oracle
 from golden_io import load as load_golden, names as golden_names
 from paper_2601_05109_amd import workloads as wl
+
+
+def wl_index(name):
+    """The named workload's position in the table; its cases are seeded by it."""
+    return list(wl.WORKLOADS).index(name)
+
 
 INT64_MAX = np.iinfo(np.int64).max
 
@@ -142,22 +148,22 @@ def test_brute_force_catches_planted_mistakes():
             rem_certificate(p, bad)
 
 
-# ---------------------------------------------------------------- configs
+# ---------------------------------------------------------------- named workloads
 
-@pytest.fixture(scope="module", params=[0, 1, 2, 3])
-def config_run(request):
-    p = wl.CONFIGS[request.param]()
+@pytest.fixture(scope="module", params=list(wl.WORKLOADS))
+def workload_run(request):
+    p = wl.WORKLOADS[request.param]()
     return request.param, p, oracle.run(p)
 
 
-def test_config_certificate(config_run):
-    _, p, r = config_run
+def test_workload_certificate(workload_run):
+    _, p, r = workload_run
     assert r.status == oracle.OK
     rem_certificate(p, r.rem)
 
 
-def test_config_order_and_ready(config_run):
-    c, p, r = config_run
+def test_workload_order_and_ready(workload_run):
+    c, p, r = workload_run
     assert_sorted_permutation(p, r)
     ready = np.zeros(p.n_nodes, bool)
     ready[r.order] = True
@@ -175,11 +181,11 @@ def test_config_order_and_ready(config_run):
     np.testing.assert_array_equal(st, r.order)
 
 
-@pytest.mark.parametrize("cfg", [0, 1])
-def test_windowed_ready_locality(cfg):
+@pytest.mark.parametrize("name", ["tiny", "paper-scale"])
+def test_windowed_ready_locality(name):
     """With the first 9 of 32 futures done and parents within the previous 8,
     every ready future has local index 9..16, and local index 9 is always ready."""
-    p = wl.CONFIGS[cfg]()
+    p = wl.WORKLOADS[name]()
     r = oracle.run(p)
     local = r.order % 32
     assert local.min() >= 9 and local.max() <= 16
@@ -301,11 +307,11 @@ def wide_range(p, seed):
                   migration_cost_us=int(rng.choice([0, 200_000, 1 << 60])))
 
 
-@pytest.mark.parametrize("cfg", [0, 1])
-def test_route_exhaustive_configs(cfg):
+@pytest.mark.parametrize("name", ["tiny", "paper-scale"])
+def test_route_exhaustive_workloads(name):
     """Every ready future of the tiny and paper-scale snapshots is routed to
     the exhaustive big-integer minimum of (cost, index)."""
-    p = wl.CONFIGS[cfg]()
+    p = wl.WORKLOADS[name]()
     r = oracle.run(p)
     assert r.status == oracle.OK and r.n_ready > 0
     assert_routes_exhaustive(p, r)
@@ -410,12 +416,12 @@ def test_lpt_equals_srtf_when_deadlines_are_equal():
             np.testing.assert_array_equal(getattr(a, f), getattr(b, f))
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 3])
-def test_lpt_order_certificate(cfg):
+@pytest.mark.parametrize("name", ["tiny", "paper-scale", "wide-mapreduce"])
+def test_lpt_order_certificate(name):
     """The LPT order is a permutation of the ready set (the same set as the
     default pass) strictly increasing in (-rem, wf, v): unique under a total
     order; slack, route and cost are those of the default pass, permuted."""
-    p = wl.CONFIGS[cfg]()
+    p = wl.WORKLOADS[name]()
     a, b = oracle.run(p), oracle.run(p, policy=LPT)
     assert b.n_ready == a.n_ready
     assert sorted(b.order.tolist()) == sorted(a.order.tolist())
@@ -481,12 +487,12 @@ def test_unknown_policy_bits_rejected():
 SRTF = oracle.POLICY_SRTF
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
-def test_srtf_order_certificate(cfg):
+@pytest.mark.parametrize("name", ["tiny", "paper-scale", "deep-chains", "wide-mapreduce"])
+def test_srtf_order_certificate(name):
     """SRTF (least remaining work first, Section 6.2): the ready set of the
     default pass, strictly increasing in (rem, wf, v), which is unique under
     that total order; slack, route and cost are the default pass's, permuted."""
-    p = wl.CONFIGS[cfg]()
+    p = wl.WORKLOADS[name]()
     a, b = oracle.run(p), oracle.run(p, policy=SRTF)
     assert b.n_ready == a.n_ready
     assert sorted(b.order.tolist()) == sorted(a.order.tolist())
@@ -552,14 +558,14 @@ def quota_dispatch(p, order, weights, skip=()):
     return out
 
 
-@pytest.mark.parametrize("cfg", [0, 1])
-def test_weighted_against_quota_walk(cfg):
+@pytest.mark.parametrize("name", ["tiny", "paper-scale"])
+def test_weighted_against_quota_walk(name):
     """Weighted routing (Table 2's route by a list of instances and weights):
     every weighted future goes where the quota walk sends it, at the
     exhaustive cost of that instance; unweighted types keep the default route;
     the order is untouched."""
-    p = wl.CONFIGS[cfg]()
-    rng = np.random.default_rng(40 + cfg)
+    p = wl.WORKLOADS[name]()
+    rng = np.random.default_rng(40 + wl_index(name))
     w = rng.integers(0, 5, p.n_instances).astype(np.uint32)
     w[p.inst_type == 1] = 0            # one type without weights: default routing
     a, r = oracle.run(p), oracle.run(p, policy=WEIGHTED, weights=w)
@@ -670,12 +676,12 @@ def test_greedy_identical_instances_round_robin():
     np.testing.assert_array_equal(r.cost, 500 + (k // m + 1) * 40)
 
 
-@pytest.mark.parametrize("cfg", [0, 1])
-def test_greedy_invariants(cfg):
+@pytest.mark.parametrize("name", ["tiny", "paper-scale"])
+def test_greedy_invariants(name):
     """Loads only grow, so no future costs less than under the snapshot loads;
     the first future of each type in the order is routed exactly as by the
     default rule; order and slack are untouched."""
-    p = wl.CONFIGS[cfg]()
+    p = wl.WORKLOADS[name]()
     a, g = oracle.run(p), oracle.run(p, policy=GREEDY)
     for f in ("order", "slack", "rem"):
         np.testing.assert_array_equal(getattr(a, f), getattr(g, f))
@@ -708,13 +714,13 @@ def test_greedy_load_overflow_is_erange():
     assert oracle.run(p, policy=GREEDY).status == oracle.ERANGE
 
 
-@pytest.mark.parametrize("cfg", [0, 1])
-def test_priority_levels_partition_the_order(cfg):
+@pytest.mark.parametrize("name", ["tiny", "paper-scale"])
+def test_priority_levels_partition_the_order(name):
     """set_priority levels per workflow: the order is the default order split
     stably by level, highest level first; slack, route and cost travel with
     their futures; equal levels change nothing."""
-    p = wl.CONFIGS[cfg]()
-    rng = np.random.default_rng(cfg)
+    p = wl.WORKLOADS[name]()
+    rng = np.random.default_rng(wl_index(name))
     base = oracle.run(p)
     flat = oracle.run(p, priority=np.full(p.n_workflows, 7, np.uint8))
     for f in ("order", "slack", "route", "cost", "rem"):

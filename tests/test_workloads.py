@@ -5,10 +5,11 @@ import pytest
 from paper_2601_05109_amd import workloads as wl
 
 
-@pytest.mark.parametrize("cfg,N,W,M,K", [(0, 2048, 64, 16, 4), (1, 131072, 4096, 64, 8),
-                                        (2, 524288, 1024, 128, 8), (3, 1049088, 256, 256, 8)])
-def test_shapes_and_ranges(cfg, N, W, M, K):
-    p = wl.CONFIGS[cfg]()
+@pytest.mark.parametrize("name,N,W,M,K", [("tiny", 2048, 64, 16, 4), ("paper-scale", 131072, 4096, 64, 8),
+                                         ("deep-chains", 524288, 1024, 128, 8),
+                                         ("wide-mapreduce", 1049088, 256, 256, 8)])
+def test_shapes_and_ranges(name, N, W, M, K):
+    p = wl.WORKLOADS[name]()
     p.check_dtypes()
     assert (p.n_nodes, p.n_workflows, p.n_instances) == (N, W, M)
     assert p.wf_contiguous and np.all(np.diff(p.wf) >= 0)
