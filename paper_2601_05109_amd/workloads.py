@@ -32,7 +32,7 @@ from typing import Iterator, Optional
 import numpy as np
 
 NOW_US = 1_767_225_600_000_000          # fixed "now" of every synthetic snapshot
-MIGRATION_COST_US = 200_000             # state-migration penalty of every config
+MIGRATION_COST_US = 200_000             # state-migration penalty of every workload
 EST_MAX_US = 1 << 40                    # largest service-time estimate accepted
 SEED_BASE = 260105109
 
